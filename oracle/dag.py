@@ -1,0 +1,355 @@
+"""CPU oracle for Poseidon's DAG-based training-time model (test infrastructure).
+
+This package is test infrastructure.  Only the test-suite, the smoke check
+and the CPU-baseline leg of the benchmark may import it.  It shares no code
+with the HIP library: it builds the paper's DAG explicitly and takes the
+longest path in topological order, slowly and in the most literal form.
+
+Every function cites the passage of the paper (Poseidon, arXiv 2609.06086)
+it follows.  Where the paper is silent the reading is named in the
+docstring; the list of readings:
+
+* R1 (1F1B order, Sec. 4.1.2 "Intra-stage edges"): the paper does not state
+  the warm-up length of plain 1F1B.  Stage s of S runs w_s = min(S - s, M)
+  forward passes, then alternates (F_{w+i}, B_i) for i = 1..M-w, then runs
+  the remaining M - (M - w) backward passes (the PipeDream-Flush order).
+* R2 (auxiliary edges, Sec. 4.1.2): one zero-weight edge from the start node
+  to F_{1,1} per pipeline.  Further zero-weight edges from the start node to
+  F_{1,m} would change nothing.
+* R3 (inter-stage weights, Sec. 4.1.3): one activation-transfer time per
+  stage boundary and direction, independent of the layer cut.
+* R4 (path weight, Def. "critical path" in App. B.1): the sum over the
+  path's nodes and edges; the start node begins at time 0.
+* R5 (DP all-reduce, Sec. 4.1.1/4.1.3): one pipeline (D = 1); R_s carries
+  the per-layer all-reduce time summed over the stage (zero by default), so
+  T = finish(E) = finish(B_{1,M}) when all-reduce times are zero.
+* R6 (node weights, Sec. 4.1.3): "per-layer time x #layers" generalised to
+  the sum of the per-layer times of the stage's layers on its device type.
+* R7 (memory, Sec. 3.2 / App. C): a stage is feasible iff the sum of its
+  layers' memory footprints is <= the cap of its device type.
+* R8 (candidate order): compositions in lexicographic order of the sorted
+  cut tuple (itertools.combinations order), assignments in base-T order
+  with stage 1 most significant; joint index = comp_rank * A + a.
+* R9 (ties): the argmin returns the smallest index among equal makespans;
+  infeasible candidates still get their raw DAG makespan but never win.
+* R10 (stage-level bound, Eq. 2): g(S_x) as printed, with f_i, b_i the
+  stage totals and d_i the stage all-reduce time; a candidate is pruned
+  iff max_x g(S_x) > bound (strict, as in Theorem 1).
+"""
+from __future__ import annotations
+
+import itertools
+import math
+from collections import deque
+from dataclasses import dataclass
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+Node = Tuple[str, int, int]      # ('F'|'B', stage s in 1..S, micro-batch m in 1..M), or ('S',0,0)...
+
+START: Node = ("S", 0, 0)
+END: Node = ("E", 0, 0)
+
+
+def one_f_one_b_order(S: int, M: int, s: int) -> List[Tuple[str, int]]:
+    """Execution order of stage s under 1F1B (Sec. 4.1.2, reading R1)."""
+    w = min(S - s, M)
+    order = [("F", m) for m in range(1, w + 1)]
+    for i in range(1, M - w + 1):
+        order.append(("F", w + i))
+        order.append(("B", i))
+    order += [("B", m) for m in range(M - w + 1, M + 1)]
+    return order
+
+
+@dataclass
+class Dag:
+    """The explicit DAG of Sec. 4.1.1-4.1.2 for one pipeline (D = 1)."""
+    S: int
+    M: int
+    nodes: List[Node]
+    # edges as (u, v, kind): kind in {'intra', 'fwd', 'bwd', 'allreduce', 'aux'}
+    edges: List[Tuple[Node, Node, str]]
+    topo: List[Node]
+    preds: Dict[Node, List[Tuple[Node, str]]]
+
+    def counts(self) -> Dict[str, int]:
+        c: Dict[str, int] = {}
+        for _, _, k in self.edges:
+            c[k] = c.get(k, 0) + 1
+        c["compute_nodes"] = sum(1 for n in self.nodes if n[0] in ("F", "B"))
+        c["allreduce_nodes"] = sum(1 for n in self.nodes if n[0] == "R")
+        return c
+
+
+def build_dag(S: int, M: int, order=one_f_one_b_order) -> Dag:
+    """Node and edge construction of Sec. 4.1.1-4.1.2 plus Kahn's order.
+
+    Compute nodes F_{s,m}, B_{s,m} (2SM); all-reduce nodes R_s (S); the
+    control nodes S and E.  Edges: inter-stage F_{s,m}->F_{s+1,m} and
+    B_{s+1,m}->B_{s,m} (2(S-1)M); intra-stage edges along the schedule
+    order (S(2M-1)); B_{s,M}->R_s (S); auxiliary S->F_{1,1} and R_s->E.
+    """
+    nodes: List[Node] = [START]
+    for s in range(1, S + 1):
+        for m in range(1, M + 1):
+            nodes.append(("F", s, m))
+            nodes.append(("B", s, m))
+    for s in range(1, S + 1):
+        nodes.append(("R", s, 0))
+    nodes.append(END)
+    edges: List[Tuple[Node, Node, str]] = []
+    for m in range(1, M + 1):
+        for s in range(1, S):
+            edges.append((("F", s, m), ("F", s + 1, m), "fwd"))
+            edges.append((("B", s + 1, m), ("B", s, m), "bwd"))
+    for s in range(1, S + 1):
+        seq = order(S, M, s)
+        for (t0, m0), (t1, m1) in zip(seq, seq[1:]):
+            edges.append(((t0, s, m0), (t1, s, m1), "intra"))
+    for s in range(1, S + 1):
+        edges.append((("B", s, M), ("R", s, 0), "allreduce"))
+    edges.append((START, ("F", 1, 1), "aux"))
+    for s in range(1, S + 1):
+        edges.append((("R", s, 0), END, "aux"))
+
+    preds: Dict[Node, List[Tuple[Node, str]]] = {n: [] for n in nodes}
+    succs: Dict[Node, List[Node]] = {n: [] for n in nodes}
+    indeg: Dict[Node, int] = {n: 0 for n in nodes}
+    for u, v, k in edges:
+        preds[v].append((u, k))
+        succs[u].append(v)
+        indeg[v] += 1
+    # Kahn's algorithm
+    ready = deque(n for n in nodes if indeg[n] == 0)
+    topo: List[Node] = []
+    while ready:
+        u = ready.popleft()
+        topo.append(u)
+        for v in succs[u]:
+            indeg[v] -= 1
+            if indeg[v] == 0:
+                ready.append(v)
+    if len(topo) != len(nodes):
+        raise ValueError("schedule order produced a cycle")
+    return Dag(S, M, nodes, edges, topo, preds)
+
+
+_DAG_CACHE: Dict[Tuple[int, int], Dag] = {}
+
+
+def dag_for(S: int, M: int) -> Dag:
+    """The topology depends only on (S, M); reuse it (Sec. 5, simulator design)."""
+    key = (S, M)
+    if key not in _DAG_CACHE:
+        _DAG_CACHE[key] = build_dag(S, M)
+    return _DAG_CACHE[key]
+
+
+def longest_path(dag: Dag, F: Sequence[int], B: Sequence[int], cf: Sequence[int],
+                 cb: Sequence[int], d: Optional[Sequence[int]] = None,
+                 return_finish: bool = False):
+    """Critical-path length by DP in topological order (Sec. 4.1, reading R4).
+
+    Weights (Sec. 4.1.3): node F_{s,m} -> F[s-1], B_{s,m} -> B[s-1],
+    R_s -> d[s-1] (0 if absent); edge F_{s,m}->F_{s+1,m} -> cf[s-1],
+    B_{s+1,m}->B_{s,m} -> cb[s-1]; intra-stage, all-reduce and auxiliary
+    edges -> 0.  finish(v) = w(v) + max(0, max over preds u of
+    finish(u) + w(u, v)); T = finish(E).
+    """
+    finish: Dict[Node, int] = {}
+    for v in dag.topo:
+        kind, s, _ = v
+        if kind == "F":
+            wv = int(F[s - 1])
+        elif kind == "B":
+            wv = int(B[s - 1])
+        elif kind == "R":
+            wv = int(d[s - 1]) if d is not None else 0
+        else:
+            wv = 0
+        best = 0
+        for u, ek in dag.preds[v]:
+            if ek == "fwd":
+                we = int(cf[u[1] - 1])           # boundary u.s -> u.s + 1
+            elif ek == "bwd":
+                we = int(cb[v[1] - 1])           # boundary v.s <- v.s + 1
+            else:
+                we = 0
+            best = max(best, finish[u] + we)
+        finish[v] = wv + best
+    if return_finish:
+        return finish[END], finish
+    return finish[END]
+
+
+# ---------------------------------------------------------------------------
+# candidates: compositions x assignments (reading R8)
+# ---------------------------------------------------------------------------
+
+def unrank_composition(L: int, S: int, r: int) -> Tuple[int, ...]:
+    """Cut tuple (c_1 < ... < c_{S-1}) of lexicographic rank r among all
+    (S-1)-subsets of {1..L-1}: count, for each candidate value of the next
+    cut, how many subsets start with it (a Pascal-table count), skip whole
+    blocks until r falls inside one."""
+    k = S - 1
+    if not 0 <= r < math.comb(L - 1, k):
+        raise ValueError("rank out of range")
+    cuts = []
+    v = 0
+    for j in range(1, k + 1):
+        v += 1
+        while True:
+            cnt = math.comb(L - 1 - v, k - j)
+            if r < cnt:
+                cuts.append(v)
+                break
+            r -= cnt
+            v += 1
+    return tuple(cuts)
+
+
+def assignment_row(prob, a: int) -> Tuple[int, ...]:
+    """Stage -> device-type row a: explicit table row, or base-T digits of a
+    with stage 1 the most significant digit (itertools.product order)."""
+    if prob.assign is not None:
+        return tuple(int(x) for x in prob.assign[a])
+    digits = []
+    for _ in range(prob.S):
+        digits.append(a % prob.T)
+        a //= prob.T
+    return tuple(reversed(digits))
+
+
+def all_assignments(prob):
+    if prob.assign is not None:
+        return [tuple(int(x) for x in row) for row in prob.assign]
+    return list(itertools.product(range(prob.T), repeat=prob.S))
+
+
+def enumerate_all(prob):
+    """(index, cuts, types) over every candidate, composition-major."""
+    idx = 0
+    rows = all_assignments(prob)
+    for cuts in itertools.combinations(range(1, prob.L), prob.S - 1):
+        for types in rows:
+            yield idx, cuts, types
+            idx += 1
+
+
+def stage_weights(prob, cuts: Sequence[int], types: Sequence[int],
+                  allreduce: Optional[np.ndarray] = None):
+    """Per-stage F_s, B_s, memory, R_s weight and feasibility (Sec. 4.1.3,
+    readings R6/R7): plain sums over each stage's layers."""
+    bounds = [0] + list(cuts) + [prob.L]
+    F, B, MEM, D = [], [], [], []
+    feasible = True
+    for s in range(prob.S):
+        lo, hi = bounds[s], bounds[s + 1]
+        t = types[s]
+        f = sum(int(prob.fwd[t][k]) for k in range(lo, hi))
+        b = sum(int(prob.bwd[t][k]) for k in range(lo, hi))
+        mm = sum(int(prob.mem[k]) for k in range(lo, hi))
+        dd = sum(int(allreduce[t][k]) for k in range(lo, hi)) if allreduce is not None else 0
+        F.append(f)
+        B.append(b)
+        MEM.append(mm)
+        D.append(dd)
+        if mm > int(prob.cap[t]):
+            feasible = False
+    return F, B, MEM, D, feasible
+
+
+def candidate_list(prob, cands):
+    """(index, cuts, types) for a Candidates object (range or list mode)."""
+    if cands.is_list:
+        out = []
+        for i in range(len(cands)):
+            r = int(cands.comp_rank[i])
+            a = int(cands.assign_idx[i]) if cands.assign_idx is not None else 0
+            out.append((i, unrank_composition(prob.L, prob.S, r), assignment_row(prob, a)))
+        return out
+    out = []
+    lo, hi = cands.first, cands.first + cands.count
+    for idx, cuts, types in enumerate_all(prob):
+        if idx >= hi:
+            break
+        if idx >= lo:
+            out.append((idx - lo, cuts, types))
+    return out
+
+
+def evaluate(prob, cands, allreduce=None):
+    """Makespan of every candidate and its feasibility (uint32 / bool arrays)."""
+    dag = dag_for(prob.S, prob.M)
+    lst = candidate_list(prob, cands)
+    T = np.zeros(len(lst), dtype=np.int64)
+    feas = np.zeros(len(lst), dtype=bool)
+    for i, cuts, types in lst:
+        F, B, _, D, ok = stage_weights(prob, cuts, types, allreduce)
+        T[i] = longest_path(dag, F, B, prob.comm_fwd, prob.comm_bwd,
+                            D if allreduce is not None else None)
+        feas[i] = ok
+    return T, feas
+
+
+def argmin(makespans, feasible):
+    """Smallest makespan over feasible candidates, smallest index on ties
+    (reading R9).  Returns (index, makespan) or None if nothing is feasible."""
+    best = None
+    for i in range(len(makespans)):
+        if not feasible[i]:
+            continue
+        t = int(makespans[i])
+        if best is None or t < best[1]:
+            best = (i, t)
+    return best
+
+
+def eq2_bound(F: Sequence[int], B: Sequence[int], M: int,
+              d: Optional[Sequence[int]] = None) -> int:
+    """max over x of g(S_x), Eq. 2:
+    g(S_x) = sum_{i<x} f_i + M (f_x + b_x) + max_{1<=i<=x} (sum_{j=i}^{x-1} b_j + d_i)."""
+    S = len(F)
+    dd = d if d is not None else [0] * S
+    best = 0
+    for x in range(1, S + 1):
+        g = sum(F[i - 1] for i in range(1, x)) + M * (F[x - 1] + B[x - 1])
+        inner = max(sum(B[j - 1] for j in range(i, x)) + dd[i - 1] for i in range(1, x + 1))
+        best = max(best, g + inner)
+    return best
+
+
+def bounded_search(prob, cands, bound: int, chunk: int = 0):
+    """Early-stop pass (Thm. 1, reading R10) over a candidate list.
+
+    The list is cut into consecutive chunks of `chunk` entries (0 = one
+    chunk).  Each chunk prunes against b = min(bound, best makespan found in
+    earlier chunks); a feasible candidate with max_x g(S_x) > b is pruned,
+    every other feasible one is evaluated exactly.  The result is the
+    (makespan, index)-smallest evaluated candidate if its makespan is
+    <= bound, else None.  Returns (best, evaluated, pruned, infeasible)."""
+    dag = dag_for(prob.S, prob.M)
+    lst = candidate_list(prob, cands)
+    n = len(lst)
+    chunk = n if chunk <= 0 else chunk
+    best = None
+    evaluated = pruned = infeasible = 0
+    for c0 in range(0, n, chunk):
+        b = bound if best is None else min(bound, best[1])
+        for i, cuts, types in lst[c0:c0 + chunk]:
+            F, B, _, _, ok = stage_weights(prob, cuts, types)
+            if not ok:
+                infeasible += 1
+                continue
+            if eq2_bound(F, B, prob.M) > b:
+                pruned += 1
+                continue
+            evaluated += 1
+            t = longest_path(dag, F, B, prob.comm_fwd, prob.comm_bwd)
+            if best is None or (t, i) < best[::-1]:
+                best = (i, t)
+    if best is not None and best[1] > bound:
+        best = None
+    return best, evaluated, pruned, infeasible

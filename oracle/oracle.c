@@ -1,0 +1,428 @@
+/*
+ * CPU oracle for Poseidon's DAG-based training-time model, multithreaded C.
+ *
+ * TEST INFRASTRUCTURE.  Only the test-suite, the smoke check and the
+ * CPU-baseline leg of the benchmark may load this library.  It shares no
+ * code, header or table with the HIP library; it is the paper's definition
+ * written out plainly so that large workloads can be checked on the host.
+ *
+ *  - DAG (Poseidon, Sec. 4.1.1-4.1.2): compute nodes F_{s,m}, B_{s,m}; one
+ *    all-reduce node R_s per stage (weight 0: one pipeline, no DP traffic);
+ *    start node and end node.  Inter-stage edges F_{s,m}->F_{s+1,m} and
+ *    B_{s+1,m}->B_{s,m}; intra-stage edges along each stage's 1F1B order;
+ *    B_{s,M}->R_s; start->F_{1,1}; R_s->end.  The topology depends only on
+ *    (S, M) and is built once (Sec. 5, simulator design), then ordered with
+ *    Kahn's algorithm.
+ *  - 1F1B order (reading of Sec. 4.1.2; the paper does not state the warm-up
+ *    length): stage s runs w = min(S - s, M) forwards, then (F_{w+i}, B_i)
+ *    for i = 1..M-w, then the remaining backwards.
+ *  - Weights (Sec. 4.1.3): F_{s,m} = sum of the stage's per-layer forward
+ *    times on its device type, likewise B_{s,m}; inter-stage edges carry the
+ *    per-boundary transfer time; all other edges and control nodes weigh 0.
+ *  - Makespan = critical path (App. B.1): finish(v) = w(v) + max(0, max over
+ *    predecessors u of finish(u) + w(u,v)), T = finish(end).
+ *  - Feasibility (reading of Sec. 3.2): every stage's summed layer memory
+ *    <= the cap of its device type.
+ *  - Candidates: lexicographic rank of the sorted cut tuple (unranked with a
+ *    Pascal table), assignment row or base-T digits (stage 1 most
+ *    significant); range mode index = rank * A + a.
+ *  - Early stop (Eq. 2, Theorem 1): g(S_x) = sum_{i<x} F_i + M (F_x + B_x)
+ *    + max_{1<=i<=x} sum_{j=i}^{x-1} B_j (d_i = 0); prune iff max_x g > b.
+ *
+ * Finish times are held in 64-bit integers, so no intermediate can wrap.
+ */
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+typedef struct {
+    uint32_t L, S, M, T;
+    const uint32_t *fwd, *bwd;     /* [T][L] */
+    const uint32_t *cf, *cb;       /* [S-1] */
+    const uint32_t *mem;           /* [L] */
+    const uint32_t *cap;           /* [T] */
+    const uint8_t *assign;         /* [A][S] or NULL (all T^S rows) */
+    uint64_t A;
+} oc_problem;
+
+enum { K_F = 0, K_B = 1, K_R = 2, K_START = 3, K_END = 4 };
+enum { E_ZERO = 0, E_FWD = 1, E_BWD = 2 };
+
+typedef struct {
+    int kind, stage;               /* stage 1-based for F/B/R */
+    int npred;
+    int pred[2];                   /* compute nodes have <= 2 predecessors */
+    int ekind[2];
+    int eb[2];                     /* boundary index (0-based) of a weighted edge */
+    int *xpred;                    /* end node: S predecessors */
+} oc_node;
+
+typedef struct {
+    int S, M, n;
+    oc_node *nodes;
+    int *topo;
+    int end;
+} oc_dag;
+
+static int idF(int M, int s, int m) { return 2 * ((s - 1) * M + (m - 1)); }
+static int idB(int M, int s, int m) { return 2 * ((s - 1) * M + (m - 1)) + 1; }
+
+static void add_pred(oc_node *v, int u, int ek, int b) {
+    v->pred[v->npred] = u;
+    v->ekind[v->npred] = ek;
+    v->eb[v->npred] = b;
+    v->npred++;
+}
+
+static void dag_free(oc_dag *g) {
+    if (!g) return;
+    if (g->nodes) free(g->nodes[g->end].xpred);
+    free(g->nodes);
+    free(g->topo);
+    free(g);
+}
+
+/* 1F1B order of stage s as (kind, m) pairs written to ko/mo (2M entries). */
+static void stage_order(int S, int M, int s, int *ko, int *mo) {
+    int w = S - s < M ? S - s : M, k = 0;
+    for (int m = 1; m <= w; ++m) { ko[k] = K_F; mo[k] = m; ++k; }
+    for (int i = 1; i <= M - w; ++i) {
+        ko[k] = K_F; mo[k] = w + i; ++k;
+        ko[k] = K_B; mo[k] = i; ++k;
+    }
+    for (int m = M - w + 1; m <= M; ++m) { ko[k] = K_B; mo[k] = m; ++k; }
+}
+
+static oc_dag *dag_build(int S, int M) {
+    oc_dag *g = calloc(1, sizeof(oc_dag));
+    if (!g) return NULL;
+    int ncomp = 2 * S * M;
+    g->S = S; g->M = M;
+    g->n = ncomp + S + 2;
+    int start = ncomp + S;
+    g->end = ncomp + S + 1;
+    g->nodes = calloc((size_t)g->n, sizeof(oc_node));
+    g->topo = malloc(sizeof(int) * (size_t)g->n);
+    int *ko = malloc(sizeof(int) * 2 * (size_t)M), *mo = malloc(sizeof(int) * 2 * (size_t)M);
+    int *indeg = calloc((size_t)g->n, sizeof(int));
+    int *queue = malloc(sizeof(int) * (size_t)g->n);
+    if (!g->nodes || !g->topo || !ko || !mo || !indeg || !queue) {
+        free(ko); free(mo); free(indeg); free(queue); dag_free(g); return NULL;
+    }
+    for (int s = 1; s <= S; ++s)
+        for (int m = 1; m <= M; ++m) {
+            g->nodes[idF(M, s, m)].kind = K_F; g->nodes[idF(M, s, m)].stage = s;
+            g->nodes[idB(M, s, m)].kind = K_B; g->nodes[idB(M, s, m)].stage = s;
+        }
+    for (int s = 1; s <= S; ++s) { g->nodes[ncomp + s - 1].kind = K_R; g->nodes[ncomp + s - 1].stage = s; }
+    g->nodes[start].kind = K_START;
+    g->nodes[g->end].kind = K_END;
+    /* inter-stage edges */
+    for (int m = 1; m <= M; ++m)
+        for (int s = 1; s < S; ++s) {
+            add_pred(&g->nodes[idF(M, s + 1, m)], idF(M, s, m), E_FWD, s - 1);
+            add_pred(&g->nodes[idB(M, s, m)], idB(M, s + 1, m), E_BWD, s - 1);
+        }
+    /* intra-stage edges along the schedule */
+    for (int s = 1; s <= S; ++s) {
+        stage_order(S, M, s, ko, mo);
+        for (int k = 1; k < 2 * M; ++k) {
+            int u = ko[k - 1] == K_F ? idF(M, s, mo[k - 1]) : idB(M, s, mo[k - 1]);
+            int v = ko[k] == K_F ? idF(M, s, mo[k]) : idB(M, s, mo[k]);
+            add_pred(&g->nodes[v], u, E_ZERO, 0);
+        }
+    }
+    /* all-reduce, auxiliary */
+    for (int s = 1; s <= S; ++s) add_pred(&g->nodes[ncomp + s - 1], idB(M, s, M), E_ZERO, 0);
+    add_pred(&g->nodes[idF(M, 1, 1)], start, E_ZERO, 0);
+    g->nodes[g->end].xpred = malloc(sizeof(int) * (size_t)S);
+    for (int s = 1; s <= S; ++s) g->nodes[g->end].xpred[s - 1] = ncomp + s - 1;
+    /* Kahn */
+    for (int v = 0; v < g->n; ++v) {
+        oc_node *nv = &g->nodes[v];
+        indeg[v] = nv->kind == K_END ? S : nv->npred;
+    }
+    int head = 0, tail = 0, cnt = 0;
+    for (int v = 0; v < g->n; ++v) if (indeg[v] == 0) queue[tail++] = v;
+    /* successor scan: simple O(n^2)-free approach via reverse lists */
+    int *succ_cnt = calloc((size_t)g->n, sizeof(int));
+    for (int v = 0; v < g->n; ++v) {
+        oc_node *nv = &g->nodes[v];
+        int np = nv->kind == K_END ? S : nv->npred;
+        for (int i = 0; i < np; ++i) succ_cnt[nv->kind == K_END ? nv->xpred[i] : nv->pred[i]]++;
+    }
+    int *succ_off = malloc(sizeof(int) * ((size_t)g->n + 1));
+    succ_off[0] = 0;
+    for (int v = 0; v < g->n; ++v) succ_off[v + 1] = succ_off[v] + succ_cnt[v];
+    int *succ = malloc(sizeof(int) * (size_t)(succ_off[g->n] + 1));
+    memset(succ_cnt, 0, sizeof(int) * (size_t)g->n);
+    for (int v = 0; v < g->n; ++v) {
+        oc_node *nv = &g->nodes[v];
+        int np = nv->kind == K_END ? S : nv->npred;
+        for (int i = 0; i < np; ++i) {
+            int u = nv->kind == K_END ? nv->xpred[i] : nv->pred[i];
+            succ[succ_off[u] + succ_cnt[u]++] = v;
+        }
+    }
+    while (head < tail) {
+        int u = queue[head++];
+        g->topo[cnt++] = u;
+        for (int i = succ_off[u]; i < succ_off[u + 1]; ++i)
+            if (--indeg[succ[i]] == 0) queue[tail++] = succ[i];
+    }
+    free(succ_cnt); free(succ_off); free(succ);
+    free(ko); free(mo); free(indeg); free(queue);
+    if (cnt != g->n) { dag_free(g); return NULL; }
+    return g;
+}
+
+/* finish times: caller-provided scratch of g->n uint64 */
+static uint64_t dag_longest(const oc_dag *g, const uint64_t *F, const uint64_t *B,
+                            const uint32_t *cf, const uint32_t *cb, uint64_t *fin) {
+    for (int i = 0; i < g->n; ++i) {
+        int v = g->topo[i];
+        const oc_node *nv = &g->nodes[v];
+        uint64_t best = 0, w = 0;
+        if (nv->kind == K_END) {
+            for (int j = 0; j < g->S; ++j) if (fin[nv->xpred[j]] > best) best = fin[nv->xpred[j]];
+        } else {
+            for (int j = 0; j < nv->npred; ++j) {
+                uint64_t c = fin[nv->pred[j]];
+                if (nv->ekind[j] == E_FWD) c += cf[nv->eb[j]];
+                else if (nv->ekind[j] == E_BWD) c += cb[nv->eb[j]];
+                if (c > best) best = c;
+            }
+        }
+        if (nv->kind == K_F) w = F[nv->stage - 1];
+        else if (nv->kind == K_B) w = B[nv->stage - 1];
+        fin[v] = w + best;
+    }
+    return fin[g->end];
+}
+
+/* Pascal table C(n, k), n <= L-1, k <= S-1, saturating at UINT64_MAX */
+static uint64_t *pascal(int nmax, int kmax) {
+    uint64_t *c = calloc((size_t)(nmax + 1) * (size_t)(kmax + 1), sizeof(uint64_t));
+    if (!c) return NULL;
+    for (int n = 0; n <= nmax; ++n)
+        for (int k = 0; k <= kmax; ++k) {
+            uint64_t v;
+            if (k == 0) v = 1;
+            else if (n == 0) v = 0;
+            else {
+                uint64_t a = c[(size_t)(n - 1) * (kmax + 1) + k - 1], b = c[(size_t)(n - 1) * (kmax + 1) + k];
+                v = a + b;
+                if (v < a) v = UINT64_MAX;
+            }
+            c[(size_t)n * (kmax + 1) + k] = v;
+        }
+    return c;
+}
+
+typedef struct {
+    const oc_problem *p;
+    const oc_dag *g;
+    const uint64_t *binom;
+    uint64_t first, count;
+    const uint64_t *rank;
+    const uint32_t *aidx;
+    uint32_t *out_T;
+    uint8_t *out_feas;
+    uint64_t lo, hi;          /* slice of [0, count) */
+    /* bounded mode */
+    int bounded;
+    uint64_t bound;
+    uint64_t best_key_T, best_idx;
+    uint64_t evaluated, pruned, infeasible;
+    int err;
+} oc_job;
+
+/* decode candidate i: cut points (c_0 = 0 ... c_S = L) and stage types */
+static int decode(const oc_job *j, uint64_t i, int *cuts, int *types) {
+    const oc_problem *p = j->p;
+    uint64_t r, a;
+    if (j->rank) {
+        r = j->rank[i];
+        a = j->aidx ? j->aidx[i] : 0;
+    } else {
+        uint64_t idx = j->first + i;
+        r = idx / p->A;
+        a = idx % p->A;
+    }
+    if (a >= p->A) return -1;
+    int S = (int)p->S, L = (int)p->L, k = S - 1;
+    if (r >= j->binom[(size_t)(L - 1) * (k + 1) + k]) return -1;
+    cuts[0] = 0;
+    int v = 0;
+    for (int jj = 1; jj <= k; ++jj) {
+        ++v;
+        for (;;) {
+            uint64_t cnt = j->binom[(size_t)(L - 1 - v) * (k + 1) + (k - jj)];
+            if (r < cnt) { cuts[jj] = v; break; }
+            r -= cnt;
+            ++v;
+        }
+    }
+    cuts[S] = L;
+    if (p->assign) {
+        for (int s = 0; s < S; ++s) types[s] = p->assign[a * S + s];
+    } else {
+        for (int s = S - 1; s >= 0; --s) { types[s] = (int)(a % p->T); a /= p->T; }
+    }
+    for (int s = 0; s < S; ++s) if (types[s] >= (int)p->T) return -1;
+    return 0;
+}
+
+static void *worker(void *arg) {
+    oc_job *j = arg;
+    const oc_problem *p = j->p;
+    int S = (int)p->S;
+    int cuts[65], types[64];
+    uint64_t F[64], B[64];
+    uint64_t *fin = malloc(sizeof(uint64_t) * (size_t)j->g->n);
+    if (!fin) { j->err = -3; return NULL; }
+    j->best_key_T = UINT64_MAX; j->best_idx = UINT64_MAX;
+    for (uint64_t i = j->lo; i < j->hi; ++i) {
+        if (decode(j, i, cuts, types)) { j->err = -1; break; }
+        int feasible = 1;
+        for (int s = 0; s < S; ++s) {
+            uint64_t f = 0, b = 0, mm = 0;
+            for (int l = cuts[s]; l < cuts[s + 1]; ++l) {
+                f += p->fwd[(size_t)types[s] * p->L + l];
+                b += p->bwd[(size_t)types[s] * p->L + l];
+                mm += p->mem[l];
+            }
+            F[s] = f; B[s] = b;
+            if (mm > p->cap[types[s]]) feasible = 0;
+        }
+        if (j->bounded) {
+            if (!feasible) { j->infeasible++; continue; }
+            uint64_t lb = 0;
+            for (int x = 1; x <= S; ++x) {
+                uint64_t g = 0, inner = 0;
+                for (int i2 = 1; i2 < x; ++i2) g += F[i2 - 1];
+                g += (uint64_t)p->M * (F[x - 1] + B[x - 1]);
+                for (int i2 = 1; i2 <= x; ++i2) {
+                    uint64_t sb = 0;
+                    for (int jj = i2; jj <= x - 1; ++jj) sb += B[jj - 1];
+                    if (sb > inner) inner = sb;
+                }
+                if (g + inner > lb) lb = g + inner;
+            }
+            if (lb > j->bound) { j->pruned++; continue; }
+            j->evaluated++;
+        }
+        uint64_t T = dag_longest(j->g, F, B, p->cf, p->cb, fin);
+        if (T > UINT32_MAX) { j->err = -2; break; }
+        if (j->out_T) j->out_T[i] = (uint32_t)T;
+        if (j->out_feas) j->out_feas[i] = (uint8_t)feasible;
+        if (j->bounded && (T < j->best_key_T || (T == j->best_key_T && i < j->best_idx))) {
+            j->best_key_T = T; j->best_idx = i;
+        }
+    }
+    free(fin);
+    return NULL;
+}
+
+static int run_jobs(oc_job *proto, uint64_t lo, uint64_t hi, int nthreads, oc_job *jobs) {
+    pthread_t th[256];
+    if (nthreads < 1) nthreads = 1;
+    if (nthreads > 256) nthreads = 256;
+    uint64_t n = hi - lo;
+    if ((uint64_t)nthreads > n) nthreads = n ? (int)n : 1;
+    for (int t = 0; t < nthreads; ++t) {
+        jobs[t] = *proto;
+        jobs[t].lo = lo + n * (uint64_t)t / (uint64_t)nthreads;
+        jobs[t].hi = lo + n * (uint64_t)(t + 1) / (uint64_t)nthreads;
+        jobs[t].evaluated = jobs[t].pruned = jobs[t].infeasible = 0;
+        jobs[t].err = 0;
+    }
+    for (int t = 1; t < nthreads; ++t) pthread_create(&th[t], NULL, worker, &jobs[t]);
+    worker(&jobs[0]);
+    for (int t = 1; t < nthreads; ++t) pthread_join(th[t], NULL);
+    return nthreads;
+}
+
+static int check(const oc_problem *p) {
+    if (!p || p->S < 1 || p->S > 64 || p->L < p->S || p->M < 1 || p->T < 1 || p->A < 1) return -1;
+    if (!p->fwd || !p->bwd || !p->mem || !p->cap) return -1;
+    if (p->S > 1 && (!p->cf || !p->cb)) return -1;
+    return 0;
+}
+
+/* Evaluate `count` candidates: range mode if rank == NULL (index first + i),
+ * else list mode.  Writes makespans and feasibility.  Returns 0, or <0. */
+int oc_eval(const oc_problem *p, uint64_t first, uint64_t count, const uint64_t *rank,
+            const uint32_t *aidx, uint32_t *out_T, uint8_t *out_feas, int nthreads) {
+    if (check(p)) return -1;
+    oc_dag *g = dag_build((int)p->S, (int)p->M);
+    uint64_t *binom = pascal((int)p->L - 1, (int)p->S - 1);
+    if (!g || !binom) { dag_free(g); free(binom); return -3; }
+    oc_job proto = {0};
+    proto.p = p; proto.g = g; proto.binom = binom; proto.first = first; proto.count = count;
+    proto.rank = rank; proto.aidx = aidx; proto.out_T = out_T; proto.out_feas = out_feas;
+    oc_job jobs[256];
+    int nt = run_jobs(&proto, 0, count, nthreads, jobs);
+    int err = 0;
+    for (int t = 0; t < nt; ++t) if (jobs[t].err) err = jobs[t].err;
+    dag_free(g); free(binom);
+    return err;
+}
+
+/* Early-stop pass in chunks (0 = one chunk); see header comment.  Returns 0
+ * with *best_idx = UINT64_MAX if nothing evaluated has makespan <= bound. */
+int oc_bounded(const oc_problem *p, uint64_t first, uint64_t count, const uint64_t *rank,
+               const uint32_t *aidx, uint32_t bound, uint64_t chunk, uint64_t *best_idx,
+               uint32_t *best_T, uint64_t *evaluated, uint64_t *pruned, uint64_t *infeasible,
+               int nthreads) {
+    if (check(p)) return -1;
+    oc_dag *g = dag_build((int)p->S, (int)p->M);
+    uint64_t *binom = pascal((int)p->L - 1, (int)p->S - 1);
+    if (!g || !binom) { dag_free(g); free(binom); return -3; }
+    if (chunk == 0) chunk = count ? count : 1;
+    oc_job proto = {0};
+    proto.p = p; proto.g = g; proto.binom = binom; proto.first = first; proto.count = count;
+    proto.rank = rank; proto.aidx = aidx; proto.bounded = 1;
+    uint64_t bT = UINT64_MAX, bI = UINT64_MAX, ev = 0, pr = 0, inf = 0;
+    int err = 0;
+    oc_job jobs[256];
+    for (uint64_t c0 = 0; c0 < count && !err; c0 += chunk) {
+        uint64_t c1 = c0 + chunk < count ? c0 + chunk : count;
+        proto.bound = bT < bound ? bT : bound;
+        int nt = run_jobs(&proto, c0, c1, nthreads, jobs);
+        for (int t = 0; t < nt; ++t) {
+            if (jobs[t].err) err = jobs[t].err;
+            ev += jobs[t].evaluated; pr += jobs[t].pruned; inf += jobs[t].infeasible;
+            if (jobs[t].best_key_T < bT || (jobs[t].best_key_T == bT && jobs[t].best_idx < bI)) {
+                bT = jobs[t].best_key_T; bI = jobs[t].best_idx;
+            }
+        }
+    }
+    dag_free(g); free(binom);
+    if (err) return err;
+    if (bT > bound) { bT = UINT32_MAX; bI = UINT64_MAX; }
+    *best_idx = bI; *best_T = (uint32_t)bT;
+    *evaluated = ev; *pruned = pr; *infeasible = inf;
+    return 0;
+}
+
+/* DAG shape for pins: compute nodes, edges by kind. */
+int oc_dag_counts(int S, int M, int *n_nodes, int *n_fwd, int *n_bwd, int *n_intra, int *n_other) {
+    oc_dag *g = dag_build(S, M);
+    if (!g) return -1;
+    int f = 0, b = 0, in = 0, o = 0;
+    for (int v = 0; v < g->n; ++v) {
+        const oc_node *nv = &g->nodes[v];
+        if (nv->kind == K_END) { o += S; continue; }
+        for (int j = 0; j < nv->npred; ++j) {
+            if (nv->ekind[j] == E_FWD) ++f;
+            else if (nv->ekind[j] == E_BWD) ++b;
+            else if ((nv->kind == K_F || nv->kind == K_B) && g->nodes[nv->pred[j]].kind <= K_B) ++in;
+            else ++o;
+        }
+    }
+    *n_nodes = g->n; *n_fwd = f; *n_bwd = b; *n_intra = in; *n_other = o;
+    dag_free(g);
+    return 0;
+}

@@ -1,0 +1,436 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle.
+
+Each test checks the oracle (Python and C) against something fixed by the
+paper or by mathematics: the node/edge counts of Sec. 4.1.1-4.1.2, closed
+forms of uniform pipelines, hand-derived worked examples, an independent
+event-driven simulation, brute-force path enumeration, symmetry and
+monotonicity of longest paths, Eq. 2's lower bound and Theorem 1.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import coracle, dag, des
+from paper_2609_06086_amd import workloads as W
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def T_of(S, M, F, B, cf, cb):
+    return dag.longest_path(dag.dag_for(S, M), F, B, cf, cb)
+
+
+# ---------------------------------------------------------------- DAG shape
+
+@pytest.mark.parametrize("S,M", [(1, 1), (2, 4), (3, 2), (4, 8), (4, 3), (8, 32), (5, 1)])
+def test_dag_counts_sec_4_1(S, M):
+    """Sec. 4.1.1-4.1.2: 2SM compute nodes, 2(S-1)M inter-stage edges,
+    S(2M-1) intra-stage edges, S all-reduce nodes and edges, D + S auxiliary
+    edges (D = 1)."""
+    c = dag.build_dag(S, M).counts()
+    assert c["compute_nodes"] == 2 * S * M
+    assert c.get("fwd", 0) + c.get("bwd", 0) == 2 * (S - 1) * M
+    assert c["intra"] == S * (2 * M - 1)
+    assert c["allreduce_nodes"] == S and c["allreduce"] == S
+    assert c["aux"] == 1 + S
+    cc = coracle.dag_counts(S, M)
+    assert cc["nodes"] == 2 * S * M + S + 2
+    assert cc["fwd"] + cc["bwd"] == 2 * (S - 1) * M
+    assert cc["intra"] == S * (2 * M - 1)
+    assert cc["other"] == S + 1 + S
+
+
+def test_1f1b_order_is_a_permutation_with_f_before_b():
+    for S in range(1, 7):
+        for M in range(1, 9):
+            for s in range(1, S + 1):
+                o = dag.one_f_one_b_order(S, M, s)
+                assert sorted(o) == sorted([("F", m) for m in range(1, M + 1)] +
+                                           [("B", m) for m in range(1, M + 1)])
+                pos = {x: i for i, x in enumerate(o)}
+                assert all(pos[("F", m)] < pos[("B", m)] for m in range(1, M + 1))
+                # forward passes run in micro-batch order, as do backward passes
+                assert [m for k, m in o if k == "F"] == list(range(1, M + 1))
+                assert [m for k, m in o if k == "B"] == list(range(1, M + 1))
+                # in-flight forwards never exceed the warm-up depth + 1
+                infl, peak = 0, 0
+                for k, _ in o:
+                    infl += 1 if k == "F" else -1
+                    peak = max(peak, infl)
+                assert peak == min(S - s + 1, M)
+
+
+# ------------------------------------------------------------ closed forms
+
+@pytest.mark.parametrize("S", range(1, 7))
+@pytest.mark.parametrize("M", range(1, 12))
+def test_uniform_zero_comm_closed_form(S, M):
+    """Uniform stages, no transfer time: T = (M + S - 1)(t_f + t_b)."""
+    tf, tb = 7, 13
+    assert T_of(S, M, [tf] * S, [tb] * S, [0] * (S - 1), [0] * (S - 1)) == (M + S - 1) * (tf + tb)
+
+
+def test_uniform_closed_form_c_oracle_large():
+    """Same closed form through the C oracle at the workloads' (S, M) shapes."""
+    for S, M in [(2, 4), (4, 16), (8, 32), (8, 64), (16, 128), (16, 3), (9, 20)]:
+        L = S * 3
+        prob = W.Problem(L, S, M, 1, np.full((1, L), 5, np.uint32), np.full((1, L), 11, np.uint32),
+                         np.zeros(S - 1, np.uint32), np.zeros(S - 1, np.uint32),
+                         np.ones(L, np.uint32), np.array([10**6], np.uint32),
+                         np.full((1, S), 0, np.uint8))
+        # the composition with 3 layers on every stage
+        cuts = tuple(range(3, L, 3))
+        r = list(itertools.combinations(range(1, L), S - 1)).index(cuts) if L <= 24 else None
+        if r is None:
+            # rank of the all-3 composition by direct counting of smaller tuples
+            r = 0
+            prev = 0
+            for j, c in enumerate(cuts, start=1):
+                for v in range(prev + 1, c):
+                    r += math.comb(L - 1 - v, S - 1 - j)
+                prev = c
+        cands = W.Candidates(comp_rank=np.array([r], np.uint64))
+        T, f = coracle.evaluate(prob, cands)
+        assert int(T[0]) == (M + S - 1) * 3 * (5 + 11)
+
+
+@pytest.mark.parametrize("M", [1, 2, 5, 9])
+def test_single_stage(M):
+    """S = 1: the stage runs F, B alternately with nothing else: T = M(F + B)."""
+    assert T_of(1, M, [17], [29], [], []) == M * (17 + 29)
+
+
+@pytest.mark.parametrize("S", [1, 2, 3, 6])
+def test_single_microbatch(S):
+    """M = 1: the DAG is one chain F_1..F_S, B_S..B_1: T = sum(F+B) + sum(cf+cb)."""
+    rng = np.random.default_rng(S)
+    F, B = rng.integers(1, 100, S), rng.integers(1, 100, S)
+    cf, cb = rng.integers(0, 50, S - 1), rng.integers(0, 50, S - 1)
+    assert T_of(S, 1, F, B, cf, cb) == int(F.sum() + B.sum() + cf.sum() + cb.sum())
+
+
+def test_worked_examples_golden():
+    """Hand-derived per-node finish times (tests/golden/worked_examples.json)."""
+    ex = json.load(open(os.path.join(GOLD, "worked_examples.json")))["examples"]
+    for e in ex:
+        T, fin = dag.longest_path(dag.build_dag(e["S"], e["M"]), e["F"], e["B"], e["cf"], e["cb"],
+                                  return_finish=True)
+        assert T == e["T"], e["name"]
+        for key, val in e["finish"].items():
+            k, s, m = key.split(",")
+            assert fin[(k, int(s), int(m))] == val, (e["name"], key)
+        # the same value through the C oracle: one composition with one layer per stage
+        S = e["S"]
+        prob = W.Problem(S, S, e["M"], 1, np.array([e["F"]], np.uint32), np.array([e["B"]], np.uint32),
+                         np.array(e["cf"], np.uint32), np.array(e["cb"], np.uint32),
+                         np.ones(S, np.uint32), np.array([S], np.uint32), np.zeros((1, S), np.uint8))
+        Tc, fc = coracle.evaluate(prob, W.Candidates(first=0, count=1))
+        assert int(Tc[0]) == e["T"] and bool(fc[0])
+
+
+# ----------------------------------------------------- independent models
+
+def _rand_case(rng, S, M, hi=60):
+    return (rng.integers(1, hi, S), rng.integers(1, hi, S),
+            rng.integers(0, hi, S - 1), rng.integers(0, hi, S - 1))
+
+
+def test_event_driven_simulation_matches_dag():
+    """An event-queue simulation of the 1F1B schedule gives the DAG's T."""
+    rng = np.random.default_rng(7)
+    for _ in range(250):
+        S, M = int(rng.integers(1, 7)), int(rng.integers(1, 9))
+        F, B, cf, cb = _rand_case(rng, S, M)
+        assert des.simulate_1f1b(S, M, F, B, cf, cb, dag.one_f_one_b_order) == T_of(S, M, F, B, cf, cb)
+
+
+def test_brute_force_paths_match_dp():
+    """Every start->end path enumerated; the heaviest equals the DP value."""
+    rng = np.random.default_rng(8)
+    for S, M in [(1, 3), (2, 2), (2, 4), (3, 2), (3, 3), (4, 2)]:
+        d = dag.build_dag(S, M)
+        for _ in range(20):
+            F, B, cf, cb = _rand_case(rng, S, M)
+            assert des.all_paths_longest(d, F, B, cf, cb) == dag.longest_path(d, F, B, cf, cb)
+
+
+def test_allreduce_nodes_extend_the_sink():
+    """With per-stage all-reduce weights d_s the end node takes
+    max_s(finish(B_{s,M}) + d_s) (Sec. 4.1.1/4.1.3); with d = 0 it is finish(B_{1,M})."""
+    rng = np.random.default_rng(9)
+    for _ in range(50):
+        S, M = int(rng.integers(1, 6)), int(rng.integers(1, 7))
+        F, B, cf, cb = _rand_case(rng, S, M)
+        d = rng.integers(0, 500, S)
+        g = dag.build_dag(S, M)
+        T0, fin = dag.longest_path(g, F, B, cf, cb, return_finish=True)
+        assert T0 == fin[("B", 1, M)]
+        assert all(fin[("B", s, M)] <= T0 for s in range(1, S + 1))
+        T1 = dag.longest_path(g, F, B, cf, cb, d)
+        assert T1 == max(fin[("B", s, M)] + int(d[s - 1]) for s in range(1, S + 1))
+        assert des.all_paths_longest(g, F, B, cf, cb, d) == T1 if S * M <= 6 else True
+
+
+# ----------------------------------------------------------- invariants
+
+def test_reversal_symmetry():
+    """Reversing every edge maps the 1F1B DAG onto itself with F<->B and
+    cf<->cb swapped (F_{s,m} <-> B_{s,M+1-m}), so T is unchanged."""
+    rng = np.random.default_rng(10)
+    for _ in range(200):
+        S, M = int(rng.integers(1, 7)), int(rng.integers(1, 9))
+        F, B, cf, cb = _rand_case(rng, S, M)
+        assert T_of(S, M, F, B, cf, cb) == T_of(S, M, B, F, cb, cf)
+
+
+def test_monotone_and_homogeneous():
+    rng = np.random.default_rng(11)
+    for _ in range(150):
+        S, M = int(rng.integers(1, 6)), int(rng.integers(1, 8))
+        F, B, cf, cb = _rand_case(rng, S, M)
+        T = T_of(S, M, F, B, cf, cb)
+        assert T_of(S, M, 3 * F, 3 * B, 3 * cf, 3 * cb) == 3 * T
+        assert T_of(S, M + 1, F, B, cf, cb) >= T
+        which = int(rng.integers(0, 4))
+        arrs = [F.copy(), B.copy(), cf.copy(), cb.copy()]
+        if len(arrs[which]):
+            arrs[which][int(rng.integers(0, len(arrs[which])))] += int(rng.integers(1, 40))
+            assert T_of(S, M, *arrs) >= T
+        # upper bound: every node and edge weight counted once
+        assert T <= M * int(F.sum() + B.sum()) + M * int(cf.sum() + cb.sum())
+        # the busiest stage must run all its work
+        assert T >= M * int((F + B).max())
+
+
+def test_eq2_lower_bound_holds():
+    """Theorem 1 needs g(S_x) <= T for every completion: check T >= max_x g(S_x)."""
+    rng = np.random.default_rng(12)
+    for _ in range(300):
+        S, M = int(rng.integers(1, 7)), int(rng.integers(1, 10))
+        F, B, cf, cb = _rand_case(rng, S, M)
+        assert dag.eq2_bound(list(F), list(B), M) <= T_of(S, M, F, B, cf, cb)
+
+
+def test_eq2_bound_is_a_real_path_when_uniform():
+    """Uniform stages, no comm: g(S_S) = (S-1)(f+b) + M(f+b) = T, the bound is tight."""
+    for S in range(1, 6):
+        for M in range(1, 8):
+            assert dag.eq2_bound([3] * S, [5] * S, M) == (M + S - 1) * 8 == T_of(S, M, [3] * S, [5] * S,
+                                                                                 [0] * (S - 1), [0] * (S - 1))
+
+
+def test_static_model_eq1_differs():
+    """Sec. 2.2: the static model sum t_s + (B-1) max t_j is not the DAG's
+    T; it overestimates when communication overlaps with computation."""
+    S, M, F, B, c = 2, 2, [10, 10], [20, 20], [3]
+    t = [F[0] + B[0] + c[0], F[1] + B[1] + c[0]]
+    eq1 = sum(t) + (M - 1) * max(t)
+    assert eq1 != T_of(S, M, F, B, c, c)
+
+
+# ---------------------------------------------------------- enumeration
+
+def test_candidate_counts():
+    assert W.workload(1).problem.n_candidates == 28
+    assert W.workload(2).problem.n_candidates == 71920
+    assert W.workload(3).problem.n_candidates == 62891499
+    assert math.comb(79, 7) == 2898753715 and math.comb(125, 15) < 2 ** 63
+
+
+@pytest.mark.parametrize("L,S", [(8, 2), (9, 4), (10, 10), (12, 1), (13, 6)])
+def test_unrank_is_lexicographic(L, S):
+    allc = list(itertools.combinations(range(1, L), S - 1))
+    assert len(allc) == math.comb(L - 1, S - 1)
+    for r, c in enumerate(allc):
+        assert dag.unrank_composition(L, S, r) == c
+
+
+def test_c_oracle_matches_python_oracle_random():
+    rng = np.random.default_rng(13)
+    for trial in range(25):
+        S = int(rng.integers(1, 6))
+        L = int(rng.integers(S, S + 6))
+        M = int(rng.integers(1, 9))
+        T = int(rng.integers(1, 4))
+        rows = None if trial % 2 else int(rng.integers(1, 5))
+        prob = W.random_problem(rng, L, S, M, T, assign_rows=rows, mem_hi=30, cap=int(rng.integers(30, 120)))
+        full = W.Candidates(first=0, count=prob.n_candidates)
+        Tp, fp = dag.evaluate(prob, full)
+        Tc, fc = coracle.evaluate(prob, full, nthreads=3)
+        assert (Tp == Tc).all() and (fp == fc).all()
+        lst = W.random_candidates(rng, prob, 40)
+        Tp, fp = dag.evaluate(prob, lst)
+        Tc, fc = coracle.evaluate(prob, lst, nthreads=2)
+        assert (Tp == Tc).all() and (fp == fc).all()
+
+
+def test_c_oracle_matches_python_oracle_cfg1_cfg2():
+    wl = W.workload(1)
+    Tp, fp = dag.evaluate(wl.problem, wl.cands)
+    Tc, fc = coracle.evaluate(wl.problem, wl.cands)
+    assert (Tp == Tc).all() and (fp == fc).all()
+    wl = W.workload(2)
+    # a strided sample of config 2 through the Python enumeration
+    sub = W.Candidates(first=0, count=wl.problem.n_candidates)
+    Tc, fc = coracle.evaluate(wl.problem, sub)
+    picks = list(range(0, wl.problem.n_candidates, 997))
+    full = {i: (c, t) for i, c, t in dag.enumerate_all(wl.problem) if i % 997 == 0}
+    g = dag.dag_for(wl.problem.S, wl.problem.M)
+    for i in picks:
+        cuts, types = full[i]
+        F, B, _, _, ok = dag.stage_weights(wl.problem, cuts, types)
+        assert dag.longest_path(g, F, B, wl.problem.comm_fwd, wl.problem.comm_bwd) == int(Tc[i])
+        assert ok == bool(fc[i])
+
+
+# ---------------------------------------------------- argmin, feasibility
+
+def test_argmin_tie_break_and_no_feasible():
+    T = np.array([5, 3, 3, 7, 3], np.uint32)
+    f = np.array([True, False, True, True, True])
+    assert dag.argmin(T, f) == (2, 3)
+    assert coracle.argmin(T, f) == (2, 3)
+    assert dag.argmin(T, np.zeros(5, bool)) is None
+    assert coracle.argmin(T, np.zeros(5, bool)) is None
+
+
+def test_cap_equality_is_feasible():
+    prob = W.Problem(2, 2, 2, 1, np.ones((1, 2), np.uint32), np.ones((1, 2), np.uint32),
+                     np.zeros(1, np.uint32), np.zeros(1, np.uint32), np.array([7, 9], np.uint32),
+                     np.array([9], np.uint32), None)
+    _, fc = coracle.evaluate(prob, W.Candidates(first=0, count=1))
+    assert bool(fc[0])
+    prob.cap = np.array([8], np.uint32)
+    _, fc = coracle.evaluate(prob, W.Candidates(first=0, count=1))
+    assert not bool(fc[0])
+    _, _, _, _, ok = dag.stage_weights(prob, (1,), (0, 0))
+    assert not ok
+
+
+def test_duplicate_candidates_tie_to_first():
+    wl = W.workload(2)
+    prob = wl.problem
+    rng = np.random.default_rng(3)
+    lst = W.random_candidates(rng, prob, 300)
+    lst.comp_rank[250] = lst.comp_rank[40]
+    lst.assign_idx[250] = lst.assign_idx[40]
+    T, f = coracle.evaluate(prob, lst)
+    assert T[250] == T[40] and f[250] == f[40]
+    best = coracle.argmin(T, f)
+    assert best[0] != 250
+
+
+# ------------------------------------------------------------ early stop
+
+def test_bounded_search_theorem1():
+    """Pruning with g(S_x) > bound never loses the optimum (Theorem 1); the
+    pruned candidates all have T > bound; Python and C agree on counts."""
+    rng = np.random.default_rng(14)
+    for trial in range(12):
+        S = int(rng.integers(2, 6))
+        L = int(rng.integers(S + 2, S + 9))
+        M = int(rng.integers(1, 12))
+        prob = W.random_problem(rng, L, S, M, 2, mem_hi=20, cap=int(rng.integers(40, 120)))
+        lst = W.random_candidates(rng, prob, 150)
+        Tx, fx = dag.evaluate(prob, lst)
+        exact = dag.argmin(Tx, fx)
+        if exact is None:
+            continue
+        warm = dag.argmin(Tx[:20], fx[:20])
+        bound = warm[1] if warm else 2 ** 32 - 1
+        for chunk in (0, 17, 64):
+            best, ev, pr, inf = dag.bounded_search(prob, lst, bound, chunk)
+            assert best == exact
+            bc = coracle.bounded(prob, lst, bound, chunk, nthreads=3)
+            assert bc == (best, ev, pr, inf)
+            assert ev + pr + inf == len(lst) and inf == int((~fx).sum())
+        # every candidate pruned against the fixed bound is strictly worse than it
+        for i, cuts, types in dag.candidate_list(prob, lst):
+            F, B, _, _, ok = dag.stage_weights(prob, cuts, types)
+            if ok and dag.eq2_bound(F, B, M) > bound:
+                assert Tx[i] > bound
+
+
+def test_bounded_search_no_candidate_under_bound():
+    rng = np.random.default_rng(15)
+    prob = W.random_problem(rng, 8, 3, 4, 2, mem_hi=10, cap=200)
+    lst = W.random_candidates(rng, prob, 50)
+    Tx, fx = dag.evaluate(prob, lst)
+    lo = int(Tx[fx].min())
+    assert dag.bounded_search(prob, lst, lo - 1)[0] is None
+    assert coracle.bounded(prob, lst, lo - 1)[0] is None
+    assert dag.bounded_search(prob, lst, lo)[0][1] == lo
+
+
+# -------------------------------------------------- planted mistakes
+
+def _wrong_warmup(S, M, s):
+    w = min(S - s + 1, M)
+    o = [("F", m) for m in range(1, w + 1)]
+    for i in range(1, M - w + 1):
+        o += [("F", w + i), ("B", i)]
+    return o + [("B", m) for m in range(M - w + 1, M + 1)]
+
+
+def _gpipe(S, M, s):
+    return [("F", m) for m in range(1, M + 1)] + [("B", m) for m in range(1, M + 1)]
+
+
+@pytest.mark.parametrize("mutant", [_wrong_warmup, _gpipe])
+def test_planted_schedule_mistakes_are_caught(mutant):
+    """A wrong intra-stage order must fail the worked examples."""
+    ex = json.load(open(os.path.join(GOLD, "worked_examples.json")))["examples"]
+    fails = 0
+    for e in ex:
+        g = dag.build_dag(e["S"], e["M"], order=mutant)
+        fails += dag.longest_path(g, e["F"], e["B"], e["cf"], e["cb"]) != e["T"]
+    assert fails > 0
+
+
+def test_planted_weight_mistakes_are_caught():
+    """Weight mix-ups planted in the DP's inputs (a boundary index reversed,
+    an edge weight dropped) are caught by the event-driven simulation on
+    random cases.  (Swapping F with B, or cf with cb, leaves T unchanged on
+    every random case tried, so such a swap is harmless to the makespan;
+    the per-node finish times of the worked examples still catch it.)"""
+    rng = np.random.default_rng(16)
+    mutants = {
+        "cb_reversed": lambda F, B, cf, cb: (F, B, cf, cb[::-1]),
+        "cf_reversed": lambda F, B, cf, cb: (F, B, cf[::-1], cb),
+        "cb_dropped": lambda F, B, cf, cb: (F, B, cf, 0 * cb),
+    }
+    caught = {k: False for k in mutants}
+    for _ in range(300):
+        S, M = int(rng.integers(3, 6)), int(rng.integers(2, 7))
+        F, B, cf, cb = _rand_case(rng, S, M)
+        ref = des.simulate_1f1b(S, M, F, B, cf, cb, dag.one_f_one_b_order)
+        assert T_of(S, M, F, B, cf, cb) == ref
+        for k, mut in mutants.items():
+            if T_of(S, M, *mut(F, B, cf, cb)) != ref:
+                caught[k] = True
+    assert all(caught.values()), caught
+
+
+def test_stage_weights_cover_exactly_the_stage_layers():
+    """With fwd[t][k] = 2^k + t * 2^40 a stage's sum spells out which layers
+    and which type it took: F_s = 2^{c_s} - 2^{c_{s-1}} + n_s t_s 2^40."""
+    L, S, T = 12, 4, 3
+    fwd = np.array([[2 ** k + t * 2 ** 40 for k in range(L)] for t in range(T)], dtype=object)
+    prob = W.Problem(L, S, 2, T, fwd, fwd, np.zeros(S - 1, np.uint32), np.zeros(S - 1, np.uint32),
+                     np.arange(1, L + 1, dtype=np.uint32), np.full(T, 10 ** 6, np.uint32), None)
+    rng = np.random.default_rng(17)
+    for _ in range(40):
+        r = int(rng.integers(0, math.comb(L - 1, S - 1)))
+        a = int(rng.integers(0, T ** S))
+        cuts, types = dag.unrank_composition(L, S, r), dag.assignment_row(prob, a)
+        assert a == sum(t * T ** (S - 1 - s) for s, t in enumerate(types))
+        F, B, MEM, _, _ = dag.stage_weights(prob, cuts, types)
+        b = [0] + list(cuts) + [L]
+        for s in range(S):
+            n = b[s + 1] - b[s]
+            assert F[s] == 2 ** b[s + 1] - 2 ** b[s] + n * types[s] * 2 ** 40
+            assert MEM[s] == sum(range(b[s] + 1, b[s + 1] + 1))
