@@ -1,0 +1,200 @@
+"""Throughput of the batched Poseidon DAG-cost evaluation on one MI355X.
+
+One step = one pass of the whole hot path over the workload's candidate
+list: decode every (composition rank, assignment) pair, build the stage
+weights from the LDS prefix tables, check the memory caps, take the longest
+path of the 1F1B DAG, write every makespan and the packed feasibility bits,
+and min-reduce to the best feasible candidate.  Inputs are resident in HBM
+before timing starts.
+
+Default workload: L=126 layers, S=16 stages, M=128 micro-batches, T=4
+device types, 2^24 sampled compositions (the largest of the five synthetic
+workloads).  Prints one JSON line.
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_INT32_TOPS = 256 * 64 * 2.4e9 / 1e12   # CUs x lanes x clock: one 32-bit op per lane per cycle
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_06086_amd", "csrc", "poseidon_kernels.hip")
+TRAFFIC = os.path.join(ROOT, "profiles", "eval_kernel_traffic_L126_S16_M128.json")
+
+
+def dp_ops(S, M):
+    """add/max operations of the DAG recurrence per candidate: three per node
+    (edge add, max, node add) minus the missing inputs of the first stage's
+    forwards, the last stage's backwards and each stage's first node."""
+    return 6 * S * M - 4 * M - S
+
+
+def kernel_sha():
+    h = hashlib.sha256()
+    for f in (KERNEL_SRC, os.path.join(ROOT, "paper_2609_06086_amd", "csrc", "poseidon_internal.h")):
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
+def traffic_per_launch():
+    """HBM bytes per launch from the committed rocprofv3 counter summary,
+    or None if the kernel source changed since it was taken."""
+    if not os.path.exists(TRAFFIC):
+        return None
+    t = json.load(open(TRAFFIC))
+    if t.get("kernel_source_sha256") != kernel_sha():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, target_s):
+    from oracle import coracle
+    coracle.lib()
+    threads = coracle.default_threads()
+    n = len(wl.cands)
+    probe = min(n, 20000)
+    t0 = time.perf_counter()
+    coracle.evaluate(wl.problem, wl.cands, nthreads=threads, lo=0, hi=probe)
+    dt = time.perf_counter() - t0
+    m = int(min(n, max(probe, probe * target_s / max(dt, 1e-6))))
+    t0 = time.perf_counter()
+    coracle.evaluate(wl.problem, wl.cands, nthreads=threads, lo=0, hi=m)
+    dt = time.perf_counter() - t0
+    return {"value": m / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {m} of the {n} candidates of the same workload, C oracle (explicit DAG, "
+                      f"Kahn order, topological DP) on {threads} host threads, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=5, choices=[3, 4, 5])
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run one plain device copy of this size (for counter scaling)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the evaluation of "
+              f"independent candidates would shard by index range, see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_06086_amd import poseidon as P
+    from paper_2609_06086_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    wl = W.workload(args.workload)
+    prob = wl.problem
+    n = len(wl.cands)
+    ctx = P.poseidon_load_costs(prob, 0)
+    if wl.cands.is_list:
+        cand = dict(comp_rank=torch.from_numpy(wl.cands.comp_rank.view(np.int64)).to(dev))
+        if wl.cands.assign_idx is not None:
+            cand["assign_idx"] = torch.from_numpy(wl.cands.assign_idx.view(np.int32)).to(dev)
+        in_bytes = 8 + (4 if wl.cands.assign_idx is not None else 0)
+    else:
+        cand = dict(first=wl.cands.first, count=wl.cands.count)
+        in_bytes = 0
+    Tout = torch.empty(n, dtype=torch.int32, device=dev)
+    bits = torch.empty((n + 31) // 32, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    if args.copy_calibration_mib:
+        a = torch.empty(args.copy_calibration_mib << 18, dtype=torch.int32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+
+    def step():
+        P.poseidon_eval_candidates(ctx, makespan_out=Tout, feasible_bits_out=bits, want_best=False,
+                                   stream=stream, **cand)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for e0, e1 in evs:
+        e0.record(stream)
+        step()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    best = P.poseidon_last_best(ctx, stream=stream)
+    kms = [e0.elapsed_time(e1) for e0, e1 in evs]
+    k_avg = sum(kms) / len(kms)
+    ms_per_step = wall * 1e3 / args.steps
+
+    S, M = prob.S, prob.M
+    ops = n * dp_ops(S, M)
+    achieved = ops / (k_avg * 1e-3) / 1e12
+    nodes_per_s = n * 2 * S * M / (ms_per_step * 1e-3)
+    value = n / (ms_per_step * 1e-3)
+    algo_bytes = n * in_bytes + n * 4 + ((n + 31) // 32) * 4
+
+    # early-stop pass (Eq. 2 bound) over the same list, warm-up bound from its first 500 entries
+    es = None
+    if wl.cands.is_list:
+        warm = {k: v[:500] for k, v in cand.items()}
+        wb = P.poseidon_eval_candidates(ctx, **warm)
+        bound = wb.makespan if wb.makespan is not None else 2 ** 31
+        reps = 5
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            bb, st = P.poseidon_eval_candidates_bounded(ctx, bound, chunk=1 << 22, stream=stream, **cand)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        es_ms = e0.elapsed_time(e1) / reps
+        es = {"ms": round(es_ms, 3), "candidates_per_s": n / (es_ms * 1e-3), "warmup_bound": bound,
+              "evaluated": st.evaluated, "pruned": st.pruned, "infeasible": st.infeasible,
+              "best_index": bb.index, "best_makespan": bb.makespan,
+              "same_argmin_as_exhaustive": (bb.index, bb.makespan) == (best.index, best.makespan),
+              "chunk": 1 << 22}
+
+    out = {
+        "metric": "candidate configs evaluated/sec + DAG nodes/sec (fraction of INT32 VALU peak)",
+        "value": value,
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic (seeded per-layer profile tables and sampled candidates)",
+        "config": {"workload": f"L={prob.L} S={S} M={M} T={prob.T}, {n} sampled compositions, fixed 4x4 "
+                               f"stage-type permutation" if args.workload == 5 else wl.description,
+                   "candidates_per_step": n, "dag_nodes_per_candidate": 2 * S * M,
+                   "parallelism": "single GPU"},
+        "dag_nodes_per_s": nodes_per_s,
+        "int32_valu_frac": achieved / PEAK_INT32_TOPS,
+        "best": {"index": best.index, "makespan_us": best.makespan},
+        "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_INT32_TOPS, "unit": "Top/s",
+                     "frac": achieved / PEAK_INT32_TOPS, "traffic": traffic_per_launch(),
+                     "kernel_ms": k_avg, "algorithmic_ops_per_launch": ops,
+                     "algorithmic_bytes_per_launch": algo_bytes},
+        "early_stop": es,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    ctx.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

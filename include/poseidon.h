@@ -1,0 +1,170 @@
+/*
+ * poseidon.h - batched evaluation of Poseidon's DAG-based training-time
+ * model over many pipeline configurations, with a min-reduction to the best
+ * one, on one AMD Instinct MI355X (gfx950).
+ *
+ * Model (Poseidon, arXiv 2609.06086, Sec. 4.1): a configuration places L
+ * layers onto S pipeline stages (a composition of L into S positive parts)
+ * and gives every stage a device type.  With M micro-batches, the 1F1B
+ * schedule is a DAG of forward nodes F_{s,m} and backward nodes B_{s,m}
+ * (Sec. 4.1.1), joined by inter-stage edges F_{s,m}->F_{s+1,m} and
+ * B_{s+1,m}->B_{s,m} that carry the activation-transfer time, and by
+ * zero-weight intra-stage edges along each stage's execution order
+ * (Sec. 4.1.2).  A node weighs the stage's summed per-layer compute time on
+ * its device type (Sec. 4.1.3).  The estimated iteration time T is the
+ * critical path, the heaviest start-to-end path counting node and edge
+ * weights (App. B.1).  A configuration is feasible when every stage's summed
+ * per-layer memory fits the memory of its device type (Sec. 3.2).  The
+ * search keeps the feasible configuration with the smallest T (Sec. 4.2.3);
+ * Eq. 2 / Theorem 1 give a per-configuration lower bound used to skip
+ * configurations that cannot beat the best one found so far.
+ *
+ * Stage s of S runs min(S - s, M) forward passes, then alternates one
+ * forward and one backward pass, then drains the remaining backward passes
+ * (the common 1F1B order; the paper does not spell out the warm-up length).
+ *
+ * All times are integer microseconds and all memory sizes integer MB, held
+ * in uint32; every result is exact integer arithmetic.
+ *
+ * Candidate indexing: compositions are ranked lexicographically by their
+ * sorted cut tuple (c_1 < ... < c_{S-1}, stage s holds layers
+ * [c_{s-1}, c_s) with c_0 = 0, c_S = L); assignment a is row a of the
+ * caller's table, or, without a table, the base-T digits of a with stage 1
+ * the most significant digit.  In range mode candidate i of a call is the
+ * joint index first + i = comp_rank * A + a; in list mode it is the pair
+ * (comp_rank[i], assign_idx[i]).  "index" in results is always i, the
+ * position within the call.
+ *
+ * Errors: 0 = OK, 1 = POSEIDON_NO_FEASIBLE (the call completed but no
+ * candidate qualified; best.index = UINT64_MAX), negative = error.  All
+ * argument checks happen before any HIP call; nothing aborts or throws
+ * across this interface.  A context is not thread-safe: use one per host
+ * thread / stream.  Calls enqueue work on `hip_stream` (a hipStream_t; NULL
+ * = the default stream); calls given a host result pointer synchronise that
+ * stream before returning.
+ */
+#ifndef POSEIDON_H
+#define POSEIDON_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define POSEIDON_S_MAX 16   /* stages */
+#define POSEIDON_L_MAX 256  /* layers */
+#define POSEIDON_T_MAX 8    /* device types */
+
+enum {
+    POSEIDON_OK = 0,
+    POSEIDON_NO_FEASIBLE = 1,
+    POSEIDON_E_INVAL = -1,   /* null pointer, bad size, type id >= T, ... */
+    POSEIDON_E_RANGE = -2,   /* a makespan could exceed 2^31, or a count 2^64 */
+    POSEIDON_E_DEVICE = -3,  /* a HIP call failed */
+    POSEIDON_E_NOMEM = -4    /* host or device allocation failed */
+};
+
+typedef struct poseidon_ctx poseidon_ctx;
+
+/* Per-layer profile of one model on T device types (Sec. 4.1.3): all
+ * HOST pointers, read during poseidon_load_costs only. */
+typedef struct {
+    uint32_t L, S, M, T;          /* 1 <= S <= min(L, S_MAX), M >= 1, 1 <= T <= T_MAX */
+    const uint32_t *fwd_us;       /* [T][L] forward time of layer l on type t */
+    const uint32_t *bwd_us;       /* [T][L] backward time */
+    const uint32_t *comm_fwd_us;  /* [S-1] weight of F_{b,m}->F_{b+1,m} (NULL iff S == 1) */
+    const uint32_t *comm_bwd_us;  /* [S-1] weight of B_{b+1,m}->B_{b,m} (NULL iff S == 1) */
+    const uint32_t *mem_mb;       /* [L] memory footprint of layer l */
+    const uint32_t *cap_mb;       /* [T] memory of one device of type t */
+    const uint8_t *assign;        /* [A][S] allowed stage->type rows, or NULL = all T^S */
+    uint64_t A;                   /* rows of `assign` (ignored when assign == NULL) */
+} poseidon_problem;
+
+/* Candidates of one call.  comp_rank == NULL: range mode over joint indices
+ * [first, first + count).  Otherwise list mode: `count` DEVICE arrays
+ * comp_rank[count] (uint64) and assign_idx[count] (uint32, or NULL meaning
+ * assignment 0); `first` is ignored.  count < 2^32 per call. */
+typedef struct {
+    uint64_t first, count;
+    const uint64_t *comp_rank;
+    const uint32_t *assign_idx;
+} poseidon_cands;
+
+typedef struct {
+    uint64_t index;     /* position within the call, UINT64_MAX if none */
+    uint32_t makespan;  /* critical-path length T in microseconds */
+    uint32_t feasible;  /* 1 if every stage fits its memory cap */
+} poseidon_best;
+
+typedef struct {
+    uint64_t evaluated;   /* feasible candidates whose DAG was evaluated */
+    uint64_t pruned;      /* feasible candidates skipped by the Eq. 2 bound */
+    uint64_t infeasible;  /* candidates over a memory cap (never evaluated) */
+} poseidon_prune_stats;
+
+/* Check a problem without touching the GPU and return the number of
+ * candidates C(L-1, S-1) * A (Sec. 4.2.3: the search space of layer
+ * allocations and device assignments).  Pure host code. */
+int poseidon_validate(const poseidon_problem *problem, uint64_t *n_candidates);
+
+/* Copy the profile tables to device `hip_device` and build the lookup
+ * tables every candidate evaluation shares: per-type prefix sums of the
+ * per-layer costs and memory, the Pascal table used to unrank compositions,
+ * and the schedule of the 1F1B DAG for (S, M) (Sec. 5: the DAG depends only
+ * on the pipeline depth, so it is built once and only re-weighted).  Fails
+ * with POSEIDON_E_RANGE if some candidate's makespan could reach 2^31.  The
+ * caller may free the host tables after return; the context owns its device
+ * memory until poseidon_free. */
+int poseidon_load_costs(const poseidon_problem *problem, int hip_device, poseidon_ctx **out);
+
+/* Evaluate every candidate of `cands` (Sec. 4.1: stage weights, longest path
+ * of the 1F1B DAG; Sec. 3.2 memory feasibility) and reduce to the feasible
+ * candidate with the smallest makespan, ties to the smaller index.
+ * makespan_out: DEVICE uint32[count] or NULL; gets every candidate's raw T,
+ *   feasible or not.
+ * feasible_bits_out: DEVICE uint32[ceil(count/32)] or NULL; bit i % 32 of
+ *   word i / 32 is candidate i's feasibility.
+ * best_out: HOST pointer or NULL.  Non-NULL synchronises the stream and
+ *   returns the best; NULL leaves it on the device for
+ *   poseidon_last_best.  Returns POSEIDON_NO_FEASIBLE if no candidate fits. */
+int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands,
+                             uint32_t *makespan_out, uint32_t *feasible_bits_out,
+                             poseidon_best *best_out, void *hip_stream);
+
+/* Result of the most recent poseidon_eval_candidates on this context
+ * (synchronises the stream). */
+int poseidon_last_best(poseidon_ctx *ctx, poseidon_best *best_out, void *hip_stream);
+
+/* Early-stop search (Eq. 2, Theorem 1).  The candidates are processed in
+ * consecutive chunks of `chunk` entries (0 = one chunk).  Within a chunk,
+ * a feasible candidate whose lower bound max_x g(S_x) exceeds
+ * b = min(bound, best makespan found in earlier chunks) is skipped; all
+ * other feasible candidates are evaluated exactly.  The reduction is the
+ * same as poseidon_eval_candidates', over evaluated candidates; if its
+ * makespan is > bound the call returns POSEIDON_NO_FEASIBLE.  The result
+ * is deterministic for a given chunk size.  best_out and stats_out are HOST
+ * pointers (either may be NULL); the call synchronises the stream. */
+int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *cands,
+                                     uint32_t bound, uint64_t chunk, poseidon_best *best_out,
+                                     poseidon_prune_stats *stats_out, void *hip_stream);
+
+/* Argmin over arrays a previous evaluation wrote (DEVICE pointers,
+ * `count` entries, layouts as for poseidon_eval_candidates; feasible_bits
+ * may be NULL = all feasible).  best_out->index = index_base + position.
+ * HOST best_out, required; synchronises the stream. */
+int poseidon_argmin(poseidon_ctx *ctx, const uint32_t *makespan, const uint32_t *feasible_bits,
+                    uint64_t count, uint64_t index_base, poseidon_best *best_out,
+                    void *hip_stream);
+
+/* Release the context's device memory.  NULL is ignored. */
+void poseidon_free(poseidon_ctx *ctx);
+
+/* Static text for a status code. */
+const char *poseidon_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* POSEIDON_H */

@@ -1,0 +1,540 @@
+// C-ABI of the batched Poseidon DAG-cost evaluator (declared in poseidon.h).
+//
+// Host side: argument validation (no HIP call before it completes), the
+// lookup tables shared by every evaluation, launch sizing, and the chunk
+// loop of the early-stop search.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+#include <vector>
+
+#include "../../include/poseidon.h"
+#include "poseidon_internal.h"
+
+namespace {
+
+// device state words of a context (one u64 each)
+enum { W_ACC = 0, W_RESULT, W_RUN, W_STAT_EVAL, W_STAT_PRUNED, W_STAT_INFEAS, W_ERR, W_DONE, W_COUNT };
+
+uint64_t binom_sat(uint64_t n, uint64_t k) {
+    // exact C(n, k) for small k, saturating at UINT64_MAX
+    if (k > n) return 0;
+    k = std::min(k, n - k);
+    unsigned __int128 c = 1;
+    for (uint64_t i = 1; i <= k; ++i) {
+        c = c * (n - k + i) / i;
+        if (c > (unsigned __int128)UINT64_MAX) return UINT64_MAX;
+    }
+    return (uint64_t)c;
+}
+
+bool pow_fits(uint64_t base, uint64_t e, uint64_t limit, uint64_t *out) {
+    unsigned __int128 v = 1;
+    for (uint64_t i = 0; i < e; ++i) {
+        v *= base;
+        if (v > limit) return false;
+    }
+    *out = (uint64_t)v;
+    return true;
+}
+
+uint32_t next_pow2(uint32_t x) {
+    uint32_t p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+// 1F1B order of stage s (1-based): min(S-s, M) forwards, then alternating
+// forward / backward, then the remaining backwards.  Kind 0 = F, 1 = B.
+void stage_order(int S, int M, int s, std::vector<std::pair<int, int>> &o) {
+    o.clear();
+    const int w = std::min(S - s, M);
+    for (int m = 1; m <= w; ++m) o.push_back({0, m});
+    for (int i = 1; i <= M - w; ++i) {
+        o.push_back({0, w + i});
+        o.push_back({1, i});
+    }
+    for (int m = M - w + 1; m <= M; ++m) o.push_back({1, m});
+}
+
+// Unit-weight as-soon-as-possible slots of every node of the 1F1B DAG; fills
+// per-slot stage masks and checks the property the register stencil relies
+// on: at most one node per stage per slot, and every cross-stage predecessor
+// is still the newest node of its stage at the end of the previous slot.
+bool build_slots(int S, int M, std::vector<uint32_t> *masks, uint32_t *nslots) {
+    std::vector<std::vector<std::pair<int, int>>> ord(S + 1);
+    for (int s = 1; s <= S; ++s) stage_order(S, M, s, ord[s]);
+    // finish slot of F_{s,m} / B_{s,m}
+    std::vector<int> finF((size_t)(S + 2) * (M + 1), -1), finB((size_t)(S + 2) * (M + 1), -1);
+    auto at = [M](int s, int m) { return (size_t)s * (M + 1) + m; };
+    std::vector<int> pos(S + 1, 0), slot_of_last(S + 1, 0);
+    std::vector<int> startF(finF.size(), -1), startB(finB.size(), -1);
+    int placed = 0, total = 2 * S * M;
+    while (placed < total) {
+        bool progress = false;
+        for (int s = 1; s <= S; ++s) {
+            while (pos[s] < 2 * M) {
+                const int kind = ord[s][pos[s]].first, m = ord[s][pos[s]].second;
+                int ready = pos[s] ? slot_of_last[s] : 0;
+                int dep = 0;
+                if (kind == 0 && s > 1) dep = finF[at(s - 1, m)];
+                if (kind == 1 && s < S) dep = finB[at(s + 1, m)];
+                if (dep < 0) break;
+                const int st = std::max(ready, dep);
+                if (kind == 0) { startF[at(s, m)] = st; finF[at(s, m)] = st + 1; }
+                else { startB[at(s, m)] = st; finB[at(s, m)] = st + 1; }
+                slot_of_last[s] = st + 1;
+                ++pos[s];
+                ++placed;
+                progress = true;
+            }
+        }
+        if (!progress) return false;
+    }
+    const int n = 2 * (M + S - 1);
+    std::vector<uint32_t> fm(n, 0), bm(n, 0);
+    // newest node per stage per slot: kind*2^20 + m
+    for (int s = 1; s <= S; ++s)
+        for (int m = 1; m <= M; ++m) {
+            const int a = startF[at(s, m)], b = startB[at(s, m)];
+            if (a < 0 || b < 0 || a >= n || b >= n) return false;
+            if ((fm[a] | bm[a]) >> (s - 1) & 1u) return false;
+            fm[a] |= 1u << (s - 1);
+            if ((fm[b] | bm[b]) >> (s - 1) & 1u) return false;
+            bm[b] |= 1u << (s - 1);
+        }
+    // stencil property: the input of F_{s,m} (F_{s-1,m}) must be the newest
+    // node of stage s-1 at slot start(F_{s,m}) - 1, likewise for B.
+    for (int s = 1; s <= S; ++s) {
+        int k = 0;
+        for (const auto &node : ord[s]) {
+            (void)k;
+            const int kind = node.first, m = node.second;
+            const int st = kind == 0 ? startF[at(s, m)] : startB[at(s, m)];
+            int u = kind == 0 ? s - 1 : s + 1;
+            if (u < 1 || u > S) continue;
+            const int ust = kind == 0 ? startF[at(u, m)] : startB[at(u, m)];
+            if (ust >= st) return false;
+            // no node of stage u may start in (ust, st)
+            for (int q = ust + 1; q < st; ++q)
+                if ((fm[q] | bm[q]) >> (u - 1) & 1u) return false;
+        }
+    }
+    if (masks) {
+        masks->assign(2 * (size_t)n, 0);
+        for (int k = 0; k < n; ++k) {
+            (*masks)[2 * k] = fm[k];
+            (*masks)[2 * k + 1] = bm[k];
+        }
+    }
+    *nslots = (uint32_t)n;
+    return true;
+}
+
+// The closed-form slot pattern the fast kernel path hard-codes, checked
+// against the simulated schedule (M >= S).
+bool closed_form_matches(int S, int M, const std::vector<uint32_t> &masks) {
+    const int n = 2 * (M + S - 1);
+    for (int k = 0; k < n; ++k) {
+        for (int s = 1; s <= S; ++s) {
+            int op;
+            if (k < 2 * S - 1) op = pk::prologue_op(S, s, k);
+            else if (k <= 2 * M - 1) op = ((k - s - 1) & 1) == 0 ? 1 : 2;
+            else op = pk::epilogue_op(S, s, k - 2 * M);
+            const int f = (masks[2 * k] >> (s - 1)) & 1u, b = (masks[2 * k + 1] >> (s - 1)) & 1u;
+            const int sim = f ? 1 : (b ? 2 : 0);
+            if (sim != op) return false;
+        }
+    }
+    return true;
+}
+
+}  // namespace
+
+struct poseidon_ctx {
+    int device;
+    uint32_t L, S, M, T;
+    uint64_t A, n_comp;
+    bool wide;
+    uint32_t NB;
+    pk::KParams base;      // table pointers and problem constants
+    void *dmem;
+    unsigned long long *state;
+    size_t lds_bytes;
+    uint32_t grid_max;
+};
+
+extern "C" {
+
+const char *poseidon_strerror(int status) {
+    switch (status) {
+    case POSEIDON_OK: return "ok";
+    case POSEIDON_NO_FEASIBLE: return "no candidate satisfies the memory caps (or the bound)";
+    case POSEIDON_E_INVAL: return "invalid argument";
+    case POSEIDON_E_RANGE: return "value out of range (makespan could reach 2^31, or count overflow)";
+    case POSEIDON_E_DEVICE: return "HIP device error";
+    case POSEIDON_E_NOMEM: return "out of memory";
+    default: return "unknown status";
+    }
+}
+
+int poseidon_validate(const poseidon_problem *p, uint64_t *n_candidates) {
+    if (!p) return POSEIDON_E_INVAL;
+    if (p->S < 1 || p->S > POSEIDON_S_MAX || p->L < p->S || p->L > POSEIDON_L_MAX || p->M < 1 || p->T < 1 ||
+        p->T > POSEIDON_T_MAX)
+        return POSEIDON_E_INVAL;
+    if (!p->fwd_us || !p->bwd_us || !p->mem_mb || !p->cap_mb) return POSEIDON_E_INVAL;
+    if (p->S > 1 && (!p->comm_fwd_us || !p->comm_bwd_us)) return POSEIDON_E_INVAL;
+    uint64_t A;
+    if (p->assign) {
+        if (p->A < 1 || p->A > (1ull << 32)) return p->A < 1 ? POSEIDON_E_INVAL : POSEIDON_E_RANGE;
+        for (uint64_t i = 0; i < p->A * p->S; ++i)
+            if (p->assign[i] >= p->T) return POSEIDON_E_INVAL;
+        A = p->A;
+    } else if (!pow_fits(p->T, p->S, 1ull << 32, &A)) {
+        return POSEIDON_E_RANGE;
+    }
+    const uint64_t nc = binom_sat(p->L - 1, p->S - 1);
+    if (nc == UINT64_MAX) return POSEIDON_E_RANGE;
+    unsigned __int128 tot = (unsigned __int128)nc * A;
+    if (tot > (unsigned __int128)UINT64_MAX - 1) return POSEIDON_E_RANGE;
+    // Every path weight is at most the sum of all node and edge weights:
+    // M * (sum over layers of the slowest type's fwd + bwd + all transfers).
+    unsigned __int128 w = 0;
+    for (uint32_t l = 0; l < p->L; ++l) {
+        uint64_t mx = 0;
+        for (uint32_t t = 0; t < p->T; ++t)
+            mx = std::max<uint64_t>(mx, (uint64_t)p->fwd_us[(size_t)t * p->L + l] + p->bwd_us[(size_t)t * p->L + l]);
+        w += mx;
+    }
+    for (uint32_t b = 0; b + 1 < p->S; ++b) w += (uint64_t)p->comm_fwd_us[b] + p->comm_bwd_us[b];
+    w *= p->M;
+    if (w >= ((unsigned __int128)1 << 31)) return POSEIDON_E_RANGE;
+    unsigned __int128 mem = 0;
+    for (uint32_t l = 0; l < p->L; ++l) mem += p->mem_mb[l];
+    if (mem >= ((unsigned __int128)1 << 32)) return POSEIDON_E_RANGE;
+    if (n_candidates) *n_candidates = (uint64_t)tot;
+    return POSEIDON_OK;
+}
+
+int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx **out) {
+    if (!out) return POSEIDON_E_INVAL;
+    *out = nullptr;
+    uint64_t ncand = 0;
+    int rc = poseidon_validate(p, &ncand);
+    if (rc != POSEIDON_OK) return rc;
+    const uint32_t L = p->L, S = p->S, M = p->M, T = p->T;
+    const uint64_t n_comp = binom_sat(L - 1, S - 1);
+    const uint64_t A = n_comp ? ncand / n_comp : 0;
+    const bool wide = n_comp > 0xFFFFFFFFull;
+    const uint32_t NB = next_pow2(L);
+
+    // schedule of the DAG: closed form for M >= S (self-checked), table otherwise
+    std::vector<uint32_t> masks;
+    uint32_t nslots = 0;
+    const bool table_path = M < S;
+    if (table_path || (uint64_t)S * M <= 4096) {
+        if (!build_slots((int)S, (int)M, &masks, &nslots)) return POSEIDON_E_INVAL;
+        if (!table_path && !closed_form_matches((int)S, (int)M, masks)) return POSEIDON_E_INVAL;
+    }
+
+    // host images of the device tables
+    std::vector<uint64_t> cost((size_t)T * (L + 1));
+    for (uint32_t t = 0; t < T; ++t) {
+        uint64_t f = 0, b = 0;
+        cost[(size_t)t * (L + 1)] = 0;
+        for (uint32_t l = 0; l < L; ++l) {
+            f += p->fwd_us[(size_t)t * L + l];
+            b += p->bwd_us[(size_t)t * L + l];
+            cost[(size_t)t * (L + 1) + l + 1] = (b << 32) | f;
+        }
+    }
+    std::vector<uint32_t> pm(L + 1, 0);
+    for (uint32_t l = 0; l < L; ++l) pm[l + 1] = pm[l] + p->mem_mb[l];
+    const size_t rsz = wide ? 8 : 4;
+    std::vector<unsigned char> binom((size_t)S * NB * rsz);
+    for (uint32_t k = 0; k < S; ++k)
+        for (uint32_t n = 0; n < NB; ++n) {
+            uint64_t v = binom_sat(n, k);
+            if (wide) memcpy(&binom[((size_t)k * NB + n) * 8], &v, 8);
+            else {
+                uint32_t v32 = v > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)v;
+                memcpy(&binom[((size_t)k * NB + n) * 4], &v32, 4);
+            }
+        }
+
+    pk::KParams kp;
+    memset(&kp, 0, sizeof(kp));
+    kp.A = A;
+    kp.n_comp = n_comp;
+    kp.L = L; kp.S = S; kp.M = M; kp.T = T; kp.NB = NB;
+    kp.wide = wide;
+    for (uint32_t b = 0; b + 1 < S; ++b) { kp.cf[b] = p->comm_fwd_us[b]; kp.cb[b] = p->comm_bwd_us[b]; }
+    const bool has_table = p->assign && A > 1;
+    if (A == 1) {
+        kp.assign_mode = pk::kAssignFixed;
+        for (uint32_t s = 0; s < S; ++s) kp.fixed_types[s] = p->assign ? p->assign[s] : 0;
+    } else if (has_table) {
+        kp.assign_mode = pk::kAssignTable;
+    } else {
+        kp.assign_mode = pk::kAssignDigits;
+        kp.magicT = (uint32_t)((1ull << 32) / T + 1);
+    }
+
+    // one device block: state words | cost | pm | cap | binom | assign | slots
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    size_t off = 0;
+    const size_t o_state = off; off = al(off + W_COUNT * 8);
+    const size_t o_cost = off; off = al(off + cost.size() * 8);
+    const size_t o_pm = off; off = al(off + pm.size() * 4);
+    const size_t o_cap = off; off = al(off + (size_t)T * 4);
+    const size_t o_binom = off; off = al(off + binom.size());
+    const size_t o_assign = off; off = al(off + (has_table ? (size_t)A * S : 0));
+    const size_t o_slots = off; off = al(off + (table_path ? masks.size() * 4 : 0));
+    const size_t total = off;
+
+    poseidon_ctx *ctx = new (std::nothrow) poseidon_ctx;
+    if (!ctx) return POSEIDON_E_NOMEM;
+    memset(ctx, 0, sizeof(*ctx));
+    int prev = 0;
+    if (hipGetDevice(&prev) != hipSuccess || hipSetDevice(hip_device) != hipSuccess) {
+        delete ctx;
+        return POSEIDON_E_DEVICE;
+    }
+    int status = POSEIDON_OK;
+    void *d = nullptr;
+    do {
+        if (hipMalloc(&d, total) != hipSuccess) { status = POSEIDON_E_NOMEM; break; }
+        unsigned char *b = (unsigned char *)d;
+        std::vector<unsigned long long> st(W_COUNT, 0);
+        st[W_ACC] = ~0ull; st[W_RESULT] = ~0ull; st[W_RUN] = ~0ull;
+        bool ok = hipMemcpy(b + o_state, st.data(), W_COUNT * 8, hipMemcpyHostToDevice) == hipSuccess &&
+                  hipMemcpy(b + o_cost, cost.data(), cost.size() * 8, hipMemcpyHostToDevice) == hipSuccess &&
+                  hipMemcpy(b + o_pm, pm.data(), pm.size() * 4, hipMemcpyHostToDevice) == hipSuccess &&
+                  hipMemcpy(b + o_cap, p->cap_mb, (size_t)T * 4, hipMemcpyHostToDevice) == hipSuccess &&
+                  hipMemcpy(b + o_binom, binom.data(), binom.size(), hipMemcpyHostToDevice) == hipSuccess;
+        if (ok && has_table)
+            ok = hipMemcpy(b + o_assign, p->assign, (size_t)A * S, hipMemcpyHostToDevice) == hipSuccess;
+        if (ok && table_path)
+            ok = hipMemcpy(b + o_slots, masks.data(), masks.size() * 4, hipMemcpyHostToDevice) == hipSuccess;
+        if (!ok) { status = POSEIDON_E_DEVICE; break; }
+        kp.cost = (const uint64_t *)(b + o_cost);
+        kp.pm = (const uint32_t *)(b + o_pm);
+        kp.cap = (const uint32_t *)(b + o_cap);
+        kp.binom = b + o_binom;
+        kp.assign = has_table ? (const uint8_t *)(b + o_assign) : nullptr;
+        kp.slot_mask = table_path ? (const uint32_t *)(b + o_slots) : nullptr;
+        kp.nslots = table_path ? nslots : 0;
+        ctx->state = (unsigned long long *)(b + o_state);
+        kp.acc = ctx->state + W_ACC;
+        kp.result = ctx->state + W_RESULT;
+        kp.run_best = ctx->state + W_RUN;
+        kp.stats = ctx->state + W_STAT_EVAL;
+        kp.err = (unsigned int *)(ctx->state + W_ERR);
+        kp.done = (unsigned int *)(ctx->state + W_DONE);
+        const size_t lds = ((cost.size() * 8 + binom.size() + pm.size() * 4 + (size_t)T * 4) + 15) & ~(size_t)15;
+        if (lds > 64 * 1024) { status = POSEIDON_E_RANGE; break; }
+        int occ = 0;
+        hipDeviceProp_t prop;
+        if (pk::eval_occupancy(S, wide, lds, &occ) != hipSuccess || hipGetDeviceProperties(&prop, hip_device) != hipSuccess) {
+            status = POSEIDON_E_DEVICE;
+            break;
+        }
+        ctx->lds_bytes = lds;
+        ctx->grid_max = (uint32_t)std::max(1, occ) * (uint32_t)std::max(1, prop.multiProcessorCount);
+    } while (0);
+    (void)hipSetDevice(prev);
+    if (status != POSEIDON_OK) {
+        if (d) (void)hipFree(d);
+        delete ctx;
+        return status;
+    }
+    ctx->device = hip_device;
+    ctx->L = L; ctx->S = S; ctx->M = M; ctx->T = T;
+    ctx->A = A; ctx->n_comp = n_comp; ctx->wide = wide; ctx->NB = NB;
+    ctx->base = kp;
+    ctx->dmem = d;
+    *out = ctx;
+    return POSEIDON_OK;
+}
+
+void poseidon_free(poseidon_ctx *ctx) {
+    if (!ctx) return;
+    int prev = 0;
+    if (hipGetDevice(&prev) == hipSuccess && hipSetDevice(ctx->device) == hipSuccess) {
+        (void)hipFree(ctx->dmem);
+        (void)hipSetDevice(prev);
+    }
+    delete ctx;
+}
+
+}  // extern "C"
+
+namespace {
+
+int check_cands(const poseidon_ctx *ctx, const poseidon_cands *c) {
+    if (!ctx || !c) return POSEIDON_E_INVAL;
+    if (c->count >= (1ull << 32)) return POSEIDON_E_RANGE;
+    if (!c->comp_rank) {
+        if (c->assign_idx) return POSEIDON_E_INVAL;
+        const unsigned __int128 tot = (unsigned __int128)ctx->n_comp * ctx->A;
+        if ((unsigned __int128)c->first + c->count > tot) return POSEIDON_E_INVAL;
+    }
+    return POSEIDON_OK;
+}
+
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = false;
+    explicit DeviceGuard(int dev) {
+        ok = hipGetDevice(&prev) == hipSuccess && hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+int read_best(poseidon_ctx *ctx, hipStream_t st, unsigned long long word_index, poseidon_best *best) {
+    unsigned long long w[W_COUNT];
+    if (hipMemcpyAsync(w, ctx->state, sizeof(w), hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+        return POSEIDON_E_DEVICE;
+    if (w[W_ERR] & 0xFFFFFFFFull) {
+        const unsigned long long zero = 0;
+        (void)hipMemcpy(ctx->state + W_ERR, &zero, 8, hipMemcpyHostToDevice);
+        return POSEIDON_E_INVAL;
+    }
+    const unsigned long long k = w[word_index];
+    if (k == ~0ull || (k >> 32) == 0xFFFFFFFFull) {
+        best->index = UINT64_MAX;
+        best->makespan = 0xFFFFFFFFu;
+        best->feasible = 0;
+        return POSEIDON_NO_FEASIBLE;
+    }
+    best->index = k & 0xFFFFFFFFull;
+    best->makespan = (uint32_t)(k >> 32);
+    best->feasible = 1;
+    return POSEIDON_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands, uint32_t *makespan_out,
+                             uint32_t *feasible_bits_out, poseidon_best *best_out, void *hip_stream) {
+    int rc = check_cands(ctx, cands);
+    if (rc != POSEIDON_OK) return rc;
+    hipStream_t st = (hipStream_t)hip_stream;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return POSEIDON_E_DEVICE;
+    if (cands->count == 0) {
+        // nothing to evaluate: publish an empty result
+        if (pk::launch_fill(ctx->base.result, 1, ~0ull, st) != hipSuccess) return POSEIDON_E_DEVICE;
+        if (best_out) return read_best(ctx, st, W_RESULT, best_out);
+        return POSEIDON_OK;
+    }
+    pk::KParams kp = ctx->base;
+    kp.first = cands->first;
+    kp.count = cands->count;
+    kp.comp_rank = cands->comp_rank;
+    kp.assign_idx = cands->assign_idx;
+    kp.makespan_out = makespan_out;
+    kp.feas_bits_out = feasible_bits_out;
+    kp.nwords = (cands->count + 31) / 32;
+    pk::LaunchCfg lc;
+    lc.lds_bytes = ctx->lds_bytes;
+    const uint64_t want = (cands->count + 255) / 256;
+    lc.grid = (uint32_t)std::min<uint64_t>(want, ctx->grid_max);
+    if (pk::launch_eval(kp, lc, st) != hipSuccess) return POSEIDON_E_DEVICE;
+    if (best_out) return read_best(ctx, st, W_RESULT, best_out);
+    return POSEIDON_OK;
+}
+
+int poseidon_last_best(poseidon_ctx *ctx, poseidon_best *best_out, void *hip_stream) {
+    if (!ctx || !best_out) return POSEIDON_E_INVAL;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return POSEIDON_E_DEVICE;
+    return read_best(ctx, (hipStream_t)hip_stream, W_RESULT, best_out);
+}
+
+int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *cands, uint32_t bound,
+                                     uint64_t chunk, poseidon_best *best_out, poseidon_prune_stats *stats_out,
+                                     void *hip_stream) {
+    int rc = check_cands(ctx, cands);
+    if (rc != POSEIDON_OK) return rc;
+    hipStream_t st = (hipStream_t)hip_stream;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return POSEIDON_E_DEVICE;
+    // re-arm the running best and the counters (a fill kernel, not a memset)
+    if (pk::launch_fill(ctx->state + W_RUN, 1, ~0ull, st) != hipSuccess ||
+        pk::launch_fill(ctx->state + W_STAT_EVAL, 3, 0ull, st) != hipSuccess)
+        return POSEIDON_E_DEVICE;
+    pk::KParams kp = ctx->base;
+    kp.first = cands->first;
+    kp.count = cands->count;
+    kp.comp_rank = cands->comp_rank;
+    kp.assign_idx = cands->assign_idx;
+    pk::LaunchCfg lc;
+    lc.lds_bytes = ctx->lds_bytes;
+    lc.grid = 0;
+    const uint64_t n = cands->count;
+    if (chunk == 0 || chunk > n) chunk = n;
+    for (uint64_t lo = 0; lo < n; lo += chunk) {
+        const uint64_t hi = std::min(n, lo + chunk);
+        if (pk::launch_bounded(kp, lc, st, lo, hi, bound) != hipSuccess) return POSEIDON_E_DEVICE;
+    }
+    unsigned long long w[W_COUNT];
+    if (hipMemcpyAsync(w, ctx->state, sizeof(w), hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+        return POSEIDON_E_DEVICE;
+    if (stats_out) {
+        stats_out->evaluated = w[W_STAT_EVAL];
+        stats_out->pruned = w[W_STAT_PRUNED];
+        stats_out->infeasible = w[W_STAT_INFEAS];
+    }
+    if (w[W_ERR] & 0xFFFFFFFFull) {
+        const unsigned long long zero = 0;
+        (void)hipMemcpy(ctx->state + W_ERR, &zero, 8, hipMemcpyHostToDevice);
+        return POSEIDON_E_INVAL;
+    }
+    const unsigned long long k = w[W_RUN];
+    poseidon_best b;
+    int out;
+    if (k == ~0ull || (uint32_t)(k >> 32) > bound) {
+        b.index = UINT64_MAX; b.makespan = 0xFFFFFFFFu; b.feasible = 0;
+        out = POSEIDON_NO_FEASIBLE;
+    } else {
+        b.index = k & 0xFFFFFFFFull; b.makespan = (uint32_t)(k >> 32); b.feasible = 1;
+        out = POSEIDON_OK;
+    }
+    if (best_out) *best_out = b;
+    return out;
+}
+
+int poseidon_argmin(poseidon_ctx *ctx, const uint32_t *makespan, const uint32_t *feasible_bits, uint64_t count,
+                    uint64_t index_base, poseidon_best *best_out, void *hip_stream) {
+    if (!ctx || !makespan || !best_out) return POSEIDON_E_INVAL;
+    if (count >= (1ull << 32)) return POSEIDON_E_RANGE;
+    hipStream_t st = (hipStream_t)hip_stream;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return POSEIDON_E_DEVICE;
+    if (count == 0) {
+        if (pk::launch_fill(ctx->base.result, 1, ~0ull, st) != hipSuccess) return POSEIDON_E_DEVICE;
+    } else {
+        const uint32_t grid = (uint32_t)std::min<uint64_t>((count + 255) / 256, 1024);
+        if (pk::launch_argmin(makespan, feasible_bits, count, grid, ctx->base.acc, ctx->base.done, ctx->base.result,
+                              st) != hipSuccess)
+            return POSEIDON_E_DEVICE;
+    }
+    int rc = read_best(ctx, st, W_RESULT, best_out);
+    if (rc == POSEIDON_OK) best_out->index += index_base;
+    return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,60 @@
+// Internal interface between the C-ABI host code and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pk {
+
+constexpr int kSMax = 16;
+
+enum AssignMode : uint32_t { kAssignFixed = 0, kAssignTable = 1, kAssignDigits = 2 };
+
+// Kernel arguments, passed by value (uniform values land in SGPRs).
+struct KParams {
+    // device tables owned by the context
+    const uint64_t *cost;      // [T][L+1] (prefix bwd << 32) | prefix fwd
+    const uint32_t *pm;        // [L+1] prefix memory
+    const uint32_t *cap;       // [T]
+    const void *binom;         // [S][NB] C(n, k), uint32 or uint64 (wide)
+    const uint8_t *assign;     // [A][S] (table mode)
+    const uint32_t *slot_mask; // [nslots][2] forward / backward stage masks (M < S)
+    uint64_t A, n_comp;
+    uint32_t L, S, M, T, NB, nslots;
+    uint32_t magicT, assign_mode;
+    uint32_t wide;
+    uint32_t cf[kSMax], cb[kSMax];
+    uint8_t fixed_types[kSMax];
+    // candidates of the call
+    uint64_t first, count;
+    const uint64_t *comp_rank;
+    const uint32_t *assign_idx;
+    // outputs
+    uint32_t *makespan_out;
+    uint32_t *feas_bits_out;
+    uint64_t nwords;
+    // reduction state (device words owned by the context)
+    unsigned long long *acc;
+    unsigned int *done;
+    unsigned long long *result;
+    unsigned long long *run_best;
+    unsigned long long *stats;   // evaluated, pruned, infeasible
+    unsigned int *err;
+};
+
+struct LaunchCfg {
+    uint32_t grid;
+    size_t lds_bytes;
+};
+
+hipError_t launch_eval(const KParams &p, const LaunchCfg &lc, hipStream_t st);
+hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
+                          uint32_t bound);
+hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, int *blocks);
+hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,
+                         unsigned long long *acc, unsigned int *done, unsigned long long *result, hipStream_t st);
+hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, hipStream_t st);
+int prologue_op(int S, int s, int k);
+int epilogue_op(int S, int s, int j);
+
+}  // namespace pk

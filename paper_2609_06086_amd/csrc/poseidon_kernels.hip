@@ -1,0 +1,555 @@
+// Device code for batched evaluation of Poseidon's 1F1B-DAG training-time
+// model on gfx950 (CDNA4), one candidate configuration per lane.
+//
+// Per lane the path is:
+//   (a1) decode: index -> (composition rank, assignment) -> cut points, types
+//   (a2) stage weights from per-type prefix sums held in LDS, memory check
+//   (a3) the longest path of the 1F1B DAG as a register stencil
+//   (a4) a wave / block / grid min-reduction of (makespan, index) keys
+// and, for the early-stop variant, (a5) the Eq. 2 lower bound with
+// block-local compaction of the surviving candidates.
+//
+// The DAG's longest path is integer add/max work with no contraction, so
+// it runs on the VALU; there is nothing here for the matrix cores.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "poseidon_internal.h"
+
+namespace pk {
+
+constexpr int kBlock = 256;            // 4 waves of 64
+constexpr int kWaves = kBlock / 64;
+constexpr int kTile = 4096;            // candidates filtered per block (early stop)
+
+// ---------------------------------------------------------------------------
+// LDS image of the context's tables (one copy per block)
+// ---------------------------------------------------------------------------
+template <typename R>
+struct Lds {
+    const uint64_t *cost;   // [T][L+1]  (prefix bwd << 32) | prefix fwd
+    const uint32_t *pm;     // [L+1]     prefix memory
+    const uint32_t *cap;    // [T]
+    const R *binom;         // [S][NB]   C(n, k), saturated to R's maximum
+};
+
+template <typename R>
+__device__ __forceinline__ Lds<R> stage_tables(const KParams &p, unsigned char *smem) {
+    // layout: cost (8-byte aligned) | binom | pm | cap
+    uint64_t *cost = reinterpret_cast<uint64_t *>(smem);
+    const uint32_t ncost = p.T * (p.L + 1);
+    R *binom = reinterpret_cast<R *>(cost + ncost);
+    const uint32_t nbin = p.S * p.NB;
+    uint32_t *pm = reinterpret_cast<uint32_t *>(binom + nbin);
+    uint32_t *cap = pm + (p.L + 1);
+    for (uint32_t i = threadIdx.x; i < ncost; i += kBlock) cost[i] = p.cost[i];
+    const R *gb = reinterpret_cast<const R *>(p.binom);
+    for (uint32_t i = threadIdx.x; i < nbin; i += kBlock) binom[i] = gb[i];
+    for (uint32_t i = threadIdx.x; i <= p.L; i += kBlock) pm[i] = p.pm[i];
+    for (uint32_t i = threadIdx.x; i < p.T; i += kBlock) cap[i] = p.cap[i];
+    __syncthreads();
+    return Lds<R>{cost, pm, cap, binom};
+}
+
+// ---------------------------------------------------------------------------
+// (a1) decode
+// ---------------------------------------------------------------------------
+
+// Cut points of the composition with lexicographic rank r.  For the j-th cut
+// with k = S-1-j cuts left after it and a = c_{j-1} + 1 its smallest value,
+// the number of tuples whose j-th cut is below c is C(L-a, k+1) - C(L-c, k+1)
+// (hockey-stick identity).  With Q = C(L-a, k+1) - r the cut is c = L - n*,
+// n* the smallest n with C(n, k+1) >= Q, found by a branch-free binary
+// search over column k+1 of the Pascal table; the rank left is C(n*, k+1) - Q.
+template <int S, typename R>
+__device__ __forceinline__ void decode_cuts(R r, const R *binom, uint32_t L, uint32_t NB,
+                                            uint32_t (&cut)[S + 1]) {
+    cut[0] = 0;
+    cut[S] = L;
+    uint32_t a = 1;
+#pragma unroll
+    for (int j = 1; j <= S - 1; ++j) {
+        const R *col = binom + (S - j) * NB;
+        const R Q = col[L - a] - r;
+        uint32_t pos = 0;
+        for (uint32_t step = NB >> 1; step >= 1; step >>= 1)
+            if (col[pos + step - 1] < Q) pos += step;
+        r = col[pos] - Q;
+        cut[j] = L - pos;
+        a = cut[j] + 1;
+    }
+}
+
+template <int S>
+__device__ __forceinline__ void decode_types(const KParams &p, uint32_t a, uint32_t (&ty)[S]) {
+    if (p.assign_mode == kAssignFixed) {
+#pragma unroll
+        for (int s = 0; s < S; ++s) ty[s] = p.fixed_types[s];
+    } else if (p.assign_mode == kAssignTable) {
+        const uint8_t *row = p.assign + (uint64_t)a * S;
+#pragma unroll
+        for (int s = 0; s < S; ++s) ty[s] = row[s];
+    } else {
+        // base-T digits, stage 1 most significant.  q = umulhi(a, m) with
+        // m = floor(2^32 / T) + 1 is floor(a / T) or one more; one
+        // correction makes it exact for every 32-bit a.
+#pragma unroll
+        for (int s = S - 1; s >= 0; --s) {
+            uint32_t q = __umulhi(a, p.magicT);
+            int32_t rem = (int32_t)(a - q * p.T);
+            if (rem < 0) { q -= 1; rem += (int32_t)p.T; }
+            ty[s] = (uint32_t)rem;
+            a = q;
+        }
+    }
+}
+
+// Candidate i of the call -> (rank, assignment); false if out of range.
+template <typename R>
+__device__ __forceinline__ bool candidate(const KParams &p, uint64_t i, R &r, uint32_t &a) {
+    uint64_t rank, asg;
+    if (p.comp_rank) {
+        rank = p.comp_rank[i];
+        asg = p.assign_idx ? p.assign_idx[i] : 0u;
+    } else {
+        const uint64_t idx = p.first + i;
+        if (p.A == 1) { rank = idx; asg = 0; }
+        else { rank = idx / p.A; asg = idx - rank * p.A; }
+    }
+    const bool ok = rank < p.n_comp && asg < p.A;
+    r = ok ? (R)rank : (R)0;
+    a = ok ? (uint32_t)asg : 0u;
+    return ok;
+}
+
+// ---------------------------------------------------------------------------
+// (a2) stage weights and memory feasibility
+// ---------------------------------------------------------------------------
+template <int S, typename R>
+__device__ __forceinline__ bool stage_weights(const KParams &p, const Lds<R> &t,
+                                              const uint32_t (&cut)[S + 1], const uint32_t (&ty)[S],
+                                              uint32_t (&F)[S], uint32_t (&B)[S]) {
+    bool feas = true;
+    const uint32_t row = p.L + 1;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        const uint64_t *c = t.cost + ty[s] * row;
+        const uint64_t hi = c[cut[s + 1]], lo = c[cut[s]];
+        F[s] = (uint32_t)hi - (uint32_t)lo;
+        B[s] = (uint32_t)(hi >> 32) - (uint32_t)(lo >> 32);
+        const uint32_t mem = t.pm[cut[s + 1]] - t.pm[cut[s]];
+        feas = feas && (mem <= t.cap[ty[s]]);
+    }
+    return feas;
+}
+
+// ---------------------------------------------------------------------------
+// (a3) longest path of the 1F1B DAG
+// ---------------------------------------------------------------------------
+// With unit node weights the as-soon-as-possible start slot of every node
+// puts at most one node per stage in a slot, and each cross-stage
+// predecessor is still the newest node of its stage one slot later.  One
+// register per stage, X[s] = finish time of stage s's newest node, therefore
+// suffices: slot by slot every active stage updates from the previous
+// slot's values,
+//   forward : X[s] <- F_s + max(X[s], X[s-1] + cf_{s-1})
+//   backward: X[s] <- B_s + max(X[s], X[s+1] + cb_s)
+// and T = X[1] after the last slot (B_{1,M} is the DAG's only sink).
+// For M >= S the 2(M+S-1) slots are a prologue of 2S-1 slots, a steady part
+// in which stage s (1-based) runs a forward pass in slots k = s+1 (mod 2)
+// and a backward pass in the others, and an epilogue of 2S-2 slots.
+
+constexpr int kIdle = 0, kFwd = 1, kBwd = 2;
+
+// slot k < 2S-1 (prologue), 1-based stage s
+__host__ __device__ constexpr int pro_op(int S, int s, int k) {
+    return (k >= s - 1 && k <= S - 1) ? kFwd
+         : (k >= 2 * S - s + 1 && ((k - s - 1) & 1) == 0) ? kFwd
+         : (k >= 2 * S - s && ((k - s) & 1) == 0) ? kBwd
+         : kIdle;
+}
+// slot 2M + j, j < 2S-2 (epilogue)
+__host__ __device__ constexpr int epi_op(int S, int s, int j) {
+    return (((j - s - 1) & 1) == 0 && j <= s - 3) ? kFwd
+         : (((j - s) & 1) == 0 && j <= 2 * S - s - 2) ? kBwd
+         : kIdle;
+}
+
+template <int S>
+struct Comm {
+    uint32_t f[S > 1 ? S - 1 : 1], b[S > 1 ? S - 1 : 1];
+};
+
+template <int S>
+__device__ __forceinline__ uint32_t node(int op, int s, const uint32_t (&X)[S], const uint32_t (&F)[S],
+                                         const uint32_t (&B)[S], const Comm<S> &c) {
+    // s is 0-based here
+    if (op == kFwd) {
+        const uint32_t in = (s > 0) ? X[s > 0 ? s - 1 : 0] + c.f[s > 0 ? s - 1 : 0] : 0u;
+        return F[s] + max(X[s], in);
+    }
+    if (op == kBwd) {
+        const uint32_t in = (s < S - 1) ? X[s < S - 1 ? s + 1 : 0] + c.b[s < S - 1 ? s : 0] : 0u;
+        return B[s] + max(X[s], in);
+    }
+    return X[s];
+}
+
+template <int S>
+__device__ __forceinline__ void steady_slot(int parity, uint32_t (&X)[S], const uint32_t (&F)[S],
+                                            const uint32_t (&B)[S], const Comm<S> &c) {
+    uint32_t N[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        // 1-based stage s+1 runs forward when k = s+2 (mod 2), i.e. k = s (mod 2)
+        const int op = (((s & 1) == parity) ? kFwd : kBwd);
+        N[s] = node<S>(op, s, X, F, B, c);
+    }
+#pragma unroll
+    for (int s = 0; s < S; ++s) X[s] = N[s];
+}
+
+template <int S>
+__device__ __forceinline__ uint32_t dp_1f1b(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                            const Comm<S> &c) {
+    uint32_t X[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) X[s] = 0;
+#pragma unroll
+    for (int k = 0; k < 2 * S - 1; ++k) {
+        uint32_t N[S];
+#pragma unroll
+        for (int s = 0; s < S; ++s) N[s] = node<S>(pro_op(S, s + 1, k), s, X, F, B, c);
+#pragma unroll
+        for (int s = 0; s < S; ++s) X[s] = N[s];
+    }
+    // steady: slots 2S-1 .. 2M-1; 2S-1 is odd
+    for (uint32_t it = S; it < M; ++it) {
+        steady_slot<S>(1, X, F, B, c);
+        steady_slot<S>(0, X, F, B, c);
+    }
+    steady_slot<S>(1, X, F, B, c);
+#pragma unroll
+    for (int j = 0; j < 2 * S - 2; ++j) {
+        uint32_t N[S];
+#pragma unroll
+        for (int s = 0; s < S; ++s) N[s] = node<S>(epi_op(S, s + 1, j), s, X, F, B, c);
+#pragma unroll
+        for (int s = 0; s < S; ++s) X[s] = N[s];
+    }
+    return X[0];
+}
+
+// Any M (used when M < S): the slot schedule comes from a table of
+// per-slot forward / backward stage masks built on the host.
+template <int S>
+__device__ __forceinline__ uint32_t dp_table(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                             const Comm<S> &c) {
+    uint32_t X[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) X[s] = 0;
+    for (uint32_t k = 0; k < p.nslots; ++k) {
+        const uint32_t fm = p.slot_mask[2 * k], bm = p.slot_mask[2 * k + 1];
+        uint32_t N[S];
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            const int op = ((fm >> s) & 1u) ? kFwd : (((bm >> s) & 1u) ? kBwd : kIdle);
+            N[s] = node<S>(op, s, X, F, B, c);
+        }
+#pragma unroll
+        for (int s = 0; s < S; ++s) X[s] = N[s];
+    }
+    return X[0];
+}
+
+template <int S>
+__device__ __forceinline__ uint32_t makespan(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                             const Comm<S> &c) {
+    if (p.M >= (uint32_t)S) return dp_1f1b<S>(p.M, F, B, c);
+    return dp_table<S>(p, F, B, c);
+}
+
+template <int S>
+__device__ __forceinline__ Comm<S> load_comm(const KParams &p) {
+    Comm<S> c;
+#pragma unroll
+    for (int s = 0; s < (S > 1 ? S - 1 : 1); ++s) {
+        c.f[s] = p.cf[s];
+        c.b[s] = p.cb[s];
+    }
+    return c;
+}
+
+// ---------------------------------------------------------------------------
+// (a5) Eq. 2 lower bound with d_i = 0: g(S_x) = sum_{i<x}(F_i + B_i) + M (F_x + B_x)
+// ---------------------------------------------------------------------------
+template <int S>
+__device__ __forceinline__ uint32_t eq2_bound(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S]) {
+    uint32_t pre = 0, lb = 0;
+#pragma unroll
+    for (int x = 0; x < S; ++x) {
+        const uint32_t fb = F[x] + B[x];
+        lb = max(lb, pre + M * fb);
+        pre += fb;
+    }
+    return lb;
+}
+
+// ---------------------------------------------------------------------------
+// (a4) reductions
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ unsigned long long wave_min(unsigned long long v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const unsigned long long w = __shfl_xor(v, o, 64);
+        v = w < v ? w : v;
+    }
+    return v;
+}
+
+// Block min of `v`, folded into *acc; the last block of the grid moves *acc
+// to *result and re-arms *acc and *done for the next launch.  Returns true
+// in thread 0 of the last block (after the hand-over).
+__device__ __forceinline__ bool block_min_and_finish(unsigned long long v, unsigned long long *acc,
+                                                     unsigned int *done, unsigned long long *result,
+                                                     unsigned long long *run_best) {
+    __shared__ unsigned long long part[kWaves];
+    __shared__ int last;
+    v = wave_min(v);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) part[wave] = v;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long m = part[0];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) m = part[w] < m ? part[w] : m;
+        if (m != ~0ull) atomicMin(acc, m);
+        __threadfence();
+        const unsigned int ticket = atomicAdd(done, 1u);
+        last = (ticket == gridDim.x - 1);
+        if (last) {
+            __threadfence();
+            const unsigned long long k = atomicExch(acc, ~0ull);
+            if (result) atomicExch(result, k);
+            if (run_best) atomicMin(run_best, k);
+            atomicExch(done, 0u);
+        }
+    }
+    __syncthreads();
+    return last && threadIdx.x == 0;
+}
+
+__device__ __forceinline__ unsigned long long make_key(bool feasible, uint32_t T, uint32_t i) {
+    return ((unsigned long long)(feasible ? T : 0xFFFFFFFFu) << 32) | i;
+}
+
+// ---------------------------------------------------------------------------
+// kernels
+// ---------------------------------------------------------------------------
+
+// Exhaustive evaluation; grid-stride over the call's candidates.
+template <int S, typename R>
+__global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const Lds<R> tab = stage_tables<R>(p, smem);
+    const Comm<S> comm = load_comm<S>(p);
+    unsigned long long best = ~0ull;
+    bool bad = false;
+    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    // every wave runs the same trip count so that ballots see whole waves
+    const uint64_t span = (p.count + stride - 1) / stride;
+    uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+    for (uint64_t it = 0; it < span; ++it, i += stride) {
+        const bool active = i < p.count;
+        R r;
+        uint32_t a;
+        const bool ok = candidate<R>(p, active ? i : 0, r, a);
+        bad |= active && !ok;
+        uint32_t cut[S + 1], ty[S], F[S], B[S];
+        decode_cuts<S, R>(r, tab.binom, p.L, p.NB, cut);
+        decode_types<S>(p, a, ty);
+        const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B) && ok && active;
+        uint32_t T = makespan<S>(p, F, B, comm);
+        if (!ok) T = 0xFFFFFFFFu;
+        if (active && p.makespan_out) p.makespan_out[i] = T;
+        if (p.feas_bits_out) {
+            const unsigned long long bits = __ballot(feas);
+            const uint64_t w0 = (i - (threadIdx.x & 63)) >> 5;
+            if ((threadIdx.x & 63) == 0 && w0 < p.nwords) p.feas_bits_out[w0] = (uint32_t)bits;
+            if ((threadIdx.x & 63) == 32 && w0 + 1 < p.nwords) p.feas_bits_out[w0 + 1] = (uint32_t)(bits >> 32);
+        }
+        if (active) {
+            const unsigned long long key = make_key(feas, T, (uint32_t)i);
+            best = key < best ? key : best;
+        }
+    }
+    if (__ballot(bad) != 0 && (threadIdx.x & 63) == 0) atomicOr(p.err, 1u);
+    block_min_and_finish(best, p.acc, p.done, p.result, nullptr);
+}
+
+// Early stop (Eq. 2 / Theorem 1) over one chunk: each block filters a tile
+// of kTile candidates, compacts the survivors in LDS and evaluates them.
+template <int S, typename R>
+__global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chunk_lo, uint64_t chunk_hi,
+                                                         uint32_t bound) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ uint16_t surv[kTile];
+    __shared__ unsigned int nsurv;
+    __shared__ unsigned int cnt_pruned, cnt_infeas, cnt_bad;
+    const Lds<R> tab = stage_tables<R>(p, smem);
+    const Comm<S> comm = load_comm<S>(p);
+    if (threadIdx.x == 0) { nsurv = 0; cnt_pruned = 0; cnt_infeas = 0; cnt_bad = 0; }
+    // bound in force: min(caller's bound, best of earlier chunks)
+    const unsigned long long rb = __hip_atomic_load(p.run_best, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t rbT = (uint32_t)(rb >> 32);
+    const uint32_t b = rbT < bound ? rbT : bound;
+    __syncthreads();
+    const uint64_t base = chunk_lo + (uint64_t)blockIdx.x * kTile;
+    uint32_t my_pruned = 0, my_infeas = 0, my_bad = 0;
+    for (int q = 0; q < kTile / kBlock; ++q) {
+        const uint32_t off = q * kBlock + threadIdx.x;
+        const uint64_t i = base + off;
+        const bool active = i < chunk_hi;
+        R r;
+        uint32_t a;
+        const bool ok = candidate<R>(p, active ? i : 0, r, a);
+        uint32_t cut[S + 1], ty[S], F[S], B[S];
+        decode_cuts<S, R>(r, tab.binom, p.L, p.NB, cut);
+        decode_types<S>(p, a, ty);
+        const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B);
+        bool keep = false;
+        if (active) {
+            if (!ok) my_bad++;
+            else if (!feas) my_infeas++;
+            else if (eq2_bound<S>(p.M, F, B) > b) my_pruned++;
+            else keep = true;
+        }
+        const unsigned long long m = __ballot(keep);
+        const unsigned int lane = threadIdx.x & 63;
+        unsigned int slot0 = 0;
+        if (lane == 0 && m) slot0 = atomicAdd(&nsurv, (unsigned int)__popcll(m));
+        slot0 = __shfl(slot0, 0, 64);
+        if (keep) {
+            const unsigned long long below = lane ? (m & ((1ull << lane) - 1ull)) : 0ull;
+            surv[slot0 + __popcll(below)] = (uint16_t)off;
+        }
+    }
+    if (my_pruned) atomicAdd(&cnt_pruned, my_pruned);
+    if (my_infeas) atomicAdd(&cnt_infeas, my_infeas);
+    if (my_bad) atomicAdd(&cnt_bad, my_bad);
+    __syncthreads();
+    const unsigned int n = nsurv;
+    unsigned long long best = ~0ull;
+    for (unsigned int k = threadIdx.x; k < n; k += kBlock) {
+        const uint64_t i = base + surv[k];
+        R r;
+        uint32_t a;
+        candidate<R>(p, i, r, a);
+        uint32_t cut[S + 1], ty[S], F[S], B[S];
+        decode_cuts<S, R>(r, tab.binom, p.L, p.NB, cut);
+        decode_types<S>(p, a, ty);
+        stage_weights<S, R>(p, tab, cut, ty, F, B);
+        const uint32_t T = makespan<S>(p, F, B, comm);
+        const unsigned long long key = make_key(true, T, (uint32_t)i);
+        best = key < best ? key : best;
+    }
+    if (threadIdx.x == 0) {
+        atomicAdd(&p.stats[0], (unsigned long long)n);
+        atomicAdd(&p.stats[1], (unsigned long long)cnt_pruned);
+        atomicAdd(&p.stats[2], (unsigned long long)cnt_infeas);
+        if (cnt_bad) atomicOr(p.err, 1u);
+    }
+    block_min_and_finish(best, p.acc, p.done, nullptr, p.run_best);
+}
+
+// Argmin over stored makespans / feasibility bits.
+__global__ __launch_bounds__(kBlock) void argmin_kernel(const uint32_t *T, const uint32_t *bits, uint64_t count,
+                                                        unsigned long long *acc, unsigned int *done,
+                                                        unsigned long long *result) {
+    unsigned long long best = ~0ull;
+    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < count; i += stride) {
+        const bool f = bits ? ((bits[i >> 5] >> (i & 31)) & 1u) : true;
+        const unsigned long long key = make_key(f, T[i], (uint32_t)i);
+        best = key < best ? key : best;
+    }
+    block_min_and_finish(best, acc, done, result, nullptr);
+}
+
+// Small fill kernel used instead of memset so that the calls stay capturable.
+__global__ void fill_u64(unsigned long long *p, uint32_t n, unsigned long long v) {
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+// ---------------------------------------------------------------------------
+// host-side launchers
+// ---------------------------------------------------------------------------
+template <int S, typename R>
+static hipError_t launch_eval_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
+    hipLaunchKernelGGL((eval_kernel<S, R>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
+    return hipGetLastError();
+}
+
+template <int S, typename R>
+static hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
+                                   uint32_t bound) {
+    const uint64_t grid = (hi - lo + kTile - 1) / kTile;
+    hipLaunchKernelGGL((bounded_kernel<S, R>), dim3((uint32_t)grid), dim3(kBlock), lc.lds_bytes, st, p, lo, hi, bound);
+    return hipGetLastError();
+}
+
+template <int S, typename R>
+static hipError_t occupancy_s(int *blocks, size_t lds) {
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, eval_kernel<S, R>, kBlock, lds);
+}
+
+#define PK_DISPATCH(FN, S_, WIDE_, ...)                                                        \
+    switch (S_) {                                                                              \
+    case 1: return WIDE_ ? FN<1, uint64_t>(__VA_ARGS__) : FN<1, uint32_t>(__VA_ARGS__);       \
+    case 2: return WIDE_ ? FN<2, uint64_t>(__VA_ARGS__) : FN<2, uint32_t>(__VA_ARGS__);       \
+    case 3: return WIDE_ ? FN<3, uint64_t>(__VA_ARGS__) : FN<3, uint32_t>(__VA_ARGS__);       \
+    case 4: return WIDE_ ? FN<4, uint64_t>(__VA_ARGS__) : FN<4, uint32_t>(__VA_ARGS__);       \
+    case 5: return WIDE_ ? FN<5, uint64_t>(__VA_ARGS__) : FN<5, uint32_t>(__VA_ARGS__);       \
+    case 6: return WIDE_ ? FN<6, uint64_t>(__VA_ARGS__) : FN<6, uint32_t>(__VA_ARGS__);       \
+    case 7: return WIDE_ ? FN<7, uint64_t>(__VA_ARGS__) : FN<7, uint32_t>(__VA_ARGS__);       \
+    case 8: return WIDE_ ? FN<8, uint64_t>(__VA_ARGS__) : FN<8, uint32_t>(__VA_ARGS__);       \
+    case 9: return WIDE_ ? FN<9, uint64_t>(__VA_ARGS__) : FN<9, uint32_t>(__VA_ARGS__);       \
+    case 10: return WIDE_ ? FN<10, uint64_t>(__VA_ARGS__) : FN<10, uint32_t>(__VA_ARGS__);    \
+    case 11: return WIDE_ ? FN<11, uint64_t>(__VA_ARGS__) : FN<11, uint32_t>(__VA_ARGS__);    \
+    case 12: return WIDE_ ? FN<12, uint64_t>(__VA_ARGS__) : FN<12, uint32_t>(__VA_ARGS__);    \
+    case 13: return WIDE_ ? FN<13, uint64_t>(__VA_ARGS__) : FN<13, uint32_t>(__VA_ARGS__);    \
+    case 14: return WIDE_ ? FN<14, uint64_t>(__VA_ARGS__) : FN<14, uint32_t>(__VA_ARGS__);    \
+    case 15: return WIDE_ ? FN<15, uint64_t>(__VA_ARGS__) : FN<15, uint32_t>(__VA_ARGS__);    \
+    case 16: return WIDE_ ? FN<16, uint64_t>(__VA_ARGS__) : FN<16, uint32_t>(__VA_ARGS__);    \
+    default: return hipErrorInvalidValue;                                                      \
+    }
+
+hipError_t launch_eval(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
+    PK_DISPATCH(launch_eval_s, p.S, p.wide, p, lc, st)
+}
+
+hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
+                          uint32_t bound) {
+    PK_DISPATCH(launch_bounded_s, p.S, p.wide, p, lc, st, lo, hi, bound)
+}
+
+hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, int *blocks) {
+    PK_DISPATCH(occupancy_s, S, wide, blocks, lds)
+}
+
+hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,
+                         unsigned long long *acc, unsigned int *done, unsigned long long *result, hipStream_t st) {
+    hipLaunchKernelGGL(argmin_kernel, dim3(grid), dim3(kBlock), 0, st, T, bits, count, acc, done, result);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, hipStream_t st) {
+    hipLaunchKernelGGL(fill_u64, dim3((n + 63) / 64), dim3(64), 0, st, p, n, v);
+    return hipGetLastError();
+}
+
+int prologue_op(int S, int s, int k) { return pro_op(S, s, k); }
+int epilogue_op(int S, int s, int j) { return epi_op(S, s, j); }
+
+}  // namespace pk

@@ -1,0 +1,71 @@
+"""Write tests/golden/full_workloads.json from the CPU oracle only.
+
+For each large workload (3, 4, 5) this records, over every candidate:
+the SHA-256 of the makespan array (uint32 little-endian), the SHA-256 of the
+feasibility bit array packed as the library's output (bit i % 32 of uint32
+word i / 32), the number of feasible candidates and the argmin.  For
+workload 4 it also records the early-stop pass: the warm-up bound (best of
+the first 500 list entries) and, per chunk size, the oracle's
+(best, evaluated, pruned, infeasible).
+
+Run from the repository root:  python tests/golden/make_golden.py
+"""
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+sys.path.insert(0, ROOT)
+
+from oracle import coracle  # noqa: E402
+from paper_2609_06086_amd import workloads as W  # noqa: E402
+
+OUT = os.path.join(os.path.dirname(os.path.abspath(__file__)), "full_workloads.json")
+WARMUP = 500
+CHUNKS = (0, 1 << 22)
+
+
+def pack_bits(f: np.ndarray) -> np.ndarray:
+    pad = (-len(f)) % 32
+    return np.packbits(np.concatenate([f.astype(bool), np.zeros(pad, bool)]), bitorder="little").view("<u4")
+
+
+def main():
+    res = {"note": "written by tests/golden/make_golden.py from the C oracle; see that script"}
+    for cfg in (3, 4, 5):
+        wl = W.workload(cfg)
+        t0 = time.time()
+        T, f = coracle.evaluate(wl.problem, wl.cands)
+        best = coracle.argmin(T, f)
+        ent = {
+            "n": int(len(T)),
+            "makespan_sha256": hashlib.sha256(T.astype("<u4").tobytes()).hexdigest(),
+            "feasible_bits_sha256": hashlib.sha256(pack_bits(f).astype("<u4").tobytes()).hexdigest(),
+            "n_feasible": int(f.sum()),
+            "best_index": best[0], "best_makespan": best[1],
+            "makespan_min": int(T.min()), "makespan_max": int(T.max()),
+        }
+        if cfg == 4:
+            wb = coracle.argmin(T[:WARMUP], f[:WARMUP])
+            bound = wb[1]
+            ent["warmup"] = WARMUP
+            ent["warmup_bound"] = bound
+            ent["bounded"] = {}
+            for ch in CHUNKS:
+                b, ev, pr, inf = coracle.bounded(wl.problem, wl.cands, bound, ch)
+                ent["bounded"][str(ch)] = {"best_index": b[0], "best_makespan": b[1], "evaluated": ev,
+                                           "pruned": pr, "infeasible": inf}
+        ent["oracle_seconds"] = round(time.time() - t0, 1)
+        res[f"cfg{cfg}"] = ent
+        print(cfg, ent, flush=True)
+    with open(OUT, "w") as fh:
+        json.dump(res, fh, indent=1)
+        fh.write("\n")
+
+
+if __name__ == "__main__":
+    main()

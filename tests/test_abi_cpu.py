@@ -1,0 +1,106 @@
+"""The C-ABI library on the CPU: it loads, exports every declared entry
+point, and rejects invalid problems before touching the GPU."""
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2609_06086_amd import poseidon as P
+from paper_2609_06086_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "poseidon.h")
+
+
+def declared():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(poseidon_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_symbol():
+    syms = declared()
+    assert "poseidon_load_costs" in syms and "poseidon_eval_candidates" in syms
+    out = subprocess.run(["nm", "-D", "--defined-only", P.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (poseidon_[a-z_]+)", out))
+    assert set(syms) <= exported, set(syms) - exported
+    assert set(P.EXPORTS) == set(syms)
+    lib = P.lib()
+    for s in syms:
+        assert hasattr(lib, s)
+
+
+def test_strerror():
+    assert P.strerror(0) == "ok"
+    assert "invalid" in P.strerror(P.POSEIDON_E_INVAL)
+    assert P.strerror(12345) == "unknown status"
+
+
+def test_validate_counts_candidates():
+    assert P.poseidon_validate(W.workload(1).problem) == 28
+    assert P.poseidon_validate(W.workload(2).problem) == 71920
+    assert P.poseidon_validate(W.workload(3).problem) == 62891499
+    assert P.poseidon_validate(W.workload(4, n_samples=4).problem) == 2898753715 * 6561
+    assert P.poseidon_validate(W.workload(5, n_samples=4).problem) == 9064807833193439800
+
+
+def _small():
+    rng = np.random.default_rng(0)
+    return W.random_problem(rng, 10, 3, 4, 2)
+
+
+def _status(prob):
+    with pytest.raises(P.PoseidonError) as ei:
+        P.poseidon_validate(prob)
+    return ei.value.status
+
+
+def test_validation_errors():
+    p = _small()
+    p.S = 11                              # S > L
+    assert _status(p) == P.POSEIDON_E_INVAL
+    p = _small(); p.S = 0
+    assert _status(p) == P.POSEIDON_E_INVAL
+    p = _small(); p.T = 0
+    assert _status(p) == P.POSEIDON_E_INVAL
+    p = _small(); p.M = 0
+    assert _status(p) == P.POSEIDON_E_INVAL
+    p = _small(); p.fwd = None
+    assert _status(p) == P.POSEIDON_E_INVAL
+    p = _small(); p.comm_fwd = None
+    assert _status(p) == P.POSEIDON_E_INVAL
+    p = _small(); p.assign = np.array([[0, 1, 2]], np.uint8)   # type id 2 >= T = 2
+    assert _status(p) == P.POSEIDON_E_INVAL
+    # S above the compiled maximum
+    rng = np.random.default_rng(1)
+    p = W.random_problem(rng, 40, 17, 4, 1)
+    assert _status(p) == P.POSEIDON_E_INVAL
+    # L above the maximum
+    p = W.random_problem(rng, 300, 4, 4, 1)
+    assert _status(p) == P.POSEIDON_E_INVAL
+
+
+def test_overflow_guard():
+    """A makespan that could reach 2^31 is refused (E_RANGE)."""
+    rng = np.random.default_rng(2)
+    p = W.random_problem(rng, 16, 4, 1000, 2, cost_lo=1000, cost_hi=1000)
+    # every path is at most M * (sum of slowest fwd+bwd + comm) = 1000*(16*2000 + comm) < 2^31
+    assert P.poseidon_validate(p) > 0
+    p.M = 100000
+    assert _status(p) == P.POSEIDON_E_RANGE
+
+
+def test_too_many_assignments():
+    rng = np.random.default_rng(3)
+    p = W.random_problem(rng, 40, 16, 4, 8)   # 8^16 assignments > 2^32
+    assert _status(p) == P.POSEIDON_E_RANGE
+
+
+def test_load_costs_rejects_before_device():
+    p = _small()
+    p.S = 11
+    with pytest.raises(P.PoseidonError) as ei:
+        P.poseidon_load_costs(p, 0)
+    assert ei.value.status == P.POSEIDON_E_INVAL

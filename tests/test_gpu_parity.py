@@ -1,0 +1,360 @@
+"""GPU parity: the HIP path through the C-ABI against the CPU oracle.
+
+Makespans, feasibility bits and the argmin must be bit-identical (all
+arithmetic is exact integer arithmetic).  Small and mid-size cases compare
+every output with the oracle; the full-size workloads compare SHA-256
+digests of the full output arrays and the argmin with values the committed
+script tests/golden/make_golden.py wrote from the oracle.
+"""
+import hashlib
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import coracle, dag  # noqa: E402
+from paper_2609_06086_amd import poseidon as P  # noqa: E402
+from paper_2609_06086_amd import workloads as W  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+GOLD = os.path.join(os.path.dirname(__file__), "golden", "full_workloads.json")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def unpack_bits(words: np.ndarray, n: int) -> np.ndarray:
+    """Feasibility of candidate i = bit i % 32 of uint32 word i / 32."""
+    return np.unpackbits(words.astype("<u4").view(np.uint8), bitorder="little")[:n].astype(bool)
+
+
+def pack_bits(f: np.ndarray) -> np.ndarray:
+    """Bit i % 32 of uint32 word i / 32, as the library writes them."""
+    pad = (-len(f)) % 32
+    return np.packbits(np.concatenate([f.astype(bool), np.zeros(pad, bool)]), bitorder="little").view("<u4")
+
+
+def to_dev(cands, dev):
+    if not cands.is_list:
+        return dict(first=cands.first, count=cands.count)
+    d = dict(comp_rank=torch.from_numpy(cands.comp_rank.view(np.int64)).to(dev))
+    if cands.assign_idx is not None:
+        d["assign_idx"] = torch.from_numpy(cands.assign_idx.view(np.int32)).to(dev)
+    return d
+
+
+def gpu_eval(ctx, cands, dev, n=None):
+    n = len(cands) if n is None else n
+    T = torch.full((max(n, 1),), -1, dtype=torch.int32, device=dev)
+    bits = torch.full((max((n + 31) // 32, 1),), -1, dtype=torch.int32, device=dev)
+    best = P.poseidon_eval_candidates(ctx, makespan_out=T, feasible_bits_out=bits, **to_dev(cands, dev))
+    Tg = T.cpu().numpy().view(np.uint32)[:n]
+    fg = unpack_bits(bits.cpu().numpy().view(np.uint32), n)
+    return Tg, fg, best
+
+
+def check_against_oracle(prob, cands, dev, python_oracle=False):
+    ctx = P.poseidon_load_costs(prob, 0)
+    Tg, fg, best = gpu_eval(ctx, cands, dev)
+    if python_oracle:
+        To, fo = dag.evaluate(prob, cands)
+        To = To.astype(np.uint32)
+    else:
+        To, fo = coracle.evaluate(prob, cands)
+    assert np.array_equal(Tg, To), f"makespans differ at {np.nonzero(Tg != To)[0][:10]}"
+    assert np.array_equal(fg, fo), "feasibility differs"
+    ob = coracle.argmin(To, fo)
+    if ob is None:
+        assert best.status == P.POSEIDON_NO_FEASIBLE and best.index is None
+    else:
+        assert (best.index, best.makespan) == ob
+    ctx.close()
+    return Tg, fg, best
+
+
+# ------------------------------------------------------------ named workloads
+
+def test_workload1_exhaustive_vs_python_oracle(dev):
+    wl = W.workload(1)
+    check_against_oracle(wl.problem, wl.cands, dev, python_oracle=True)
+
+
+def test_workload2_exhaustive(dev):
+    wl = W.workload(2)
+    check_against_oracle(wl.problem, wl.cands, dev)
+
+
+def test_workload3_subrange_ragged(dev):
+    wl = W.workload(3)
+    first, count = 12_345_679, 3_000_001
+    check_against_oracle(wl.problem, W.Candidates(first=first, count=count), dev)
+
+
+def test_workload4_list_prefix(dev):
+    wl = W.workload(4)
+    n = 1_000_003
+    c = W.Candidates(comp_rank=wl.cands.comp_rank[:n].copy(), assign_idx=wl.cands.assign_idx[:n].copy())
+    check_against_oracle(wl.problem, c, dev)
+
+
+def test_workload5_list_prefix(dev):
+    wl = W.workload(5)
+    n = 300_001
+    c = W.Candidates(comp_rank=wl.cands.comp_rank[:n].copy())
+    check_against_oracle(wl.problem, c, dev)
+
+
+# ------------------------------------------------------------- random shapes
+
+def test_every_stage_count_fast_path(dev):
+    """S = 1..16 with M >= S (register-stencil path), random tables."""
+    rng = np.random.default_rng(100)
+    for S in range(1, 17):
+        for M in (S, S + 1, S + int(rng.integers(2, 40))):
+            L = S + int(rng.integers(0, 12))
+            T = int(rng.integers(1, 4))
+            prob = W.random_problem(rng, L, S, M, T, cost_hi=500, mem_hi=40, cap=int(rng.integers(40, 200)),
+                                    assign_rows=None if T ** S < 5000 else 6)
+            cands = W.random_candidates(rng, prob, int(rng.integers(1, 700)))
+            check_against_oracle(prob, cands, dev)
+
+
+def test_short_pipelines_table_path(dev):
+    """M < S (slot-table path)."""
+    rng = np.random.default_rng(101)
+    for _ in range(40):
+        S = int(rng.integers(2, 17))
+        M = int(rng.integers(1, S))
+        L = S + int(rng.integers(0, 10))
+        prob = W.random_problem(rng, L, S, M, 2, mem_hi=30, cap=int(rng.integers(30, 200)), assign_rows=3)
+        check_against_oracle(prob, W.random_candidates(rng, prob, int(rng.integers(1, 400))), dev)
+
+
+def test_range_mode_with_assignments(dev):
+    """Range mode over joint indices r * A + a with A > 1 (digits and table)."""
+    rng = np.random.default_rng(102)
+    for trial in range(12):
+        S = int(rng.integers(1, 6))
+        L = S + int(rng.integers(0, 8))
+        M = int(rng.integers(1, 20))
+        T = int(rng.integers(1, 4))
+        prob = W.random_problem(rng, L, S, M, T, mem_hi=30, cap=int(rng.integers(30, 150)),
+                                assign_rows=None if trial % 2 else int(rng.integers(1, 6)))
+        n = prob.n_candidates
+        first = int(rng.integers(0, n))
+        count = int(rng.integers(1, n - first + 1))
+        check_against_oracle(prob, W.Candidates(first=first, count=count), dev)
+        check_against_oracle(prob, W.Candidates(first=0, count=n), dev)
+
+
+def test_random_problems_python_oracle(dev):
+    rng = np.random.default_rng(103)
+    for _ in range(10):
+        S = int(rng.integers(1, 5))
+        L = S + int(rng.integers(0, 5))
+        M = int(rng.integers(1, 7))
+        prob = W.random_problem(rng, L, S, M, 2, mem_hi=30, cap=int(rng.integers(30, 120)))
+        check_against_oracle(prob, W.Candidates(first=0, count=prob.n_candidates), dev, python_oracle=True)
+
+
+def test_duplicates_tie_to_smallest_index(dev):
+    wl = W.workload(2)
+    rng = np.random.default_rng(104)
+    c = W.random_candidates(rng, wl.problem, 5000)
+    To, fo = coracle.evaluate(wl.problem, c)
+    b = coracle.argmin(To, fo)
+    # copy the winner to several later positions and to one earlier position
+    for j in (4999, 3000, 17):
+        c.comp_rank[j] = c.comp_rank[b[0]]
+        c.assign_idx[j] = c.assign_idx[b[0]]
+    _, _, best = check_against_oracle(wl.problem, c, dev)
+    assert best.index == min(17, b[0])
+
+
+def test_no_feasible_candidate(dev):
+    wl = W.workload(2)
+    prob = wl.problem
+    prob.cap = np.array([1000, 1000], np.uint32)     # below any stage's memory
+    _, fg, best = check_against_oracle(prob, W.Candidates(first=0, count=5000), dev)
+    assert not fg.any() and best.status == P.POSEIDON_NO_FEASIBLE
+
+
+def test_empty_and_single(dev):
+    wl = W.workload(2)
+    ctx = P.poseidon_load_costs(wl.problem, 0)
+    b = P.poseidon_eval_candidates(ctx, first=0, count=0)
+    assert b.status == P.POSEIDON_NO_FEASIBLE
+    To, fo = coracle.evaluate(wl.problem, W.Candidates(first=71919, count=1))
+    T = torch.zeros(1, dtype=torch.int32, device=dev)
+    b = P.poseidon_eval_candidates(ctx, first=71919, count=1, makespan_out=T)
+    assert int(T.cpu().numpy().view(np.uint32)[0]) == int(To[0])
+    assert (b.index, b.makespan) == (0, int(To[0]))
+    ctx.close()
+
+
+def test_invalid_rank_in_list_reports_einval(dev):
+    wl = W.workload(2)
+    ctx = P.poseidon_load_costs(wl.problem, 0)
+    ranks = torch.tensor([0, 5, 4495, 7], dtype=torch.int64, device=dev)   # 4495 = C(31,3): out of range
+    with pytest.raises(P.PoseidonError) as ei:
+        P.poseidon_eval_candidates(ctx, comp_rank=ranks)
+    assert ei.value.status == P.POSEIDON_E_INVAL
+    # the context stays usable
+    b = P.poseidon_eval_candidates(ctx, first=0, count=100)
+    To, fo = coracle.evaluate(wl.problem, W.Candidates(first=0, count=100))
+    assert (b.index, b.makespan) == coracle.argmin(To, fo)
+    ctx.close()
+
+
+def test_range_past_end_is_rejected(dev):
+    wl = W.workload(2)
+    ctx = P.poseidon_load_costs(wl.problem, 0)
+    with pytest.raises(P.PoseidonError) as ei:
+        P.poseidon_eval_candidates(ctx, first=71000, count=921)
+    assert ei.value.status == P.POSEIDON_E_INVAL
+    ctx.close()
+
+
+# --------------------------------------------------------- argmin, async
+
+def test_argmin_entry_point(dev):
+    rng = np.random.default_rng(105)
+    wl = W.workload(2)
+    ctx = P.poseidon_load_costs(wl.problem, 0)
+    n = 100_001
+    Tn = rng.integers(1, 1000, n).astype(np.uint32)
+    fn = rng.random(n) < 0.3
+    words = pack_bits(fn)
+    Td = torch.from_numpy(Tn.view(np.int32)).to(dev)
+    Bd = torch.from_numpy(words.view(np.int32)).to(dev)
+    b = P.poseidon_argmin(ctx, Td, Bd, index_base=1000)
+    ob = coracle.argmin(Tn, fn)
+    assert (b.index, b.makespan) == (ob[0] + 1000, ob[1])
+    b = P.poseidon_argmin(ctx, Td)          # no bits: all feasible
+    assert (b.index, b.makespan) == (int(np.argmin(Tn)), int(Tn.min()))
+    ctx.close()
+
+
+def test_async_then_last_best(dev):
+    wl = W.workload(2)
+    ctx = P.poseidon_load_costs(wl.problem, 0)
+    s = torch.cuda.current_stream()
+    P.poseidon_eval_candidates(ctx, first=0, count=71920, want_best=False, stream=s)
+    b = P.poseidon_last_best(ctx, stream=s)
+    To, fo = coracle.evaluate(wl.problem, wl.cands)
+    assert (b.index, b.makespan) == coracle.argmin(To, fo)
+    # repeated calls give identical results
+    for _ in range(3):
+        b2 = P.poseidon_eval_candidates(ctx, first=0, count=71920)
+        assert (b2.index, b2.makespan) == (b.index, b.makespan)
+    ctx.close()
+
+
+# ------------------------------------------------------------- early stop
+
+def bounded_vs_oracle(prob, cands, bound, chunk, dev):
+    ctx = P.poseidon_load_costs(prob, 0)
+    b, st = P.poseidon_eval_candidates_bounded(ctx, bound, chunk=chunk, **to_dev(cands, dev))
+    ob, ev, pr, inf = coracle.bounded(prob, cands, bound, chunk)
+    got = (b.index, b.makespan) if b.index is not None else None
+    assert got == ob
+    assert (st.evaluated, st.pruned, st.infeasible) == (ev, pr, inf)
+    ctx.close()
+    return b, st
+
+
+def test_bounded_random(dev):
+    rng = np.random.default_rng(106)
+    for trial in range(20):
+        S = int(rng.integers(1, 9))
+        L = S + int(rng.integers(1, 14))
+        M = int(rng.integers(1, 30))
+        prob = W.random_problem(rng, L, S, M, 3, mem_hi=30, cap=int(rng.integers(40, 200)))
+        cands = W.random_candidates(rng, prob, int(rng.integers(1, 20000)))
+        To, fo = coracle.evaluate(prob, cands)
+        warm = coracle.argmin(To[:50], fo[:50])
+        bound = warm[1] if warm else 2 ** 31
+        for chunk in (0, 4096, 777):
+            b, _ = bounded_vs_oracle(prob, cands, bound, chunk, dev)
+            ex = coracle.argmin(To, fo)
+            if ex is not None and ex[1] <= bound:
+                assert (b.index, b.makespan) == ex   # Theorem 1: same argmin as exhaustive
+
+
+def test_bounded_workload4_prefix(dev):
+    wl = W.workload(4)
+    n = 1 << 20
+    c = W.Candidates(comp_rank=wl.cands.comp_rank[:n].copy(), assign_idx=wl.cands.assign_idx[:n].copy())
+    To, fo = coracle.evaluate(wl.problem, W.Candidates(comp_rank=c.comp_rank[:500], assign_idx=c.assign_idx[:500]))
+    bound = coracle.argmin(To, fo)[1]
+    for chunk in (0, 1 << 16, 100_000):
+        b, st = bounded_vs_oracle(wl.problem, c, bound, chunk, dev)
+        assert st.pruned > 0
+
+
+def test_bounded_bound_below_optimum(dev):
+    wl = W.workload(2)
+    To, fo = coracle.evaluate(wl.problem, wl.cands)
+    opt = coracle.argmin(To, fo)[1]
+    b, st = bounded_vs_oracle(wl.problem, wl.cands, opt - 1, 0, dev)
+    assert b.status == P.POSEIDON_NO_FEASIBLE
+    b, st = bounded_vs_oracle(wl.problem, wl.cands, opt, 0, dev)
+    assert b.makespan == opt
+
+
+# ---------------------------------------------------------- full sizes
+
+def _golden():
+    if not os.path.exists(GOLD):
+        pytest.skip("golden file missing")
+    return json.load(open(GOLD))
+
+
+@pytest.mark.parametrize("cfg", [3, 4, 5])
+def test_full_workload_matches_golden(cfg, dev):
+    g = _golden()[f"cfg{cfg}"]
+    wl = W.workload(cfg)
+    ctx = P.poseidon_load_costs(wl.problem, 0)
+    Tg, fg, best = gpu_eval(ctx, wl.cands, dev)
+    assert len(Tg) == g["n"]
+    words = pack_bits(fg)
+    assert int(fg.sum()) == g["n_feasible"]
+    assert (best.index, best.makespan) == (g["best_index"], g["best_makespan"])
+    assert int(Tg.min()) == g["makespan_min"] and int(Tg.max()) == g["makespan_max"]
+    assert hashlib.sha256(Tg.astype("<u4").tobytes()).hexdigest() == g["makespan_sha256"]
+    assert hashlib.sha256(words.astype("<u4").tobytes()).hexdigest() == g["feasible_bits_sha256"]
+    # sampled entries recomputed by the oracle one by one
+    rng = np.random.default_rng(cfg)
+    pick = rng.choice(len(Tg), 2000, replace=False)
+    if wl.cands.is_list:
+        sub = W.Candidates(comp_rank=wl.cands.comp_rank[pick],
+                           assign_idx=None if wl.cands.assign_idx is None else wl.cands.assign_idx[pick])
+        To, fo = coracle.evaluate(wl.problem, sub)
+        assert np.array_equal(Tg[pick], To) and np.array_equal(fg[pick], fo)
+    ctx.close()
+
+
+def test_full_workload4_bounded_matches_golden(dev):
+    g = _golden()["cfg4"]
+    wl = W.workload(4)
+    ctx = P.poseidon_load_costs(wl.problem, 0)
+    d = to_dev(wl.cands, dev)
+    # warm-up: exact evaluation of the first 500 entries sets the bound
+    wb = P.poseidon_eval_candidates(ctx, comp_rank=d["comp_rank"][:g["warmup"]],
+                                    assign_idx=d["assign_idx"][:g["warmup"]])
+    assert wb.makespan == g["warmup_bound"]
+    for chunk, exp in g["bounded"].items():
+        b, st = P.poseidon_eval_candidates_bounded(ctx, wb.makespan, chunk=int(chunk), **d)
+        assert (b.index, b.makespan) == (exp["best_index"], exp["best_makespan"])
+        assert (st.evaluated, st.pruned, st.infeasible) == (exp["evaluated"], exp["pruned"], exp["infeasible"])
+        # Theorem 1: the early-stop pass finds the exhaustive argmin
+        assert (b.index, b.makespan) == (g["best_index"], g["best_makespan"])
+    ctx.close()
