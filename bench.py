@@ -78,6 +78,7 @@ def main():
     ap.add_argument("--workload", type=int, default=5, choices=[3, 4, 5])
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-early-stop", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (for counter scaling)")
     args = ap.parse_args()
@@ -145,7 +146,7 @@ def main():
 
     # early-stop pass (Eq. 2 bound) over the same list, warm-up bound from its first 500 entries
     es = None
-    if wl.cands.is_list:
+    if wl.cands.is_list and not args.no_early_stop:
         warm = {k: v[:500] for k, v in cand.items()}
         wb = P.poseidon_eval_candidates(ctx, **warm)
         bound = wb.makespan if wb.makespan is not None else 2 ** 31

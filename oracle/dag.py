@@ -25,7 +25,7 @@ docstring; the list of readings:
   T = finish(E) = finish(B_{1,M}) when all-reduce times are zero.
 * R6 (node weights, Sec. 4.1.3): "per-layer time x #layers" generalised to
   the sum of the per-layer times of the stage's layers on its device type.
-* R7 (memory, Sec. 3.2 / App. C): a stage is feasible iff the sum of its
+* R7 (memory, Sec. 3.2 and Sec. 4.2.2): a stage is feasible iff the sum of its
   layers' memory footprints is <= the cap of its device type.
 * R8 (candidate order): compositions in lexicographic order of the sorted
   cut tuple (itertools.combinations order), assignments in base-T order

@@ -12,7 +12,7 @@ memory footprint and a per-device memory cap).  A *candidate set* is either
 an index range over all (composition, assignment) pairs or an explicit list
 of sampled (composition rank, assignment index) pairs.
 
-The five named workloads bracket the scale of the paper's search (Sec. 5.2:
+The five named workloads bracket the scale of the paper's search (Sec. 6.1, 6.2.3:
 tens of layers, up to 16 stages, 2-4 device types with speed ratios up to
 about 3x and memory caps of tens of GB).  There is no profiled data in the
 paper's text, so these synthetic tables stand in for the profiling module's
