@@ -155,6 +155,16 @@ __device__ __forceinline__ bool stage_weights(const KParams &p, const Lds<R> &t,
 //   forward : X[s] <- F_s + max(X[s], X[s-1] + cf_{s-1})
 //   backward: X[s] <- B_s + max(X[s], X[s+1] + cb_s)
 // and T = X[1] after the last slot (B_{1,M} is the DAG's only sink).
+//
+// The registers hold Y[s] = X[s] + phi_s with phi_s = cf_s + ... + cf_{S-1}
+// (the transfer times of the boundaries below stage s).  A constant shift
+// per stage does not change any max, and with this one the forward input
+// Y[s-1] already contains cf_{s-1}, so the updates become
+//   forward : Y[s] <- F_s + max(Y[s], Y[s-1])
+//   backward: Y[s] <- B_s + max(Y[s], Y[s+1] + (cf_s + cb_s))
+// which saves one add per forward node that has an upstream stage; the
+// result is T = Y[1] - phi_1.
+//
 // For M >= S the 2(M+S-1) slots are a prologue of 2S-1 slots, a steady part
 // in which stage s (1-based) runs a forward pass in slots k = s+1 (mod 2)
 // and a backward pass in the others, and an epilogue of 2S-2 slots.
@@ -175,69 +185,75 @@ __host__ __device__ constexpr int epi_op(int S, int s, int j) {
          : kIdle;
 }
 
+// wave-uniform transfer weights after the shift (SGPRs)
 template <int S>
 struct Comm {
-    uint32_t f[S > 1 ? S - 1 : 1], b[S > 1 ? S - 1 : 1];
+    uint32_t e[S > 1 ? S - 1 : 1];   // cf_s + cb_s, 0-based boundary s
+    uint32_t phi0;                   // cf_0 + ... + cf_{S-2}
 };
 
 template <int S>
-__device__ __forceinline__ uint32_t node(int op, int s, const uint32_t (&X)[S], const uint32_t (&F)[S],
+__device__ __forceinline__ uint32_t node(int op, int s, const uint32_t (&Y)[S], const uint32_t (&F)[S],
                                          const uint32_t (&B)[S], const Comm<S> &c) {
     // s is 0-based here
-    if (op == kFwd) {
-        const uint32_t in = (s > 0) ? X[s > 0 ? s - 1 : 0] + c.f[s > 0 ? s - 1 : 0] : 0u;
-        return F[s] + max(X[s], in);
-    }
-    if (op == kBwd) {
-        const uint32_t in = (s < S - 1) ? X[s < S - 1 ? s + 1 : 0] + c.b[s < S - 1 ? s : 0] : 0u;
-        return B[s] + max(X[s], in);
-    }
-    return X[s];
+    if (op == kFwd) return F[s] + (s > 0 ? max(Y[s], Y[s > 0 ? s - 1 : 0]) : Y[s]);
+    if (op == kBwd)
+        return B[s] + (s < S - 1 ? max(Y[s], Y[s < S - 1 ? s + 1 : 0] + c.e[s < S - 1 ? s : 0]) : Y[s]);
+    return Y[s];
+}
+
+// Registers before the first slot: stage 1 starts at phi_1 (its X is 0);
+// every other stage's first node is a forward pass whose upstream input is
+// at least phi_s, so 0 there leaves every max unchanged.
+template <int S>
+__device__ __forceinline__ void dp_init(uint32_t (&Y)[S], const Comm<S> &c) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) Y[s] = 0;
+    Y[0] = c.phi0;
 }
 
 template <int S>
-__device__ __forceinline__ void steady_slot(int parity, uint32_t (&X)[S], const uint32_t (&F)[S],
+__device__ __forceinline__ void steady_slot(int parity, uint32_t (&Y)[S], const uint32_t (&F)[S],
                                             const uint32_t (&B)[S], const Comm<S> &c) {
     uint32_t N[S];
 #pragma unroll
     for (int s = 0; s < S; ++s) {
         // 1-based stage s+1 runs forward when k = s+2 (mod 2), i.e. k = s (mod 2)
         const int op = (((s & 1) == parity) ? kFwd : kBwd);
-        N[s] = node<S>(op, s, X, F, B, c);
+        N[s] = node<S>(op, s, Y, F, B, c);
     }
 #pragma unroll
-    for (int s = 0; s < S; ++s) X[s] = N[s];
+    for (int s = 0; s < S; ++s) Y[s] = N[s];
 }
 
 template <int S>
 __device__ __forceinline__ uint32_t dp_1f1b(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S],
                                             const Comm<S> &c) {
-    uint32_t X[S];
-#pragma unroll
-    for (int s = 0; s < S; ++s) X[s] = 0;
+    uint32_t Y[S];
+    dp_init<S>(Y, c);
 #pragma unroll
     for (int k = 0; k < 2 * S - 1; ++k) {
         uint32_t N[S];
 #pragma unroll
-        for (int s = 0; s < S; ++s) N[s] = node<S>(pro_op(S, s + 1, k), s, X, F, B, c);
+        for (int s = 0; s < S; ++s) N[s] = node<S>(pro_op(S, s + 1, k), s, Y, F, B, c);
 #pragma unroll
-        for (int s = 0; s < S; ++s) X[s] = N[s];
+        for (int s = 0; s < S; ++s) Y[s] = N[s];
     }
     // steady: slots 2S-1 .. 2M-1; 2S-1 is odd
     for (uint32_t it = S; it < M; ++it) {
-        steady_slot<S>(1, X, F, B, c);
-        steady_slot<S>(0, X, F, B, c);
+        steady_slot<S>(1, Y, F, B, c);
+        steady_slot<S>(0, Y, F, B, c);
     }
-    steady_slot<S>(1, X, F, B, c);
+    steady_slot<S>(1, Y, F, B, c);
 #pragma unroll
     for (int j = 0; j < 2 * S - 2; ++j) {
         uint32_t N[S];
 #pragma unroll
-        for (int s = 0; s < S; ++s) N[s] = node<S>(epi_op(S, s + 1, j), s, X, F, B, c);
+        for (int s = 0; s < S; ++s) N[s] = node<S>(epi_op(S, s + 1, j), s, Y, F, B, c);
 #pragma unroll
-        for (int s = 0; s < S; ++s) X[s] = N[s];
+        for (int s = 0; s < S; ++s) Y[s] = N[s];
     }
-    return X[0];
+    return Y[0] - c.phi0;
 }
 
 // Any M (used when M < S): the slot schedule comes from a table of
@@ -245,21 +261,20 @@ __device__ __forceinline__ uint32_t dp_1f1b(uint32_t M, const uint32_t (&F)[S], 
 template <int S>
 __device__ __forceinline__ uint32_t dp_table(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
                                              const Comm<S> &c) {
-    uint32_t X[S];
-#pragma unroll
-    for (int s = 0; s < S; ++s) X[s] = 0;
+    uint32_t Y[S];
+    dp_init<S>(Y, c);
     for (uint32_t k = 0; k < p.nslots; ++k) {
         const uint32_t fm = p.slot_mask[2 * k], bm = p.slot_mask[2 * k + 1];
         uint32_t N[S];
 #pragma unroll
         for (int s = 0; s < S; ++s) {
             const int op = ((fm >> s) & 1u) ? kFwd : (((bm >> s) & 1u) ? kBwd : kIdle);
-            N[s] = node<S>(op, s, X, F, B, c);
+            N[s] = node<S>(op, s, Y, F, B, c);
         }
 #pragma unroll
-        for (int s = 0; s < S; ++s) X[s] = N[s];
+        for (int s = 0; s < S; ++s) Y[s] = N[s];
     }
-    return X[0];
+    return Y[0] - c.phi0;
 }
 
 template <int S>
@@ -272,11 +287,13 @@ __device__ __forceinline__ uint32_t makespan(const KParams &p, const uint32_t (&
 template <int S>
 __device__ __forceinline__ Comm<S> load_comm(const KParams &p) {
     Comm<S> c;
+    uint32_t phi = 0;
 #pragma unroll
     for (int s = 0; s < (S > 1 ? S - 1 : 1); ++s) {
-        c.f[s] = p.cf[s];
-        c.b[s] = p.cb[s];
+        c.e[s] = p.cf[s] + p.cb[s];
+        phi += p.cf[s];
     }
+    c.phi0 = phi;
     return c;
 }
 
