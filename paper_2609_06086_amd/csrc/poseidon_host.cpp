@@ -167,6 +167,8 @@ struct poseidon_ctx {
     unsigned long long *state;
     size_t lds_bytes;
     uint32_t grid_max;
+    void *ws;              // cut codes + straggler queues of the steady-state cascade
+    uint64_t ws_cap;       // candidates per chunk the workspace holds
 };
 
 extern "C" {
@@ -275,6 +277,15 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     kp.L = L; kp.S = S; kp.M = M; kp.T = T; kp.NB = NB;
     kp.wide = wide;
     for (uint32_t b = 0; b + 1 < S; ++b) { kp.cf[b] = p->comm_fwd_us[b]; kp.cb[b] = p->comm_bwd_us[b]; }
+    // cascade checkpoints of the steady loop: S, 2S, 4S, ... below M - S
+    if (M >= S) {
+        const uint32_t nit = M - S;
+        uint32_t k = std::max<uint32_t>(2, S);
+        while (k < nit && kp.nlevels < (uint32_t)pk::kMaxLevels) {
+            kp.lvl_k[kp.nlevels++] = k;
+            k *= 2;
+        }
+    }
     const bool has_table = p->assign && A > 1;
     if (A == 1) {
         kp.assign_mode = pk::kAssignFixed;
@@ -367,6 +378,7 @@ void poseidon_free(poseidon_ctx *ctx) {
     if (!ctx) return;
     int prev = 0;
     if (hipGetDevice(&prev) == hipSuccess && hipSetDevice(ctx->device) == hipSuccess) {
+        if (ctx->ws) (void)hipFree(ctx->ws);
         (void)hipFree(ctx->dmem);
         (void)hipSetDevice(prev);
     }
@@ -422,6 +434,47 @@ int read_best(poseidon_ctx *ctx, hipStream_t st, unsigned long long word_index, 
     return POSEIDON_OK;
 }
 
+// Largest number of candidates one launch sequence handles; longer calls
+// are processed in chunks of this size.
+constexpr uint64_t kChunk = 1ull << 26;
+
+// Workspace for chunks of up to `n` candidates: the cut codes [words][n]
+// and, with a cascade, two straggler queues of qcap x (1 + words + S) uint32
+// (qcap = n plus one block of slack per segment) and the per-block queue
+// counts [levels][grid_max].  Grown on demand; the old buffer is released
+// only after the stream has drained.
+uint64_t queue_cap(const poseidon_ctx *ctx, uint64_t n) { return n + (uint64_t)ctx->grid_max * 256; }
+
+int ensure_workspace(poseidon_ctx *ctx, uint64_t n, hipStream_t st) {
+    if (ctx->ws_cap >= n) return POSEIDON_OK;
+    if (ctx->ws) {
+        if (hipStreamSynchronize(st) != hipSuccess) return POSEIDON_E_DEVICE;
+        (void)hipFree(ctx->ws);
+        ctx->ws = nullptr;
+        ctx->ws_cap = 0;
+    }
+    const uint64_t cap = std::max<uint64_t>(n, 1024);
+    const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
+    uint64_t elems = words * cap;
+    if (ctx->base.nlevels)
+        elems += 2 * (1 + words + ctx->S) * queue_cap(ctx, cap) + (uint64_t)pk::kMaxLevels * ctx->grid_max;
+    void *q = nullptr;
+    if (hipMalloc(&q, elems * 4) != hipSuccess) {
+        (void)hipGetLastError();
+        return POSEIDON_E_NOMEM;
+    }
+    ctx->ws = q;
+    ctx->ws_cap = cap;
+    return POSEIDON_OK;
+}
+
+// After a failed launch: re-arm the reduction words and queue counters.
+int rearm(poseidon_ctx *ctx, hipStream_t st) {
+    (void)pk::launch_fill(ctx->state + W_ACC, 1, ~0ull, st);
+    (void)pk::launch_fill(ctx->state + W_DONE, 1, 0ull, st);
+    return POSEIDON_E_DEVICE;
+}
+
 }  // namespace
 
 extern "C" {
@@ -447,11 +500,37 @@ int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands, uin
     kp.makespan_out = makespan_out;
     kp.feas_bits_out = feasible_bits_out;
     kp.nwords = (cands->count + 31) / 32;
-    pk::LaunchCfg lc;
-    lc.lds_bytes = ctx->lds_bytes;
-    const uint64_t want = (cands->count + 255) / 256;
-    lc.grid = (uint32_t)std::min<uint64_t>(want, ctx->grid_max);
-    if (pk::launch_eval(kp, lc, st) != hipSuccess) return POSEIDON_E_DEVICE;
+    const uint64_t chunk = std::min<uint64_t>(cands->count, kChunk);
+    rc = ensure_workspace(ctx, chunk, st);
+    if (rc != POSEIDON_OK) return rc;
+    const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
+    uint32_t *ws = (uint32_t *)ctx->ws;
+    kp.codes = ws;
+    kp.ccap = ctx->ws_cap;
+    if (kp.nlevels) {
+        kp.qcap = queue_cap(ctx, ctx->ws_cap);
+        kp.queue[0] = ws + words * ctx->ws_cap;
+        kp.queue[1] = kp.queue[0] + (1 + words + ctx->S) * kp.qcap;
+        kp.qcount = kp.queue[1] + (1 + words + ctx->S) * kp.qcap;
+    }
+    for (uint64_t c0 = 0; c0 < cands->count; c0 += chunk) {
+        kp.first_i = c0;
+        kp.n_i = std::min(chunk, cands->count - c0);
+        kp.accumulate = c0 > 0;
+        pk::LaunchCfg lc;
+        lc.lds_bytes = ctx->lds_bytes;
+        lc.grid = (uint32_t)std::min<uint64_t>((kp.n_i + 255) / 256, ctx->grid_max);
+        // queue segments: block b of every level owns seg_cap slots
+        const uint64_t stride = (uint64_t)lc.grid * 256;
+        kp.nseg = lc.grid;
+        kp.seg_cap = (kp.n_i + stride - 1) / stride * 256;
+        pk::LaunchCfg ld = lc;
+        ld.grid = (uint32_t)std::min<uint64_t>((kp.n_i + 4 * 256 - 1) / (4 * 256), ctx->grid_max);
+        if (pk::launch_decode(kp, ld, st) != hipSuccess) return rearm(ctx, st);
+        if (pk::launch_eval(kp, lc, st) != hipSuccess) return rearm(ctx, st);
+        for (uint32_t l = 1; l <= kp.nlevels; ++l)
+            if (pk::launch_resume(kp, lc, st, l) != hipSuccess) return rearm(ctx, st);
+    }
     if (best_out) return read_best(ctx, st, W_RESULT, best_out);
     return POSEIDON_OK;
 }

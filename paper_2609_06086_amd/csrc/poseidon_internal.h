@@ -7,6 +7,7 @@
 namespace pk {
 
 constexpr int kSMax = 16;
+constexpr int kMaxLevels = 6;   // cascade checkpoints of the steady loop
 
 enum AssignMode : uint32_t { kAssignFixed = 0, kAssignTable = 1, kAssignDigits = 2 };
 
@@ -40,6 +41,21 @@ struct KParams {
     unsigned long long *run_best;
     unsigned long long *stats;   // evaluated, pruned, infeasible
     unsigned int *err;
+    // steady-state cascade: lanes not settled at iteration lvl_k[l-1] are
+    // queued (candidate index + registers) and resumed by level l
+    uint32_t nlevels;                 // 0 = no cascade
+    uint32_t lvl_k[kMaxLevels];
+    unsigned int *qcount;             // [level][nseg]: entries block b queued for level + 1
+    uint32_t *queue[2];               // ping-pong queues: level l reads queue (l-1) & 1;
+                                      // each idx[qcap] | codes[words][qcap] | Y[S][qcap],
+                                      // block b owning slots [b * seg_cap, (b+1) * seg_cap)
+    uint64_t qcap, seg_cap;
+    uint32_t nseg;                    // blocks of the level-0 grid (= every level's grid)
+    // the current chunk of the call: candidates first_i .. first_i + n_i - 1
+    uint64_t first_i, n_i;
+    uint32_t *codes;                  // [words][ccap] compact cut points of the chunk
+    uint64_t ccap;
+    uint32_t accumulate;              // fold the chunk's best into *result (not the first chunk)
 };
 
 struct LaunchCfg {
@@ -48,12 +64,15 @@ struct LaunchCfg {
 };
 
 hipError_t launch_eval(const KParams &p, const LaunchCfg &lc, hipStream_t st);
+hipError_t launch_decode(const KParams &p, const LaunchCfg &lc, hipStream_t st);
+hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl);
 hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
                           uint32_t bound);
 hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, int *blocks);
 hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,
                          unsigned long long *acc, unsigned int *done, unsigned long long *result, hipStream_t st);
 hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, hipStream_t st);
+int code_words(int S);
 int prologue_op(int S, int s, int k);
 int epilogue_op(int S, int s, int j);
 

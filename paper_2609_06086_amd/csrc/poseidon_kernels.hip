@@ -71,13 +71,54 @@ __device__ __forceinline__ void decode_cuts(R r, const R *binom, uint32_t L, uin
     for (int j = 1; j <= S - 1; ++j) {
         const R *col = binom + (S - j) * NB;
         const R Q = col[L - a] - r;
+        // fixed 8 halvings (NB <= 256); halvings wider than the table are
+        // no-ops, so the search is straight-line code for any NB
         uint32_t pos = 0;
-        for (uint32_t step = NB >> 1; step >= 1; step >>= 1)
-            if (col[pos + step - 1] < Q) pos += step;
+#pragma unroll
+        for (int b = 7; b >= 0; --b) {
+            const uint32_t step = 1u << b;
+            const uint32_t at = min(pos + step - 1u, NB - 1u);
+            pos += (step < NB && col[at] < Q) ? step : 0u;
+        }
         r = col[pos] - Q;
         cut[j] = L - pos;
         a = cut[j] + 1;
     }
+}
+
+// Cut points in compact form: cut j (1-based) is byte (j-1) % 4 of word
+// (j-1) / 4; a valid composition has c_1 >= 1, so an all-zero first byte
+// marks an invalid candidate (for S = 1 the single byte is 1 when valid).
+template <int S>
+struct Codes {
+    static constexpr int kWords = S > 1 ? (S - 1 + 3) / 4 : 1;
+};
+
+template <int S>
+__device__ __forceinline__ void pack_cuts(const uint32_t (&cut)[S + 1], bool ok, uint32_t (&w)[Codes<S>::kWords]) {
+#pragma unroll
+    for (int k = 0; k < Codes<S>::kWords; ++k) w[k] = 0;
+    if (S == 1) {
+        w[0] = ok ? 1u : 0u;
+        return;
+    }
+#pragma unroll
+    for (int j = 1; j <= S - 1; ++j) w[(j - 1) / 4] |= (ok ? cut[j] : 0u) << (8 * ((j - 1) % 4));
+}
+
+template <int S>
+__device__ __forceinline__ bool unpack_cuts(const uint32_t (&w)[Codes<S>::kWords], uint32_t L,
+                                            uint32_t (&cut)[S + 1]) {
+    cut[0] = 0;
+    cut[S] = L;
+#pragma unroll
+    for (int j = 1; j <= S - 1; ++j) cut[j] = (w[(j - 1) / 4] >> (8 * ((j - 1) % 4))) & 0xFFu;
+    const bool ok = (w[0] & 0xFFu) != 0u;
+    if (!ok) {
+#pragma unroll
+        for (int j = 1; j <= S - 1; ++j) cut[j] = 0;
+    }
+    return ok;
 }
 
 template <int S>
@@ -120,6 +161,13 @@ __device__ __forceinline__ bool candidate(const KParams &p, uint64_t i, R &r, ui
     r = ok ? (R)rank : (R)0;
     a = ok ? (uint32_t)asg : 0u;
     return ok;
+}
+
+// Assignment index of candidate i (valid candidates only).
+__device__ __forceinline__ uint32_t assign_of(const KParams &p, uint64_t i) {
+    if (p.comp_rank) return p.assign_idx ? p.assign_idx[i] : 0u;
+    if (p.A == 1) return 0u;
+    return (uint32_t)((p.first + i) % p.A);
 }
 
 // ---------------------------------------------------------------------------
@@ -226,10 +274,10 @@ __device__ __forceinline__ void steady_slot(int parity, uint32_t (&Y)[S], const 
     for (int s = 0; s < S; ++s) Y[s] = N[s];
 }
 
+// init + prologue (slots 0 .. 2S-2)
 template <int S>
-__device__ __forceinline__ uint32_t dp_1f1b(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S],
+__device__ __forceinline__ void dp_prologue(uint32_t (&Y)[S], const uint32_t (&F)[S], const uint32_t (&B)[S],
                                             const Comm<S> &c) {
-    uint32_t Y[S];
     dp_init<S>(Y, c);
 #pragma unroll
     for (int k = 0; k < 2 * S - 1; ++k) {
@@ -239,11 +287,20 @@ __device__ __forceinline__ uint32_t dp_1f1b(uint32_t M, const uint32_t (&F)[S], 
 #pragma unroll
         for (int s = 0; s < S; ++s) Y[s] = N[s];
     }
-    // steady: slots 2S-1 .. 2M-1; 2S-1 is odd
-    for (uint32_t it = S; it < M; ++it) {
-        steady_slot<S>(1, Y, F, B, c);
-        steady_slot<S>(0, Y, F, B, c);
-    }
+}
+
+// one steady iteration: an odd slot then an even slot (slots 2S-1+2i, 2S+2i)
+template <int S>
+__device__ __forceinline__ void dp_iter(uint32_t (&Y)[S], const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                        const Comm<S> &c) {
+    steady_slot<S>(1, Y, F, B, c);
+    steady_slot<S>(0, Y, F, B, c);
+}
+
+// the last steady slot (2M-1) and the epilogue; returns T
+template <int S>
+__device__ __forceinline__ uint32_t dp_finish(uint32_t (&Y)[S], const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                              const Comm<S> &c) {
     steady_slot<S>(1, Y, F, B, c);
 #pragma unroll
     for (int j = 0; j < 2 * S - 2; ++j) {
@@ -254,6 +311,53 @@ __device__ __forceinline__ uint32_t dp_1f1b(uint32_t M, const uint32_t (&F)[S], 
         for (int s = 0; s < S; ++s) Y[s] = N[s];
     }
     return Y[0] - c.phi0;
+}
+
+template <int S>
+__device__ __forceinline__ uint32_t dp_1f1b(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                            const Comm<S> &c) {
+    uint32_t Y[S];
+    dp_prologue<S>(Y, F, B, c);
+    for (uint32_t it = S; it < M; ++it) dp_iter<S>(Y, F, B, c);
+    return dp_finish<S>(Y, F, B, c);
+}
+
+// The steady iteration is one fixed map Y -> A(Y) built from max and +
+// only, so A(Y + c) = A(Y) + c for every constant c.  Once one iteration
+// raises every stage by the same amount d, every later iteration does the
+// same: after n more iterations the state is exactly Y + n d.  The kernels
+// check this at a few iteration counts; a lane that passes jumps to the end
+// of the steady part, the others are queued and resumed by the next level.
+template <int S>
+__device__ __forceinline__ bool dp_settled(const uint32_t (&Y)[S], const uint32_t (&Yp)[S], uint32_t &d) {
+    d = Y[0] - Yp[0];
+    bool same = true;
+#pragma unroll
+    for (int s = 1; s < S; ++s) same = same && (Y[s] - Yp[s] == d);
+    return same;
+}
+
+// run iterations k0+1 .. k1 (k0 <= k1 <= nit); returns whether the state
+// settled by iteration k1 and, if so, moves it to iteration `nit` (the end).
+// With k1 = nit it simply runs to the end.
+template <int S>
+__device__ __forceinline__ bool dp_advance(uint32_t (&Y)[S], const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                           const Comm<S> &c, uint32_t k0, uint32_t k1, uint32_t nit) {
+    if (k1 >= nit) {
+        for (uint32_t it = k0; it < nit; ++it) dp_iter<S>(Y, F, B, c);
+        return true;
+    }
+    for (uint32_t it = k0 + 1; it < k1; ++it) dp_iter<S>(Y, F, B, c);
+    uint32_t Yp[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) Yp[s] = Y[s];
+    dp_iter<S>(Y, F, B, c);
+    uint32_t d;
+    const bool ok = dp_settled<S>(Y, Yp, d);
+    const uint32_t jump = ok ? (nit - k1) * d : 0u;
+#pragma unroll
+    for (int s = 0; s < S; ++s) Y[s] += jump;
+    return ok;
 }
 
 // Any M (used when M < S): the slot schedule comes from a table of
@@ -324,14 +428,16 @@ __device__ __forceinline__ unsigned long long wave_min(unsigned long long v) {
     return v;
 }
 
-// Block min of `v`, folded into *acc; the last block of the grid moves *acc
-// to *result and re-arms *acc and *done for the next launch.  Returns true
-// in thread 0 of the last block (after the hand-over).
-__device__ __forceinline__ bool block_min_and_finish(unsigned long long v, unsigned long long *acc,
+// Block min of `v`, folded into *acc.  When `finalize` is set (the last
+// kernel of an evaluation chunk), the last block of the grid also moves *acc
+// to *result (or folds it in, for the second and later chunks of a call,
+// and/or into *run_best) and re-arms *acc, *done and the straggler-queue
+// counters.
+__device__ __forceinline__ void block_min_and_finish(unsigned long long v, unsigned long long *acc,
                                                      unsigned int *done, unsigned long long *result,
-                                                     unsigned long long *run_best) {
+                                                     unsigned long long *run_best, bool finalize,
+                                                     bool accumulate = false) {
     __shared__ unsigned long long part[kWaves];
-    __shared__ int last;
     v = wave_min(v);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     if (lane == 0) part[wave] = v;
@@ -341,19 +447,21 @@ __device__ __forceinline__ bool block_min_and_finish(unsigned long long v, unsig
 #pragma unroll
         for (int w = 1; w < kWaves; ++w) m = part[w] < m ? part[w] : m;
         if (m != ~0ull) atomicMin(acc, m);
-        __threadfence();
-        const unsigned int ticket = atomicAdd(done, 1u);
-        last = (ticket == gridDim.x - 1);
-        if (last) {
+        if (finalize) {
             __threadfence();
-            const unsigned long long k = atomicExch(acc, ~0ull);
-            if (result) atomicExch(result, k);
-            if (run_best) atomicMin(run_best, k);
-            atomicExch(done, 0u);
+            const unsigned int ticket = atomicAdd(done, 1u);
+            if (ticket == gridDim.x - 1) {
+                __threadfence();
+                const unsigned long long k = atomicExch(acc, ~0ull);
+                if (result) {
+                    if (accumulate) atomicMin(result, k);
+                    else atomicExch(result, k);
+                }
+                if (run_best) atomicMin(run_best, k);
+                atomicExch(done, 0u);
+            }
         }
     }
-    __syncthreads();
-    return last && threadIdx.x == 0;
 }
 
 __device__ __forceinline__ unsigned long long make_key(bool feasible, uint32_t T, uint32_t i) {
@@ -364,44 +472,231 @@ __device__ __forceinline__ unsigned long long make_key(bool feasible, uint32_t T
 // kernels
 // ---------------------------------------------------------------------------
 
-// Exhaustive evaluation; grid-stride over the call's candidates.
+// Layout of one straggler queue: idx[cap] | codes[kWords][cap] | Y[S][cap].
+template <int S>
+struct QueueView {
+    uint32_t *idx, *codes, *Y;
+    __device__ __forceinline__ QueueView(const KParams &p, int which) {
+        idx = p.queue[which];
+        codes = idx + p.qcap;
+        Y = codes + (uint64_t)Codes<S>::kWords * p.qcap;
+    }
+};
+
+// Queue a wave's unsettled lanes (candidate index, cut codes, registers)
+// for the next level.  Block b owns slots [b * seg_cap, (b + 1) * seg_cap)
+// of the queue and counts its entries in LDS (*nq), so no global atomic is
+// involved; every lane of the wave must call this.
+template <int S>
+__device__ __forceinline__ void enqueue(const KParams &p, int which, unsigned int *nq, bool want, uint32_t idx,
+                                        const uint32_t (&w)[Codes<S>::kWords], const uint32_t (&Y)[S]) {
+    const unsigned long long m = __ballot(want);
+    if (m == 0) return;
+    const unsigned int lane = threadIdx.x & 63;
+    unsigned int base = 0;
+    if (lane == 0) base = atomicAdd(nq, (unsigned int)__popcll(m));
+    base = __shfl(base, 0, 64);
+    if (want) {
+        const unsigned long long below = lane ? (m & ((1ull << lane) - 1ull)) : 0ull;
+        const uint64_t slot = (uint64_t)blockIdx.x * p.seg_cap + base + __popcll(below);
+        const QueueView<S> q(p, which);
+        q.idx[slot] = idx;
+#pragma unroll
+        for (int k = 0; k < Codes<S>::kWords; ++k) q.codes[(uint64_t)k * p.qcap + slot] = w[k];
+#pragma unroll
+        for (int s = 0; s < S; ++s) q.Y[(uint64_t)s * p.qcap + slot] = Y[s];
+    }
+}
+
+// (a1) Unrank every candidate of the chunk [p.first_i, p.first_i + p.n_i)
+// into compact cut codes.  Each lane walks kIlp candidates through their
+// searches together so that the dependent LDS reads of one overlap those of
+// the others.  Invalid (rank, assignment) pairs get the invalid code and
+// raise the error flag.
+constexpr int kIlp = 4;
+
+template <int S, typename R>
+__global__ __launch_bounds__(kBlock) void decode_kernel(KParams p) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    R *binom = reinterpret_cast<R *>(smem);
+    const uint32_t nbin = p.S * p.NB;
+    const R *gb = reinterpret_cast<const R *>(p.binom);
+    for (uint32_t i = threadIdx.x; i < nbin; i += kBlock) binom[i] = gb[i];
+    __syncthreads();
+    constexpr int NW = Codes<S>::kWords;
+    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    bool bad = false;
+    for (uint64_t base = (uint64_t)blockIdx.x * kBlock + threadIdx.x; base < p.n_i; base += kIlp * stride) {
+        R r[kIlp];
+        bool ok[kIlp];
+        uint32_t w[kIlp][NW], at[kIlp];
+#pragma unroll
+        for (int u = 0; u < kIlp; ++u) {
+            const uint64_t i = base + u * stride;
+            const bool act = i < p.n_i;
+            uint32_t a;
+            ok[u] = candidate<R>(p, p.first_i + (act ? i : 0), r[u], a) && act;
+            bad |= act && !ok[u];
+            at[u] = 1;
+#pragma unroll
+            for (int k = 0; k < NW; ++k) w[u][k] = 0;
+        }
+        // the searches, cut by cut, interleaved over the kIlp candidates;
+        // each cut goes straight into its byte of the code words
+#pragma unroll
+        for (int j = 1; j <= S - 1; ++j) {
+            const R *col = binom + (S - j) * p.NB;
+            R Q[kIlp];
+            uint32_t pos[kIlp];
+#pragma unroll
+            for (int u = 0; u < kIlp; ++u) {
+                Q[u] = col[p.L - at[u]] - r[u];
+                pos[u] = 0;
+            }
+#pragma unroll
+            for (int b = 7; b >= 0; --b) {
+                const uint32_t step = 1u << b;
+#pragma unroll
+                for (int u = 0; u < kIlp; ++u) {
+                    const uint32_t x = min(pos[u] + step - 1u, p.NB - 1u);
+                    pos[u] += (step < p.NB && col[x] < Q[u]) ? step : 0u;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kIlp; ++u) {
+                r[u] = col[pos[u]] - Q[u];
+                const uint32_t c = p.L - pos[u];
+                w[u][(j - 1) / 4] |= c << (8 * ((j - 1) % 4));
+                at[u] = c + 1;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kIlp; ++u) {
+            const uint64_t i = base + u * stride;
+            if (i < p.n_i) {
+                if (S == 1) w[u][0] = 1u;
+                if (!ok[u]) {
+#pragma unroll
+                    for (int k = 0; k < NW; ++k) w[u][k] = 0u;
+                }
+#pragma unroll
+                for (int k = 0; k < NW; ++k) p.codes[(uint64_t)k * p.ccap + i] = w[u][k];
+            }
+        }
+    }
+    if (bad) atomicOr(p.err, 1u);
+}
+
+// (a2)-(a4), (a6) for the chunk: stage weights from the cut codes, memory
+// check, the DP and the reduction.  With a cascade (p.nlevels > 0) a lane
+// whose steady state has not settled by iteration p.lvl_k[0] is queued for
+// resume_kernel instead of finishing here.
 template <int S, typename R>
 __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
     const Lds<R> tab = stage_tables<R>(p, smem);
     const Comm<S> comm = load_comm<S>(p);
+    constexpr int NW = Codes<S>::kWords;
     unsigned long long best = ~0ull;
-    bool bad = false;
     const uint64_t stride = (uint64_t)gridDim.x * kBlock;
     // every wave runs the same trip count so that ballots see whole waves
-    const uint64_t span = (p.count + stride - 1) / stride;
+    const uint64_t span = (p.n_i + stride - 1) / stride;
+    const uint32_t nit = p.M >= (uint32_t)S ? p.M - S : 0u;
+    __shared__ unsigned int nq;
+    if (threadIdx.x == 0) nq = 0;
+    __syncthreads();
     uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
     for (uint64_t it = 0; it < span; ++it, i += stride) {
-        const bool active = i < p.count;
-        R r;
-        uint32_t a;
-        const bool ok = candidate<R>(p, active ? i : 0, r, a);
-        bad |= active && !ok;
+        const bool active = i < p.n_i;
+        const uint64_t gi = p.first_i + i;   // index within the call
+        uint32_t w[NW];
+#pragma unroll
+        for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[(uint64_t)k * p.ccap + i] : 0u;
         uint32_t cut[S + 1], ty[S], F[S], B[S];
-        decode_cuts<S, R>(r, tab.binom, p.L, p.NB, cut);
-        decode_types<S>(p, a, ty);
+        const bool ok = unpack_cuts<S>(w, p.L, cut);
+        decode_types<S>(p, ok ? assign_of(p, gi) : 0u, ty);
         const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B) && ok && active;
-        uint32_t T = makespan<S>(p, F, B, comm);
+        uint32_t T;
+        bool done_here = true;
+        if (p.M < (uint32_t)S) {
+            T = dp_table<S>(p, F, B, comm);
+        } else {
+            uint32_t Y[S];
+            dp_prologue<S>(Y, F, B, comm);
+            const uint32_t k1 = p.nlevels ? p.lvl_k[0] : nit;
+            done_here = dp_advance<S>(Y, F, B, comm, 0, k1, nit);
+            if (p.nlevels) enqueue<S>(p, 0, &nq, !done_here && active && ok, (uint32_t)gi, w, Y);
+            T = dp_finish<S>(Y, F, B, comm);
+        }
         if (!ok) T = 0xFFFFFFFFu;
-        if (active && p.makespan_out) p.makespan_out[i] = T;
+        const bool write = active && (done_here || !ok);
+        if (write && p.makespan_out) p.makespan_out[gi] = T;
         if (p.feas_bits_out) {
+            // chunks start at multiples of 64, so a wave covers 64 aligned candidates
             const unsigned long long bits = __ballot(feas);
-            const uint64_t w0 = (i - (threadIdx.x & 63)) >> 5;
+            const uint64_t w0 = (gi - (threadIdx.x & 63)) >> 5;
             if ((threadIdx.x & 63) == 0 && w0 < p.nwords) p.feas_bits_out[w0] = (uint32_t)bits;
             if ((threadIdx.x & 63) == 32 && w0 + 1 < p.nwords) p.feas_bits_out[w0 + 1] = (uint32_t)(bits >> 32);
         }
-        if (active) {
-            const unsigned long long key = make_key(feas, T, (uint32_t)i);
+        if (write) {
+            const unsigned long long key = make_key(feas, T, (uint32_t)gi);
             best = key < best ? key : best;
         }
     }
-    if (__ballot(bad) != 0 && (threadIdx.x & 63) == 0) atomicOr(p.err, 1u);
-    block_min_and_finish(best, p.acc, p.done, p.result, nullptr);
+    if (p.nlevels) {
+        __syncthreads();
+        if (threadIdx.x == 0) p.qcount[blockIdx.x] = nq;   // entries for level 1
+    }
+    block_min_and_finish(best, p.acc, p.done, p.result, nullptr, p.nlevels == 0, p.accumulate);
+}
+
+// Level `lvl` of the cascade: resume the queued lanes from iteration
+// p.lvl_k[lvl-1] to p.lvl_k[lvl] (the end at the last level).
+template <int S, typename R>
+__global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const Lds<R> tab = stage_tables<R>(p, smem);
+    const Comm<S> comm = load_comm<S>(p);
+    constexpr int NW = Codes<S>::kWords;
+    const uint32_t nit = p.M - S;
+    const uint32_t k0 = p.lvl_k[lvl - 1];
+    const uint32_t k1 = lvl < p.nlevels ? p.lvl_k[lvl] : nit;
+    // this block's segment of the queue written by level lvl - 1
+    const uint32_t n = __hip_atomic_load(&p.qcount[(uint64_t)(lvl - 1) * p.nseg + blockIdx.x], __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+    const QueueView<S> qin(p, (lvl - 1) & 1);
+    __shared__ unsigned int nq;
+    if (threadIdx.x == 0) nq = 0;
+    __syncthreads();
+    unsigned long long best = ~0ull;
+    const uint32_t span = (n + kBlock - 1) / kBlock;
+    const uint64_t seg = (uint64_t)blockIdx.x * p.seg_cap;
+    for (uint32_t it = 0; it < span; ++it) {
+        const uint32_t q = it * kBlock + threadIdx.x;
+        const bool active = q < n;
+        const uint32_t i = active ? qin.idx[seg + q] : 0u;
+        uint32_t w[NW], cut[S + 1], ty[S], F[S], B[S], Y[S];
+#pragma unroll
+        for (int k = 0; k < NW; ++k) w[k] = active ? qin.codes[(uint64_t)k * p.qcap + seg + q] : 0u;
+#pragma unroll
+        for (int s = 0; s < S; ++s) Y[s] = active ? qin.Y[(uint64_t)s * p.qcap + seg + q] : 0u;
+        const bool ok = unpack_cuts<S>(w, p.L, cut);
+        decode_types<S>(p, ok ? assign_of(p, i) : 0u, ty);
+        const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B);
+        const bool settled = dp_advance<S>(Y, F, B, comm, k0, k1, nit);
+        if (lvl < p.nlevels) enqueue<S>(p, lvl & 1, &nq, active && !settled, i, w, Y);
+        const uint32_t T = dp_finish<S>(Y, F, B, comm);
+        if (active && settled) {
+            if (p.makespan_out) p.makespan_out[i] = T;
+            const unsigned long long key = make_key(feas, T, i);
+            best = key < best ? key : best;
+        }
+    }
+    if (lvl < p.nlevels) {
+        __syncthreads();
+        if (threadIdx.x == 0) p.qcount[(uint64_t)lvl * p.nseg + blockIdx.x] = nq;
+    }
+    block_min_and_finish(best, p.acc, p.done, p.result, nullptr, lvl == p.nlevels, p.accumulate);
 }
 
 // Early stop (Eq. 2 / Theorem 1) over one chunk: each block filters a tile
@@ -476,7 +771,7 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
         atomicAdd(&p.stats[2], (unsigned long long)cnt_infeas);
         if (cnt_bad) atomicOr(p.err, 1u);
     }
-    block_min_and_finish(best, p.acc, p.done, nullptr, p.run_best);
+    block_min_and_finish(best, p.acc, p.done, nullptr, p.run_best, true);
 }
 
 // Argmin over stored makespans / feasibility bits.
@@ -490,7 +785,7 @@ __global__ __launch_bounds__(kBlock) void argmin_kernel(const uint32_t *T, const
         const unsigned long long key = make_key(f, T[i], (uint32_t)i);
         best = key < best ? key : best;
     }
-    block_min_and_finish(best, acc, done, result, nullptr);
+    block_min_and_finish(best, acc, done, result, nullptr, true);
 }
 
 // Small fill kernel used instead of memset so that the calls stay capturable.
@@ -505,6 +800,19 @@ __global__ void fill_u64(unsigned long long *p, uint32_t n, unsigned long long v
 template <int S, typename R>
 static hipError_t launch_eval_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
     hipLaunchKernelGGL((eval_kernel<S, R>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
+    return hipGetLastError();
+}
+
+template <int S, typename R>
+static hipError_t launch_decode_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
+    const size_t lds = (size_t)p.S * p.NB * sizeof(R);
+    hipLaunchKernelGGL((decode_kernel<S, R>), dim3(lc.grid), dim3(kBlock), lds, st, p);
+    return hipGetLastError();
+}
+
+template <int S, typename R>
+static hipError_t launch_resume_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl) {
+    hipLaunchKernelGGL((resume_kernel<S, R>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p, lvl);
     return hipGetLastError();
 }
 
@@ -546,6 +854,14 @@ hipError_t launch_eval(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
     PK_DISPATCH(launch_eval_s, p.S, p.wide, p, lc, st)
 }
 
+hipError_t launch_decode(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
+    PK_DISPATCH(launch_decode_s, p.S, p.wide, p, lc, st)
+}
+
+hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl) {
+    PK_DISPATCH(launch_resume_s, p.S, p.wide, p, lc, st, lvl)
+}
+
 hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
                           uint32_t bound) {
     PK_DISPATCH(launch_bounded_s, p.S, p.wide, p, lc, st, lo, hi, bound)
@@ -566,6 +882,7 @@ hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, 
     return hipGetLastError();
 }
 
+int code_words(int S) { return S > 1 ? (S - 1 + 3) / 4 : 1; }
 int prologue_op(int S, int s, int k) { return pro_op(S, s, k); }
 int epilogue_op(int S, int s, int j) { return epi_op(S, s, j); }
 

@@ -223,6 +223,29 @@ def test_range_past_end_is_rejected(dev):
     ctx.close()
 
 
+def test_context_reuse_across_sizes(dev):
+    """One context, calls of growing and shrinking size (the straggler queues
+    of the steady-state cascade are grown on demand and reused)."""
+    wl = W.workload(4)
+    ctx = P.poseidon_load_costs(wl.problem, 0)
+    for n in (1000, 200_003, 77, 1_000_001, 5000):
+        c = W.Candidates(comp_rank=wl.cands.comp_rank[:n].copy(), assign_idx=wl.cands.assign_idx[:n].copy())
+        Tg, fg, best = gpu_eval(ctx, c, dev)
+        To, fo = coracle.evaluate(wl.problem, c)
+        assert np.array_equal(Tg, To) and np.array_equal(fg, fo)
+        assert (best.index, best.makespan) == coracle.argmin(To, fo)
+    ctx.close()
+
+
+def test_long_steady_part_small_stage_count(dev):
+    """Many steady iterations for few stages (a deep cascade)."""
+    rng = np.random.default_rng(107)
+    for S, M in ((1, 300), (2, 200), (3, 150), (5, 400), (16, 600)):
+        L = S + 10
+        prob = W.random_problem(rng, L, S, M, 2, cost_hi=300, comm_hi=60, mem_hi=30, cap=300)
+        check_against_oracle(prob, W.random_candidates(rng, prob, 3000), dev)
+
+
 # --------------------------------------------------------- argmin, async
 
 def test_argmin_entry_point(dev):
