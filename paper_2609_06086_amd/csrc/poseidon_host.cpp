@@ -16,6 +16,10 @@
 #include "../../include/poseidon.h"
 #include "poseidon_internal.h"
 
+#ifndef PK_CASCADE_K0
+#define PK_CASCADE_K0 S   // first checkpoint of the steady-state cascade
+#endif
+
 namespace {
 
 // device state words of a context (one u64 each)
@@ -41,12 +45,6 @@ bool pow_fits(uint64_t base, uint64_t e, uint64_t limit, uint64_t *out) {
     }
     *out = (uint64_t)v;
     return true;
-}
-
-uint32_t next_pow2(uint32_t x) {
-    uint32_t p = 1;
-    while (p < x) p <<= 1;
-    return p;
 }
 
 // 1F1B order of stage s (1-based): min(S-s, M) forwards, then alternating
@@ -165,7 +163,7 @@ struct poseidon_ctx {
     pk::KParams base;      // table pointers and problem constants
     void *dmem;
     unsigned long long *state;
-    size_t lds_bytes;
+    size_t lds_bytes, lds_bounded;
     uint32_t grid_max;
     void *ws;              // cut codes + straggler queues of the steady-state cascade
     uint64_t ws_cap;       // candidates per chunk the workspace holds
@@ -234,7 +232,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     const uint64_t n_comp = binom_sat(L - 1, S - 1);
     const uint64_t A = n_comp ? ncand / n_comp : 0;
     const bool wide = n_comp > 0xFFFFFFFFull;
-    const uint32_t NB = next_pow2(L);
+    const uint32_t NB = pk::kNB;   // Pascal-table column length (L <= kNB)
 
     // schedule of the DAG: closed form for M >= S (self-checked), table otherwise
     std::vector<uint32_t> masks;
@@ -277,10 +275,10 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     kp.L = L; kp.S = S; kp.M = M; kp.T = T; kp.NB = NB;
     kp.wide = wide;
     for (uint32_t b = 0; b + 1 < S; ++b) { kp.cf[b] = p->comm_fwd_us[b]; kp.cb[b] = p->comm_bwd_us[b]; }
-    // cascade checkpoints of the steady loop: S, 2S, 4S, ... below M - S
+    // cascade checkpoints of the steady loop: K0, 2 K0, 4 K0, ... below M - S
     if (M >= S) {
         const uint32_t nit = M - S;
-        uint32_t k = std::max<uint32_t>(2, S);
+        uint32_t k = std::max<uint32_t>(2, PK_CASCADE_K0);
         while (k < nit && kp.nlevels < (uint32_t)pk::kMaxLevels) {
             kp.lvl_k[kp.nlevels++] = k;
             k *= 2;
@@ -348,8 +346,9 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         kp.stats = ctx->state + W_STAT_EVAL;
         kp.err = (unsigned int *)(ctx->state + W_ERR);
         kp.done = (unsigned int *)(ctx->state + W_DONE);
-        const size_t lds = ((cost.size() * 8 + binom.size() + pm.size() * 4 + (size_t)T * 4) + 15) & ~(size_t)15;
-        if (lds > 64 * 1024) { status = POSEIDON_E_RANGE; break; }
+        const size_t lds = ((cost.size() * 8 + pm.size() * 4 + (size_t)T * 4) + 15) & ~(size_t)15;
+        const size_t lds_bounded = lds + binom.size() + 8;
+        if (lds_bounded > 64 * 1024) { status = POSEIDON_E_RANGE; break; }
         int occ = 0;
         hipDeviceProp_t prop;
         if (pk::eval_occupancy(S, wide, lds, &occ) != hipSuccess || hipGetDeviceProperties(&prop, hip_device) != hipSuccess) {
@@ -357,6 +356,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
             break;
         }
         ctx->lds_bytes = lds;
+        ctx->lds_bounded = lds_bounded;
         ctx->grid_max = (uint32_t)std::max(1, occ) * (uint32_t)std::max(1, prop.multiProcessorCount);
     } while (0);
     (void)hipSetDevice(prev);
@@ -519,6 +519,7 @@ int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands, uin
         kp.accumulate = c0 > 0;
         pk::LaunchCfg lc;
         lc.lds_bytes = ctx->lds_bytes;
+        lc.lds_bounded = ctx->lds_bounded;
         lc.grid = (uint32_t)std::min<uint64_t>((kp.n_i + 255) / 256, ctx->grid_max);
         // queue segments: block b of every level owns seg_cap slots
         const uint64_t stride = (uint64_t)lc.grid * 256;
@@ -561,6 +562,7 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
     kp.assign_idx = cands->assign_idx;
     pk::LaunchCfg lc;
     lc.lds_bytes = ctx->lds_bytes;
+    lc.lds_bounded = ctx->lds_bounded;
     lc.grid = 0;
     const uint64_t n = cands->count;
     if (chunk == 0 || chunk > n) chunk = n;

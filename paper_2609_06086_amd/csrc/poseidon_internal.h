@@ -7,6 +7,7 @@
 namespace pk {
 
 constexpr int kSMax = 16;
+constexpr uint32_t kNB = 256;   // Pascal-table column length (n = 0..255; L <= 256)
 constexpr int kMaxLevels = 6;   // cascade checkpoints of the steady loop
 
 enum AssignMode : uint32_t { kAssignFixed = 0, kAssignTable = 1, kAssignDigits = 2 };
@@ -17,7 +18,7 @@ struct KParams {
     const uint64_t *cost;      // [T][L+1] (prefix bwd << 32) | prefix fwd
     const uint32_t *pm;        // [L+1] prefix memory
     const uint32_t *cap;       // [T]
-    const void *binom;         // [S][NB] C(n, k), uint32 or uint64 (wide)
+    const void *binom;         // [S][kNB] C(n, k), uint32 or uint64 (wide)
     const uint8_t *assign;     // [A][S] (table mode)
     const uint32_t *slot_mask; // [nslots][2] forward / backward stage masks (M < S)
     uint64_t A, n_comp;
@@ -60,7 +61,8 @@ struct KParams {
 
 struct LaunchCfg {
     uint32_t grid;
-    size_t lds_bytes;
+    size_t lds_bytes;     // eval / resume kernels: cost, pm, cap
+    size_t lds_bounded;   // early-stop kernel: the same plus the Pascal table
 };
 
 hipError_t launch_eval(const KParams &p, const LaunchCfg &lc, hipStream_t st);

@@ -30,23 +30,28 @@ struct Lds {
     const uint64_t *cost;   // [T][L+1]  (prefix bwd << 32) | prefix fwd
     const uint32_t *pm;     // [L+1]     prefix memory
     const uint32_t *cap;    // [T]
-    const R *binom;         // [S][NB]   C(n, k), saturated to R's maximum
+    const R *binom;         // [S][kNB]  C(n, k), saturated to R's maximum
 };
 
-template <typename R>
+// Layout: cost (8-byte entries) | pm | cap | binom (early-stop kernel only,
+// placed last and 8-byte aligned).
+template <typename R, bool kBinom>
 __device__ __forceinline__ Lds<R> stage_tables(const KParams &p, unsigned char *smem) {
-    // layout: cost (8-byte aligned) | binom | pm | cap
     uint64_t *cost = reinterpret_cast<uint64_t *>(smem);
     const uint32_t ncost = p.T * (p.L + 1);
-    R *binom = reinterpret_cast<R *>(cost + ncost);
-    const uint32_t nbin = p.S * p.NB;
-    uint32_t *pm = reinterpret_cast<uint32_t *>(binom + nbin);
+    uint32_t *pm = reinterpret_cast<uint32_t *>(cost + ncost);
     uint32_t *cap = pm + (p.L + 1);
+    R *binom = nullptr;
     for (uint32_t i = threadIdx.x; i < ncost; i += kBlock) cost[i] = p.cost[i];
-    const R *gb = reinterpret_cast<const R *>(p.binom);
-    for (uint32_t i = threadIdx.x; i < nbin; i += kBlock) binom[i] = gb[i];
     for (uint32_t i = threadIdx.x; i <= p.L; i += kBlock) pm[i] = p.pm[i];
     for (uint32_t i = threadIdx.x; i < p.T; i += kBlock) cap[i] = p.cap[i];
+    if (kBinom) {
+        const uintptr_t end = reinterpret_cast<uintptr_t>(cap + p.T);
+        binom = reinterpret_cast<R *>((end + 7) & ~(uintptr_t)7);
+        const uint32_t nbin = p.S * kNB;
+        const R *gb = reinterpret_cast<const R *>(p.binom);
+        for (uint32_t i = threadIdx.x; i < nbin; i += kBlock) binom[i] = gb[i];
+    }
     __syncthreads();
     return Lds<R>{cost, pm, cap, binom};
 }
@@ -62,23 +67,20 @@ __device__ __forceinline__ Lds<R> stage_tables(const KParams &p, unsigned char *
 // n* the smallest n with C(n, k+1) >= Q, found by a branch-free binary
 // search over column k+1 of the Pascal table; the rank left is C(n*, k+1) - Q.
 template <int S, typename R>
-__device__ __forceinline__ void decode_cuts(R r, const R *binom, uint32_t L, uint32_t NB,
-                                            uint32_t (&cut)[S + 1]) {
+__device__ __forceinline__ void decode_cuts(R r, const R *binom, uint32_t L, uint32_t (&cut)[S + 1]) {
     cut[0] = 0;
     cut[S] = L;
     uint32_t a = 1;
 #pragma unroll
     for (int j = 1; j <= S - 1; ++j) {
-        const R *col = binom + (S - j) * NB;
+        const R *col = binom + (S - j) * kNB;
         const R Q = col[L - a] - r;
-        // fixed 8 halvings (NB <= 256); halvings wider than the table are
-        // no-ops, so the search is straight-line code for any NB
+        // 8 halvings over the 256-entry column: straight-line code
         uint32_t pos = 0;
 #pragma unroll
         for (int b = 7; b >= 0; --b) {
             const uint32_t step = 1u << b;
-            const uint32_t at = min(pos + step - 1u, NB - 1u);
-            pos += (step < NB && col[at] < Q) ? step : 0u;
+            pos += col[pos + step - 1] < Q ? step : 0u;
         }
         r = col[pos] - Q;
         cut[j] = L - pos;
@@ -513,77 +515,97 @@ __device__ __forceinline__ void enqueue(const KParams &p, int which, unsigned in
 // searches together so that the dependent LDS reads of one overlap those of
 // the others.  Invalid (rank, assignment) pairs get the invalid code and
 // raise the error flag.
-constexpr int kIlp = 4;
+#ifndef PK_ILP
+#define PK_ILP 4
+#endif
+constexpr int kIlp = PK_ILP;
+
+// kIlp candidates per lane, H halvings per search (L <= 2^H).  The last cut
+// needs no search: with one cut left, C(n, 1) = n, so c_{S-1} = a + r.
+template <int S, typename R, int H>
+__device__ __forceinline__ void decode_batch(const KParams &p, const R *binom, uint64_t base, uint64_t stride,
+                                             bool &bad) {
+    constexpr int NW = Codes<S>::kWords;
+    R r[kIlp];
+    bool ok[kIlp];
+    uint32_t w[kIlp][NW], at[kIlp];
+#pragma unroll
+    for (int u = 0; u < kIlp; ++u) {
+        const uint64_t i = base + u * stride;
+        const bool act = i < p.n_i;
+        uint32_t a;
+        ok[u] = candidate<R>(p, p.first_i + (act ? i : 0), r[u], a) && act;
+        bad |= act && !ok[u];
+        at[u] = 1;
+#pragma unroll
+        for (int k = 0; k < NW; ++k) w[u][k] = 0;
+    }
+    // the searches, cut by cut, interleaved over the kIlp candidates; each
+    // cut goes straight into its byte of the code words
+#pragma unroll
+    for (int j = 1; j <= S - 2; ++j) {
+        const R *col = binom + (S - j) * kNB;
+        R Q[kIlp];
+        const R *q[kIlp];
+#pragma unroll
+        for (int u = 0; u < kIlp; ++u) {
+            Q[u] = col[p.L - at[u]] - r[u];
+            q[u] = col;
+        }
+#pragma unroll
+        for (int b = H - 1; b >= 0; --b) {
+            const uint32_t step = 1u << b;
+#pragma unroll
+            for (int u = 0; u < kIlp; ++u) q[u] += q[u][step - 1] < Q[u] ? step : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kIlp; ++u) {
+            const uint32_t pos = (uint32_t)(q[u] - col);
+            r[u] = col[pos] - Q[u];
+            const uint32_t c = p.L - pos;
+            w[u][(j - 1) / 4] |= c << (8 * ((j - 1) % 4));
+            at[u] = c + 1;
+        }
+    }
+    if (S >= 2) {
+#pragma unroll
+        for (int u = 0; u < kIlp; ++u) w[u][(S - 2) / 4] |= (at[u] + (uint32_t)r[u]) << (8 * ((S - 2) % 4));
+    }
+#pragma unroll
+    for (int u = 0; u < kIlp; ++u) {
+        const uint64_t i = base + u * stride;
+        if (i < p.n_i) {
+            if (S == 1) w[u][0] = 1u;
+            if (!ok[u]) {
+#pragma unroll
+                for (int k = 0; k < NW; ++k) w[u][k] = 0u;
+            }
+#pragma unroll
+            for (int k = 0; k < NW; ++k) p.codes[(uint64_t)k * p.ccap + i] = w[u][k];
+        }
+    }
+}
+
+template <int S, typename R, int H>
+__device__ __forceinline__ void decode_all(const KParams &p, const R *binom, bool &bad) {
+    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    for (uint64_t base = (uint64_t)blockIdx.x * kBlock + threadIdx.x; base < p.n_i; base += kIlp * stride)
+        decode_batch<S, R, H>(p, binom, base, stride, bad);
+}
 
 template <int S, typename R>
 __global__ __launch_bounds__(kBlock) void decode_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
     R *binom = reinterpret_cast<R *>(smem);
-    const uint32_t nbin = p.S * p.NB;
+    const uint32_t nbin = p.S * kNB;
     const R *gb = reinterpret_cast<const R *>(p.binom);
     for (uint32_t i = threadIdx.x; i < nbin; i += kBlock) binom[i] = gb[i];
     __syncthreads();
-    constexpr int NW = Codes<S>::kWords;
-    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
     bool bad = false;
-    for (uint64_t base = (uint64_t)blockIdx.x * kBlock + threadIdx.x; base < p.n_i; base += kIlp * stride) {
-        R r[kIlp];
-        bool ok[kIlp];
-        uint32_t w[kIlp][NW], at[kIlp];
-#pragma unroll
-        for (int u = 0; u < kIlp; ++u) {
-            const uint64_t i = base + u * stride;
-            const bool act = i < p.n_i;
-            uint32_t a;
-            ok[u] = candidate<R>(p, p.first_i + (act ? i : 0), r[u], a) && act;
-            bad |= act && !ok[u];
-            at[u] = 1;
-#pragma unroll
-            for (int k = 0; k < NW; ++k) w[u][k] = 0;
-        }
-        // the searches, cut by cut, interleaved over the kIlp candidates;
-        // each cut goes straight into its byte of the code words
-#pragma unroll
-        for (int j = 1; j <= S - 1; ++j) {
-            const R *col = binom + (S - j) * p.NB;
-            R Q[kIlp];
-            uint32_t pos[kIlp];
-#pragma unroll
-            for (int u = 0; u < kIlp; ++u) {
-                Q[u] = col[p.L - at[u]] - r[u];
-                pos[u] = 0;
-            }
-#pragma unroll
-            for (int b = 7; b >= 0; --b) {
-                const uint32_t step = 1u << b;
-#pragma unroll
-                for (int u = 0; u < kIlp; ++u) {
-                    const uint32_t x = min(pos[u] + step - 1u, p.NB - 1u);
-                    pos[u] += (step < p.NB && col[x] < Q[u]) ? step : 0u;
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < kIlp; ++u) {
-                r[u] = col[pos[u]] - Q[u];
-                const uint32_t c = p.L - pos[u];
-                w[u][(j - 1) / 4] |= c << (8 * ((j - 1) % 4));
-                at[u] = c + 1;
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < kIlp; ++u) {
-            const uint64_t i = base + u * stride;
-            if (i < p.n_i) {
-                if (S == 1) w[u][0] = 1u;
-                if (!ok[u]) {
-#pragma unroll
-                    for (int k = 0; k < NW; ++k) w[u][k] = 0u;
-                }
-#pragma unroll
-                for (int k = 0; k < NW; ++k) p.codes[(uint64_t)k * p.ccap + i] = w[u][k];
-            }
-        }
-    }
+    if (p.L > 128) decode_all<S, R, 8>(p, binom, bad);
+    else if (p.L > 64) decode_all<S, R, 7>(p, binom, bad);
+    else if (p.L > 32) decode_all<S, R, 6>(p, binom, bad);
+    else decode_all<S, R, 5>(p, binom, bad);
     if (bad) atomicOr(p.err, 1u);
 }
 
@@ -594,7 +616,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(KParams p) {
 template <int S, typename R>
 __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Lds<R> tab = stage_tables<R>(p, smem);
+    const Lds<R> tab = stage_tables<R, false>(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     unsigned long long best = ~0ull;
@@ -655,7 +677,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
 template <int S, typename R>
 __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Lds<R> tab = stage_tables<R>(p, smem);
+    const Lds<R> tab = stage_tables<R, false>(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     const uint32_t nit = p.M - S;
@@ -708,7 +730,7 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
     __shared__ uint16_t surv[kTile];
     __shared__ unsigned int nsurv;
     __shared__ unsigned int cnt_pruned, cnt_infeas, cnt_bad;
-    const Lds<R> tab = stage_tables<R>(p, smem);
+    const Lds<R> tab = stage_tables<R, true>(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     if (threadIdx.x == 0) { nsurv = 0; cnt_pruned = 0; cnt_infeas = 0; cnt_bad = 0; }
     // bound in force: min(caller's bound, best of earlier chunks)
@@ -726,7 +748,7 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
         uint32_t a;
         const bool ok = candidate<R>(p, active ? i : 0, r, a);
         uint32_t cut[S + 1], ty[S], F[S], B[S];
-        decode_cuts<S, R>(r, tab.binom, p.L, p.NB, cut);
+        decode_cuts<S, R>(r, tab.binom, p.L, cut);
         decode_types<S>(p, a, ty);
         const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B);
         bool keep = false;
@@ -758,7 +780,7 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
         uint32_t a;
         candidate<R>(p, i, r, a);
         uint32_t cut[S + 1], ty[S], F[S], B[S];
-        decode_cuts<S, R>(r, tab.binom, p.L, p.NB, cut);
+        decode_cuts<S, R>(r, tab.binom, p.L, cut);
         decode_types<S>(p, a, ty);
         stage_weights<S, R>(p, tab, cut, ty, F, B);
         const uint32_t T = makespan<S>(p, F, B, comm);
@@ -805,7 +827,7 @@ static hipError_t launch_eval_s(const KParams &p, const LaunchCfg &lc, hipStream
 
 template <int S, typename R>
 static hipError_t launch_decode_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
-    const size_t lds = (size_t)p.S * p.NB * sizeof(R);
+    const size_t lds = (size_t)p.S * kNB * sizeof(R);
     hipLaunchKernelGGL((decode_kernel<S, R>), dim3(lc.grid), dim3(kBlock), lds, st, p);
     return hipGetLastError();
 }
@@ -820,7 +842,8 @@ template <int S, typename R>
 static hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
                                    uint32_t bound) {
     const uint64_t grid = (hi - lo + kTile - 1) / kTile;
-    hipLaunchKernelGGL((bounded_kernel<S, R>), dim3((uint32_t)grid), dim3(kBlock), lc.lds_bytes, st, p, lo, hi, bound);
+    hipLaunchKernelGGL((bounded_kernel<S, R>), dim3((uint32_t)grid), dim3(kBlock), lc.lds_bounded, st, p, lo, hi,
+                       bound);
     return hipGetLastError();
 }
 
