@@ -23,8 +23,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_INT32_TOPS = 256 * 64 * 2.4e9 / 1e12   # CUs x lanes x clock: one 32-bit op per lane per cycle
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_06086_amd", "csrc", "poseidon_kernels.hip")
-TRAFFIC = os.path.join(ROOT, "profiles", "eval_kernel_traffic_L126_S16_M128.json")
+N_SIMD, PEAK_CLOCK = 256 * 4, 2.4e9
+CSRC = os.path.join(ROOT, "paper_2609_06086_amd", "csrc")
+COUNTERS = os.path.join(ROOT, "profiles", "eval_pipeline_counters_L126_S16_M128.json")
 
 
 def dp_ops(S, M):
@@ -35,21 +36,22 @@ def dp_ops(S, M):
 
 
 def kernel_sha():
+    """Hash of the device and launch code the counters depend on."""
     h = hashlib.sha256()
-    for f in (KERNEL_SRC, os.path.join(ROOT, "paper_2609_06086_amd", "csrc", "poseidon_internal.h")):
-        h.update(open(f, "rb").read())
+    for f in ("poseidon_kernels.hip", "poseidon_internal.h", "poseidon_host.cpp"):
+        h.update(open(os.path.join(CSRC, f), "rb").read())
     return h.hexdigest()
 
 
-def traffic_per_launch():
-    """HBM bytes per launch from the committed rocprofv3 counter summary,
-    or None if the kernel source changed since it was taken."""
-    if not os.path.exists(TRAFFIC):
+def committed_counters():
+    """Per-call HBM bytes and VALU instructions from the committed rocprofv3
+    counter summary, or None if the code changed since it was taken."""
+    if not os.path.exists(COUNTERS):
         return None
-    t = json.load(open(TRAFFIC))
-    if t.get("kernel_source_sha256") != kernel_sha():
+    t = json.load(open(COUNTERS))
+    if t.get("source_sha256") != kernel_sha():
         return None
-    return t.get("bytes_per_launch")
+    return t
 
 
 def cpu_baseline(wl, target_s):
@@ -140,6 +142,7 @@ def main():
     S, M = prob.S, prob.M
     ops = n * dp_ops(S, M)
     achieved = ops / (k_avg * 1e-3) / 1e12
+    ctr = committed_counters() if args.workload == 5 else None
     nodes_per_s = n * 2 * S * M / (ms_per_step * 1e-3)
     value = n / (ms_per_step * 1e-3)
     algo_bytes = n * in_bytes + n * 4 + ((n + 31) // 32) * 4
@@ -186,9 +189,15 @@ def main():
         "int32_valu_frac": achieved / PEAK_INT32_TOPS,
         "best": {"index": best.index, "makespan_us": best.makespan},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_INT32_TOPS, "unit": "Top/s",
-                     "frac": achieved / PEAK_INT32_TOPS, "traffic": traffic_per_launch(),
+                     "frac": achieved / PEAK_INT32_TOPS,
+                     "traffic": None if ctr is None else ctr["hbm_bytes_per_call"],
                      "kernel_ms": k_avg, "algorithmic_ops_per_launch": ops,
-                     "algorithmic_bytes_per_launch": algo_bytes},
+                     "algorithmic_bytes_per_launch": algo_bytes,
+                     "launch": "one poseidon_eval_candidates call: decode, eval and resume kernels",
+                     # hardware side: VALU wave-instructions the call issues (counters) x 4 cycles
+                     # over all SIMD cycles at peak clock during the measured call time
+                     "valu_issue_frac": None if ctr is None else
+                     ctr["valu_wave_insts_per_call"] * 4 / (N_SIMD * PEAK_CLOCK * k_avg * 1e-3)},
         "early_stop": es,
     }
     if not args.no_cpu_baseline:

@@ -23,7 +23,7 @@
 namespace {
 
 // device state words of a context (one u64 each)
-enum { W_ACC = 0, W_RESULT, W_RUN, W_STAT_EVAL, W_STAT_PRUNED, W_STAT_INFEAS, W_ERR, W_DONE, W_COUNT };
+enum { W_ACC = 0, W_RESULT, W_RUN, W_STAT_EVAL, W_STAT_PRUNED, W_STAT_INFEAS, W_ERR, W_DONE, W_SNAP, W_COUNT };
 
 uint64_t binom_sat(uint64_t n, uint64_t k) {
     // exact C(n, k) for small k, saturating at UINT64_MAX
@@ -163,7 +163,7 @@ struct poseidon_ctx {
     pk::KParams base;      // table pointers and problem constants
     void *dmem;
     unsigned long long *state;
-    size_t lds_bytes, lds_bounded;
+    size_t lds_bytes;
     uint32_t grid_max;
     void *ws;              // cut codes + straggler queues of the steady-state cascade
     uint64_t ws_cap;       // candidates per chunk the workspace holds
@@ -321,7 +321,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         if (hipMalloc(&d, total) != hipSuccess) { status = POSEIDON_E_NOMEM; break; }
         unsigned char *b = (unsigned char *)d;
         std::vector<unsigned long long> st(W_COUNT, 0);
-        st[W_ACC] = ~0ull; st[W_RESULT] = ~0ull; st[W_RUN] = ~0ull;
+        st[W_ACC] = ~0ull; st[W_RESULT] = ~0ull; st[W_RUN] = ~0ull; st[W_SNAP] = ~0ull;
         bool ok = hipMemcpy(b + o_state, st.data(), W_COUNT * 8, hipMemcpyHostToDevice) == hipSuccess &&
                   hipMemcpy(b + o_cost, cost.data(), cost.size() * 8, hipMemcpyHostToDevice) == hipSuccess &&
                   hipMemcpy(b + o_pm, pm.data(), pm.size() * 4, hipMemcpyHostToDevice) == hipSuccess &&
@@ -343,12 +343,12 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         kp.acc = ctx->state + W_ACC;
         kp.result = ctx->state + W_RESULT;
         kp.run_best = ctx->state + W_RUN;
+        kp.snap = ctx->state + W_SNAP;
         kp.stats = ctx->state + W_STAT_EVAL;
         kp.err = (unsigned int *)(ctx->state + W_ERR);
         kp.done = (unsigned int *)(ctx->state + W_DONE);
         const size_t lds = ((cost.size() * 8 + pm.size() * 4 + (size_t)T * 4) + 15) & ~(size_t)15;
-        const size_t lds_bounded = lds + binom.size() + 8;
-        if (lds_bounded > 64 * 1024) { status = POSEIDON_E_RANGE; break; }
+        if (lds > 64 * 1024) { status = POSEIDON_E_RANGE; break; }
         int occ = 0;
         hipDeviceProp_t prop;
         if (pk::eval_occupancy(S, wide, lds, &occ) != hipSuccess || hipGetDeviceProperties(&prop, hip_device) != hipSuccess) {
@@ -356,7 +356,6 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
             break;
         }
         ctx->lds_bytes = lds;
-        ctx->lds_bounded = lds_bounded;
         ctx->grid_max = (uint32_t)std::max(1, occ) * (uint32_t)std::max(1, prop.multiProcessorCount);
     } while (0);
     (void)hipSetDevice(prev);
@@ -519,7 +518,6 @@ int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands, uin
         kp.accumulate = c0 > 0;
         pk::LaunchCfg lc;
         lc.lds_bytes = ctx->lds_bytes;
-        lc.lds_bounded = ctx->lds_bounded;
         lc.grid = (uint32_t)std::min<uint64_t>((kp.n_i + 255) / 256, ctx->grid_max);
         // queue segments: block b of every level owns seg_cap slots
         const uint64_t stride = (uint64_t)lc.grid * 256;
@@ -551,8 +549,9 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
     hipStream_t st = (hipStream_t)hip_stream;
     DeviceGuard g(ctx->device);
     if (!g.ok) return POSEIDON_E_DEVICE;
-    // re-arm the running best and the counters (a fill kernel, not a memset)
+    // re-arm the running best, its snapshot and the counters (fill kernels, not memsets)
     if (pk::launch_fill(ctx->state + W_RUN, 1, ~0ull, st) != hipSuccess ||
+        pk::launch_fill(ctx->state + W_SNAP, 1, ~0ull, st) != hipSuccess ||
         pk::launch_fill(ctx->state + W_STAT_EVAL, 3, 0ull, st) != hipSuccess)
         return POSEIDON_E_DEVICE;
     pk::KParams kp = ctx->base;
@@ -560,15 +559,28 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
     kp.count = cands->count;
     kp.comp_rank = cands->comp_rank;
     kp.assign_idx = cands->assign_idx;
-    pk::LaunchCfg lc;
-    lc.lds_bytes = ctx->lds_bytes;
-    lc.lds_bounded = ctx->lds_bounded;
-    lc.grid = 0;
     const uint64_t n = cands->count;
     if (chunk == 0 || chunk > n) chunk = n;
+    // the cut codes of at most kChunk candidates are resident at a time; a
+    // longer chunk is decoded and filtered in pieces that all see the bound
+    // in force at the chunk's start (the snapshot moves only at chunk ends)
+    rc = ensure_workspace(ctx, std::min<uint64_t>(chunk, kChunk), st);
+    if (rc != POSEIDON_OK) return rc;
+    kp.codes = (uint32_t *)ctx->ws;
+    kp.ccap = ctx->ws_cap;
+    pk::LaunchCfg lc;
+    lc.lds_bytes = ctx->lds_bytes;
     for (uint64_t lo = 0; lo < n; lo += chunk) {
         const uint64_t hi = std::min(n, lo + chunk);
-        if (pk::launch_bounded(kp, lc, st, lo, hi, bound) != hipSuccess) return POSEIDON_E_DEVICE;
+        for (uint64_t s0 = lo; s0 < hi; s0 += kChunk) {
+            const uint64_t s1 = std::min(hi, s0 + kChunk);
+            kp.first_i = s0;
+            kp.n_i = s1 - s0;
+            pk::LaunchCfg ld = lc;
+            ld.grid = (uint32_t)std::min<uint64_t>((kp.n_i + 4 * 256 - 1) / (4 * 256), ctx->grid_max);
+            if (pk::launch_decode(kp, ld, st) != hipSuccess) return rearm(ctx, st);
+            if (pk::launch_bounded(kp, lc, st, s0, s1, bound, s1 == hi) != hipSuccess) return rearm(ctx, st);
+        }
     }
     unsigned long long w[W_COUNT];
     if (hipMemcpyAsync(w, ctx->state, sizeof(w), hipMemcpyDeviceToHost, st) != hipSuccess ||

@@ -39,7 +39,8 @@ struct KParams {
     unsigned long long *acc;
     unsigned int *done;
     unsigned long long *result;
-    unsigned long long *run_best;
+    unsigned long long *run_best;     // early stop: best over the chunks so far
+    unsigned long long *snap;         // early stop: run_best as of the previous chunk
     unsigned long long *stats;   // evaluated, pruned, infeasible
     unsigned int *err;
     // steady-state cascade: lanes not settled at iteration lvl_k[l-1] are
@@ -61,15 +62,14 @@ struct KParams {
 
 struct LaunchCfg {
     uint32_t grid;
-    size_t lds_bytes;     // eval / resume kernels: cost, pm, cap
-    size_t lds_bounded;   // early-stop kernel: the same plus the Pascal table
+    size_t lds_bytes;     // eval / resume / early-stop kernels: cost, pm, cap
 };
 
 hipError_t launch_eval(const KParams &p, const LaunchCfg &lc, hipStream_t st);
 hipError_t launch_decode(const KParams &p, const LaunchCfg &lc, hipStream_t st);
 hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl);
 hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
-                          uint32_t bound);
+                          uint32_t bound, uint32_t publish);
 hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, int *blocks);
 hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,
                          unsigned long long *acc, unsigned int *done, unsigned long long *result, hipStream_t st);

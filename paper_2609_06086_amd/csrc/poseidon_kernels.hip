@@ -30,30 +30,20 @@ struct Lds {
     const uint64_t *cost;   // [T][L+1]  (prefix bwd << 32) | prefix fwd
     const uint32_t *pm;     // [L+1]     prefix memory
     const uint32_t *cap;    // [T]
-    const R *binom;         // [S][kNB]  C(n, k), saturated to R's maximum
 };
 
-// Layout: cost (8-byte entries) | pm | cap | binom (early-stop kernel only,
-// placed last and 8-byte aligned).
-template <typename R, bool kBinom>
+// Layout: cost (8-byte entries) | pm | cap.
+template <typename R>
 __device__ __forceinline__ Lds<R> stage_tables(const KParams &p, unsigned char *smem) {
     uint64_t *cost = reinterpret_cast<uint64_t *>(smem);
     const uint32_t ncost = p.T * (p.L + 1);
     uint32_t *pm = reinterpret_cast<uint32_t *>(cost + ncost);
     uint32_t *cap = pm + (p.L + 1);
-    R *binom = nullptr;
     for (uint32_t i = threadIdx.x; i < ncost; i += kBlock) cost[i] = p.cost[i];
     for (uint32_t i = threadIdx.x; i <= p.L; i += kBlock) pm[i] = p.pm[i];
     for (uint32_t i = threadIdx.x; i < p.T; i += kBlock) cap[i] = p.cap[i];
-    if (kBinom) {
-        const uintptr_t end = reinterpret_cast<uintptr_t>(cap + p.T);
-        binom = reinterpret_cast<R *>((end + 7) & ~(uintptr_t)7);
-        const uint32_t nbin = p.S * kNB;
-        const R *gb = reinterpret_cast<const R *>(p.binom);
-        for (uint32_t i = threadIdx.x; i < nbin; i += kBlock) binom[i] = gb[i];
-    }
     __syncthreads();
-    return Lds<R>{cost, pm, cap, binom};
+    return Lds<R>{cost, pm, cap};
 }
 
 // ---------------------------------------------------------------------------
@@ -66,28 +56,6 @@ __device__ __forceinline__ Lds<R> stage_tables(const KParams &p, unsigned char *
 // (hockey-stick identity).  With Q = C(L-a, k+1) - r the cut is c = L - n*,
 // n* the smallest n with C(n, k+1) >= Q, found by a branch-free binary
 // search over column k+1 of the Pascal table; the rank left is C(n*, k+1) - Q.
-template <int S, typename R>
-__device__ __forceinline__ void decode_cuts(R r, const R *binom, uint32_t L, uint32_t (&cut)[S + 1]) {
-    cut[0] = 0;
-    cut[S] = L;
-    uint32_t a = 1;
-#pragma unroll
-    for (int j = 1; j <= S - 1; ++j) {
-        const R *col = binom + (S - j) * kNB;
-        const R Q = col[L - a] - r;
-        // 8 halvings over the 256-entry column: straight-line code
-        uint32_t pos = 0;
-#pragma unroll
-        for (int b = 7; b >= 0; --b) {
-            const uint32_t step = 1u << b;
-            pos += col[pos + step - 1] < Q ? step : 0u;
-        }
-        r = col[pos] - Q;
-        cut[j] = L - pos;
-        a = cut[j] + 1;
-    }
-}
-
 // Cut points in compact form: cut j (1-based) is byte (j-1) % 4 of word
 // (j-1) / 4; a valid composition has c_1 >= 1, so an all-zero first byte
 // marks an invalid candidate (for S = 1 the single byte is 1 when valid).
@@ -438,7 +406,8 @@ __device__ __forceinline__ unsigned long long wave_min(unsigned long long v) {
 __device__ __forceinline__ void block_min_and_finish(unsigned long long v, unsigned long long *acc,
                                                      unsigned int *done, unsigned long long *result,
                                                      unsigned long long *run_best, bool finalize,
-                                                     bool accumulate = false) {
+                                                     bool accumulate = false,
+                                                     unsigned long long *snap = nullptr) {
     __shared__ unsigned long long part[kWaves];
     v = wave_min(v);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -459,7 +428,10 @@ __device__ __forceinline__ void block_min_and_finish(unsigned long long v, unsig
                     if (accumulate) atomicMin(result, k);
                     else atomicExch(result, k);
                 }
-                if (run_best) atomicMin(run_best, k);
+                if (run_best) {
+                    const unsigned long long old = atomicMin(run_best, k);
+                    if (snap) atomicExch(snap, old < k ? old : k);
+                }
                 atomicExch(done, 0u);
             }
         }
@@ -616,7 +588,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(KParams p) {
 template <int S, typename R>
 __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Lds<R> tab = stage_tables<R, false>(p, smem);
+    const Lds<R> tab = stage_tables<R>(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     unsigned long long best = ~0ull;
@@ -677,7 +649,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
 template <int S, typename R>
 __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Lds<R> tab = stage_tables<R, false>(p, smem);
+    const Lds<R> tab = stage_tables<R>(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     const uint32_t nit = p.M - S;
@@ -725,16 +697,17 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
 // of kTile candidates, compacts the survivors in LDS and evaluates them.
 template <int S, typename R>
 __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chunk_lo, uint64_t chunk_hi,
-                                                         uint32_t bound) {
+                                                         uint32_t bound, uint32_t publish) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ uint16_t surv[kTile];
     __shared__ unsigned int nsurv;
     __shared__ unsigned int cnt_pruned, cnt_infeas, cnt_bad;
-    const Lds<R> tab = stage_tables<R, true>(p, smem);
+    const Lds<R> tab = stage_tables<R>(p, smem);
     const Comm<S> comm = load_comm<S>(p);
+    constexpr int NW = Codes<S>::kWords;
     if (threadIdx.x == 0) { nsurv = 0; cnt_pruned = 0; cnt_infeas = 0; cnt_bad = 0; }
-    // bound in force: min(caller's bound, best of earlier chunks)
-    const unsigned long long rb = __hip_atomic_load(p.run_best, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // bound in force: min(caller's bound, best of the chunks before this one)
+    const unsigned long long rb = __hip_atomic_load(p.snap, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t rbT = (uint32_t)(rb >> 32);
     const uint32_t b = rbT < bound ? rbT : bound;
     __syncthreads();
@@ -744,12 +717,11 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
         const uint32_t off = q * kBlock + threadIdx.x;
         const uint64_t i = base + off;
         const bool active = i < chunk_hi;
-        R r;
-        uint32_t a;
-        const bool ok = candidate<R>(p, active ? i : 0, r, a);
-        uint32_t cut[S + 1], ty[S], F[S], B[S];
-        decode_cuts<S, R>(r, tab.binom, p.L, cut);
-        decode_types<S>(p, a, ty);
+        uint32_t w[NW], cut[S + 1], ty[S], F[S], B[S];
+#pragma unroll
+        for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[(uint64_t)k * p.ccap + (i - p.first_i)] : 0u;
+        const bool ok = unpack_cuts<S>(w, p.L, cut);
+        decode_types<S>(p, ok ? assign_of(p, i) : 0u, ty);
         const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B);
         bool keep = false;
         if (active) {
@@ -776,12 +748,11 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
     unsigned long long best = ~0ull;
     for (unsigned int k = threadIdx.x; k < n; k += kBlock) {
         const uint64_t i = base + surv[k];
-        R r;
-        uint32_t a;
-        candidate<R>(p, i, r, a);
-        uint32_t cut[S + 1], ty[S], F[S], B[S];
-        decode_cuts<S, R>(r, tab.binom, p.L, cut);
-        decode_types<S>(p, a, ty);
+        uint32_t w[NW], cut[S + 1], ty[S], F[S], B[S];
+#pragma unroll
+        for (int kk = 0; kk < NW; ++kk) w[kk] = p.codes[(uint64_t)kk * p.ccap + (i - p.first_i)];
+        unpack_cuts<S>(w, p.L, cut);
+        decode_types<S>(p, assign_of(p, i), ty);
         stage_weights<S, R>(p, tab, cut, ty, F, B);
         const uint32_t T = makespan<S>(p, F, B, comm);
         const unsigned long long key = make_key(true, T, (uint32_t)i);
@@ -793,7 +764,7 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
         atomicAdd(&p.stats[2], (unsigned long long)cnt_infeas);
         if (cnt_bad) atomicOr(p.err, 1u);
     }
-    block_min_and_finish(best, p.acc, p.done, nullptr, p.run_best, true);
+    block_min_and_finish(best, p.acc, p.done, nullptr, p.run_best, true, false, publish ? p.snap : nullptr);
 }
 
 // Argmin over stored makespans / feasibility bits.
@@ -840,10 +811,10 @@ static hipError_t launch_resume_s(const KParams &p, const LaunchCfg &lc, hipStre
 
 template <int S, typename R>
 static hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
-                                   uint32_t bound) {
+                                   uint32_t bound, uint32_t publish) {
     const uint64_t grid = (hi - lo + kTile - 1) / kTile;
-    hipLaunchKernelGGL((bounded_kernel<S, R>), dim3((uint32_t)grid), dim3(kBlock), lc.lds_bounded, st, p, lo, hi,
-                       bound);
+    hipLaunchKernelGGL((bounded_kernel<S, R>), dim3((uint32_t)grid), dim3(kBlock), lc.lds_bytes, st, p, lo, hi,
+                       bound, publish);
     return hipGetLastError();
 }
 
@@ -886,8 +857,8 @@ hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, 
 }
 
 hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
-                          uint32_t bound) {
-    PK_DISPATCH(launch_bounded_s, p.S, p.wide, p, lc, st, lo, hi, bound)
+                          uint32_t bound, uint32_t publish) {
+    PK_DISPATCH(launch_bounded_s, p.S, p.wide, p, lc, st, lo, hi, bound, publish)
 }
 
 hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, int *blocks) {

@@ -381,3 +381,29 @@ def test_full_workload4_bounded_matches_golden(dev):
         # Theorem 1: the early-stop pass finds the exhaustive argmin
         assert (b.index, b.makespan) == (g["best_index"], g["best_makespan"])
     ctx.close()
+
+
+def test_call_longer_than_one_chunk(dev):
+    """2^26 + 5,000 candidates: the library works in chunks of 2^26, so the
+    argmin is folded across chunks and the early-stop pass decodes in pieces."""
+    g = _golden()["cfg4"]
+    wl = W.workload(4)
+    rng = np.random.default_rng(108)
+    extra = W.random_candidates(rng, wl.problem, 5000)
+    c = W.Candidates(comp_rank=np.concatenate([wl.cands.comp_rank, extra.comp_rank]),
+                     assign_idx=np.concatenate([wl.cands.assign_idx, extra.assign_idx]))
+    n0 = len(wl.cands)
+    Te, fe = coracle.evaluate(wl.problem, extra)
+    ctx = P.poseidon_load_costs(wl.problem, 0)
+    Tg, fg, best = gpu_eval(ctx, c, dev)
+    assert np.array_equal(Tg[n0:], Te) and np.array_equal(fg[n0:], fe)
+    assert hashlib.sha256(Tg[:n0].astype("<u4").tobytes()).hexdigest() == g["makespan_sha256"]
+    be = coracle.argmin(Te, fe)
+    exp = min((g["best_makespan"], g["best_index"]), (be[1], be[0] + n0))
+    assert (best.makespan, best.index) == exp
+    d = to_dev(c, dev)
+    b, st = P.poseidon_eval_candidates_bounded(ctx, g["warmup_bound"], chunk=0, **d)
+    assert (b.makespan, b.index) == exp
+    assert st.evaluated + st.pruned + st.infeasible == len(c)
+    assert st.infeasible == (g["n"] - g["n_feasible"]) + int((~fe).sum())
+    ctx.close()
