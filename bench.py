@@ -38,8 +38,10 @@ def dp_ops(S, M):
 def kernel_sha():
     """Hash of the device and launch code the counters depend on."""
     h = hashlib.sha256()
-    for f in ("poseidon_kernels.hip", "poseidon_internal.h", "poseidon_host.cpp"):
-        h.update(open(os.path.join(CSRC, f), "rb").read())
+    for f in sorted(os.listdir(CSRC)):
+        if f.endswith((".hip", ".h", ".cpp")):
+            h.update(f.encode())
+            h.update(open(os.path.join(CSRC, f), "rb").read())
     return h.hexdigest()
 
 
@@ -77,7 +79,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=5, choices=[3, 4, 5])
+    ap.add_argument("--workload", type=int, default=5, choices=[3, 4, 5, 6])
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-early-stop", action="store_true")

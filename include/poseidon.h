@@ -79,6 +79,10 @@ typedef struct {
     const uint32_t *cap_mb;       /* [T] memory of one device of type t */
     const uint8_t *assign;        /* [A][S] allowed stage->type rows, or NULL = all T^S */
     uint64_t A;                   /* rows of `assign` (ignored when assign == NULL) */
+    const uint32_t *allreduce_us; /* [T][L] data-parallel gradient all-reduce time of layer l on
+                                     type t, or NULL = none.  Stage s's all-reduce node R_s
+                                     weighs the sum over its layers and follows B_{s,M};
+                                     T = max_s(finish(B_{s,M}) + R_s) (Sec. 4.1.1, 4.1.3) */
 } poseidon_problem;
 
 /* Candidates of one call.  comp_rank == NULL: range mode over joint indices

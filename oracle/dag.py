@@ -281,7 +281,10 @@ def candidate_list(prob, cands):
 
 
 def evaluate(prob, cands, allreduce=None):
-    """Makespan of every candidate and its feasibility (uint32 / bool arrays)."""
+    """Makespan of every candidate and its feasibility (uint32 / bool arrays).
+    The all-reduce table defaults to the problem's own (``prob.allreduce``)."""
+    if allreduce is None:
+        allreduce = getattr(prob, "allreduce", None)
     dag = dag_for(prob.S, prob.M)
     lst = candidate_list(prob, cands)
     T = np.zeros(len(lst), dtype=np.int64)
@@ -330,6 +333,7 @@ def bounded_search(prob, cands, bound: int, chunk: int = 0):
     every other feasible one is evaluated exactly.  The result is the
     (makespan, index)-smallest evaluated candidate if its makespan is
     <= bound, else None.  Returns (best, evaluated, pruned, infeasible)."""
+    allreduce = getattr(prob, "allreduce", None)
     dag = dag_for(prob.S, prob.M)
     lst = candidate_list(prob, cands)
     n = len(lst)
@@ -339,15 +343,16 @@ def bounded_search(prob, cands, bound: int, chunk: int = 0):
     for c0 in range(0, n, chunk):
         b = bound if best is None else min(bound, best[1])
         for i, cuts, types in lst[c0:c0 + chunk]:
-            F, B, _, _, ok = stage_weights(prob, cuts, types)
+            F, B, _, D, ok = stage_weights(prob, cuts, types, allreduce)
+            d = D if allreduce is not None else None
             if not ok:
                 infeasible += 1
                 continue
-            if eq2_bound(F, B, prob.M) > b:
+            if eq2_bound(F, B, prob.M, d) > b:
                 pruned += 1
                 continue
             evaluated += 1
-            t = longest_path(dag, F, B, prob.comm_fwd, prob.comm_bwd)
+            t = longest_path(dag, F, B, prob.comm_fwd, prob.comm_bwd, d)
             if best is None or (t, i) < best[::-1]:
                 best = (i, t)
     if best is not None and best[1] > bound:

@@ -21,9 +21,11 @@ from typing import Sequence
 
 
 def simulate_1f1b(S: int, M: int, F: Sequence[int], B: Sequence[int],
-                  cf: Sequence[int], cb: Sequence[int], order) -> int:
+                  cf: Sequence[int], cb: Sequence[int], order, allreduce=None) -> int:
     """Iteration time of the event-driven run; `order(S, M, s)` gives stage
-    s's task list as ('F'|'B', m) pairs."""
+    s's task list as ('F'|'B', m) pairs.  With `allreduce`, stage s starts
+    its gradient all-reduce (allreduce[s-1] long) once its task list is done,
+    and the iteration ends when the last all-reduce ends."""
     tasks = {s: order(S, M, s) for s in range(1, S + 1)}
     nxt = {s: 0 for s in tasks}
     busy_until = {s: 0 for s in tasks}
@@ -73,6 +75,8 @@ def simulate_1f1b(S: int, M: int, F: Sequence[int], B: Sequence[int],
             try_start(payload[1], now)
     if any(nxt[s] != len(tasks[s]) for s in tasks):
         raise RuntimeError("pipeline deadlocked")
+    if allreduce is not None:
+        return max(busy_until[s] + int(allreduce[s - 1]) for s in tasks)
     return max(busy_until.values()) if busy_until else end
 
 

@@ -7,8 +7,8 @@
  * written out plainly so that large workloads can be checked on the host.
  *
  *  - DAG (Poseidon, Sec. 4.1.1-4.1.2): compute nodes F_{s,m}, B_{s,m}; one
- *    all-reduce node R_s per stage (weight 0: one pipeline, no DP traffic);
- *    start node and end node.  Inter-stage edges F_{s,m}->F_{s+1,m} and
+ *    all-reduce node R_s per stage (Sec. 4.1.3: per-layer all-reduce time
+ *    summed over the stage, or 0 without a table); start node and end node.  Inter-stage edges F_{s,m}->F_{s+1,m} and
  *    B_{s+1,m}->B_{s,m}; intra-stage edges along each stage's 1F1B order;
  *    B_{s,M}->R_s; start->F_{1,1}; R_s->end.  The topology depends only on
  *    (S, M) and is built once (Sec. 5, simulator design), then ordered with
@@ -27,7 +27,8 @@
  *    Pascal table), assignment row or base-T digits (stage 1 most
  *    significant); range mode index = rank * A + a.
  *  - Early stop (Eq. 2, Theorem 1): g(S_x) = sum_{i<x} F_i + M (F_x + B_x)
- *    + max_{1<=i<=x} sum_{j=i}^{x-1} B_j (d_i = 0); prune iff max_x g > b.
+ *    + max_{1<=i<=x} (sum_{j=i}^{x-1} B_j + d_i), d_i = stage all-reduce
+ *    time; prune iff max_x g > b.
  *
  * Finish times are held in 64-bit integers, so no intermediate can wrap.
  */
@@ -44,6 +45,7 @@ typedef struct {
     const uint32_t *cap;           /* [T] */
     const uint8_t *assign;         /* [A][S] or NULL (all T^S rows) */
     uint64_t A;
+    const uint32_t *allreduce;     /* [T][L] or NULL (no DP all-reduce) */
 } oc_problem;
 
 enum { K_F = 0, K_B = 1, K_R = 2, K_START = 3, K_END = 4 };
@@ -178,7 +180,7 @@ static oc_dag *dag_build(int S, int M) {
 }
 
 /* finish times: caller-provided scratch of g->n uint64 */
-static uint64_t dag_longest(const oc_dag *g, const uint64_t *F, const uint64_t *B,
+static uint64_t dag_longest(const oc_dag *g, const uint64_t *F, const uint64_t *B, const uint64_t *D,
                             const uint32_t *cf, const uint32_t *cb, uint64_t *fin) {
     for (int i = 0; i < g->n; ++i) {
         int v = g->topo[i];
@@ -196,6 +198,7 @@ static uint64_t dag_longest(const oc_dag *g, const uint64_t *F, const uint64_t *
         }
         if (nv->kind == K_F) w = F[nv->stage - 1];
         else if (nv->kind == K_B) w = B[nv->stage - 1];
+        else if (nv->kind == K_R) w = D[nv->stage - 1];
         fin[v] = w + best;
     }
     return fin[g->end];
@@ -279,7 +282,7 @@ static void *worker(void *arg) {
     const oc_problem *p = j->p;
     int S = (int)p->S;
     int cuts[65], types[64];
-    uint64_t F[64], B[64];
+    uint64_t F[64], B[64], D[64];
     uint64_t *fin = malloc(sizeof(uint64_t) * (size_t)j->g->n);
     if (!fin) { j->err = -3; return NULL; }
     j->best_key_T = UINT64_MAX; j->best_idx = UINT64_MAX;
@@ -287,13 +290,14 @@ static void *worker(void *arg) {
         if (decode(j, i, cuts, types)) { j->err = -1; break; }
         int feasible = 1;
         for (int s = 0; s < S; ++s) {
-            uint64_t f = 0, b = 0, mm = 0;
+            uint64_t f = 0, b = 0, mm = 0, d = 0;
             for (int l = cuts[s]; l < cuts[s + 1]; ++l) {
                 f += p->fwd[(size_t)types[s] * p->L + l];
                 b += p->bwd[(size_t)types[s] * p->L + l];
                 mm += p->mem[l];
+                if (p->allreduce) d += p->allreduce[(size_t)types[s] * p->L + l];
             }
-            F[s] = f; B[s] = b;
+            F[s] = f; B[s] = b; D[s] = d;
             if (mm > p->cap[types[s]]) feasible = 0;
         }
         if (j->bounded) {
@@ -304,7 +308,7 @@ static void *worker(void *arg) {
                 for (int i2 = 1; i2 < x; ++i2) g += F[i2 - 1];
                 g += (uint64_t)p->M * (F[x - 1] + B[x - 1]);
                 for (int i2 = 1; i2 <= x; ++i2) {
-                    uint64_t sb = 0;
+                    uint64_t sb = D[i2 - 1];
                     for (int jj = i2; jj <= x - 1; ++jj) sb += B[jj - 1];
                     if (sb > inner) inner = sb;
                 }
@@ -313,7 +317,7 @@ static void *worker(void *arg) {
             if (lb > j->bound) { j->pruned++; continue; }
             j->evaluated++;
         }
-        uint64_t T = dag_longest(j->g, F, B, p->cf, p->cb, fin);
+        uint64_t T = dag_longest(j->g, F, B, D, p->cf, p->cb, fin);
         if (T > UINT32_MAX) { j->err = -2; break; }
         if (j->out_T) j->out_T[i] = (uint32_t)T;
         if (j->out_feas) j->out_feas[i] = (uint8_t)feasible;

@@ -1,18 +1,25 @@
-"""Build ``libposeidon.so`` for gfx950 with hipcc (in-tree)."""
+"""Build ``libposeidon.so`` for gfx950 with hipcc (in-tree).
+
+The kernel templates are instantiated in several translation units (split
+by stage count), compiled in parallel and linked into one shared library.
+"""
 from __future__ import annotations
 
+import glob
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRC = [os.path.join(HERE, "csrc", "poseidon_host.cpp"), os.path.join(HERE, "csrc", "poseidon_kernels.hip")]
+CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libposeidon.so")
+OBJ = os.path.join(HERE, "_build")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-Wall", "-Wno-unused-function",
     # no packed FP32 instructions anywhere in the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -20,9 +27,36 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
+def sources():
+    return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
+
+
+def build(verbose: bool = False, jobs: int = 0) -> str:
+    os.makedirs(OBJ, exist_ok=True)
+    srcs = sources()
+    objs = [os.path.join(OBJ, os.path.basename(s) + ".o") for s in srcs]
+
+    def compile_one(pair):
+        src, obj = pair
+        cmd = [HIPCC] + FLAGS + ["-c", src, "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        return src, r
+
+    jobs = jobs or min(len(srcs), max(1, os.cpu_count() or 1), 16)
+    failed = []
+    with ThreadPoolExecutor(max_workers=jobs) as ex:
+        for src, r in ex.map(compile_one, zip(srcs, objs)):
+            err = "\n".join(l for l in r.stderr.splitlines() if "packed-fp32-ops" not in l)
+            if err.strip() and (verbose or r.returncode):
+                print(err, file=sys.stderr, flush=True)
+            if r.returncode:
+                failed.append(src)
+    if failed:
+        raise RuntimeError(f"hipcc failed on {failed}")
     tmp = OUT + ".tmp"
-    cmd = [HIPCC] + FLAGS + SRC + ["-o", tmp]
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC"] + objs + ["-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

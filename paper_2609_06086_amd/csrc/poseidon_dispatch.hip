@@ -1,0 +1,109 @@
+// Launch dispatch over the stage count S and the rank width, plus the
+// non-templated kernels.  The templated kernels are instantiated in
+// poseidon_inst_*.hip, split by S so that they compile in parallel.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "poseidon_kernels.h"
+
+namespace pk {
+
+#define PK_EXTERN(S)                                                                                     \
+    extern template hipError_t launch_eval_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t);    \
+    extern template hipError_t launch_eval_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t);    \
+    extern template hipError_t launch_decode_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t);  \
+    extern template hipError_t launch_decode_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t);  \
+    extern template hipError_t launch_resume_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t,   \
+                                                             uint32_t);                                       \
+    extern template hipError_t launch_resume_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t,   \
+                                                             uint32_t);                                       \
+    extern template hipError_t launch_bounded_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t,  \
+                                                              uint64_t, uint64_t, uint32_t, uint32_t);        \
+    extern template hipError_t launch_bounded_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t,  \
+                                                              uint64_t, uint64_t, uint32_t, uint32_t);        \
+    extern template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool);                                 \
+    extern template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool);
+
+PK_EXTERN(1) PK_EXTERN(2) PK_EXTERN(3) PK_EXTERN(4) PK_EXTERN(5) PK_EXTERN(6) PK_EXTERN(7) PK_EXTERN(8)
+PK_EXTERN(9) PK_EXTERN(10) PK_EXTERN(11) PK_EXTERN(12) PK_EXTERN(13) PK_EXTERN(14) PK_EXTERN(15) PK_EXTERN(16)
+
+// Argmin over stored makespans / feasibility bits.
+__global__ __launch_bounds__(kBlock) void argmin_kernel(const uint32_t *T, const uint32_t *bits, uint64_t count,
+                                                        unsigned long long *acc, unsigned int *done,
+                                                        unsigned long long *result) {
+    unsigned long long best = ~0ull;
+    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < count; i += stride) {
+        const bool f = bits ? ((bits[i >> 5] >> (i & 31)) & 1u) : true;
+        const unsigned long long key = make_key(f, T[i], (uint32_t)i);
+        best = key < best ? key : best;
+    }
+    block_min_and_finish(best, acc, done, result, nullptr, true);
+}
+
+// Small fill kernel used instead of memset so that the calls stay capturable.
+__global__ void fill_u64(unsigned long long *p, uint32_t n, unsigned long long v) {
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+// ---------------------------------------------------------------------------
+
+#define PK_DISPATCH(FN, S_, WIDE_, ...)                                                        \
+    switch (S_) {                                                                              \
+    case 1: return WIDE_ ? FN<1, uint64_t>(__VA_ARGS__) : FN<1, uint32_t>(__VA_ARGS__);       \
+    case 2: return WIDE_ ? FN<2, uint64_t>(__VA_ARGS__) : FN<2, uint32_t>(__VA_ARGS__);       \
+    case 3: return WIDE_ ? FN<3, uint64_t>(__VA_ARGS__) : FN<3, uint32_t>(__VA_ARGS__);       \
+    case 4: return WIDE_ ? FN<4, uint64_t>(__VA_ARGS__) : FN<4, uint32_t>(__VA_ARGS__);       \
+    case 5: return WIDE_ ? FN<5, uint64_t>(__VA_ARGS__) : FN<5, uint32_t>(__VA_ARGS__);       \
+    case 6: return WIDE_ ? FN<6, uint64_t>(__VA_ARGS__) : FN<6, uint32_t>(__VA_ARGS__);       \
+    case 7: return WIDE_ ? FN<7, uint64_t>(__VA_ARGS__) : FN<7, uint32_t>(__VA_ARGS__);       \
+    case 8: return WIDE_ ? FN<8, uint64_t>(__VA_ARGS__) : FN<8, uint32_t>(__VA_ARGS__);       \
+    case 9: return WIDE_ ? FN<9, uint64_t>(__VA_ARGS__) : FN<9, uint32_t>(__VA_ARGS__);       \
+    case 10: return WIDE_ ? FN<10, uint64_t>(__VA_ARGS__) : FN<10, uint32_t>(__VA_ARGS__);    \
+    case 11: return WIDE_ ? FN<11, uint64_t>(__VA_ARGS__) : FN<11, uint32_t>(__VA_ARGS__);    \
+    case 12: return WIDE_ ? FN<12, uint64_t>(__VA_ARGS__) : FN<12, uint32_t>(__VA_ARGS__);    \
+    case 13: return WIDE_ ? FN<13, uint64_t>(__VA_ARGS__) : FN<13, uint32_t>(__VA_ARGS__);    \
+    case 14: return WIDE_ ? FN<14, uint64_t>(__VA_ARGS__) : FN<14, uint32_t>(__VA_ARGS__);    \
+    case 15: return WIDE_ ? FN<15, uint64_t>(__VA_ARGS__) : FN<15, uint32_t>(__VA_ARGS__);    \
+    case 16: return WIDE_ ? FN<16, uint64_t>(__VA_ARGS__) : FN<16, uint32_t>(__VA_ARGS__);    \
+    default: return hipErrorInvalidValue;                                                      \
+    }
+
+hipError_t launch_eval(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
+    PK_DISPATCH(launch_eval_s, p.S, p.wide, p, lc, st)
+}
+
+hipError_t launch_decode(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
+    PK_DISPATCH(launch_decode_s, p.S, p.wide, p, lc, st)
+}
+
+hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl) {
+    PK_DISPATCH(launch_resume_s, p.S, p.wide, p, lc, st, lvl)
+}
+
+hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
+                          uint32_t bound, uint32_t publish) {
+    PK_DISPATCH(launch_bounded_s, p.S, p.wide, p, lc, st, lo, hi, bound, publish)
+}
+
+hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, bool ar, int *blocks) {
+    PK_DISPATCH(occupancy_s, S, wide, blocks, lds, ar)
+}
+
+hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,
+                         unsigned long long *acc, unsigned int *done, unsigned long long *result, hipStream_t st) {
+    hipLaunchKernelGGL(argmin_kernel, dim3(grid), dim3(kBlock), 0, st, T, bits, count, acc, done, result);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, hipStream_t st) {
+    hipLaunchKernelGGL(fill_u64, dim3((n + 63) / 64), dim3(64), 0, st, p, n, v);
+    return hipGetLastError();
+}
+
+int code_words(int S) { return S > 1 ? (S - 1 + 3) / 4 : 1; }
+int prologue_op(int S, int s, int k) { return pro_op(S, s, k); }
+int epilogue_op(int S, int s, int j) { return epi_op(S, s, j); }
+
+}  // namespace pk

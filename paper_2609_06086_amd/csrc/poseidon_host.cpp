@@ -214,6 +214,15 @@ int poseidon_validate(const poseidon_problem *p, uint64_t *n_candidates) {
     }
     for (uint32_t b = 0; b + 1 < p->S; ++b) w += (uint64_t)p->comm_fwd_us[b] + p->comm_bwd_us[b];
     w *= p->M;
+    if (p->allreduce_us) {
+        // the end node adds at most one stage's all-reduce, which is at most
+        // the sum over all layers of the slowest type's all-reduce
+        for (uint32_t l = 0; l < p->L; ++l) {
+            uint64_t mx = 0;
+            for (uint32_t t = 0; t < p->T; ++t) mx = std::max<uint64_t>(mx, p->allreduce_us[(size_t)t * p->L + l]);
+            w += mx;
+        }
+    }
     if (w >= ((unsigned __int128)1 << 31)) return POSEIDON_E_RANGE;
     unsigned __int128 mem = 0;
     for (uint32_t l = 0; l < p->L; ++l) mem += p->mem_mb[l];
@@ -256,6 +265,11 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     }
     std::vector<uint32_t> pm(L + 1, 0);
     for (uint32_t l = 0; l < L; ++l) pm[l + 1] = pm[l] + p->mem_mb[l];
+    const bool has_ar = p->allreduce_us != nullptr;
+    std::vector<uint32_t> pd(has_ar ? (size_t)T * (L + 1) : 0, 0);
+    for (uint32_t t = 0; has_ar && t < T; ++t)
+        for (uint32_t l = 0; l < L; ++l)
+            pd[(size_t)t * (L + 1) + l + 1] = pd[(size_t)t * (L + 1) + l] + p->allreduce_us[(size_t)t * L + l];
     const size_t rsz = wide ? 8 : 4;
     std::vector<unsigned char> binom((size_t)S * NB * rsz);
     for (uint32_t k = 0; k < S; ++k)
@@ -275,6 +289,8 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     kp.L = L; kp.S = S; kp.M = M; kp.T = T; kp.NB = NB;
     kp.wide = wide;
     for (uint32_t b = 0; b + 1 < S; ++b) { kp.cf[b] = p->comm_fwd_us[b]; kp.cb[b] = p->comm_bwd_us[b]; }
+    kp.has_ar = has_ar;
+    for (uint32_t s = 1; s < S; ++s) kp.psi[s] = kp.psi[s - 1] + kp.cf[s - 1];
     // cascade checkpoints of the steady loop: K0, 2 K0, 4 K0, ... below M - S
     if (M >= S) {
         const uint32_t nit = M - S;
@@ -305,6 +321,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     const size_t o_binom = off; off = al(off + binom.size());
     const size_t o_assign = off; off = al(off + (has_table ? (size_t)A * S : 0));
     const size_t o_slots = off; off = al(off + (table_path ? masks.size() * 4 : 0));
+    const size_t o_pd = off; off = al(off + pd.size() * 4);
     const size_t total = off;
 
     poseidon_ctx *ctx = new (std::nothrow) poseidon_ctx;
@@ -331,6 +348,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
             ok = hipMemcpy(b + o_assign, p->assign, (size_t)A * S, hipMemcpyHostToDevice) == hipSuccess;
         if (ok && table_path)
             ok = hipMemcpy(b + o_slots, masks.data(), masks.size() * 4, hipMemcpyHostToDevice) == hipSuccess;
+        if (ok && has_ar) ok = hipMemcpy(b + o_pd, pd.data(), pd.size() * 4, hipMemcpyHostToDevice) == hipSuccess;
         if (!ok) { status = POSEIDON_E_DEVICE; break; }
         kp.cost = (const uint64_t *)(b + o_cost);
         kp.pm = (const uint32_t *)(b + o_pm);
@@ -338,6 +356,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         kp.binom = b + o_binom;
         kp.assign = has_table ? (const uint8_t *)(b + o_assign) : nullptr;
         kp.slot_mask = table_path ? (const uint32_t *)(b + o_slots) : nullptr;
+        kp.pd = has_ar ? (const uint32_t *)(b + o_pd) : nullptr;
         kp.nslots = table_path ? nslots : 0;
         ctx->state = (unsigned long long *)(b + o_state);
         kp.acc = ctx->state + W_ACC;
@@ -347,11 +366,11 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         kp.stats = ctx->state + W_STAT_EVAL;
         kp.err = (unsigned int *)(ctx->state + W_ERR);
         kp.done = (unsigned int *)(ctx->state + W_DONE);
-        const size_t lds = ((cost.size() * 8 + pm.size() * 4 + (size_t)T * 4) + 15) & ~(size_t)15;
+        const size_t lds = ((cost.size() * 8 + pm.size() * 4 + (size_t)T * 4 + pd.size() * 4) + 15) & ~(size_t)15;
         if (lds > 64 * 1024) { status = POSEIDON_E_RANGE; break; }
         int occ = 0;
         hipDeviceProp_t prop;
-        if (pk::eval_occupancy(S, wide, lds, &occ) != hipSuccess || hipGetDeviceProperties(&prop, hip_device) != hipSuccess) {
+        if (pk::eval_occupancy(S, wide, lds, has_ar, &occ) != hipSuccess || hipGetDeviceProperties(&prop, hip_device) != hipSuccess) {
             status = POSEIDON_E_DEVICE;
             break;
         }

@@ -1,0 +1,23 @@
+// Kernel instantiations for stage counts 9, 10, 11, 12 (split so that the library
+// compiles in parallel).
+#include "poseidon_kernels.h"
+
+namespace pk {
+
+#define PK_INST(S)                                                                                        \
+    template hipError_t launch_eval_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t);           \
+    template hipError_t launch_eval_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t);           \
+    template hipError_t launch_decode_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t);         \
+    template hipError_t launch_decode_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t);         \
+    template hipError_t launch_resume_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t, uint32_t); \
+    template hipError_t launch_resume_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t, uint32_t); \
+    template hipError_t launch_bounded_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t, uint64_t, \
+                                                       uint64_t, uint32_t, uint32_t);                          \
+    template hipError_t launch_bounded_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t, uint64_t, \
+                                                       uint64_t, uint32_t, uint32_t);                          \
+    template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool);                                        \
+    template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool);
+
+PK_INST(9) PK_INST(10) PK_INST(11) PK_INST(12)
+
+}  // namespace pk

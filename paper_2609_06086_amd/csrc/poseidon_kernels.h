@@ -1,4 +1,5 @@
-// Device code for batched evaluation of Poseidon's 1F1B-DAG training-time
+#pragma once
+// Device code (templates) for batched evaluation of Poseidon's 1F1B-DAG training-time
 // model on gfx950 (CDNA4), one candidate configuration per lane.
 //
 // Per lane the path is:
@@ -30,9 +31,10 @@ struct Lds {
     const uint64_t *cost;   // [T][L+1]  (prefix bwd << 32) | prefix fwd
     const uint32_t *pm;     // [L+1]     prefix memory
     const uint32_t *cap;    // [T]
+    const uint32_t *pd;     // [T][L+1]  prefix all-reduce time (when the problem has one)
 };
 
-// Layout: cost (8-byte entries) | pm | cap.
+// Layout: cost (8-byte entries) | pm | cap | pd.
 template <typename R>
 __device__ __forceinline__ Lds<R> stage_tables(const KParams &p, unsigned char *smem) {
     uint64_t *cost = reinterpret_cast<uint64_t *>(smem);
@@ -42,8 +44,11 @@ __device__ __forceinline__ Lds<R> stage_tables(const KParams &p, unsigned char *
     for (uint32_t i = threadIdx.x; i < ncost; i += kBlock) cost[i] = p.cost[i];
     for (uint32_t i = threadIdx.x; i <= p.L; i += kBlock) pm[i] = p.pm[i];
     for (uint32_t i = threadIdx.x; i < p.T; i += kBlock) cap[i] = p.cap[i];
+    uint32_t *pd = cap + p.T;
+    if (p.has_ar)
+        for (uint32_t i = threadIdx.x; i < ncost; i += kBlock) pd[i] = p.pd[i];
     __syncthreads();
-    return Lds<R>{cost, pm, cap};
+    return Lds<R>{cost, pm, cap, pd};
 }
 
 // ---------------------------------------------------------------------------
@@ -267,10 +272,11 @@ __device__ __forceinline__ void dp_iter(uint32_t (&Y)[S], const uint32_t (&F)[S]
     steady_slot<S>(0, Y, F, B, c);
 }
 
-// the last steady slot (2M-1) and the epilogue; returns T
+// the last steady slot (2M-1) and the epilogue; afterwards Y[s] holds the
+// (shifted) finish of B_{s,M}, the last node of every stage
 template <int S>
-__device__ __forceinline__ uint32_t dp_finish(uint32_t (&Y)[S], const uint32_t (&F)[S], const uint32_t (&B)[S],
-                                              const Comm<S> &c) {
+__device__ __forceinline__ void dp_finish(uint32_t (&Y)[S], const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                          const Comm<S> &c) {
     steady_slot<S>(1, Y, F, B, c);
 #pragma unroll
     for (int j = 0; j < 2 * S - 2; ++j) {
@@ -280,16 +286,14 @@ __device__ __forceinline__ uint32_t dp_finish(uint32_t (&Y)[S], const uint32_t (
 #pragma unroll
         for (int s = 0; s < S; ++s) Y[s] = N[s];
     }
-    return Y[0] - c.phi0;
 }
 
 template <int S>
-__device__ __forceinline__ uint32_t dp_1f1b(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S],
-                                            const Comm<S> &c) {
-    uint32_t Y[S];
+__device__ __forceinline__ void dp_1f1b(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                        const Comm<S> &c, uint32_t (&Y)[S]) {
     dp_prologue<S>(Y, F, B, c);
     for (uint32_t it = S; it < M; ++it) dp_iter<S>(Y, F, B, c);
-    return dp_finish<S>(Y, F, B, c);
+    dp_finish<S>(Y, F, B, c);
 }
 
 // The steady iteration is one fixed map Y -> A(Y) built from max and +
@@ -333,9 +337,8 @@ __device__ __forceinline__ bool dp_advance(uint32_t (&Y)[S], const uint32_t (&F)
 // Any M (used when M < S): the slot schedule comes from a table of
 // per-slot forward / backward stage masks built on the host.
 template <int S>
-__device__ __forceinline__ uint32_t dp_table(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
-                                             const Comm<S> &c) {
-    uint32_t Y[S];
+__device__ __forceinline__ void dp_table(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                         const Comm<S> &c, uint32_t (&Y)[S]) {
     dp_init<S>(Y, c);
     for (uint32_t k = 0; k < p.nslots; ++k) {
         const uint32_t fm = p.slot_mask[2 * k], bm = p.slot_mask[2 * k + 1];
@@ -348,14 +351,14 @@ __device__ __forceinline__ uint32_t dp_table(const KParams &p, const uint32_t (&
 #pragma unroll
         for (int s = 0; s < S; ++s) Y[s] = N[s];
     }
-    return Y[0] - c.phi0;
 }
 
+// registers after the whole DP (any M)
 template <int S>
-__device__ __forceinline__ uint32_t makespan(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
-                                             const Comm<S> &c) {
-    if (p.M >= (uint32_t)S) return dp_1f1b<S>(p.M, F, B, c);
-    return dp_table<S>(p, F, B, c);
+__device__ __forceinline__ void dp_full(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                        const Comm<S> &c, uint32_t (&Y)[S]) {
+    if (p.M >= (uint32_t)S) dp_1f1b<S>(p.M, F, B, c, Y);
+    else dp_table<S>(p, F, B, c, Y);
 }
 
 template <int S>
@@ -372,18 +375,50 @@ __device__ __forceinline__ Comm<S> load_comm(const KParams &p) {
 }
 
 // ---------------------------------------------------------------------------
-// (a5) Eq. 2 lower bound with d_i = 0: g(S_x) = sum_{i<x}(F_i + B_i) + M (F_x + B_x)
+// (a5) Eq. 2: g(S_x) = sum_{i<x} F_i + M (F_x + B_x) + max_{i<=x}(sum_{j=i}^{x-1} B_j + d_i)
 // ---------------------------------------------------------------------------
 template <int S>
-__device__ __forceinline__ uint32_t eq2_bound(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S]) {
-    uint32_t pre = 0, lb = 0;
+__device__ __forceinline__ uint32_t eq2_bound(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                              const uint32_t (&D)[S]) {
+    uint32_t pre = 0, inner = 0, lb = 0;
 #pragma unroll
     for (int x = 0; x < S; ++x) {
-        const uint32_t fb = F[x] + B[x];
-        lb = max(lb, pre + M * fb);
-        pre += fb;
+        // inner = max over i <= x of (B_i + ... + B_{x-1} + d_i)
+        inner = x == 0 ? D[0] : max(inner + B[x - 1], D[x]);
+        lb = max(lb, pre + M * (F[x] + B[x]) + inner);
+        pre += F[x];
     }
     return lb;
+}
+
+// ---------------------------------------------------------------------------
+// end of the iteration: the end node E follows every R_s (Sec. 4.1.1), and
+// R_s follows B_{s,M} with the stage's summed per-layer all-reduce time
+// (Sec. 4.1.3).  Without all-reduce times T = finish(B_{1,M}).
+// ---------------------------------------------------------------------------
+template <int S, typename R>
+__device__ __forceinline__ void stage_allreduce(const KParams &p, const Lds<R> &t, const uint32_t (&cut)[S + 1],
+                                                const uint32_t (&ty)[S], uint32_t (&D)[S]) {
+    const uint32_t row = p.L + 1;
+#pragma unroll
+    for (int s = 0; s < S; ++s) D[s] = t.pd[ty[s] * row + cut[s + 1]] - t.pd[ty[s] * row + cut[s]];
+}
+
+// T from the registers after the epilogue; with all-reduce times the
+// stage's cut codes `w` and assignment `a` give R_s
+template <int S, typename R, bool AR>
+__device__ __forceinline__ uint32_t end_time(const KParams &p, const Lds<R> &t, const uint32_t (&Y)[S],
+                                             const Comm<S> &c, const uint32_t (&w)[Codes<S>::kWords], uint32_t a) {
+    if (!AR) return Y[0] - c.phi0;
+    uint32_t cut[S + 1], ty[S], D[S];
+    unpack_cuts<S>(w, p.L, cut);
+    decode_types<S>(p, a, ty);
+    stage_allreduce<S, R>(p, t, cut, ty, D);
+    // Y[s] - phi_s = finish(B_{s,M}); phi_0 - phi_s = psi_s
+    uint32_t e = 0;
+#pragma unroll
+    for (int s = 0; s < S; ++s) e = max(e, Y[s] + p.psi[s] + D[s]);
+    return e - c.phi0;
 }
 
 // ---------------------------------------------------------------------------
@@ -585,7 +620,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(KParams p) {
 // check, the DP and the reduction.  With a cascade (p.nlevels > 0) a lane
 // whose steady state has not settled by iteration p.lvl_k[0] is queued for
 // resume_kernel instead of finishing here.
-template <int S, typename R>
+template <int S, typename R, bool AR>
 __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
     const Lds<R> tab = stage_tables<R>(p, smem);
@@ -606,22 +641,22 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
         uint32_t w[NW];
 #pragma unroll
         for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[(uint64_t)k * p.ccap + i] : 0u;
-        uint32_t cut[S + 1], ty[S], F[S], B[S];
+        uint32_t cut[S + 1], ty[S], F[S], B[S], Y[S];
         const bool ok = unpack_cuts<S>(w, p.L, cut);
-        decode_types<S>(p, ok ? assign_of(p, gi) : 0u, ty);
+        const uint32_t a = ok ? assign_of(p, gi) : 0u;
+        decode_types<S>(p, a, ty);
         const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B) && ok && active;
-        uint32_t T;
         bool done_here = true;
         if (p.M < (uint32_t)S) {
-            T = dp_table<S>(p, F, B, comm);
+            dp_table<S>(p, F, B, comm, Y);
         } else {
-            uint32_t Y[S];
             dp_prologue<S>(Y, F, B, comm);
             const uint32_t k1 = p.nlevels ? p.lvl_k[0] : nit;
             done_here = dp_advance<S>(Y, F, B, comm, 0, k1, nit);
             if (p.nlevels) enqueue<S>(p, 0, &nq, !done_here && active && ok, (uint32_t)gi, w, Y);
-            T = dp_finish<S>(Y, F, B, comm);
+            dp_finish<S>(Y, F, B, comm);
         }
+        uint32_t T = end_time<S, R, AR>(p, tab, Y, comm, w, a);
         if (!ok) T = 0xFFFFFFFFu;
         const bool write = active && (done_here || !ok);
         if (write && p.makespan_out) p.makespan_out[gi] = T;
@@ -646,7 +681,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
 
 // Level `lvl` of the cascade: resume the queued lanes from iteration
 // p.lvl_k[lvl-1] to p.lvl_k[lvl] (the end at the last level).
-template <int S, typename R>
+template <int S, typename R, bool AR>
 __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl) {
     extern __shared__ __align__(16) unsigned char smem[];
     const Lds<R> tab = stage_tables<R>(p, smem);
@@ -675,11 +710,13 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
 #pragma unroll
         for (int s = 0; s < S; ++s) Y[s] = active ? qin.Y[(uint64_t)s * p.qcap + seg + q] : 0u;
         const bool ok = unpack_cuts<S>(w, p.L, cut);
-        decode_types<S>(p, ok ? assign_of(p, i) : 0u, ty);
+        const uint32_t a = ok ? assign_of(p, i) : 0u;
+        decode_types<S>(p, a, ty);
         const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B);
         const bool settled = dp_advance<S>(Y, F, B, comm, k0, k1, nit);
         if (lvl < p.nlevels) enqueue<S>(p, lvl & 1, &nq, active && !settled, i, w, Y);
-        const uint32_t T = dp_finish<S>(Y, F, B, comm);
+        dp_finish<S>(Y, F, B, comm);
+        const uint32_t T = end_time<S, R, AR>(p, tab, Y, comm, w, a);
         if (active && settled) {
             if (p.makespan_out) p.makespan_out[i] = T;
             const unsigned long long key = make_key(feas, T, i);
@@ -695,7 +732,7 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
 
 // Early stop (Eq. 2 / Theorem 1) over one chunk: each block filters a tile
 // of kTile candidates, compacts the survivors in LDS and evaluates them.
-template <int S, typename R>
+template <int S, typename R, bool AR>
 __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chunk_lo, uint64_t chunk_hi,
                                                          uint32_t bound, uint32_t publish) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -723,11 +760,18 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         decode_types<S>(p, ok ? assign_of(p, i) : 0u, ty);
         const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B);
+        uint32_t D[S];
+        if (AR) {
+            stage_allreduce<S, R>(p, tab, cut, ty, D);
+        } else {
+#pragma unroll
+            for (int s = 0; s < S; ++s) D[s] = 0;
+        }
         bool keep = false;
         if (active) {
             if (!ok) my_bad++;
             else if (!feas) my_infeas++;
-            else if (eq2_bound<S>(p.M, F, B) > b) my_pruned++;
+            else if (eq2_bound<S>(p.M, F, B, D) > b) my_pruned++;
             else keep = true;
         }
         const unsigned long long m = __ballot(keep);
@@ -752,9 +796,12 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
 #pragma unroll
         for (int kk = 0; kk < NW; ++kk) w[kk] = p.codes[(uint64_t)kk * p.ccap + (i - p.first_i)];
         unpack_cuts<S>(w, p.L, cut);
-        decode_types<S>(p, assign_of(p, i), ty);
+        const uint32_t a = assign_of(p, i);
+        decode_types<S>(p, a, ty);
         stage_weights<S, R>(p, tab, cut, ty, F, B);
-        const uint32_t T = makespan<S>(p, F, B, comm);
+        uint32_t Y[S];
+        dp_full<S>(p, F, B, comm, Y);
+        const uint32_t T = end_time<S, R, AR>(p, tab, Y, comm, w, a);
         const unsigned long long key = make_key(true, T, (uint32_t)i);
         best = key < best ? key : best;
     }
@@ -767,117 +814,47 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
     block_min_and_finish(best, p.acc, p.done, nullptr, p.run_best, true, false, publish ? p.snap : nullptr);
 }
 
-// Argmin over stored makespans / feasibility bits.
-__global__ __launch_bounds__(kBlock) void argmin_kernel(const uint32_t *T, const uint32_t *bits, uint64_t count,
-                                                        unsigned long long *acc, unsigned int *done,
-                                                        unsigned long long *result) {
-    unsigned long long best = ~0ull;
-    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-    for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < count; i += stride) {
-        const bool f = bits ? ((bits[i >> 5] >> (i & 31)) & 1u) : true;
-        const unsigned long long key = make_key(f, T[i], (uint32_t)i);
-        best = key < best ? key : best;
-    }
-    block_min_and_finish(best, acc, done, result, nullptr, true);
-}
-
-// Small fill kernel used instead of memset so that the calls stay capturable.
-__global__ void fill_u64(unsigned long long *p, uint32_t n, unsigned long long v) {
-    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) p[i] = v;
-}
-
-// ---------------------------------------------------------------------------
 // host-side launchers
 // ---------------------------------------------------------------------------
 template <int S, typename R>
-static hipError_t launch_eval_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
-    hipLaunchKernelGGL((eval_kernel<S, R>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
+hipError_t launch_eval_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
+    if (p.has_ar) hipLaunchKernelGGL((eval_kernel<S, R, true>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
+    else hipLaunchKernelGGL((eval_kernel<S, R, false>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
     return hipGetLastError();
 }
 
 template <int S, typename R>
-static hipError_t launch_decode_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
+hipError_t launch_decode_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
     const size_t lds = (size_t)p.S * kNB * sizeof(R);
     hipLaunchKernelGGL((decode_kernel<S, R>), dim3(lc.grid), dim3(kBlock), lds, st, p);
     return hipGetLastError();
 }
 
 template <int S, typename R>
-static hipError_t launch_resume_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl) {
-    hipLaunchKernelGGL((resume_kernel<S, R>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p, lvl);
+hipError_t launch_resume_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl) {
+    if (p.has_ar) hipLaunchKernelGGL((resume_kernel<S, R, true>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p, lvl);
+    else hipLaunchKernelGGL((resume_kernel<S, R, false>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p, lvl);
     return hipGetLastError();
 }
 
 template <int S, typename R>
-static hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
+hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
                                    uint32_t bound, uint32_t publish) {
     const uint64_t grid = (hi - lo + kTile - 1) / kTile;
-    hipLaunchKernelGGL((bounded_kernel<S, R>), dim3((uint32_t)grid), dim3(kBlock), lc.lds_bytes, st, p, lo, hi,
-                       bound, publish);
+    if (p.has_ar)
+        hipLaunchKernelGGL((bounded_kernel<S, R, true>), dim3((uint32_t)grid), dim3(kBlock), lc.lds_bytes, st, p, lo,
+                           hi, bound, publish);
+    else
+        hipLaunchKernelGGL((bounded_kernel<S, R, false>), dim3((uint32_t)grid), dim3(kBlock), lc.lds_bytes, st, p, lo,
+                           hi, bound, publish);
     return hipGetLastError();
 }
 
 template <int S, typename R>
-static hipError_t occupancy_s(int *blocks, size_t lds) {
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, eval_kernel<S, R>, kBlock, lds);
+hipError_t occupancy_s(int *blocks, size_t lds, bool ar) {
+    if (ar) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, eval_kernel<S, R, true>, kBlock, lds);
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, eval_kernel<S, R, false>, kBlock, lds);
 }
 
-#define PK_DISPATCH(FN, S_, WIDE_, ...)                                                        \
-    switch (S_) {                                                                              \
-    case 1: return WIDE_ ? FN<1, uint64_t>(__VA_ARGS__) : FN<1, uint32_t>(__VA_ARGS__);       \
-    case 2: return WIDE_ ? FN<2, uint64_t>(__VA_ARGS__) : FN<2, uint32_t>(__VA_ARGS__);       \
-    case 3: return WIDE_ ? FN<3, uint64_t>(__VA_ARGS__) : FN<3, uint32_t>(__VA_ARGS__);       \
-    case 4: return WIDE_ ? FN<4, uint64_t>(__VA_ARGS__) : FN<4, uint32_t>(__VA_ARGS__);       \
-    case 5: return WIDE_ ? FN<5, uint64_t>(__VA_ARGS__) : FN<5, uint32_t>(__VA_ARGS__);       \
-    case 6: return WIDE_ ? FN<6, uint64_t>(__VA_ARGS__) : FN<6, uint32_t>(__VA_ARGS__);       \
-    case 7: return WIDE_ ? FN<7, uint64_t>(__VA_ARGS__) : FN<7, uint32_t>(__VA_ARGS__);       \
-    case 8: return WIDE_ ? FN<8, uint64_t>(__VA_ARGS__) : FN<8, uint32_t>(__VA_ARGS__);       \
-    case 9: return WIDE_ ? FN<9, uint64_t>(__VA_ARGS__) : FN<9, uint32_t>(__VA_ARGS__);       \
-    case 10: return WIDE_ ? FN<10, uint64_t>(__VA_ARGS__) : FN<10, uint32_t>(__VA_ARGS__);    \
-    case 11: return WIDE_ ? FN<11, uint64_t>(__VA_ARGS__) : FN<11, uint32_t>(__VA_ARGS__);    \
-    case 12: return WIDE_ ? FN<12, uint64_t>(__VA_ARGS__) : FN<12, uint32_t>(__VA_ARGS__);    \
-    case 13: return WIDE_ ? FN<13, uint64_t>(__VA_ARGS__) : FN<13, uint32_t>(__VA_ARGS__);    \
-    case 14: return WIDE_ ? FN<14, uint64_t>(__VA_ARGS__) : FN<14, uint32_t>(__VA_ARGS__);    \
-    case 15: return WIDE_ ? FN<15, uint64_t>(__VA_ARGS__) : FN<15, uint32_t>(__VA_ARGS__);    \
-    case 16: return WIDE_ ? FN<16, uint64_t>(__VA_ARGS__) : FN<16, uint32_t>(__VA_ARGS__);    \
-    default: return hipErrorInvalidValue;                                                      \
-    }
-
-hipError_t launch_eval(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
-    PK_DISPATCH(launch_eval_s, p.S, p.wide, p, lc, st)
-}
-
-hipError_t launch_decode(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
-    PK_DISPATCH(launch_decode_s, p.S, p.wide, p, lc, st)
-}
-
-hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl) {
-    PK_DISPATCH(launch_resume_s, p.S, p.wide, p, lc, st, lvl)
-}
-
-hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
-                          uint32_t bound, uint32_t publish) {
-    PK_DISPATCH(launch_bounded_s, p.S, p.wide, p, lc, st, lo, hi, bound, publish)
-}
-
-hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, int *blocks) {
-    PK_DISPATCH(occupancy_s, S, wide, blocks, lds)
-}
-
-hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,
-                         unsigned long long *acc, unsigned int *done, unsigned long long *result, hipStream_t st) {
-    hipLaunchKernelGGL(argmin_kernel, dim3(grid), dim3(kBlock), 0, st, T, bits, count, acc, done, result);
-    return hipGetLastError();
-}
-
-hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, hipStream_t st) {
-    hipLaunchKernelGGL(fill_u64, dim3((n + 63) / 64), dim3(64), 0, st, p, n, v);
-    return hipGetLastError();
-}
-
-int code_words(int S) { return S > 1 ? (S - 1 + 3) / 4 : 1; }
-int prologue_op(int S, int s, int k) { return pro_op(S, s, k); }
-int epilogue_op(int S, int s, int j) { return epi_op(S, s, j); }
 
 }  // namespace pk

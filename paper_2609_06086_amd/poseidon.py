@@ -38,7 +38,7 @@ class _Problem(C.Structure):
                 ("fwd_us", C.c_void_p), ("bwd_us", C.c_void_p),
                 ("comm_fwd_us", C.c_void_p), ("comm_bwd_us", C.c_void_p),
                 ("mem_mb", C.c_void_p), ("cap_mb", C.c_void_p),
-                ("assign", C.c_void_p), ("A", C.c_uint64)]
+                ("assign", C.c_void_p), ("A", C.c_uint64), ("allreduce_us", C.c_void_p)]
 
 
 class _Cands(C.Structure):
@@ -143,7 +143,8 @@ def _problem_struct(prob):
                   host(prob.comm_bwd, np.uint32) if S > 1 else None,
                   host(prob.mem, np.uint32), host(prob.cap, np.uint32),
                   host(prob.assign, np.uint8),
-                  int(prob.assign.shape[0]) if prob.assign is not None else 0)
+                  int(prob.assign.shape[0]) if prob.assign is not None else 0,
+                  host(getattr(prob, "allreduce", None), np.uint32))
     return st, keep
 
 

@@ -45,6 +45,7 @@ class Problem:
     cap: np.ndarray          # uint32 [T]
     assign: Optional[np.ndarray] = None   # uint8 [A][S]; None => all T^S rows
     seed: Optional[int] = None
+    allreduce: Optional[np.ndarray] = None  # uint32 [T][L] DP all-reduce time per layer, or None
 
     @property
     def A(self) -> int:
@@ -101,7 +102,7 @@ def _u32(a) -> np.ndarray:
     return np.ascontiguousarray(a.astype(np.uint32))
 
 
-WORKLOAD_IDS = (1, 2, 3, 4, 5)
+WORKLOAD_IDS = (1, 2, 3, 4, 5, 6)
 
 
 def workload(cfg: int, n_samples: Optional[int] = None) -> Workload:
@@ -146,11 +147,11 @@ def workload(cfg: int, n_samples: Optional[int] = None) -> Workload:
         prob = Problem(L, S, M, T, _u32(fwd), _u32(2 * fwd), _u32(comm), _u32(comm),
                        _u32(mem), _u32(cap), assign, seed)
         cands = Candidates(first=0, count=prob.n_candidates)
-    elif cfg in (4, 5):
-        if cfg == 4:
+    elif cfg in (4, 5, 6):
+        if cfg in (4, 6):
             L, S, M, T = 80, 8, 64, 3
             speeds, cap, comm_hi = (10, 17, 26), [65536, 81920, 196608], 120
-            n = 1 << 26
+            n = 1 << 26 if cfg == 4 else 1 << 24
         else:
             L, S, M, T = 126, 16, 128, 4
             speeds, cap, comm_hi = (10, 14, 20, 30), [49152, 65536, 98304, 196608], 160
@@ -168,8 +169,14 @@ def workload(cfg: int, n_samples: Optional[int] = None) -> Workload:
             assign = perm.astype(np.uint8)[None, :]
         else:
             assign = None
+        ar = None
+        if cfg == 6:
+            # gradient all-reduce per layer (data parallelism, Sec. 4.1.3): a
+            # per-layer base time, slower on the device types with slower links
+            ar_base = rng.integers(20000, 60001, size=L)
+            ar = np.stack([_rhu_scale(ar_base, 10, sp) for sp in speeds])
         prob = Problem(L, S, M, T, _u32(fwd), _u32(2 * fwd), _u32(comm), _u32(comm),
-                       _u32(mem), _u32(cap), assign, seed)
+                       _u32(mem), _u32(cap), assign, seed, None if ar is None else _u32(ar))
         ncomp = prob.n_compositions
         ranks = rng.integers(0, ncomp, size=n, dtype=np.uint64)
         if assign is None:
@@ -178,7 +185,9 @@ def workload(cfg: int, n_samples: Optional[int] = None) -> Workload:
             aidx = None
         cands = Candidates(comp_rank=np.ascontiguousarray(ranks),
                            assign_idx=None if aidx is None else np.ascontiguousarray(aidx))
-        if cfg == 4:
+        if cfg == 6:
+            desc = "L=80 S=8 M=64 T=3 with DP all-reduce, 2^24 sampled (composition, assignment) pairs"
+        elif cfg == 4:
             desc = "L=80 S=8 M=64 T=3, 2^26 sampled (composition, assignment) pairs"
         else:
             desc = "L=126 S=16 M=128 T=4, fixed 4x4 type permutation, 2^24 sampled compositions"

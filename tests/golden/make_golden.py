@@ -1,14 +1,14 @@
 """Write tests/golden/full_workloads.json from the CPU oracle only.
 
-For each large workload (3, 4, 5) this records, over every candidate:
+For each large workload (3, 4, 5, 6) this records, over every candidate:
 the SHA-256 of the makespan array (uint32 little-endian), the SHA-256 of the
 feasibility bit array packed as the library's output (bit i % 32 of uint32
 word i / 32), the number of feasible candidates and the argmin.  For
-workload 4 it also records the early-stop pass: the warm-up bound (best of
+workloads 4 and 6 it also records the early-stop pass: the warm-up bound (best of
 the first 500 list entries) and, per chunk size, the oracle's
 (best, evaluated, pruned, infeasible).
 
-Run from the repository root:  python tests/golden/make_golden.py
+Run from the repository root:  python tests/golden/make_golden.py [workload ...]
 """
 import hashlib
 import json
@@ -36,7 +36,10 @@ def pack_bits(f: np.ndarray) -> np.ndarray:
 
 def main():
     res = {"note": "written by tests/golden/make_golden.py from the C oracle; see that script"}
-    for cfg in (3, 4, 5):
+    only = [int(a) for a in sys.argv[1:]] or [3, 4, 5, 6]
+    if os.path.exists(OUT):
+        res.update({k: v for k, v in json.load(open(OUT)).items() if k != "note"})
+    for cfg in only:
         wl = W.workload(cfg)
         t0 = time.time()
         T, f = coracle.evaluate(wl.problem, wl.cands)
@@ -49,7 +52,7 @@ def main():
             "best_index": best[0], "best_makespan": best[1],
             "makespan_min": int(T.min()), "makespan_max": int(T.max()),
         }
-        if cfg == 4:
+        if cfg in (4, 6):
             wb = coracle.argmin(T[:WARMUP], f[:WARMUP])
             bound = wb[1]
             ent["warmup"] = WARMUP

@@ -407,3 +407,73 @@ def test_call_longer_than_one_chunk(dev):
     assert st.evaluated + st.pruned + st.infeasible == len(c)
     assert st.infeasible == (g["n"] - g["n_feasible"]) + int((~fe).sum())
     ctx.close()
+
+
+# ------------------------------------------------------ DP all-reduce
+
+def _with_allreduce(rng, prob, hi=3000):
+    prob.allreduce = rng.integers(0, hi, size=(prob.T, prob.L)).astype(np.uint32)
+    return prob
+
+
+def test_allreduce_random_problems(dev):
+    """R_s nodes: T = max_s(finish(B_{s,M}) + R_s), both DP paths and the cascade."""
+    rng = np.random.default_rng(109)
+    for trial in range(30):
+        S = int(rng.integers(1, 17))
+        M = int(rng.integers(1, 3 * S + 20))
+        L = S + int(rng.integers(0, 10))
+        T = int(rng.integers(1, 4))
+        prob = W.random_problem(rng, L, S, M, T, cost_hi=400, mem_hi=30, cap=int(rng.integers(30, 200)),
+                                assign_rows=None if T ** S < 5000 else 5)
+        # all-reduce large enough to decide the makespan in some candidates
+        _with_allreduce(rng, prob, hi=int(rng.integers(1, 400)) * max(M, 1))
+        check_against_oracle(prob, W.random_candidates(rng, prob, int(rng.integers(1, 2000))), dev)
+
+
+def test_allreduce_python_oracle_and_bounded(dev):
+    rng = np.random.default_rng(110)
+    for _ in range(6):
+        S = int(rng.integers(1, 5))
+        L = S + int(rng.integers(0, 5))
+        M = int(rng.integers(1, 7))
+        prob = _with_allreduce(rng, W.random_problem(rng, L, S, M, 2, mem_hi=30, cap=int(rng.integers(30, 120))),
+                               hi=2000)
+        full = W.Candidates(first=0, count=prob.n_candidates)
+        check_against_oracle(prob, full, dev, python_oracle=True)
+        To, fo = coracle.evaluate(prob, full)
+        ex = coracle.argmin(To, fo)
+        if ex is not None:
+            for chunk in (0, 5):
+                b, _ = bounded_vs_oracle(prob, full, int(To[fo].max()), chunk, dev)
+                assert (b.index, b.makespan) == ex
+
+
+def test_workload6_prefix_exhaustive_and_bounded(dev):
+    wl = W.workload(6)
+    n = 500_003
+    c = W.Candidates(comp_rank=wl.cands.comp_rank[:n].copy(), assign_idx=wl.cands.assign_idx[:n].copy())
+    check_against_oracle(wl.problem, c, dev)
+    To, fo = coracle.evaluate(wl.problem, W.Candidates(comp_rank=c.comp_rank[:500], assign_idx=c.assign_idx[:500]))
+    bound = coracle.argmin(To, fo)[1]
+    for chunk in (0, 100_000):
+        bounded_vs_oracle(wl.problem, c, bound, chunk, dev)
+
+
+def test_full_workload6_matches_golden(dev):
+    gall = _golden()
+    if "cfg6" not in gall:
+        pytest.skip("no golden for workload 6")
+    g = gall["cfg6"]
+    wl = W.workload(6)
+    ctx = P.poseidon_load_costs(wl.problem, 0)
+    Tg, fg, best = gpu_eval(ctx, wl.cands, dev)
+    assert hashlib.sha256(Tg.astype("<u4").tobytes()).hexdigest() == g["makespan_sha256"]
+    assert hashlib.sha256(pack_bits(fg).astype("<u4").tobytes()).hexdigest() == g["feasible_bits_sha256"]
+    assert (best.index, best.makespan) == (g["best_index"], g["best_makespan"])
+    d = to_dev(wl.cands, dev)
+    for chunk, exp in g["bounded"].items():
+        b, st = P.poseidon_eval_candidates_bounded(ctx, g["warmup_bound"], chunk=int(chunk), **d)
+        assert (b.index, b.makespan) == (exp["best_index"], exp["best_makespan"])
+        assert (st.evaluated, st.pruned, st.infeasible) == (exp["evaluated"], exp["pruned"], exp["infeasible"])
+    ctx.close()

@@ -434,3 +434,53 @@ def test_stage_weights_cover_exactly_the_stage_layers():
             n = b[s + 1] - b[s]
             assert F[s] == 2 ** b[s + 1] - 2 ** b[s] + n * types[s] * 2 ** 40
             assert MEM[s] == sum(range(b[s] + 1, b[s + 1] + 1))
+
+
+# ------------------------------------------------------- DP all-reduce
+
+def test_c_oracle_allreduce_matches_python():
+    """R_s weights (per-layer all-reduce summed over the stage, Sec. 4.1.3)
+    and the d_i term of Eq. 2, Python vs C, exhaustive and early stop."""
+    rng = np.random.default_rng(18)
+    for trial in range(12):
+        S = int(rng.integers(1, 6))
+        L = S + int(rng.integers(0, 6))
+        M = int(rng.integers(1, 9))
+        prob = W.random_problem(rng, L, S, M, 2, mem_hi=30, cap=int(rng.integers(30, 150)),
+                                assign_rows=None if trial % 2 else 3)
+        prob.allreduce = rng.integers(0, 800, size=(2, L)).astype(np.uint32)
+        full = W.Candidates(first=0, count=prob.n_candidates)
+        Tp, fp = dag.evaluate(prob, full)
+        Tc, fc = coracle.evaluate(prob, full, nthreads=3)
+        assert (Tp == Tc).all() and (fp == fc).all()
+        Tx, fx = Tp, fp
+        ex = dag.argmin(Tx, fx)
+        if ex is None:
+            continue
+        bound = int(Tx[fx].max())
+        for chunk in (0, 7):
+            best, ev, pr, inf = dag.bounded_search(prob, full, bound, chunk)
+            assert best == ex
+            assert coracle.bounded(prob, full, bound, chunk, nthreads=2) == (best, ev, pr, inf)
+
+
+def test_allreduce_event_simulation():
+    """The event-driven run extended with a gradient all-reduce that each
+    stage starts after its last backward pass: iteration end = max over
+    stages of (last backward finish + d_s); equals the DAG's finish(E)."""
+    rng = np.random.default_rng(19)
+    for _ in range(100):
+        S, M = int(rng.integers(1, 6)), int(rng.integers(1, 8))
+        F, B, cf, cb = _rand_case(rng, S, M)
+        d = rng.integers(0, 400, S)
+        t_end = des.simulate_1f1b(S, M, F, B, cf, cb, dag.one_f_one_b_order, allreduce=d)
+        assert t_end == dag.longest_path(dag.dag_for(S, M), F, B, cf, cb, d)
+
+
+def test_eq2_with_allreduce_is_a_lower_bound():
+    rng = np.random.default_rng(20)
+    for _ in range(300):
+        S, M = int(rng.integers(1, 7)), int(rng.integers(1, 10))
+        F, B, cf, cb = _rand_case(rng, S, M)
+        d = rng.integers(0, 500, S)
+        assert dag.eq2_bound(list(F), list(B), M, list(d)) <= dag.longest_path(dag.dag_for(S, M), F, B, cf, cb, d)
