@@ -35,6 +35,9 @@ docstring; the list of readings:
 * R10 (stage-level bound, Eq. 2): g(S_x) as printed, with f_i, b_i the
   stage totals and d_i the stage all-reduce time; a candidate is pruned
   iff max_x g(S_x) > bound (strict, as in Theorem 1).
+* R11 (Eager 1F1B, App. B.1): stage s runs w = min(2(S-s)+1, M) forward
+  passes, then M - w groups of one backward and one forward pass, then the
+  remaining backward passes.
 """
 from __future__ import annotations
 
@@ -61,6 +64,22 @@ def one_f_one_b_order(S: int, M: int, s: int) -> List[Tuple[str, int]]:
         order.append(("B", i))
     order += [("B", m) for m in range(M - w + 1, M + 1)]
     return order
+
+
+def eager_1f1b_order(S: int, M: int, s: int) -> List[Tuple[str, int]]:
+    """Execution order of stage s under Eager 1F1B (App. B.1, reading R11):
+    a warm-up of 2(S-s)+1 forwards, steady groups of (backward, forward),
+    a cool-down of the remaining backwards."""
+    w = min(2 * (S - s) + 1, M)
+    order = [("F", m) for m in range(1, w + 1)]
+    for k in range(1, M - w + 1):
+        order.append(("B", k))
+        order.append(("F", w + k))
+    order += [("B", m) for m in range(M - w + 1, M + 1)]
+    return order
+
+
+SCHEDULES = {0: one_f_one_b_order, 1: eager_1f1b_order}
 
 
 @dataclass
@@ -136,14 +155,15 @@ def build_dag(S: int, M: int, order=one_f_one_b_order) -> Dag:
     return Dag(S, M, nodes, edges, topo, preds)
 
 
-_DAG_CACHE: Dict[Tuple[int, int], Dag] = {}
+_DAG_CACHE: Dict[Tuple[int, int, int], Dag] = {}
 
 
-def dag_for(S: int, M: int) -> Dag:
-    """The topology depends only on (S, M); reuse it (Sec. 5, simulator design)."""
-    key = (S, M)
+def dag_for(S: int, M: int, schedule: int = 0) -> Dag:
+    """The topology depends only on (S, M) and the schedule; reuse it
+    (Sec. 5, simulator design)."""
+    key = (S, M, schedule)
     if key not in _DAG_CACHE:
-        _DAG_CACHE[key] = build_dag(S, M)
+        _DAG_CACHE[key] = build_dag(S, M, order=SCHEDULES[schedule])
     return _DAG_CACHE[key]
 
 
@@ -285,7 +305,7 @@ def evaluate(prob, cands, allreduce=None):
     The all-reduce table defaults to the problem's own (``prob.allreduce``)."""
     if allreduce is None:
         allreduce = getattr(prob, "allreduce", None)
-    dag = dag_for(prob.S, prob.M)
+    dag = dag_for(prob.S, prob.M, getattr(prob, "schedule", 0))
     lst = candidate_list(prob, cands)
     T = np.zeros(len(lst), dtype=np.int64)
     feas = np.zeros(len(lst), dtype=bool)
@@ -334,7 +354,7 @@ def bounded_search(prob, cands, bound: int, chunk: int = 0):
     (makespan, index)-smallest evaluated candidate if its makespan is
     <= bound, else None.  Returns (best, evaluated, pruned, infeasible)."""
     allreduce = getattr(prob, "allreduce", None)
-    dag = dag_for(prob.S, prob.M)
+    dag = dag_for(prob.S, prob.M, getattr(prob, "schedule", 0))
     lst = candidate_list(prob, cands)
     n = len(lst)
     chunk = n if chunk <= 0 else chunk

@@ -15,7 +15,9 @@
  *    Kahn's algorithm.
  *  - 1F1B order (reading of Sec. 4.1.2; the paper does not state the warm-up
  *    length): stage s runs w = min(S - s, M) forwards, then (F_{w+i}, B_i)
- *    for i = 1..M-w, then the remaining backwards.
+ *    for i = 1..M-w, then the remaining backwards.  Eager 1F1B (App. B.1):
+ *    w = min(2(S - s) + 1, M) forwards, then (B_i, F_{w+i}) for
+ *    i = 1..M-w, then the remaining backwards.
  *  - Weights (Sec. 4.1.3): F_{s,m} = sum of the stage's per-layer forward
  *    times on its device type, likewise B_{s,m}; inter-stage edges carry the
  *    per-boundary transfer time; all other edges and control nodes weigh 0.
@@ -46,6 +48,7 @@ typedef struct {
     const uint8_t *assign;         /* [A][S] or NULL (all T^S rows) */
     uint64_t A;
     const uint32_t *allreduce;     /* [T][L] or NULL (no DP all-reduce) */
+    uint32_t schedule;             /* 0 = 1F1B, 1 = Eager 1F1B */
 } oc_problem;
 
 enum { K_F = 0, K_B = 1, K_R = 2, K_START = 3, K_END = 4 };
@@ -85,18 +88,25 @@ static void dag_free(oc_dag *g) {
     free(g);
 }
 
-/* 1F1B order of stage s as (kind, m) pairs written to ko/mo (2M entries). */
-static void stage_order(int S, int M, int s, int *ko, int *mo) {
-    int w = S - s < M ? S - s : M, k = 0;
+/* Order of stage s as (kind, m) pairs written to ko/mo (2M entries). */
+static void stage_order(int S, int M, int s, int schedule, int *ko, int *mo) {
+    int w, k = 0;
+    if (schedule == 1) w = 2 * (S - s) + 1 < M ? 2 * (S - s) + 1 : M;
+    else w = S - s < M ? S - s : M;
     for (int m = 1; m <= w; ++m) { ko[k] = K_F; mo[k] = m; ++k; }
     for (int i = 1; i <= M - w; ++i) {
-        ko[k] = K_F; mo[k] = w + i; ++k;
-        ko[k] = K_B; mo[k] = i; ++k;
+        if (schedule == 1) {
+            ko[k] = K_B; mo[k] = i; ++k;
+            ko[k] = K_F; mo[k] = w + i; ++k;
+        } else {
+            ko[k] = K_F; mo[k] = w + i; ++k;
+            ko[k] = K_B; mo[k] = i; ++k;
+        }
     }
     for (int m = M - w + 1; m <= M; ++m) { ko[k] = K_B; mo[k] = m; ++k; }
 }
 
-static oc_dag *dag_build(int S, int M) {
+static oc_dag *dag_build(int S, int M, int schedule) {
     oc_dag *g = calloc(1, sizeof(oc_dag));
     if (!g) return NULL;
     int ncomp = 2 * S * M;
@@ -128,7 +138,7 @@ static oc_dag *dag_build(int S, int M) {
         }
     /* intra-stage edges along the schedule */
     for (int s = 1; s <= S; ++s) {
-        stage_order(S, M, s, ko, mo);
+        stage_order(S, M, s, schedule, ko, mo);
         for (int k = 1; k < 2 * M; ++k) {
             int u = ko[k - 1] == K_F ? idF(M, s, mo[k - 1]) : idB(M, s, mo[k - 1]);
             int v = ko[k] == K_F ? idF(M, s, mo[k]) : idB(M, s, mo[k]);
@@ -350,6 +360,7 @@ static int run_jobs(oc_job *proto, uint64_t lo, uint64_t hi, int nthreads, oc_jo
 
 static int check(const oc_problem *p) {
     if (!p || p->S < 1 || p->S > 64 || p->L < p->S || p->M < 1 || p->T < 1 || p->A < 1) return -1;
+    if (p->schedule > 1) return -1;
     if (!p->fwd || !p->bwd || !p->mem || !p->cap) return -1;
     if (p->S > 1 && (!p->cf || !p->cb)) return -1;
     return 0;
@@ -360,7 +371,7 @@ static int check(const oc_problem *p) {
 int oc_eval(const oc_problem *p, uint64_t first, uint64_t count, const uint64_t *rank,
             const uint32_t *aidx, uint32_t *out_T, uint8_t *out_feas, int nthreads) {
     if (check(p)) return -1;
-    oc_dag *g = dag_build((int)p->S, (int)p->M);
+    oc_dag *g = dag_build((int)p->S, (int)p->M, (int)p->schedule);
     uint64_t *binom = pascal((int)p->L - 1, (int)p->S - 1);
     if (!g || !binom) { dag_free(g); free(binom); return -3; }
     oc_job proto = {0};
@@ -381,7 +392,7 @@ int oc_bounded(const oc_problem *p, uint64_t first, uint64_t count, const uint64
                uint32_t *best_T, uint64_t *evaluated, uint64_t *pruned, uint64_t *infeasible,
                int nthreads) {
     if (check(p)) return -1;
-    oc_dag *g = dag_build((int)p->S, (int)p->M);
+    oc_dag *g = dag_build((int)p->S, (int)p->M, (int)p->schedule);
     uint64_t *binom = pascal((int)p->L - 1, (int)p->S - 1);
     if (!g || !binom) { dag_free(g); free(binom); return -3; }
     if (chunk == 0) chunk = count ? count : 1;
@@ -413,7 +424,7 @@ int oc_bounded(const oc_problem *p, uint64_t first, uint64_t count, const uint64
 
 /* DAG shape for pins: compute nodes, edges by kind. */
 int oc_dag_counts(int S, int M, int *n_nodes, int *n_fwd, int *n_bwd, int *n_intra, int *n_other) {
-    oc_dag *g = dag_build(S, M);
+    oc_dag *g = dag_build(S, M, 0);
     if (!g) return -1;
     int f = 0, b = 0, in = 0, o = 0;
     for (int v = 0; v < g->n; ++v) {

@@ -46,6 +46,7 @@ class Problem:
     assign: Optional[np.ndarray] = None   # uint8 [A][S]; None => all T^S rows
     seed: Optional[int] = None
     allreduce: Optional[np.ndarray] = None  # uint32 [T][L] DP all-reduce time per layer, or None
+    schedule: int = 0                       # 0 = 1F1B, 1 = Eager 1F1B
 
     @property
     def A(self) -> int:

@@ -484,3 +484,124 @@ def test_eq2_with_allreduce_is_a_lower_bound():
         F, B, cf, cb = _rand_case(rng, S, M)
         d = rng.integers(0, 500, S)
         assert dag.eq2_bound(list(F), list(B), M, list(d)) <= dag.longest_path(dag.dag_for(S, M), F, B, cf, cb, d)
+
+
+# ------------------------------------------------------- Eager 1F1B
+
+def _kxyw_cost(N, M, F, B, tf, tb, x, y, w):
+    """Cost of the canonical path K(x, y, w) (App. B.2, Eq. formula.cost)."""
+    c = sum(F[i] + B[i] + tf[i] + tb[i] for i in range(x - 1)) + F[x - 1] + B[x - 1]
+    c += 2 * (N - x) * F[w - 1] + 2 * (N - y) * B[w - 1]
+    c += (M - 2 * (N - y) - 1) * (F[y - 1] + B[y - 1])
+    return c
+
+
+def _kxyw_max(N, M, F, B, tf, tb):
+    best = 0
+    for x in range(1, N + 1):
+        for y in range(1, x + 1):
+            if F[y - 1] != max(F[y - 1:x]):
+                continue
+            for w in range(1, y + 1):
+                if F[w - 1] == max(F[:x]):
+                    best = max(best, _kxyw_cost(N, M, F, B, tf, tb, x, y, w))
+    return best
+
+
+def _assumption_case(rng):
+    """Random Eager-1F1B instance satisfying Assumptions 1-4 of App. B.1:
+    b_i = r f_i (r > 1), t <= (r-1)/2 F_min, M >= 2N, F_min >= alpha F_max."""
+    N = int(rng.integers(1, 6))
+    M = int(rng.integers(2 * N, 2 * N + 12))
+    p, q = int(rng.integers(12, 31)), 10          # r = p / q in [1.2, 3.0]
+    r = p / q
+    alpha = max(2 / 3, r / (1 + r))
+    fmax = int(rng.integers(50, 200))
+    F = [q * int(rng.integers(int(np.ceil(alpha * fmax)), fmax + 1)) for _ in range(N)]
+    B = [f * p // q for f in F]
+    tmax = int((r - 1) / 2 * min(F))
+    tf = [int(rng.integers(0, tmax + 1)) for _ in range(N - 1)]
+    tb = [int(rng.integers(0, tmax + 1)) for _ in range(N - 1)]
+    return N, M, F, B, tf, tb
+
+
+def test_eager_matches_the_papers_critical_path_theorem():
+    """Under Assumptions 1-4 some K(x, y, w) is a critical path of the
+    Eager-1F1B DAG (App. B.2), so the DAG's longest path equals the largest
+    C(K(x, y, w)) over the admissible (x, y, w) of Def. 4."""
+    rng = np.random.default_rng(21)
+    for _ in range(300):
+        N, M, F, B, tf, tb = _assumption_case(rng)
+        g = dag.dag_for(N, M, 1)
+        assert dag.longest_path(g, F, B, tf, tb) == _kxyw_max(N, M, F, B, tf + [0], tb + [0])
+
+
+def test_eager_planted_order_mistakes_fail_the_theorem():
+    """Reading the warm-up as 2(N-i) forwards, or the steady groups as
+    (forward, backward), breaks the equality with C(K(x, y, w))."""
+    def wrong_warmup(S, M, s):
+        w = min(2 * (S - s), M)
+        o = [("F", m) for m in range(1, w + 1)]
+        for k in range(1, M - w + 1):
+            o += [("B", k), ("F", w + k)]
+        return o + [("B", m) for m in range(M - w + 1, M + 1)]
+
+    def wrong_group(S, M, s):
+        w = min(2 * (S - s) + 1, M)
+        o = [("F", m) for m in range(1, w + 1)]
+        for k in range(1, M - w + 1):
+            o += [("F", w + k), ("B", k)]
+        return o + [("B", m) for m in range(M - w + 1, M + 1)]
+
+    rng = np.random.default_rng(22)
+    for mutant in (wrong_warmup, wrong_group, dag.one_f_one_b_order):
+        caught = False
+        for _ in range(200):
+            N, M, F, B, tf, tb = _assumption_case(rng)
+            try:
+                g = dag.build_dag(N, M, order=mutant)
+            except ValueError:
+                caught = True
+                break
+            if dag.longest_path(g, F, B, tf, tb) != _kxyw_max(N, M, F, B, tf + [0], tb + [0]):
+                caught = True
+                break
+        assert caught, mutant.__name__
+
+
+def test_eager_event_simulation_and_c_oracle():
+    rng = np.random.default_rng(23)
+    for _ in range(150):
+        S, M = int(rng.integers(1, 7)), int(rng.integers(1, 12))
+        F, B, cf, cb = _rand_case(rng, S, M)
+        assert des.simulate_1f1b(S, M, F, B, cf, cb, dag.eager_1f1b_order) == \
+            dag.longest_path(dag.dag_for(S, M, 1), F, B, cf, cb)
+    for trial in range(10):
+        S = int(rng.integers(1, 6))
+        L = S + int(rng.integers(0, 6))
+        M = int(rng.integers(1, 14))
+        prob = W.random_problem(rng, L, S, M, 2, mem_hi=30, cap=int(rng.integers(30, 150)))
+        prob.schedule = 1
+        if trial % 2:
+            prob.allreduce = rng.integers(0, 500, size=(2, L)).astype(np.uint32)
+        full = W.Candidates(first=0, count=prob.n_candidates)
+        Tp, fp = dag.evaluate(prob, full)
+        Tc, fc = coracle.evaluate(prob, full, nthreads=2)
+        assert (Tp == Tc).all() and (fp == fc).all()
+        ex = dag.argmin(Tp, fp)
+        if ex is not None:
+            bound = int(Tp[fp].max())
+            best = dag.bounded_search(prob, full, bound, 9)
+            assert best[0] == ex
+            assert coracle.bounded(prob, full, bound, 9, nthreads=2) == best
+
+
+def test_eager_same_uniform_closed_form_and_dag_shape():
+    """Eager 1F1B has the same nodes and edge counts (Sec. 4.1.2) and, with
+    uniform stages and no transfer time, the same (M+S-1)(f+b)."""
+    for S in range(1, 6):
+        for M in range(1, 10):
+            c = dag.dag_for(S, M, 1).counts()
+            assert c["compute_nodes"] == 2 * S * M and c["intra"] == S * (2 * M - 1)
+            assert dag.longest_path(dag.dag_for(S, M, 1), [3] * S, [5] * S, [0] * (S - 1), [0] * (S - 1)) == \
+                (M + S - 1) * 8
