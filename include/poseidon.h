@@ -19,9 +19,11 @@
  * Eq. 2 / Theorem 1 give a per-configuration lower bound used to skip
  * configurations that cannot beat the best one found so far.
  *
- * Stage s of S runs min(S - s, M) forward passes, then alternates one
- * forward and one backward pass, then drains the remaining backward passes
- * (the common 1F1B order; the paper does not spell out the warm-up length).
+ * Under 1F1B, stage s of S runs min(S - s, M) forward passes, then
+ * alternates one forward and one backward pass, then drains the remaining
+ * backward passes (the common order; the paper does not spell out the
+ * warm-up length).  Eager 1F1B (App. B.1) runs 2(S - s) + 1 warm-up
+ * forwards and then alternates a backward and a forward pass.
  *
  * All times are integer microseconds and all memory sizes integer MB, held
  * in uint32; every result is exact integer arithmetic.
@@ -56,6 +58,13 @@ extern "C" {
 #define POSEIDON_L_MAX 256  /* layers */
 #define POSEIDON_T_MAX 8    /* device types */
 
+/* Pipeline schedules (poseidon_problem.schedule). */
+enum {
+    POSEIDON_SCHEDULE_1F1B = 0,        /* min(S-s, M) warm-up forwards, then (F, B) pairs */
+    POSEIDON_SCHEDULE_EAGER_1F1B = 1   /* min(2(S-s)+1, M) warm-up forwards, then (B, F)
+                                          pairs (App. B.1) */
+};
+
 enum {
     POSEIDON_OK = 0,
     POSEIDON_NO_FEASIBLE = 1,
@@ -83,6 +92,9 @@ typedef struct {
                                      type t, or NULL = none.  Stage s's all-reduce node R_s
                                      weighs the sum over its layers and follows B_{s,M};
                                      T = max_s(finish(B_{s,M}) + R_s) (Sec. 4.1.1, 4.1.3) */
+    uint32_t schedule;            /* POSEIDON_SCHEDULE_*: the intra-stage order of the DAG
+                                     (Sec. 4.1.4: other schedules change only the intra-stage
+                                     edges) */
 } poseidon_problem;
 
 /* Candidates of one call.  comp_rank == NULL: range mode over joint indices

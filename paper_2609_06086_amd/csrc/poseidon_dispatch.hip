@@ -21,8 +21,8 @@ namespace pk {
                                                               uint64_t, uint64_t, uint32_t, uint32_t);        \
     extern template hipError_t launch_bounded_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t,  \
                                                               uint64_t, uint64_t, uint32_t, uint32_t);        \
-    extern template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool);                                 \
-    extern template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool);
+    extern template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool, bool);                                 \
+    extern template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool, bool);
 
 PK_EXTERN(1) PK_EXTERN(2) PK_EXTERN(3) PK_EXTERN(4) PK_EXTERN(5) PK_EXTERN(6) PK_EXTERN(7) PK_EXTERN(8)
 PK_EXTERN(9) PK_EXTERN(10) PK_EXTERN(11) PK_EXTERN(12) PK_EXTERN(13) PK_EXTERN(14) PK_EXTERN(15) PK_EXTERN(16)
@@ -87,8 +87,8 @@ hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st,
     PK_DISPATCH(launch_bounded_s, p.S, p.wide, p, lc, st, lo, hi, bound, publish)
 }
 
-hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, bool ar, int *blocks) {
-    PK_DISPATCH(occupancy_s, S, wide, blocks, lds, ar)
+hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, bool ar, bool sched, int *blocks) {
+    PK_DISPATCH(occupancy_s, S, wide, blocks, lds, ar, sched)
 }
 
 hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,

@@ -47,32 +47,42 @@ bool pow_fits(uint64_t base, uint64_t e, uint64_t limit, uint64_t *out) {
     return true;
 }
 
-// 1F1B order of stage s (1-based): min(S-s, M) forwards, then alternating
-// forward / backward, then the remaining backwards.  Kind 0 = F, 1 = B.
-void stage_order(int S, int M, int s, std::vector<std::pair<int, int>> &o) {
+// Order of stage s (1-based) under a schedule; kind 0 = F, 1 = B.
+//   1F1B:       min(S-s, M) forwards, then (F, B) pairs, then the remaining backwards.
+//   Eager 1F1B: min(2(S-s)+1, M) forwards, then (B, F) pairs, then the remaining backwards.
+void stage_order(int S, int M, int s, int schedule, std::vector<std::pair<int, int>> &o) {
     o.clear();
-    const int w = std::min(S - s, M);
+    const int w = schedule == POSEIDON_SCHEDULE_EAGER_1F1B ? std::min(2 * (S - s) + 1, M) : std::min(S - s, M);
     for (int m = 1; m <= w; ++m) o.push_back({0, m});
     for (int i = 1; i <= M - w; ++i) {
-        o.push_back({0, w + i});
-        o.push_back({1, i});
+        if (schedule == POSEIDON_SCHEDULE_EAGER_1F1B) {
+            o.push_back({1, i});
+            o.push_back({0, w + i});
+        } else {
+            o.push_back({0, w + i});
+            o.push_back({1, i});
+        }
     }
     for (int m = M - w + 1; m <= M; ++m) o.push_back({1, m});
 }
 
-// Unit-weight as-soon-as-possible slots of every node of the 1F1B DAG; fills
-// per-slot stage masks and checks the property the register stencil relies
-// on: at most one node per stage per slot, and every cross-stage predecessor
-// is still the newest node of its stage at the end of the previous slot.
-bool build_slots(int S, int M, std::vector<uint32_t> *masks, uint32_t *nslots) {
+// Unit-weight as-soon-as-possible slots of every node of the DAG; fills
+// three stage masks per slot (forward, forward whose input is the upstream
+// stage's second-newest forward, backward) and checks what the register
+// stencil relies on: at most one node per stage per slot, every input
+// finished in an earlier slot, a backward input still the newest backward
+// of its stage, and a forward input the newest or second-newest forward.
+// With `newest_only` (the single-register path) every input must still be
+// the newest node of its stage of either kind.
+bool build_slots(int S, int M, int schedule, bool newest_only, std::vector<uint32_t> *masks, uint32_t *nslots) {
     std::vector<std::vector<std::pair<int, int>>> ord(S + 1);
-    for (int s = 1; s <= S; ++s) stage_order(S, M, s, ord[s]);
+    for (int s = 1; s <= S; ++s) stage_order(S, M, s, schedule, ord[s]);
     // finish slot of F_{s,m} / B_{s,m}
     std::vector<int> finF((size_t)(S + 2) * (M + 1), -1), finB((size_t)(S + 2) * (M + 1), -1);
     auto at = [M](int s, int m) { return (size_t)s * (M + 1) + m; };
     std::vector<int> pos(S + 1, 0), slot_of_last(S + 1, 0);
     std::vector<int> startF(finF.size(), -1), startB(finB.size(), -1);
-    int placed = 0, total = 2 * S * M;
+    int placed = 0, total = 2 * S * M, n = 0;
     while (placed < total) {
         bool progress = false;
         for (int s = 1; s <= S; ++s) {
@@ -87,6 +97,7 @@ bool build_slots(int S, int M, std::vector<uint32_t> *masks, uint32_t *nslots) {
                 if (kind == 0) { startF[at(s, m)] = st; finF[at(s, m)] = st + 1; }
                 else { startB[at(s, m)] = st; finB[at(s, m)] = st + 1; }
                 slot_of_last[s] = st + 1;
+                n = std::max(n, st + 1);
                 ++pos[s];
                 ++placed;
                 progress = true;
@@ -94,9 +105,7 @@ bool build_slots(int S, int M, std::vector<uint32_t> *masks, uint32_t *nslots) {
         }
         if (!progress) return false;
     }
-    const int n = 2 * (M + S - 1);
-    std::vector<uint32_t> fm(n, 0), bm(n, 0);
-    // newest node per stage per slot: kind*2^20 + m
+    std::vector<uint32_t> fm(n, 0), fd(n, 0), bm(n, 0);
     for (int s = 1; s <= S; ++s)
         for (int m = 1; m <= M; ++m) {
             const int a = startF[at(s, m)], b = startB[at(s, m)];
@@ -106,28 +115,33 @@ bool build_slots(int S, int M, std::vector<uint32_t> *masks, uint32_t *nslots) {
             if ((fm[b] | bm[b]) >> (s - 1) & 1u) return false;
             bm[b] |= 1u << (s - 1);
         }
-    // stencil property: the input of F_{s,m} (F_{s-1,m}) must be the newest
-    // node of stage s-1 at slot start(F_{s,m}) - 1, likewise for B.
+    // inputs: F_{s,m} reads F_{s-1,m}; B_{s,m} reads B_{s+1,m}
     for (int s = 1; s <= S; ++s) {
-        int k = 0;
         for (const auto &node : ord[s]) {
-            (void)k;
             const int kind = node.first, m = node.second;
             const int st = kind == 0 ? startF[at(s, m)] : startB[at(s, m)];
-            int u = kind == 0 ? s - 1 : s + 1;
+            const int u = kind == 0 ? s - 1 : s + 1;
             if (u < 1 || u > S) continue;
             const int ust = kind == 0 ? startF[at(u, m)] : startB[at(u, m)];
             if (ust >= st) return false;
-            // no node of stage u may start in (ust, st)
-            for (int q = ust + 1; q < st; ++q)
-                if ((fm[q] | bm[q]) >> (u - 1) & 1u) return false;
+            int newer_same = 0, newer_any = 0;
+            for (int q = ust + 1; q < st; ++q) {
+                const bool f = (fm[q] >> (u - 1)) & 1u, b = (bm[q] >> (u - 1)) & 1u;
+                newer_any += f || b;
+                newer_same += kind == 0 ? f : b;
+            }
+            if (newest_only && newer_any) return false;
+            if (kind == 1 && newer_same) return false;
+            if (kind == 0 && newer_same > 1) return false;
+            if (kind == 0 && newer_same == 1) fd[st] |= 1u << (s - 1);
         }
     }
     if (masks) {
-        masks->assign(2 * (size_t)n, 0);
+        masks->assign(3 * (size_t)n, 0);
         for (int k = 0; k < n; ++k) {
-            (*masks)[2 * k] = fm[k];
-            (*masks)[2 * k + 1] = bm[k];
+            (*masks)[3 * k] = fm[k];
+            (*masks)[3 * k + 1] = fd[k];
+            (*masks)[3 * k + 2] = bm[k];
         }
     }
     *nslots = (uint32_t)n;
@@ -144,7 +158,7 @@ bool closed_form_matches(int S, int M, const std::vector<uint32_t> &masks) {
             if (k < 2 * S - 1) op = pk::prologue_op(S, s, k);
             else if (k <= 2 * M - 1) op = ((k - s - 1) & 1) == 0 ? 1 : 2;
             else op = pk::epilogue_op(S, s, k - 2 * M);
-            const int f = (masks[2 * k] >> (s - 1)) & 1u, b = (masks[2 * k + 1] >> (s - 1)) & 1u;
+            const int f = (masks[3 * k] >> (s - 1)) & 1u, b = (masks[3 * k + 2] >> (s - 1)) & 1u;
             const int sim = f ? 1 : (b ? 2 : 0);
             if (sim != op) return false;
         }
@@ -190,6 +204,7 @@ int poseidon_validate(const poseidon_problem *p, uint64_t *n_candidates) {
         return POSEIDON_E_INVAL;
     if (!p->fwd_us || !p->bwd_us || !p->mem_mb || !p->cap_mb) return POSEIDON_E_INVAL;
     if (p->S > 1 && (!p->comm_fwd_us || !p->comm_bwd_us)) return POSEIDON_E_INVAL;
+    if (p->schedule != POSEIDON_SCHEDULE_1F1B && p->schedule != POSEIDON_SCHEDULE_EAGER_1F1B) return POSEIDON_E_INVAL;
     uint64_t A;
     if (p->assign) {
         if (p->A < 1 || p->A > (1ull << 32)) return p->A < 1 ? POSEIDON_E_INVAL : POSEIDON_E_RANGE;
@@ -246,9 +261,13 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     // schedule of the DAG: closed form for M >= S (self-checked), table otherwise
     std::vector<uint32_t> masks;
     uint32_t nslots = 0;
-    const bool table_path = M < S;
+    // 1F1B with M >= S: the closed form the fast kernel path hard-codes
+    // (self-checked against the simulated schedule); otherwise a slot table
+    const uint32_t sched = p->schedule;
+    const bool table_path = sched != POSEIDON_SCHEDULE_1F1B || M < S;
     if (table_path || (uint64_t)S * M <= 4096) {
-        if (!build_slots((int)S, (int)M, &masks, &nslots)) return POSEIDON_E_INVAL;
+        if (!build_slots((int)S, (int)M, (int)sched, sched == POSEIDON_SCHEDULE_1F1B, &masks, &nslots))
+            return POSEIDON_E_INVAL;
         if (!table_path && !closed_form_matches((int)S, (int)M, masks)) return POSEIDON_E_INVAL;
     }
 
@@ -290,9 +309,10 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     kp.wide = wide;
     for (uint32_t b = 0; b + 1 < S; ++b) { kp.cf[b] = p->comm_fwd_us[b]; kp.cb[b] = p->comm_bwd_us[b]; }
     kp.has_ar = has_ar;
+    kp.sched = sched;
     for (uint32_t s = 1; s < S; ++s) kp.psi[s] = kp.psi[s - 1] + kp.cf[s - 1];
     // cascade checkpoints of the steady loop: K0, 2 K0, 4 K0, ... below M - S
-    if (M >= S) {
+    if (M >= S && p->schedule == POSEIDON_SCHEDULE_1F1B) {
         const uint32_t nit = M - S;
         uint32_t k = std::max<uint32_t>(2, PK_CASCADE_K0);
         while (k < nit && kp.nlevels < (uint32_t)pk::kMaxLevels) {
@@ -370,7 +390,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         if (lds > 64 * 1024) { status = POSEIDON_E_RANGE; break; }
         int occ = 0;
         hipDeviceProp_t prop;
-        if (pk::eval_occupancy(S, wide, lds, has_ar, &occ) != hipSuccess || hipGetDeviceProperties(&prop, hip_device) != hipSuccess) {
+        if (pk::eval_occupancy(S, wide, lds, has_ar, sched != POSEIDON_SCHEDULE_1F1B, &occ) != hipSuccess || hipGetDeviceProperties(&prop, hip_device) != hipSuccess) {
             status = POSEIDON_E_DEVICE;
             break;
         }

@@ -15,8 +15,8 @@ namespace pk {
                                                        uint64_t, uint32_t, uint32_t);                          \
     template hipError_t launch_bounded_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t, uint64_t, \
                                                        uint64_t, uint32_t, uint32_t);                          \
-    template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool);                                        \
-    template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool);
+    template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool, bool);                                        \
+    template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool, bool);
 
 PK_INST(1) PK_INST(2) PK_INST(3) PK_INST(4) PK_INST(5) PK_INST(6) PK_INST(7) PK_INST(8)
 

@@ -15,8 +15,8 @@ namespace pk {
                                                        uint64_t, uint32_t, uint32_t);                          \
     template hipError_t launch_bounded_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t, uint64_t, \
                                                        uint64_t, uint32_t, uint32_t);                          \
-    template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool);                                        \
-    template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool);
+    template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool, bool);                                        \
+    template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool, bool);
 
 PK_INST(9) PK_INST(10) PK_INST(11) PK_INST(12)
 

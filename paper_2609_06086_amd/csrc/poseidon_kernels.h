@@ -334,14 +334,15 @@ __device__ __forceinline__ bool dp_advance(uint32_t (&Y)[S], const uint32_t (&F)
     return ok;
 }
 
-// Any M (used when M < S): the slot schedule comes from a table of
-// per-slot forward / backward stage masks built on the host.
+// 1F1B with M < S: the slot schedule comes from a table of per-slot
+// forward / backward stage masks built on the host (the host checks that
+// every input is still its stage's newest node, so one register suffices).
 template <int S>
 __device__ __forceinline__ void dp_table(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
                                          const Comm<S> &c, uint32_t (&Y)[S]) {
     dp_init<S>(Y, c);
     for (uint32_t k = 0; k < p.nslots; ++k) {
-        const uint32_t fm = p.slot_mask[2 * k], bm = p.slot_mask[2 * k + 1];
+        const uint32_t fm = p.slot_mask[3 * k], bm = p.slot_mask[3 * k + 2];
         uint32_t N[S];
 #pragma unroll
         for (int s = 0; s < S; ++s) {
@@ -353,11 +354,48 @@ __device__ __forceinline__ void dp_table(const KParams &p, const uint32_t (&F)[S
     }
 }
 
-// registers after the whole DP (any M)
+// Any schedule table (Eager 1F1B, Sec. 4.1.4 / App. B.1).  A stage can
+// run ahead of its downstream neighbour by more than one forward pass, so
+// a forward node may need the upstream stage's second-newest forward; the
+// host marks those nodes in a third mask.  Per stage the registers are the
+// newest node of either kind (Y), the newest and previous forward (Fn, Fp)
+// and the newest backward (Bn), all shifted by the stage's potential.
+template <int S>
+__device__ __forceinline__ void dp_sched(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                         const Comm<S> &c, uint32_t (&Y)[S]) {
+    uint32_t Fn[S], Fp[S], Bn[S];
+    dp_init<S>(Y, c);
+#pragma unroll
+    for (int s = 0; s < S; ++s) { Fn[s] = 0; Fp[s] = 0; Bn[s] = 0; }
+    for (uint32_t k = 0; k < p.nslots; ++k) {
+        const uint32_t fm = p.slot_mask[3 * k], fd = p.slot_mask[3 * k + 1], bm = p.slot_mask[3 * k + 2];
+        uint32_t N[S];
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            if ((fm >> s) & 1u) {
+                const uint32_t in = s == 0 ? 0u : (((fd >> s) & 1u) ? Fp[s > 0 ? s - 1 : 0] : Fn[s > 0 ? s - 1 : 0]);
+                N[s] = F[s] + max(Y[s], in);
+            } else if ((bm >> s) & 1u) {
+                N[s] = B[s] + (s < S - 1 ? max(Y[s], Bn[s < S - 1 ? s + 1 : 0] + c.e[s < S - 1 ? s : 0]) : Y[s]);
+            } else {
+                N[s] = Y[s];
+            }
+        }
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            if ((fm >> s) & 1u) { Fp[s] = Fn[s]; Fn[s] = N[s]; }
+            if ((bm >> s) & 1u) Bn[s] = N[s];
+            Y[s] = N[s];
+        }
+    }
+}
+
+// registers after the whole DP (any M, any schedule)
 template <int S>
 __device__ __forceinline__ void dp_full(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
                                         const Comm<S> &c, uint32_t (&Y)[S]) {
-    if (p.M >= (uint32_t)S) dp_1f1b<S>(p.M, F, B, c, Y);
+    if (p.sched) dp_sched<S>(p, F, B, c, Y);
+    else if (p.M >= (uint32_t)S) dp_1f1b<S>(p.M, F, B, c, Y);
     else dp_table<S>(p, F, B, c, Y);
 }
 
@@ -679,6 +717,47 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
     block_min_and_finish(best, p.acc, p.done, p.result, nullptr, p.nlevels == 0, p.accumulate);
 }
 
+// Schedules other than 1F1B: the same pass as eval_kernel with the
+// schedule-table DP and no cascade.
+template <int S, typename R, bool AR>
+__global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const Lds<R> tab = stage_tables<R>(p, smem);
+    const Comm<S> comm = load_comm<S>(p);
+    constexpr int NW = Codes<S>::kWords;
+    unsigned long long best = ~0ull;
+    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    const uint64_t span = (p.n_i + stride - 1) / stride;
+    uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+    for (uint64_t it = 0; it < span; ++it, i += stride) {
+        const bool active = i < p.n_i;
+        const uint64_t gi = p.first_i + i;
+        uint32_t w[NW];
+#pragma unroll
+        for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[(uint64_t)k * p.ccap + i] : 0u;
+        uint32_t cut[S + 1], ty[S], F[S], B[S], Y[S];
+        const bool ok = unpack_cuts<S>(w, p.L, cut);
+        const uint32_t a = ok ? assign_of(p, gi) : 0u;
+        decode_types<S>(p, a, ty);
+        const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B) && ok && active;
+        dp_sched<S>(p, F, B, comm, Y);
+        uint32_t T = end_time<S, R, AR>(p, tab, Y, comm, w, a);
+        if (!ok) T = 0xFFFFFFFFu;
+        if (active && p.makespan_out) p.makespan_out[gi] = T;
+        if (p.feas_bits_out) {
+            const unsigned long long bits = __ballot(feas);
+            const uint64_t w0 = (gi - (threadIdx.x & 63)) >> 5;
+            if ((threadIdx.x & 63) == 0 && w0 < p.nwords) p.feas_bits_out[w0] = (uint32_t)bits;
+            if ((threadIdx.x & 63) == 32 && w0 + 1 < p.nwords) p.feas_bits_out[w0 + 1] = (uint32_t)(bits >> 32);
+        }
+        if (active) {
+            const unsigned long long key = make_key(feas, T, (uint32_t)gi);
+            best = key < best ? key : best;
+        }
+    }
+    block_min_and_finish(best, p.acc, p.done, p.result, nullptr, true, p.accumulate);
+}
+
 // Level `lvl` of the cascade: resume the queued lanes from iteration
 // p.lvl_k[lvl-1] to p.lvl_k[lvl] (the end at the last level).
 template <int S, typename R, bool AR>
@@ -818,6 +897,11 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
 // ---------------------------------------------------------------------------
 template <int S, typename R>
 hipError_t launch_eval_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
+    if (p.sched) {
+        if (p.has_ar) hipLaunchKernelGGL((sched_kernel<S, R, true>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
+        else hipLaunchKernelGGL((sched_kernel<S, R, false>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
+        return hipGetLastError();
+    }
     if (p.has_ar) hipLaunchKernelGGL((eval_kernel<S, R, true>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
     else hipLaunchKernelGGL((eval_kernel<S, R, false>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
     return hipGetLastError();
@@ -851,7 +935,9 @@ hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t s
 }
 
 template <int S, typename R>
-hipError_t occupancy_s(int *blocks, size_t lds, bool ar) {
+hipError_t occupancy_s(int *blocks, size_t lds, bool ar, bool sched) {
+    if (sched && ar) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, sched_kernel<S, R, true>, kBlock, lds);
+    if (sched) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, sched_kernel<S, R, false>, kBlock, lds);
     if (ar) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, eval_kernel<S, R, true>, kBlock, lds);
     return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, eval_kernel<S, R, false>, kBlock, lds);
 }

@@ -24,6 +24,7 @@ POSEIDON_E_INVAL = -1
 POSEIDON_E_RANGE = -2
 POSEIDON_E_DEVICE = -3
 POSEIDON_E_NOMEM = -4
+SCHEDULE_1F1B, SCHEDULE_EAGER_1F1B = 0, 1
 S_MAX, L_MAX, T_MAX = 16, 256, 8
 
 
@@ -38,7 +39,8 @@ class _Problem(C.Structure):
                 ("fwd_us", C.c_void_p), ("bwd_us", C.c_void_p),
                 ("comm_fwd_us", C.c_void_p), ("comm_bwd_us", C.c_void_p),
                 ("mem_mb", C.c_void_p), ("cap_mb", C.c_void_p),
-                ("assign", C.c_void_p), ("A", C.c_uint64), ("allreduce_us", C.c_void_p)]
+                ("assign", C.c_void_p), ("A", C.c_uint64), ("allreduce_us", C.c_void_p),
+                ("schedule", C.c_uint32)]
 
 
 class _Cands(C.Structure):
@@ -144,7 +146,8 @@ def _problem_struct(prob):
                   host(prob.mem, np.uint32), host(prob.cap, np.uint32),
                   host(prob.assign, np.uint8),
                   int(prob.assign.shape[0]) if prob.assign is not None else 0,
-                  host(getattr(prob, "allreduce", None), np.uint32))
+                  host(getattr(prob, "allreduce", None), np.uint32),
+                  int(getattr(prob, "schedule", 0)))
     return st, keep
 
 

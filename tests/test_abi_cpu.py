@@ -80,6 +80,11 @@ def test_validation_errors():
     # L above the maximum
     p = W.random_problem(rng, 300, 4, 4, 1)
     assert _status(p) == P.POSEIDON_E_INVAL
+    # unknown schedule
+    p = _small(); p.schedule = 2
+    assert _status(p) == P.POSEIDON_E_INVAL
+    p = _small(); p.schedule = P.SCHEDULE_EAGER_1F1B
+    assert P.poseidon_validate(p) > 0
 
 
 def test_overflow_guard():

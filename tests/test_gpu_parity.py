@@ -477,3 +477,73 @@ def test_full_workload6_matches_golden(dev):
         assert (b.index, b.makespan) == (exp["best_index"], exp["best_makespan"])
         assert (st.evaluated, st.pruned, st.infeasible) == (exp["evaluated"], exp["pruned"], exp["infeasible"])
     ctx.close()
+
+
+# ---------------------------------------------------------- Eager 1F1B
+
+def test_eager_random_problems(dev):
+    """Schedule-table DP (newest / previous forward, newest backward per
+    stage) against the oracle's Eager 1F1B DAG, S = 1..16, any M."""
+    rng = np.random.default_rng(111)
+    for trial in range(48):
+        S = trial % 16 + 1
+        M = int(rng.integers(1, 3 * S + 24))
+        L = S + int(rng.integers(0, 10))
+        T = int(rng.integers(1, 4))
+        prob = W.random_problem(rng, L, S, M, T, cost_hi=400, mem_hi=30, cap=int(rng.integers(30, 200)),
+                                assign_rows=None if T ** S < 5000 else 5)
+        prob.schedule = P.SCHEDULE_EAGER_1F1B
+        if trial % 3 == 0:
+            _with_allreduce(rng, prob, hi=int(rng.integers(1, 400)) * M)
+        check_against_oracle(prob, W.random_candidates(rng, prob, int(rng.integers(1, 1500))), dev)
+
+
+def test_eager_python_oracle_and_bounded(dev):
+    rng = np.random.default_rng(112)
+    for trial in range(8):
+        S = int(rng.integers(1, 5))
+        L = S + int(rng.integers(0, 5))
+        M = int(rng.integers(1, 9))
+        prob = W.random_problem(rng, L, S, M, 2, mem_hi=30, cap=int(rng.integers(30, 120)))
+        prob.schedule = P.SCHEDULE_EAGER_1F1B
+        if trial % 2:
+            _with_allreduce(rng, prob, hi=1500)
+        full = W.Candidates(first=0, count=prob.n_candidates)
+        check_against_oracle(prob, full, dev, python_oracle=True)
+        To, fo = coracle.evaluate(prob, full)
+        ex = coracle.argmin(To, fo)
+        if ex is not None:
+            for chunk in (0, 7):
+                b, _ = bounded_vs_oracle(prob, full, int(To[fo].max()), chunk, dev)
+                assert (b.index, b.makespan) == ex
+
+
+def test_eager_workload4_prefix_and_bounded(dev):
+    """The 8-stage, 64-micro-batch, 3-type workload under Eager 1F1B."""
+    wl = W.workload(4)
+    prob = wl.problem
+    prob.schedule = P.SCHEDULE_EAGER_1F1B
+    n = 400_003
+    c = W.Candidates(comp_rank=wl.cands.comp_rank[:n].copy(), assign_idx=wl.cands.assign_idx[:n].copy())
+    check_against_oracle(prob, c, dev)
+    To, fo = coracle.evaluate(prob, W.Candidates(comp_rank=c.comp_rank[:500], assign_idx=c.assign_idx[:500]))
+    bound = coracle.argmin(To, fo)[1]
+    for chunk in (0, 100_000):
+        b, st = bounded_vs_oracle(prob, c, bound, chunk, dev)
+        assert st.pruned > 0
+
+
+def test_eager_differs_from_1f1b(dev):
+    """The schedule field reaches the kernels: same candidates, other makespans."""
+    wl = W.workload(2)
+    prob = wl.problem
+    c0 = P.poseidon_load_costs(prob, 0)
+    T0, _, _ = gpu_eval(c0, wl.cands, dev)
+    prob.schedule = P.SCHEDULE_EAGER_1F1B
+    c1 = P.poseidon_load_costs(prob, 0)
+    T1, _, _ = gpu_eval(c1, wl.cands, dev)
+    assert (T0 != T1).any()
+    To, _ = coracle.evaluate(prob, wl.cands)
+    assert np.array_equal(T1, To)
+    c0.close()
+    c1.close()

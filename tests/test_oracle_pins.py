@@ -605,3 +605,15 @@ def test_eager_same_uniform_closed_form_and_dag_shape():
             assert c["compute_nodes"] == 2 * S * M and c["intra"] == S * (2 * M - 1)
             assert dag.longest_path(dag.dag_for(S, M, 1), [3] * S, [5] * S, [0] * (S - 1), [0] * (S - 1)) == \
                 (M + S - 1) * 8
+
+
+def test_eq2_lower_bound_holds_under_eager():
+    """Eq. 2 only uses that a stage runs its 2M nodes one after another, so it
+    bounds the Eager 1F1B critical path too (with and without R_s)."""
+    rng = np.random.default_rng(24)
+    for trial in range(300):
+        S, M = int(rng.integers(1, 7)), int(rng.integers(1, 12))
+        F, B, cf, cb = _rand_case(rng, S, M)
+        d = list(rng.integers(0, 500, S)) if trial % 2 else None
+        T = dag.longest_path(dag.dag_for(S, M, 1), F, B, cf, cb, d)
+        assert dag.eq2_bound(list(F), list(B), M, d) <= T
