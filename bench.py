@@ -3,7 +3,8 @@
 One step = one pass of the whole hot path over the workload's candidate
 list: decode every (composition rank, assignment) pair, build the stage
 weights from the LDS prefix tables, check the memory caps, take the longest
-path of the 1F1B DAG, write every makespan and the packed feasibility bits,
+path of the pipeline DAG (1F1B, or Eager 1F1B with --schedule eager),
+write every makespan and the packed feasibility bits,
 and min-reduce to the best feasible candidate.  Inputs are resident in HBM
 before timing starts.
 
@@ -83,6 +84,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-early-stop", action="store_true")
+    ap.add_argument("--schedule", default="1f1b", choices=["1f1b", "eager"],
+                    help="pipeline schedule of the DAG (1F1B or Eager 1F1B)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (for counter scaling)")
     args = ap.parse_args()
@@ -100,6 +103,7 @@ def main():
     dev = torch.device("cuda:0")
     wl = W.workload(args.workload)
     prob = wl.problem
+    prob.schedule = P.SCHEDULE_EAGER_1F1B if args.schedule == "eager" else P.SCHEDULE_1F1B
     n = len(wl.cands)
     ctx = P.poseidon_load_costs(prob, 0)
     if wl.cands.is_list:
@@ -144,7 +148,7 @@ def main():
     S, M = prob.S, prob.M
     ops = n * dp_ops(S, M)
     achieved = ops / (k_avg * 1e-3) / 1e12
-    ctr = committed_counters() if args.workload == 5 else None
+    ctr = committed_counters() if args.workload == 5 and args.schedule == "1f1b" else None
     nodes_per_s = n * 2 * S * M / (ms_per_step * 1e-3)
     value = n / (ms_per_step * 1e-3)
     algo_bytes = n * in_bytes + n * 4 + ((n + 31) // 32) * 4
@@ -185,6 +189,7 @@ def main():
         "data": "synthetic (seeded per-layer profile tables and sampled candidates)",
         "config": {"workload": f"L={prob.L} S={S} M={M} T={prob.T}, {n} sampled compositions, fixed 4x4 "
                                f"stage-type permutation" if args.workload == 5 else wl.description,
+                   "schedule": "Eager 1F1B" if args.schedule == "eager" else "1F1B",
                    "candidates_per_step": n, "dag_nodes_per_candidate": 2 * S * M,
                    "parallelism": "single GPU"},
         "dag_nodes_per_s": nodes_per_s,

@@ -104,6 +104,11 @@ hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, 
 
 int code_words(int S) { return S > 1 ? (S - 1 + 3) / 4 : 1; }
 int prologue_op(int S, int s, int k) { return pro_op(S, s, k); }
+int eager_op(int S, int M, int s, int k) {
+    if (k <= 2 * S - 2) return eager_pro_op(S, s, k);
+    if (k <= 2 * M - 2 * S) return eager_steady_op(s, k & 1);
+    return eager_epi_op(S, s, k - (2 * M - 2 * S + 1));
+}
 int epilogue_op(int S, int s, int j) { return epi_op(S, s, j); }
 
 }  // namespace pk

@@ -166,6 +166,21 @@ bool closed_form_matches(int S, int M, const std::vector<uint32_t> &masks) {
     return true;
 }
 
+// The Eager 1F1B closed form (M >= 2S-1), including which forwards read
+// the upstream stage's previous forward, checked against the simulation.
+bool eager_closed_form_matches(int S, int M, const std::vector<uint32_t> &masks) {
+    const int n = 2 * (M + S - 1);
+    if (masks.size() != 3 * (size_t)n) return false;
+    for (int k = 0; k < n; ++k)
+        for (int s = 1; s <= S; ++s) {
+            const int f = (masks[3 * k] >> (s - 1)) & 1u, d = (masks[3 * k + 1] >> (s - 1)) & 1u,
+                      b = (masks[3 * k + 2] >> (s - 1)) & 1u;
+            const int sim = f ? (d ? 3 : 1) : (b ? 2 : 0);
+            if (sim != pk::eager_op(S, M, s, k)) return false;
+        }
+    return true;
+}
+
 }  // namespace
 
 struct poseidon_ctx {
@@ -258,17 +273,19 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     const bool wide = n_comp > 0xFFFFFFFFull;
     const uint32_t NB = pk::kNB;   // Pascal-table column length (L <= kNB)
 
-    // schedule of the DAG: closed form for M >= S (self-checked), table otherwise
+    // schedule of the DAG: 1F1B with M >= S and Eager 1F1B with M >= 2S-1
+    // run the closed forms the kernels hard-code (self-checked against the
+    // simulated schedule here); other cases run a slot table
     std::vector<uint32_t> masks;
     uint32_t nslots = 0;
-    // 1F1B with M >= S: the closed form the fast kernel path hard-codes
-    // (self-checked against the simulated schedule); otherwise a slot table
     const uint32_t sched = p->schedule;
-    const bool table_path = sched != POSEIDON_SCHEDULE_1F1B || M < S;
+    const bool eager = sched == POSEIDON_SCHEDULE_EAGER_1F1B;
+    const bool table_path = eager ? M + 1 < 2 * S : M < S;
     if (table_path || (uint64_t)S * M <= 4096) {
-        if (!build_slots((int)S, (int)M, (int)sched, sched == POSEIDON_SCHEDULE_1F1B, &masks, &nslots))
+        if (!build_slots((int)S, (int)M, (int)sched, !eager, &masks, &nslots)) return POSEIDON_E_INVAL;
+        if (!table_path && !(eager ? eager_closed_form_matches((int)S, (int)M, masks)
+                                   : closed_form_matches((int)S, (int)M, masks)))
             return POSEIDON_E_INVAL;
-        if (!table_path && !closed_form_matches((int)S, (int)M, masks)) return POSEIDON_E_INVAL;
     }
 
     // host images of the device tables

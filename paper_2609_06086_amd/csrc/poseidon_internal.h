@@ -80,6 +80,7 @@ hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count
 hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, hipStream_t st);
 int code_words(int S);
 int prologue_op(int S, int s, int k);
+int eager_op(int S, int M, int s, int k);   // Eager 1F1B closed form, M >= 2S-1: 0 idle, 1 F, 2 B, 3 F of depth 2
 int epilogue_op(int S, int s, int j);
 
 }  // namespace pk

@@ -15,6 +15,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 #include "poseidon_internal.h"
 
 namespace pk {
@@ -26,7 +28,6 @@ constexpr int kTile = 4096;            // candidates filtered per block (early s
 // ---------------------------------------------------------------------------
 // LDS image of the context's tables (one copy per block)
 // ---------------------------------------------------------------------------
-template <typename R>
 struct Lds {
     const uint64_t *cost;   // [T][L+1]  (prefix bwd << 32) | prefix fwd
     const uint32_t *pm;     // [L+1]     prefix memory
@@ -35,8 +36,7 @@ struct Lds {
 };
 
 // Layout: cost (8-byte entries) | pm | cap | pd.
-template <typename R>
-__device__ __forceinline__ Lds<R> stage_tables(const KParams &p, unsigned char *smem) {
+__device__ __forceinline__ Lds stage_tables(const KParams &p, unsigned char *smem) {
     uint64_t *cost = reinterpret_cast<uint64_t *>(smem);
     const uint32_t ncost = p.T * (p.L + 1);
     uint32_t *pm = reinterpret_cast<uint32_t *>(cost + ncost);
@@ -48,7 +48,7 @@ __device__ __forceinline__ Lds<R> stage_tables(const KParams &p, unsigned char *
     if (p.has_ar)
         for (uint32_t i = threadIdx.x; i < ncost; i += kBlock) pd[i] = p.pd[i];
     __syncthreads();
-    return Lds<R>{cost, pm, cap, pd};
+    return Lds{cost, pm, cap, pd};
 }
 
 // ---------------------------------------------------------------------------
@@ -148,8 +148,8 @@ __device__ __forceinline__ uint32_t assign_of(const KParams &p, uint64_t i) {
 // ---------------------------------------------------------------------------
 // (a2) stage weights and memory feasibility
 // ---------------------------------------------------------------------------
-template <int S, typename R>
-__device__ __forceinline__ bool stage_weights(const KParams &p, const Lds<R> &t,
+template <int S>
+__device__ __forceinline__ bool stage_weights(const KParams &p, const Lds &t,
                                               const uint32_t (&cut)[S + 1], const uint32_t (&ty)[S],
                                               uint32_t (&F)[S], uint32_t (&B)[S]) {
     bool feas = true;
@@ -390,11 +390,122 @@ __device__ __forceinline__ void dp_sched(const KParams &p, const uint32_t (&F)[S
     }
 }
 
-// registers after the whole DP (any M, any schedule)
+// ---------------------------------------------------------------------------
+// Eager 1F1B in closed form (M >= 2S-1).  Under unit weights, stage s
+// (1-based) runs its 2(S-s)+1 warm-up forwards in slots s-1 .. 2S-s-1;
+// from slot 2S-s on it runs a backward in every slot with k + s even and a
+// forward in the others, up to its last forward in slot 2M-2S+3s-3; then
+// backwards in the slots with k + s even up to 2M+2S-s-2.  That is
+// 2(M+S-1) slots: a prologue of 2S-1 slots, M-2S+1 steady pairs of slots
+// (2S-1+2i, 2S+2i) and an epilogue of 4S-3 slots.  A forward in the
+// alternating part reads the upstream stage's previous forward (kFwdDeep),
+// except the stage's last one, which reads the upstream's newest; a
+// backward always reads the downstream stage's newest node.
+// ---------------------------------------------------------------------------
+constexpr int kFwdDeep = 3;
+
+// prologue slot k (0 .. 2S-2), 1-based stage s
+__host__ __device__ constexpr int eager_pro_op(int S, int s, int k) {
+    return k < s - 1 ? kIdle : k <= 2 * S - s - 1 ? kFwd : (((k + s) & 1) == 0 ? kBwd : kFwdDeep);
+}
+// steady slot of parity `odd` (slot 2S-1+2i is odd)
+__host__ __device__ constexpr int eager_steady_op(int s, int odd) {
+    return odd ? ((s & 1) ? kBwd : kFwdDeep) : ((s & 1) ? (s == 1 ? kFwd : kFwdDeep) : kBwd);
+}
+// epilogue slot 2M-2S+1+j (j = 0 .. 4S-4)
+__host__ __device__ constexpr int eager_epi_op(int S, int s, int j) {
+    return j <= 3 * s - 4 ? (((j + 1 + s) & 1) == 0 ? kBwd : (j < 3 * s - 4 ? kFwdDeep : kFwd))
+         : (j <= 4 * S - s - 3 && ((j + 1 + s) & 1) == 0) ? kBwd
+         : kIdle;
+}
+
+// phase of a slot: prologue slot K, steady odd / even slot, epilogue slot K
+enum EagerPhase { kPro = 0, kOdd = 1, kEven = 2, kEpi = 3 };
+
+template <int S, int PH, int K>
+__host__ __device__ constexpr int eager_op_at(int s) {
+    return PH == kPro ? eager_pro_op(S, s, K)
+         : PH == kOdd ? eager_steady_op(s, 1)
+         : PH == kEven ? eager_steady_op(s, 0)
+         : eager_epi_op(S, s, K);
+}
+
+// node of 0-based stage s with a compile-time op
+template <int S, int OP, int s>
+__device__ __forceinline__ uint32_t eager_node(const uint32_t (&Y)[S], const uint32_t (&Fn)[S],
+                                               const uint32_t (&Fp)[S], const uint32_t (&F)[S],
+                                               const uint32_t (&B)[S], const Comm<S> &c) {
+    constexpr int u = s > 0 ? s - 1 : 0, d = s < S - 1 ? s + 1 : 0;
+    if constexpr (OP == kFwd) return F[s] + (s > 0 ? max(Y[s], Fn[u]) : Y[s]);
+    else if constexpr (OP == kFwdDeep) return F[s] + (s > 0 ? max(Y[s], Fp[u]) : Y[s]);
+    else if constexpr (OP == kBwd) return B[s] + (s < S - 1 ? max(Y[s], Y[d] + c.e[d > 0 ? d - 1 : 0]) : Y[s]);
+    else return Y[s];
+}
+
+template <int OP>
+__device__ __forceinline__ void eager_store(uint32_t n, uint32_t &y, uint32_t &fn, uint32_t &fp) {
+    if constexpr (OP == kFwd || OP == kFwdDeep) { fp = fn; fn = n; }
+    y = n;
+}
+
+// one slot, every stage's op fixed at compile time (synchronous update)
+template <int S, int PH, int K, int... I>
+__device__ __forceinline__ void eager_slot(std::integer_sequence<int, I...>, uint32_t (&Y)[S], uint32_t (&Fn)[S],
+                                           uint32_t (&Fp)[S], const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                           const Comm<S> &c) {
+    uint32_t N[S];
+    ((N[I] = eager_node<S, eager_op_at<S, PH, K>(I + 1), I>(Y, Fn, Fp, F, B, c)), ...);
+    (eager_store<eager_op_at<S, PH, K>(I + 1)>(N[I], Y[I], Fn[I], Fp[I]), ...);
+}
+
+// the slots K... of a phase, in order
+template <int S, int PH, int... K>
+__device__ __forceinline__ void eager_run(std::integer_sequence<int, K...>, uint32_t (&Y)[S], uint32_t (&Fn)[S],
+                                          uint32_t (&Fp)[S], const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                          const Comm<S> &c) {
+    (eager_slot<S, PH, K>(std::make_integer_sequence<int, S>{}, Y, Fn, Fp, F, B, c), ...);
+}
+
 template <int S>
+__device__ __forceinline__ void eager_pair(uint32_t (&Y)[S], uint32_t (&Fn)[S], uint32_t (&Fp)[S],
+                                           const uint32_t (&F)[S], const uint32_t (&B)[S], const Comm<S> &c) {
+    eager_slot<S, kOdd, 0>(std::make_integer_sequence<int, S>{}, Y, Fn, Fp, F, B, c);
+    eager_slot<S, kEven, 0>(std::make_integer_sequence<int, S>{}, Y, Fn, Fp, F, B, c);
+}
+
+template <int S>
+__device__ __forceinline__ void dp_eager(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                         const Comm<S> &c, uint32_t (&Y)[S]) {
+    uint32_t Fn[S], Fp[S];
+    dp_init<S>(Y, c);
+#pragma unroll
+    for (int s = 0; s < S; ++s) { Fn[s] = 0; Fp[s] = 0; }
+    eager_run<S, kPro>(std::make_integer_sequence<int, 2 * S - 1>{}, Y, Fn, Fp, F, B, c);
+    // two pairs per trip, so that the forward registers come back to the
+    // same roles at the loop edge
+    const uint32_t npairs = M - 2 * S + 1;
+    for (uint32_t i = 1; i < npairs; i += 2) {
+        eager_pair<S>(Y, Fn, Fp, F, B, c);
+        eager_pair<S>(Y, Fn, Fp, F, B, c);
+    }
+    if (npairs & 1u) eager_pair<S>(Y, Fn, Fp, F, B, c);
+    eager_run<S, kEpi>(std::make_integer_sequence<int, 4 * S - 3>{}, Y, Fn, Fp, F, B, c);
+}
+
+// schedules other than 1F1B: the slot table (TAB) or the closed form
+template <int S, bool TAB>
+__device__ __forceinline__ void dp_other(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                         const Comm<S> &c, uint32_t (&Y)[S]) {
+    if (TAB) dp_sched<S>(p, F, B, c, Y);
+    else dp_eager<S>(p.M, F, B, c, Y);
+}
+
+// registers after the whole DP (any M); SCH = the problem is not 1F1B
+template <int S, bool SCH>
 __device__ __forceinline__ void dp_full(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
                                         const Comm<S> &c, uint32_t (&Y)[S]) {
-    if (p.sched) dp_sched<S>(p, F, B, c, Y);
+    if (SCH && p.nslots) dp_sched<S>(p, F, B, c, Y);
+    else if (SCH) dp_eager<S>(p.M, F, B, c, Y);
     else if (p.M >= (uint32_t)S) dp_1f1b<S>(p.M, F, B, c, Y);
     else dp_table<S>(p, F, B, c, Y);
 }
@@ -434,8 +545,8 @@ __device__ __forceinline__ uint32_t eq2_bound(uint32_t M, const uint32_t (&F)[S]
 // R_s follows B_{s,M} with the stage's summed per-layer all-reduce time
 // (Sec. 4.1.3).  Without all-reduce times T = finish(B_{1,M}).
 // ---------------------------------------------------------------------------
-template <int S, typename R>
-__device__ __forceinline__ void stage_allreduce(const KParams &p, const Lds<R> &t, const uint32_t (&cut)[S + 1],
+template <int S>
+__device__ __forceinline__ void stage_allreduce(const KParams &p, const Lds &t, const uint32_t (&cut)[S + 1],
                                                 const uint32_t (&ty)[S], uint32_t (&D)[S]) {
     const uint32_t row = p.L + 1;
 #pragma unroll
@@ -444,14 +555,14 @@ __device__ __forceinline__ void stage_allreduce(const KParams &p, const Lds<R> &
 
 // T from the registers after the epilogue; with all-reduce times the
 // stage's cut codes `w` and assignment `a` give R_s
-template <int S, typename R, bool AR>
-__device__ __forceinline__ uint32_t end_time(const KParams &p, const Lds<R> &t, const uint32_t (&Y)[S],
+template <int S, bool AR>
+__device__ __forceinline__ uint32_t end_time(const KParams &p, const Lds &t, const uint32_t (&Y)[S],
                                              const Comm<S> &c, const uint32_t (&w)[Codes<S>::kWords], uint32_t a) {
     if (!AR) return Y[0] - c.phi0;
     uint32_t cut[S + 1], ty[S], D[S];
     unpack_cuts<S>(w, p.L, cut);
     decode_types<S>(p, a, ty);
-    stage_allreduce<S, R>(p, t, cut, ty, D);
+    stage_allreduce<S>(p, t, cut, ty, D);
     // Y[s] - phi_s = finish(B_{s,M}); phi_0 - phi_s = psi_s
     uint32_t e = 0;
 #pragma unroll
@@ -658,10 +769,10 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(KParams p) {
 // check, the DP and the reduction.  With a cascade (p.nlevels > 0) a lane
 // whose steady state has not settled by iteration p.lvl_k[0] is queued for
 // resume_kernel instead of finishing here.
-template <int S, typename R, bool AR>
+template <int S, bool AR>
 __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Lds<R> tab = stage_tables<R>(p, smem);
+    const Lds tab = stage_tables(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     unsigned long long best = ~0ull;
@@ -683,7 +794,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = ok ? assign_of(p, gi) : 0u;
         decode_types<S>(p, a, ty);
-        const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B) && ok && active;
+        const bool feas = stage_weights<S>(p, tab, cut, ty, F, B) && ok && active;
         bool done_here = true;
         if (p.M < (uint32_t)S) {
             dp_table<S>(p, F, B, comm, Y);
@@ -694,7 +805,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
             if (p.nlevels) enqueue<S>(p, 0, &nq, !done_here && active && ok, (uint32_t)gi, w, Y);
             dp_finish<S>(Y, F, B, comm);
         }
-        uint32_t T = end_time<S, R, AR>(p, tab, Y, comm, w, a);
+        uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, a);
         if (!ok) T = 0xFFFFFFFFu;
         const bool write = active && (done_here || !ok);
         if (write && p.makespan_out) p.makespan_out[gi] = T;
@@ -719,10 +830,10 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
 
 // Schedules other than 1F1B: the same pass as eval_kernel with the
 // schedule-table DP and no cascade.
-template <int S, typename R, bool AR>
+template <int S, bool AR, bool TAB>
 __global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Lds<R> tab = stage_tables<R>(p, smem);
+    const Lds tab = stage_tables(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     unsigned long long best = ~0ull;
@@ -739,9 +850,9 @@ __global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = ok ? assign_of(p, gi) : 0u;
         decode_types<S>(p, a, ty);
-        const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B) && ok && active;
-        dp_sched<S>(p, F, B, comm, Y);
-        uint32_t T = end_time<S, R, AR>(p, tab, Y, comm, w, a);
+        const bool feas = stage_weights<S>(p, tab, cut, ty, F, B) && ok && active;
+        dp_other<S, TAB>(p, F, B, comm, Y);
+        uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, a);
         if (!ok) T = 0xFFFFFFFFu;
         if (active && p.makespan_out) p.makespan_out[gi] = T;
         if (p.feas_bits_out) {
@@ -760,10 +871,10 @@ __global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
 
 // Level `lvl` of the cascade: resume the queued lanes from iteration
 // p.lvl_k[lvl-1] to p.lvl_k[lvl] (the end at the last level).
-template <int S, typename R, bool AR>
+template <int S, bool AR>
 __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Lds<R> tab = stage_tables<R>(p, smem);
+    const Lds tab = stage_tables(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     const uint32_t nit = p.M - S;
@@ -791,11 +902,11 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = ok ? assign_of(p, i) : 0u;
         decode_types<S>(p, a, ty);
-        const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B);
+        const bool feas = stage_weights<S>(p, tab, cut, ty, F, B);
         const bool settled = dp_advance<S>(Y, F, B, comm, k0, k1, nit);
         if (lvl < p.nlevels) enqueue<S>(p, lvl & 1, &nq, active && !settled, i, w, Y);
         dp_finish<S>(Y, F, B, comm);
-        const uint32_t T = end_time<S, R, AR>(p, tab, Y, comm, w, a);
+        const uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, a);
         if (active && settled) {
             if (p.makespan_out) p.makespan_out[i] = T;
             const unsigned long long key = make_key(feas, T, i);
@@ -811,14 +922,14 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
 
 // Early stop (Eq. 2 / Theorem 1) over one chunk: each block filters a tile
 // of kTile candidates, compacts the survivors in LDS and evaluates them.
-template <int S, typename R, bool AR>
+template <int S, bool AR, bool SCH>
 __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chunk_lo, uint64_t chunk_hi,
                                                          uint32_t bound, uint32_t publish) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ uint16_t surv[kTile];
     __shared__ unsigned int nsurv;
     __shared__ unsigned int cnt_pruned, cnt_infeas, cnt_bad;
-    const Lds<R> tab = stage_tables<R>(p, smem);
+    const Lds tab = stage_tables(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     if (threadIdx.x == 0) { nsurv = 0; cnt_pruned = 0; cnt_infeas = 0; cnt_bad = 0; }
@@ -838,10 +949,10 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
         for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[(uint64_t)k * p.ccap + (i - p.first_i)] : 0u;
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         decode_types<S>(p, ok ? assign_of(p, i) : 0u, ty);
-        const bool feas = stage_weights<S, R>(p, tab, cut, ty, F, B);
+        const bool feas = stage_weights<S>(p, tab, cut, ty, F, B);
         uint32_t D[S];
         if (AR) {
-            stage_allreduce<S, R>(p, tab, cut, ty, D);
+            stage_allreduce<S>(p, tab, cut, ty, D);
         } else {
 #pragma unroll
             for (int s = 0; s < S; ++s) D[s] = 0;
@@ -877,10 +988,10 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
         unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = assign_of(p, i);
         decode_types<S>(p, a, ty);
-        stage_weights<S, R>(p, tab, cut, ty, F, B);
+        stage_weights<S>(p, tab, cut, ty, F, B);
         uint32_t Y[S];
-        dp_full<S>(p, F, B, comm, Y);
-        const uint32_t T = end_time<S, R, AR>(p, tab, Y, comm, w, a);
+        dp_full<S, SCH>(p, F, B, comm, Y);
+        const uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, a);
         const unsigned long long key = make_key(true, T, (uint32_t)i);
         best = key < best ? key : best;
     }
@@ -898,12 +1009,15 @@ __global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chu
 template <int S, typename R>
 hipError_t launch_eval_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
     if (p.sched) {
-        if (p.has_ar) hipLaunchKernelGGL((sched_kernel<S, R, true>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
-        else hipLaunchKernelGGL((sched_kernel<S, R, false>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
+        const dim3 g(lc.grid), b(kBlock);
+        if (p.has_ar && p.nslots) hipLaunchKernelGGL((sched_kernel<S, true, true>), g, b, lc.lds_bytes, st, p);
+        else if (p.has_ar) hipLaunchKernelGGL((sched_kernel<S, true, false>), g, b, lc.lds_bytes, st, p);
+        else if (p.nslots) hipLaunchKernelGGL((sched_kernel<S, false, true>), g, b, lc.lds_bytes, st, p);
+        else hipLaunchKernelGGL((sched_kernel<S, false, false>), g, b, lc.lds_bytes, st, p);
         return hipGetLastError();
     }
-    if (p.has_ar) hipLaunchKernelGGL((eval_kernel<S, R, true>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
-    else hipLaunchKernelGGL((eval_kernel<S, R, false>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
+    if (p.has_ar) hipLaunchKernelGGL((eval_kernel<S, true>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
+    else hipLaunchKernelGGL((eval_kernel<S, false>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p);
     return hipGetLastError();
 }
 
@@ -916,30 +1030,39 @@ hipError_t launch_decode_s(const KParams &p, const LaunchCfg &lc, hipStream_t st
 
 template <int S, typename R>
 hipError_t launch_resume_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl) {
-    if (p.has_ar) hipLaunchKernelGGL((resume_kernel<S, R, true>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p, lvl);
-    else hipLaunchKernelGGL((resume_kernel<S, R, false>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p, lvl);
+    if (p.has_ar) hipLaunchKernelGGL((resume_kernel<S, true>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p, lvl);
+    else hipLaunchKernelGGL((resume_kernel<S, false>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p, lvl);
     return hipGetLastError();
 }
 
 template <int S, typename R>
 hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
                                    uint32_t bound, uint32_t publish) {
-    const uint64_t grid = (hi - lo + kTile - 1) / kTile;
-    if (p.has_ar)
-        hipLaunchKernelGGL((bounded_kernel<S, R, true>), dim3((uint32_t)grid), dim3(kBlock), lc.lds_bytes, st, p, lo,
-                           hi, bound, publish);
+    const dim3 grid((uint32_t)((hi - lo + kTile - 1) / kTile));
+    const bool sch = p.sched != 0;
+    if (p.has_ar && sch)
+        hipLaunchKernelGGL((bounded_kernel<S, true, true>), grid, dim3(kBlock), lc.lds_bytes, st, p, lo, hi,
+                           bound, publish);
+    else if (p.has_ar)
+        hipLaunchKernelGGL((bounded_kernel<S, true, false>), grid, dim3(kBlock), lc.lds_bytes, st, p, lo, hi,
+                           bound, publish);
+    else if (sch)
+        hipLaunchKernelGGL((bounded_kernel<S, false, true>), grid, dim3(kBlock), lc.lds_bytes, st, p, lo, hi,
+                           bound, publish);
     else
-        hipLaunchKernelGGL((bounded_kernel<S, R, false>), dim3((uint32_t)grid), dim3(kBlock), lc.lds_bytes, st, p, lo,
-                           hi, bound, publish);
+        hipLaunchKernelGGL((bounded_kernel<S, false, false>), grid, dim3(kBlock), lc.lds_bytes, st, p, lo, hi,
+                           bound, publish);
     return hipGetLastError();
 }
 
 template <int S, typename R>
 hipError_t occupancy_s(int *blocks, size_t lds, bool ar, bool sched) {
-    if (sched && ar) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, sched_kernel<S, R, true>, kBlock, lds);
-    if (sched) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, sched_kernel<S, R, false>, kBlock, lds);
-    if (ar) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, eval_kernel<S, R, true>, kBlock, lds);
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, eval_kernel<S, R, false>, kBlock, lds);
+    // schedules other than 1F1B: the closed-form kernel (the table kernel
+    // runs few candidates per call in practice and takes the same grid)
+    if (sched && ar) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, sched_kernel<S, true, false>, kBlock, lds);
+    if (sched) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, sched_kernel<S, false, false>, kBlock, lds);
+    if (ar) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, eval_kernel<S, true>, kBlock, lds);
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, eval_kernel<S, false>, kBlock, lds);
 }
 
 

@@ -109,3 +109,23 @@ def test_load_costs_rejects_before_device():
     with pytest.raises(P.PoseidonError) as ei:
         P.poseidon_load_costs(p, 0)
     assert ei.value.status == P.POSEIDON_E_INVAL
+
+
+def test_closed_form_schedules_pass_the_host_self_check():
+    """poseidon_load_costs simulates the slot schedule and compares it with
+    the closed forms the kernels hard-code (1F1B for M >= S, Eager 1F1B for
+    M >= 2S-1, including which forwards read the upstream's previous
+    forward); a mismatch returns E_INVAL before any device call.  Without a
+    GPU a passing check ends at the device step (E_DEVICE)."""
+    torch = pytest.importorskip("torch")
+    if torch.cuda.is_available():
+        pytest.skip("needs a host without a GPU")
+    rng = np.random.default_rng(4)
+    for sched in (P.SCHEDULE_1F1B, P.SCHEDULE_EAGER_1F1B):
+        for S in range(1, 17):
+            for M in list(range(1, 2 * S + 6)) + [64, 255]:
+                p = W.random_problem(rng, S + 2, S, M, 1)
+                p.schedule = sched
+                with pytest.raises(P.PoseidonError) as ei:
+                    P.poseidon_load_costs(p, 0)
+                assert ei.value.status == P.POSEIDON_E_DEVICE, (sched, S, M)

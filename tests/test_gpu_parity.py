@@ -498,6 +498,19 @@ def test_eager_random_problems(dev):
         check_against_oracle(prob, W.random_candidates(rng, prob, int(rng.integers(1, 1500))), dev)
 
 
+def test_eager_closed_form_edges(dev):
+    """Closed form at its smallest M = 2S-1 (no steady pair for stage 1),
+    odd and even steady pair counts, long steady parts."""
+    rng = np.random.default_rng(113)
+    for S, M in [(1, 1), (1, 2), (2, 3), (2, 4), (5, 9), (5, 10), (8, 15), (8, 16), (16, 31), (16, 32),
+                 (16, 33), (3, 200), (3, 201), (12, 129)]:
+        L = S + int(rng.integers(0, 8))
+        prob = W.random_problem(rng, L, S, M, 2, cost_hi=300, mem_hi=30, cap=int(rng.integers(30, 200)),
+                                assign_rows=None if 2 ** S < 5000 else 5)
+        prob.schedule = P.SCHEDULE_EAGER_1F1B
+        check_against_oracle(prob, W.random_candidates(rng, prob, int(rng.integers(100, 1200))), dev)
+
+
 def test_eager_python_oracle_and_bounded(dev):
     rng = np.random.default_rng(112)
     for trial in range(8):
