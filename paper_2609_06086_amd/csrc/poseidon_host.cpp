@@ -17,7 +17,10 @@
 #include "poseidon_internal.h"
 
 #ifndef PK_CASCADE_K0
-#define PK_CASCADE_K0 S   // first checkpoint of the steady-state cascade
+#define PK_CASCADE_K0 S   // first checkpoint of the steady-state cascade (1F1B)
+#endif
+#ifndef PK_EAGER_K0
+#define PK_EAGER_K0 (2 * S)   // the same for Eager 1F1B, whose steady state settles later
 #endif
 
 namespace {
@@ -329,9 +332,11 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     kp.sched = sched;
     for (uint32_t s = 1; s < S; ++s) kp.psi[s] = kp.psi[s - 1] + kp.cf[s - 1];
     // cascade checkpoints of the steady loop: K0, 2 K0, 4 K0, ... below M - S
-    if (M >= S && p->schedule == POSEIDON_SCHEDULE_1F1B) {
-        const uint32_t nit = M - S;
-        uint32_t k = std::max<uint32_t>(2, PK_CASCADE_K0);
+    // (steady iterations: 1F1B slot pairs after its prologue, Eager 1F1B
+    // slot pairs between its prologue and epilogue)
+    if (!table_path) {
+        const uint32_t nit = eager ? M + 1 - 2 * S : M - S;
+        uint32_t k = std::max<uint32_t>(2, eager ? PK_EAGER_K0 : PK_CASCADE_K0);
         while (k < nit && kp.nlevels < (uint32_t)pk::kMaxLevels) {
             kp.lvl_k[kp.nlevels++] = k;
             k *= 2;
@@ -500,6 +505,9 @@ constexpr uint64_t kChunk = 1ull << 26;
 // only after the stream has drained.
 uint64_t queue_cap(const poseidon_ctx *ctx, uint64_t n) { return n + (uint64_t)ctx->grid_max * 256; }
 
+// DP state words per queue entry: S registers for 1F1B, 2S for Eager 1F1B
+uint64_t queue_state_words(const poseidon_ctx *ctx) { return ctx->base.sched ? 2ull * ctx->S : ctx->S; }
+
 int ensure_workspace(poseidon_ctx *ctx, uint64_t n, hipStream_t st) {
     if (ctx->ws_cap >= n) return POSEIDON_OK;
     if (ctx->ws) {
@@ -512,7 +520,8 @@ int ensure_workspace(poseidon_ctx *ctx, uint64_t n, hipStream_t st) {
     const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
     uint64_t elems = words * cap;
     if (ctx->base.nlevels)
-        elems += 2 * (1 + words + ctx->S) * queue_cap(ctx, cap) + (uint64_t)pk::kMaxLevels * ctx->grid_max;
+        elems += 2 * (1 + words + queue_state_words(ctx)) * queue_cap(ctx, cap) +
+                 (uint64_t)pk::kMaxLevels * ctx->grid_max;
     void *q = nullptr;
     if (hipMalloc(&q, elems * 4) != hipSuccess) {
         (void)hipGetLastError();
@@ -565,8 +574,8 @@ int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands, uin
     if (kp.nlevels) {
         kp.qcap = queue_cap(ctx, ctx->ws_cap);
         kp.queue[0] = ws + words * ctx->ws_cap;
-        kp.queue[1] = kp.queue[0] + (1 + words + ctx->S) * kp.qcap;
-        kp.qcount = kp.queue[1] + (1 + words + ctx->S) * kp.qcap;
+        kp.queue[1] = kp.queue[0] + (1 + words + queue_state_words(ctx)) * kp.qcap;
+        kp.qcount = kp.queue[1] + (1 + words + queue_state_words(ctx)) * kp.qcap;
     }
     for (uint64_t c0 = 0; c0 < cands->count; c0 += chunk) {
         kp.first_i = c0;

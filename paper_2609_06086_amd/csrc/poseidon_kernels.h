@@ -473,23 +473,89 @@ __device__ __forceinline__ void eager_pair(uint32_t (&Y)[S], uint32_t (&Fn)[S], 
     eager_slot<S, kEven, 0>(std::make_integer_sequence<int, S>{}, Y, Fn, Fp, F, B, c);
 }
 
+// n steady pairs, two per trip so that the forward registers come back to
+// the same roles at the loop edge
 template <int S>
-__device__ __forceinline__ void dp_eager(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S],
-                                         const Comm<S> &c, uint32_t (&Y)[S]) {
-    uint32_t Fn[S], Fp[S];
+__device__ __forceinline__ void eager_pairs(uint32_t n, uint32_t (&Y)[S], uint32_t (&Fn)[S], uint32_t (&Fp)[S],
+                                            const uint32_t (&F)[S], const uint32_t (&B)[S], const Comm<S> &c) {
+    for (uint32_t i = 1; i < n; i += 2) {
+        eager_pair<S>(Y, Fn, Fp, F, B, c);
+        eager_pair<S>(Y, Fn, Fp, F, B, c);
+    }
+    if (n & 1u) eager_pair<S>(Y, Fn, Fp, F, B, c);
+}
+
+template <int S>
+__device__ __forceinline__ void eager_prologue(uint32_t (&Y)[S], uint32_t (&Fn)[S], uint32_t (&Fp)[S],
+                                               const uint32_t (&F)[S], const uint32_t (&B)[S], const Comm<S> &c) {
     dp_init<S>(Y, c);
 #pragma unroll
     for (int s = 0; s < S; ++s) { Fn[s] = 0; Fp[s] = 0; }
     eager_run<S, kPro>(std::make_integer_sequence<int, 2 * S - 1>{}, Y, Fn, Fp, F, B, c);
-    // two pairs per trip, so that the forward registers come back to the
-    // same roles at the loop edge
-    const uint32_t npairs = M - 2 * S + 1;
-    for (uint32_t i = 1; i < npairs; i += 2) {
-        eager_pair<S>(Y, Fn, Fp, F, B, c);
-        eager_pair<S>(Y, Fn, Fp, F, B, c);
-    }
-    if (npairs & 1u) eager_pair<S>(Y, Fn, Fp, F, B, c);
+}
+
+template <int S>
+__device__ __forceinline__ void eager_epilogue(uint32_t (&Y)[S], uint32_t (&Fn)[S], uint32_t (&Fp)[S],
+                                               const uint32_t (&F)[S], const uint32_t (&B)[S], const Comm<S> &c) {
     eager_run<S, kEpi>(std::make_integer_sequence<int, 4 * S - 3>{}, Y, Fn, Fp, F, B, c);
+}
+
+template <int S>
+__device__ __forceinline__ void dp_eager(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                         const Comm<S> &c, uint32_t (&Y)[S]) {
+    uint32_t Fn[S], Fp[S];
+    eager_prologue<S>(Y, Fn, Fp, F, B, c);
+    eager_pairs<S>(M - 2 * S + 1, Y, Fn, Fp, F, B, c);
+    eager_epilogue<S>(Y, Fn, Fp, F, B, c);
+}
+
+// Between steady pairs the state that the rest of the DP reads is, per
+// stage, the newest forward Fn and, for a stage with odd 1-based index (its
+// newest node is that forward), the previous forward Fp, else the newest
+// node Y (a backward; its Fp is rewritten before any read).  The pair map is
+// built from max and + only, so once one pair raises all 2S values by the
+// same d, every later pair does the same (as for 1F1B).  Checking it needs
+// one saved value per stage: a pair moves the old Fn into Fp, so
+// Fn - Fp is the forward's increment.
+template <int S>
+__device__ __forceinline__ bool eager_advance(uint32_t (&Y)[S], uint32_t (&Fn)[S], uint32_t (&Fp)[S],
+                                              const uint32_t (&F)[S], const uint32_t (&B)[S], const Comm<S> &c,
+                                              uint32_t k0, uint32_t k1, uint32_t npairs) {
+    const bool last = k1 >= npairs;
+    eager_pairs<S>(last ? npairs - k0 : k1 - k0 - 1, Y, Fn, Fp, F, B, c);
+    if (last) return true;
+    uint32_t Z[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) Z[s] = (s & 1) == 0 ? Fp[s] : Y[s];
+    eager_pair<S>(Y, Fn, Fp, F, B, c);
+    const uint32_t d = Fn[0] - Fp[0];
+    bool ok = true;
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+        ok = ok && Fn[s] - Fp[s] == d && ((s & 1) == 0 ? Fp[s] : Y[s]) - Z[s] == d;
+    const uint32_t jump = ok ? (npairs - k1) * d : 0u;
+#pragma unroll
+    for (int s = 0; s < S; ++s) { Y[s] += jump; Fn[s] += jump; Fp[s] += jump; }
+    return ok;
+}
+
+// queue image of the state between pairs (2S words) and back
+template <int S>
+__device__ __forceinline__ void eager_pack(const uint32_t (&Y)[S], const uint32_t (&Fn)[S], const uint32_t (&Fp)[S],
+                                           uint32_t (&X)[2 * S]) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) { X[s] = Fn[s]; X[S + s] = (s & 1) == 0 ? Fp[s] : Y[s]; }
+}
+
+template <int S>
+__device__ __forceinline__ void eager_unpack(const uint32_t (&X)[2 * S], uint32_t (&Y)[S], uint32_t (&Fn)[S],
+                                             uint32_t (&Fp)[S]) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        Fn[s] = X[s];
+        Y[s] = (s & 1) == 0 ? X[s] : X[S + s];
+        Fp[s] = (s & 1) == 0 ? X[S + s] : 0u;
+    }
 }
 
 // schedules other than 1F1B: the slot table (TAB) or the closed form
@@ -645,9 +711,9 @@ struct QueueView {
 // for the next level.  Block b owns slots [b * seg_cap, (b + 1) * seg_cap)
 // of the queue and counts its entries in LDS (*nq), so no global atomic is
 // involved; every lane of the wave must call this.
-template <int S>
+template <int S, int NX>
 __device__ __forceinline__ void enqueue(const KParams &p, int which, unsigned int *nq, bool want, uint32_t idx,
-                                        const uint32_t (&w)[Codes<S>::kWords], const uint32_t (&Y)[S]) {
+                                        const uint32_t (&w)[Codes<S>::kWords], const uint32_t (&Y)[NX]) {
     const unsigned long long m = __ballot(want);
     if (m == 0) return;
     const unsigned int lane = threadIdx.x & 63;
@@ -662,7 +728,7 @@ __device__ __forceinline__ void enqueue(const KParams &p, int which, unsigned in
 #pragma unroll
         for (int k = 0; k < Codes<S>::kWords; ++k) q.codes[(uint64_t)k * p.qcap + slot] = w[k];
 #pragma unroll
-        for (int s = 0; s < S; ++s) q.Y[(uint64_t)s * p.qcap + slot] = Y[s];
+        for (int s = 0; s < NX; ++s) q.Y[(uint64_t)s * p.qcap + slot] = Y[s];
     }
 }
 
@@ -802,7 +868,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
             dp_prologue<S>(Y, F, B, comm);
             const uint32_t k1 = p.nlevels ? p.lvl_k[0] : nit;
             done_here = dp_advance<S>(Y, F, B, comm, 0, k1, nit);
-            if (p.nlevels) enqueue<S>(p, 0, &nq, !done_here && active && ok, (uint32_t)gi, w, Y);
+            if (p.nlevels) enqueue<S, S>(p, 0, &nq, !done_here && active && ok, (uint32_t)gi, w, Y);
             dp_finish<S>(Y, F, B, comm);
         }
         uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, a);
@@ -829,7 +895,8 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
 }
 
 // Schedules other than 1F1B: the same pass as eval_kernel with the
-// schedule-table DP and no cascade.
+// schedule-table DP (TAB) or the Eager 1F1B closed form, whose steady part
+// takes the same cascade (queue entries carry 2S state words).
 template <int S, bool AR, bool TAB>
 __global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -839,6 +906,10 @@ __global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
     unsigned long long best = ~0ull;
     const uint64_t stride = (uint64_t)gridDim.x * kBlock;
     const uint64_t span = (p.n_i + stride - 1) / stride;
+    const uint32_t npairs = TAB ? 0u : p.M - 2 * S + 1;
+    __shared__ unsigned int nq;
+    if (threadIdx.x == 0) nq = 0;
+    __syncthreads();
     uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
     for (uint64_t it = 0; it < span; ++it, i += stride) {
         const bool active = i < p.n_i;
@@ -851,33 +922,54 @@ __global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
         const uint32_t a = ok ? assign_of(p, gi) : 0u;
         decode_types<S>(p, a, ty);
         const bool feas = stage_weights<S>(p, tab, cut, ty, F, B) && ok && active;
-        dp_other<S, TAB>(p, F, B, comm, Y);
+        bool done_here = true;
+        if (TAB) {
+            dp_sched<S>(p, F, B, comm, Y);
+        } else {
+            uint32_t Fn[S], Fp[S];
+            eager_prologue<S>(Y, Fn, Fp, F, B, comm);
+            const uint32_t k1 = p.nlevels ? p.lvl_k[0] : npairs;
+            done_here = eager_advance<S>(Y, Fn, Fp, F, B, comm, 0, k1, npairs);
+            if (p.nlevels) {
+                uint32_t X[2 * S];
+                eager_pack<S>(Y, Fn, Fp, X);
+                enqueue<S, 2 * S>(p, 0, &nq, !done_here && active && ok, (uint32_t)gi, w, X);
+            }
+            eager_epilogue<S>(Y, Fn, Fp, F, B, comm);
+        }
         uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, a);
         if (!ok) T = 0xFFFFFFFFu;
-        if (active && p.makespan_out) p.makespan_out[gi] = T;
+        const bool write = active && (done_here || !ok);
+        if (write && p.makespan_out) p.makespan_out[gi] = T;
         if (p.feas_bits_out) {
             const unsigned long long bits = __ballot(feas);
             const uint64_t w0 = (gi - (threadIdx.x & 63)) >> 5;
             if ((threadIdx.x & 63) == 0 && w0 < p.nwords) p.feas_bits_out[w0] = (uint32_t)bits;
             if ((threadIdx.x & 63) == 32 && w0 + 1 < p.nwords) p.feas_bits_out[w0 + 1] = (uint32_t)(bits >> 32);
         }
-        if (active) {
+        if (write) {
             const unsigned long long key = make_key(feas, T, (uint32_t)gi);
             best = key < best ? key : best;
         }
     }
-    block_min_and_finish(best, p.acc, p.done, p.result, nullptr, true, p.accumulate);
+    if (!TAB && p.nlevels) {
+        __syncthreads();
+        if (threadIdx.x == 0) p.qcount[blockIdx.x] = nq;
+    }
+    block_min_and_finish(best, p.acc, p.done, p.result, nullptr, TAB || p.nlevels == 0, p.accumulate);
 }
 
-// Level `lvl` of the cascade: resume the queued lanes from iteration
-// p.lvl_k[lvl-1] to p.lvl_k[lvl] (the end at the last level).
-template <int S, bool AR>
+// Level `lvl` of the cascade: resume the queued lanes from steady
+// iteration p.lvl_k[lvl-1] to p.lvl_k[lvl] (the end at the last level).
+// SCH: Eager 1F1B (2S state words per entry, steady pairs), else 1F1B.
+template <int S, bool AR, bool SCH>
 __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl) {
     extern __shared__ __align__(16) unsigned char smem[];
     const Lds tab = stage_tables(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
-    const uint32_t nit = p.M - S;
+    constexpr int NX = SCH ? 2 * S : S;
+    const uint32_t nit = SCH ? p.M - 2 * S + 1 : p.M - S;
     const uint32_t k0 = p.lvl_k[lvl - 1];
     const uint32_t k1 = lvl < p.nlevels ? p.lvl_k[lvl] : nit;
     // this block's segment of the queue written by level lvl - 1
@@ -894,18 +986,32 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
         const uint32_t q = it * kBlock + threadIdx.x;
         const bool active = q < n;
         const uint32_t i = active ? qin.idx[seg + q] : 0u;
-        uint32_t w[NW], cut[S + 1], ty[S], F[S], B[S], Y[S];
+        uint32_t w[NW], cut[S + 1], ty[S], F[S], B[S], X[NX], Y[S];
 #pragma unroll
         for (int k = 0; k < NW; ++k) w[k] = active ? qin.codes[(uint64_t)k * p.qcap + seg + q] : 0u;
 #pragma unroll
-        for (int s = 0; s < S; ++s) Y[s] = active ? qin.Y[(uint64_t)s * p.qcap + seg + q] : 0u;
+        for (int s = 0; s < NX; ++s) X[s] = active ? qin.Y[(uint64_t)s * p.qcap + seg + q] : 0u;
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = ok ? assign_of(p, i) : 0u;
         decode_types<S>(p, a, ty);
         const bool feas = stage_weights<S>(p, tab, cut, ty, F, B);
-        const bool settled = dp_advance<S>(Y, F, B, comm, k0, k1, nit);
-        if (lvl < p.nlevels) enqueue<S>(p, lvl & 1, &nq, active && !settled, i, w, Y);
-        dp_finish<S>(Y, F, B, comm);
+        bool settled;
+        if constexpr (SCH) {
+            uint32_t Fn[S], Fp[S];
+            eager_unpack<S>(X, Y, Fn, Fp);
+            settled = eager_advance<S>(Y, Fn, Fp, F, B, comm, k0, k1, nit);
+            if (lvl < p.nlevels) {
+                eager_pack<S>(Y, Fn, Fp, X);
+                enqueue<S, NX>(p, lvl & 1, &nq, active && !settled, i, w, X);
+            }
+            eager_epilogue<S>(Y, Fn, Fp, F, B, comm);
+        } else {
+#pragma unroll
+            for (int s = 0; s < S; ++s) Y[s] = X[s];
+            settled = dp_advance<S>(Y, F, B, comm, k0, k1, nit);
+            if (lvl < p.nlevels) enqueue<S, S>(p, lvl & 1, &nq, active && !settled, i, w, Y);
+            dp_finish<S>(Y, F, B, comm);
+        }
         const uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, a);
         if (active && settled) {
             if (p.makespan_out) p.makespan_out[i] = T;
@@ -1030,8 +1136,12 @@ hipError_t launch_decode_s(const KParams &p, const LaunchCfg &lc, hipStream_t st
 
 template <int S, typename R>
 hipError_t launch_resume_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl) {
-    if (p.has_ar) hipLaunchKernelGGL((resume_kernel<S, true>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p, lvl);
-    else hipLaunchKernelGGL((resume_kernel<S, false>), dim3(lc.grid), dim3(kBlock), lc.lds_bytes, st, p, lvl);
+    const dim3 g(lc.grid), b(kBlock);
+    const bool sch = p.sched != 0;
+    if (p.has_ar && sch) hipLaunchKernelGGL((resume_kernel<S, true, true>), g, b, lc.lds_bytes, st, p, lvl);
+    else if (p.has_ar) hipLaunchKernelGGL((resume_kernel<S, true, false>), g, b, lc.lds_bytes, st, p, lvl);
+    else if (sch) hipLaunchKernelGGL((resume_kernel<S, false, true>), g, b, lc.lds_bytes, st, p, lvl);
+    else hipLaunchKernelGGL((resume_kernel<S, false, false>), g, b, lc.lds_bytes, st, p, lvl);
     return hipGetLastError();
 }
 

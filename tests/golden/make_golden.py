@@ -1,12 +1,13 @@
 """Write tests/golden/full_workloads.json from the CPU oracle only.
 
-For each large workload (3, 4, 5, 6) this records, over every candidate:
+For each large workload (3, 4, 5, 6, and 4 and 5 under Eager 1F1B, written
+"4e" and "5e") this records, over every candidate:
 the SHA-256 of the makespan array (uint32 little-endian), the SHA-256 of the
 feasibility bit array packed as the library's output (bit i % 32 of uint32
 word i / 32), the number of feasible candidates and the argmin.  For
 workloads 4 and 6 it also records the early-stop pass: the warm-up bound (best of
 the first 500 list entries) and, per chunk size, the oracle's
-(best, evaluated, pruned, infeasible).
+(best, evaluated, pruned, infeasible); likewise for 4e and 5e.
 
 Run from the repository root:  python tests/golden/make_golden.py [workload ...]
 """
@@ -36,11 +37,15 @@ def pack_bits(f: np.ndarray) -> np.ndarray:
 
 def main():
     res = {"note": "written by tests/golden/make_golden.py from the C oracle; see that script"}
-    only = [int(a) for a in sys.argv[1:]] or [3, 4, 5, 6]
+    only = sys.argv[1:] or ["3", "4", "5", "6", "4e", "5e"]
     if os.path.exists(OUT):
         res.update({k: v for k, v in json.load(open(OUT)).items() if k != "note"})
-    for cfg in only:
+    for spec in only:
+        eager = spec.endswith("e")
+        cfg = int(spec.rstrip("e"))
         wl = W.workload(cfg)
+        if eager:
+            wl.problem.schedule = 1   # Eager 1F1B
         t0 = time.time()
         T, f = coracle.evaluate(wl.problem, wl.cands)
         best = coracle.argmin(T, f)
@@ -52,7 +57,7 @@ def main():
             "best_index": best[0], "best_makespan": best[1],
             "makespan_min": int(T.min()), "makespan_max": int(T.max()),
         }
-        if cfg in (4, 6):
+        if cfg in (4, 6) or eager:
             wb = coracle.argmin(T[:WARMUP], f[:WARMUP])
             bound = wb[1]
             ent["warmup"] = WARMUP
@@ -63,8 +68,8 @@ def main():
                 ent["bounded"][str(ch)] = {"best_index": b[0], "best_makespan": b[1], "evaluated": ev,
                                            "pruned": pr, "infeasible": inf}
         ent["oracle_seconds"] = round(time.time() - t0, 1)
-        res[f"cfg{cfg}"] = ent
-        print(cfg, ent, flush=True)
+        res[f"cfg{cfg}_eager" if eager else f"cfg{cfg}"] = ent
+        print(spec, ent, flush=True)
     with open(OUT, "w") as fh:
         json.dump(res, fh, indent=1)
         fh.write("\n")

@@ -560,3 +560,27 @@ def test_eager_differs_from_1f1b(dev):
     assert np.array_equal(T1, To)
     c0.close()
     c1.close()
+
+
+@pytest.mark.parametrize("cfg", [4, 5])
+def test_full_workload_eager_matches_golden(cfg, dev):
+    """Full-size workloads under Eager 1F1B: closed form, steady-state
+    cascade and early stop against digests the oracle wrote."""
+    gall = _golden()
+    key = f"cfg{cfg}_eager"
+    if key not in gall:
+        pytest.skip(f"no golden for {key}")
+    g = gall[key]
+    wl = W.workload(cfg)
+    wl.problem.schedule = P.SCHEDULE_EAGER_1F1B
+    ctx = P.poseidon_load_costs(wl.problem, 0)
+    Tg, fg, best = gpu_eval(ctx, wl.cands, dev)
+    assert hashlib.sha256(Tg.astype("<u4").tobytes()).hexdigest() == g["makespan_sha256"]
+    assert hashlib.sha256(pack_bits(fg).astype("<u4").tobytes()).hexdigest() == g["feasible_bits_sha256"]
+    assert (best.index, best.makespan) == (g["best_index"], g["best_makespan"])
+    d = to_dev(wl.cands, dev)
+    for chunk, exp in g["bounded"].items():
+        b, st = P.poseidon_eval_candidates_bounded(ctx, g["warmup_bound"], chunk=int(chunk), **d)
+        assert (b.index, b.makespan) == (exp["best_index"], exp["best_makespan"])
+        assert (st.evaluated, st.pruned, st.infeasible) == (exp["evaluated"], exp["pruned"], exp["infeasible"])
+    ctx.close()
