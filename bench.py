@@ -62,7 +62,7 @@ def cpu_baseline(wl, target_s):
     coracle.lib()
     threads = coracle.default_threads()
     n = len(wl.cands)
-    probe = min(n, 20000)
+    probe = min(n, 200000)
     t0 = time.perf_counter()
     coracle.evaluate(wl.problem, wl.cands, nthreads=threads, lo=0, hi=probe)
     dt = time.perf_counter() - t0
@@ -81,7 +81,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=5, choices=[3, 4, 5, 6])
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-early-stop", action="store_true")
     ap.add_argument("--schedule", default="1f1b", choices=["1f1b", "eager"],
