@@ -53,6 +53,10 @@ def lib():
                                     C.POINTER(C.c_uint64), C.POINTER(C.c_uint32),
                                     C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
                                     C.POINTER(C.c_uint64), C.c_int]
+        _lib.oc_search.restype = C.c_int
+        _lib.oc_search.argtypes = [C.POINTER(_Problem), C.c_uint64, C.c_uint64, C.c_uint32, C.c_uint64,
+                                   C.c_uint32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint32),
+                                   C.POINTER(C.c_uint64), C.c_int]
         _lib.oc_dag_counts.restype = C.c_int
         _lib.oc_dag_counts.argtypes = [C.c_int, C.c_int] + [C.POINTER(C.c_int)] * 5
     return _lib
@@ -133,6 +137,28 @@ def bounded(prob, cands, bound: int, chunk: int = 0, nthreads: Optional[int] = N
     del keep
     best = None if bi.value == 2**64 - 1 else (int(bi.value), int(bt.value))
     return best, int(ev.value), int(pr.value), int(inf.value)
+
+
+SEARCH_RIDGE, SEARCH_NO_STAGE_PRUNING = 1, 2
+SEARCH_COUNTERS = ("visited", "evaluated", "pruned_memory", "pruned_ridge", "pruned_bound")
+
+
+def search(prob, bound: int, first_row: int = 0, n_rows: Optional[int] = None, rows_per_chunk: int = 0,
+           ridge: bool = False, stage_pruning: bool = True, nthreads: Optional[int] = None):
+    """Pruned search (same semantics and counters as oracle.search.stage_search)."""
+    st, keep = _problem(prob)
+    n_rows = prob.A - first_row if n_rows is None else n_rows
+    bi, bt = C.c_uint64(), C.c_uint32()
+    cnt = (C.c_uint64 * 5)()
+    flags = (SEARCH_RIDGE if ridge else 0) | (0 if stage_pruning else SEARCH_NO_STAGE_PRUNING)
+    rc = lib().oc_search(C.byref(st), first_row, n_rows, bound, rows_per_chunk, flags, C.byref(bi), C.byref(bt),
+                         cnt, nthreads or default_threads())
+    if rc != 0:
+        raise RuntimeError(f"oracle oc_search failed: {rc}")
+    del keep
+    out = {k: int(v) for k, v in zip(SEARCH_COUNTERS, cnt)}
+    out["best"] = None if bi.value == 2**64 - 1 else (int(bi.value), int(bt.value))
+    return out
 
 
 def dag_counts(S: int, M: int):

@@ -31,6 +31,14 @@
  *  - Early stop (Eq. 2, Theorem 1): g(S_x) = sum_{i<x} F_i + M (F_x + B_x)
  *    + max_{1<=i<=x} (sum_{j=i}^{x-1} B_j + d_i), d_i = stage all-reduce
  *    time; prune iff max_x g > b.
+ *  - Pruned search (Sec. 4.2.3; readings R16-R19 of oracle/search.py): per
+ *    assignment row, layers are allocated stage by stage, smaller counts
+ *    first; a stage choice is cut (with every larger count) when the stage
+ *    exceeds its memory cap, when a type's layer counts stop being
+ *    ridge-like (Theorem 2, with layer-level pruning on), or when g(S_x)
+ *    exceeds the chunk's bound (Theorem 1).  Rows are processed in chunks
+ *    with a fixed bound per chunk; the result is the first candidate in
+ *    (row, rank) order with the smallest makespan <= bound.
  *
  * Finish times are held in 64-bit integers, so no intermediate can wrap.
  */
@@ -439,5 +447,152 @@ int oc_dag_counts(int S, int M, int *n_nodes, int *n_fwd, int *n_bwd, int *n_int
     }
     *n_nodes = g->n; *n_fwd = f; *n_bwd = b; *n_intra = in; *n_other = o;
     dag_free(g);
+    return 0;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Pruned search over assignment rows (see header).                        */
+
+typedef struct {
+    const oc_problem *p;
+    const oc_dag *g;
+    const uint64_t *binom;
+    uint64_t row_lo, row_hi;
+    uint64_t bound;
+    int ridge, stage_pruning;
+    /* results */
+    uint64_t best_T, best_row, best_rank;
+    uint64_t visited, evaluated, pr_mem, pr_ridge, pr_bound;
+    int err;
+    /* per-row DFS state */
+    int types[64];
+    int last[64], falling[64];     /* ridge state per type (last = -1: none yet) */
+    uint64_t F[64], B[64], D[64];
+    uint64_t *fin;
+    uint64_t row;
+} oc_sjob;
+
+static void s_stage(oc_sjob *j, int x, int lo, uint64_t pre_f, uint64_t inner, uint64_t rank) {
+    const oc_problem *p = j->p;
+    int S = (int)p->S, L = (int)p->L, k = S - 1;
+    int t = j->types[x - 1];
+    int last_stage = x == S;
+    int hi_min = last_stage ? L : lo + 1, hi_max = last_stage ? L : L - (S - x);
+    uint64_t f = 0, b = 0, mm = 0, d = 0, acc = 0;
+    for (int l = lo; l < hi_min - 1; ++l) {
+        f += p->fwd[(size_t)t * L + l]; b += p->bwd[(size_t)t * L + l]; mm += p->mem[l];
+        if (p->allreduce) d += p->allreduce[(size_t)t * L + l];
+    }
+    for (int hi = hi_min; hi <= hi_max; ++hi) {
+        int l = hi - 1;   /* add layer hi-1 */
+        f += p->fwd[(size_t)t * L + l]; b += p->bwd[(size_t)t * L + l]; mm += p->mem[l];
+        if (p->allreduce) d += p->allreduce[(size_t)t * L + l];
+        if (mm > p->cap[t]) { j->pr_mem++; break; }
+        int cnt = hi - lo;
+        if (j->ridge && j->last[t] >= 0 && j->falling[t] && cnt > j->last[t]) { j->pr_ridge++; break; }
+        uint64_t inn = x == 1 ? d : (inner + j->B[x - 2] > d ? inner + j->B[x - 2] : d);
+        uint64_t gx = pre_f + (uint64_t)p->M * (f + b) + inn;
+        if (j->stage_pruning && gx > j->bound) { j->pr_bound++; break; }
+        j->visited++;
+        int sv_last = j->last[t], sv_fall = j->falling[t];
+        if (j->last[t] >= 0 && cnt < j->last[t]) j->falling[t] = 1;
+        j->last[t] = cnt;
+        j->F[x - 1] = f; j->B[x - 1] = b; j->D[x - 1] = d;
+        uint64_t r = rank + acc;
+        if (last_stage) {
+            j->evaluated++;
+            uint64_t T = dag_longest(j->g, j->F, j->B, j->D, p->cf, p->cb, j->fin);
+            if (T <= j->bound && (T < j->best_T || (T == j->best_T && (j->row < j->best_row ||
+                                   (j->row == j->best_row && r < j->best_rank))))) {
+                j->best_T = T; j->best_row = j->row; j->best_rank = r;
+            }
+        } else {
+            s_stage(j, x + 1, hi, pre_f + f, inn, r);
+            /* the next value of cut x skips the tuples whose cut x is hi */
+            acc += j->binom[(size_t)(L - 1 - hi) * (k + 1) + (k - x)];
+        }
+        j->last[t] = sv_last; j->falling[t] = sv_fall;
+    }
+}
+
+static void *s_worker(void *arg) {
+    oc_sjob *j = arg;
+    const oc_problem *p = j->p;
+    int S = (int)p->S;
+    j->fin = malloc(sizeof(uint64_t) * (size_t)j->g->n);
+    if (!j->fin) { j->err = -3; return NULL; }
+    for (uint64_t a = j->row_lo; a < j->row_hi; ++a) {
+        uint64_t aa = a;
+        if (p->assign) {
+            for (int s = 0; s < S; ++s) j->types[s] = p->assign[a * S + s];
+        } else {
+            for (int s = S - 1; s >= 0; --s) { j->types[s] = (int)(aa % p->T); aa /= p->T; }
+        }
+        for (int t = 0; t < 64; ++t) { j->last[t] = -1; j->falling[t] = 0; }
+        j->row = a;
+        s_stage(j, 1, 0, 0, 0, 0);
+    }
+    free(j->fin);
+    return NULL;
+}
+
+/* Pruned search over rows [first_row, first_row + n_rows), chunks of
+ * rows_per_chunk rows (0 = one chunk).  flags: bit 0 = layer-level (ridge)
+ * pruning, bit 1 = no stage-level pruning.  Outputs the joint index
+ * rank * A + row and the makespan (UINT64_MAX / UINT32_MAX if nothing
+ * qualifies) and the counters visited, evaluated, pruned by memory, by the
+ * ridge test and by the bound. */
+int oc_search(const oc_problem *p, uint64_t first_row, uint64_t n_rows, uint32_t bound, uint64_t rows_per_chunk,
+              uint32_t flags, uint64_t *best_idx, uint32_t *best_T, uint64_t *counters, int nthreads) {
+    if (check(p) || first_row + n_rows > p->A || p->S > 64 || p->T > 64) return -1;
+    oc_dag *g = dag_build((int)p->S, (int)p->M, (int)p->schedule);
+    uint64_t *binom = pascal((int)p->L - 1, (int)p->S - 1);
+    if (!g || !binom) { dag_free(g); free(binom); return -3; }
+    if (rows_per_chunk == 0) rows_per_chunk = n_rows ? n_rows : 1;
+    if (nthreads < 1) nthreads = 1;
+    if (nthreads > 256) nthreads = 256;
+    oc_sjob *jobs = calloc((size_t)nthreads, sizeof(oc_sjob));
+    pthread_t th[256];
+    if (!jobs) { dag_free(g); free(binom); return -3; }
+    uint64_t bT = UINT64_MAX, bR = UINT64_MAX, bK = UINT64_MAX;
+    uint64_t cnt[5] = {0, 0, 0, 0, 0};
+    int err = 0;
+    for (uint64_t c0 = 0; c0 < n_rows && !err; c0 += rows_per_chunk) {
+        uint64_t c1 = c0 + rows_per_chunk < n_rows ? c0 + rows_per_chunk : n_rows;
+        uint64_t n = c1 - c0;
+        int nt = (uint64_t)nthreads > n ? (int)n : nthreads;
+        for (int t = 0; t < nt; ++t) {
+            oc_sjob *j = &jobs[t];
+            memset(j, 0, sizeof(*j));
+            j->p = p; j->g = g; j->binom = binom;
+            j->row_lo = first_row + c0 + n * (uint64_t)t / (uint64_t)nt;
+            j->row_hi = first_row + c0 + n * (uint64_t)(t + 1) / (uint64_t)nt;
+            j->bound = bT < bound ? bT : bound;
+            j->ridge = (int)(flags & 1u);
+            j->stage_pruning = !(flags & 2u);
+            j->best_T = j->best_row = j->best_rank = UINT64_MAX;
+        }
+        for (int t = 1; t < nt; ++t) pthread_create(&th[t], NULL, s_worker, &jobs[t]);
+        s_worker(&jobs[0]);
+        for (int t = 1; t < nt; ++t) pthread_join(th[t], NULL);
+        /* the chunk's best, then strictly better than the earlier chunks' */
+        uint64_t cT = UINT64_MAX, cR = UINT64_MAX, cK = UINT64_MAX;
+        for (int t = 0; t < nt; ++t) {
+            oc_sjob *j = &jobs[t];
+            if (j->err) err = j->err;
+            cnt[0] += j->visited; cnt[1] += j->evaluated; cnt[2] += j->pr_mem;
+            cnt[3] += j->pr_ridge; cnt[4] += j->pr_bound;
+            if (j->best_T < cT || (j->best_T == cT && (j->best_row < cR ||
+                                   (j->best_row == cR && j->best_rank < cK)))) {
+                cT = j->best_T; cR = j->best_row; cK = j->best_rank;
+            }
+        }
+        if (cT < bT) { bT = cT; bR = cR; bK = cK; }
+    }
+    dag_free(g); free(binom); free(jobs);
+    if (err) return err;
+    if (bT > bound) { *best_idx = UINT64_MAX; *best_T = UINT32_MAX; }
+    else { *best_idx = bK * p->A + bR; *best_T = (uint32_t)bT; }
+    for (int i = 0; i < 5; ++i) counters[i] = cnt[i];
     return 0;
 }
