@@ -173,6 +173,46 @@ int poseidon_argmin(poseidon_ctx *ctx, const uint32_t *makespan, const uint32_t 
                     uint64_t count, uint64_t index_base, poseidon_best *best_out,
                     void *hip_stream);
 
+/* Pruned configuration search (Sec. 4.2.3).  For every assignment row a in
+ * [first_row, first_row + n_rows) (rows of the table, or base-T digits), the
+ * layers are allocated stage by stage, smaller layer counts first, and a
+ * partial configuration S_x (stages 1..x fixed) is discarded with all its
+ * extensions when stage x exceeds the memory of its device type, when
+ * (flag POSEIDON_SEARCH_RIDGE, layer-level pruning, Theorem 2) the layer
+ * counts of the stages of some device type are no longer ridge-like
+ * (non-decreasing, then non-increasing), or when g(S_x) of Eq. 2 exceeds the
+ * bound (stage-level pruning, Theorem 1; off with
+ * POSEIDON_SEARCH_NO_STAGE_PRUNING).  Complete configurations that pass are
+ * evaluated on the DAG.
+ * The rows are processed in consecutive chunks of rows_per_chunk rows
+ * (0 = one chunk); a chunk prunes against min(bound, best makespan of the
+ * earlier chunks), so every counter is deterministic for a given chunking.
+ * Result: among feasible (and, with the ridge flag, ridge-like) candidates
+ * of the rows with makespan <= bound, the smallest makespan, ties to the
+ * first in search order (row, then composition rank); best_out->index is
+ * its joint index rank * A + row.  Theorem 1 makes it the exhaustive
+ * optimum of those candidates.  POSEIDON_NO_FEASIBLE if there is none.
+ * best_out and stats_out are HOST pointers (either may be NULL); the call
+ * synchronises the stream after every level of the search.  Device memory
+ * for the frontiers (about 20 S MB per stage at S = 16) is allocated on the
+ * first call and kept by the context. */
+enum {
+    POSEIDON_SEARCH_RIDGE = 1,               /* layer-level pruning (Theorem 2) */
+    POSEIDON_SEARCH_NO_STAGE_PRUNING = 2     /* no Eq. 2 test on partial configurations */
+};
+
+typedef struct {
+    uint64_t visited;         /* partial or complete configurations accepted at a stage */
+    uint64_t evaluated;       /* complete configurations evaluated on the DAG */
+    uint64_t pruned_memory;   /* stage choices cut by a memory cap */
+    uint64_t pruned_ridge;    /* stage choices cut by the ridge test */
+    uint64_t pruned_bound;    /* stage choices cut by g(S_x) > bound */
+} poseidon_search_stats;
+
+int poseidon_search(poseidon_ctx *ctx, uint64_t first_row, uint64_t n_rows, uint32_t bound,
+                    uint64_t rows_per_chunk, uint32_t flags, poseidon_best *best_out,
+                    poseidon_search_stats *stats_out, void *hip_stream);
+
 /* Release the context's device memory.  NULL is ignored. */
 void poseidon_free(poseidon_ctx *ctx);
 

@@ -4,7 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "poseidon_kernels.h"
+#include "poseidon_search.h"
 
 namespace pk {
 
@@ -22,7 +22,11 @@ namespace pk {
     extern template hipError_t launch_bounded_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t,  \
                                                               uint64_t, uint64_t, uint32_t, uint32_t);        \
     extern template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool, bool);                                 \
-    extern template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool, bool);
+    extern template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool, bool);                                 \
+    extern template hipError_t launch_search_s<S, uint32_t>(int, const KParams &, const SearchParams &, uint32_t,   \
+                                                             size_t, hipStream_t);                                  \
+    extern template hipError_t launch_search_s<S, uint64_t>(int, const KParams &, const SearchParams &, uint32_t,   \
+                                                             size_t, hipStream_t);
 
 PK_EXTERN(1) PK_EXTERN(2) PK_EXTERN(3) PK_EXTERN(4) PK_EXTERN(5) PK_EXTERN(6) PK_EXTERN(7) PK_EXTERN(8)
 PK_EXTERN(9) PK_EXTERN(10) PK_EXTERN(11) PK_EXTERN(12) PK_EXTERN(13) PK_EXTERN(14) PK_EXTERN(15) PK_EXTERN(16)
@@ -39,6 +43,32 @@ __global__ __launch_bounds__(kBlock) void argmin_kernel(const uint32_t *T, const
         best = key < best ? key : best;
     }
     block_min_and_finish(best, acc, done, result, nullptr, true);
+}
+
+// Exclusive offsets of the block totals (one block); total to q.total.
+__global__ __launch_bounds__(kBlock) void search_scan_kernel(SearchParams q, uint32_t nblk) {
+    const uint32_t per = (nblk + kBlock - 1) / kBlock;
+    const uint32_t b0 = threadIdx.x * per, b1 = min(nblk, b0 + per);
+    unsigned long long s = 0;
+    for (uint32_t b = b0; b < b1; ++b) s += q.blk_tot[b];
+    unsigned long long total;
+    unsigned long long off = block_exclusive_scan_u64(s, total);
+    for (uint32_t b = b0; b < b1; ++b) {
+        q.blk_off[b] = off;
+        off += q.blk_tot[b];
+    }
+    if (threadIdx.x == 0) {
+        q.blk_off[nblk] = total;
+        *q.total = total;
+    }
+}
+
+// Start of a chunk: its bound is min(caller's bound, best so far).
+__global__ void search_bound_kernel(SearchParams q, uint32_t bound) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) {
+        const unsigned long long b = q.best[0];
+        *const_cast<uint32_t *>(q.bound) = b < bound ? (uint32_t)b : bound;
+    }
 }
 
 // Small fill kernel used instead of memset so that the calls stay capturable.
@@ -94,6 +124,20 @@ hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, bool ar, bool sched
 hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,
                          unsigned long long *acc, unsigned int *done, unsigned long long *result, hipStream_t st) {
     hipLaunchKernelGGL(argmin_kernel, dim3(grid), dim3(kBlock), 0, st, T, bits, count, acc, done, result);
+    return hipGetLastError();
+}
+
+hipError_t launch_search(int op, const KParams &p, const SearchParams &q, uint32_t grid, size_t lds, hipStream_t st) {
+    PK_DISPATCH(launch_search_s, p.S, p.wide, op, p, q, grid, lds, st)
+}
+
+hipError_t launch_search_scan(const SearchParams &q, uint32_t nblk, hipStream_t st) {
+    hipLaunchKernelGGL(search_scan_kernel, dim3(1), dim3(kBlock), 0, st, q, nblk);
+    return hipGetLastError();
+}
+
+hipError_t launch_search_bound(const SearchParams &q, uint32_t bound, hipStream_t st) {
+    hipLaunchKernelGGL(search_bound_kernel, dim3(1), dim3(64), 0, st, q, bound);
     return hipGetLastError();
 }
 

@@ -199,6 +199,7 @@ struct poseidon_ctx {
     uint32_t grid_max;
     void *ws;              // cut codes + straggler queues of the steady-state cascade
     uint64_t ws_cap;       // candidates per chunk the workspace holds
+    void *sws;             // search frontiers (allocated on the first poseidon_search)
 };
 
 extern "C" {
@@ -439,6 +440,7 @@ void poseidon_free(poseidon_ctx *ctx) {
     int prev = 0;
     if (hipGetDevice(&prev) == hipSuccess && hipSetDevice(ctx->device) == hipSuccess) {
         if (ctx->ws) (void)hipFree(ctx->ws);
+        if (ctx->sws) (void)hipFree(ctx->sws);
         (void)hipFree(ctx->dmem);
         (void)hipSetDevice(prev);
     }
@@ -696,3 +698,183 @@ int poseidon_argmin(poseidon_ctx *ctx, const uint32_t *makespan, const uint32_t 
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Pruned search (Sec. 4.2.3)
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr uint64_t kSearchCap = 1ull << 22;            // nodes per frontier piece
+constexpr uint32_t kSearchBlk = kSearchCap / 256;      // blocks per piece
+
+enum { SW_STATS = 0, SW_ACC = 5, SW_BEST = 6, SW_TOTAL = 9, SW_BOUND = 10, SW_COUNT = 11 };
+
+struct SearchWs {
+    uint32_t *row[pk::kSMax], *codes[pk::kSMax];
+    unsigned int *tot[pk::kSMax];
+    unsigned long long *off[pk::kSMax];
+    unsigned long long *words;
+};
+
+// Per level: rows, cut codes, block counts and offsets; then the state words.
+SearchWs search_layout(poseidon_ctx *ctx, size_t *bytes) {
+    SearchWs w;
+    memset(&w, 0, sizeof(w));
+    const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
+    unsigned char *b = (unsigned char *)ctx->sws;
+    size_t o = 0;
+    for (uint32_t l = 0; l < ctx->S; ++l) {
+        w.row[l] = (uint32_t *)(b + o); o += kSearchCap * 4;
+        w.codes[l] = (uint32_t *)(b + o); o += words * kSearchCap * 4;
+        w.tot[l] = (unsigned int *)(b + o); o += (size_t)kSearchBlk * 4;
+        w.off[l] = (unsigned long long *)(b + o); o += ((size_t)kSearchBlk + 1) * 8;
+    }
+    w.words = (unsigned long long *)(b + o); o += SW_COUNT * 8;
+    if (bytes) *bytes = o;
+    return w;
+}
+
+struct SearchRun {
+    poseidon_ctx *ctx;
+    pk::KParams kp;
+    pk::SearchParams q;
+    SearchWs w;
+    hipStream_t st;
+    std::vector<unsigned long long> off;
+};
+
+int search_read_total(SearchRun &r, unsigned long long *total) {
+    if (hipMemcpyAsync(total, r.w.words + SW_TOTAL, 8, hipMemcpyDeviceToHost, r.st) != hipSuccess ||
+        hipStreamSynchronize(r.st) != hipSuccess)
+        return POSEIDON_E_DEVICE;
+    return POSEIDON_OK;
+}
+
+// Expand the n nodes at level x (stored in the level's arrays) depth first.
+int search_expand(SearchRun &r, uint32_t x, uint64_t n) {
+    const uint32_t S = r.ctx->S;
+    pk::SearchParams q = r.q;
+    q.in_row = r.w.row[x];
+    q.in_codes = r.w.codes[x];
+    q.in_cap = kSearchCap;
+    q.n_in = (uint32_t)n;
+    q.level = x;
+    const uint32_t grid = (uint32_t)((n + 255) / 256);
+    const size_t lds = r.ctx->lds_bytes;
+    if (x + 1 == S) {
+        if (pk::launch_search(pk::kSearchOpLeaf, r.kp, q, grid, lds, r.st) != hipSuccess ||
+            pk::launch_search(pk::kSearchOpMerge, r.kp, q, 1, 0, r.st) != hipSuccess)
+            return POSEIDON_E_DEVICE;
+        return POSEIDON_OK;
+    }
+    q.blk_tot = r.w.tot[x];
+    q.blk_off = r.w.off[x];
+    q.out_row = r.w.row[x + 1];
+    q.out_codes = r.w.codes[x + 1];
+    q.out_cap = kSearchCap;
+    if (pk::launch_search(pk::kSearchOpCount, r.kp, q, grid, lds, r.st) != hipSuccess ||
+        pk::launch_search_scan(q, grid, r.st) != hipSuccess)
+        return POSEIDON_E_DEVICE;
+    unsigned long long total = 0;
+    int rc = search_read_total(r, &total);
+    if (rc != POSEIDON_OK) return rc;
+    if (total == 0) return POSEIDON_OK;
+    if (total <= kSearchCap) {
+        q.blk_base = 0;
+        if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, grid, lds, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
+        return search_expand(r, x + 1, total);
+    }
+    // more children than a level holds: write and expand them in pieces of
+    // whole blocks (one block has at most 256 * L < kSearchCap children)
+    std::vector<unsigned long long> off(grid + 1);
+    if (hipMemcpyAsync(off.data(), q.blk_off, (grid + 1) * 8, hipMemcpyDeviceToHost, r.st) != hipSuccess ||
+        hipStreamSynchronize(r.st) != hipSuccess)
+        return POSEIDON_E_DEVICE;
+    uint32_t b0 = 0;
+    while (b0 < grid) {
+        uint32_t b1 = b0 + 1;
+        while (b1 < grid && off[b1 + 1] - off[b0] <= kSearchCap) ++b1;
+        q.blk_base = b0;
+        if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, b1 - b0, lds, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
+        if (off[b1] > off[b0]) {
+            rc = search_expand(r, x + 1, off[b1] - off[b0]);
+            if (rc != POSEIDON_OK) return rc;
+        }
+        b0 = b1;
+    }
+    return POSEIDON_OK;
+}
+
+}  // namespace
+
+extern "C" int poseidon_search(poseidon_ctx *ctx, uint64_t first_row, uint64_t n_rows, uint32_t bound,
+                               uint64_t rows_per_chunk, uint32_t flags, poseidon_best *best_out,
+                               poseidon_search_stats *stats_out, void *hip_stream) {
+    if (!ctx || (flags & ~(uint32_t)(POSEIDON_SEARCH_RIDGE | POSEIDON_SEARCH_NO_STAGE_PRUNING))) return POSEIDON_E_INVAL;
+    if (first_row > ctx->A || n_rows > ctx->A - first_row) return POSEIDON_E_INVAL;
+    hipStream_t st = (hipStream_t)hip_stream;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return POSEIDON_E_DEVICE;
+    if (!ctx->sws) {
+        size_t bytes = 0;
+        search_layout(ctx, &bytes);
+        if (hipMalloc(&ctx->sws, bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            ctx->sws = nullptr;
+            return POSEIDON_E_NOMEM;
+        }
+    }
+    SearchRun r;
+    r.ctx = ctx;
+    r.kp = ctx->base;
+    r.st = st;
+    r.w = search_layout(ctx, nullptr);
+    memset(&r.q, 0, sizeof(r.q));
+    r.q.flags = flags;
+    r.q.stats = r.w.words + SW_STATS;
+    r.q.acc = r.w.words + SW_ACC;
+    r.q.best = r.w.words + SW_BEST;
+    r.q.total = r.w.words + SW_TOTAL;
+    r.q.bound = (uint32_t *)(r.w.words + SW_BOUND);
+    if (pk::launch_fill(r.q.stats, 5, 0ull, st) != hipSuccess ||
+        pk::launch_fill(r.q.acc, 4, ~0ull, st) != hipSuccess)
+        return POSEIDON_E_DEVICE;
+    const uint64_t chunk = rows_per_chunk ? rows_per_chunk : (n_rows ? n_rows : 1);
+    int rc = POSEIDON_OK;
+    for (uint64_t c0 = 0; c0 < n_rows && rc == POSEIDON_OK; c0 += chunk) {
+        const uint64_t c1 = std::min(n_rows, c0 + chunk);
+        // the chunk prunes against min(bound, best of the earlier chunks)
+        if (pk::launch_search_bound(r.q, bound, st) != hipSuccess) return POSEIDON_E_DEVICE;
+        for (uint64_t r0 = c0; r0 < c1 && rc == POSEIDON_OK; r0 += kSearchCap) {
+            const uint32_t n = (uint32_t)std::min<uint64_t>(kSearchCap, c1 - r0);
+            pk::SearchParams q = r.q;
+            q.out_row = r.w.row[0];
+            q.out_codes = r.w.codes[0];
+            q.out_cap = kSearchCap;
+            q.n_in = n;
+            q.root_first = (uint32_t)(first_row + r0);
+            if (pk::launch_search(pk::kSearchOpRoot, r.kp, q, (n + 255) / 256, 0, st) != hipSuccess)
+                return POSEIDON_E_DEVICE;
+            rc = search_expand(r, 0, n);
+        }
+    }
+    if (rc != POSEIDON_OK) return rc;
+    unsigned long long w[SW_COUNT];
+    if (hipMemcpyAsync(w, r.w.words, sizeof(w), hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+        return POSEIDON_E_DEVICE;
+    if (stats_out) {
+        stats_out->visited = w[SW_STATS];
+        stats_out->evaluated = w[SW_STATS + 1];
+        stats_out->pruned_memory = w[SW_STATS + 2];
+        stats_out->pruned_ridge = w[SW_STATS + 3];
+        stats_out->pruned_bound = w[SW_STATS + 4];
+    }
+    const bool found = w[SW_BEST] != ~0ull;
+    if (best_out) {
+        best_out->index = found ? w[SW_BEST + 2] * ctx->A + w[SW_BEST + 1] : UINT64_MAX;
+        best_out->makespan = found ? (uint32_t)w[SW_BEST] : 0xFFFFFFFFu;
+        best_out->feasible = found ? 1u : 0u;
+    }
+    return found ? POSEIDON_OK : POSEIDON_NO_FEASIBLE;
+}

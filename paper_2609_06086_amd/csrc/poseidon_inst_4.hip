@@ -1,6 +1,6 @@
 // Kernel instantiations for stage counts 16 (split so that the library
 // compiles in parallel).
-#include "poseidon_kernels.h"
+#include "poseidon_search.h"
 
 namespace pk {
 
@@ -16,7 +16,11 @@ namespace pk {
     template hipError_t launch_bounded_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t, uint64_t, \
                                                        uint64_t, uint32_t, uint32_t);                          \
     template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool, bool);                                        \
-    template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool, bool);
+    template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool, bool);                                        \
+    template hipError_t launch_search_s<S, uint32_t>(int, const KParams &, const SearchParams &, uint32_t, size_t,  \
+                                                      hipStream_t);                                                 \
+    template hipError_t launch_search_s<S, uint64_t>(int, const KParams &, const SearchParams &, uint32_t, size_t,  \
+                                                      hipStream_t);
 
 PK_INST(16)
 

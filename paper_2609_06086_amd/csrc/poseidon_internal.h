@@ -65,6 +65,30 @@ struct KParams {
     uint32_t accumulate;              // fold the chunk's best into *result (not the first chunk)
 };
 
+// Pruned search (Sec. 4.2.3): one piece of one frontier level.
+struct SearchParams {
+    const uint32_t *in_row;           // [in_cap] assignment row of each node
+    const uint32_t *in_codes;         // [words][in_cap] cut codes, cuts 1..level set
+    uint64_t in_cap;
+    uint32_t n_in;                    // nodes of this piece
+    uint32_t level;                   // stages 1..level fixed
+    uint32_t *out_row;                // children (or roots)
+    uint32_t *out_codes;              // [words][out_cap]
+    uint64_t out_cap;
+    unsigned int *blk_tot;            // children per block (count kernel)
+    unsigned long long *blk_off;      // exclusive offsets, [nblk] = total (scan kernel)
+    uint32_t blk_base;                // first block a write launch covers
+    uint32_t flags;                   // kSearchRidge | kSearchNoStage
+    uint32_t *bound;                  // the current chunk's bound
+    unsigned long long *stats;        // visited, evaluated, pruned by memory / ridge / bound
+    unsigned long long *acc;          // best (T << 32 | position) of a leaf piece
+    unsigned long long *best;         // makespan, row, composition rank of the best so far
+    unsigned long long *total;        // children of the last scanned level piece
+    uint32_t root_first;              // first row of a root piece
+};
+
+enum SearchOp { kSearchOpCount = 0, kSearchOpWrite = 1, kSearchOpLeaf = 2, kSearchOpMerge = 3, kSearchOpRoot = 4 };
+
 struct LaunchCfg {
     uint32_t grid;
     size_t lds_bytes;     // eval / resume / early-stop kernels: cost, pm, cap
@@ -79,6 +103,9 @@ hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, bool ar, bool sched
 hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,
                          unsigned long long *acc, unsigned int *done, unsigned long long *result, hipStream_t st);
 hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, hipStream_t st);
+hipError_t launch_search(int op, const KParams &p, const SearchParams &q, uint32_t grid, size_t lds, hipStream_t st);
+hipError_t launch_search_scan(const SearchParams &q, uint32_t nblk, hipStream_t st);
+hipError_t launch_search_bound(const SearchParams &q, uint32_t bound, hipStream_t st);
 int code_words(int S);
 int prologue_op(int S, int s, int k);
 int eager_op(int S, int M, int s, int k);   // Eager 1F1B closed form, M >= 2S-1: 0 idle, 1 F, 2 B, 3 F of depth 2

@@ -688,6 +688,38 @@ __device__ __forceinline__ void block_min_and_finish(unsigned long long v, unsig
     }
 }
 
+__device__ __forceinline__ unsigned long long wave_sum_u32(uint32_t v) {
+    unsigned long long s = v;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+    return s;
+}
+
+// Exclusive prefix sum over the block's threads in thread order; every
+// thread gets its offset and the block total.  All threads must call it.
+__device__ __forceinline__ unsigned long long block_exclusive_scan_u64(unsigned long long v,
+                                                                       unsigned long long &total) {
+    __shared__ unsigned long long wtot[kWaves];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    unsigned long long inc = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const unsigned long long u = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += u;
+    }
+    if (lane == 63) wtot[wave] = inc;
+    __syncthreads();
+    unsigned long long before = 0, all = 0;
+#pragma unroll
+    for (int k = 0; k < kWaves; ++k) {
+        before += k < wave ? wtot[k] : 0ull;
+        all += wtot[k];
+    }
+    __syncthreads();
+    total = all;
+    return before + inc - v;
+}
+
 __device__ __forceinline__ unsigned long long make_key(bool feasible, uint32_t T, uint32_t i) {
     return ((unsigned long long)(feasible ? T : 0xFFFFFFFFu) << 32) | i;
 }

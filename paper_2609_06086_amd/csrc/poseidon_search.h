@@ -1,0 +1,291 @@
+#pragma once
+// Device code of the pruned configuration search (Sec. 4.2.3): stage-level
+// pruning with Eq. 2 (Theorem 1) and layer-level pruning with the ridge
+// pattern (Theorem 2) over partial configurations, level by level.
+//
+// A frontier node is a partial configuration of one assignment row: the
+// row and the cut codes of stages 1..x (one byte per cut).  Every quantity
+// the tests need (prefix forward time, the inner max of Eq. 2, the last
+// backward time, the ridge state of a type) is recomputed from the cuts and
+// the LDS prefix tables, so a node is 4 + 4 * ceil((S-1)/4) bytes.
+//
+// Level x -> x+1 runs two kernels over the frontier.  The children of a node
+// are the end points hi = c_x+1, c_x+2, ... of stage x+1 up to the first
+// one that fails a test: the memory sum and g(S_{x+1}) only grow with hi,
+// and once a type's counts are falling the ridge test fails for every
+// larger count too, so the accepted children form one contiguous range.
+// search_count_kernel counts them per block; search_scan_kernel turns the
+// block counts into offsets; search_write_kernel writes the children in
+// node order (a block-local scan places each node's range), so the next
+// frontier is again in search order (row, then composition rank).  Nodes at
+// level S-1 go to search_leaf_kernel: last stage, tests, then the full DP.
+#include "poseidon_kernels.h"
+
+namespace pk {
+
+constexpr uint32_t kSearchRidge = 1u, kSearchNoStage = 2u;
+
+struct SearchNode {
+    uint32_t row, lo, t;          // row, c_x, type of stage x+1
+    uint32_t pre_f, inner, last_b;
+    int32_t last_l;               // last layer count of type t among stages 1..x (-1: none)
+    bool falling;                 // type t's counts have started to fall
+};
+
+// Prefix quantities of a node at level x (stages 1..x fixed).
+template <int S>
+__device__ __forceinline__ SearchNode search_node(const KParams &p, const Lds &tab, uint32_t row,
+                                                  const uint32_t (&w)[Codes<S>::kWords], uint32_t x,
+                                                  uint32_t (&ty)[S], uint32_t (&cut)[S + 1]) {
+    decode_types<S>(p, row, ty);
+    cut[0] = 0;
+#pragma unroll
+    for (int s = 1; s < S; ++s) cut[s] = (w[(s - 1) >> 2] >> (8 * ((s - 1) & 3))) & 0xFFu;
+    cut[S] = p.L;
+    SearchNode n;
+    n.row = row;
+    n.lo = 0;
+    n.t = ty[0];
+    n.pre_f = 0;
+    n.inner = 0;
+    n.last_b = 0;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        if ((uint32_t)s == x) { n.lo = cut[s]; n.t = ty[s]; }
+    }
+    n.last_l = -1;
+    n.falling = false;
+    const uint32_t row_len = p.L + 1;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        if ((uint32_t)s < x) {
+            const uint64_t *c = tab.cost + ty[s] * row_len;
+            const uint64_t hi = c[cut[s + 1]], lo = c[cut[s]];
+            const uint32_t f = (uint32_t)hi - (uint32_t)lo, b = (uint32_t)(hi >> 32) - (uint32_t)(lo >> 32);
+            const uint32_t d = p.has_ar ? tab.pd[ty[s] * row_len + cut[s + 1]] - tab.pd[ty[s] * row_len + cut[s]] : 0u;
+            n.inner = s == 0 ? d : max(n.inner + n.last_b, d);
+            n.pre_f += f;
+            n.last_b = b;
+            if (ty[s] == n.t) {
+                const int32_t l = (int32_t)(cut[s + 1] - cut[s]);
+                if (n.last_l >= 0 && l < n.last_l) n.falling = true;
+                n.last_l = l;
+            }
+        }
+    }
+    return n;
+}
+
+// Outcome of trying stage x+1 = [lo, hi): 0 accepted, 1 memory, 2 ridge, 3 bound.
+__device__ __forceinline__ int search_try(const KParams &p, const Lds &tab, const SearchNode &n, uint32_t x,
+                                          uint32_t hi, uint32_t flags, uint32_t bound) {
+    const uint32_t row_len = p.L + 1;
+    if (tab.pm[hi] - tab.pm[n.lo] > tab.cap[n.t]) return 1;
+    const int32_t l = (int32_t)(hi - n.lo);
+    if ((flags & kSearchRidge) && n.last_l >= 0 && n.falling && l > n.last_l) return 2;
+    if (!(flags & kSearchNoStage)) {
+        const uint64_t *c = tab.cost + n.t * row_len;
+        const uint64_t ch = c[hi], cl = c[n.lo];
+        const uint32_t f = (uint32_t)ch - (uint32_t)cl, b = (uint32_t)(ch >> 32) - (uint32_t)(cl >> 32);
+        const uint32_t d = p.has_ar ? tab.pd[n.t * row_len + hi] - tab.pd[n.t * row_len + n.lo] : 0u;
+        const uint32_t inn = x == 0 ? d : max(n.inner + n.last_b, d);
+        // Eq. 2: g(S_{x+1}) = sum_{i<=x} F_i + M (F_{x+1} + B_{x+1}) + inner
+        if (n.pre_f + p.M * (f + b) + inn > bound) return 3;
+    }
+    return 0;
+}
+
+// Children of a node at level x < S-1: accepted count and the rule that
+// stopped the range (0 if the range ran to its structural end).
+template <int S>
+__device__ __forceinline__ uint32_t search_children(const KParams &p, const Lds &tab, const SearchNode &n, uint32_t x,
+                                                    uint32_t flags, uint32_t bound, int &why) {
+    const uint32_t hmax = p.L - (S - 1 - x);   // every later stage keeps one layer
+    uint32_t cnt = 0;
+    why = 0;
+    for (uint32_t hi = n.lo + 1; hi <= hmax; ++hi) {
+        why = search_try(p, tab, n, x, hi, flags, bound);
+        if (why) break;
+        ++cnt;
+    }
+    return cnt;
+}
+
+__device__ __forceinline__ void search_flush(const SearchParams &q, unsigned int visited, unsigned int evaluated,
+                                             unsigned int mem, unsigned int ridge, unsigned int bound) {
+    __shared__ unsigned int c[5];
+    if (threadIdx.x < 5) c[threadIdx.x] = 0;
+    __syncthreads();
+    if (visited) atomicAdd(&c[0], visited);
+    if (evaluated) atomicAdd(&c[1], evaluated);
+    if (mem) atomicAdd(&c[2], mem);
+    if (ridge) atomicAdd(&c[3], ridge);
+    if (bound) atomicAdd(&c[4], bound);
+    __syncthreads();
+    if (threadIdx.x < 5 && c[threadIdx.x]) atomicAdd(&q.stats[threadIdx.x], (unsigned long long)c[threadIdx.x]);
+}
+
+template <int S>
+__device__ __forceinline__ void search_load(const SearchParams &q, uint32_t i, bool active, uint32_t &row,
+                                            uint32_t (&w)[Codes<S>::kWords]) {
+    row = active ? q.in_row[i] : 0u;
+#pragma unroll
+    for (int k = 0; k < Codes<S>::kWords; ++k) w[k] = active ? q.in_codes[(uint64_t)k * q.in_cap + i] : 0u;
+}
+
+// Count the children of every node of the piece; one total per block.
+template <int S>
+__global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchParams q) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const Lds tab = stage_tables(p, smem);
+    const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+    const bool active = i < q.n_in;
+    const uint32_t bound = *q.bound;
+    uint32_t row, w[Codes<S>::kWords], ty[S], cut[S + 1];
+    search_load<S>(q, i, active, row, w);
+    uint32_t cnt = 0;
+    int why = 0;
+    if (active) {
+        const SearchNode n = search_node<S>(p, tab, row, w, q.level, ty, cut);
+        cnt = search_children<S>(p, tab, n, q.level, q.flags, bound, why);
+    }
+    __shared__ unsigned int tot;
+    if (threadIdx.x == 0) tot = 0;
+    __syncthreads();
+    const unsigned int wsum = (unsigned int)wave_sum_u32(cnt);
+    if ((threadIdx.x & 63) == 0 && wsum) atomicAdd(&tot, wsum);
+    search_flush(q, cnt, 0, why == 1, why == 2, why == 3);
+    if (threadIdx.x == 0) q.blk_tot[blockIdx.x] = tot;
+}
+
+// Write the children of blocks [blk_base, blk_base + gridDim.x) in node
+// order, the first one at position 0 of the output.
+template <int S>
+__global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchParams q) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const Lds tab = stage_tables(p, smem);
+    constexpr int NW = Codes<S>::kWords;
+    const uint32_t blk = q.blk_base + blockIdx.x;
+    const uint32_t i = blk * kBlock + threadIdx.x;
+    const bool active = i < q.n_in;
+    const uint32_t bound = *q.bound;
+    uint32_t row, w[NW], ty[S], cut[S + 1];
+    search_load<S>(q, i, active, row, w);
+    uint32_t cnt = 0;
+    int why = 0;
+    SearchNode n{};
+    if (active) {
+        n = search_node<S>(p, tab, row, w, q.level, ty, cut);
+        cnt = search_children<S>(p, tab, n, q.level, q.flags, bound, why);
+    }
+    unsigned long long total;
+    const unsigned long long local = block_exclusive_scan_u64(cnt, total);
+    const unsigned long long base = q.blk_off[blk] - q.blk_off[q.blk_base] + local;
+    const uint32_t x = q.level;   // the new cut is byte x of the codes
+    for (uint32_t j = 0; j < cnt; ++j) {
+        const uint64_t o = base + j;
+        const uint32_t hi = n.lo + 1 + j;
+        q.out_row[o] = row;
+#pragma unroll
+        for (int k = 0; k < NW; ++k) {
+            const uint32_t v = (uint32_t)k == (x >> 2) ? (w[k] | (hi << (8 * (x & 3)))) : w[k];
+            q.out_codes[(uint64_t)k * q.out_cap + o] = v;
+        }
+    }
+}
+
+// Level S-1: the last stage is [c_{S-1}, L); test it like any stage, then
+// evaluate the complete configuration on the DAG.  Reduces
+// (T << 32 | position) over the candidates with T <= bound into *q.acc.
+template <int S, bool AR, bool SCH>
+__global__ __launch_bounds__(kBlock) void search_leaf_kernel(KParams p, SearchParams q) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const Lds tab = stage_tables(p, smem);
+    const Comm<S> comm = load_comm<S>(p);
+    constexpr int NW = Codes<S>::kWords;
+    const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+    const bool active = i < q.n_in;
+    const uint32_t bound = *q.bound;
+    uint32_t row, w[NW], ty[S], cut[S + 1];
+    search_load<S>(q, i, active, row, w);
+    int why = 4;
+    unsigned long long key = ~0ull;
+    if (active) {
+        const SearchNode n = search_node<S>(p, tab, row, w, S - 1, ty, cut);
+        why = search_try(p, tab, n, S - 1, p.L, q.flags, bound);
+    }
+    const bool leaf = why == 0;
+    if (leaf) {
+        uint32_t F[S], B[S], Y[S];
+        stage_weights<S>(p, tab, cut, ty, F, B);
+        dp_full<S, SCH>(p, F, B, comm, Y);
+        const uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, row);
+        if (T <= bound) key = ((unsigned long long)T << 32) | i;
+    }
+    search_flush(q, leaf, leaf, why == 1, why == 2, why == 3);
+    block_min_and_finish(key, q.acc, nullptr, nullptr, nullptr, false);
+}
+
+// After a leaf piece: the piece's best candidate replaces the best so far
+// only if strictly better (earlier pieces and chunks come first in search
+// order).  best[0..2] = makespan, row, composition rank.
+template <typename R>
+__global__ void search_merge_kernel(KParams p, SearchParams q) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    const unsigned long long key = *q.acc;
+    *q.acc = ~0ull;
+    if (key == ~0ull) return;
+    const uint64_t T = key >> 32;
+    const uint32_t pos = (uint32_t)key;
+    if (T >= q.best[0]) return;
+    const R *binom = reinterpret_cast<const R *>(p.binom);
+    const uint32_t S = p.S, L = p.L;
+    // rank = sum_j C(L - 1 - c_{j-1}, S - j) - C(L - c_j, S - j)   (hockey-stick identity)
+    uint64_t rank = 0;
+    uint32_t prev = 0;
+    for (uint32_t j = 1; j < S; ++j) {
+        const uint32_t wj = q.in_codes[(uint64_t)((j - 1) >> 2) * q.in_cap + pos];
+        const uint32_t c = (wj >> (8 * ((j - 1) & 3))) & 0xFFu;
+        const uint32_t k = S - j;
+        rank += (uint64_t)binom[k * kNB + (L - 1 - prev)] - (uint64_t)binom[k * kNB + (L - c)];
+        prev = c;
+    }
+    q.best[0] = T;
+    q.best[1] = q.in_row[pos];
+    q.best[2] = rank;
+}
+
+// Roots of a piece of rows: level-0 nodes with no cut.
+template <int S>
+__global__ __launch_bounds__(kBlock) void search_root_kernel(SearchParams q, uint32_t first_row, uint32_t n) {
+    const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n) return;
+    q.out_row[i] = first_row + i;
+#pragma unroll
+    for (int k = 0; k < Codes<S>::kWords; ++k) q.out_codes[(uint64_t)k * q.out_cap + i] = 0u;
+}
+
+// ---------------------------------------------------------------------------
+template <int S, typename R>
+hipError_t launch_search_s(int op, const KParams &p, const SearchParams &q, uint32_t grid, size_t lds,
+                           hipStream_t st) {
+    const dim3 g(grid), b(kBlock);
+    switch (op) {
+    case kSearchOpCount: hipLaunchKernelGGL((search_count_kernel<S>), g, b, lds, st, p, q); break;
+    case kSearchOpWrite: hipLaunchKernelGGL((search_write_kernel<S>), g, b, lds, st, p, q); break;
+    case kSearchOpLeaf: {
+        const bool sch = p.sched != 0;
+        if (p.has_ar && sch) hipLaunchKernelGGL((search_leaf_kernel<S, true, true>), g, b, lds, st, p, q);
+        else if (p.has_ar) hipLaunchKernelGGL((search_leaf_kernel<S, true, false>), g, b, lds, st, p, q);
+        else if (sch) hipLaunchKernelGGL((search_leaf_kernel<S, false, true>), g, b, lds, st, p, q);
+        else hipLaunchKernelGGL((search_leaf_kernel<S, false, false>), g, b, lds, st, p, q);
+        break;
+    }
+    case kSearchOpMerge: hipLaunchKernelGGL((search_merge_kernel<R>), dim3(1), dim3(64), 0, st, p, q); break;
+    case kSearchOpRoot: hipLaunchKernelGGL((search_root_kernel<S>), g, b, 0, st, q, q.root_first, q.n_in); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace pk

@@ -25,6 +25,7 @@ POSEIDON_E_RANGE = -2
 POSEIDON_E_DEVICE = -3
 POSEIDON_E_NOMEM = -4
 SCHEDULE_1F1B, SCHEDULE_EAGER_1F1B = 0, 1
+SEARCH_RIDGE, SEARCH_NO_STAGE_PRUNING = 1, 2
 S_MAX, L_MAX, T_MAX = 16, 256, 8
 
 
@@ -52,6 +53,11 @@ class _Best(C.Structure):
     _fields_ = [("index", C.c_uint64), ("makespan", C.c_uint32), ("feasible", C.c_uint32)]
 
 
+class _SearchStats(C.Structure):
+    _fields_ = [("visited", C.c_uint64), ("evaluated", C.c_uint64), ("pruned_memory", C.c_uint64),
+                ("pruned_ridge", C.c_uint64), ("pruned_bound", C.c_uint64)]
+
+
 class _Stats(C.Structure):
     _fields_ = [("evaluated", C.c_uint64), ("pruned", C.c_uint64), ("infeasible", C.c_uint64)]
 
@@ -70,9 +76,18 @@ class PruneStats:
     infeasible: int
 
 
+@dataclass
+class SearchStats:
+    visited: int
+    evaluated: int
+    pruned_memory: int
+    pruned_ridge: int
+    pruned_bound: int
+
+
 EXPORTS = ("poseidon_validate", "poseidon_load_costs", "poseidon_eval_candidates",
            "poseidon_last_best", "poseidon_eval_candidates_bounded", "poseidon_argmin",
-           "poseidon_free", "poseidon_strerror")
+           "poseidon_search", "poseidon_free", "poseidon_strerror")
 
 _lib = None
 
@@ -99,6 +114,9 @@ def lib():
         L.poseidon_argmin.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_uint64, C.c_uint64,
                                       C.POINTER(_Best), C.c_void_p]
         L.poseidon_argmin.restype = C.c_int
+        L.poseidon_search.argtypes = [C.c_void_p, C.c_uint64, C.c_uint64, C.c_uint32, C.c_uint64, C.c_uint32,
+                                      C.POINTER(_Best), C.POINTER(_SearchStats), C.c_void_p]
+        L.poseidon_search.restype = C.c_int
         L.poseidon_free.argtypes = [C.c_void_p]
         L.poseidon_free.restype = None
         L.poseidon_strerror.argtypes = [C.c_int]
@@ -167,6 +185,7 @@ class Context:
     def __init__(self, handle: int, prob):
         self.handle = handle
         self.S, self.M, self.L, self.T = prob.S, prob.M, prob.L, prob.T
+        self.A = int(prob.A)
 
     def close(self):
         if self.handle:
@@ -246,6 +265,21 @@ def poseidon_argmin(ctx: Context, makespan, feasible_bits=None, *, count: Option
     if rc < 0:
         raise PoseidonError(rc, "poseidon_argmin")
     return _best(rc, b)
+
+
+def poseidon_search(ctx: Context, bound: int = 2 ** 31 - 1, *, first_row: int = 0, n_rows: Optional[int] = None,
+                    rows_per_chunk: int = 0, ridge: bool = False, stage_pruning: bool = True, stream=None):
+    """Pruned configuration search over assignment rows; returns (Best, SearchStats).
+    Best.index is the joint index rank * A + row."""
+    n = ctx.A - first_row if n_rows is None else n_rows
+    flags = (SEARCH_RIDGE if ridge else 0) | (0 if stage_pruning else SEARCH_NO_STAGE_PRUNING)
+    b, s = _Best(), _SearchStats()
+    rc = lib().poseidon_search(ctx.handle, int(first_row), int(n), int(bound), int(rows_per_chunk), flags,
+                               C.byref(b), C.byref(s), _stream(stream))
+    if rc < 0:
+        raise PoseidonError(rc, "poseidon_search")
+    return _best(rc, b), SearchStats(int(s.visited), int(s.evaluated), int(s.pruned_memory),
+                                     int(s.pruned_ridge), int(s.pruned_bound))
 
 
 def poseidon_free(ctx: Context) -> None:

@@ -129,3 +129,8 @@ def test_closed_form_schedules_pass_the_host_self_check():
                 with pytest.raises(P.PoseidonError) as ei:
                     P.poseidon_load_costs(p, 0)
                 assert ei.value.status == P.POSEIDON_E_DEVICE, (sched, S, M)
+
+
+def test_search_rejects_bad_arguments_before_device():
+    b, st = P._Best(), P._SearchStats()
+    assert P.lib().poseidon_search(None, 0, 1, 100, 0, 0, P.C.byref(b), P.C.byref(st), None) == P.POSEIDON_E_INVAL
