@@ -17,8 +17,11 @@
 // search_count_kernel counts them per block; search_scan_kernel turns the
 // block counts into offsets; search_write_kernel writes the children in
 // node order (a block-local scan places each node's range), so the next
-// frontier is again in search order (row, then composition rank).  Nodes at
-// level S-1 go to search_leaf_kernel: last stage, tests, then the full DP.
+// frontier is again in search order (row, then composition rank).  The
+// level that fixes the last cut (x = S-2) also tests the last stage, which
+// that cut determines, and keeps only the children that pass, so the widest
+// level is never written in full.  search_leaf_kernel runs the full DP on
+// the complete configurations.
 #include "poseidon_kernels.h"
 
 namespace pk {
@@ -30,6 +33,9 @@ struct SearchNode {
     uint32_t pre_f, inner, last_b;
     int32_t last_l;               // last layer count of type t among stages 1..x (-1: none)
     bool falling;                 // type t's counts have started to fall
+    uint32_t tS;                  // type of stage S, with its ridge state over stages 1..x
+    int32_t last_lS;
+    bool fallingS;
 };
 
 // Prefix quantities of a node at level x (stages 1..x fixed).
@@ -55,6 +61,9 @@ __device__ __forceinline__ SearchNode search_node(const KParams &p, const Lds &t
     }
     n.last_l = -1;
     n.falling = false;
+    n.tS = ty[S - 1];
+    n.last_lS = -1;
+    n.fallingS = false;
     const uint32_t row_len = p.L + 1;
 #pragma unroll
     for (int s = 0; s < S; ++s) {
@@ -66,10 +75,14 @@ __device__ __forceinline__ SearchNode search_node(const KParams &p, const Lds &t
             n.inner = s == 0 ? d : max(n.inner + n.last_b, d);
             n.pre_f += f;
             n.last_b = b;
+            const int32_t l = (int32_t)(cut[s + 1] - cut[s]);
             if (ty[s] == n.t) {
-                const int32_t l = (int32_t)(cut[s + 1] - cut[s]);
                 if (n.last_l >= 0 && l < n.last_l) n.falling = true;
                 n.last_l = l;
+            }
+            if (ty[s] == n.tS) {
+                if (n.last_lS >= 0 && l < n.last_lS) n.fallingS = true;
+                n.last_lS = l;
             }
         }
     }
@@ -95,20 +108,70 @@ __device__ __forceinline__ int search_try(const KParams &p, const Lds &tab, cons
     return 0;
 }
 
-// Children of a node at level x < S-1: accepted count and the rule that
-// stopped the range (0 if the range ran to its structural end).
-template <int S>
-__device__ __forceinline__ uint32_t search_children(const KParams &p, const Lds &tab, const SearchNode &n, uint32_t x,
-                                                    uint32_t flags, uint32_t bound, int &why) {
+// The node extended by stage x+1 = [lo, hi), as seen by the test of the
+// last stage S = [hi, L) (used when x + 2 == S).
+__device__ __forceinline__ SearchNode search_extend_to_last(const KParams &p, const Lds &tab, const SearchNode &n,
+                                                            uint32_t x, uint32_t hi, uint32_t typ_next) {
+    const uint32_t row_len = p.L + 1;
+    const uint64_t *c = tab.cost + n.t * row_len;
+    const uint64_t ch = c[hi], cl = c[n.lo];
+    const uint32_t f = (uint32_t)ch - (uint32_t)cl, b = (uint32_t)(ch >> 32) - (uint32_t)(cl >> 32);
+    const uint32_t d = p.has_ar ? tab.pd[n.t * row_len + hi] - tab.pd[n.t * row_len + n.lo] : 0u;
+    SearchNode m = n;
+    m.inner = x == 0 ? d : max(n.inner + n.last_b, d);
+    m.pre_f = n.pre_f + f;
+    m.last_b = b;
+    m.lo = hi;
+    m.t = typ_next;
+    m.last_l = n.last_lS;
+    m.falling = n.fallingS;
+    if (n.t == typ_next) {
+        const int32_t l = (int32_t)(hi - n.lo);
+        if (m.last_l >= 0 && l < m.last_l) m.falling = true;
+        m.last_l = l;
+    }
+    return m;
+}
+
+// Children of a node at level x < S-1.  The accepted choices of stage x+1
+// form the range lo+1 .. lo+acc; why = the rule that stopped it (0: it ran
+// to its structural end).  When x + 2 == S a child fixes every cut, so the
+// last stage is tested here too and only children that pass it are kept
+// (out of acc; the failures are counted per rule in lp[1..3]).  With
+// WRITE the kept children are written from position `base` on, in order.
+template <int S, bool WRITE>
+__device__ __forceinline__ uint32_t search_children(const KParams &p, const Lds &tab, const SearchNode &n,
+                                                    uint32_t x, uint32_t flags, uint32_t bound, int &why,
+                                                    uint32_t &acc, uint32_t (&lp)[4], const SearchParams &q,
+                                                    uint64_t base, const uint32_t (&w)[Codes<S>::kWords]) {
+    constexpr int NW = Codes<S>::kWords;
     const uint32_t hmax = p.L - (S - 1 - x);   // every later stage keeps one layer
-    uint32_t cnt = 0;
+    const bool last_cut = x + 2 == (uint32_t)S;
+    uint32_t out = 0;
+    acc = 0;
     why = 0;
     for (uint32_t hi = n.lo + 1; hi <= hmax; ++hi) {
         why = search_try(p, tab, n, x, hi, flags, bound);
         if (why) break;
-        ++cnt;
+        ++acc;
+        if (last_cut) {
+            const SearchNode m = search_extend_to_last(p, tab, n, x, hi, n.tS);
+            const int w2 = search_try(p, tab, m, x + 1, p.L, flags, bound);
+            lp[w2] += 1;
+            if (w2) continue;
+        }
+        if (WRITE) {
+            const uint64_t o = base + out;
+            q.out_row[o] = n.row;
+#pragma unroll
+            for (int k = 0; k < NW; ++k) {
+                const uint32_t v = (uint32_t)k == (x >> 2) ? (w[k] | (hi << (8 * (x & 3)))) : w[k];
+                q.out_codes[(uint64_t)k * q.out_cap + o] = v;
+            }
+        }
+        ++out;
     }
-    return cnt;
+    return out;
 }
 
 __device__ __forceinline__ void search_flush(const SearchParams &q, unsigned int visited, unsigned int evaluated,
@@ -143,18 +206,20 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
     const uint32_t bound = *q.bound;
     uint32_t row, w[Codes<S>::kWords], ty[S], cut[S + 1];
     search_load<S>(q, i, active, row, w);
-    uint32_t cnt = 0;
+    uint32_t cnt = 0, acc = 0, lp[4] = {0, 0, 0, 0};
     int why = 0;
     if (active) {
         const SearchNode n = search_node<S>(p, tab, row, w, q.level, ty, cut);
-        cnt = search_children<S>(p, tab, n, q.level, q.flags, bound, why);
+        cnt = search_children<S, false>(p, tab, n, q.level, q.flags, bound, why, acc, lp, q, 0, w);
     }
     __shared__ unsigned int tot;
     if (threadIdx.x == 0) tot = 0;
     __syncthreads();
     const unsigned int wsum = (unsigned int)wave_sum_u32(cnt);
     if ((threadIdx.x & 63) == 0 && wsum) atomicAdd(&tot, wsum);
-    search_flush(q, cnt, 0, why == 1, why == 2, why == 3);
+    // a child that completes the configuration and passes the last stage
+    // counts as visited twice (its stage x+1 and its stage S) and evaluated
+    search_flush(q, acc + lp[0], lp[0], (why == 1) + lp[1], (why == 2) + lp[2], (why == 3) + lp[3]);
     if (threadIdx.x == 0) q.blk_tot[blockIdx.x] = tot;
 }
 
@@ -164,34 +229,24 @@ template <int S>
 __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchParams q) {
     extern __shared__ __align__(16) unsigned char smem[];
     const Lds tab = stage_tables(p, smem);
-    constexpr int NW = Codes<S>::kWords;
     const uint32_t blk = q.blk_base + blockIdx.x;
     const uint32_t i = blk * kBlock + threadIdx.x;
     const bool active = i < q.n_in;
     const uint32_t bound = *q.bound;
-    uint32_t row, w[NW], ty[S], cut[S + 1];
+    uint32_t row, w[Codes<S>::kWords], ty[S], cut[S + 1];
     search_load<S>(q, i, active, row, w);
-    uint32_t cnt = 0;
+    uint32_t cnt = 0, acc = 0, lp[4] = {0, 0, 0, 0};
     int why = 0;
     SearchNode n{};
     if (active) {
         n = search_node<S>(p, tab, row, w, q.level, ty, cut);
-        cnt = search_children<S>(p, tab, n, q.level, q.flags, bound, why);
+        cnt = search_children<S, false>(p, tab, n, q.level, q.flags, bound, why, acc, lp, q, 0, w);
     }
     unsigned long long total;
     const unsigned long long local = block_exclusive_scan_u64(cnt, total);
-    const unsigned long long base = q.blk_off[blk] - q.blk_off[q.blk_base] + local;
-    const uint32_t x = q.level;   // the new cut is byte x of the codes
-    for (uint32_t j = 0; j < cnt; ++j) {
-        const uint64_t o = base + j;
-        const uint32_t hi = n.lo + 1 + j;
-        q.out_row[o] = row;
-#pragma unroll
-        for (int k = 0; k < NW; ++k) {
-            const uint32_t v = (uint32_t)k == (x >> 2) ? (w[k] | (hi << (8 * (x & 3)))) : w[k];
-            q.out_codes[(uint64_t)k * q.out_cap + o] = v;
-        }
-    }
+    if (active && cnt)
+        search_children<S, true>(p, tab, n, q.level, q.flags, bound, why, acc, lp, q,
+                                 q.blk_off[blk] - q.blk_off[q.blk_base] + local, w);
 }
 
 // Level S-1: the last stage is [c_{S-1}, L); test it like any stage, then
@@ -212,7 +267,8 @@ __global__ __launch_bounds__(kBlock) void search_leaf_kernel(KParams p, SearchPa
     unsigned long long key = ~0ull;
     if (active) {
         const SearchNode n = search_node<S>(p, tab, row, w, S - 1, ty, cut);
-        why = search_try(p, tab, n, S - 1, p.L, q.flags, bound);
+        // for S > 1 the level that fixed the last cut already tested the last stage
+        why = S == 1 ? search_try(p, tab, n, S - 1, p.L, q.flags, bound) : 0;
     }
     const bool leaf = why == 0;
     if (leaf) {
@@ -222,7 +278,7 @@ __global__ __launch_bounds__(kBlock) void search_leaf_kernel(KParams p, SearchPa
         const uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, row);
         if (T <= bound) key = ((unsigned long long)T << 32) | i;
     }
-    search_flush(q, leaf, leaf, why == 1, why == 2, why == 3);
+    if (S == 1) search_flush(q, leaf, leaf, why == 1, why == 2, why == 3);
     block_min_and_finish(key, q.acc, nullptr, nullptr, nullptr, false);
 }
 
