@@ -49,14 +49,31 @@ __global__ __launch_bounds__(kBlock) void argmin_kernel(const uint32_t *T, const
 __global__ __launch_bounds__(kBlock) void search_scan_kernel(SearchParams q, uint32_t nblk) {
     const uint32_t per = (nblk + kBlock - 1) / kBlock;
     const uint32_t b0 = threadIdx.x * per, b1 = min(nblk, b0 + per);
-    unsigned long long s = 0;
+    unsigned long long s = 0, c[5] = {0, 0, 0, 0, 0};
+    // independent loads, several in flight per thread
+#pragma unroll 8
     for (uint32_t b = b0; b < b1; ++b) s += q.blk_tot[b];
+    // the counters need no order: coalesced strided sums
+    for (uint32_t b = threadIdx.x; b < nblk; b += kBlock) {
+#pragma unroll
+        for (int k = 0; k < 5; ++k) c[k] += q.blk_cnt[(uint64_t)k * q.blk_stride + b];
+    }
     unsigned long long total;
     unsigned long long off = block_exclusive_scan_u64(s, total);
+#pragma unroll 8
     for (uint32_t b = b0; b < b1; ++b) {
         q.blk_off[b] = off;
         off += q.blk_tot[b];
     }
+    // the level's counters: one global atomic per counter
+    __shared__ unsigned long long sum[5];
+    if (threadIdx.x < 5) sum[threadIdx.x] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 5; ++k)
+        if (c[k]) atomicAdd(&sum[k], c[k]);
+    __syncthreads();
+    if (threadIdx.x < 5 && sum[threadIdx.x]) atomicAdd(&q.stats[threadIdx.x], sum[threadIdx.x]);
     if (threadIdx.x == 0) {
         q.blk_off[nblk] = total;
         *q.total = total;

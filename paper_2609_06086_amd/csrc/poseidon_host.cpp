@@ -712,6 +712,7 @@ enum { SW_STATS = 0, SW_ACC = 5, SW_BEST = 6, SW_TOTAL = 9, SW_BOUND = 10, SW_CO
 struct SearchWs {
     uint32_t *row[pk::kSMax], *codes[pk::kSMax];
     unsigned int *tot[pk::kSMax];
+    unsigned int *cnt[pk::kSMax];
     unsigned long long *off[pk::kSMax];
     unsigned long long *words;
 };
@@ -727,6 +728,7 @@ SearchWs search_layout(poseidon_ctx *ctx, size_t *bytes) {
         w.row[l] = (uint32_t *)(b + o); o += kSearchCap * 4;
         w.codes[l] = (uint32_t *)(b + o); o += words * kSearchCap * 4;
         w.tot[l] = (unsigned int *)(b + o); o += (size_t)kSearchBlk * 4;
+        w.cnt[l] = (unsigned int *)(b + o); o += (size_t)kSearchBlk * 4 * 5;
         w.off[l] = (unsigned long long *)(b + o); o += ((size_t)kSearchBlk + 1) * 8;
     }
     w.words = (unsigned long long *)(b + o); o += SW_COUNT * 8;
@@ -769,6 +771,8 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n) {
     }
     q.blk_tot = r.w.tot[x];
     q.blk_off = r.w.off[x];
+    q.blk_cnt = r.w.cnt[x];
+    q.blk_stride = kSearchBlk;
     q.out_row = r.w.row[x + 1];
     q.out_codes = r.w.codes[x + 1];
     q.out_cap = kSearchCap;

@@ -77,6 +77,8 @@ struct SearchParams {
     uint64_t out_cap;
     unsigned int *blk_tot;            // children per block (count kernel)
     unsigned long long *blk_off;      // exclusive offsets, [nblk] = total (scan kernel)
+    unsigned int *blk_cnt;            // [5][blk_stride] per-block counters (count kernel)
+    uint64_t blk_stride;
     uint32_t blk_base;                // first block a write launch covers
     uint32_t flags;                   // kSearchRidge | kSearchNoStage
     uint32_t *bound;                  // the current chunk's bound

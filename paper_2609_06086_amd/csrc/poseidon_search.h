@@ -133,16 +133,21 @@ __device__ __forceinline__ SearchNode search_extend_to_last(const KParams &p, co
     return m;
 }
 
+// Outcomes of the last-stage test of the children of one node.
+struct LastStage {
+    uint32_t pass = 0, mem = 0, ridge = 0, bound = 0;
+};
+
 // Children of a node at level x < S-1.  The accepted choices of stage x+1
 // form the range lo+1 .. lo+acc; why = the rule that stopped it (0: it ran
 // to its structural end).  When x + 2 == S a child fixes every cut, so the
 // last stage is tested here too and only children that pass it are kept
-// (out of acc; the failures are counted per rule in lp[1..3]).  With
-// WRITE the kept children are written from position `base` on, in order.
+// (lp counts the outcomes).  With WRITE the kept children are written from
+// position `base` on, in order.
 template <int S, bool WRITE>
 __device__ __forceinline__ uint32_t search_children(const KParams &p, const Lds &tab, const SearchNode &n,
                                                     uint32_t x, uint32_t flags, uint32_t bound, int &why,
-                                                    uint32_t &acc, uint32_t (&lp)[4], const SearchParams &q,
+                                                    uint32_t &acc, LastStage &lp, const SearchParams &q,
                                                     uint64_t base, const uint32_t (&w)[Codes<S>::kWords]) {
     constexpr int NW = Codes<S>::kWords;
     const uint32_t hmax = p.L - (S - 1 - x);   // every later stage keeps one layer
@@ -157,7 +162,10 @@ __device__ __forceinline__ uint32_t search_children(const KParams &p, const Lds 
         if (last_cut) {
             const SearchNode m = search_extend_to_last(p, tab, n, x, hi, n.tS);
             const int w2 = search_try(p, tab, m, x + 1, p.L, flags, bound);
-            lp[w2] += 1;
+            lp.pass += w2 == 0;
+            lp.mem += w2 == 1;
+            lp.ridge += w2 == 2;
+            lp.bound += w2 == 3;
             if (w2) continue;
         }
         if (WRITE) {
@@ -188,6 +196,20 @@ __device__ __forceinline__ void search_flush(const SearchParams &q, unsigned int
     if (threadIdx.x < 5 && c[threadIdx.x]) atomicAdd(&q.stats[threadIdx.x], (unsigned long long)c[threadIdx.x]);
 }
 
+__device__ __forceinline__ void search_block_counts(const SearchParams &q, unsigned int visited, unsigned int evaluated,
+                                                    unsigned int mem, unsigned int ridge, unsigned int bound) {
+    __shared__ unsigned int c[5];
+    if (threadIdx.x < 5) c[threadIdx.x] = 0;
+    __syncthreads();
+    if (visited) atomicAdd(&c[0], visited);
+    if (evaluated) atomicAdd(&c[1], evaluated);
+    if (mem) atomicAdd(&c[2], mem);
+    if (ridge) atomicAdd(&c[3], ridge);
+    if (bound) atomicAdd(&c[4], bound);
+    __syncthreads();
+    if (threadIdx.x < 5) q.blk_cnt[(uint64_t)threadIdx.x * q.blk_stride + blockIdx.x] = c[threadIdx.x];
+}
+
 template <int S>
 __device__ __forceinline__ void search_load(const SearchParams &q, uint32_t i, bool active, uint32_t &row,
                                             uint32_t (&w)[Codes<S>::kWords]) {
@@ -206,7 +228,8 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
     const uint32_t bound = *q.bound;
     uint32_t row, w[Codes<S>::kWords], ty[S], cut[S + 1];
     search_load<S>(q, i, active, row, w);
-    uint32_t cnt = 0, acc = 0, lp[4] = {0, 0, 0, 0};
+    uint32_t cnt = 0, acc = 0;
+    LastStage lp;
     int why = 0;
     if (active) {
         const SearchNode n = search_node<S>(p, tab, row, w, q.level, ty, cut);
@@ -218,8 +241,10 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
     const unsigned int wsum = (unsigned int)wave_sum_u32(cnt);
     if ((threadIdx.x & 63) == 0 && wsum) atomicAdd(&tot, wsum);
     // a child that completes the configuration and passes the last stage
-    // counts as visited twice (its stage x+1 and its stage S) and evaluated
-    search_flush(q, acc + lp[0], lp[0], (why == 1) + lp[1], (why == 2) + lp[2], (why == 3) + lp[3]);
+    // counts as visited twice (its stage x+1 and its stage S) and evaluated.
+    // The block's counts go to per-block slots that the scan kernel sums
+    // (one global atomic per counter and launch instead of per block).
+    search_block_counts(q, acc + lp.pass, lp.pass, (why == 1) + lp.mem, (why == 2) + lp.ridge, (why == 3) + lp.bound);
     if (threadIdx.x == 0) q.blk_tot[blockIdx.x] = tot;
 }
 
@@ -235,7 +260,8 @@ __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchP
     const uint32_t bound = *q.bound;
     uint32_t row, w[Codes<S>::kWords], ty[S], cut[S + 1];
     search_load<S>(q, i, active, row, w);
-    uint32_t cnt = 0, acc = 0, lp[4] = {0, 0, 0, 0};
+    uint32_t cnt = 0, acc = 0;
+    LastStage lp;
     int why = 0;
     SearchNode n{};
     if (active) {
