@@ -75,6 +75,88 @@ def cpu_baseline(wl, target_s):
                       f"Kahn order, topological DP) on {threads} host threads, {dt:.1f} s"}
 
 
+SEARCH_OPS_PER_TEST = 15   # integer ops of one stage-choice test (memory 2, ridge 2, Eq. 2 11)
+
+
+def search_bench(args):
+    """The pruned configuration search (Sec. 4.2.3) over every assignment row
+    and composition of the 8-stage, 3-type workload: one step = one
+    poseidon_search call over all 6561 x C(79,7) = 1.9 x 10^13 candidates."""
+    import numpy as np
+    import torch
+
+    from oracle import coracle
+    from paper_2609_06086_amd import poseidon as P
+    from paper_2609_06086_amd import workloads as W
+
+    wl = W.workload(4)
+    prob = wl.problem
+    c = wl.cands
+    # warm-up bound (Sec. 4.2.3): the best of the first 500 sampled candidates, evaluated on the GPU
+    ctx = P.poseidon_load_costs(prob, 0)
+    dev = torch.device("cuda:0")
+    warm = P.poseidon_eval_candidates(ctx, comp_rank=torch.from_numpy(c.comp_rank[:500].view(np.int64)).to(dev),
+                                      assign_idx=torch.from_numpy(c.assign_idx[:500].view(np.int32)).to(dev))
+    bound = warm.makespan
+    rpc = args.rows_per_chunk
+    stream = torch.cuda.current_stream()
+
+    def step():
+        return P.poseidon_search(ctx, bound, rows_per_chunk=rpc, ridge=args.ridge, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for e0, e1 in evs:
+        e0.record(stream)
+        best, st = step()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    call_ms = sum(e0.elapsed_time(e1) for e0, e1 in evs) / len(evs)
+    ms = wall * 1e3 / args.steps
+    covered = prob.n_candidates
+    tested = st.visited + st.pruned_memory + st.pruned_ridge + st.pruned_bound
+    ops = tested * SEARCH_OPS_PER_TEST
+    achieved = ops / (call_ms * 1e-3) / 1e12
+    out = {
+        "metric": "pruned search (Sec. 4.2.3): candidate configurations covered per second",
+        "value": covered / (ms * 1e-3),
+        "unit": "candidates/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
+        "data": "synthetic (seeded per-layer profile tables)",
+        "config": {"workload": f"L={prob.L} S={prob.S} M={prob.M} T={prob.T}, all {prob.A} assignment rows x "
+                               f"C({prob.L - 1},{prob.S - 1}) compositions, {rpc} rows per chunk, bound = best of "
+                               f"the first 500 sampled candidates ({bound} us)" + (", ridge filter" if args.ridge else ""),
+                   "parallelism": "single GPU"},
+        "search": {"visited": st.visited, "evaluated": st.evaluated, "pruned_memory": st.pruned_memory,
+                   "pruned_ridge": st.pruned_ridge, "pruned_bound": st.pruned_bound,
+                   "stage_choices_tested_per_s": tested / (call_ms * 1e-3),
+                   "best_index": best.index, "best_makespan": best.makespan, "warmup_bound": bound},
+        "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_INT32_TOPS, "unit": "Top/s",
+                     "frac": achieved / PEAK_INT32_TOPS, "traffic": None, "kernel_ms": call_ms,
+                     "algorithmic_ops_per_launch": ops,
+                     "launch": "one poseidon_search call (count, scan, write, leaf kernels per level)"},
+    }
+    if not args.no_cpu_baseline:
+        coracle.lib()
+        rows = 128
+        t0 = time.perf_counter()
+        r = coracle.search(prob, bound, first_row=0, n_rows=rows, rows_per_chunk=rpc, ridge=args.ridge)
+        dt = time.perf_counter() - t0
+        t_cpu = r["visited"] + r["pruned_memory"] + r["pruned_ridge"] + r["pruned_bound"]
+        out["cpu_baseline"] = {"value": rows * prob.n_candidates / prob.A / dt, "unit": "candidates/s",
+                               "cores": coracle.default_threads(), "kind": "oracle",
+                               "stage_choices_tested_per_s": t_cpu / dt,
+                               "sample": f"C oracle search (oracle/oracle.c, rows split over threads) over the first "
+                                         f"{rows} assignment rows, same bound and chunking, {dt:.1f} s"}
+    ctx.close()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -86,6 +168,10 @@ def main():
     ap.add_argument("--no-early-stop", action="store_true")
     ap.add_argument("--schedule", default="1f1b", choices=["1f1b", "eager"],
                     help="pipeline schedule of the DAG (1F1B or Eager 1F1B)")
+    ap.add_argument("--search", action="store_true",
+                    help="time the pruned configuration search over the whole 8-stage workload instead")
+    ap.add_argument("--rows-per-chunk", type=int, default=64)
+    ap.add_argument("--ridge", action="store_true", help="with --search: layer-level (ridge) pruning")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (for counter scaling)")
     args = ap.parse_args()
@@ -93,6 +179,10 @@ def main():
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the evaluation of "
               f"independent candidates would shard by index range, see DESIGN.md)", file=sys.stderr)
         sys.exit(2)
+
+    if args.search:
+        search_bench(args)
+        return
 
     import numpy as np
     import torch
