@@ -32,7 +32,7 @@ class _Problem(C.Structure):
     _fields_ = [("L", C.c_uint32), ("S", C.c_uint32), ("M", C.c_uint32), ("T", C.c_uint32),
                 ("fwd", C.c_void_p), ("bwd", C.c_void_p), ("cf", C.c_void_p), ("cb", C.c_void_p),
                 ("mem", C.c_void_p), ("cap", C.c_void_p), ("assign", C.c_void_p),
-                ("A", C.c_uint64), ("allreduce", C.c_void_p), ("schedule", C.c_uint32)]
+                ("A", C.c_uint64), ("allreduce", C.c_void_p), ("schedule", C.c_uint32), ("V", C.c_uint32)]
 
 
 _lib = None
@@ -90,7 +90,7 @@ def _problem(prob):
                   _ptr(arr(prob.mem, np.uint32)), _ptr(arr(prob.cap, np.uint32)),
                   _ptr(arr(prob.assign, np.uint8)), prob.A,
                   _ptr(arr(getattr(prob, "allreduce", None), np.uint32)),
-                  int(getattr(prob, "schedule", 0)))
+                  int(getattr(prob, "schedule", 0)), int(getattr(prob, "V", 1)))
     return st, keep
 
 

@@ -38,6 +38,21 @@ docstring; the list of readings:
 * R11 (Eager 1F1B, App. B.1): stage s runs w = min(2(S-s)+1, M) forward
   passes, then M - w groups of one backward and one forward pass, then the
   remaining backward passes.
+* R20 (Interleaved 1F1B, Sec. 4.1.4; the paper gives only node and edge
+  counts): N devices each hold V >= 2 model chunks; virtual stage j
+  (1-based, j = 1..VN) is chunk (j-1) div N of device (j-1) mod N + 1, so
+  the L layers are split into VN consecutive parts and consecutive parts
+  sit on consecutive devices, wrapping from device N to device 1.  M must be
+  a multiple of N.  Device p (0-based) runs the interleaved order of
+  Megatron-LM (the paper's reference for the schedule): forward step k
+  (k = 0..VM-1) runs chunk (k mod VN) div N on micro-batch
+  (k div VN) N + k mod N + 1, backward step k runs chunk V-1 - (k mod VN) div N
+  on the same micro-batch; a warm-up of min(2(N-p-1) + (V-1) N, VM) forward
+  steps (all VM of them if M = N), then pairs (forward step w+i, backward
+  step i), then the remaining backward steps.  The intra-stage edges follow
+  each device's order; one all-reduce node per device follows its last node
+  and weighs the device's summed per-layer all-reduce time; a device fits
+  when the summed memory of all its chunks' layers fits its cap.
 """
 from __future__ import annotations
 
@@ -80,6 +95,63 @@ def eager_1f1b_order(S: int, M: int, s: int) -> List[Tuple[str, int]]:
 
 
 SCHEDULES = {0: one_f_one_b_order, 1: eager_1f1b_order}
+SCHEDULE_INTERLEAVED = 2
+
+
+def interleaved_order(N: int, V: int, M: int, p: int) -> List[Tuple[str, int, int]]:
+    """Execution order of device p (1-based) under Interleaved 1F1B (Sec.
+    4.1.4, reading R20) as (kind, virtual stage 1..VN, micro-batch)."""
+    q = p - 1
+    total = V * M
+    w = total if M == N else min(2 * (N - q - 1) + (V - 1) * N, total)
+
+    def mb(k):
+        return (k // (N * V)) * N + k % N + 1
+
+    def fwd(k):
+        c = (k % (N * V)) // N
+        return ("F", c * N + q + 1, mb(k))
+
+    def bwd(k):
+        c = V - 1 - (k % (N * V)) // N
+        return ("B", c * N + q + 1, mb(k))
+
+    order = [fwd(k) for k in range(w)]
+    for i in range(total - w):
+        order.append(fwd(w + i))
+        order.append(bwd(i))
+    order += [bwd(k) for k in range(total - w, total)]
+    return order
+
+
+def build_interleaved_dag(N: int, V: int, M: int) -> "Dag":
+    """Sec. 4.1.4: 2VNM compute nodes; inter-stage edges along the VN
+    virtual stages (2(NV-1)M); intra-stage edges along each device's order
+    (N(2VM-1)); one all-reduce node per device after its last node; start ->
+    F_{1,1}; all-reduce nodes -> end (reading R20)."""
+    S = N * V
+    nodes: List[Node] = [START]
+    for j in range(1, S + 1):
+        for m in range(1, M + 1):
+            nodes.append(("F", j, m))
+            nodes.append(("B", j, m))
+    for p in range(1, N + 1):
+        nodes.append(("R", p, 0))
+    nodes.append(END)
+    edges: List[Tuple[Node, Node, str]] = []
+    for m in range(1, M + 1):
+        for j in range(1, S):
+            edges.append((("F", j, m), ("F", j + 1, m), "fwd"))
+            edges.append((("B", j + 1, m), ("B", j, m), "bwd"))
+    for p in range(1, N + 1):
+        seq = interleaved_order(N, V, M, p)
+        for a, b in zip(seq, seq[1:]):
+            edges.append((a, b, "intra"))
+        edges.append((seq[-1], ("R", p, 0), "allreduce"))
+    edges.append((START, ("F", 1, 1), "aux"))
+    for p in range(1, N + 1):
+        edges.append((("R", p, 0), END, "aux"))
+    return _finish_dag(S, M, nodes, edges)
 
 
 @dataclass
@@ -133,6 +205,11 @@ def build_dag(S: int, M: int, order=one_f_one_b_order) -> Dag:
     for s in range(1, S + 1):
         edges.append((("R", s, 0), END, "aux"))
 
+    return _finish_dag(S, M, nodes, edges)
+
+
+def _finish_dag(S: int, M: int, nodes: List[Node], edges: List[Tuple[Node, Node, str]]) -> "Dag":
+    """Predecessor lists and Kahn's topological order."""
     preds: Dict[Node, List[Tuple[Node, str]]] = {n: [] for n in nodes}
     succs: Dict[Node, List[Node]] = {n: [] for n in nodes}
     indeg: Dict[Node, int] = {n: 0 for n in nodes}
@@ -155,15 +232,19 @@ def build_dag(S: int, M: int, order=one_f_one_b_order) -> Dag:
     return Dag(S, M, nodes, edges, topo, preds)
 
 
-_DAG_CACHE: Dict[Tuple[int, int, int], Dag] = {}
+_DAG_CACHE: Dict[Tuple[int, int, int, int], Dag] = {}
 
 
-def dag_for(S: int, M: int, schedule: int = 0) -> Dag:
-    """The topology depends only on (S, M) and the schedule; reuse it
-    (Sec. 5, simulator design)."""
-    key = (S, M, schedule)
+def dag_for(S: int, M: int, schedule: int = 0, V: int = 1) -> Dag:
+    """The topology depends only on (S, M), the schedule and V; reuse it
+    (Sec. 5, simulator design).  Under Interleaved 1F1B S counts virtual
+    stages and the devices are N = S / V."""
+    key = (S, M, schedule, V)
     if key not in _DAG_CACHE:
-        _DAG_CACHE[key] = build_dag(S, M, order=SCHEDULES[schedule])
+        if schedule == SCHEDULE_INTERLEAVED:
+            _DAG_CACHE[key] = build_interleaved_dag(S // V, V, M)
+        else:
+            _DAG_CACHE[key] = build_dag(S, M, order=SCHEDULES[schedule])
     return _DAG_CACHE[key]
 
 
@@ -236,16 +317,23 @@ def assignment_row(prob, a: int) -> Tuple[int, ...]:
     if prob.assign is not None:
         return tuple(int(x) for x in prob.assign[a])
     digits = []
-    for _ in range(prob.S):
+    for _ in range(n_devices(prob)):
         digits.append(a % prob.T)
         a //= prob.T
     return tuple(reversed(digits))
 
 
+def n_devices(prob) -> int:
+    """Devices of the pipeline: S, or S / V under Interleaved 1F1B (R20)."""
+    if getattr(prob, "schedule", 0) == SCHEDULE_INTERLEAVED:
+        return prob.S // prob.V
+    return prob.S
+
+
 def all_assignments(prob):
     if prob.assign is not None:
         return [tuple(int(x) for x in row) for row in prob.assign]
-    return list(itertools.product(range(prob.T), repeat=prob.S))
+    return list(itertools.product(range(prob.T), repeat=n_devices(prob)))
 
 
 def enumerate_all(prob):
@@ -281,6 +369,28 @@ def stage_weights(prob, cuts: Sequence[int], types: Sequence[int],
     return F, B, MEM, D, feasible
 
 
+def interleaved_weights(prob, cuts: Sequence[int], dev_types: Sequence[int],
+                        allreduce: Optional[np.ndarray] = None):
+    """Interleaved 1F1B (reading R20): F_j, B_j of every virtual stage on its
+    device's type; memory and all-reduce weight per device, summed over the
+    layers of all its chunks; feasible iff every device fits its cap."""
+    N = len(dev_types)
+    types = [dev_types[j % N] for j in range(prob.S)]
+    F, B, MEM, D, _ = stage_weights(prob, cuts, types, allreduce)
+    mem_dev = [sum(MEM[j] for j in range(prob.S) if j % N == q) for q in range(N)]
+    d_dev = [sum(D[j] for j in range(prob.S) if j % N == q) for q in range(N)]
+    ok = all(mem_dev[q] <= int(prob.cap[dev_types[q]]) for q in range(N))
+    return F, B, mem_dev, d_dev, ok
+
+
+def weights(prob, cuts, types, allreduce=None):
+    """Stage weights for the problem's schedule (see stage_weights and
+    interleaved_weights)."""
+    if getattr(prob, "schedule", 0) == SCHEDULE_INTERLEAVED:
+        return interleaved_weights(prob, cuts, types, allreduce)
+    return stage_weights(prob, cuts, types, allreduce)
+
+
 def candidate_list(prob, cands):
     """(index, cuts, types) for a Candidates object (range or list mode)."""
     if cands.is_list:
@@ -305,12 +415,12 @@ def evaluate(prob, cands, allreduce=None):
     The all-reduce table defaults to the problem's own (``prob.allreduce``)."""
     if allreduce is None:
         allreduce = getattr(prob, "allreduce", None)
-    dag = dag_for(prob.S, prob.M, getattr(prob, "schedule", 0))
+    dag = dag_for(prob.S, prob.M, getattr(prob, "schedule", 0), getattr(prob, "V", 1))
     lst = candidate_list(prob, cands)
     T = np.zeros(len(lst), dtype=np.int64)
     feas = np.zeros(len(lst), dtype=bool)
     for i, cuts, types in lst:
-        F, B, _, D, ok = stage_weights(prob, cuts, types, allreduce)
+        F, B, _, D, ok = weights(prob, cuts, types, allreduce)
         T[i] = longest_path(dag, F, B, prob.comm_fwd, prob.comm_bwd,
                             D if allreduce is not None else None)
         feas[i] = ok
@@ -353,6 +463,8 @@ def bounded_search(prob, cands, bound: int, chunk: int = 0):
     every other feasible one is evaluated exactly.  The result is the
     (makespan, index)-smallest evaluated candidate if its makespan is
     <= bound, else None.  Returns (best, evaluated, pruned, infeasible)."""
+    if getattr(prob, "schedule", 0) == SCHEDULE_INTERLEAVED:
+        raise ValueError("Eq. 2 is stated for one stage per device; no early stop under Interleaved 1F1B")
     allreduce = getattr(prob, "allreduce", None)
     dag = dag_for(prob.S, prob.M, getattr(prob, "schedule", 0))
     lst = candidate_list(prob, cands)

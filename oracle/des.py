@@ -116,3 +116,63 @@ def all_paths_longest(dag, F, B, cf, cb, d=None) -> int:
         for v, k in succ.get(u, []):
             stack.append((v, acc + wedge(u, v, k)))
     return best
+
+
+def simulate_devices(S: int, N: int, M: int, F: Sequence[int], B: Sequence[int],
+                     cf: Sequence[int], cb: Sequence[int], tasks, allreduce=None) -> int:
+    """Event-driven run of a pipeline whose N devices hold several of the S
+    virtual stages (Interleaved 1F1B): `tasks[p]` (p = 1..N) is device p's
+    list of ('F'|'B', virtual stage j, m).  F on stage j > 1 waits for the
+    activation of F_{j-1,m} (cf[j-2] after it ends); B on j < S waits for the
+    gradient of B_{j+1,m} (cb[j-1] after it ends).  With `allreduce` (per
+    device) each device then runs its all-reduce; the iteration ends with
+    the last device."""
+    nxt = {p: 0 for p in tasks}
+    busy_until = {p: 0 for p in tasks}
+    idle = {p: True for p in tasks}
+    arrived = set()
+    events = []
+    seq = 0
+
+    def push(t, kind, payload):
+        nonlocal seq
+        heapq.heappush(events, (t, seq, kind, payload))
+        seq += 1
+
+    def try_start(p, now):
+        if not idle[p] or nxt[p] >= len(tasks[p]):
+            return
+        kind, j, m = tasks[p][nxt[p]]
+        if kind == "F" and j > 1 and ("F", j, m) not in arrived:
+            return
+        if kind == "B" and j < S and ("B", j, m) not in arrived:
+            return
+        idle[p] = False
+        push(now + (F[j - 1] if kind == "F" else B[j - 1]), "done", (p, kind, j, m))
+
+    dev_of = {}
+    for p, lst in tasks.items():
+        for kind, j, m in lst:
+            dev_of[j] = p
+    for p in tasks:
+        try_start(p, 0)
+    while events:
+        now, _, ev, payload = heapq.heappop(events)
+        if ev == "done":
+            p, kind, j, m = payload
+            idle[p] = True
+            busy_until[p] = now
+            nxt[p] += 1
+            if kind == "F" and j < S:
+                push(now + cf[j - 1], "arrive", ("F", j + 1, m))
+            if kind == "B" and j > 1:
+                push(now + cb[j - 2], "arrive", ("B", j - 1, m))
+            try_start(p, now)
+        else:
+            arrived.add(payload)
+            try_start(dev_of[payload[1]], now)
+    if any(nxt[p] != len(tasks[p]) for p in tasks):
+        raise RuntimeError("pipeline deadlocked")
+    if allreduce is not None:
+        return max(busy_until[p] + int(allreduce[p - 1]) for p in tasks)
+    return max(busy_until.values())

@@ -56,7 +56,8 @@ typedef struct {
     const uint8_t *assign;         /* [A][S] or NULL (all T^S rows) */
     uint64_t A;
     const uint32_t *allreduce;     /* [T][L] or NULL (no DP all-reduce) */
-    uint32_t schedule;             /* 0 = 1F1B, 1 = Eager 1F1B */
+    uint32_t schedule;             /* 0 = 1F1B, 1 = Eager 1F1B, 2 = Interleaved 1F1B */
+    uint32_t V;                    /* model chunks per device (Interleaved 1F1B) */
 } oc_problem;
 
 enum { K_F = 0, K_B = 1, K_R = 2, K_START = 3, K_END = 4 };
@@ -73,6 +74,7 @@ typedef struct {
 
 typedef struct {
     int S, M, n;
+    int ND;                        /* devices: all-reduce nodes and end-node predecessors */
     oc_node *nodes;
     int *topo;
     int end;
@@ -114,28 +116,51 @@ static void stage_order(int S, int M, int s, int schedule, int *ko, int *mo) {
     for (int m = M - w + 1; m <= M; ++m) { ko[k] = K_B; mo[k] = m; ++k; }
 }
 
-static oc_dag *dag_build(int S, int M, int schedule) {
+/* Interleaved 1F1B order of device p (1-based) of N, V chunks each: (kind,
+ * virtual stage, m) triples (2VM entries); see oracle/dag.py, reading R20. */
+static void interleaved_order(int N, int V, int M, int p, int *ko, int *jo, int *mo) {
+    int q = p - 1, total = V * M, k = 0;
+    int w = M == N ? total : (2 * (N - q - 1) + (V - 1) * N < total ? 2 * (N - q - 1) + (V - 1) * N : total);
+#define IL_MB(x) (((x) / (N * V)) * N + (x) % N + 1)
+#define IL_FC(x) (((x) % (N * V)) / N)
+    for (int x = 0; x < w; ++x) { ko[k] = K_F; jo[k] = IL_FC(x) * N + q + 1; mo[k] = IL_MB(x); ++k; }
+    for (int i = 0; i < total - w; ++i) {
+        int x = w + i;
+        ko[k] = K_F; jo[k] = IL_FC(x) * N + q + 1; mo[k] = IL_MB(x); ++k;
+        ko[k] = K_B; jo[k] = (V - 1 - IL_FC(i)) * N + q + 1; mo[k] = IL_MB(i); ++k;
+    }
+    for (int x = total - w; x < total; ++x) {
+        ko[k] = K_B; jo[k] = (V - 1 - IL_FC(x)) * N + q + 1; mo[k] = IL_MB(x); ++k;
+    }
+#undef IL_MB
+#undef IL_FC
+}
+
+static oc_dag *dag_build(int S, int M, int schedule, int V) {
     oc_dag *g = calloc(1, sizeof(oc_dag));
     if (!g) return NULL;
     int ncomp = 2 * S * M;
-    g->S = S; g->M = M;
-    g->n = ncomp + S + 2;
-    int start = ncomp + S;
-    g->end = ncomp + S + 1;
+    const int interleaved = schedule == 2;
+    const int ND = interleaved ? S / V : S;
+    g->S = S; g->M = M; g->ND = ND;
+    g->n = ncomp + ND + 2;
+    int start = ncomp + ND;
+    g->end = ncomp + ND + 1;
     g->nodes = calloc((size_t)g->n, sizeof(oc_node));
     g->topo = malloc(sizeof(int) * (size_t)g->n);
-    int *ko = malloc(sizeof(int) * 2 * (size_t)M), *mo = malloc(sizeof(int) * 2 * (size_t)M);
+    size_t olen = 2 * (size_t)M * (size_t)(interleaved ? V : 1);
+    int *ko = malloc(sizeof(int) * olen), *mo = malloc(sizeof(int) * olen), *jo = malloc(sizeof(int) * olen);
     int *indeg = calloc((size_t)g->n, sizeof(int));
     int *queue = malloc(sizeof(int) * (size_t)g->n);
-    if (!g->nodes || !g->topo || !ko || !mo || !indeg || !queue) {
-        free(ko); free(mo); free(indeg); free(queue); dag_free(g); return NULL;
+    if (!g->nodes || !g->topo || !ko || !mo || !jo || !indeg || !queue) {
+        free(ko); free(mo); free(jo); free(indeg); free(queue); dag_free(g); return NULL;
     }
     for (int s = 1; s <= S; ++s)
         for (int m = 1; m <= M; ++m) {
             g->nodes[idF(M, s, m)].kind = K_F; g->nodes[idF(M, s, m)].stage = s;
             g->nodes[idB(M, s, m)].kind = K_B; g->nodes[idB(M, s, m)].stage = s;
         }
-    for (int s = 1; s <= S; ++s) { g->nodes[ncomp + s - 1].kind = K_R; g->nodes[ncomp + s - 1].stage = s; }
+    for (int s = 1; s <= ND; ++s) { g->nodes[ncomp + s - 1].kind = K_R; g->nodes[ncomp + s - 1].stage = s; }
     g->nodes[start].kind = K_START;
     g->nodes[g->end].kind = K_END;
     /* inter-stage edges */
@@ -144,24 +169,33 @@ static oc_dag *dag_build(int S, int M, int schedule) {
             add_pred(&g->nodes[idF(M, s + 1, m)], idF(M, s, m), E_FWD, s - 1);
             add_pred(&g->nodes[idB(M, s, m)], idB(M, s + 1, m), E_BWD, s - 1);
         }
-    /* intra-stage edges along the schedule */
-    for (int s = 1; s <= S; ++s) {
-        stage_order(S, M, s, schedule, ko, mo);
-        for (int k = 1; k < 2 * M; ++k) {
-            int u = ko[k - 1] == K_F ? idF(M, s, mo[k - 1]) : idB(M, s, mo[k - 1]);
-            int v = ko[k] == K_F ? idF(M, s, mo[k]) : idB(M, s, mo[k]);
+    /* intra-stage edges along each device's order; the device's all-reduce
+     * node follows its last node */
+    for (int p = 1; p <= ND; ++p) {
+        int len;
+        if (interleaved) {
+            interleaved_order(ND, V, M, p, ko, jo, mo);
+            len = 2 * V * M;
+        } else {
+            stage_order(S, M, p, schedule, ko, mo);
+            for (int k = 0; k < 2 * M; ++k) jo[k] = p;
+            len = 2 * M;
+        }
+        for (int k = 1; k < len; ++k) {
+            int u = ko[k - 1] == K_F ? idF(M, jo[k - 1], mo[k - 1]) : idB(M, jo[k - 1], mo[k - 1]);
+            int v = ko[k] == K_F ? idF(M, jo[k], mo[k]) : idB(M, jo[k], mo[k]);
             add_pred(&g->nodes[v], u, E_ZERO, 0);
         }
+        int last = ko[len - 1] == K_F ? idF(M, jo[len - 1], mo[len - 1]) : idB(M, jo[len - 1], mo[len - 1]);
+        add_pred(&g->nodes[ncomp + p - 1], last, E_ZERO, 0);
     }
-    /* all-reduce, auxiliary */
-    for (int s = 1; s <= S; ++s) add_pred(&g->nodes[ncomp + s - 1], idB(M, s, M), E_ZERO, 0);
     add_pred(&g->nodes[idF(M, 1, 1)], start, E_ZERO, 0);
-    g->nodes[g->end].xpred = malloc(sizeof(int) * (size_t)S);
-    for (int s = 1; s <= S; ++s) g->nodes[g->end].xpred[s - 1] = ncomp + s - 1;
+    g->nodes[g->end].xpred = malloc(sizeof(int) * (size_t)ND);
+    for (int s = 1; s <= ND; ++s) g->nodes[g->end].xpred[s - 1] = ncomp + s - 1;
     /* Kahn */
     for (int v = 0; v < g->n; ++v) {
         oc_node *nv = &g->nodes[v];
-        indeg[v] = nv->kind == K_END ? S : nv->npred;
+        indeg[v] = nv->kind == K_END ? ND : nv->npred;
     }
     int head = 0, tail = 0, cnt = 0;
     for (int v = 0; v < g->n; ++v) if (indeg[v] == 0) queue[tail++] = v;
@@ -169,7 +203,7 @@ static oc_dag *dag_build(int S, int M, int schedule) {
     int *succ_cnt = calloc((size_t)g->n, sizeof(int));
     for (int v = 0; v < g->n; ++v) {
         oc_node *nv = &g->nodes[v];
-        int np = nv->kind == K_END ? S : nv->npred;
+        int np = nv->kind == K_END ? ND : nv->npred;
         for (int i = 0; i < np; ++i) succ_cnt[nv->kind == K_END ? nv->xpred[i] : nv->pred[i]]++;
     }
     int *succ_off = malloc(sizeof(int) * ((size_t)g->n + 1));
@@ -179,7 +213,7 @@ static oc_dag *dag_build(int S, int M, int schedule) {
     memset(succ_cnt, 0, sizeof(int) * (size_t)g->n);
     for (int v = 0; v < g->n; ++v) {
         oc_node *nv = &g->nodes[v];
-        int np = nv->kind == K_END ? S : nv->npred;
+        int np = nv->kind == K_END ? ND : nv->npred;
         for (int i = 0; i < np; ++i) {
             int u = nv->kind == K_END ? nv->xpred[i] : nv->pred[i];
             succ[succ_off[u] + succ_cnt[u]++] = v;
@@ -192,7 +226,7 @@ static oc_dag *dag_build(int S, int M, int schedule) {
             if (--indeg[succ[i]] == 0) queue[tail++] = succ[i];
     }
     free(succ_cnt); free(succ_off); free(succ);
-    free(ko); free(mo); free(indeg); free(queue);
+    free(ko); free(mo); free(jo); free(indeg); free(queue);
     if (cnt != g->n) { dag_free(g); return NULL; }
     return g;
 }
@@ -205,7 +239,7 @@ static uint64_t dag_longest(const oc_dag *g, const uint64_t *F, const uint64_t *
         const oc_node *nv = &g->nodes[v];
         uint64_t best = 0, w = 0;
         if (nv->kind == K_END) {
-            for (int j = 0; j < g->S; ++j) if (fin[nv->xpred[j]] > best) best = fin[nv->xpred[j]];
+            for (int j = 0; j < g->ND; ++j) if (fin[nv->xpred[j]] > best) best = fin[nv->xpred[j]];
         } else {
             for (int j = 0; j < nv->npred; ++j) {
                 uint64_t c = fin[nv->pred[j]];
@@ -286,12 +320,13 @@ static int decode(const oc_job *j, uint64_t i, int *cuts, int *types) {
         }
     }
     cuts[S] = L;
+    int ND = p->schedule == 2 ? S / (int)p->V : S;   /* one type per device */
     if (p->assign) {
-        for (int s = 0; s < S; ++s) types[s] = p->assign[a * S + s];
+        for (int s = 0; s < ND; ++s) types[s] = p->assign[a * ND + s];
     } else {
-        for (int s = S - 1; s >= 0; --s) { types[s] = (int)(a % p->T); a /= p->T; }
+        for (int s = ND - 1; s >= 0; --s) { types[s] = (int)(a % p->T); a /= p->T; }
     }
-    for (int s = 0; s < S; ++s) if (types[s] >= (int)p->T) return -1;
+    for (int s = 0; s < ND; ++s) if (types[s] >= (int)p->T) return -1;
     return 0;
 }
 
@@ -307,17 +342,23 @@ static void *worker(void *arg) {
     for (uint64_t i = j->lo; i < j->hi; ++i) {
         if (decode(j, i, cuts, types)) { j->err = -1; break; }
         int feasible = 1;
+        /* Interleaved 1F1B: virtual stage s runs on device s mod ND; memory
+         * and all-reduce are summed per device (reading R20) */
+        int ND = p->schedule == 2 ? S / (int)p->V : S;
+        uint64_t MM[64];
+        for (int q = 0; q < ND; ++q) { D[q] = 0; MM[q] = 0; }
         for (int s = 0; s < S; ++s) {
+            int q = s % ND, t = types[q];
             uint64_t f = 0, b = 0, mm = 0, d = 0;
             for (int l = cuts[s]; l < cuts[s + 1]; ++l) {
-                f += p->fwd[(size_t)types[s] * p->L + l];
-                b += p->bwd[(size_t)types[s] * p->L + l];
+                f += p->fwd[(size_t)t * p->L + l];
+                b += p->bwd[(size_t)t * p->L + l];
                 mm += p->mem[l];
-                if (p->allreduce) d += p->allreduce[(size_t)types[s] * p->L + l];
+                if (p->allreduce) d += p->allreduce[(size_t)t * p->L + l];
             }
-            F[s] = f; B[s] = b; D[s] = d;
-            if (mm > p->cap[types[s]]) feasible = 0;
+            F[s] = f; B[s] = b; D[q] += d; MM[q] += mm;
         }
+        for (int q = 0; q < ND; ++q) if (MM[q] > p->cap[types[q]]) feasible = 0;
         if (j->bounded) {
             if (!feasible) { j->infeasible++; continue; }
             uint64_t lb = 0;
@@ -368,7 +409,8 @@ static int run_jobs(oc_job *proto, uint64_t lo, uint64_t hi, int nthreads, oc_jo
 
 static int check(const oc_problem *p) {
     if (!p || p->S < 1 || p->S > 64 || p->L < p->S || p->M < 1 || p->T < 1 || p->A < 1) return -1;
-    if (p->schedule > 1) return -1;
+    if (p->schedule > 2) return -1;
+    if (p->schedule == 2 && (p->V < 2 || p->S % p->V || p->M % (p->S / p->V))) return -1;
     if (!p->fwd || !p->bwd || !p->mem || !p->cap) return -1;
     if (p->S > 1 && (!p->cf || !p->cb)) return -1;
     return 0;
@@ -379,7 +421,7 @@ static int check(const oc_problem *p) {
 int oc_eval(const oc_problem *p, uint64_t first, uint64_t count, const uint64_t *rank,
             const uint32_t *aidx, uint32_t *out_T, uint8_t *out_feas, int nthreads) {
     if (check(p)) return -1;
-    oc_dag *g = dag_build((int)p->S, (int)p->M, (int)p->schedule);
+    oc_dag *g = dag_build((int)p->S, (int)p->M, (int)p->schedule, (int)p->V);
     uint64_t *binom = pascal((int)p->L - 1, (int)p->S - 1);
     if (!g || !binom) { dag_free(g); free(binom); return -3; }
     oc_job proto = {0};
@@ -399,8 +441,8 @@ int oc_bounded(const oc_problem *p, uint64_t first, uint64_t count, const uint64
                const uint32_t *aidx, uint32_t bound, uint64_t chunk, uint64_t *best_idx,
                uint32_t *best_T, uint64_t *evaluated, uint64_t *pruned, uint64_t *infeasible,
                int nthreads) {
-    if (check(p)) return -1;
-    oc_dag *g = dag_build((int)p->S, (int)p->M, (int)p->schedule);
+    if (check(p) || p->schedule == 2) return -1;   /* Eq. 2 is stated for one stage per device */
+    oc_dag *g = dag_build((int)p->S, (int)p->M, (int)p->schedule, (int)p->V);
     uint64_t *binom = pascal((int)p->L - 1, (int)p->S - 1);
     if (!g || !binom) { dag_free(g); free(binom); return -3; }
     if (chunk == 0) chunk = count ? count : 1;
@@ -432,7 +474,7 @@ int oc_bounded(const oc_problem *p, uint64_t first, uint64_t count, const uint64
 
 /* DAG shape for pins: compute nodes, edges by kind. */
 int oc_dag_counts(int S, int M, int *n_nodes, int *n_fwd, int *n_bwd, int *n_intra, int *n_other) {
-    oc_dag *g = dag_build(S, M, 0);
+    oc_dag *g = dag_build(S, M, 0, 1);
     if (!g) return -1;
     int f = 0, b = 0, in = 0, o = 0;
     for (int v = 0; v < g->n; ++v) {
@@ -544,8 +586,8 @@ static void *s_worker(void *arg) {
  * ridge test and by the bound. */
 int oc_search(const oc_problem *p, uint64_t first_row, uint64_t n_rows, uint32_t bound, uint64_t rows_per_chunk,
               uint32_t flags, uint64_t *best_idx, uint32_t *best_T, uint64_t *counters, int nthreads) {
-    if (check(p) || first_row + n_rows > p->A || p->S > 64 || p->T > 64) return -1;
-    oc_dag *g = dag_build((int)p->S, (int)p->M, (int)p->schedule);
+    if (check(p) || p->schedule == 2 || first_row + n_rows > p->A || p->S > 64 || p->T > 64) return -1;
+    oc_dag *g = dag_build((int)p->S, (int)p->M, (int)p->schedule, (int)p->V);
     uint64_t *binom = pascal((int)p->L - 1, (int)p->S - 1);
     if (!g || !binom) { dag_free(g); free(binom); return -3; }
     if (rows_per_chunk == 0) rows_per_chunk = n_rows ? n_rows : 1;

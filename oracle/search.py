@@ -114,6 +114,8 @@ def stage_search(prob, bound: int, first_row: int = 0, n_rows: Optional[int] = N
     """The pruned search of Sec. 4.2.3 over assignment rows
     [first_row, first_row + n_rows) (readings R16-R19).  Returns a dict with
     `best` = (joint index, makespan) or None and the counters."""
+    if getattr(prob, "schedule", 0) == D.SCHEDULE_INTERLEAVED:
+        raise ValueError("Eq. 2 is stated for one stage per device; no search under Interleaved 1F1B")
     L, S, M = prob.L, prob.S, prob.M
     A = prob.A
     n_rows = A - first_row if n_rows is None else n_rows

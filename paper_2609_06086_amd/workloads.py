@@ -43,14 +43,20 @@ class Problem:
     comm_bwd: np.ndarray     # uint32 [S-1], B_{b+1,m} -> B_{b,m}
     mem: np.ndarray          # uint32 [L]
     cap: np.ndarray          # uint32 [T]
-    assign: Optional[np.ndarray] = None   # uint8 [A][S]; None => all T^S rows
+    assign: Optional[np.ndarray] = None   # uint8 [A][devices]; None => all T^devices rows
     seed: Optional[int] = None
     allreduce: Optional[np.ndarray] = None  # uint32 [T][L] DP all-reduce time per layer, or None
-    schedule: int = 0                       # 0 = 1F1B, 1 = Eager 1F1B
+    schedule: int = 0                       # 0 = 1F1B, 1 = Eager 1F1B, 2 = Interleaved 1F1B
+    V: int = 1                              # model chunks per device (Interleaved 1F1B)
+
+    @property
+    def devices(self) -> int:
+        """Pipeline devices: S, or S / V virtual stages under Interleaved 1F1B."""
+        return self.S // self.V if self.schedule == 2 else self.S
 
     @property
     def A(self) -> int:
-        return int(self.assign.shape[0]) if self.assign is not None else self.T ** self.S
+        return int(self.assign.shape[0]) if self.assign is not None else self.T ** self.devices
 
     @property
     def n_compositions(self) -> int:

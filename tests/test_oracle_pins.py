@@ -617,3 +617,91 @@ def test_eq2_lower_bound_holds_under_eager():
         d = list(rng.integers(0, 500, S)) if trial % 2 else None
         T = dag.longest_path(dag.dag_for(S, M, 1), F, B, cf, cb, d)
         assert dag.eq2_bound(list(F), list(B), M, d) <= T
+
+
+# ------------------------------------------------------- Interleaved 1F1B
+
+def test_interleaved_dag_counts_match_sec_4_1_4():
+    """Sec. 4.1.4: 2VNM compute nodes, 2(NV-1)M inter-stage edges and
+    N(2VM-1) intra-stage edges."""
+    for N in range(2, 6):
+        for V in range(2, 5):
+            for M in (N, 2 * N, 3 * N):
+                c = dag.dag_for(N * V, M, 2, V).counts()
+                assert c["compute_nodes"] == 2 * V * N * M
+                assert c["fwd"] + c["bwd"] == 2 * (N * V - 1) * M
+                assert c["intra"] == N * (2 * V * M - 1)
+                assert c["allreduce_nodes"] == N
+
+
+def test_interleaved_uniform_closed_form():
+    """Equal chunks, no transfer time: T = (VM + N - 1)(f + b), the
+    interleaved pipeline's bubble of N - 1 chunk slots."""
+    for N in range(2, 6):
+        for V in range(2, 5):
+            for M in (N, 2 * N, 4 * N):
+                S = N * V
+                T = dag.longest_path(dag.dag_for(S, M, 2, V), [3] * S, [5] * S, [0] * (S - 1), [0] * (S - 1))
+                assert T == (V * M + N - 1) * 8
+
+
+def test_interleaved_orders_are_device_permutations():
+    for N in range(2, 5):
+        for V in range(2, 4):
+            for M in (N, 2 * N):
+                seen = set()
+                for p in range(1, N + 1):
+                    o = dag.interleaved_order(N, V, M, p)
+                    assert len(o) == len(set(o)) == 2 * V * M
+                    assert all((j - 1) % N == p - 1 for _, j, _ in o)
+                    pos = {x: i for i, x in enumerate(o)}
+                    assert all(pos[("F", j, m)] < pos[("B", j, m)] for _, j, m in o)
+                    seen |= set(o)
+                assert len(seen) == 2 * N * V * M
+
+
+def test_interleaved_event_simulation_and_c_oracle():
+    """The DAG's T equals an event-driven run of the device task lists
+    (with per-device all-reduce); the C oracle equals the Python one."""
+    rng = np.random.default_rng(40)
+    for trial in range(150):
+        N, V = int(rng.integers(2, 5)), int(rng.integers(2, 4))
+        M, S = N * int(rng.integers(1, 4)), N * V
+        F, B, cf, cb = (list(rng.integers(1, 100, S)), list(rng.integers(1, 200, S)),
+                        list(rng.integers(0, 50, S - 1)), list(rng.integers(0, 50, S - 1)))
+        d = list(rng.integers(0, 300, N)) if trial % 2 else None
+        tasks = {p: dag.interleaved_order(N, V, M, p) for p in range(1, N + 1)}
+        assert des.simulate_devices(S, N, M, F, B, cf, cb, tasks, d) == \
+            dag.longest_path(dag.dag_for(S, M, 2, V), F, B, cf, cb, d)
+    for trial in range(12):
+        N, V = int(rng.integers(2, 5)), int(rng.integers(2, 4))
+        S, M = N * V, N * int(rng.integers(1, 3))
+        T = int(rng.integers(1, 3))
+        L = S + int(rng.integers(0, 5))
+        prob = W.random_problem(rng, L, S, M, T, mem_hi=30, cap=int(rng.integers(60, 300)))
+        prob.schedule, prob.V = 2, V
+        if trial % 3 == 0:
+            prob.assign = rng.integers(0, T, size=(5, N)).astype(np.uint8)
+        if trial % 2:
+            prob.allreduce = rng.integers(0, 400, size=(T, L)).astype(np.uint32)
+        cands = W.random_candidates(rng, prob, 150)
+        Tp, fp = dag.evaluate(prob, cands)
+        Tc, fc = coracle.evaluate(prob, cands, nthreads=2)
+        assert (Tp == Tc).all() and (fp == fc).all()
+
+
+def test_interleaved_weights_per_device():
+    """Virtual stage j runs on device (j-1) mod N; a device's memory and
+    all-reduce weight sum over all its chunks (powers of two spell out which
+    layers were summed)."""
+    L, N, V = 6, 2, 3
+    prob = W.random_problem(np.random.default_rng(41), L, N * V, N, 2)
+    prob.schedule, prob.V = 2, V
+    prob.fwd = np.array([[1 << k for k in range(L)], [1 << (k + 8) for k in range(L)]], dtype=np.uint32)
+    prob.bwd = 2 * prob.fwd
+    prob.mem = np.array([1 << k for k in range(L)], dtype=np.uint32)
+    prob.cap = np.array([0b010101, 0b101010], dtype=np.uint32)
+    ar = np.array([[1 << k for k in range(L)], [1 << (k + 8) for k in range(L)]], dtype=np.uint32)
+    F, B, mem, d, ok = dag.interleaved_weights(prob, (1, 2, 3, 4, 5), (0, 1), ar)
+    assert F == [1, 2 << 8, 4, 8 << 8, 16, 32 << 8] and B == [2 * x for x in F]
+    assert mem == [0b010101, 0b101010] and d == [0b010101, 0b101010 << 8] and ok
