@@ -166,8 +166,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-early-stop", action="store_true")
-    ap.add_argument("--schedule", default="1f1b", choices=["1f1b", "eager"],
-                    help="pipeline schedule of the DAG (1F1B or Eager 1F1B)")
+    ap.add_argument("--schedule", default="1f1b", choices=["1f1b", "eager", "interleaved"],
+                    help="pipeline schedule of the DAG (1F1B, Eager 1F1B, or Interleaved 1F1B with "
+                         "the stages as virtual stages on S/2 devices; workloads 3 and 5)")
     ap.add_argument("--search", action="store_true",
                     help="time the pruned configuration search over the whole 8-stage workload instead")
     ap.add_argument("--rows-per-chunk", type=int, default=64)
@@ -193,7 +194,10 @@ def main():
     dev = torch.device("cuda:0")
     wl = W.workload(args.workload)
     prob = wl.problem
-    prob.schedule = P.SCHEDULE_EAGER_1F1B if args.schedule == "eager" else P.SCHEDULE_1F1B
+    if args.schedule == "interleaved":
+        wl = W.interleaved_variant(wl, 2)
+    else:
+        prob.schedule = P.SCHEDULE_EAGER_1F1B if args.schedule == "eager" else P.SCHEDULE_1F1B
     n = len(wl.cands)
     ctx = P.poseidon_load_costs(prob, 0)
     if wl.cands.is_list:
@@ -245,7 +249,7 @@ def main():
 
     # early-stop pass (Eq. 2 bound) over the same list, warm-up bound from its first 500 entries
     es = None
-    if wl.cands.is_list and not args.no_early_stop:
+    if wl.cands.is_list and not args.no_early_stop and args.schedule != "interleaved":
         warm = {k: v[:500] for k, v in cand.items()}
         wb = P.poseidon_eval_candidates(ctx, **warm)
         bound = wb.makespan if wb.makespan is not None else 2 ** 31
@@ -278,8 +282,10 @@ def main():
         "dtype": "u32",
         "data": "synthetic (seeded per-layer profile tables and sampled candidates)",
         "config": {"workload": f"L={prob.L} S={S} M={M} T={prob.T}, {n} sampled compositions, fixed 4x4 "
-                               f"stage-type permutation" if args.workload == 5 else wl.description,
-                   "schedule": "Eager 1F1B" if args.schedule == "eager" else "1F1B",
+                               f"stage-type permutation" if args.workload == 5 and args.schedule != "interleaved"
+                               else wl.description,
+                   "schedule": {"eager": "Eager 1F1B", "interleaved": "Interleaved 1F1B (V = 2)"}.get(
+                       args.schedule, "1F1B"),
                    "candidates_per_step": n, "dag_nodes_per_candidate": 2 * S * M,
                    "parallelism": "single GPU"},
         "dag_nodes_per_s": nodes_per_s,

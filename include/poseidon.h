@@ -61,8 +61,10 @@ extern "C" {
 /* Pipeline schedules (poseidon_problem.schedule). */
 enum {
     POSEIDON_SCHEDULE_1F1B = 0,        /* min(S-s, M) warm-up forwards, then (F, B) pairs */
-    POSEIDON_SCHEDULE_EAGER_1F1B = 1   /* min(2(S-s)+1, M) warm-up forwards, then (B, F)
+    POSEIDON_SCHEDULE_EAGER_1F1B = 1,  /* min(2(S-s)+1, M) warm-up forwards, then (B, F)
                                           pairs (App. B.1) */
+    POSEIDON_SCHEDULE_INTERLEAVED_1F1B = 2  /* V model chunks per device (Sec. 4.1.4); see
+                                               poseidon_problem.V */
 };
 
 enum {
@@ -95,6 +97,21 @@ typedef struct {
     uint32_t schedule;            /* POSEIDON_SCHEDULE_*: the intra-stage order of the DAG
                                      (Sec. 4.1.4: other schedules change only the intra-stage
                                      edges) */
+    uint32_t V;                   /* Interleaved 1F1B only (ignored otherwise): model chunks per
+                                     device, V >= 2.  S then counts virtual stages (the
+                                     composition has S parts); the N = S / V >= 2 devices each
+                                     hold V of them, virtual stage j (0-based) on device j mod N;
+                                     M must be a multiple of N.  Device p (0-based) runs
+                                     Megatron-LM's interleaved order: forward step k runs chunk
+                                     (k mod VN) div N on micro-batch (k div VN) N + k mod N + 1,
+                                     backward step k chunk V-1 - (k mod VN) div N; a warm-up of
+                                     min(2(N-p-1) + (V-1)N, VM) forward steps (all if M = N), then
+                                     (forward, backward) pairs, then the remaining backwards.
+                                     `assign` rows, base-T digits and memory caps are per device
+                                     (a device's memory and all-reduce sum over all its chunks);
+                                     comm arrays have S-1 entries, one per virtual boundary.
+                                     The early-stop pass and the search reject such problems
+                                     (Eq. 2 is stated for one stage per device). */
 } poseidon_problem;
 
 /* Candidates of one call.  comp_rank == NULL: range mode over joint indices

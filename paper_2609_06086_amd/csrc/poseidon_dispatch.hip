@@ -118,6 +118,7 @@ __global__ void fill_u64(unsigned long long *p, uint32_t n, unsigned long long v
     }
 
 hipError_t launch_eval(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
+    if (p.sched == 2) return launch_ilv(p, lc, st);   // Interleaved 1F1B
     PK_DISPATCH(launch_eval_s, p.S, p.wide, p, lc, st)
 }
 
@@ -134,8 +135,9 @@ hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st,
     PK_DISPATCH(launch_bounded_s, p.S, p.wide, p, lc, st, lo, hi, bound, publish)
 }
 
-hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, bool ar, bool sched, int *blocks) {
-    PK_DISPATCH(occupancy_s, S, wide, blocks, lds, ar, sched)
+hipError_t eval_occupancy(const KParams &p, size_t lds, int *blocks) {
+    if (p.sched == 2) return ilv_occupancy(p, lds, blocks);
+    PK_DISPATCH(occupancy_s, p.S, p.wide, blocks, lds, p.has_ar != 0, p.sched != 0)
 }
 
 hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,

@@ -10,6 +10,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <array>
 #include <new>
 #include <vector>
 
@@ -151,6 +152,100 @@ bool build_slots(int S, int M, int schedule, bool newest_only, std::vector<uint3
     return true;
 }
 
+// Interleaved 1F1B (Sec. 4.1.4): device p (0-based) of N, V chunks each,
+// Megatron-LM's order: forward step k runs chunk (k mod VN) div N on
+// micro-batch (k div VN) N + k mod N + 1, backward step k chunk
+// V-1 - (k mod VN) div N on the same micro-batch; a warm-up of
+// min(2(N-p-1) + (V-1) N, VM) forward steps (all of them if M = N), then
+// (forward, backward) pairs, then the remaining backward steps.  Entries are
+// (kind, virtual stage 0-based, micro-batch 1-based).
+void interleaved_order(int N, int V, int M, int p, std::vector<std::array<int, 3>> &o) {
+    o.clear();
+    const int total = V * M;
+    const int w = M == N ? total : std::min(2 * (N - p - 1) + (V - 1) * N, total);
+    auto mb = [&](int k) { return (k / (N * V)) * N + k % N + 1; };
+    auto fwd = [&](int k) { return std::array<int, 3>{0, ((k % (N * V)) / N) * N + p, mb(k)}; };
+    auto bwd = [&](int k) { return std::array<int, 3>{1, (V - 1 - (k % (N * V)) / N) * N + p, mb(k)}; };
+    for (int k = 0; k < w; ++k) o.push_back(fwd(k));
+    for (int i = 0; i < total - w; ++i) {
+        o.push_back(fwd(w + i));
+        o.push_back(bwd(i));
+    }
+    for (int k = total - w; k < total; ++k) o.push_back(bwd(k));
+}
+
+// Unit-weight as-soon-as-possible slots of the Interleaved 1F1B DAG.  A
+// device runs at most one node per slot (its nodes are sequential).  Four
+// words per slot: forward, forward-of-depth-2, backward stage masks and a
+// 2-bit backward input depth per stage.  A forward must read the upstream
+// stage's newest or second-newest forward, a backward one of the downstream
+// stage's `max_db` newest backwards; otherwise the stencil does not apply.
+bool build_interleaved_slots(int N, int V, int M, int max_db, std::vector<uint32_t> *masks, uint32_t *nslots) {
+    const int S = N * V;
+    std::vector<std::vector<std::array<int, 3>>> ord(N);
+    for (int p = 0; p < N; ++p) interleaved_order(N, V, M, p, ord[p]);
+    auto at = [M](int j, int m) { return (size_t)j * (M + 1) + m; };
+    std::vector<int> stF((size_t)S * (M + 1), -1), stB((size_t)S * (M + 1), -1);
+    std::vector<int> pos(N, 0), free_at(N, 0);
+    const int total = 2 * S * M;
+    int placed = 0, n = 0;
+    while (placed < total) {
+        bool progress = false;
+        for (int p = 0; p < N; ++p) {
+            while (pos[p] < (int)ord[p].size()) {
+                const int kind = ord[p][pos[p]][0], j = ord[p][pos[p]][1], m = ord[p][pos[p]][2];
+                int dep = 0;
+                if (kind == 0 && j > 0) dep = stF[at(j - 1, m)] < 0 ? -1 : stF[at(j - 1, m)] + 1;
+                if (kind == 1 && j < S - 1) dep = stB[at(j + 1, m)] < 0 ? -1 : stB[at(j + 1, m)] + 1;
+                if (dep < 0) break;
+                const int st = std::max(free_at[p], dep);
+                (kind == 0 ? stF : stB)[at(j, m)] = st;
+                free_at[p] = st + 1;
+                n = std::max(n, st + 1);
+                ++pos[p];
+                ++placed;
+                progress = true;
+            }
+        }
+        if (!progress) return false;
+    }
+    std::vector<uint32_t> fm(n, 0), fd(n, 0), bm(n, 0), bd(n, 0);
+    for (int j = 0; j < S; ++j)
+        for (int m = 1; m <= M; ++m) {
+            const int a = stF[at(j, m)], b = stB[at(j, m)];
+            fm[a] |= 1u << j;
+            bm[b] |= 1u << j;
+            if (j > 0) {
+                // forwards of stage j-1 started after F_{j-1,m} and before slot a
+                int newer = 0;
+                for (int mm = 1; mm <= M; ++mm) {
+                    const int t = stF[at(j - 1, mm)];
+                    newer += t > stF[at(j - 1, m)] && t < a;
+                }
+                if (newer > 1) return false;
+                if (newer == 1) fd[a] |= 1u << j;
+            }
+            if (j < S - 1) {
+                int newer = 0;
+                for (int mm = 1; mm <= M; ++mm) {
+                    const int t = stB[at(j + 1, mm)];
+                    newer += t > stB[at(j + 1, m)] && t < b;
+                }
+                if (newer >= max_db) return false;
+                bd[b] |= (uint32_t)newer << (2 * j);
+            }
+        }
+    masks->assign(4 * (size_t)n, 0);
+    for (int k = 0; k < n; ++k) {
+        (*masks)[4 * k] = fm[k];
+        (*masks)[4 * k + 1] = fd[k];
+        (*masks)[4 * k + 2] = bm[k];
+        (*masks)[4 * k + 3] = bd[k];
+    }
+    *nslots = (uint32_t)n;
+    return true;
+}
+
 // The closed-form slot pattern the fast kernel path hard-codes, checked
 // against the simulated schedule (M >= S).
 bool closed_form_matches(int S, int M, const std::vector<uint32_t> &masks) {
@@ -223,14 +318,18 @@ int poseidon_validate(const poseidon_problem *p, uint64_t *n_candidates) {
         return POSEIDON_E_INVAL;
     if (!p->fwd_us || !p->bwd_us || !p->mem_mb || !p->cap_mb) return POSEIDON_E_INVAL;
     if (p->S > 1 && (!p->comm_fwd_us || !p->comm_bwd_us)) return POSEIDON_E_INVAL;
-    if (p->schedule != POSEIDON_SCHEDULE_1F1B && p->schedule != POSEIDON_SCHEDULE_EAGER_1F1B) return POSEIDON_E_INVAL;
+    if (p->schedule > POSEIDON_SCHEDULE_INTERLEAVED_1F1B) return POSEIDON_E_INVAL;
+    // Interleaved 1F1B: S virtual stages on N = S / V >= 2 devices, M a multiple of N
+    const bool ilv = p->schedule == POSEIDON_SCHEDULE_INTERLEAVED_1F1B;
+    if (ilv && (p->V < 2 || p->S % p->V || p->S / p->V < 2 || p->M % (p->S / p->V))) return POSEIDON_E_INVAL;
+    const uint32_t ndev = ilv ? p->S / p->V : p->S;
     uint64_t A;
     if (p->assign) {
         if (p->A < 1 || p->A > (1ull << 32)) return p->A < 1 ? POSEIDON_E_INVAL : POSEIDON_E_RANGE;
-        for (uint64_t i = 0; i < p->A * p->S; ++i)
+        for (uint64_t i = 0; i < p->A * ndev; ++i)
             if (p->assign[i] >= p->T) return POSEIDON_E_INVAL;
         A = p->A;
-    } else if (!pow_fits(p->T, p->S, 1ull << 32, &A)) {
+    } else if (!pow_fits(p->T, ndev, 1ull << 32, &A)) {
         return POSEIDON_E_RANGE;
     }
     const uint64_t nc = binom_sat(p->L - 1, p->S - 1);
@@ -284,8 +383,13 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     uint32_t nslots = 0;
     const uint32_t sched = p->schedule;
     const bool eager = sched == POSEIDON_SCHEDULE_EAGER_1F1B;
-    const bool table_path = eager ? M + 1 < 2 * S : M < S;
-    if (table_path || (uint64_t)S * M <= 4096) {
+    const bool ilv = sched == POSEIDON_SCHEDULE_INTERLEAVED_1F1B;
+    const uint32_t ndev = ilv ? S / p->V : S;
+    const bool table_path = ilv || (eager ? M + 1 < 2 * S : M < S);
+    if (ilv) {
+        if (!build_interleaved_slots((int)ndev, (int)p->V, (int)M, pk::ilv_max_db((int)ndev), &masks, &nslots))
+            return POSEIDON_E_INVAL;
+    } else if (table_path || (uint64_t)S * M <= 4096) {
         if (!build_slots((int)S, (int)M, (int)sched, !eager, &masks, &nslots)) return POSEIDON_E_INVAL;
         if (!table_path && !(eager ? eager_closed_form_matches((int)S, (int)M, masks)
                                    : closed_form_matches((int)S, (int)M, masks)))
@@ -331,11 +435,12 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     for (uint32_t b = 0; b + 1 < S; ++b) { kp.cf[b] = p->comm_fwd_us[b]; kp.cb[b] = p->comm_bwd_us[b]; }
     kp.has_ar = has_ar;
     kp.sched = sched;
+    kp.ndev = ndev;
     for (uint32_t s = 1; s < S; ++s) kp.psi[s] = kp.psi[s - 1] + kp.cf[s - 1];
     // cascade checkpoints of the steady loop: K0, 2 K0, 4 K0, ... below M - S
     // (steady iterations: 1F1B slot pairs after its prologue, Eager 1F1B
     // slot pairs between its prologue and epilogue)
-    if (!table_path) {
+    if (!table_path) {   // (no cascade for the slot-table paths)
         const uint32_t nit = eager ? M + 1 - 2 * S : M - S;
         uint32_t k = std::max<uint32_t>(2, eager ? PK_EAGER_K0 : PK_CASCADE_K0);
         while (k < nit && kp.nlevels < (uint32_t)pk::kMaxLevels) {
@@ -346,7 +451,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     const bool has_table = p->assign && A > 1;
     if (A == 1) {
         kp.assign_mode = pk::kAssignFixed;
-        for (uint32_t s = 0; s < S; ++s) kp.fixed_types[s] = p->assign ? p->assign[s] : 0;
+        for (uint32_t s = 0; s < ndev; ++s) kp.fixed_types[s] = p->assign ? p->assign[s] : 0;
     } else if (has_table) {
         kp.assign_mode = pk::kAssignTable;
     } else {
@@ -362,7 +467,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     const size_t o_pm = off; off = al(off + pm.size() * 4);
     const size_t o_cap = off; off = al(off + (size_t)T * 4);
     const size_t o_binom = off; off = al(off + binom.size());
-    const size_t o_assign = off; off = al(off + (has_table ? (size_t)A * S : 0));
+    const size_t o_assign = off; off = al(off + (has_table ? (size_t)A * ndev : 0));
     const size_t o_slots = off; off = al(off + (table_path ? masks.size() * 4 : 0));
     const size_t o_pd = off; off = al(off + pd.size() * 4);
     const size_t total = off;
@@ -388,7 +493,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
                   hipMemcpy(b + o_cap, p->cap_mb, (size_t)T * 4, hipMemcpyHostToDevice) == hipSuccess &&
                   hipMemcpy(b + o_binom, binom.data(), binom.size(), hipMemcpyHostToDevice) == hipSuccess;
         if (ok && has_table)
-            ok = hipMemcpy(b + o_assign, p->assign, (size_t)A * S, hipMemcpyHostToDevice) == hipSuccess;
+            ok = hipMemcpy(b + o_assign, p->assign, (size_t)A * ndev, hipMemcpyHostToDevice) == hipSuccess;
         if (ok && table_path)
             ok = hipMemcpy(b + o_slots, masks.data(), masks.size() * 4, hipMemcpyHostToDevice) == hipSuccess;
         if (ok && has_ar) ok = hipMemcpy(b + o_pd, pd.data(), pd.size() * 4, hipMemcpyHostToDevice) == hipSuccess;
@@ -413,7 +518,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         if (lds > 64 * 1024) { status = POSEIDON_E_RANGE; break; }
         int occ = 0;
         hipDeviceProp_t prop;
-        if (pk::eval_occupancy(S, wide, lds, has_ar, sched != POSEIDON_SCHEDULE_1F1B, &occ) != hipSuccess || hipGetDeviceProperties(&prop, hip_device) != hipSuccess) {
+        if (pk::eval_occupancy(kp, lds, &occ) != hipSuccess || hipGetDeviceProperties(&prop, hip_device) != hipSuccess) {
             status = POSEIDON_E_DEVICE;
             break;
         }
@@ -613,6 +718,7 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
                                      void *hip_stream) {
     int rc = check_cands(ctx, cands);
     if (rc != POSEIDON_OK) return rc;
+    if (ctx->base.sched == POSEIDON_SCHEDULE_INTERLEAVED_1F1B) return POSEIDON_E_INVAL;
     hipStream_t st = (hipStream_t)hip_stream;
     DeviceGuard g(ctx->device);
     if (!g.ok) return POSEIDON_E_DEVICE;
@@ -815,6 +921,7 @@ extern "C" int poseidon_search(poseidon_ctx *ctx, uint64_t first_row, uint64_t n
                                uint64_t rows_per_chunk, uint32_t flags, poseidon_best *best_out,
                                poseidon_search_stats *stats_out, void *hip_stream) {
     if (!ctx || (flags & ~(uint32_t)(POSEIDON_SEARCH_RIDGE | POSEIDON_SEARCH_NO_STAGE_PRUNING))) return POSEIDON_E_INVAL;
+    if (ctx->base.sched == POSEIDON_SCHEDULE_INTERLEAVED_1F1B) return POSEIDON_E_INVAL;
     if (first_row > ctx->A || n_rows > ctx->A - first_row) return POSEIDON_E_INVAL;
     hipStream_t st = (hipStream_t)hip_stream;
     DeviceGuard g(ctx->device);

@@ -21,6 +21,7 @@ struct KParams {
     const void *binom;         // [S][kNB] C(n, k), uint32 or uint64 (wide)
     const uint8_t *assign;     // [A][S] (table mode)
     const uint32_t *slot_mask; // [nslots][3] forward / deep-forward / backward stage masks
+                               // ([nslots][4] under Interleaved 1F1B: + backward depths)
     const uint32_t *pd;        // [T][L+1] prefix all-reduce time (has_ar)
     uint64_t A, n_comp;
     uint32_t L, S, M, T, NB, nslots;
@@ -29,6 +30,7 @@ struct KParams {
     uint32_t cf[kSMax], cb[kSMax];
     uint32_t has_ar;              // the problem has DP all-reduce times
     uint32_t sched;               // POSEIDON_SCHEDULE_*
+    uint32_t ndev;                // devices: S, or S / V under Interleaved 1F1B
     uint32_t psi[kSMax];          // cf_0 + ... + cf_{s-1}: undoes the per-stage shift at the end
     uint8_t fixed_types[kSMax];
     // candidates of the call
@@ -101,7 +103,10 @@ hipError_t launch_decode(const KParams &p, const LaunchCfg &lc, hipStream_t st);
 hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl);
 hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
                           uint32_t bound, uint32_t publish);
-hipError_t eval_occupancy(uint32_t S, bool wide, size_t lds, bool ar, bool sched, int *blocks);
+hipError_t eval_occupancy(const KParams &p, size_t lds, int *blocks);
+hipError_t launch_ilv(const KParams &p, const LaunchCfg &lc, hipStream_t st);
+hipError_t ilv_occupancy(const KParams &p, size_t lds, int *blocks);
+int ilv_max_db(int N);   // backward input depth the Interleaved 1F1B stencil holds for N devices
 hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,
                          unsigned long long *acc, unsigned int *done, unsigned long long *result, hipStream_t st);
 hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, hipStream_t st);

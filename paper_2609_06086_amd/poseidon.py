@@ -24,7 +24,7 @@ POSEIDON_E_INVAL = -1
 POSEIDON_E_RANGE = -2
 POSEIDON_E_DEVICE = -3
 POSEIDON_E_NOMEM = -4
-SCHEDULE_1F1B, SCHEDULE_EAGER_1F1B = 0, 1
+SCHEDULE_1F1B, SCHEDULE_EAGER_1F1B, SCHEDULE_INTERLEAVED_1F1B = 0, 1, 2
 SEARCH_RIDGE, SEARCH_NO_STAGE_PRUNING = 1, 2
 S_MAX, L_MAX, T_MAX = 16, 256, 8
 
@@ -41,7 +41,7 @@ class _Problem(C.Structure):
                 ("comm_fwd_us", C.c_void_p), ("comm_bwd_us", C.c_void_p),
                 ("mem_mb", C.c_void_p), ("cap_mb", C.c_void_p),
                 ("assign", C.c_void_p), ("A", C.c_uint64), ("allreduce_us", C.c_void_p),
-                ("schedule", C.c_uint32)]
+                ("schedule", C.c_uint32), ("V", C.c_uint32)]
 
 
 class _Cands(C.Structure):
@@ -165,7 +165,7 @@ def _problem_struct(prob):
                   host(prob.assign, np.uint8),
                   int(prob.assign.shape[0]) if prob.assign is not None else 0,
                   host(getattr(prob, "allreduce", None), np.uint32),
-                  int(getattr(prob, "schedule", 0)))
+                  int(getattr(prob, "schedule", 0)), int(getattr(prob, "V", 1)))
     return st, keep
 
 

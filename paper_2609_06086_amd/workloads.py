@@ -27,7 +27,7 @@ from typing import Optional
 import numpy as np
 
 __all__ = ["Problem", "Candidates", "Workload", "workload", "random_problem",
-           "random_candidates", "WORKLOAD_IDS"]
+           "random_candidates", "interleaved_variant", "WORKLOAD_IDS"]
 
 
 @dataclass
@@ -231,3 +231,19 @@ def random_candidates(rng: np.random.Generator, prob: Problem, n: int,
         aidx = rng.integers(0, prob.A, size=n, dtype=np.uint32)
     return Candidates(comp_rank=np.ascontiguousarray(ranks),
                       assign_idx=None if aidx is None else np.ascontiguousarray(aidx))
+
+
+def interleaved_variant(wl: "Workload", V: int = 2) -> "Workload":
+    """The same tables and samples under Interleaved 1F1B: the S stages
+    become virtual stages on S / V devices (V chunks each), and the stage
+    type row keeps its first S / V entries as the device types.  Needs a
+    fixed type row (A = 1) and M a multiple of S / V."""
+    prob = wl.problem
+    N = prob.S // V
+    if prob.assign is None or prob.assign.shape[0] != 1 or prob.S % V or prob.M % N:
+        raise ValueError("interleaved variant needs one fixed type row and M a multiple of S / V")
+    prob.schedule = 2
+    prob.V = V
+    prob.assign = np.ascontiguousarray(prob.assign[:, :N])
+    wl.description = wl.description + f", Interleaved 1F1B with {N} devices x {V} chunks"
+    return wl

@@ -1,7 +1,8 @@
 """Write tests/golden/full_workloads.json from the CPU oracle only.
 
-For each large workload (3, 4, 5, 6, and 4 and 5 under Eager 1F1B, written
-"4e" and "5e") this records, over every candidate:
+For each large workload (3, 4, 5, 6; 4 and 5 under Eager 1F1B, written "4e"
+and "5e"; 5 under Interleaved 1F1B with 8 devices x 2 chunks, "5i") this
+records, over every candidate:
 the SHA-256 of the makespan array (uint32 little-endian), the SHA-256 of the
 feasibility bit array packed as the library's output (bit i % 32 of uint32
 word i / 32), the number of feasible candidates and the argmin.  For
@@ -37,15 +38,17 @@ def pack_bits(f: np.ndarray) -> np.ndarray:
 
 def main():
     res = {"note": "written by tests/golden/make_golden.py from the C oracle; see that script"}
-    only = sys.argv[1:] or ["3", "4", "5", "6", "4e", "5e"]
+    only = sys.argv[1:] or ["3", "4", "5", "6", "4e", "5e", "5i"]
     if os.path.exists(OUT):
         res.update({k: v for k, v in json.load(open(OUT)).items() if k != "note"})
     for spec in only:
-        eager = spec.endswith("e")
-        cfg = int(spec.rstrip("e"))
+        eager, ilv = spec.endswith("e"), spec.endswith("i")
+        cfg = int(spec.rstrip("ei"))
         wl = W.workload(cfg)
         if eager:
             wl.problem.schedule = 1   # Eager 1F1B
+        if ilv:
+            wl = W.interleaved_variant(wl, 2)
         t0 = time.time()
         T, f = coracle.evaluate(wl.problem, wl.cands)
         best = coracle.argmin(T, f)
@@ -68,7 +71,7 @@ def main():
                 ent["bounded"][str(ch)] = {"best_index": b[0], "best_makespan": b[1], "evaluated": ev,
                                            "pruned": pr, "infeasible": inf}
         ent["oracle_seconds"] = round(time.time() - t0, 1)
-        res[f"cfg{cfg}_eager" if eager else f"cfg{cfg}"] = ent
+        res[f"cfg{cfg}_eager" if eager else f"cfg{cfg}_interleaved" if ilv else f"cfg{cfg}"] = ent
         print(spec, ent, flush=True)
     with open(OUT, "w") as fh:
         json.dump(res, fh, indent=1)

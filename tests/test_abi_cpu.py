@@ -1,5 +1,6 @@
 """The C-ABI library on the CPU: it loads, exports every declared entry
 point, and rejects invalid problems before touching the GPU."""
+import math
 import os
 import re
 import subprocess
@@ -134,3 +135,18 @@ def test_closed_form_schedules_pass_the_host_self_check():
 def test_search_rejects_bad_arguments_before_device():
     b, st = P._Best(), P._SearchStats()
     assert P.lib().poseidon_search(None, 0, 1, 100, 0, 0, P.C.byref(b), P.C.byref(st), None) == P.POSEIDON_E_INVAL
+
+
+def test_interleaved_validation():
+    rng = np.random.default_rng(6)
+    p = W.random_problem(rng, 12, 8, 8, 2)
+    p.schedule, p.V = P.SCHEDULE_INTERLEAVED_1F1B, 2     # 4 devices, M = 8 a multiple of 4
+    assert P.poseidon_validate(p) == math.comb(11, 7) * 2 ** 4
+    for V, M in ((1, 8), (3, 8), (2, 6), (8, 8)):        # V < 2, S % V, M % N, one device
+        q = W.random_problem(rng, 12, 8, M, 2)
+        q.schedule, q.V = P.SCHEDULE_INTERLEAVED_1F1B, V
+        assert _status(q) == P.POSEIDON_E_INVAL, (V, M)
+    p.assign = np.array([[0, 1, 1, 0], [1, 1, 0, 0]], dtype=np.uint8)   # rows per device
+    assert P.poseidon_validate(p) == math.comb(11, 7) * 2
+    p.assign = np.array([[0, 1, 2, 0]], dtype=np.uint8)
+    assert _status(p) == P.POSEIDON_E_INVAL
