@@ -23,6 +23,8 @@ FLAGS = [
     "-Wall", "-Wno-unused-function",
     # no packed FP32 instructions anywhere in the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # the Interleaved 1F1B steady pattern is simulated in a constant expression
+    "-fconstexpr-steps=50000000",
     "-I", os.path.join(ROOT, "include"),
 ]
 

@@ -436,6 +436,23 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     kp.has_ar = has_ar;
     kp.sched = sched;
     kp.ndev = ndev;
+    if (ilv) {
+        // the compiled schedule (prologue, `trips` periods, cool-down) is used
+        // only if it equals this problem's own slot table word for word
+        const uint32_t P = 2 * S;
+        std::vector<uint32_t> pro(4 * 4 * (size_t)S), per(4 * (size_t)P), cool(4 * 4 * (size_t)S);
+        int a = 0, e = 0;
+        if (pk::ilv_program_words(S, ndev, &a, &e, pro.data(), per.data(), cool.data()) &&
+            nslots >= (uint32_t)(a + e) && (nslots - a - e) % P == 0) {
+            const uint32_t trips = (nslots - a - e) / P;
+            bool same = std::equal(pro.begin(), pro.begin() + 4 * (size_t)a, masks.begin()) &&
+                        std::equal(cool.begin(), cool.begin() + 4 * (size_t)e, masks.begin() + 4 * ((size_t)nslots - e));
+            for (uint32_t t = 0; same && t < trips; ++t)
+                same = std::equal(per.begin(), per.end(), masks.begin() + 4 * ((size_t)a + (size_t)t * P));
+            kp.ilv_compiled = same;
+            kp.ilv_trips = same ? trips : 0;
+        }
+    }
     for (uint32_t s = 1; s < S; ++s) kp.psi[s] = kp.psi[s - 1] + kp.cf[s - 1];
     // cascade checkpoints of the steady loop: K0, 2 K0, 4 K0, ... below M - S
     // (steady iterations: 1F1B slot pairs after its prologue, Eager 1F1B

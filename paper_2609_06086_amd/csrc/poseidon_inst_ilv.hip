@@ -25,6 +25,50 @@ int ilv_max_db(int N) {
     }
 }
 
+template <int N, int V>
+void section_words(int sec, int n, uint32_t *w) {
+    constexpr int S = N * V;
+    const IlvPattern<N, V> &pat = IlvConst<N, V>::kPat;
+    for (int t = 0; t < n; ++t) {
+        uint32_t fm = 0, fd = 0, bm = 0, bd = 0;
+        for (int q = 0; q < N; ++q) {
+            const int k = pat.kind[sec][t][q], j = pat.chunk[sec][t][q] * N + q, d = pat.depth[sec][t][q];
+            if (k == 0) {
+                fm |= 1u << j;
+                if (d == 2) fd |= 1u << j;
+            } else if (k == 1) {
+                bm |= 1u << j;
+                if (j < S - 1) bd |= (uint32_t)(d - 1) << (2 * j);
+            }
+        }
+        w[4 * t] = fm;
+        w[4 * t + 1] = fd;
+        w[4 * t + 2] = bm;
+        w[4 * t + 3] = bd;
+    }
+}
+
+template <int N, int V>
+bool program_words(int *start, int *tail, uint32_t *pro, uint32_t *period, uint32_t *cool) {
+    const IlvPattern<N, V> &pat = IlvConst<N, V>::kPat;
+    if (pat.start < 0) return false;
+    *start = pat.start;
+    *tail = pat.tail;
+    section_words<N, V>(0, pat.start, pro);
+    section_words<N, V>(1, 2 * N * V, period);
+    section_words<N, V>(2, pat.tail, cool);
+    return true;
+}
+
+bool ilv_program_words(uint32_t S, uint32_t N, int *start, int *tail, uint32_t *pro, uint32_t *period,
+                       uint32_t *cool) {
+#define PK_ILV_PROG(S_, N_) \
+    if (S == S_ && N == N_) return program_words<N_, S_ / N_>(start, tail, pro, period, cool);
+    PK_ILV_PAIRS(PK_ILV_PROG)
+#undef PK_ILV_PROG
+    return false;
+}
+
 hipError_t launch_ilv(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
     const dim3 g(lc.grid), b(kBlock);
 #define PK_ILV_LAUNCH(S_, N_)                                                                              \

@@ -31,6 +31,8 @@ struct KParams {
     uint32_t has_ar;              // the problem has DP all-reduce times
     uint32_t sched;               // POSEIDON_SCHEDULE_*
     uint32_t ndev;                // devices: S, or S / V under Interleaved 1F1B
+    uint32_t ilv_compiled, ilv_trips; // Interleaved 1F1B: the schedule runs as compiled code with
+                                      // this many steady periods
     uint32_t psi[kSMax];          // cf_0 + ... + cf_{s-1}: undoes the per-stage shift at the end
     uint8_t fixed_types[kSMax];
     // candidates of the call
@@ -107,6 +109,11 @@ hipError_t eval_occupancy(const KParams &p, size_t lds, int *blocks);
 hipError_t launch_ilv(const KParams &p, const LaunchCfg &lc, hipStream_t st);
 hipError_t ilv_occupancy(const KParams &p, size_t lds, int *blocks);
 int ilv_max_db(int N);   // backward input depth the Interleaved 1F1B stencil holds for N devices
+// The compiled Interleaved 1F1B schedule for (S, N) as slot-table words:
+// prologue [start][4], one period [2S][4], cool-down [tail][4].  Returns
+// false if (S, N) has no compiled form.
+bool ilv_program_words(uint32_t S, uint32_t N, int *start, int *tail, uint32_t *pro, uint32_t *period,
+                       uint32_t *cool);
 hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,
                          unsigned long long *acc, unsigned int *done, unsigned long long *result, hipStream_t st);
 hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, hipStream_t st);
