@@ -209,28 +209,28 @@ bool build_interleaved_slots(int N, int V, int M, int max_db, std::vector<uint32
         }
         if (!progress) return false;
     }
+    for (int j = 0; j < S; ++j)
+        for (int m = 2; m <= M; ++m)
+            if (stF[at(j, m)] <= stF[at(j, m - 1)] || stB[at(j, m)] <= stB[at(j, m - 1)]) return false;
     std::vector<uint32_t> fm(n, 0), fd(n, 0), bm(n, 0), bd(n, 0);
     for (int j = 0; j < S; ++j)
         for (int m = 1; m <= M; ++m) {
             const int a = stF[at(j, m)], b = stB[at(j, m)];
             fm[a] |= 1u << j;
             bm[b] |= 1u << j;
+            // a stage runs its forwards, and its backwards, in micro-batch
+            // order (checked below), so the nodes newer than micro-batch m's
+            // are those of the following micro-batches that started earlier
             if (j > 0) {
                 // forwards of stage j-1 started after F_{j-1,m} and before slot a
                 int newer = 0;
-                for (int mm = 1; mm <= M; ++mm) {
-                    const int t = stF[at(j - 1, mm)];
-                    newer += t > stF[at(j - 1, m)] && t < a;
-                }
+                for (int mm = m + 1; mm <= M && stF[at(j - 1, mm)] < a; ++mm) ++newer;
                 if (newer > 1) return false;
                 if (newer == 1) fd[a] |= 1u << j;
             }
             if (j < S - 1) {
                 int newer = 0;
-                for (int mm = 1; mm <= M; ++mm) {
-                    const int t = stB[at(j + 1, mm)];
-                    newer += t > stB[at(j + 1, m)] && t < b;
-                }
+                for (int mm = m + 1; mm <= M && stB[at(j + 1, mm)] < b; ++mm) ++newer;
                 if (newer >= max_db) return false;
                 bd[b] |= (uint32_t)newer << (2 * j);
             }

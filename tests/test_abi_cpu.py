@@ -150,3 +150,23 @@ def test_interleaved_validation():
     assert P.poseidon_validate(p) == math.comb(11, 7) * 2
     p.assign = np.array([[0, 1, 2, 0]], dtype=np.uint8)
     assert _status(p) == P.POSEIDON_E_INVAL
+
+
+def test_interleaved_schedules_pass_the_host_checks():
+    """For every (virtual stages, devices) pair the library supports and a
+    range of M, the host's simulation of the Interleaved 1F1B schedule keeps
+    one node per device per slot and input depths the stencil holds (else
+    E_INVAL before any device call; without a GPU a pass ends at E_DEVICE)."""
+    torch = pytest.importorskip("torch")
+    if torch.cuda.is_available():
+        pytest.skip("needs a host without a GPU")
+    rng = np.random.default_rng(7)
+    pairs = [(4, 2), (6, 2), (6, 3), (8, 2), (8, 4), (9, 3), (10, 2), (10, 5), (12, 2), (12, 3), (12, 4), (12, 6),
+             (14, 2), (14, 7), (15, 3), (15, 5), (16, 2), (16, 4), (16, 8)]
+    for S, N in pairs:
+        for k in (1, 2, 3, 5, 8, 13, 40):
+            p = W.random_problem(rng, S + 3, S, N * k, 1)
+            p.schedule, p.V = P.SCHEDULE_INTERLEAVED_1F1B, S // N
+            with pytest.raises(P.PoseidonError) as ei:
+                P.poseidon_load_costs(p, 0)
+            assert ei.value.status == P.POSEIDON_E_DEVICE, (S, N, N * k)
