@@ -178,7 +178,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the evaluation of "
-              f"independent candidates would shard by index range, see DESIGN.md)", file=sys.stderr)
+              f"independent candidates would shard by index range)", file=sys.stderr)
         sys.exit(2)
 
     if args.search:
