@@ -436,6 +436,12 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     kp.has_ar = has_ar;
     kp.sched = sched;
     kp.ndev = ndev;
+    // a last stage [c, L) fits type t iff c >= last_lo[t] (its memory only shrinks with c)
+    for (uint32_t t = 0; t < T; ++t) {
+        uint32_t c = 0;
+        while (c < L && pm[L] - pm[c] > p->cap_mb[t]) ++c;
+        kp.last_lo[t] = c;
+    }
     if (ilv) {
         // the compiled schedule (prologue, `trips` periods, cool-down) is used
         // only if it equals this problem's own slot table word for word
@@ -837,6 +843,7 @@ struct SearchWs {
     unsigned int *tot[pk::kSMax];
     unsigned int *cnt[pk::kSMax];
     unsigned long long *off[pk::kSMax];
+    uint8_t *node[pk::kSMax];
     unsigned long long *words;
 };
 
@@ -852,6 +859,7 @@ SearchWs search_layout(poseidon_ctx *ctx, size_t *bytes) {
         w.codes[l] = (uint32_t *)(b + o); o += words * kSearchCap * 4;
         w.tot[l] = (unsigned int *)(b + o); o += (size_t)kSearchBlk * 4;
         w.cnt[l] = (unsigned int *)(b + o); o += (size_t)kSearchBlk * 4 * 5;
+        w.node[l] = (uint8_t *)(b + o); o += kSearchCap;
         w.off[l] = (unsigned long long *)(b + o); o += ((size_t)kSearchBlk + 1) * 8;
     }
     w.words = (unsigned long long *)(b + o); o += SW_COUNT * 8;
@@ -896,6 +904,7 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n) {
     q.blk_off = r.w.off[x];
     q.blk_cnt = r.w.cnt[x];
     q.blk_stride = kSearchBlk;
+    q.node_cnt = r.w.node[x];
     q.out_row = r.w.row[x + 1];
     q.out_codes = r.w.codes[x + 1];
     q.out_cap = kSearchCap;

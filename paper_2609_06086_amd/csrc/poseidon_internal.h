@@ -31,6 +31,7 @@ struct KParams {
     uint32_t has_ar;              // the problem has DP all-reduce times
     uint32_t sched;               // POSEIDON_SCHEDULE_*
     uint32_t ndev;                // devices: S, or S / V under Interleaved 1F1B
+    uint32_t last_lo[8];          // per type t: smallest c with pm[L] - pm[c] <= cap[t] (search)
     uint32_t ilv_compiled, ilv_trips; // Interleaved 1F1B: the schedule runs as compiled code with
                                       // this many steady periods
     uint32_t psi[kSMax];          // cf_0 + ... + cf_{s-1}: undoes the per-stage shift at the end
@@ -82,6 +83,7 @@ struct SearchParams {
     unsigned int *blk_tot;            // children per block (count kernel)
     unsigned long long *blk_off;      // exclusive offsets, [nblk] = total (scan kernel)
     unsigned int *blk_cnt;            // [5][blk_stride] per-block counters (count kernel)
+    uint8_t *node_cnt;                // children each node keeps (count kernel -> write kernel)
     uint64_t blk_stride;
     uint32_t blk_base;                // first block a write launch covers
     uint32_t flags;                   // kSearchRidge | kSearchNoStage

@@ -152,6 +152,8 @@ __device__ __forceinline__ uint32_t search_children(const KParams &p, const Lds 
     constexpr int NW = Codes<S>::kWords;
     const uint32_t hmax = p.L - (S - 1 - x);   // every later stage keeps one layer
     const bool last_cut = x + 2 == (uint32_t)S;
+    // the last stage [hi, L) exceeds its cap exactly for hi < last_lo[type]
+    const uint32_t mem_lo = p.last_lo[n.tS];
     uint32_t out = 0;
     acc = 0;
     why = 0;
@@ -160,6 +162,10 @@ __device__ __forceinline__ uint32_t search_children(const KParams &p, const Lds 
         if (why) break;
         ++acc;
         if (last_cut) {
+            if (hi < mem_lo) {
+                lp.mem += 1;
+                continue;
+            }
             const SearchNode m = search_extend_to_last(p, tab, n, x, hi, n.tS);
             const int w2 = search_try(p, tab, m, x + 1, p.L, flags, bound);
             lp.pass += w2 == 0;
@@ -234,6 +240,7 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
     if (active) {
         const SearchNode n = search_node<S>(p, tab, row, w, q.level, ty, cut);
         cnt = search_children<S, false>(p, tab, n, q.level, q.flags, bound, why, acc, lp, q, 0, w);
+        q.node_cnt[i] = (uint8_t)cnt;   // at most L - 1 < 256 children
     }
     __shared__ unsigned int tot;
     if (threadIdx.x == 0) tot = 0;
@@ -258,21 +265,20 @@ __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchP
     const uint32_t i = blk * kBlock + threadIdx.x;
     const bool active = i < q.n_in;
     const uint32_t bound = *q.bound;
-    uint32_t row, w[Codes<S>::kWords], ty[S], cut[S + 1];
-    search_load<S>(q, i, active, row, w);
-    uint32_t cnt = 0, acc = 0;
-    LastStage lp;
-    int why = 0;
-    SearchNode n{};
-    if (active) {
-        n = search_node<S>(p, tab, row, w, q.level, ty, cut);
-        cnt = search_children<S, false>(p, tab, n, q.level, q.flags, bound, why, acc, lp, q, 0, w);
-    }
+    // the count kernel left each node's number of children: nodes without
+    // any (most of them at the level that fixes the last cut) do nothing
+    const uint32_t cnt = active ? q.node_cnt[i] : 0u;
     unsigned long long total;
     const unsigned long long local = block_exclusive_scan_u64(cnt, total);
-    if (active && cnt)
+    if (cnt) {
+        uint32_t row, w[Codes<S>::kWords], ty[S], cut[S + 1], acc = 0;
+        LastStage lp;
+        int why = 0;
+        search_load<S>(q, i, true, row, w);
+        const SearchNode n = search_node<S>(p, tab, row, w, q.level, ty, cut);
         search_children<S, true>(p, tab, n, q.level, q.flags, bound, why, acc, lp, q,
                                  q.blk_off[blk] - q.blk_off[q.blk_base] + local, w);
+    }
 }
 
 // Level S-1: the last stage is [c_{S-1}, L); test it like any stage, then

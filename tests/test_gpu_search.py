@@ -60,6 +60,20 @@ def test_search_random_problems(dev):
             check(prob, bound, dev, **kw)
 
 
+def test_search_deep_pipelines(dev):
+    """S = 9..16 stages with few spare layers (every level of the frontier,
+    the last-cut test at level S-2, wide composition ranks)."""
+    rng = np.random.default_rng(123)
+    for S in range(9, 17):
+        L = S + int(rng.integers(1, 7))
+        M = int(rng.integers(1, 2 * S + 4))
+        prob = W.random_problem(rng, L, S, M, 2, cost_hi=300, mem_hi=30, cap=int(rng.integers(60, 200)),
+                                assign_rows=int(rng.integers(1, 6)))
+        prob.schedule = S % 2
+        for kw in (dict(), dict(ridge=True, rows_per_chunk=2)):
+            check(prob, 2 ** 31 - 1, dev, **kw)
+
+
 def test_search_row_ranges_and_no_result(dev):
     rng = np.random.default_rng(121)
     prob = W.random_problem(rng, 12, 4, 9, 3, mem_hi=30, cap=90)
