@@ -23,7 +23,11 @@
  * alternates one forward and one backward pass, then drains the remaining
  * backward passes (the common order; the paper does not spell out the
  * warm-up length).  Eager 1F1B (App. B.1) runs 2(S - s) + 1 warm-up
- * forwards and then alternates a backward and a forward pass.
+ * forwards and then alternates a backward and a forward pass.  Interleaved
+ * 1F1B (Sec. 4.1.4) puts V model chunks on every device; see
+ * poseidon_problem.V.  With data-parallel all-reduce times (Sec. 4.1.1,
+ * 4.1.3) each stage (device) ends with an all-reduce node and T is the
+ * latest of them.
  *
  * All times are integer microseconds and all memory sizes integer MB, held
  * in uint32; every result is exact integer arithmetic.
@@ -144,15 +148,17 @@ int poseidon_validate(const poseidon_problem *problem, uint64_t *n_candidates);
 /* Copy the profile tables to device `hip_device` and build the lookup
  * tables every candidate evaluation shares: per-type prefix sums of the
  * per-layer costs and memory, the Pascal table used to unrank compositions,
- * and the schedule of the 1F1B DAG for (S, M) (Sec. 5: the DAG depends only
- * on the pipeline depth, so it is built once and only re-weighted).  Fails
+ * and the slot schedule of the problem's DAG for (S, M) and its schedule
+ * (Sec. 5: the DAG depends only on the pipeline depth, so it is built once
+ * and only re-weighted); the schedule the kernels hard-code is checked
+ * against a simulation of it, and a mismatch fails with POSEIDON_E_INVAL.  Fails
  * with POSEIDON_E_RANGE if some candidate's makespan could reach 2^31.  The
  * caller may free the host tables after return; the context owns its device
  * memory until poseidon_free. */
 int poseidon_load_costs(const poseidon_problem *problem, int hip_device, poseidon_ctx **out);
 
 /* Evaluate every candidate of `cands` (Sec. 4.1: stage weights, longest path
- * of the 1F1B DAG; Sec. 3.2 memory feasibility) and reduce to the feasible
+ * of the schedule's DAG; Sec. 3.2 memory feasibility) and reduce to the feasible
  * candidate with the smallest makespan, ties to the smaller index.
  * makespan_out: DEVICE uint32[count] or NULL; gets every candidate's raw T,
  *   feasible or not.
@@ -177,7 +183,8 @@ int poseidon_last_best(poseidon_ctx *ctx, poseidon_best *best_out, void *hip_str
  * same as poseidon_eval_candidates', over evaluated candidates; if its
  * makespan is > bound the call returns POSEIDON_NO_FEASIBLE.  The result
  * is deterministic for a given chunk size.  best_out and stats_out are HOST
- * pointers (either may be NULL); the call synchronises the stream. */
+ * pointers (either may be NULL); the call synchronises the stream.
+ * POSEIDON_E_INVAL for Interleaved 1F1B problems. */
 int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *cands,
                                      uint32_t bound, uint64_t chunk, poseidon_best *best_out,
                                      poseidon_prune_stats *stats_out, void *hip_stream);
