@@ -170,3 +170,10 @@ def test_interleaved_schedules_pass_the_host_checks():
             with pytest.raises(P.PoseidonError) as ei:
                 P.poseidon_load_costs(p, 0)
             assert ei.value.status == P.POSEIDON_E_DEVICE, (S, N, N * k)
+
+
+def test_joint_index_overflow_is_refused():
+    """C(255, 7) compositions x 8^8 assignment digits exceed the 64-bit joint
+    index rank * A + a."""
+    p = W.random_problem(np.random.default_rng(8), 256, 8, 4, 8)
+    assert _status(p) == P.POSEIDON_E_RANGE

@@ -584,3 +584,26 @@ def test_full_workload_eager_matches_golden(cfg, dev):
         assert (b.index, b.makespan) == (exp["best_index"], exp["best_makespan"])
         assert (st.evaluated, st.pruned, st.infeasible) == (exp["evaluated"], exp["pruned"], exp["infeasible"])
     ctx.close()
+
+
+def test_maximum_layer_and_type_counts(dev):
+    """L = 256 (the Pascal table's full column, cut values up to 255) with
+    T = 8 device types, all-reduce nodes, 1F1B and Eager 1F1B, list mode with
+    random and extreme ranks; and T = 8 with all 8^8 assignment digits.  (Both
+    at once would overflow the 64-bit joint index, which the library refuses.)"""
+    rng = np.random.default_rng(140)
+    for schedule in (P.SCHEDULE_1F1B, P.SCHEDULE_EAGER_1F1B):
+        prob = W.random_problem(rng, 256, 8, 40, 8, cost_lo=50, cost_hi=400, mem_hi=20, cap=2000, assign_rows=97)
+        prob.schedule = schedule
+        _with_allreduce(rng, prob, hi=3000)
+        cands = W.random_candidates(rng, prob, 5000)
+        assert int(cands.comp_rank.max()) > 2 ** 32    # wide ranks (u64 Pascal table)
+        check_against_oracle(prob, cands, dev)
+        n_comp = prob.n_compositions
+        edge = W.Candidates(comp_rank=np.array([0, 1, n_comp - 2, n_comp - 1], dtype=np.uint64),
+                            assign_idx=np.array([0, prob.A - 1, 50, prob.A - 2], dtype=np.uint32))
+        check_against_oracle(prob, edge, dev)
+        digits = W.random_problem(rng, 40, 8, 24, 8, mem_hi=20, cap=400)
+        digits.schedule = schedule
+        assert digits.A == 8 ** 8
+        check_against_oracle(digits, W.random_candidates(rng, digits, 5000), dev)
