@@ -774,12 +774,24 @@ __device__ __forceinline__ void enqueue(const KParams &p, int which, unsigned in
 #endif
 constexpr int kIlp = PK_ILP;
 
-// kIlp candidates per lane, H halvings per search (L <= 2^H).  The last cut
-// needs no search: with one cut left, C(n, 1) = n, so c_{S-1} = a + r.
+// Halvings of one cut search: the smallest H with L <= 2^H (at least 5).
+__host__ __device__ constexpr uint32_t decode_levels(uint32_t L) {
+    return L > 128 ? 8u : L > 64 ? 7u : L > 32 ? 6u : 5u;
+}
+
+// kIlp candidates per lane, H halvings per search.  Each Pascal column is
+// held twice in LDS, 2^H entries each: in order (col) and in breadth-first
+// order of the search tree (ey: root at 1, children of i at 2i and 2i+1).
+// Halving b of the search probes one of 2^b neighbouring entries of ey, so
+// the lanes of a wave hit distinct banks; in sorted order those probes lie
+// 2^(H-b) entries apart and share banks.  After H steps the tree index i
+// spells the lower-bound position in its low H bits.  The last cut needs no
+// search: with one cut left, C(n, 1) = n, so c_{S-1} = a + r.
 template <int S, typename R, int H>
-__device__ __forceinline__ void decode_batch(const KParams &p, const R *binom, uint64_t base, uint64_t stride,
-                                             bool &bad) {
+__device__ __forceinline__ void decode_batch(const KParams &p, const R *sorted, const R *ey, uint64_t base,
+                                             uint64_t stride, bool &bad) {
     constexpr int NW = Codes<S>::kWords;
+    constexpr uint32_t NH = 1u << H;
     R r[kIlp];
     bool ok[kIlp];
     uint32_t w[kIlp][NW], at[kIlp];
@@ -798,23 +810,23 @@ __device__ __forceinline__ void decode_batch(const KParams &p, const R *binom, u
     // cut goes straight into its byte of the code words
 #pragma unroll
     for (int j = 1; j <= S - 2; ++j) {
-        const R *col = binom + (S - j) * kNB;
+        const R *col = sorted + (S - j) * NH;
+        const R *tree = ey + (S - j) * NH;
         R Q[kIlp];
-        const R *q[kIlp];
+        uint32_t t[kIlp];   // tree node
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) {
             Q[u] = col[p.L - at[u]] - r[u];
-            q[u] = col;
+            t[u] = 1;
         }
 #pragma unroll
-        for (int b = H - 1; b >= 0; --b) {
-            const uint32_t step = 1u << b;
+        for (int b = 0; b < H; ++b) {
 #pragma unroll
-            for (int u = 0; u < kIlp; ++u) q[u] += q[u][step - 1] < Q[u] ? step : 0u;
+            for (int u = 0; u < kIlp; ++u) t[u] = t[u] + t[u] + (uint32_t)(tree[t[u]] < Q[u]);
         }
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) {
-            const uint32_t pos = (uint32_t)(q[u] - col);
+            const uint32_t pos = t[u] - NH;
             r[u] = col[pos] - Q[u];
             const uint32_t c = p.L - pos;
             w[u][(j - 1) / 4] |= c << (8 * ((j - 1) % 4));
@@ -841,25 +853,36 @@ __device__ __forceinline__ void decode_batch(const KParams &p, const R *binom, u
 }
 
 template <int S, typename R, int H>
-__device__ __forceinline__ void decode_all(const KParams &p, const R *binom, bool &bad) {
+__device__ __forceinline__ void decode_all(const KParams &p, R *lds, bool &bad) {
+    // columns 0 .. S-1, 2^H entries each, in order and in tree order; the
+    // tree node at depth l and offset m probes sorted position
+    // (2m + 1) 2^(H-1-l) - 1 (entry 0 of the tree is unused)
+    constexpr uint32_t NH = 1u << H;
+    R *sorted = lds, *ey = lds + (uint32_t)S * NH;
+    const R *gb = reinterpret_cast<const R *>(p.binom);
+    for (uint32_t e = threadIdx.x; e < (uint32_t)S * NH; e += kBlock) {
+        const uint32_t k = e / NH, i = e % NH;
+        sorted[e] = gb[k * kNB + i];
+        const uint32_t l = i ? 31u - __clz(i) : 0u, m = i - (1u << l);
+        ey[e] = i ? gb[k * kNB + (2 * m + 1) * (NH >> (l + 1)) - 1] : (R)0;
+    }
+    __syncthreads();
     const uint64_t stride = (uint64_t)gridDim.x * kBlock;
     for (uint64_t base = (uint64_t)blockIdx.x * kBlock + threadIdx.x; base < p.n_i; base += kIlp * stride)
-        decode_batch<S, R, H>(p, binom, base, stride, bad);
+        decode_batch<S, R, H>(p, sorted, ey, base, stride, bad);
 }
 
 template <int S, typename R>
 __global__ __launch_bounds__(kBlock) void decode_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
-    R *binom = reinterpret_cast<R *>(smem);
-    const uint32_t nbin = p.S * kNB;
-    const R *gb = reinterpret_cast<const R *>(p.binom);
-    for (uint32_t i = threadIdx.x; i < nbin; i += kBlock) binom[i] = gb[i];
-    __syncthreads();
+    R *lds = reinterpret_cast<R *>(smem);
     bool bad = false;
-    if (p.L > 128) decode_all<S, R, 8>(p, binom, bad);
-    else if (p.L > 64) decode_all<S, R, 7>(p, binom, bad);
-    else if (p.L > 32) decode_all<S, R, 6>(p, binom, bad);
-    else decode_all<S, R, 5>(p, binom, bad);
+    switch (decode_levels(p.L)) {
+    case 8: decode_all<S, R, 8>(p, lds, bad); break;
+    case 7: decode_all<S, R, 7>(p, lds, bad); break;
+    case 6: decode_all<S, R, 6>(p, lds, bad); break;
+    default: decode_all<S, R, 5>(p, lds, bad); break;
+    }
     if (bad) atomicOr(p.err, 1u);
 }
 
@@ -1161,7 +1184,8 @@ hipError_t launch_eval_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) 
 
 template <int S, typename R>
 hipError_t launch_decode_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
-    const size_t lds = (size_t)p.S * kNB * sizeof(R);
+    // both copies of the S Pascal columns, 2^H entries each
+    const size_t lds = 2 * (size_t)S * ((size_t)1 << decode_levels(p.L)) * sizeof(R);
     hipLaunchKernelGGL((decode_kernel<S, R>), dim3(lc.grid), dim3(kBlock), lds, st, p);
     return hipGetLastError();
 }
