@@ -127,6 +127,7 @@ hipError_t launch_decode(const KParams &p, const LaunchCfg &lc, hipStream_t st) 
 }
 
 hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl) {
+    if (p.sched == 2) return launch_ilv_resume(p, lc, st, lvl);   // Interleaved 1F1B
     PK_DISPATCH(launch_resume_s, p.S, p.wide, p, lc, st, lvl)
 }
 

@@ -23,6 +23,9 @@
 #ifndef PK_EAGER_K0
 #define PK_EAGER_K0 (2 * S)   // the same for Eager 1F1B, whose steady state settles later
 #endif
+#ifndef PK_ILV_K0
+#define PK_ILV_K0 3   // the same for Interleaved 1F1B, in periods of 2S slots
+#endif
 
 namespace {
 
@@ -470,6 +473,12 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
             kp.lvl_k[kp.nlevels++] = k;
             k *= 2;
         }
+    } else if (ilv && kp.ilv_compiled) {   // Interleaved 1F1B: checkpoints in periods
+        uint32_t k = std::max<uint32_t>(1, PK_ILV_K0);
+        while (k < kp.ilv_trips && kp.nlevels < (uint32_t)pk::kMaxLevels) {
+            kp.lvl_k[kp.nlevels++] = k;
+            k *= 2;
+        }
     }
     const bool has_table = p->assign && A > 1;
     if (A == 1) {
@@ -635,8 +644,13 @@ constexpr uint64_t kChunk = 1ull << 26;
 // only after the stream has drained.
 uint64_t queue_cap(const poseidon_ctx *ctx, uint64_t n) { return n + (uint64_t)ctx->grid_max * 256; }
 
-// DP state words per queue entry: S registers for 1F1B, 2S for Eager 1F1B
-uint64_t queue_state_words(const poseidon_ctx *ctx) { return ctx->base.sched ? 2ull * ctx->S : ctx->S; }
+// DP state words per queue entry: S registers for 1F1B, 2S for Eager 1F1B,
+// the live registers at a period boundary for Interleaved 1F1B
+uint64_t queue_state_words(const poseidon_ctx *ctx) {
+    if (ctx->base.sched == POSEIDON_SCHEDULE_INTERLEAVED_1F1B)
+        return (uint64_t)pk::ilv_state_words(ctx->S, ctx->base.ndev);
+    return ctx->base.sched ? 2ull * ctx->S : ctx->S;
+}
 
 int ensure_workspace(poseidon_ctx *ctx, uint64_t n, hipStream_t st) {
     if (ctx->ws_cap >= n) return POSEIDON_OK;

@@ -71,22 +71,56 @@ bool ilv_program_words(uint32_t S, uint32_t N, int *start, int *tail, uint32_t *
 
 hipError_t launch_ilv(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
     const dim3 g(lc.grid), b(kBlock);
-#define PK_ILV_LAUNCH(S_, N_)                                                                              \
-    if (p.S == S_ && p.ndev == N_) {                                                                   \
-        if (p.has_ar) hipLaunchKernelGGL((ilv_kernel<S_, N_, true>), g, b, lc.lds_bytes, st, p);        \
-        else hipLaunchKernelGGL((ilv_kernel<S_, N_, false>), g, b, lc.lds_bytes, st, p);                \
-        return hipGetLastError();                                                                      \
+#define PK_ILV_LAUNCH(S_, N_)                                                                                  \
+    if (p.S == S_ && p.ndev == N_) {                                                                       \
+        if (p.ilv_compiled) {                                                                              \
+            if (p.has_ar) hipLaunchKernelGGL((ilv_kernel<S_, N_, true, false>), g, b, lc.lds_bytes, st, p);  \
+            else hipLaunchKernelGGL((ilv_kernel<S_, N_, false, false>), g, b, lc.lds_bytes, st, p);          \
+        } else {                                                                                           \
+            if (p.has_ar) hipLaunchKernelGGL((ilv_kernel<S_, N_, true, true>), g, b, lc.lds_bytes, st, p);   \
+            else hipLaunchKernelGGL((ilv_kernel<S_, N_, false, true>), g, b, lc.lds_bytes, st, p);           \
+        }                                                                                                  \
+        return hipGetLastError();                                                                          \
     }
     PK_ILV_PAIRS(PK_ILV_LAUNCH)
 #undef PK_ILV_LAUNCH
     return hipErrorInvalidValue;
 }
 
+hipError_t launch_ilv_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl) {
+    const dim3 g(lc.grid), b(kBlock);
+#define PK_ILV_RESUME(S_, N_)                                                                                   \
+    if (p.S == S_ && p.ndev == N_) {                                                                           \
+        if (p.has_ar) hipLaunchKernelGGL((ilv_resume_kernel<S_, N_, true>), g, b, lc.lds_bytes, st, p, lvl);    \
+        else hipLaunchKernelGGL((ilv_resume_kernel<S_, N_, false>), g, b, lc.lds_bytes, st, p, lvl);            \
+        return hipGetLastError();                                                                              \
+    }
+    PK_ILV_PAIRS(PK_ILV_RESUME)
+#undef PK_ILV_RESUME
+    return hipErrorInvalidValue;
+}
+
+int ilv_state_words(uint32_t S, uint32_t N) {
+#define PK_ILV_WORDS(S_, N_) \
+    if (S == S_ && N == N_) return IlvLiveConst<N_, S_ / N_>::kLive.n;
+    PK_ILV_PAIRS(PK_ILV_WORDS)
+#undef PK_ILV_WORDS
+    return 0;
+}
+
 hipError_t ilv_occupancy(const KParams &p, size_t lds, int *blocks) {
-#define PK_ILV_OCC(S_, N_)                                                                                  \
-    if (p.S == S_ && p.ndev == N_)                                                                     \
-        return p.has_ar ? hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, ilv_kernel<S_, N_, true>, kBlock, lds) \
-                        : hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, ilv_kernel<S_, N_, false>, kBlock, lds);
+#define PK_ILV_OCC(S_, N_)                                                                                   \
+    if (p.S == S_ && p.ndev == N_) {                                                                    \
+        if (p.ilv_compiled)                                                                             \
+            return p.has_ar ? hipOccupancyMaxActiveBlocksPerMultiprocessor(                             \
+                                  blocks, ilv_kernel<S_, N_, true, false>, kBlock, lds)                 \
+                            : hipOccupancyMaxActiveBlocksPerMultiprocessor(                             \
+                                  blocks, ilv_kernel<S_, N_, false, false>, kBlock, lds);               \
+        return p.has_ar ? hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, ilv_kernel<S_, N_, true, true>, \
+                                                                       kBlock, lds)                     \
+                        : hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, ilv_kernel<S_, N_, false, true>, \
+                                                                       kBlock, lds);                    \
+    }
     PK_ILV_PAIRS(PK_ILV_OCC)
 #undef PK_ILV_OCC
     return hipErrorInvalidValue;

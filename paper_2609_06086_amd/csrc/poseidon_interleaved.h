@@ -158,6 +158,121 @@ struct IlvConst {
     static constexpr IlvPattern<N, V> kPat = ilv_pattern<N, V>();
 };
 
+// ---------------------------------------------------------------------------
+// Registers live at a period boundary: read by a later node before they are
+// written again, in the next period or in the cool-down.  X[q] always is; a
+// shift-register entry at position e of stage j is when a node reads depth
+// d of that stage's queue after w writes to it with d - 1 - w = e.  The
+// live registers, packed in a fixed order (X, then the forward queues
+// stage by stage, then the backward queues), are the whole state the rest
+// of the DP depends on: the steady-state check compares them between two
+// periods and the straggler queue stores them.  Every register is written
+// in every period (each stage runs N >= 2 forwards and N >= depth
+// backwards per period), so once the live registers rise by the same d
+// over one period, every later period does the same.
+// ---------------------------------------------------------------------------
+template <int N, int V>
+struct IlvLive {
+    static constexpr int S = N * V, DB = IlvDepth<N>::kB;
+    int f[2][S] = {};   // word of Fq0[j] / Fq1[j] in the packed state, or -1
+    int b[DB][S] = {};  // word of Bq[e][j], or -1
+    int n = 0;          // live words
+};
+
+template <int N, int V>
+constexpr IlvLive<N, V> ilv_live() {
+    constexpr int S = N * V, DB = IlvDepth<N>::kB;
+    constexpr const IlvPattern<N, V> &pat = IlvConst<N, V>::kPat;
+    bool lf[2][S] = {}, lb[DB][S] = {};
+    for (int sec = 1; sec <= 2; ++sec) {
+        const int ns = sec == 1 ? 2 * N * V : pat.tail;
+        int wf[S] = {}, wb[S] = {};
+        for (int t = 0; t < ns; ++t) {
+            // a slot reads before it writes (synchronous update)
+            for (int q = 0; q < N; ++q) {
+                const int kd = pat.kind[sec][t][q], j = pat.chunk[sec][t][q] * N + q, d = pat.depth[sec][t][q];
+                if (kd == 0 && j > 0 && d - 1 - wf[j - 1] >= 0) lf[d - 1 - wf[j - 1]][j - 1] = true;
+                if (kd == 1 && j < S - 1 && d - 1 - wb[j + 1] >= 0) lb[d - 1 - wb[j + 1]][j + 1] = true;
+            }
+            for (int q = 0; q < N; ++q) {
+                const int kd = pat.kind[sec][t][q], j = pat.chunk[sec][t][q] * N + q;
+                if (kd == 0) ++wf[j];
+                if (kd == 1) ++wb[j];
+            }
+        }
+    }
+    IlvLive<N, V> r{};
+    r.n = N;
+    for (int j = 0; j < S; ++j)
+        for (int e = 0; e < 2; ++e) r.f[e][j] = lf[e][j] ? r.n++ : -1;
+    for (int e = 0; e < DB; ++e)
+        for (int j = 0; j < S; ++j) r.b[e][j] = lb[e][j] ? r.n++ : -1;
+    return r;
+}
+
+template <int N, int V>
+struct IlvLiveConst {
+    static constexpr IlvLive<N, V> kLive = ilv_live<N, V>();
+};
+
+// Apply `fn` to every live register with its packed word index W
+// (fn.template at<W>(reg); W < 0 marks a dead register).
+template <int S, int N, int E, typename Fn, int... J>
+__device__ __forceinline__ void ilv_live_bwd(std::integer_sequence<int, J...>, uint32_t (&Bq)[IlvDepth<N>::kB][S],
+                                             Fn &fn) {
+    constexpr const IlvLive<N, S / N> &lv = IlvLiveConst<N, S / N>::kLive;
+    (fn.template at<lv.b[E][J]>(Bq[E][J]), ...);
+}
+
+template <int S, int N, typename Fn, int... E>
+__device__ __forceinline__ void ilv_live_bwd_all(std::integer_sequence<int, E...>,
+                                                 uint32_t (&Bq)[IlvDepth<N>::kB][S], Fn &fn) {
+    (ilv_live_bwd<S, N, E>(std::make_integer_sequence<int, S>{}, Bq, fn), ...);
+}
+
+template <int S, int N, typename Fn, int... J>
+__device__ __forceinline__ void ilv_live_fwd(std::integer_sequence<int, J...>, uint32_t (&Fq0)[S], uint32_t (&Fq1)[S],
+                                             Fn &fn) {
+    constexpr const IlvLive<N, S / N> &lv = IlvLiveConst<N, S / N>::kLive;
+    (fn.template at<lv.f[0][J]>(Fq0[J]), ...);
+    (fn.template at<lv.f[1][J]>(Fq1[J]), ...);
+}
+
+template <int S, int N, typename Fn, int... Q>
+__device__ __forceinline__ void ilv_live_x(std::integer_sequence<int, Q...>, uint32_t (&X)[N], Fn &fn) {
+    (fn.template at<Q>(X[Q]), ...);
+}
+
+template <int S, int N, typename Fn>
+__device__ __forceinline__ void ilv_each_live(uint32_t (&X)[N], uint32_t (&Fq0)[S], uint32_t (&Fq1)[S],
+                                              uint32_t (&Bq)[IlvDepth<N>::kB][S], Fn &fn) {
+    ilv_live_x<S, N>(std::make_integer_sequence<int, N>{}, X, fn);
+    ilv_live_fwd<S, N>(std::make_integer_sequence<int, S>{}, Fq0, Fq1, fn);
+    ilv_live_bwd_all<S, N>(std::make_integer_sequence<int, IlvDepth<N>::kB>{}, Bq, fn);
+}
+
+template <int NL>
+struct IlvPack {      // registers -> packed words
+    uint32_t (&w)[NL];
+    template <int W> __device__ __forceinline__ void at(uint32_t &r) { if constexpr (W >= 0) w[W] = r; }
+};
+template <int NL>
+struct IlvUnpack {    // packed words -> registers
+    const uint32_t (&w)[NL];
+    template <int W> __device__ __forceinline__ void at(uint32_t &r) { if constexpr (W >= 0) r = w[W]; }
+};
+template <int NL>
+struct IlvSame {      // does every live register exceed its old value by d?
+    const uint32_t (&old)[NL];
+    uint32_t d;
+    bool ok;
+    template <int W> __device__ __forceinline__ void at(uint32_t &r) { if constexpr (W >= 0) ok = ok && r - old[W] == d; }
+};
+struct IlvShift {     // add a constant to every live register
+    uint32_t v;
+    template <int W> __device__ __forceinline__ void at(uint32_t &r) { if constexpr (W >= 0) r += v; }
+};
+
 // Slots [k0, k1) of the host's slot table (prologue and cool-down).
 template <int S, int N>
 __device__ __forceinline__ void ilv_table_slots(const KParams &p, uint32_t k0, uint32_t k1, const uint32_t (&F)[S],
@@ -261,17 +376,9 @@ __device__ __forceinline__ void ilv_section_ct(std::integer_sequence<int, T...>,
     (ilv_slot_ct<S, N, SEC, T>(std::make_integer_sequence<int, N>{}, p, F, B, X, Fq0, Fq1, Bq), ...);
 }
 
-// The whole DP.  Compiled form (p.ilv_trips > 0 or a schedule made only of
-// prologue and cool-down, checked by the host against the problem's own
-// table): prologue, `trips` periods and the cool-down as straight-line code.
-// Otherwise the host's slot table drives the same update.  After it X[q] is
-// the finish of device q's last node.
 template <int S, int N>
-__device__ __forceinline__ void ilv_dp(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
-                                       uint32_t (&X)[N]) {
-    constexpr int DB = IlvDepth<N>::kB, P = 2 * S;
-    constexpr IlvPattern<N, S / N> const &pat = IlvConst<N, S / N>::kPat;
-    uint32_t Fq0[S], Fq1[S], Bq[DB][S];
+__device__ __forceinline__ void ilv_init(uint32_t (&X)[N], uint32_t (&Fq0)[S], uint32_t (&Fq1)[S],
+                                         uint32_t (&Bq)[IlvDepth<N>::kB][S]) {
 #pragma unroll
     for (int q = 0; q < N; ++q) X[q] = 0;
 #pragma unroll
@@ -279,31 +386,108 @@ __device__ __forceinline__ void ilv_dp(const KParams &p, const uint32_t (&F)[S],
         Fq0[j] = 0;
         Fq1[j] = 0;
 #pragma unroll
-        for (int d = 0; d < DB; ++d) Bq[d][j] = 0;
+        for (int d = 0; d < IlvDepth<N>::kB; ++d) Bq[d][j] = 0;
     }
-    if constexpr (pat.start >= 0) {
-        if (p.ilv_compiled) {
-            ilv_section_ct<S, N, 0>(std::make_integer_sequence<int, (pat.start > 0 ? pat.start : 0)>{}, p, F, B, X,
-                                    Fq0, Fq1, Bq);
-            for (uint32_t t = 0; t < p.ilv_trips; ++t)
-                ilv_section_ct<S, N, 1>(std::make_integer_sequence<int, P>{}, p, F, B, X, Fq0, Fq1, Bq);
-            ilv_section_ct<S, N, 2>(std::make_integer_sequence<int, pat.tail>{}, p, F, B, X, Fq0, Fq1, Bq);
-            return;
-        }
-    }
-    ilv_table_slots<S, N>(p, 0, p.nslots, F, B, X, Fq0, Fq1, Bq);
 }
 
+// n steady periods of the compiled schedule
+template <int S, int N>
+__device__ __forceinline__ void ilv_periods(const KParams &p, uint32_t n, const uint32_t (&F)[S],
+                                            const uint32_t (&B)[S], uint32_t (&X)[N], uint32_t (&Fq0)[S],
+                                            uint32_t (&Fq1)[S], uint32_t (&Bq)[IlvDepth<N>::kB][S]) {
+    for (uint32_t t = 0; t < n; ++t)
+        ilv_section_ct<S, N, 1>(std::make_integer_sequence<int, 2 * S>{}, p, F, B, X, Fq0, Fq1, Bq);
+}
+
+// Periods k0+1 .. k1 of `trips` (k0 < k1).  With k1 < trips the live
+// registers after period k1 are compared with those after period k1 - 1;
+// if all rose by the same d, the period map (built from max and + only)
+// will raise them by d every time, so they jump to the end of the periods
+// at once.  Returns whether the lane is at the end of the periods.
+template <int S, int N>
+__device__ __forceinline__ bool ilv_advance(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                            uint32_t (&X)[N], uint32_t (&Fq0)[S], uint32_t (&Fq1)[S],
+                                            uint32_t (&Bq)[IlvDepth<N>::kB][S], uint32_t k0, uint32_t k1,
+                                            uint32_t trips) {
+    if (k1 >= trips) {
+        ilv_periods<S, N>(p, trips - k0, F, B, X, Fq0, Fq1, Bq);
+        return true;
+    }
+    ilv_periods<S, N>(p, k1 - k0 - 1, F, B, X, Fq0, Fq1, Bq);
+    constexpr int NL = IlvLiveConst<N, S / N>::kLive.n;
+    uint32_t old[NL];
+    IlvPack<NL> pack{old};
+    ilv_each_live<S, N>(X, Fq0, Fq1, Bq, pack);
+    ilv_section_ct<S, N, 1>(std::make_integer_sequence<int, 2 * S>{}, p, F, B, X, Fq0, Fq1, Bq);
+    IlvSame<NL> same{old, X[0] - old[0], true};
+    ilv_each_live<S, N>(X, Fq0, Fq1, Bq, same);
+    IlvShift jump{same.ok ? (trips - k1) * same.d : 0u};
+    ilv_each_live<S, N>(X, Fq0, Fq1, Bq, jump);
+    return same.ok;
+}
+
+// Stage types, weights and per-device memory check of one candidate.
+template <int S, int N>
+__device__ __forceinline__ bool ilv_weights(const KParams &p, const Lds &tab, const uint32_t (&cut)[S + 1],
+                                            uint32_t a, uint32_t (&tyd)[N], uint32_t (&F)[S], uint32_t (&B)[S]) {
+    constexpr int V = S / N;
+    uint32_t ty[S];
+    decode_types<N>(p, a, tyd);
+#pragma unroll
+    for (int j = 0; j < S; ++j) ty[j] = tyd[j % N];
+    stage_weights<S>(p, tab, cut, ty, F, B);
+    // a device fits when all its chunks' layers fit its memory
+    bool feas = true;
+#pragma unroll
+    for (int q = 0; q < N; ++q) {
+        uint32_t mem = 0;
+#pragma unroll
+        for (int c = 0; c < V; ++c) mem += tab.pm[cut[c * N + q + 1]] - tab.pm[cut[c * N + q]];
+        feas = feas && mem <= tab.cap[tyd[q]];
+    }
+    return feas;
+}
+
+// T: the end node follows every device's all-reduce node
 template <int S, int N, bool AR>
+__device__ __forceinline__ uint32_t ilv_end(const KParams &p, const Lds &tab, const uint32_t (&X)[N],
+                                            const uint32_t (&cut)[S + 1], const uint32_t (&tyd)[N]) {
+    constexpr int V = S / N;
+    const uint32_t row = p.L + 1;
+    uint32_t T = 0;
+#pragma unroll
+    for (int q = 0; q < N; ++q) {
+        uint32_t d = 0;
+        if (AR) {
+#pragma unroll
+            for (int c = 0; c < V; ++c)
+                d += tab.pd[tyd[q] * row + cut[c * N + q + 1]] - tab.pd[tyd[q] * row + cut[c * N + q]];
+        }
+        T = max(T, X[q] + d);
+    }
+    return T;
+}
+
+// (a2)-(a4), (a6) under Interleaved 1F1B.  Compiled form (TAB = false, used
+// when p.ilv_compiled, which the host sets after checking the compiled
+// schedule against the problem's own slot table): prologue, periods and
+// cool-down as straight-line code; with a cascade (p.nlevels > 0) a lane
+// whose live registers have not settled by period p.lvl_k[0] is queued for
+// ilv_resume_kernel.  TAB = true: the host's slot table drives the same
+// update (a separate instance, so that its registers do not weigh on the
+// compiled one).  X[q] ends as device q's last finish.
+template <int S, int N, bool AR, bool TAB>
 __global__ __launch_bounds__(kBlock) void ilv_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
     const Lds tab = stage_tables(p, smem);
-    constexpr int NW = Codes<S>::kWords;
-    constexpr int V = S / N;
+    constexpr int NW = Codes<S>::kWords, DB = IlvDepth<N>::kB;
+    constexpr const IlvPattern<N, S / N> &pat = IlvConst<N, S / N>::kPat;
     unsigned long long best = ~0ull;
     const uint64_t stride = (uint64_t)gridDim.x * kBlock;
     const uint64_t span = (p.n_i + stride - 1) / stride;
-    const uint32_t row = p.L + 1;
+    __shared__ unsigned int nq;
+    if (threadIdx.x == 0) nq = 0;
+    __syncthreads();
     uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
     for (uint64_t it = 0; it < span; ++it, i += stride) {
         const bool active = i < p.n_i;
@@ -311,49 +495,110 @@ __global__ __launch_bounds__(kBlock) void ilv_kernel(KParams p) {
         uint32_t w[NW];
 #pragma unroll
         for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[(uint64_t)k * p.ccap + i] : 0u;
-        uint32_t cut[S + 1], tyd[N], ty[S], F[S], B[S], X[N];
+        uint32_t cut[S + 1], tyd[N], F[S], B[S], X[N], Fq0[S], Fq1[S], Bq[DB][S];
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = ok ? assign_of(p, gi) : 0u;
-        decode_types<N>(p, a, tyd);
-#pragma unroll
-        for (int j = 0; j < S; ++j) ty[j] = tyd[j % N];
-        stage_weights<S>(p, tab, cut, ty, F, B);
-        // a device fits when all its chunks' layers fit its memory
-        bool feas = ok && active;
-#pragma unroll
-        for (int q = 0; q < N; ++q) {
-            uint32_t mem = 0;
-#pragma unroll
-            for (int c = 0; c < V; ++c) mem += tab.pm[cut[c * N + q + 1]] - tab.pm[cut[c * N + q]];
-            feas = feas && mem <= tab.cap[tyd[q]];
-        }
-        ilv_dp<S, N>(p, F, B, X);
-        // the end node follows every device's all-reduce node
-        uint32_t T = 0;
-#pragma unroll
-        for (int q = 0; q < N; ++q) {
-            uint32_t d = 0;
-            if (AR) {
-#pragma unroll
-                for (int c = 0; c < V; ++c)
-                    d += tab.pd[tyd[q] * row + cut[c * N + q + 1]] - tab.pd[tyd[q] * row + cut[c * N + q]];
+        const bool feas = ilv_weights<S, N>(p, tab, cut, a, tyd, F, B) && ok && active;
+        ilv_init<S, N>(X, Fq0, Fq1, Bq);
+        bool done_here = true;
+        if constexpr (!TAB && pat.start >= 0) {
+            ilv_section_ct<S, N, 0>(std::make_integer_sequence<int, (pat.start > 0 ? pat.start : 0)>{}, p, F, B, X,
+                                    Fq0, Fq1, Bq);
+            const uint32_t k1 = p.nlevels ? p.lvl_k[0] : p.ilv_trips;
+            done_here = ilv_advance<S, N>(p, F, B, X, Fq0, Fq1, Bq, 0, k1, p.ilv_trips);
+            if (p.nlevels) {
+                constexpr int NL = IlvLiveConst<N, S / N>::kLive.n;
+                uint32_t Z[NL];
+                IlvPack<NL> pack{Z};
+                ilv_each_live<S, N>(X, Fq0, Fq1, Bq, pack);
+                enqueue<S, NL>(p, 0, &nq, !done_here && active && ok, (uint32_t)gi, w, Z);
             }
-            T = max(T, X[q] + d);
+            ilv_section_ct<S, N, 2>(std::make_integer_sequence<int, pat.tail>{}, p, F, B, X, Fq0, Fq1, Bq);
+        } else {
+            ilv_table_slots<S, N>(p, 0, p.nslots, F, B, X, Fq0, Fq1, Bq);
         }
+        uint32_t T = ilv_end<S, N, AR>(p, tab, X, cut, tyd);
         if (!ok) T = 0xFFFFFFFFu;
-        if (active && p.makespan_out) p.makespan_out[gi] = T;
+        const bool write = active && (done_here || !ok);
+        if (write && p.makespan_out) p.makespan_out[gi] = T;
         if (p.feas_bits_out) {
             const unsigned long long bits = __ballot(feas);
             const uint64_t w0 = (gi - (threadIdx.x & 63)) >> 5;
             if ((threadIdx.x & 63) == 0 && w0 < p.nwords) p.feas_bits_out[w0] = (uint32_t)bits;
             if ((threadIdx.x & 63) == 32 && w0 + 1 < p.nwords) p.feas_bits_out[w0 + 1] = (uint32_t)(bits >> 32);
         }
-        if (active) {
+        if (write) {
             const unsigned long long key = make_key(feas, T, (uint32_t)gi);
             best = key < best ? key : best;
         }
     }
-    block_min_and_finish(best, p.acc, p.done, p.result, nullptr, true, p.accumulate);
+    if (p.nlevels) {
+        __syncthreads();
+        if (threadIdx.x == 0) p.qcount[blockIdx.x] = nq;   // entries for level 1
+    }
+    block_min_and_finish(best, p.acc, p.done, p.result, nullptr, p.nlevels == 0, p.accumulate);
+}
+
+// Level `lvl` of the Interleaved 1F1B cascade: resume the queued lanes from
+// period p.lvl_k[lvl-1] to p.lvl_k[lvl] (the end at the last level), then
+// run the cool-down (only compiled schedules have a cascade).
+template <int S, int N, bool AR>
+__global__ __launch_bounds__(kBlock) void ilv_resume_kernel(KParams p, uint32_t lvl) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const Lds tab = stage_tables(p, smem);
+    constexpr int NW = Codes<S>::kWords, DB = IlvDepth<N>::kB;
+    constexpr const IlvPattern<N, S / N> &pat = IlvConst<N, S / N>::kPat;
+    constexpr int NL = IlvLiveConst<N, S / N>::kLive.n;
+    const uint32_t trips = p.ilv_trips;
+    const uint32_t k0 = p.lvl_k[lvl - 1];
+    const uint32_t k1 = lvl < p.nlevels ? p.lvl_k[lvl] : trips;
+    const uint32_t n = __hip_atomic_load(&p.qcount[(uint64_t)(lvl - 1) * p.nseg + blockIdx.x], __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+    const QueueView<S> qin(p, (lvl - 1) & 1);
+    __shared__ unsigned int nq;
+    if (threadIdx.x == 0) nq = 0;
+    __syncthreads();
+    unsigned long long best = ~0ull;
+    const uint32_t span = (n + kBlock - 1) / kBlock;
+    const uint64_t seg = (uint64_t)blockIdx.x * p.seg_cap;
+    for (uint32_t it = 0; it < span; ++it) {
+        const uint32_t q = it * kBlock + threadIdx.x;
+        const bool active = q < n;
+        const uint32_t i = active ? qin.idx[seg + q] : 0u;
+        uint32_t w[NW], Z[NL], cut[S + 1], tyd[N], F[S], B[S], X[N], Fq0[S], Fq1[S], Bq[DB][S];
+#pragma unroll
+        for (int k = 0; k < NW; ++k) w[k] = active ? qin.codes[(uint64_t)k * p.qcap + seg + q] : 0u;
+#pragma unroll
+        for (int s = 0; s < NL; ++s) Z[s] = active ? qin.Y[(uint64_t)s * p.qcap + seg + q] : 0u;
+        const bool ok = unpack_cuts<S>(w, p.L, cut);
+        const uint32_t a = ok ? assign_of(p, i) : 0u;
+        const bool feas = ilv_weights<S, N>(p, tab, cut, a, tyd, F, B);
+        // dead registers are written before any read, so zero is as good as any value
+        ilv_init<S, N>(X, Fq0, Fq1, Bq);
+        IlvUnpack<NL> unpack{Z};
+        ilv_each_live<S, N>(X, Fq0, Fq1, Bq, unpack);
+        bool settled = true;
+        if constexpr (pat.start >= 0) {
+            settled = ilv_advance<S, N>(p, F, B, X, Fq0, Fq1, Bq, k0, k1, trips);
+            if (lvl < p.nlevels) {
+                IlvPack<NL> pack{Z};
+                ilv_each_live<S, N>(X, Fq0, Fq1, Bq, pack);
+                enqueue<S, NL>(p, lvl & 1, &nq, active && !settled, i, w, Z);
+            }
+            ilv_section_ct<S, N, 2>(std::make_integer_sequence<int, pat.tail>{}, p, F, B, X, Fq0, Fq1, Bq);
+        }
+        const uint32_t T = ilv_end<S, N, AR>(p, tab, X, cut, tyd);
+        if (active && settled) {
+            if (p.makespan_out) p.makespan_out[i] = T;
+            const unsigned long long key = make_key(feas, T, i);
+            best = key < best ? key : best;
+        }
+    }
+    if (lvl < p.nlevels) {
+        __syncthreads();
+        if (threadIdx.x == 0) p.qcount[(uint64_t)lvl * p.nseg + blockIdx.x] = nq;
+    }
+    block_min_and_finish(best, p.acc, p.done, p.result, nullptr, lvl == p.nlevels, p.accumulate);
 }
 
 }  // namespace pk

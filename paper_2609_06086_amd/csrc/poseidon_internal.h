@@ -52,14 +52,16 @@ struct KParams {
     unsigned long long *snap;         // early stop: run_best as of the previous chunk
     unsigned long long *stats;   // evaluated, pruned, infeasible
     unsigned int *err;
-    // steady-state cascade: lanes not settled at iteration lvl_k[l-1] are
+    // steady-state cascade: lanes not settled at iteration (Interleaved
+    // 1F1B: period) lvl_k[l-1] are
     // queued (candidate index + registers) and resumed by level l
     uint32_t nlevels;                 // 0 = no cascade
     uint32_t lvl_k[kMaxLevels];
     unsigned int *qcount;             // [level][nseg]: entries block b queued for level + 1
     uint32_t *queue[2];               // ping-pong queues: level l reads queue (l-1) & 1;
                                       // each idx[qcap] | codes[words][qcap] | Y[NX][qcap]
-                                      // (NX = S for 1F1B, 2S for Eager 1F1B),
+                                      // (NX = S for 1F1B, 2S for Eager 1F1B, the live
+                                      // registers under Interleaved 1F1B),
                                       // block b owning slots [b * seg_cap, (b+1) * seg_cap)
     uint64_t qcap, seg_cap;
     uint32_t nseg;                    // blocks of the level-0 grid (= every level's grid)
@@ -110,6 +112,8 @@ hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st,
 hipError_t eval_occupancy(const KParams &p, size_t lds, int *blocks);
 hipError_t launch_ilv(const KParams &p, const LaunchCfg &lc, hipStream_t st);
 hipError_t ilv_occupancy(const KParams &p, size_t lds, int *blocks);
+hipError_t launch_ilv_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl);
+int ilv_state_words(uint32_t S, uint32_t N);   // live registers of the Interleaved 1F1B stencil per queue entry
 int ilv_max_db(int N);   // backward input depth the Interleaved 1F1B stencil holds for N devices
 // The compiled Interleaved 1F1B schedule for (S, N) as slot-table words:
 // prologue [start][4], one period [2S][4], cool-down [tail][4].  Returns

@@ -46,6 +46,50 @@ def test_interleaved_every_stage_device_pair(dev):
             check_against_oracle(prob, W.random_candidates(rng, prob, int(rng.integers(1, 900))), dev)
 
 
+def test_interleaved_cascade_long_pipelines(dev):
+    """Many steady periods for every (S, N) pair: lanes whose live registers
+    settle at the first checkpoint jump to the end of the periods, the others
+    are queued and resumed level by level (checkpoints at 3, 6, 12, 24
+    periods); single-layer stages with close compute times settle late."""
+    rng = np.random.default_rng(134)
+    for k, (S, N) in enumerate(PAIRS):
+        M = N * int(rng.integers(10, 34))
+        prob = _problem(rng, S, N, M, int(rng.integers(1, 4)), ar=k % 2 == 0, table=k % 3 == 1)
+        check_against_oracle(prob, W.random_candidates(rng, prob, int(rng.integers(200, 700))), dev)
+
+
+def test_interleaved_cascade_uniform_and_tied_stages(dev):
+    """Stages with equal compute times (ties between critical cycles) and no
+    transfers: the steady state settles at once or never within the run;
+    both must give the oracle's values, and the uniform closed form
+    T = (VM + N - 1)(f + b) when every stage has one layer."""
+    rng = np.random.default_rng(135)
+    for S, N in ((8, 4), (12, 6), (16, 8), (16, 4)):
+        M = 24 * N
+        prob = _problem(rng, S, N, M, 2)
+        prob.L = S + 4
+        prob.fwd = np.full((2, prob.L), 5, np.uint32)
+        prob.fwd[1] = 9
+        prob.bwd = 2 * prob.fwd
+        prob.mem = np.ones(prob.L, np.uint32)
+        prob.comm_fwd = rng.integers(0, 2, size=S - 1).astype(np.uint32)
+        prob.comm_bwd = prob.comm_fwd.copy()
+        prob.allreduce = None
+        check_against_oracle(prob, W.random_candidates(rng, prob, 400), dev)
+        one = W.Candidates(first=0, count=1)
+        prob.L = S
+        prob.fwd, prob.bwd = prob.fwd[:, :S].copy(), prob.bwd[:, :S].copy()
+        prob.mem = prob.mem[:S].copy()
+        prob.comm_fwd = np.zeros(S - 1, np.uint32)
+        prob.comm_bwd = np.zeros(S - 1, np.uint32)
+        prob.assign = np.zeros((1, N), np.uint8)
+        ctx = P.poseidon_load_costs(prob, 0)
+        T = torch.empty(1, dtype=torch.int32, device=dev)
+        P.poseidon_eval_candidates(ctx, first=one.first, count=one.count, makespan_out=T)
+        assert int(T.cpu()[0]) == (S // N * M + N - 1) * 15
+        ctx.close()
+
+
 def test_interleaved_python_oracle_exhaustive(dev):
     rng = np.random.default_rng(131)
     for S, N in ((4, 2), (6, 3), (6, 2)):
