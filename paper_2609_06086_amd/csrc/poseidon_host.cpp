@@ -24,7 +24,7 @@
 #define PK_EAGER_K0 (2 * S)   // the same for Eager 1F1B, whose steady state settles later
 #endif
 #ifndef PK_ILV_K0
-#define PK_ILV_K0 3   // the same for Interleaved 1F1B, in periods of 2S slots
+#define PK_ILV_K0 2   // the same for Interleaved 1F1B, in periods of 2S slots
 #endif
 
 namespace {

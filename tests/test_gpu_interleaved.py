@@ -49,7 +49,7 @@ def test_interleaved_every_stage_device_pair(dev):
 def test_interleaved_cascade_long_pipelines(dev):
     """Many steady periods for every (S, N) pair: lanes whose live registers
     settle at the first checkpoint jump to the end of the periods, the others
-    are queued and resumed level by level (checkpoints at 3, 6, 12, 24
+    are queued and resumed level by level (checkpoints at 2, 4, 8, 16
     periods); single-layer stages with close compute times settle late."""
     rng = np.random.default_rng(134)
     for k, (S, N) in enumerate(PAIRS):
