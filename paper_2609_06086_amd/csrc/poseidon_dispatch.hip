@@ -45,26 +45,39 @@ __global__ __launch_bounds__(kBlock) void argmin_kernel(const uint32_t *T, const
     block_min_and_finish(best, acc, done, result, nullptr, true);
 }
 
-// Exclusive offsets of the block totals (one block); total to q.total.
+// Exclusive offsets of the block totals (one block); total to q.total.  The
+// totals are staged in LDS with coalesced loads (one padding word per 64
+// entries, so the per-thread runs of phase 2 start on different banks);
+// each thread then scans a contiguous run there, and the offsets go back
+// out coalesced.  A level piece has at most kSearchScanMax blocks, each
+// with at most 256 (L - 1) children, so every offset fits 32 bits.
+
+__device__ __forceinline__ uint32_t scan_pad(uint32_t b) { return b + (b >> 6); }
+
 __global__ __launch_bounds__(kBlock) void search_scan_kernel(SearchParams q, uint32_t nblk) {
-    const uint32_t per = (nblk + kBlock - 1) / kBlock;
-    const uint32_t b0 = threadIdx.x * per, b1 = min(nblk, b0 + per);
-    unsigned long long s = 0, c[5] = {0, 0, 0, 0, 0};
-    // independent loads, several in flight per thread
-#pragma unroll 8
-    for (uint32_t b = b0; b < b1; ++b) s += q.blk_tot[b];
-    // the counters need no order: coalesced strided sums
+    __shared__ uint32_t cnt[kSearchScanMax + kSearchScanMax / 64];
+    unsigned long long c[5] = {0, 0, 0, 0, 0};
+#pragma unroll 4
     for (uint32_t b = threadIdx.x; b < nblk; b += kBlock) {
+        cnt[scan_pad(b)] = q.blk_tot[b];
 #pragma unroll
         for (int k = 0; k < 5; ++k) c[k] += q.blk_cnt[(uint64_t)k * q.blk_stride + b];
     }
+    __syncthreads();
+    const uint32_t per = (nblk + kBlock - 1) / kBlock;
+    const uint32_t b0 = min(nblk, threadIdx.x * per), b1 = min(nblk, b0 + per);
+    unsigned long long s = 0;
+    for (uint32_t b = b0; b < b1; ++b) s += cnt[scan_pad(b)];
     unsigned long long total;
     unsigned long long off = block_exclusive_scan_u64(s, total);
-#pragma unroll 8
     for (uint32_t b = b0; b < b1; ++b) {
-        q.blk_off[b] = off;
-        off += q.blk_tot[b];
+        const uint32_t v = cnt[scan_pad(b)];
+        cnt[scan_pad(b)] = (uint32_t)off;
+        off += v;
     }
+    __syncthreads();
+#pragma unroll 4
+    for (uint32_t b = threadIdx.x; b < nblk; b += kBlock) q.blk_off[b] = cnt[scan_pad(b)];
     // the level's counters: one global atomic per counter
     __shared__ unsigned long long sum[5];
     if (threadIdx.x < 5) sum[threadIdx.x] = 0;

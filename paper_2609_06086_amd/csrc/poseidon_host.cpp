@@ -445,6 +445,16 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         while (c < L && pm[L] - pm[c] > p->cap_mb[t]) ++c;
         kp.last_lo[t] = c;
     }
+    // type pairs (t, u) whose every layer has fwd + bwd on t at most M times
+    // that on u: the search's last-stage Eq. 2 then falls as the last cut grows
+    for (uint32_t t = 0; t < T; ++t)
+        for (uint32_t u = 0; u < T; ++u) {
+            bool mono = true;
+            for (uint32_t l = 0; l < L && mono; ++l)
+                mono = (uint64_t)p->fwd_us[(size_t)t * L + l] + p->bwd_us[(size_t)t * L + l] <=
+                       (uint64_t)M * ((uint64_t)p->fwd_us[(size_t)u * L + l] + p->bwd_us[(size_t)u * L + l]);
+            if (mono) kp.g_mono |= 1ull << (8 * t + u);
+        }
     if (ilv) {
         // the compiled schedule (prologue, `trips` periods, cool-down) is used
         // only if it equals this problem's own slot table word for word
@@ -849,6 +859,7 @@ namespace {
 
 constexpr uint64_t kSearchCap = 1ull << 22;            // nodes per frontier piece
 constexpr uint32_t kSearchBlk = kSearchCap / 256;      // blocks per piece
+static_assert(kSearchBlk <= pk::kSearchScanMax, "a level piece must fit the scan kernel");
 
 enum { SW_STATS = 0, SW_ACC = 5, SW_BEST = 6, SW_TOTAL = 9, SW_BOUND = 10, SW_COUNT = 11 };
 

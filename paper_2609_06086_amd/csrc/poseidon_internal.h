@@ -9,6 +9,7 @@ namespace pk {
 constexpr int kSMax = 16;
 constexpr uint32_t kNB = 256;   // Pascal-table column length (n = 0..255; L <= 256)
 constexpr int kMaxLevels = 6;   // cascade checkpoints of the steady loop
+constexpr uint32_t kSearchScanMax = 16384;   // blocks of one search level piece (search_scan_kernel's LDS)
 
 enum AssignMode : uint32_t { kAssignFixed = 0, kAssignTable = 1, kAssignDigits = 2 };
 
@@ -32,6 +33,8 @@ struct KParams {
     uint32_t sched;               // POSEIDON_SCHEDULE_*
     uint32_t ndev;                // devices: S, or S / V under Interleaved 1F1B
     uint32_t last_lo[8];          // per type t: smallest c with pm[L] - pm[c] <= cap[t] (search)
+    uint64_t g_mono;              // bit 8 t + u: every layer's fwd + bwd on t is at most M times
+                                  // that on u (the search's last-stage Eq. 2 then falls with the cut)
     uint32_t ilv_compiled, ilv_trips; // Interleaved 1F1B: the schedule runs as compiled code with
                                       // this many steady periods
     uint32_t psi[kSMax];          // cf_0 + ... + cf_{s-1}: undoes the per-stage shift at the end

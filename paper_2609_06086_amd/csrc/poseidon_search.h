@@ -13,7 +13,8 @@
 // are the end points hi = c_x+1, c_x+2, ... of stage x+1 up to the first
 // one that fails a test: the memory sum and g(S_{x+1}) only grow with hi,
 // and once a type's counts are falling the ridge test fails for every
-// larger count too, so the accepted children form one contiguous range.
+// larger count too, so the accepted children form one contiguous range,
+// whose length a binary search finds.
 // search_count_kernel counts them per block; search_scan_kernel turns the
 // block counts into offsets; search_write_kernel writes the children in
 // node order (a block-local scan places each node's range), so the next
@@ -108,81 +109,166 @@ __device__ __forceinline__ int search_try(const KParams &p, const Lds &tab, cons
     return 0;
 }
 
-// The node extended by stage x+1 = [lo, hi), as seen by the test of the
-// last stage S = [hi, L) (used when x + 2 == S).
-__device__ __forceinline__ SearchNode search_extend_to_last(const KParams &p, const Lds &tab, const SearchNode &n,
-                                                            uint32_t x, uint32_t hi, uint32_t typ_next) {
-    const uint32_t row_len = p.L + 1;
-    const uint64_t *c = tab.cost + n.t * row_len;
-    const uint64_t ch = c[hi], cl = c[n.lo];
-    const uint32_t f = (uint32_t)ch - (uint32_t)cl, b = (uint32_t)(ch >> 32) - (uint32_t)(cl >> 32);
-    const uint32_t d = p.has_ar ? tab.pd[n.t * row_len + hi] - tab.pd[n.t * row_len + n.lo] : 0u;
-    SearchNode m = n;
-    m.inner = x == 0 ? d : max(n.inner + n.last_b, d);
-    m.pre_f = n.pre_f + f;
-    m.last_b = b;
-    m.lo = hi;
-    m.t = typ_next;
-    m.last_l = n.last_lS;
-    m.falling = n.fallingS;
-    if (n.t == typ_next) {
-        const int32_t l = (int32_t)(hi - n.lo);
-        if (m.last_l >= 0 && l < m.last_l) m.falling = true;
-        m.last_l = l;
-    }
-    return m;
-}
-
 // Outcomes of the last-stage test of the children of one node.
 struct LastStage {
     uint32_t pass = 0, mem = 0, ridge = 0, bound = 0;
 };
 
-// Children of a node at level x < S-1.  The accepted choices of stage x+1
-// form the range lo+1 .. lo+acc; why = the rule that stopped it (0: it ran
-// to its structural end).  When x + 2 == S a child fixes every cut, so the
-// last stage is tested here too and only children that pass it are kept
-// (lp counts the outcomes).  With WRITE the kept children are written from
-// position `base` on, in order.
+// Number k of accepted choices of stage x+1: the end points lo+1 .. lo+k
+// pass the memory, ridge and Eq. 2 tests and lo+k+1 (if <= hmax) fails one.
+// Each test, once failed, fails for every larger end point (the memory sum
+// and g(S_{x+1}) only grow with it; a falling type's ridge test fails for
+// every count above its last one), so k is found by a binary search over
+// the end points instead of trying them one by one.
+__device__ __forceinline__ uint32_t search_accepted(const KParams &p, const Lds &tab, const SearchNode &n,
+                                                    uint32_t x, uint32_t hmax, uint32_t flags, uint32_t bound) {
+    const uint32_t row_len = p.L + 1;
+    uint32_t len = hmax - n.lo;
+    if ((flags & kSearchRidge) && n.last_l >= 0 && n.falling) len = min(len, (uint32_t)n.last_l);
+    const uint64_t *ct = tab.cost + n.t * row_len;
+    const uint64_t cl = ct[n.lo];
+    const uint32_t pml = tab.pm[n.lo], capt = tab.cap[n.t];
+    const uint32_t *pdt = tab.pd + n.t * row_len;
+    const uint32_t dl = p.has_ar ? pdt[n.lo] : 0u;
+    const bool stage = !(flags & kSearchNoStage);
+    const uint32_t carry = n.inner + n.last_b;
+    uint32_t k = 0;
+    for (int b = (int)decode_levels(p.L) - 1; b >= 0; --b) {
+        const uint32_t t = k + (1u << b);
+        const uint32_t h = n.lo + min(t, len);
+        bool ok = tab.pm[h] - pml <= capt;
+        if (stage) {
+            const uint64_t ch = ct[h];
+            const uint32_t f = (uint32_t)ch - (uint32_t)cl, bw = (uint32_t)(ch >> 32) - (uint32_t)(cl >> 32);
+            const uint32_t d = p.has_ar ? pdt[h] - dl : 0u;
+            const uint32_t inn = x == 0 ? d : max(carry, d);
+            ok = ok && n.pre_f + p.M * (f + bw) + inn <= bound;
+        }
+        k = (t <= len && ok) ? t : k;
+    }
+    return k;
+}
+
+// Children lo+1 .. lo+k of a node at the level that fixes the last cut
+// (x + 2 == S): each fixes every cut, so the last stage [hi, L) is tested
+// here (memory in closed form through last_lo, then ridge, then Eq. 2) and
+// only children that pass it are kept; lp counts the outcomes.  With WRITE
+// the kept children go to positions base, base + 1, ... in order.
+//
+// Without all-reduce times the last stage's Eq. 2 splits into a per-node
+// constant and a function of hi alone:
+//   g(S_S) = C + G(hi),  G(hi) = Pf_t[hi] + Pb_t[hi] - M (Pf_tS[hi] + Pb_tS[hi])
+// (t, tS the types of stages S-1 and S, Pf / Pb the prefix times).  G falls
+// as hi grows when every layer costs at least M times more on tS than on t
+// (checked per type pair on the host: bit 8 t + tS of p.g_mono), and the
+// last stage's ridge test fails on a prefix of the end points too, so then
+// every outcome count is a range length: the ridge prefix in closed form,
+// the bound prefix by a binary search.  Otherwise the end points are tried
+// one by one.
+template <int S>
+__device__ __forceinline__ void search_write_child(const SearchParams &q, uint64_t o, uint32_t row, uint32_t x,
+                                                   uint32_t hi, const uint32_t (&w)[Codes<S>::kWords]) {
+    q.out_row[o] = row;
+#pragma unroll
+    for (int k = 0; k < Codes<S>::kWords; ++k) {
+        const uint32_t v = (uint32_t)k == (x >> 2) ? (w[k] | (hi << (8 * (x & 3)))) : w[k];
+        q.out_codes[(uint64_t)k * q.out_cap + o] = v;
+    }
+}
+
 template <int S, bool WRITE>
-__device__ __forceinline__ uint32_t search_children(const KParams &p, const Lds &tab, const SearchNode &n,
-                                                    uint32_t x, uint32_t flags, uint32_t bound, int &why,
-                                                    uint32_t &acc, LastStage &lp, const SearchParams &q,
-                                                    uint64_t base, const uint32_t (&w)[Codes<S>::kWords]) {
-    constexpr int NW = Codes<S>::kWords;
-    const uint32_t hmax = p.L - (S - 1 - x);   // every later stage keeps one layer
-    const bool last_cut = x + 2 == (uint32_t)S;
+__device__ __forceinline__ uint32_t search_last_children(const KParams &p, const Lds &tab, const SearchNode &n,
+                                                         uint32_t x, uint32_t k, uint32_t flags, uint32_t bound,
+                                                         LastStage &lp, const SearchParams &q, uint64_t base,
+                                                         const uint32_t (&w)[Codes<S>::kWords]) {
+    const uint32_t row_len = p.L + 1;
     // the last stage [hi, L) exceeds its cap exactly for hi < last_lo[type]
     const uint32_t mem_lo = p.last_lo[n.tS];
+    const uint32_t h0 = max(n.lo + 1, mem_lo), h1 = n.lo + k;
+    lp.mem += (h0 <= h1 ? h0 : h1 + 1) - (n.lo + 1);
+    const bool ridge = (flags & kSearchRidge) != 0, stage = !(flags & kSearchNoStage);
+    const bool same = n.t == n.tS;
+    if (!p.has_ar && ((p.g_mono >> (8 * n.t + n.tS)) & 1ull)) {
+        if (h0 > h1) return 0;
+        // ridge: the end points below r0 fail
+        uint32_t r0 = h0;
+        if (ridge) {
+            if (same) {
+                // counts of type t fall before lo + last_lS (or throughout), and the
+                // last stage is then longer than stage S-1 below ceil((L + lo) / 2)
+                const uint32_t e1 = (p.L + n.lo + 1) / 2;
+                const uint32_t e2 = n.fallingS ? 0xFFFFFFFFu : (n.last_lS >= 0 ? n.lo + (uint32_t)n.last_lS : 0u);
+                r0 = max(h0, min(e1, e2));
+            } else if (n.last_lS >= 0 && n.fallingS) {
+                r0 = max(h0, p.L - (uint32_t)n.last_lS);
+            }
+            r0 = min(r0, h1 + 1);
+            lp.ridge += r0 - h0;
+        }
+        // Eq. 2: the end points below g0 fail
+        uint32_t g0 = r0;
+        if (stage && r0 <= h1) {
+            const uint64_t *ct = tab.cost + n.t * row_len, *cs = tab.cost + n.tS * row_len;
+            const uint64_t cl = ct[n.lo], cL = cs[p.L];
+            const int64_t M = p.M;
+            const int64_t C = (int64_t)n.pre_f - (int64_t)(uint32_t)cl - (int64_t)(cl >> 32) +
+                              (x == 0 ? 0 : (int64_t)(n.inner + n.last_b)) +
+                              M * ((int64_t)(uint32_t)cL + (int64_t)(cL >> 32));
+            const uint32_t len = h1 + 1 - r0;
+            uint32_t j = 0;
+            for (int b = (int)decode_levels(p.L) - 1; b >= 0; --b) {
+                const uint32_t t = j + (1u << b);
+                const uint32_t h = r0 + min(t, len) - 1;
+                const uint64_t ch = ct[h], sh = cs[h];
+                const int64_t G = (int64_t)(uint32_t)ch + (int64_t)(ch >> 32) -
+                                  M * ((int64_t)(uint32_t)sh + (int64_t)(sh >> 32));
+                j = (t <= len && C + G > (int64_t)bound) ? t : j;
+            }
+            g0 = r0 + j;
+            lp.bound += j;
+        }
+        lp.pass += h1 + 1 - g0;
+        if (WRITE) {
+            for (uint32_t hi = g0; hi <= h1; ++hi) search_write_child<S>(q, base + (hi - g0), n.row, x, hi, w);
+        }
+        return h1 + 1 - g0;
+    }
+    const uint64_t *ct = tab.cost + n.t * row_len, *cs = tab.cost + n.tS * row_len;
+    const uint64_t cl = ct[n.lo], cL = cs[p.L];
+    const uint32_t *pdt = tab.pd + n.t * row_len, *pds = tab.pd + n.tS * row_len;
+    const uint32_t dl = p.has_ar ? pdt[n.lo] : 0u, dL = p.has_ar ? pds[p.L] : 0u;
+    const uint32_t carry = n.inner + n.last_b;
     uint32_t out = 0;
-    acc = 0;
-    why = 0;
-    for (uint32_t hi = n.lo + 1; hi <= hmax; ++hi) {
-        why = search_try(p, tab, n, x, hi, flags, bound);
-        if (why) break;
-        ++acc;
-        if (last_cut) {
-            if (hi < mem_lo) {
-                lp.mem += 1;
+    for (uint32_t hi = h0; hi <= h1; ++hi) {
+        if (ridge) {
+            // type tS's counts with stage x+1 appended when it has that type
+            const int32_t l = (int32_t)(hi - n.lo);
+            int32_t ll = n.last_lS;
+            bool fall = n.fallingS;
+            if (same) {
+                fall = fall || (ll >= 0 && l < ll);
+                ll = l;
+            }
+            if (ll >= 0 && fall && (int32_t)(p.L - hi) > ll) {
+                lp.ridge += 1;
                 continue;
             }
-            const SearchNode m = search_extend_to_last(p, tab, n, x, hi, n.tS);
-            const int w2 = search_try(p, tab, m, x + 1, p.L, flags, bound);
-            lp.pass += w2 == 0;
-            lp.mem += w2 == 1;
-            lp.ridge += w2 == 2;
-            lp.bound += w2 == 3;
-            if (w2) continue;
         }
-        if (WRITE) {
-            const uint64_t o = base + out;
-            q.out_row[o] = n.row;
-#pragma unroll
-            for (int k = 0; k < NW; ++k) {
-                const uint32_t v = (uint32_t)k == (x >> 2) ? (w[k] | (hi << (8 * (x & 3)))) : w[k];
-                q.out_codes[(uint64_t)k * q.out_cap + o] = v;
+        if (stage) {
+            const uint64_t ch = ct[hi], sh = cs[hi];
+            const uint32_t f = (uint32_t)ch - (uint32_t)cl, b = (uint32_t)(ch >> 32) - (uint32_t)(cl >> 32);
+            const uint32_t d = p.has_ar ? pdt[hi] - dl : 0u;
+            const uint32_t inn = x == 0 ? d : max(carry, d);
+            const uint32_t fS = (uint32_t)cL - (uint32_t)sh, bS = (uint32_t)(cL >> 32) - (uint32_t)(sh >> 32);
+            const uint32_t dS = p.has_ar ? dL - pds[hi] : 0u;
+            // Eq. 2 for the last stage: g(S_S) = sum_{i<S} F_i + M (F_S + B_S) + max(inner + B_{S-1}, d_S)
+            if (n.pre_f + f + p.M * (fS + bS) + max(inn + b, dS) > bound) {
+                lp.bound += 1;
+                continue;
             }
         }
+        lp.pass += 1;
+        if (WRITE) search_write_child<S>(q, base + out, n.row, x, hi, w);
         ++out;
     }
     return out;
@@ -238,8 +324,14 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
     LastStage lp;
     int why = 0;
     if (active) {
-        const SearchNode n = search_node<S>(p, tab, row, w, q.level, ty, cut);
-        cnt = search_children<S, false>(p, tab, n, q.level, q.flags, bound, why, acc, lp, q, 0, w);
+        const uint32_t x = q.level;
+        const SearchNode n = search_node<S>(p, tab, row, w, x, ty, cut);
+        const uint32_t hmax = p.L - (S - 1 - x);   // every later stage keeps one layer
+        acc = search_accepted(p, tab, n, x, hmax, q.flags, bound);
+        // the rule that stopped the range (0: it ran to its structural end)
+        why = n.lo + acc < hmax ? search_try(p, tab, n, x, n.lo + acc + 1, q.flags, bound) : 0;
+        cnt = x + 2 == (uint32_t)S ? search_last_children<S, false>(p, tab, n, x, acc, q.flags, bound, lp, q, 0, w)
+                                   : acc;
         q.node_cnt[i] = (uint8_t)cnt;   // at most L - 1 < 256 children
     }
     __shared__ unsigned int tot;
@@ -271,13 +363,24 @@ __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchP
     unsigned long long total;
     const unsigned long long local = block_exclusive_scan_u64(cnt, total);
     if (cnt) {
-        uint32_t row, w[Codes<S>::kWords], ty[S], cut[S + 1], acc = 0;
-        LastStage lp;
-        int why = 0;
+        constexpr int NW = Codes<S>::kWords;
+        uint32_t row, w[NW], ty[S], cut[S + 1];
+        const uint32_t x = q.level;
         search_load<S>(q, i, true, row, w);
-        const SearchNode n = search_node<S>(p, tab, row, w, q.level, ty, cut);
-        search_children<S, true>(p, tab, n, q.level, q.flags, bound, why, acc, lp, q,
-                                 q.blk_off[blk] - q.blk_off[q.blk_base] + local, w);
+        const uint64_t base = q.blk_off[blk] - q.blk_off[q.blk_base] + local;
+        if (x + 2 == (uint32_t)S) {
+            LastStage lp;
+            const SearchNode n = search_node<S>(p, tab, row, w, x, ty, cut);
+            const uint32_t acc = search_accepted(p, tab, n, x, p.L - (S - 1 - x), q.flags, bound);
+            search_last_children<S, true>(p, tab, n, x, acc, q.flags, bound, lp, q, base, w);
+        } else {
+            // every accepted choice is a child: c_{x+1} = lo+1 .. lo+cnt
+            uint32_t lo = 0;
+#pragma unroll
+            for (int s = 1; s < S; ++s)
+                if ((uint32_t)s == x) lo = (w[(s - 1) >> 2] >> (8 * ((s - 1) & 3))) & 0xFFu;
+            for (uint32_t c = 0; c < cnt; ++c) search_write_child<S>(q, base + c, row, x, lo + 1 + c, w);
+        }
     }
 }
 

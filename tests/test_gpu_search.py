@@ -60,6 +60,28 @@ def test_search_random_problems(dev):
             check(prob, bound, dev, **kw)
 
 
+def test_search_monotone_last_stage(dev):
+    """Per-layer costs within 30 % of each other across types and M >= 2: every
+    type pair satisfies the condition under which the last stage's outcomes
+    are counted as ranges (ridge prefix in closed form, Eq. 2 prefix by
+    binary search), with ridge on and off, stage pruning on and off, tight
+    and loose bounds, 2..8 stages, and M = 1 where only same-type pairs do."""
+    rng = np.random.default_rng(124)
+    for trial in range(40):
+        S = trial % 7 + 2
+        L = S + int(rng.integers(1, 14))
+        M = 1 if trial % 10 == 9 else int(rng.integers(2, 3 * S + 8))
+        T = int(rng.integers(2, 4))
+        prob = W.random_problem(rng, L, S, M, T, cost_lo=300, cost_hi=390, mem_hi=30,
+                                cap=int(rng.integers(40, 250)), assign_rows=None if T ** S < 300 else 11)
+        prob.schedule = trial % 3 == 2
+        To, fo = coracle.evaluate(prob, W.random_candidates(rng, prob, 300))
+        tight = int(np.sort(To[fo])[min(3, int(fo.sum()) - 1)]) if fo.any() else 2 ** 31 - 1
+        for bound, kw in ((tight, dict()), (tight, dict(ridge=True, rows_per_chunk=2)),
+                          (2 ** 31 - 1, dict(ridge=True)), (tight, dict(stage_pruning=False, ridge=True))):
+            check(prob, bound, dev, **kw)
+
+
 def test_search_deep_pipelines(dev):
     """S = 9..16 stages with few spare layers (every level of the frontier,
     the last-cut test at level S-2, wide composition ranks)."""
