@@ -868,7 +868,7 @@ struct SearchWs {
     unsigned int *tot[pk::kSMax];
     unsigned int *cnt[pk::kSMax];
     unsigned long long *off[pk::kSMax];
-    uint8_t *node[pk::kSMax];
+    uint16_t *node[pk::kSMax];
     unsigned long long *words;
 };
 
@@ -884,7 +884,7 @@ SearchWs search_layout(poseidon_ctx *ctx, size_t *bytes) {
         w.codes[l] = (uint32_t *)(b + o); o += words * kSearchCap * 4;
         w.tot[l] = (unsigned int *)(b + o); o += (size_t)kSearchBlk * 4;
         w.cnt[l] = (unsigned int *)(b + o); o += (size_t)kSearchBlk * 4 * 5;
-        w.node[l] = (uint8_t *)(b + o); o += kSearchCap;
+        w.node[l] = (uint16_t *)(b + o); o += kSearchCap * 2;
         w.off[l] = (unsigned long long *)(b + o); o += ((size_t)kSearchBlk + 1) * 8;
     }
     w.words = (unsigned long long *)(b + o); o += SW_COUNT * 8;
@@ -906,6 +906,14 @@ int search_read_total(SearchRun &r, unsigned long long *total) {
         hipStreamSynchronize(r.st) != hipSuccess)
         return POSEIDON_E_DEVICE;
     return POSEIDON_OK;
+}
+
+// The level before the one that fixes the last cut (x = S - 3) is expanded
+// together with it when one block's grandchildren, at most 256 (L - 1)^2,
+// always fit a frontier piece.
+bool search_fused(const poseidon_ctx *ctx, uint32_t x) {
+    const uint64_t L = ctx->L;
+    return ctx->S >= 3 && x + 3 == ctx->S && 256 * (L - 1) * (L - 1) <= kSearchCap;
 }
 
 // Expand the n nodes at level x (stored in the level's arrays) depth first.
@@ -930,8 +938,11 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n) {
     q.blk_cnt = r.w.cnt[x];
     q.blk_stride = kSearchBlk;
     q.node_cnt = r.w.node[x];
-    q.out_row = r.w.row[x + 1];
-    q.out_codes = r.w.codes[x + 1];
+    // a fused step writes level x + 2 (complete configurations when x = S - 3)
+    const uint32_t step = search_fused(r.ctx, x) ? 2 : 1;
+    q.fused = step == 2;
+    q.out_row = r.w.row[x + step];
+    q.out_codes = r.w.codes[x + step];
     q.out_cap = kSearchCap;
     if (pk::launch_search(pk::kSearchOpCount, r.kp, q, grid, lds, r.st) != hipSuccess ||
         pk::launch_search_scan(q, grid, r.st) != hipSuccess)
@@ -943,10 +954,11 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n) {
     if (total <= kSearchCap) {
         q.blk_base = 0;
         if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, grid, lds, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
-        return search_expand(r, x + 1, total);
+        return search_expand(r, x + step, total);
     }
     // more children than a level holds: write and expand them in pieces of
-    // whole blocks (one block has at most 256 * L < kSearchCap children)
+    // whole blocks (one block has at most 256 (L - 1) < kSearchCap children,
+    // or 256 (L - 1)^2 <= kSearchCap when fused)
     std::vector<unsigned long long> off(grid + 1);
     if (hipMemcpyAsync(off.data(), q.blk_off, (grid + 1) * 8, hipMemcpyDeviceToHost, r.st) != hipSuccess ||
         hipStreamSynchronize(r.st) != hipSuccess)
@@ -958,7 +970,7 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n) {
         q.blk_base = b0;
         if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, b1 - b0, lds, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
         if (off[b1] > off[b0]) {
-            rc = search_expand(r, x + 1, off[b1] - off[b0]);
+            rc = search_expand(r, x + step, off[b1] - off[b0]);
             if (rc != POSEIDON_OK) return rc;
         }
         b0 = b1;

@@ -88,10 +88,11 @@ struct SearchParams {
     unsigned int *blk_tot;            // children per block (count kernel)
     unsigned long long *blk_off;      // exclusive offsets, [nblk] = total (scan kernel)
     unsigned int *blk_cnt;            // [5][blk_stride] per-block counters (count kernel)
-    uint8_t *node_cnt;                // children each node keeps (count kernel -> write kernel)
+    uint16_t *node_cnt;               // children each node keeps (count kernel -> write kernel)
     uint64_t blk_stride;
     uint32_t blk_base;                // first block a write launch covers
     uint32_t flags;                   // kSearchRidge | kSearchNoStage
+    uint32_t fused;                   // level S-3 expanded together with the level that fixes the last cut
     uint32_t *bound;                  // the current chunk's bound
     unsigned long long *stats;        // visited, evaluated, pruned by memory / ridge / bound
     unsigned long long *acc;          // best (T << 32 | position) of a leaf piece

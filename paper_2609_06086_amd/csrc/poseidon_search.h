@@ -21,8 +21,11 @@
 // frontier is again in search order (row, then composition rank).  The
 // level that fixes the last cut (x = S-2) also tests the last stage, which
 // that cut determines, and keeps only the children that pass, so the widest
-// level is never written in full.  search_leaf_kernel runs the full DP on
-// the complete configurations.
+// level is never written in full.  When the children of one block always fit
+// a frontier piece, the level before it (x = S-3) is fused with it: the count
+// and write kernels expand each accepted child there at once (its prefix
+// quantities extended by one stage), so the widest level is not written at
+// all.  search_leaf_kernel runs the full DP on the complete configurations.
 #include "poseidon_kernels.h"
 
 namespace pk {
@@ -37,6 +40,9 @@ struct SearchNode {
     uint32_t tS;                  // type of stage S, with its ridge state over stages 1..x
     int32_t last_lS;
     bool fallingS;
+    uint32_t tN;                  // type of stage x+2, with its ridge state over stages 1..x
+    int32_t last_lN;              // (what a child's own stage test needs)
+    bool fallingN;
 };
 
 // Prefix quantities of a node at level x (stages 1..x fixed).
@@ -65,6 +71,13 @@ __device__ __forceinline__ SearchNode search_node(const KParams &p, const Lds &t
     n.tS = ty[S - 1];
     n.last_lS = -1;
     n.fallingS = false;
+    n.tN = ty[0];
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        if ((uint32_t)s == x + 1) n.tN = ty[s];
+    }
+    n.last_lN = -1;
+    n.fallingN = false;
     const uint32_t row_len = p.L + 1;
 #pragma unroll
     for (int s = 0; s < S; ++s) {
@@ -85,9 +98,44 @@ __device__ __forceinline__ SearchNode search_node(const KParams &p, const Lds &t
                 if (n.last_lS >= 0 && l < n.last_lS) n.fallingS = true;
                 n.last_lS = l;
             }
+            if (ty[s] == n.tN) {
+                if (n.last_lN >= 0 && l < n.last_lN) n.fallingN = true;
+                n.last_lN = l;
+            }
         }
     }
     return n;
+}
+
+// The child of a node at level x with stage x+1 = [lo, c): its prefix
+// quantities at level x+1, extended by that one stage (the type of its
+// stage x+3 is not tracked: used for the level that fixes the last cut,
+// whose children are complete).
+__device__ __forceinline__ SearchNode search_child(const KParams &p, const Lds &tab, const SearchNode &n, uint32_t x,
+                                                   uint32_t c) {
+    const uint32_t row_len = p.L + 1;
+    const uint64_t *ct = tab.cost + n.t * row_len;
+    const uint64_t ch = ct[c], cl = ct[n.lo];
+    const uint32_t f = (uint32_t)ch - (uint32_t)cl, b = (uint32_t)(ch >> 32) - (uint32_t)(cl >> 32);
+    const uint32_t d = p.has_ar ? tab.pd[n.t * row_len + c] - tab.pd[n.t * row_len + n.lo] : 0u;
+    const int32_t l = (int32_t)(c - n.lo);
+    SearchNode m = n;
+    m.lo = c;
+    m.t = n.tN;
+    m.inner = x == 0 ? d : max(n.inner + n.last_b, d);
+    m.pre_f = n.pre_f + f;
+    m.last_b = b;
+    m.last_l = n.last_lN;
+    m.falling = n.fallingN;
+    if (n.t == n.tN) {
+        m.falling = m.falling || (m.last_l >= 0 && l < m.last_l);
+        m.last_l = l;
+    }
+    if (n.t == n.tS) {
+        m.fallingS = m.fallingS || (m.last_lS >= 0 && l < m.last_lS);
+        m.last_lS = l;
+    }
+    return m;
 }
 
 // Outcome of trying stage x+1 = [lo, hi): 0 accepted, 1 memory, 2 ridge, 3 bound.
@@ -320,19 +368,39 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
     const uint32_t bound = *q.bound;
     uint32_t row, w[Codes<S>::kWords], ty[S], cut[S + 1];
     search_load<S>(q, i, active, row, w);
-    uint32_t cnt = 0, acc = 0;
+    uint32_t cnt = 0, visited = 0;
     LastStage lp;
-    int why = 0;
+    uint32_t why_mem = 0, why_ridge = 0, why_bound = 0;
     if (active) {
         const uint32_t x = q.level;
         const SearchNode n = search_node<S>(p, tab, row, w, x, ty, cut);
         const uint32_t hmax = p.L - (S - 1 - x);   // every later stage keeps one layer
-        acc = search_accepted(p, tab, n, x, hmax, q.flags, bound);
+        const uint32_t acc = search_accepted(p, tab, n, x, hmax, q.flags, bound);
         // the rule that stopped the range (0: it ran to its structural end)
-        why = n.lo + acc < hmax ? search_try(p, tab, n, x, n.lo + acc + 1, q.flags, bound) : 0;
-        cnt = x + 2 == (uint32_t)S ? search_last_children<S, false>(p, tab, n, x, acc, q.flags, bound, lp, q, 0, w)
-                                   : acc;
-        q.node_cnt[i] = (uint8_t)cnt;   // at most L - 1 < 256 children
+        const int why = n.lo + acc < hmax ? search_try(p, tab, n, x, n.lo + acc + 1, q.flags, bound) : 0;
+        visited = acc;
+        why_mem = why == 1;
+        why_ridge = why == 2;
+        why_bound = why == 3;
+        if (q.fused) {
+            // x + 3 == S: each child fixes stage S-2 and is expanded here at
+            // once; its children fix the last cut, and those that pass the last
+            // stage are kept (complete configurations)
+            for (uint32_t c = n.lo + 1; c <= n.lo + acc; ++c) {
+                const SearchNode m = search_child(p, tab, n, x, c);
+                const uint32_t acc2 = search_accepted(p, tab, m, x + 1, p.L - 1, q.flags, bound);
+                const int why2 = m.lo + acc2 < p.L - 1 ? search_try(p, tab, m, x + 1, m.lo + acc2 + 1, q.flags, bound) : 0;
+                visited += acc2;
+                why_mem += why2 == 1;
+                why_ridge += why2 == 2;
+                why_bound += why2 == 3;
+                cnt += search_last_children<S, false>(p, tab, m, x + 1, acc2, q.flags, bound, lp, q, 0, w);
+            }
+        } else {
+            cnt = x + 2 == (uint32_t)S ? search_last_children<S, false>(p, tab, n, x, acc, q.flags, bound, lp, q, 0, w)
+                                       : acc;
+        }
+        q.node_cnt[i] = (uint16_t)cnt;   // at most (L - 1)^2 < 2^16 children (fused), else L - 1
     }
     __shared__ unsigned int tot;
     if (threadIdx.x == 0) tot = 0;
@@ -343,7 +411,7 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
     // counts as visited twice (its stage x+1 and its stage S) and evaluated.
     // The block's counts go to per-block slots that the scan kernel sums
     // (one global atomic per counter and launch instead of per block).
-    search_block_counts(q, acc + lp.pass, lp.pass, (why == 1) + lp.mem, (why == 2) + lp.ridge, (why == 3) + lp.bound);
+    search_block_counts(q, visited + lp.pass, lp.pass, why_mem + lp.mem, why_ridge + lp.ridge, why_bound + lp.bound);
     if (threadIdx.x == 0) q.blk_tot[blockIdx.x] = tot;
 }
 
@@ -368,7 +436,21 @@ __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchP
         const uint32_t x = q.level;
         search_load<S>(q, i, true, row, w);
         const uint64_t base = q.blk_off[blk] - q.blk_off[q.blk_base] + local;
-        if (x + 2 == (uint32_t)S) {
+        if (q.fused) {
+            // the complete configurations under each child, child by child
+            LastStage lp;
+            const SearchNode n = search_node<S>(p, tab, row, w, x, ty, cut);
+            const uint32_t acc = search_accepted(p, tab, n, x, p.L - (S - 1 - x), q.flags, bound);
+            uint64_t o = base;
+            for (uint32_t c = n.lo + 1; c <= n.lo + acc; ++c) {
+                const SearchNode m = search_child(p, tab, n, x, c);
+                const uint32_t acc2 = search_accepted(p, tab, m, x + 1, p.L - 1, q.flags, bound);
+                uint32_t wc[NW];
+#pragma unroll
+                for (int k = 0; k < NW; ++k) wc[k] = (uint32_t)k == (x >> 2) ? (w[k] | (c << (8 * (x & 3)))) : w[k];
+                o += search_last_children<S, true>(p, tab, m, x + 1, acc2, q.flags, bound, lp, q, o, wc);
+            }
+        } else if (x + 2 == (uint32_t)S) {
             LastStage lp;
             const SearchNode n = search_node<S>(p, tab, row, w, x, ty, cut);
             const uint32_t acc = search_accepted(p, tab, n, x, p.L - (S - 1 - x), q.flags, bound);

@@ -82,6 +82,21 @@ def test_search_monotone_last_stage(dev):
             check(prob, bound, dev, **kw)
 
 
+def test_search_long_models_unfused(dev):
+    """L > 129 layers: one block's grandchildren could exceed a frontier piece,
+    so the level before the last cut is expanded on its own (the fused
+    expansion covers L <= 129 everywhere else)."""
+    rng = np.random.default_rng(125)
+    for S, rows in ((3, 4), (4, 3), (5, 2)):
+        L = 140 + int(rng.integers(0, 20))
+        prob = W.random_problem(rng, L, S, 2 * S + 3, 2, cost_lo=200, cost_hi=300, mem_hi=30,
+                                cap=int(rng.integers(900, 1600)), assign_rows=rows)
+        To, fo = coracle.evaluate(prob, W.random_candidates(rng, prob, 400))
+        bound = int(np.sort(To[fo])[2]) if fo.sum() > 2 else 2 ** 31 - 1
+        for kw in (dict(), dict(ridge=True, rows_per_chunk=1)):
+            check(prob, bound, dev, **kw)
+
+
 def test_search_deep_pipelines(dev):
     """S = 9..16 stages with few spare layers (every level of the frontier,
     the last-cut test at level S-2, wide composition ranks)."""
