@@ -18,9 +18,9 @@ namespace pk {
     extern template hipError_t launch_resume_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t,   \
                                                              uint32_t);                                       \
     extern template hipError_t launch_bounded_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t,  \
-                                                              uint64_t, uint64_t, uint32_t, uint32_t);        \
+                                                              uint32_t);                                      \
     extern template hipError_t launch_bounded_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t,  \
-                                                              uint64_t, uint64_t, uint32_t, uint32_t);        \
+                                                              uint32_t);                                      \
     extern template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool, bool);                                 \
     extern template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool, bool);                                 \
     extern template hipError_t launch_search_s<S, uint32_t>(int, const KParams &, const SearchParams &, uint32_t,   \
@@ -144,9 +144,8 @@ hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, 
     PK_DISPATCH(launch_resume_s, p.S, p.wide, p, lc, st, lvl)
 }
 
-hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
-                          uint32_t bound, uint32_t publish) {
-    PK_DISPATCH(launch_bounded_s, p.S, p.wide, p, lc, st, lo, hi, bound, publish)
+hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t publish) {
+    PK_DISPATCH(launch_bounded_s, p.S, p.wide, p, lc, st, publish)
 }
 
 hipError_t eval_occupancy(const KParams &p, size_t lds, int *blocks) {

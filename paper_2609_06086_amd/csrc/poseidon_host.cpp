@@ -647,8 +647,11 @@ int read_best(poseidon_ctx *ctx, hipStream_t st, unsigned long long word_index, 
 // are processed in chunks of this size.
 constexpr uint64_t kChunk = 1ull << 26;
 
-// Workspace for chunks of up to `n` candidates: the cut codes [words][n]
-// and, with a cascade, two straggler queues of qcap x (1 + words + S) uint32
+// Workspace for chunks of up to `n` candidates: the cut codes [words][cap],
+// the early-stop survivor indices [cap] and per-block survivor counts
+// [grid_max] (cap = n plus one decode batch per block of slack, so the
+// per-block survivor segments fit) and, with a cascade, two straggler
+// queues of qcap x (1 + words + S) uint32
 // (qcap = n plus one block of slack per segment) and the per-block queue
 // counts [levels][grid_max].  Grown on demand; the old buffer is released
 // only after the stream has drained.
@@ -670,9 +673,9 @@ int ensure_workspace(poseidon_ctx *ctx, uint64_t n, hipStream_t st) {
         ctx->ws = nullptr;
         ctx->ws_cap = 0;
     }
-    const uint64_t cap = std::max<uint64_t>(n, 1024);
+    const uint64_t cap = std::max<uint64_t>(n, 1024) + (uint64_t)ctx->grid_max * pk::kDecodeIlp * 256;
     const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
-    uint64_t elems = words * cap;
+    uint64_t elems = (words + 1) * cap + ctx->grid_max;   // cut codes, survivor indices and counts
     if (ctx->base.nlevels)
         elems += 2 * (1 + words + queue_state_words(ctx)) * queue_cap(ctx, cap) +
                  (uint64_t)pk::kMaxLevels * ctx->grid_max;
@@ -727,7 +730,7 @@ int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands, uin
     kp.ccap = ctx->ws_cap;
     if (kp.nlevels) {
         kp.qcap = queue_cap(ctx, ctx->ws_cap);
-        kp.queue[0] = ws + words * ctx->ws_cap;
+        kp.queue[0] = ws + (words + 1) * ctx->ws_cap + ctx->grid_max;
         kp.queue[1] = kp.queue[0] + (1 + words + queue_state_words(ctx)) * kp.qcap;
         kp.qcount = kp.queue[1] + (1 + words + queue_state_words(ctx)) * kp.qcap;
     }
@@ -788,6 +791,9 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
     if (rc != POSEIDON_OK) return rc;
     kp.codes = (uint32_t *)ctx->ws;
     kp.ccap = ctx->ws_cap;
+    kp.sidx = (uint32_t *)ctx->ws + (uint64_t)pk::code_words((int)ctx->S) * ctx->ws_cap;
+    kp.scount = (unsigned int *)(kp.sidx + ctx->ws_cap);
+    kp.es_bound = bound;
     pk::LaunchCfg lc;
     lc.lds_bytes = ctx->lds_bytes;
     for (uint64_t lo = 0; lo < n; lo += chunk) {
@@ -797,9 +803,11 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
             kp.first_i = s0;
             kp.n_i = s1 - s0;
             pk::LaunchCfg ld = lc;
-            ld.grid = (uint32_t)std::min<uint64_t>((kp.n_i + 4 * 256 - 1) / (4 * 256), ctx->grid_max);
-            if (pk::launch_decode(kp, ld, st) != hipSuccess) return rearm(ctx, st);
-            if (pk::launch_bounded(kp, lc, st, s0, s1, bound, s1 == hi) != hipSuccess) return rearm(ctx, st);
+            const uint64_t batch = (uint64_t)pk::kDecodeIlp * 256;
+            ld.grid = (uint32_t)std::min<uint64_t>((kp.n_i + batch - 1) / batch, ctx->grid_max);
+            // block b filters kDecodeIlp candidates per lane per pass, ceil(n / (grid * batch)) passes
+            kp.seg_cap = (kp.n_i + ld.grid * batch - 1) / (ld.grid * batch) * batch;
+            if (pk::launch_bounded(kp, ld, st, s1 == hi) != hipSuccess) return rearm(ctx, st);
         }
     }
     unsigned long long w[W_COUNT];

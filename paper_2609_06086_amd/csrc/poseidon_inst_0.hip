@@ -11,10 +11,10 @@ namespace pk {
     template hipError_t launch_decode_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t);         \
     template hipError_t launch_resume_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t, uint32_t); \
     template hipError_t launch_resume_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t, uint32_t); \
-    template hipError_t launch_bounded_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t, uint64_t, \
-                                                       uint64_t, uint32_t, uint32_t);                          \
-    template hipError_t launch_bounded_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t, uint64_t, \
-                                                       uint64_t, uint32_t, uint32_t);                          \
+    template hipError_t launch_bounded_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t,          \
+                                                       uint32_t);                                              \
+    template hipError_t launch_bounded_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t,          \
+                                                       uint32_t);                                              \
     template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool, bool);                                        \
     template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool, bool);                                        \
     template hipError_t launch_search_s<S, uint32_t>(int, const KParams &, const SearchParams &, uint32_t, size_t,  \

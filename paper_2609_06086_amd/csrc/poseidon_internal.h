@@ -55,6 +55,12 @@ struct KParams {
     unsigned long long *snap;         // early stop: run_best as of the previous chunk
     unsigned long long *stats;   // evaluated, pruned, infeasible
     unsigned int *err;
+    // early stop: the caller's bound, and the list of the candidates that
+    // pass the memory and Eq. 2 tests (call index, cut codes in `codes`), in
+    // per-block segments of seg_cap entries with their counts in scount
+    uint32_t es_bound;
+    uint32_t *sidx;
+    unsigned int *scount;
     // steady-state cascade: lanes not settled at iteration (Interleaved
     // 1F1B: period) lvl_k[l-1] are
     // queued (candidate index + registers) and resumed by level l
@@ -111,8 +117,8 @@ struct LaunchCfg {
 hipError_t launch_eval(const KParams &p, const LaunchCfg &lc, hipStream_t st);
 hipError_t launch_decode(const KParams &p, const LaunchCfg &lc, hipStream_t st);
 hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl);
-hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
-                          uint32_t bound, uint32_t publish);
+hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t publish);
+constexpr int kDecodeIlp = 4;   // candidates per lane of the decode and early-stop filter kernels
 hipError_t eval_occupancy(const KParams &p, size_t lds, int *blocks);
 hipError_t launch_ilv(const KParams &p, const LaunchCfg &lc, hipStream_t st);
 hipError_t ilv_occupancy(const KParams &p, size_t lds, int *blocks);

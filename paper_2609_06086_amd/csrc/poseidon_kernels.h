@@ -23,7 +23,6 @@ namespace pk {
 
 constexpr int kBlock = 256;            // 4 waves of 64
 constexpr int kWaves = kBlock / 64;
-constexpr int kTile = 4096;            // candidates filtered per block (early stop)
 
 // ---------------------------------------------------------------------------
 // LDS image of the context's tables (one copy per block)
@@ -576,6 +575,44 @@ __device__ __forceinline__ void dp_full(const KParams &p, const uint32_t (&F)[S]
     else dp_table<S>(p, F, B, c, Y);
 }
 
+// The whole DP for the few lanes of a wave that survive the early-stop test:
+// the closed forms take the steady-state check every kSurvStep iterations,
+// and the wave leaves the steady loop as soon as all its active lanes have
+// settled (jumped to its end) or reached it.
+constexpr uint32_t kSurvStep = 8;
+
+template <int S, bool SCH>
+__device__ __forceinline__ void dp_full_settle(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                               const Comm<S> &c, uint32_t (&Y)[S]) {
+    const unsigned long long act = __ballot(true);
+    if (SCH && !p.nslots) {
+        uint32_t Fn[S], Fp[S];
+        eager_prologue<S>(Y, Fn, Fp, F, B, c);
+        const uint32_t np = p.M - 2 * S + 1;
+        bool done = false;
+        for (uint32_t k = 0; k < np;) {
+            const uint32_t k1 = min(k + kSurvStep, np);
+            if (!done) done = eager_advance<S>(Y, Fn, Fp, F, B, c, k, k1, np);
+            k = k1;
+            if (__ballot(done) == act) break;
+        }
+        eager_epilogue<S>(Y, Fn, Fp, F, B, c);
+    } else if (!SCH && p.M >= (uint32_t)S) {
+        dp_prologue<S>(Y, F, B, c);
+        const uint32_t nit = p.M - S;
+        bool done = false;
+        for (uint32_t k = 0; k < nit;) {
+            const uint32_t k1 = min(k + kSurvStep, nit);
+            if (!done) done = dp_advance<S>(Y, F, B, c, k, k1, nit);
+            k = k1;
+            if (__ballot(done) == act) break;
+        }
+        dp_finish<S>(Y, F, B, c);
+    } else {
+        dp_full<S, SCH>(p, F, B, c, Y);
+    }
+}
+
 template <int S>
 __device__ __forceinline__ Comm<S> load_comm(const KParams &p) {
     Comm<S> c;
@@ -769,10 +806,7 @@ __device__ __forceinline__ void enqueue(const KParams &p, int which, unsigned in
 // searches together so that the dependent LDS reads of one overlap those of
 // the others.  Invalid (rank, assignment) pairs get the invalid code and
 // raise the error flag.
-#ifndef PK_ILP
-#define PK_ILP 4
-#endif
-constexpr int kIlp = PK_ILP;
+constexpr int kIlp = kDecodeIlp;
 
 // Halvings of one cut search: the smallest H with L <= 2^H (at least 5).
 __host__ __device__ constexpr uint32_t decode_levels(uint32_t L) {
@@ -788,20 +822,18 @@ __host__ __device__ constexpr uint32_t decode_levels(uint32_t L) {
 // spells the lower-bound position in its low H bits.  The last cut needs no
 // search: with one cut left, C(n, 1) = n, so c_{S-1} = a + r.
 template <int S, typename R, int H>
-__device__ __forceinline__ void decode_batch(const KParams &p, const R *sorted, const R *ey, uint64_t base,
-                                             uint64_t stride, bool &bad) {
+__device__ __forceinline__ void decode_ilp(const KParams &p, const R *sorted, const R *ey, uint64_t base,
+                                           uint64_t stride, bool (&act)[kIlp], bool (&ok)[kIlp],
+                                           uint32_t (&asg)[kIlp], uint32_t (&w)[kIlp][Codes<S>::kWords]) {
     constexpr int NW = Codes<S>::kWords;
     constexpr uint32_t NH = 1u << H;
     R r[kIlp];
-    bool ok[kIlp];
-    uint32_t w[kIlp][NW], at[kIlp];
+    uint32_t at[kIlp];
 #pragma unroll
     for (int u = 0; u < kIlp; ++u) {
         const uint64_t i = base + u * stride;
-        const bool act = i < p.n_i;
-        uint32_t a;
-        ok[u] = candidate<R>(p, p.first_i + (act ? i : 0), r[u], a) && act;
-        bad |= act && !ok[u];
+        act[u] = i < p.n_i;
+        ok[u] = candidate<R>(p, p.first_i + (act[u] ? i : 0), r[u], asg[u]) && act[u];
         at[u] = 1;
 #pragma unroll
         for (int k = 0; k < NW; ++k) w[u][k] = 0;
@@ -839,24 +871,37 @@ __device__ __forceinline__ void decode_batch(const KParams &p, const R *sorted, 
     }
 #pragma unroll
     for (int u = 0; u < kIlp; ++u) {
-        const uint64_t i = base + u * stride;
-        if (i < p.n_i) {
-            if (S == 1) w[u][0] = 1u;
-            if (!ok[u]) {
+        if (S == 1) w[u][0] = 1u;
+        if (!ok[u]) {
 #pragma unroll
-                for (int k = 0; k < NW; ++k) w[u][k] = 0u;
-            }
+            for (int k = 0; k < NW; ++k) w[u][k] = 0u;
+        }
+    }
+}
+
+template <int S, typename R, int H>
+__device__ __forceinline__ void decode_batch(const KParams &p, const R *sorted, const R *ey, uint64_t base,
+                                             uint64_t stride, bool &bad) {
+    constexpr int NW = Codes<S>::kWords;
+    bool act[kIlp], ok[kIlp];
+    uint32_t asg[kIlp], w[kIlp][NW];
+    decode_ilp<S, R, H>(p, sorted, ey, base, stride, act, ok, asg, w);
+#pragma unroll
+    for (int u = 0; u < kIlp; ++u) {
+        const uint64_t i = base + u * stride;
+        bad |= act[u] && !ok[u];
+        if (act[u]) {
 #pragma unroll
             for (int k = 0; k < NW; ++k) p.codes[(uint64_t)k * p.ccap + i] = w[u][k];
         }
     }
 }
 
+// Columns 0 .. S-1 of the Pascal table, 2^H entries each, into LDS in order
+// and in tree order; the tree node at depth l and offset m probes sorted
+// position (2m + 1) 2^(H-1-l) - 1 (entry 0 of the tree is unused).
 template <int S, typename R, int H>
-__device__ __forceinline__ void decode_all(const KParams &p, R *lds, bool &bad) {
-    // columns 0 .. S-1, 2^H entries each, in order and in tree order; the
-    // tree node at depth l and offset m probes sorted position
-    // (2m + 1) 2^(H-1-l) - 1 (entry 0 of the tree is unused)
+__device__ __forceinline__ void pascal_tables(const KParams &p, R *lds) {
     constexpr uint32_t NH = 1u << H;
     R *sorted = lds, *ey = lds + (uint32_t)S * NH;
     const R *gb = reinterpret_cast<const R *>(p.binom);
@@ -866,6 +911,19 @@ __device__ __forceinline__ void decode_all(const KParams &p, R *lds, bool &bad) 
         const uint32_t l = i ? 31u - __clz(i) : 0u, m = i - (1u << l);
         ey[e] = i ? gb[k * kNB + (2 * m + 1) * (NH >> (l + 1)) - 1] : (R)0;
     }
+}
+
+// LDS bytes of both copies of the S Pascal columns
+template <int S, typename R>
+__host__ __device__ constexpr size_t pascal_bytes(uint32_t L) {
+    return 2 * (size_t)S * ((size_t)1 << decode_levels(L)) * sizeof(R);
+}
+
+template <int S, typename R, int H>
+__device__ __forceinline__ void decode_all(const KParams &p, R *lds, bool &bad) {
+    constexpr uint32_t NH = 1u << H;
+    R *sorted = lds, *ey = lds + (uint32_t)S * NH;
+    pascal_tables<S, R, H>(p, lds);
     __syncthreads();
     const uint64_t stride = (uint64_t)gridDim.x * kBlock;
     for (uint64_t base = (uint64_t)blockIdx.x * kBlock + threadIdx.x; base < p.n_i; base += kIlp * stride)
@@ -1081,86 +1139,131 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
     block_min_and_finish(best, p.acc, p.done, p.result, nullptr, lvl == p.nlevels, p.accumulate);
 }
 
-// Early stop (Eq. 2 / Theorem 1) over one chunk: each block filters a tile
-// of kTile candidates, compacts the survivors in LDS and evaluates them.
-template <int S, bool AR, bool SCH>
-__global__ __launch_bounds__(kBlock) void bounded_kernel(KParams p, uint64_t chunk_lo, uint64_t chunk_hi,
-                                                         uint32_t bound, uint32_t publish) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    __shared__ uint16_t surv[kTile];
-    __shared__ unsigned int nsurv;
-    __shared__ unsigned int cnt_pruned, cnt_infeas, cnt_bad;
-    const Lds tab = stage_tables(p, smem);
-    const Comm<S> comm = load_comm<S>(p);
+// Early stop (Eq. 2 / Theorem 1) over one piece of a chunk, in two kernels.
+// filter_kernel decodes each candidate (a1), builds its stage weights (a2)
+// and tests memory and Eq. 2 against the bound in force (min of the caller's
+// bound and the best of the earlier chunks, fixed within a chunk) while the
+// cut codes are still in registers; only the survivors go to a list (call
+// index + cut codes), block b filling segment b of p.seg_cap entries and
+// counting them in LDS.  surv_kernel evaluates the list on the DAG (a3) and
+// folds it into the running best (a4).
+template <int S, typename R, int H, bool AR>
+__device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const Lds &tab, uint32_t b,
+                                           unsigned int *nq, uint32_t &n_keep, uint32_t &n_pruned,
+                                           uint32_t &n_infeas, bool &bad) {
     constexpr int NW = Codes<S>::kWords;
-    if (threadIdx.x == 0) { nsurv = 0; cnt_pruned = 0; cnt_infeas = 0; cnt_bad = 0; }
+    constexpr uint32_t NH = 1u << H;
+    const R *sorted = pas, *ey = pas + (uint32_t)S * NH;
+    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    const unsigned int lane = threadIdx.x & 63;
+    const uint64_t seg = (uint64_t)blockIdx.x * p.seg_cap;
+    for (uint64_t base = (uint64_t)blockIdx.x * kBlock + threadIdx.x; base < p.n_i; base += kIlp * stride) {
+        bool act[kIlp], ok[kIlp];
+        uint32_t asg[kIlp], w[kIlp][NW];
+        decode_ilp<S, R, H>(p, sorted, ey, base, stride, act, ok, asg, w);
+#pragma unroll
+        for (int u = 0; u < kIlp; ++u) {
+            uint32_t cut[S + 1], ty[S], F[S], B[S], D[S];
+            unpack_cuts<S>(w[u], p.L, cut);
+            decode_types<S>(p, ok[u] ? asg[u] : 0u, ty);
+            const bool feas = stage_weights<S>(p, tab, cut, ty, F, B);
+            if (AR) {
+                stage_allreduce<S>(p, tab, cut, ty, D);
+            } else {
+#pragma unroll
+                for (int s = 0; s < S; ++s) D[s] = 0;
+            }
+            bool keep = false;
+            if (act[u]) {
+                if (!ok[u]) bad = true;
+                else if (!feas) ++n_infeas;
+                else if (eq2_bound<S>(p.M, F, B, D) > b) ++n_pruned;
+                else keep = true;
+            }
+            // survivors go to this block's segment of the list (LDS counter:
+            // no global atomic, whose single address would serialise waves)
+            const unsigned long long m = __ballot(keep);
+            if (m) {
+                unsigned int slot0 = 0;
+                if (lane == 0) slot0 = atomicAdd(nq, (unsigned int)__popcll(m));
+                slot0 = __shfl(slot0, 0, 64);
+                if (keep) {
+                    const unsigned long long below = lane ? (m & ((1ull << lane) - 1ull)) : 0ull;
+                    const uint64_t o = seg + slot0 + (uint32_t)__popcll(below);
+                    p.sidx[o] = (uint32_t)(p.first_i + base + u * stride);
+#pragma unroll
+                    for (int k = 0; k < NW; ++k) p.codes[(uint64_t)k * p.ccap + o] = w[u][k];
+                }
+                n_keep += lane == 0 ? (uint32_t)__popcll(m) : 0u;
+            }
+        }
+    }
+}
+
+// GTAB: the stage tables are read from global memory (L2) instead of LDS,
+// for the largest Pascal columns (L > 128 with 64-bit ranks), which fill
+// the 64 KB of LDS one block may use on their own.
+template <int S, typename R, bool AR, bool GTAB>
+__global__ __launch_bounds__(kBlock) void filter_kernel(KParams p) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    R *pas = reinterpret_cast<R *>(smem);
+    const uint32_t H = decode_levels(p.L);
+    Lds tab;
+    if constexpr (GTAB) tab = Lds{p.cost, p.pm, p.cap, p.pd};
+    else tab = stage_tables(p, smem + pascal_bytes<S, R>(p.L));   // (its barrier covers both tables)
     // bound in force: min(caller's bound, best of the chunks before this one)
     const unsigned long long rb = __hip_atomic_load(p.snap, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t rbT = (uint32_t)(rb >> 32);
-    const uint32_t b = rbT < bound ? rbT : bound;
-    __syncthreads();
-    const uint64_t base = chunk_lo + (uint64_t)blockIdx.x * kTile;
-    uint32_t my_pruned = 0, my_infeas = 0, my_bad = 0;
-    for (int q = 0; q < kTile / kBlock; ++q) {
-        const uint32_t off = q * kBlock + threadIdx.x;
-        const uint64_t i = base + off;
-        const bool active = i < chunk_hi;
-        uint32_t w[NW], cut[S + 1], ty[S], F[S], B[S];
-#pragma unroll
-        for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[(uint64_t)k * p.ccap + (i - p.first_i)] : 0u;
-        const bool ok = unpack_cuts<S>(w, p.L, cut);
-        decode_types<S>(p, ok ? assign_of(p, i) : 0u, ty);
-        const bool feas = stage_weights<S>(p, tab, cut, ty, F, B);
-        uint32_t D[S];
-        if (AR) {
-            stage_allreduce<S>(p, tab, cut, ty, D);
-        } else {
-#pragma unroll
-            for (int s = 0; s < S; ++s) D[s] = 0;
-        }
-        bool keep = false;
-        if (active) {
-            if (!ok) my_bad++;
-            else if (!feas) my_infeas++;
-            else if (eq2_bound<S>(p.M, F, B, D) > b) my_pruned++;
-            else keep = true;
-        }
-        const unsigned long long m = __ballot(keep);
-        const unsigned int lane = threadIdx.x & 63;
-        unsigned int slot0 = 0;
-        if (lane == 0 && m) slot0 = atomicAdd(&nsurv, (unsigned int)__popcll(m));
-        slot0 = __shfl(slot0, 0, 64);
-        if (keep) {
-            const unsigned long long below = lane ? (m & ((1ull << lane) - 1ull)) : 0ull;
-            surv[slot0 + __popcll(below)] = (uint16_t)off;
-        }
+    const uint32_t b = rbT < p.es_bound ? rbT : p.es_bound;
+    uint32_t n_keep = 0, n_pruned = 0, n_infeas = 0;
+    bool bad = false;
+    __shared__ unsigned int nq;
+    if (threadIdx.x == 0) nq = 0;
+    switch (H) {
+    case 8: pascal_tables<S, R, 8>(p, pas); __syncthreads(); filter_all<S, R, 8, AR>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
+    case 7: pascal_tables<S, R, 7>(p, pas); __syncthreads(); filter_all<S, R, 7, AR>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
+    case 6: pascal_tables<S, R, 6>(p, pas); __syncthreads(); filter_all<S, R, 6, AR>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
+    default: pascal_tables<S, R, 5>(p, pas); __syncthreads(); filter_all<S, R, 5, AR>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
     }
-    if (my_pruned) atomicAdd(&cnt_pruned, my_pruned);
-    if (my_infeas) atomicAdd(&cnt_infeas, my_infeas);
-    if (my_bad) atomicAdd(&cnt_bad, my_bad);
+    // per-block sums, one global atomic per counter and block
+    const unsigned long long sk = wave_sum_u32(n_keep), sp = wave_sum_u32(n_pruned), si = wave_sum_u32(n_infeas);
+    __shared__ unsigned long long cnt[3];
+    if (threadIdx.x < 3) cnt[threadIdx.x] = 0;
     __syncthreads();
-    const unsigned int n = nsurv;
+    if ((threadIdx.x & 63) == 0) {
+        if (sk) atomicAdd(&cnt[0], sk);
+        if (sp) atomicAdd(&cnt[1], sp);
+        if (si) atomicAdd(&cnt[2], si);
+    }
+    __syncthreads();
+    if (threadIdx.x < 3 && cnt[threadIdx.x]) atomicAdd(&p.stats[threadIdx.x], cnt[threadIdx.x]);
+    if (threadIdx.x == 0) p.scount[blockIdx.x] = nq;   // (after the barrier above: every wave has added)
+    if (bad) atomicOr(p.err, 1u);
+}
+
+// Block b evaluates segment b of the survivor list (filter_kernel's block b).
+template <int S, bool AR, bool SCH>
+__global__ __launch_bounds__(kBlock) void surv_kernel(KParams p, uint32_t publish) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const Lds tab = stage_tables(p, smem);
+    const Comm<S> comm = load_comm<S>(p);
+    constexpr int NW = Codes<S>::kWords;
+    const uint32_t n = __hip_atomic_load(&p.scount[blockIdx.x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t seg = (uint64_t)blockIdx.x * p.seg_cap;
     unsigned long long best = ~0ull;
-    for (unsigned int k = threadIdx.x; k < n; k += kBlock) {
-        const uint64_t i = base + surv[k];
-        uint32_t w[NW], cut[S + 1], ty[S], F[S], B[S];
+    for (uint32_t k = threadIdx.x; k < n; k += kBlock) {
+        const uint32_t i = p.sidx[seg + k];
+        uint32_t w[NW], cut[S + 1], ty[S], F[S], B[S], Y[S];
 #pragma unroll
-        for (int kk = 0; kk < NW; ++kk) w[kk] = p.codes[(uint64_t)kk * p.ccap + (i - p.first_i)];
+        for (int kk = 0; kk < NW; ++kk) w[kk] = p.codes[(uint64_t)kk * p.ccap + seg + k];
         unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = assign_of(p, i);
         decode_types<S>(p, a, ty);
         stage_weights<S>(p, tab, cut, ty, F, B);
-        uint32_t Y[S];
-        dp_full<S, SCH>(p, F, B, comm, Y);
+        dp_full_settle<S, SCH>(p, F, B, comm, Y);
         const uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, a);
-        const unsigned long long key = make_key(true, T, (uint32_t)i);
+        const unsigned long long key = make_key(true, T, i);
         best = key < best ? key : best;
-    }
-    if (threadIdx.x == 0) {
-        atomicAdd(&p.stats[0], (unsigned long long)n);
-        atomicAdd(&p.stats[1], (unsigned long long)cnt_pruned);
-        atomicAdd(&p.stats[2], (unsigned long long)cnt_infeas);
-        if (cnt_bad) atomicOr(p.err, 1u);
     }
     block_min_and_finish(best, p.acc, p.done, nullptr, p.run_best, true, false, publish ? p.snap : nullptr);
 }
@@ -1184,8 +1287,7 @@ hipError_t launch_eval_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) 
 
 template <int S, typename R>
 hipError_t launch_decode_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
-    // both copies of the S Pascal columns, 2^H entries each
-    const size_t lds = 2 * (size_t)S * ((size_t)1 << decode_levels(p.L)) * sizeof(R);
+    const size_t lds = pascal_bytes<S, R>(p.L);
     hipLaunchKernelGGL((decode_kernel<S, R>), dim3(lc.grid), dim3(kBlock), lds, st, p);
     return hipGetLastError();
 }
@@ -1201,23 +1303,31 @@ hipError_t launch_resume_s(const KParams &p, const LaunchCfg &lc, hipStream_t st
     return hipGetLastError();
 }
 
+// One piece of an early-stop chunk: filter_kernel on the grid in lc (LDS:
+// Pascal columns, then the stage tables of lc.lds_bytes), then surv_kernel
+// on the same grid (one block per survivor segment).
+constexpr size_t kLdsBlockMax = 64 * 1024;   // LDS bytes one block of these kernels may use
+
 template <int S, typename R>
-hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint64_t lo, uint64_t hi,
-                                   uint32_t bound, uint32_t publish) {
-    const dim3 grid((uint32_t)((hi - lo + kTile - 1) / kTile));
+hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t publish) {
+    const size_t pas = pascal_bytes<S, R>(p.L);
+    const dim3 fg(lc.grid), fb(kBlock);
+    if (pas + lc.lds_bytes > kLdsBlockMax) {
+        if (p.has_ar) hipLaunchKernelGGL((filter_kernel<S, R, true, true>), fg, fb, pas, st, p);
+        else hipLaunchKernelGGL((filter_kernel<S, R, false, true>), fg, fb, pas, st, p);
+    } else {
+        const size_t lds = pas + lc.lds_bytes;
+        if (p.has_ar) hipLaunchKernelGGL((filter_kernel<S, R, true, false>), fg, fb, lds, st, p);
+        else hipLaunchKernelGGL((filter_kernel<S, R, false, false>), fg, fb, lds, st, p);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 g(lc.grid), b(kBlock);
     const bool sch = p.sched != 0;
-    if (p.has_ar && sch)
-        hipLaunchKernelGGL((bounded_kernel<S, true, true>), grid, dim3(kBlock), lc.lds_bytes, st, p, lo, hi,
-                           bound, publish);
-    else if (p.has_ar)
-        hipLaunchKernelGGL((bounded_kernel<S, true, false>), grid, dim3(kBlock), lc.lds_bytes, st, p, lo, hi,
-                           bound, publish);
-    else if (sch)
-        hipLaunchKernelGGL((bounded_kernel<S, false, true>), grid, dim3(kBlock), lc.lds_bytes, st, p, lo, hi,
-                           bound, publish);
-    else
-        hipLaunchKernelGGL((bounded_kernel<S, false, false>), grid, dim3(kBlock), lc.lds_bytes, st, p, lo, hi,
-                           bound, publish);
+    if (p.has_ar && sch) hipLaunchKernelGGL((surv_kernel<S, true, true>), g, b, lc.lds_bytes, st, p, publish);
+    else if (p.has_ar) hipLaunchKernelGGL((surv_kernel<S, true, false>), g, b, lc.lds_bytes, st, p, publish);
+    else if (sch) hipLaunchKernelGGL((surv_kernel<S, false, true>), g, b, lc.lds_bytes, st, p, publish);
+    else hipLaunchKernelGGL((surv_kernel<S, false, false>), g, b, lc.lds_bytes, st, p, publish);
     return hipGetLastError();
 }
 

@@ -491,7 +491,7 @@ __global__ __launch_bounds__(kBlock) void search_leaf_kernel(KParams p, SearchPa
     if (leaf) {
         uint32_t F[S], B[S], Y[S];
         stage_weights<S>(p, tab, cut, ty, F, B);
-        dp_full<S, SCH>(p, F, B, comm, Y);
+        dp_full_settle<S, SCH>(p, F, B, comm, Y);
         const uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, row);
         if (T <= bound) key = ((unsigned long long)T << 32) | i;
     }

@@ -294,6 +294,23 @@ def bounded_vs_oracle(prob, cands, bound, chunk, dev):
     return b, st
 
 
+def test_bounded_largest_pascal_columns(dev):
+    """S = 16 with L > 128 and 64-bit ranks: the early-stop filter's Pascal
+    columns fill a block's 64 KB of LDS, so it reads the stage tables from
+    global memory; with and without all-reduce times, several chunk sizes."""
+    rng = np.random.default_rng(141)
+    for ar in (False, True):
+        prob = W.random_problem(rng, 130, 16, 40, 3, cost_lo=50, cost_hi=400, mem_hi=20, cap=400, assign_rows=1)
+        if ar:
+            _with_allreduce(rng, prob, hi=3000)
+        cands = W.random_candidates(rng, prob, 6000)
+        assert int(cands.comp_rank.max()) > 2 ** 32
+        To, fo = check_against_oracle(prob, cands, dev)[:2]
+        bound = int(np.sort(To[fo])[40]) if fo.sum() > 40 else 2 ** 31 - 1
+        for chunk in (0, 777, 4096):
+            bounded_vs_oracle(prob, cands, bound, chunk, dev)
+
+
 def test_bounded_random(dev):
     rng = np.random.default_rng(106)
     for trial in range(20):
