@@ -218,8 +218,8 @@ int poseidon_argmin(poseidon_ctx *ctx, const uint32_t *makespan, const uint32_t 
  * optimum of those candidates.  POSEIDON_NO_FEASIBLE if there is none.
  * best_out and stats_out are HOST pointers (either may be NULL); the call
  * synchronises the stream after every level of the search.  The frontier
- * memory, 4 Mi partial configurations per stage of (5 + 4 ceil((S-1)/4))
- * bytes each (1.4 GB at S = 16), is allocated on the first call and kept by
+ * memory, 4 Mi partial configurations per stage of (6 + 4 ceil((S-1)/4))
+ * bytes each (1.5 GB at S = 16), is allocated on the first call and kept by
  * the context.  The work grows with the pruned tree, which for many stages
  * and a loose bound can be very large (Sec. 4.2.3). */
 enum {
