@@ -869,7 +869,8 @@ constexpr uint64_t kSearchCap = 1ull << 22;            // nodes per frontier pie
 constexpr uint32_t kSearchBlk = kSearchCap / 256;      // blocks per piece
 static_assert(kSearchBlk <= pk::kSearchScanMax, "a level piece must fit the scan kernel");
 
-enum { SW_STATS = 0, SW_ACC = 5, SW_BEST = 6, SW_TOTAL = 9, SW_BOUND = 10, SW_COUNT = 11 };
+// state words: counters, leaf key, best, bound, then one child total per level
+enum { SW_STATS = 0, SW_ACC = 5, SW_BEST = 6, SW_BOUND = 9, SW_TOTAL = 10, SW_COUNT = SW_TOTAL + pk::kSMax };
 
 struct SearchWs {
     uint32_t *row[pk::kSMax], *codes[pk::kSMax];
@@ -909,8 +910,8 @@ struct SearchRun {
     std::vector<unsigned long long> off;
 };
 
-int search_read_total(SearchRun &r, unsigned long long *total) {
-    if (hipMemcpyAsync(total, r.w.words + SW_TOTAL, 8, hipMemcpyDeviceToHost, r.st) != hipSuccess ||
+int search_read_total(SearchRun &r, uint32_t x, unsigned long long *total) {
+    if (hipMemcpyAsync(total, r.w.words + SW_TOTAL + x, 8, hipMemcpyDeviceToHost, r.st) != hipSuccess ||
         hipStreamSynchronize(r.st) != hipSuccess)
         return POSEIDON_E_DEVICE;
     return POSEIDON_OK;
@@ -924,14 +925,20 @@ bool search_fused(const poseidon_ctx *ctx, uint32_t x) {
     return ctx->S >= 3 && x + 3 == ctx->S && 256 * (L - 1) * (L - 1) <= kSearchCap;
 }
 
-// Expand the n nodes at level x (stored in the level's arrays) depth first.
-int search_expand(SearchRun &r, uint32_t x, uint64_t n) {
+// Expand the nodes at level x (stored in the level's arrays) depth first:
+// n of them, or, with n_dev, at most n, their number being on the device.
+// When every child of the level fits one frontier piece (n times the most
+// children a node can have), the next level is launched on that bound
+// without reading the total back; otherwise the host reads it and splits the
+// level into pieces.
+int search_expand(SearchRun &r, uint32_t x, uint64_t n, const unsigned long long *n_dev) {
     const uint32_t S = r.ctx->S;
     pk::SearchParams q = r.q;
     q.in_row = r.w.row[x];
     q.in_codes = r.w.codes[x];
     q.in_cap = kSearchCap;
     q.n_in = (uint32_t)n;
+    q.n_dev = n_dev;
     q.level = x;
     const uint32_t grid = (uint32_t)((n + 255) / 256);
     const size_t lds = r.ctx->lds_bytes;
@@ -952,17 +959,24 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n) {
     q.out_row = r.w.row[x + step];
     q.out_codes = r.w.codes[x + step];
     q.out_cap = kSearchCap;
+    q.total = r.w.words + SW_TOTAL + x;
     if (pk::launch_search(pk::kSearchOpCount, r.kp, q, grid, lds, r.st) != hipSuccess ||
         pk::launch_search_scan(q, grid, r.st) != hipSuccess)
         return POSEIDON_E_DEVICE;
+    const uint64_t most = step == 2 ? (uint64_t)(r.ctx->L - 1) * (r.ctx->L - 1) : r.ctx->L - 1;
+    if (n * most <= kSearchCap) {
+        q.blk_base = 0;
+        if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, grid, lds, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
+        return search_expand(r, x + step, n * most, q.total);
+    }
     unsigned long long total = 0;
-    int rc = search_read_total(r, &total);
+    int rc = search_read_total(r, x, &total);
     if (rc != POSEIDON_OK) return rc;
     if (total == 0) return POSEIDON_OK;
     if (total <= kSearchCap) {
         q.blk_base = 0;
         if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, grid, lds, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
-        return search_expand(r, x + step, total);
+        return search_expand(r, x + step, total, nullptr);
     }
     // more children than a level holds: write and expand them in pieces of
     // whole blocks (one block has at most 256 (L - 1) < kSearchCap children,
@@ -978,7 +992,7 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n) {
         q.blk_base = b0;
         if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, b1 - b0, lds, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
         if (off[b1] > off[b0]) {
-            rc = search_expand(r, x + step, off[b1] - off[b0]);
+            rc = search_expand(r, x + step, off[b1] - off[b0], nullptr);
             if (rc != POSEIDON_OK) return rc;
         }
         b0 = b1;
@@ -1016,7 +1030,6 @@ extern "C" int poseidon_search(poseidon_ctx *ctx, uint64_t first_row, uint64_t n
     r.q.stats = r.w.words + SW_STATS;
     r.q.acc = r.w.words + SW_ACC;
     r.q.best = r.w.words + SW_BEST;
-    r.q.total = r.w.words + SW_TOTAL;
     r.q.bound = (uint32_t *)(r.w.words + SW_BOUND);
     if (pk::launch_fill(r.q.stats, 5, 0ull, st) != hipSuccess ||
         pk::launch_fill(r.q.acc, 4, ~0ull, st) != hipSuccess)
@@ -1037,7 +1050,7 @@ extern "C" int poseidon_search(poseidon_ctx *ctx, uint64_t first_row, uint64_t n
             q.root_first = (uint32_t)(first_row + r0);
             if (pk::launch_search(pk::kSearchOpRoot, r.kp, q, (n + 255) / 256, 0, st) != hipSuccess)
                 return POSEIDON_E_DEVICE;
-            rc = search_expand(r, 0, n);
+            rc = search_expand(r, 0, n, nullptr);
         }
     }
     if (rc != POSEIDON_OK) return rc;

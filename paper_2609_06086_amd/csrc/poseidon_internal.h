@@ -86,7 +86,8 @@ struct SearchParams {
     const uint32_t *in_row;           // [in_cap] assignment row of each node
     const uint32_t *in_codes;         // [words][in_cap] cut codes, cuts 1..level set
     uint64_t in_cap;
-    uint32_t n_in;                    // nodes of this piece
+    uint32_t n_in;                    // nodes of this piece (an upper bound when n_dev is set)
+    const unsigned long long *n_dev;  // the piece's node count on the device, or null: n_in
     uint32_t level;                   // stages 1..level fixed
     uint32_t *out_row;                // children (or roots)
     uint32_t *out_codes;              // [words][out_cap]
@@ -103,7 +104,7 @@ struct SearchParams {
     unsigned long long *stats;        // visited, evaluated, pruned by memory / ridge / bound
     unsigned long long *acc;          // best (T << 32 | position) of a leaf piece
     unsigned long long *best;         // makespan, row, composition rank of the best so far
-    unsigned long long *total;        // children of the last scanned level piece
+    unsigned long long *total;        // children of the scanned level piece (one word per level)
     uint32_t root_first;              // first row of a root piece
 };
 

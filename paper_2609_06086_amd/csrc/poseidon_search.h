@@ -358,13 +358,26 @@ __device__ __forceinline__ void search_load(const SearchParams &q, uint32_t i, b
     for (int k = 0; k < Codes<S>::kWords; ++k) w[k] = active ? q.in_codes[(uint64_t)k * q.in_cap + i] : 0u;
 }
 
+// Nodes of the level: counted on the device by the previous level's scan
+// when the host launched on an upper bound (q.n_dev), else q.n_in.
+__device__ __forceinline__ uint32_t search_n_in(const SearchParams &q) {
+    return q.n_dev ? (uint32_t)*q.n_dev : q.n_in;
+}
+
 // Count the children of every node of the piece; one total per block.
 template <int S>
 __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchParams q) {
     extern __shared__ __align__(16) unsigned char smem[];
+    const uint32_t n_in = search_n_in(q);
+    if (blockIdx.x * kBlock >= n_in) {
+        // a block past the level's nodes (grid from an upper bound): zero totals
+        if (threadIdx.x < 5) q.blk_cnt[(uint64_t)threadIdx.x * q.blk_stride + blockIdx.x] = 0;
+        if (threadIdx.x == 0) q.blk_tot[blockIdx.x] = 0;
+        return;
+    }
     const Lds tab = stage_tables(p, smem);
     const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
-    const bool active = i < q.n_in;
+    const bool active = i < n_in;
     const uint32_t bound = *q.bound;
     uint32_t row, w[Codes<S>::kWords], ty[S], cut[S + 1];
     search_load<S>(q, i, active, row, w);
@@ -420,10 +433,12 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
 template <int S>
 __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchParams q) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Lds tab = stage_tables(p, smem);
     const uint32_t blk = q.blk_base + blockIdx.x;
+    const uint32_t n_in = search_n_in(q);
+    if (blk * kBlock >= n_in) return;   // past the level's nodes
+    const Lds tab = stage_tables(p, smem);
     const uint32_t i = blk * kBlock + threadIdx.x;
-    const bool active = i < q.n_in;
+    const bool active = i < n_in;
     const uint32_t bound = *q.bound;
     // the count kernel left each node's number of children: nodes without
     // any (most of them at the level that fixes the last cut) do nothing
@@ -472,11 +487,13 @@ __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchP
 template <int S, bool AR, bool SCH>
 __global__ __launch_bounds__(kBlock) void search_leaf_kernel(KParams p, SearchParams q) {
     extern __shared__ __align__(16) unsigned char smem[];
+    const uint32_t n_in = search_n_in(q);
+    if (blockIdx.x * kBlock >= n_in) return;   // past the level's nodes
     const Lds tab = stage_tables(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
-    const bool active = i < q.n_in;
+    const bool active = i < n_in;
     const uint32_t bound = *q.bound;
     uint32_t row, w[NW], ty[S], cut[S + 1];
     search_load<S>(q, i, active, row, w);
