@@ -821,6 +821,20 @@ __host__ __device__ constexpr uint32_t decode_levels(uint32_t L) {
 // 2^(H-b) entries apart and share banks.  After H steps the tree index i
 // spells the lower-bound position in its low H bits.  The last cut needs no
 // search: with one cut left, C(n, 1) = n, so c_{S-1} = a + r.
+// One halving of the tree search: t <- 2 t + (probe < Q), as a compare into
+// VCC and an add with carry-in (the compiler's select and shift-or take one
+// VALU operation more).
+__device__ __forceinline__ uint32_t tree_step(uint32_t t, uint64_t probe, uint64_t q) {
+    asm("v_cmp_lt_u64_e32 vcc, %1, %2\n\tv_addc_co_u32_e32 %0, vcc, %0, %0, vcc"
+                 : "+v"(t) : "v"(probe), "v"(q) : "vcc");
+    return t;
+}
+__device__ __forceinline__ uint32_t tree_step(uint32_t t, uint32_t probe, uint32_t q) {
+    asm("v_cmp_lt_u32_e32 vcc, %1, %2\n\tv_addc_co_u32_e32 %0, vcc, %0, %0, vcc"
+                 : "+v"(t) : "v"(probe), "v"(q) : "vcc");
+    return t;
+}
+
 template <int S, typename R, int H>
 __device__ __forceinline__ void decode_ilp(const KParams &p, const R *sorted, const R *ey, uint64_t base,
                                            uint64_t stride, bool (&act)[kIlp], bool (&ok)[kIlp],
@@ -854,7 +868,7 @@ __device__ __forceinline__ void decode_ilp(const KParams &p, const R *sorted, co
 #pragma unroll
         for (int b = 0; b < H; ++b) {
 #pragma unroll
-            for (int u = 0; u < kIlp; ++u) t[u] = t[u] + t[u] + (uint32_t)(tree[t[u]] < Q[u]);
+            for (int u = 0; u < kIlp; ++u) t[u] = tree_step(t[u], tree[t[u]], Q[u]);
         }
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) {
