@@ -1255,21 +1255,39 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(KParams p) {
     if (bad) atomicOr(p.err, 1u);
 }
 
-// Block b evaluates segment b of the survivor list (filter_kernel's block b).
+// Block b evaluates segments [b kSurvSegs, (b + 1) kSurvSegs) of the survivor
+// list (those of filter_kernel's blocks), their entries spread over its
+// threads as one list.  Fewer blocks than segments: each block pays for the
+// LDS tables and one ticket on the grid's done counter, whose single address
+// serialises the blocks.
+constexpr uint32_t kSurvSegs = 8;
+
 template <int S, bool AR, bool SCH>
-__global__ __launch_bounds__(kBlock) void surv_kernel(KParams p, uint32_t publish) {
+__global__ __launch_bounds__(kBlock) void surv_kernel(KParams p, uint32_t publish, uint32_t nseg) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Lds tab = stage_tables(p, smem);
+    __shared__ uint32_t pre[kSurvSegs + 1];
+    const uint32_t s0 = blockIdx.x * kSurvSegs, ns = min(kSurvSegs, nseg - s0);
+    if (threadIdx.x == 0) {
+        uint32_t t = 0;
+        pre[0] = 0;
+        for (uint32_t j = 0; j < ns; ++j) {
+            t += __hip_atomic_load(&p.scount[s0 + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            pre[j + 1] = t;
+        }
+    }
+    const Lds tab = stage_tables(p, smem);   // (its barrier also publishes pre)
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
-    const uint32_t n = __hip_atomic_load(&p.scount[blockIdx.x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint64_t seg = (uint64_t)blockIdx.x * p.seg_cap;
+    const uint32_t n = pre[ns];
     unsigned long long best = ~0ull;
     for (uint32_t k = threadIdx.x; k < n; k += kBlock) {
-        const uint32_t i = p.sidx[seg + k];
+        uint32_t j = 0;
+        while (j + 1 < ns && pre[j + 1] <= k) ++j;
+        const uint64_t at = (uint64_t)(s0 + j) * p.seg_cap + (k - pre[j]);
+        const uint32_t i = p.sidx[at];
         uint32_t w[NW], cut[S + 1], ty[S], F[S], B[S], Y[S];
 #pragma unroll
-        for (int kk = 0; kk < NW; ++kk) w[kk] = p.codes[(uint64_t)kk * p.ccap + seg + k];
+        for (int kk = 0; kk < NW; ++kk) w[kk] = p.codes[(uint64_t)kk * p.ccap + at];
         unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = assign_of(p, i);
         decode_types<S>(p, a, ty);
@@ -1319,7 +1337,7 @@ hipError_t launch_resume_s(const KParams &p, const LaunchCfg &lc, hipStream_t st
 
 // One piece of an early-stop chunk: filter_kernel on the grid in lc (LDS:
 // Pascal columns, then the stage tables of lc.lds_bytes), then surv_kernel
-// on the same grid (one block per survivor segment).
+// (one block per kSurvSegs survivor segments).
 constexpr size_t kLdsBlockMax = 64 * 1024;   // LDS bytes one block of these kernels may use
 
 template <int S, typename R>
@@ -1336,12 +1354,13 @@ hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t s
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const dim3 g(lc.grid), b(kBlock);
+    const uint32_t nseg = lc.grid;
+    const dim3 g((nseg + kSurvSegs - 1) / kSurvSegs), b(kBlock);
     const bool sch = p.sched != 0;
-    if (p.has_ar && sch) hipLaunchKernelGGL((surv_kernel<S, true, true>), g, b, lc.lds_bytes, st, p, publish);
-    else if (p.has_ar) hipLaunchKernelGGL((surv_kernel<S, true, false>), g, b, lc.lds_bytes, st, p, publish);
-    else if (sch) hipLaunchKernelGGL((surv_kernel<S, false, true>), g, b, lc.lds_bytes, st, p, publish);
-    else hipLaunchKernelGGL((surv_kernel<S, false, false>), g, b, lc.lds_bytes, st, p, publish);
+    if (p.has_ar && sch) hipLaunchKernelGGL((surv_kernel<S, true, true>), g, b, lc.lds_bytes, st, p, publish, nseg);
+    else if (p.has_ar) hipLaunchKernelGGL((surv_kernel<S, true, false>), g, b, lc.lds_bytes, st, p, publish, nseg);
+    else if (sch) hipLaunchKernelGGL((surv_kernel<S, false, true>), g, b, lc.lds_bytes, st, p, publish, nseg);
+    else hipLaunchKernelGGL((surv_kernel<S, false, false>), g, b, lc.lds_bytes, st, p, publish, nseg);
     return hipGetLastError();
 }
 
