@@ -180,8 +180,11 @@ __device__ __forceinline__ uint32_t search_accepted(const KParams &p, const Lds 
     const uint32_t dl = p.has_ar ? pdt[n.lo] : 0u;
     const bool stage = !(flags & kSearchNoStage);
     const uint32_t carry = n.inner + n.last_b;
+    const int H = (int)decode_levels(p.L);   // (uniform: the steps above it are skipped by scalar branches)
     uint32_t k = 0;
-    for (int b = (int)decode_levels(p.L) - 1; b >= 0; --b) {
+#pragma unroll
+    for (int b = 7; b >= 0; --b) {
+        if (b >= H) continue;
         const uint32_t t = k + (1u << b);
         const uint32_t h = n.lo + min(t, len);
         bool ok = tab.pm[h] - pml <= capt;
@@ -258,19 +261,27 @@ __device__ __forceinline__ uint32_t search_last_children(const KParams &p, const
         if (stage && r0 <= h1) {
             const uint64_t *ct = tab.cost + n.t * row_len, *cs = tab.cost + n.tS * row_len;
             const uint64_t cl = ct[n.lo], cL = cs[p.L];
-            const int64_t M = p.M;
+            // g(hi) = C + G(hi) > bound  <=>  G(hi) > bound - C.  Every prefix time
+            // and M times any type's prefix stays below 2^31 (checked at load), so
+            // G fits 32 bits; the threshold is clamped to that range
             const int64_t C = (int64_t)n.pre_f - (int64_t)(uint32_t)cl - (int64_t)(cl >> 32) +
                               (x == 0 ? 0 : (int64_t)(n.inner + n.last_b)) +
-                              M * ((int64_t)(uint32_t)cL + (int64_t)(cL >> 32));
+                              (int64_t)p.M * ((int64_t)(uint32_t)cL + (int64_t)(cL >> 32));
+            const int64_t thr64 = (int64_t)bound - C;
+            const int32_t thr = thr64 > INT32_MAX ? INT32_MAX : thr64 < INT32_MIN ? INT32_MIN : (int32_t)thr64;
+            const bool none = thr64 < INT32_MIN;   // every G(hi) > thr (G > -2^31 always)
             const uint32_t len = h1 + 1 - r0;
+            const int H = (int)decode_levels(p.L);
             uint32_t j = 0;
-            for (int b = (int)decode_levels(p.L) - 1; b >= 0; --b) {
+#pragma unroll
+            for (int b = 7; b >= 0; --b) {
+                if (b >= H) continue;
                 const uint32_t t = j + (1u << b);
                 const uint32_t h = r0 + min(t, len) - 1;
                 const uint64_t ch = ct[h], sh = cs[h];
-                const int64_t G = (int64_t)(uint32_t)ch + (int64_t)(ch >> 32) -
-                                  M * ((int64_t)(uint32_t)sh + (int64_t)(sh >> 32));
-                j = (t <= len && C + G > (int64_t)bound) ? t : j;
+                const int32_t G = (int32_t)((uint32_t)ch + (uint32_t)(ch >> 32)) -
+                                  (int32_t)(p.M * ((uint32_t)sh + (uint32_t)(sh >> 32)));
+                j = (t <= len && (none || G > thr)) ? t : j;
             }
             g0 = r0 + j;
             lp.bound += j;
