@@ -1,9 +1,10 @@
-// Kernel instantiations for stage counts 9, 10, 11, 12 (split so that the library
-// compiles in parallel).
+// Explicit instantiation of the templated kernels for one stage count S:
+// every instantiation unit includes this and lists its stage counts, so
+// that the library compiles in parallel, one unit per core.
+#pragma once
 #include "poseidon_search.h"
 
-namespace pk {
-
+// (expanded inside namespace pk)
 #define PK_INST(S)                                                                                        \
     template hipError_t launch_eval_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t);           \
     template hipError_t launch_eval_s<S, uint64_t>(const KParams &, const LaunchCfg &, hipStream_t);           \
@@ -21,7 +22,3 @@ namespace pk {
                                                       hipStream_t);                                                 \
     template hipError_t launch_search_s<S, uint64_t>(int, const KParams &, const SearchParams &, uint32_t, size_t,  \
                                                       hipStream_t);
-
-PK_INST(9) PK_INST(10) PK_INST(11) PK_INST(12)
-
-}  // namespace pk
