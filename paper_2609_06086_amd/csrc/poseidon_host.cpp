@@ -784,9 +784,9 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
     kp.assign_idx = cands->assign_idx;
     const uint64_t n = cands->count;
     if (chunk == 0 || chunk > n) chunk = n;
-    // the cut codes of at most kChunk candidates are resident at a time; a
-    // longer chunk is decoded and filtered in pieces that all see the bound
-    // in force at the chunk's start (the snapshot moves only at chunk ends)
+    // the survivor list has room for the survivors of kChunk candidates; a
+    // longer chunk is filtered in pieces that all see the bound in force at
+    // the chunk's start (the snapshot moves only at chunk ends)
     rc = ensure_workspace(ctx, std::min<uint64_t>(chunk, kChunk), st);
     if (rc != POSEIDON_OK) return rc;
     kp.codes = (uint32_t *)ctx->ws;
