@@ -99,10 +99,12 @@ def search_bench(args):
                                       assign_idx=torch.from_numpy(c.assign_idx[:500].view(np.int32)).to(dev))
     bound = warm.makespan
     rpc = args.rows_per_chunk
+    ramp = not args.fixed_chunks
+    chunking = f"chunks of 1, 2, 4, ... up to {rpc} rows" if ramp else f"{rpc} rows per chunk"
     stream = torch.cuda.current_stream()
 
     def step():
-        return P.poseidon_search(ctx, bound, rows_per_chunk=rpc, ridge=args.ridge, stream=stream)
+        return P.poseidon_search(ctx, bound, rows_per_chunk=rpc, ridge=args.ridge, ramp=ramp, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -129,7 +131,7 @@ def search_bench(args):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
         "data": "synthetic (seeded per-layer profile tables)",
         "config": {"workload": f"L={prob.L} S={prob.S} M={prob.M} T={prob.T}, all {prob.A} assignment rows x "
-                               f"C({prob.L - 1},{prob.S - 1}) compositions, {rpc} rows per chunk, bound = best of "
+                               f"C({prob.L - 1},{prob.S - 1}) compositions, {chunking}, bound = best of "
                                f"the first 500 sampled candidates ({bound} us)" + (", ridge filter" if args.ridge else ""),
                    "parallelism": "single GPU"},
         "search": {"visited": st.visited, "evaluated": st.evaluated, "pruned_memory": st.pruned_memory,
@@ -145,7 +147,7 @@ def search_bench(args):
         coracle.lib()
         rows = 128
         t0 = time.perf_counter()
-        r = coracle.search(prob, bound, first_row=0, n_rows=rows, rows_per_chunk=rpc, ridge=args.ridge)
+        r = coracle.search(prob, bound, first_row=0, n_rows=rows, rows_per_chunk=rpc, ridge=args.ridge, ramp=ramp)
         dt = time.perf_counter() - t0
         t_cpu = r["visited"] + r["pruned_memory"] + r["pruned_ridge"] + r["pruned_bound"]
         out["cpu_baseline"] = {"value": rows * prob.n_candidates / prob.A / dt, "unit": "candidates/s",
@@ -171,7 +173,10 @@ def main():
                          "the stages as virtual stages on S/2 devices; workloads 3 and 5)")
     ap.add_argument("--search", action="store_true",
                     help="time the pruned configuration search over the whole 8-stage workload instead")
-    ap.add_argument("--rows-per-chunk", type=int, default=64)
+    ap.add_argument("--rows-per-chunk", type=int, default=512)
+    ap.add_argument("--fixed-chunks", action="store_true",
+                    help="with --search: every chunk has --rows-per-chunk rows (default: chunks of 1, 2, 4, ... rows "
+                         "up to --rows-per-chunk)")
     ap.add_argument("--ridge", action="store_true", help="with --search: layer-level (ridge) pruning")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (for counter scaling)")

@@ -209,8 +209,11 @@ int poseidon_argmin(poseidon_ctx *ctx, const uint32_t *makespan, const uint32_t 
  * POSEIDON_SEARCH_NO_STAGE_PRUNING).  Complete configurations that pass are
  * evaluated on the DAG.
  * The rows are processed in consecutive chunks of rows_per_chunk rows
- * (0 = one chunk); a chunk prunes against min(bound, best makespan of the
- * earlier chunks), so every counter is deterministic for a given chunking.
+ * (0 = one chunk), or with POSEIDON_SEARCH_RAMP in chunks that grow 1, 2,
+ * 4, ... rows until they reach rows_per_chunk; a chunk prunes against
+ * min(bound, best makespan of the earlier chunks), so every counter is
+ * deterministic for a given chunking.  Small first chunks tighten the
+ * bound early; large later ones need fewer levels of launches per row.
  * Result: among feasible (and, with the ridge flag, ridge-like) candidates
  * of the rows with makespan <= bound, the smallest makespan, ties to the
  * first in search order (row, then composition rank); best_out->index is
@@ -224,7 +227,8 @@ int poseidon_argmin(poseidon_ctx *ctx, const uint32_t *makespan, const uint32_t 
  * and a loose bound can be very large (Sec. 4.2.3). */
 enum {
     POSEIDON_SEARCH_RIDGE = 1,               /* layer-level pruning (Theorem 2) */
-    POSEIDON_SEARCH_NO_STAGE_PRUNING = 2     /* no Eq. 2 test on partial configurations */
+    POSEIDON_SEARCH_NO_STAGE_PRUNING = 2,    /* no Eq. 2 test on partial configurations */
+    POSEIDON_SEARCH_RAMP = 4                 /* chunks of 1, 2, 4, ... rows up to rows_per_chunk */
 };
 
 typedef struct {

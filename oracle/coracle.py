@@ -19,8 +19,9 @@ LIB = os.path.join(HERE, "liboracle.so")
 
 
 def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (no HIP, no shared headers)."""
-    if force or not os.path.exists(LIB):
+    """Compile the oracle with gcc (no HIP, no shared headers); without
+    force, only when the library is missing or older than its source."""
+    if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
         tmp = LIB + ".tmp"
         subprocess.run(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-Wno-unused-parameter",
                         "-shared", "-fPIC", "-pthread", SRC, "-o", tmp], check=True)
@@ -41,8 +42,7 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB):
-            build(force=False)
+        build(force=False)
         _lib = C.CDLL(LIB)
         _lib.oc_eval.restype = C.c_int
         _lib.oc_eval.argtypes = [C.POINTER(_Problem), C.c_uint64, C.c_uint64, C.c_void_p,
@@ -139,18 +139,19 @@ def bounded(prob, cands, bound: int, chunk: int = 0, nthreads: Optional[int] = N
     return best, int(ev.value), int(pr.value), int(inf.value)
 
 
-SEARCH_RIDGE, SEARCH_NO_STAGE_PRUNING = 1, 2
+SEARCH_RIDGE, SEARCH_NO_STAGE_PRUNING, SEARCH_RAMP = 1, 2, 4
 SEARCH_COUNTERS = ("visited", "evaluated", "pruned_memory", "pruned_ridge", "pruned_bound")
 
 
 def search(prob, bound: int, first_row: int = 0, n_rows: Optional[int] = None, rows_per_chunk: int = 0,
-           ridge: bool = False, stage_pruning: bool = True, nthreads: Optional[int] = None):
+           ridge: bool = False, stage_pruning: bool = True, ramp: bool = False, nthreads: Optional[int] = None):
     """Pruned search (same semantics and counters as oracle.search.stage_search)."""
     st, keep = _problem(prob)
     n_rows = prob.A - first_row if n_rows is None else n_rows
     bi, bt = C.c_uint64(), C.c_uint32()
     cnt = (C.c_uint64 * 5)()
-    flags = (SEARCH_RIDGE if ridge else 0) | (0 if stage_pruning else SEARCH_NO_STAGE_PRUNING)
+    flags = (SEARCH_RIDGE if ridge else 0) | (0 if stage_pruning else SEARCH_NO_STAGE_PRUNING) | \
+        (SEARCH_RAMP if ramp else 0)
     rc = lib().oc_search(C.byref(st), first_row, n_rows, bound, rows_per_chunk, flags, C.byref(bi), C.byref(bt),
                          cnt, nthreads or default_threads())
     if rc != 0:

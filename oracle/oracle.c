@@ -580,7 +580,8 @@ static void *s_worker(void *arg) {
 
 /* Pruned search over rows [first_row, first_row + n_rows), chunks of
  * rows_per_chunk rows (0 = one chunk).  flags: bit 0 = layer-level (ridge)
- * pruning, bit 1 = no stage-level pruning.  Outputs the joint index
+ * pruning, bit 1 = no stage-level pruning, bit 2 = growing chunks (chunk k
+ * holds min(2^k, rows_per_chunk) rows).  Outputs the joint index
  * rank * A + row and the makespan (UINT64_MAX / UINT32_MAX if nothing
  * qualifies) and the counters visited, evaluated, pruned by memory, by the
  * ridge test and by the bound. */
@@ -599,8 +600,11 @@ int oc_search(const oc_problem *p, uint64_t first_row, uint64_t n_rows, uint32_t
     uint64_t bT = UINT64_MAX, bR = UINT64_MAX, bK = UINT64_MAX;
     uint64_t cnt[5] = {0, 0, 0, 0, 0};
     int err = 0;
-    for (uint64_t c0 = 0; c0 < n_rows && !err; c0 += rows_per_chunk) {
-        uint64_t c1 = c0 + rows_per_chunk < n_rows ? c0 + rows_per_chunk : n_rows;
+    uint64_t size = 1;
+    for (uint64_t c0 = 0, c1; c0 < n_rows && !err; c0 = c1) {
+        uint64_t step = (flags & 4u) && size < rows_per_chunk ? size : rows_per_chunk;
+        c1 = step < n_rows - c0 ? c0 + step : n_rows;
+        if (size < rows_per_chunk) size *= 2;
         uint64_t n = c1 - c0;
         int nt = (uint64_t)nthreads > n ? (int)n : nthreads;
         for (int t = 0; t < nt; ++t) {

@@ -26,6 +26,9 @@ numbering continues that of ``oracle/dag.py``):
   chunk prunes against b = min(bound, best makespan of the earlier chunks),
   fixed within the chunk, so every counter is deterministic for a given
   chunk size.  A chunk of one row updates the bound after every assignment.
+  With ``ramp`` the chunks grow: chunk k (k = 0, 1, ...) holds
+  min(2^k, rows_per_chunk) rows, so the bound tightens after the first row,
+  then after every doubling, while the later chunks stay large.
 * R18 (result and ties): the result is, among feasible (and, with the
   ridge filter, ridge-like) candidates whose makespan is <= bound, the
   one with the smallest makespan that comes first in the search's order
@@ -109,8 +112,21 @@ class _Ridge:
         self.last[t], self.falling[t] = saved
 
 
+def chunk_bounds(n_rows: int, chunk: int, ramp: bool):
+    """Row ranges [c0, c1) of the consecutive chunks (R17): `chunk` rows
+    each, or with `ramp` 1, 2, 4, ... rows until the size reaches `chunk`."""
+    out, c0, size = [], 0, 1
+    while c0 < n_rows:
+        step = min(size, chunk) if ramp else chunk
+        out.append((c0, min(n_rows, c0 + step)))
+        c0 += step
+        size *= 2
+    return out
+
+
 def stage_search(prob, bound: int, first_row: int = 0, n_rows: Optional[int] = None,
-                 rows_per_chunk: int = 0, ridge: bool = False, stage_pruning: bool = True):
+                 rows_per_chunk: int = 0, ridge: bool = False, stage_pruning: bool = True,
+                 ramp: bool = False):
     """The pruned search of Sec. 4.2.3 over assignment rows
     [first_row, first_row + n_rows) (readings R16-R19).  Returns a dict with
     `best` = (joint index, makespan) or None and the counters."""
@@ -125,10 +141,10 @@ def stage_search(prob, bound: int, first_row: int = 0, n_rows: Optional[int] = N
     chunk = n_rows if rows_per_chunk <= 0 else rows_per_chunk
     best = None            # (makespan, row, rank)
 
-    for c0 in range(0, n_rows, chunk):
+    for c0, c1 in chunk_bounds(n_rows, chunk, ramp):
         b = bound if best is None else min(bound, best[0])
         chunk_best = None
-        for a in range(first_row + c0, first_row + min(c0 + chunk, n_rows)):
+        for a in range(first_row + c0, first_row + c1):
             types = D.assignment_row(prob, a)
             rs = _Ridge(prob.T)
             cuts = []

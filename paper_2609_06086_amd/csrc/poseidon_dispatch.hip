@@ -49,20 +49,18 @@ __global__ __launch_bounds__(kBlock) void argmin_kernel(const uint32_t *T, const
 // totals are staged in LDS with coalesced loads (one padding word per 64
 // entries, so the per-thread runs of phase 2 start on different banks);
 // each thread then scans a contiguous run there, and the offsets go back
-// out coalesced.  A level piece has at most kSearchScanMax blocks, each
-// with at most 256 (L - 1) children, so every offset fits 32 bits.
+// out coalesced.  The kernel sits between the count and write launches of
+// every level and its time is the latency of its loads, so it reads nothing
+// else (the counters go to slots the host sums).  A level piece has at most
+// kSearchScanMax blocks, each with at most 256 (L - 1) children, so every
+// offset fits 32 bits.
 
 __device__ __forceinline__ uint32_t scan_pad(uint32_t b) { return b + (b >> 6); }
 
 __global__ __launch_bounds__(kBlock) void search_scan_kernel(SearchParams q, uint32_t nblk) {
     __shared__ uint32_t cnt[kSearchScanMax + kSearchScanMax / 64];
-    unsigned long long c[5] = {0, 0, 0, 0, 0};
-#pragma unroll 4
-    for (uint32_t b = threadIdx.x; b < nblk; b += kBlock) {
-        cnt[scan_pad(b)] = q.blk_tot[b];
-#pragma unroll
-        for (int k = 0; k < 5; ++k) c[k] += q.blk_cnt[(uint64_t)k * q.blk_stride + b];
-    }
+#pragma unroll 8
+    for (uint32_t b = threadIdx.x; b < nblk; b += kBlock) cnt[scan_pad(b)] = q.blk_tot[b];
     __syncthreads();
     const uint32_t per = (nblk + kBlock - 1) / kBlock;
     const uint32_t b0 = min(nblk, threadIdx.x * per), b1 = min(nblk, b0 + per);
@@ -76,17 +74,8 @@ __global__ __launch_bounds__(kBlock) void search_scan_kernel(SearchParams q, uin
         off += v;
     }
     __syncthreads();
-#pragma unroll 4
+#pragma unroll 8
     for (uint32_t b = threadIdx.x; b < nblk; b += kBlock) q.blk_off[b] = cnt[scan_pad(b)];
-    // the level's counters: one global atomic per counter
-    __shared__ unsigned long long sum[5];
-    if (threadIdx.x < 5) sum[threadIdx.x] = 0;
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < 5; ++k)
-        if (c[k]) atomicAdd(&sum[k], c[k]);
-    __syncthreads();
-    if (threadIdx.x < 5 && sum[threadIdx.x]) atomicAdd(&q.stats[threadIdx.x], sum[threadIdx.x]);
     if (threadIdx.x == 0) {
         q.blk_off[nblk] = total;
         *q.total = total;

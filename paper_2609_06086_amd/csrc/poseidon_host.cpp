@@ -869,13 +869,16 @@ constexpr uint64_t kSearchCap = 1ull << 22;            // nodes per frontier pie
 constexpr uint32_t kSearchBlk = kSearchCap / 256;      // blocks per piece
 static_assert(kSearchBlk <= pk::kSearchScanMax, "a level piece must fit the scan kernel");
 
-// state words: counters, leaf key, best, bound, then one child total per level
-enum { SW_STATS = 0, SW_ACC = 5, SW_BEST = 6, SW_BOUND = 9, SW_TOTAL = 10, SW_COUNT = SW_TOTAL + pk::kSMax };
+// state words: counters, leaf key, best, bound, one child total per level,
+// then the count kernels' counter slots
+enum {
+    SW_STATS = 0, SW_ACC = 5, SW_BEST = 6, SW_BOUND = 9, SW_TOTAL = 10, SW_PART = SW_TOTAL + pk::kSMax,
+    SW_COUNT = SW_PART + 5 * pk::kStatSlots
+};
 
 struct SearchWs {
     uint32_t *row[pk::kSMax], *codes[pk::kSMax];
     unsigned int *tot[pk::kSMax];
-    unsigned int *cnt[pk::kSMax];
     unsigned long long *off[pk::kSMax];
     uint16_t *node[pk::kSMax];
     unsigned long long *words;
@@ -892,7 +895,6 @@ SearchWs search_layout(poseidon_ctx *ctx, size_t *bytes) {
         w.row[l] = (uint32_t *)(b + o); o += kSearchCap * 4;
         w.codes[l] = (uint32_t *)(b + o); o += words * kSearchCap * 4;
         w.tot[l] = (unsigned int *)(b + o); o += (size_t)kSearchBlk * 4;
-        w.cnt[l] = (unsigned int *)(b + o); o += (size_t)kSearchBlk * 4 * 5;
         w.node[l] = (uint16_t *)(b + o); o += kSearchCap * 2;
         w.off[l] = (unsigned long long *)(b + o); o += ((size_t)kSearchBlk + 1) * 8;
     }
@@ -942,6 +944,8 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n, const unsigned long long
     q.level = x;
     const uint32_t grid = (uint32_t)((n + 255) / 256);
     const size_t lds = r.ctx->lds_bytes;
+    // the count and write kernels add three per-type tables (fb, mfb, hm)
+    const size_t lds_cw = lds + 3 * (size_t)r.ctx->T * (r.ctx->L + 1) * 4;
     if (x + 1 == S) {
         if (pk::launch_search(pk::kSearchOpLeaf, r.kp, q, grid, lds, r.st) != hipSuccess ||
             pk::launch_search(pk::kSearchOpMerge, r.kp, q, 1, 0, r.st) != hipSuccess)
@@ -950,8 +954,6 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n, const unsigned long long
     }
     q.blk_tot = r.w.tot[x];
     q.blk_off = r.w.off[x];
-    q.blk_cnt = r.w.cnt[x];
-    q.blk_stride = kSearchBlk;
     q.node_cnt = r.w.node[x];
     // a fused step writes level x + 2 (complete configurations when x = S - 3)
     const uint32_t step = search_fused(r.ctx, x) ? 2 : 1;
@@ -960,13 +962,13 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n, const unsigned long long
     q.out_codes = r.w.codes[x + step];
     q.out_cap = kSearchCap;
     q.total = r.w.words + SW_TOTAL + x;
-    if (pk::launch_search(pk::kSearchOpCount, r.kp, q, grid, lds, r.st) != hipSuccess ||
+    if (pk::launch_search(pk::kSearchOpCount, r.kp, q, grid, lds_cw, r.st) != hipSuccess ||
         pk::launch_search_scan(q, grid, r.st) != hipSuccess)
         return POSEIDON_E_DEVICE;
     const uint64_t most = step == 2 ? (uint64_t)(r.ctx->L - 1) * (r.ctx->L - 1) : r.ctx->L - 1;
     if (n * most <= kSearchCap) {
         q.blk_base = 0;
-        if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, grid, lds, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
+        if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, grid, lds_cw, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
         return search_expand(r, x + step, n * most, q.total);
     }
     unsigned long long total = 0;
@@ -975,7 +977,7 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n, const unsigned long long
     if (total == 0) return POSEIDON_OK;
     if (total <= kSearchCap) {
         q.blk_base = 0;
-        if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, grid, lds, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
+        if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, grid, lds_cw, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
         return search_expand(r, x + step, total, nullptr);
     }
     // more children than a level holds: write and expand them in pieces of
@@ -990,7 +992,7 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n, const unsigned long long
         uint32_t b1 = b0 + 1;
         while (b1 < grid && off[b1 + 1] - off[b0] <= kSearchCap) ++b1;
         q.blk_base = b0;
-        if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, b1 - b0, lds, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
+        if (pk::launch_search(pk::kSearchOpWrite, r.kp, q, b1 - b0, lds_cw, r.st) != hipSuccess) return POSEIDON_E_DEVICE;
         if (off[b1] > off[b0]) {
             rc = search_expand(r, x + step, off[b1] - off[b0], nullptr);
             if (rc != POSEIDON_OK) return rc;
@@ -1005,7 +1007,8 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n, const unsigned long long
 extern "C" int poseidon_search(poseidon_ctx *ctx, uint64_t first_row, uint64_t n_rows, uint32_t bound,
                                uint64_t rows_per_chunk, uint32_t flags, poseidon_best *best_out,
                                poseidon_search_stats *stats_out, void *hip_stream) {
-    if (!ctx || (flags & ~(uint32_t)(POSEIDON_SEARCH_RIDGE | POSEIDON_SEARCH_NO_STAGE_PRUNING))) return POSEIDON_E_INVAL;
+    if (!ctx || (flags & ~(uint32_t)(POSEIDON_SEARCH_RIDGE | POSEIDON_SEARCH_NO_STAGE_PRUNING | POSEIDON_SEARCH_RAMP)))
+        return POSEIDON_E_INVAL;
     if (ctx->base.sched == POSEIDON_SCHEDULE_INTERLEAVED_1F1B) return POSEIDON_E_INVAL;
     if (first_row > ctx->A || n_rows > ctx->A - first_row) return POSEIDON_E_INVAL;
     hipStream_t st = (hipStream_t)hip_stream;
@@ -1028,16 +1031,21 @@ extern "C" int poseidon_search(poseidon_ctx *ctx, uint64_t first_row, uint64_t n
     memset(&r.q, 0, sizeof(r.q));
     r.q.flags = flags;
     r.q.stats = r.w.words + SW_STATS;
+    r.q.stats_part = r.w.words + SW_PART;
     r.q.acc = r.w.words + SW_ACC;
     r.q.best = r.w.words + SW_BEST;
     r.q.bound = (uint32_t *)(r.w.words + SW_BOUND);
     if (pk::launch_fill(r.q.stats, 5, 0ull, st) != hipSuccess ||
+        pk::launch_fill(r.q.stats_part, 5 * pk::kStatSlots, 0ull, st) != hipSuccess ||
         pk::launch_fill(r.q.acc, 4, ~0ull, st) != hipSuccess)
         return POSEIDON_E_DEVICE;
     const uint64_t chunk = rows_per_chunk ? rows_per_chunk : (n_rows ? n_rows : 1);
+    const bool ramp = (flags & POSEIDON_SEARCH_RAMP) != 0;
     int rc = POSEIDON_OK;
-    for (uint64_t c0 = 0; c0 < n_rows && rc == POSEIDON_OK; c0 += chunk) {
-        const uint64_t c1 = std::min(n_rows, c0 + chunk);
+    uint64_t size = 1;   // with ramp: the next chunk's rows, doubling up to chunk
+    for (uint64_t c0 = 0, c1; c0 < n_rows && rc == POSEIDON_OK; c0 = c1) {
+        c1 = c0 + std::min(n_rows - c0, ramp ? std::min(size, chunk) : chunk);
+        if (size < chunk) size *= 2;
         // the chunk prunes against min(bound, best of the earlier chunks)
         if (pk::launch_search_bound(r.q, bound, st) != hipSuccess) return POSEIDON_E_DEVICE;
         for (uint64_t r0 = c0; r0 < c1 && rc == POSEIDON_OK; r0 += kSearchCap) {
@@ -1058,6 +1066,8 @@ extern "C" int poseidon_search(poseidon_ctx *ctx, uint64_t first_row, uint64_t n
     if (hipMemcpyAsync(w, r.w.words, sizeof(w), hipMemcpyDeviceToHost, st) != hipSuccess ||
         hipStreamSynchronize(st) != hipSuccess)
         return POSEIDON_E_DEVICE;
+    for (uint32_t k = 0; k < 5; ++k)
+        for (uint32_t j = 0; j < pk::kStatSlots; ++j) w[SW_STATS + k] += w[SW_PART + k * pk::kStatSlots + j];
     if (stats_out) {
         stats_out->visited = w[SW_STATS];
         stats_out->evaluated = w[SW_STATS + 1];

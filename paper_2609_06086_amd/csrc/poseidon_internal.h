@@ -82,6 +82,10 @@ struct KParams {
 };
 
 // Pruned search (Sec. 4.2.3): one piece of one frontier level.
+// count-kernel blocks spread their counters over this many slots, so that
+// no single address takes one atomic per block
+constexpr uint32_t kStatSlots = 64;
+
 struct SearchParams {
     const uint32_t *in_row;           // [in_cap] assignment row of each node
     const uint32_t *in_codes;         // [words][in_cap] cut codes, cuts 1..level set
@@ -94,14 +98,14 @@ struct SearchParams {
     uint64_t out_cap;
     unsigned int *blk_tot;            // children per block (count kernel)
     unsigned long long *blk_off;      // exclusive offsets, [nblk] = total (scan kernel)
-    unsigned int *blk_cnt;            // [5][blk_stride] per-block counters (count kernel)
     uint16_t *node_cnt;               // children each node keeps (count kernel -> write kernel)
-    uint64_t blk_stride;
     uint32_t blk_base;                // first block a write launch covers
     uint32_t flags;                   // kSearchRidge | kSearchNoStage
     uint32_t fused;                   // level S-3 expanded together with the level that fixes the last cut
     uint32_t *bound;                  // the current chunk's bound
     unsigned long long *stats;        // visited, evaluated, pruned by memory / ridge / bound
+    unsigned long long *stats_part;   // [5][kStatSlots] the same counters from the count kernels:
+                                      // block b adds to slot b % kStatSlots (the host sums them)
     unsigned long long *acc;          // best (T << 32 | position) of a leaf piece
     unsigned long long *best;         // makespan, row, composition rank of the best so far
     unsigned long long *total;        // children of the scanned level piece (one word per level)

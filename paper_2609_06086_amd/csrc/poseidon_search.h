@@ -157,6 +157,57 @@ __device__ __forceinline__ int search_try(const KParams &p, const Lds &tab, cons
     return 0;
 }
 
+// Per-type tables of the stage tests, built in LDS behind the stage tables
+// by the count and write kernels: fb = prefix fwd + prefix bwd, mfb = M fb
+// (below 2^31 like every path weight, checked at load), and hm[t][lo] = the
+// largest h with layers [lo, h) within type t's memory cap.  Without
+// all-reduce times a stage's Eq. 2 test is then one compare, mfb[h] against
+// a per-node threshold, and its memory test a cap on the range.
+struct SearchTab {
+    const uint32_t *fb, *mfb, *hm;
+};
+
+// LDS bytes of the stage tables (the layout of stage_tables), where the
+// search tables start; the host sizes the launch the same way.
+__device__ __forceinline__ uint32_t search_tab_offset(const KParams &p) {
+    const uint32_t n = p.T * (p.L + 1);
+    return (n * 8 + (p.L + 1) * 4 + p.T * 4 + (p.has_ar ? n * 4 : 0) + 15) & ~15u;
+}
+
+__device__ __forceinline__ SearchTab search_tables(const KParams &p, const Lds &tab, unsigned char *smem) {
+    const uint32_t row = p.L + 1, n = p.T * row;
+    uint32_t *fb = reinterpret_cast<uint32_t *>(smem + search_tab_offset(p)), *mfb = fb + n, *hm = mfb + n;
+    for (uint32_t i = threadIdx.x; i < n; i += kBlock) {
+        const uint64_t c = tab.cost[i];
+        const uint32_t v = (uint32_t)c + (uint32_t)(c >> 32);
+        fb[i] = v;
+        mfb[i] = p.M * v;
+        const uint32_t t = i / row, lo = i - t * row;
+        // pm only grows: the largest h that fits, by halving steps from lo
+        uint32_t h = lo;
+        for (uint32_t st = 256; st; st >>= 1)
+            if (h + st <= p.L && tab.pm[h + st] - tab.pm[lo] <= tab.cap[t]) h += st;
+        hm[i] = h;
+    }
+    __syncthreads();
+    return SearchTab{fb, mfb, hm};
+}
+
+// The rule that ended a node's accepted range of k end points (0: it ran to
+// hmax): the first test end point lo+k+1 fails, in the order memory, ridge,
+// bound.  Without all-reduce times the memory and ridge outcomes are range
+// limits, and a maximal range that neither ended must have met the bound.
+__device__ __forceinline__ int search_stop(const KParams &p, const Lds &tab, const SearchTab &sx,
+                                           const SearchNode &n, uint32_t x, uint32_t k, uint32_t hmax,
+                                           uint32_t flags, uint32_t bound) {
+    const uint32_t h = n.lo + k + 1;
+    if (h > hmax) return 0;
+    if (p.has_ar) return search_try(p, tab, n, x, h, flags, bound);
+    if (h > sx.hm[n.t * (p.L + 1) + n.lo]) return 1;
+    if ((flags & kSearchRidge) && n.last_l >= 0 && n.falling && (int32_t)(h - n.lo) > n.last_l) return 2;
+    return 3;
+}
+
 // Outcomes of the last-stage test of the children of one node.
 struct LastStage {
     uint32_t pass = 0, mem = 0, ridge = 0, bound = 0;
@@ -168,11 +219,33 @@ struct LastStage {
 // and g(S_{x+1}) only grow with it; a falling type's ridge test fails for
 // every count above its last one), so k is found by a binary search over
 // the end points instead of trying them one by one.
-__device__ __forceinline__ uint32_t search_accepted(const KParams &p, const Lds &tab, const SearchNode &n,
-                                                    uint32_t x, uint32_t hmax, uint32_t flags, uint32_t bound) {
+__device__ __forceinline__ uint32_t search_accepted(const KParams &p, const Lds &tab, const SearchTab &sx,
+                                                    const SearchNode &n, uint32_t x, uint32_t hmax, uint32_t flags,
+                                                    uint32_t bound) {
     const uint32_t row_len = p.L + 1;
     uint32_t len = hmax - n.lo;
     if ((flags & kSearchRidge) && n.last_l >= 0 && n.falling) len = min(len, (uint32_t)n.last_l);
+    const int H = (int)decode_levels(p.L);   // (uniform: the steps above it are skipped by scalar branches)
+    if (!p.has_ar) {
+        // memory caps the range; Eq. 2, pre_f + M (fb[h] - fb[lo]) + inn <= bound
+        // with inn = inner + last_b (0 for the first stage), is mfb[h] <= thr
+        const uint32_t *mf = sx.mfb + n.t * row_len;
+        len = min(len, sx.hm[n.t * row_len + n.lo] - n.lo);
+        if (flags & kSearchNoStage) return len;
+        const int64_t thr64 = (int64_t)bound + mf[n.lo] - n.pre_f - (x == 0 ? 0u : n.inner + n.last_b);
+        const int32_t thr = thr64 > INT32_MAX ? INT32_MAX : thr64 < 0 ? -1 : (int32_t)thr64;
+        // each step loads (an in-range entry) and combines its tests without
+        // branches, so the wave never splits over them
+        uint32_t k = 0;
+#pragma unroll
+        for (int b = 7; b >= 0; --b) {
+            if (b >= H) continue;
+            const uint32_t t = k + (1u << b);
+            const int32_t v = (int32_t)mf[n.lo + min(t, len)];
+            k = ((t <= len) & (v <= thr)) ? t : k;
+        }
+        return k;
+    }
     const uint64_t *ct = tab.cost + n.t * row_len;
     const uint64_t cl = ct[n.lo];
     const uint32_t pml = tab.pm[n.lo], capt = tab.cap[n.t];
@@ -180,7 +253,6 @@ __device__ __forceinline__ uint32_t search_accepted(const KParams &p, const Lds 
     const uint32_t dl = p.has_ar ? pdt[n.lo] : 0u;
     const bool stage = !(flags & kSearchNoStage);
     const uint32_t carry = n.inner + n.last_b;
-    const int H = (int)decode_levels(p.L);   // (uniform: the steps above it are skipped by scalar branches)
     uint32_t k = 0;
 #pragma unroll
     for (int b = 7; b >= 0; --b) {
@@ -228,8 +300,9 @@ __device__ __forceinline__ void search_write_child(const SearchParams &q, uint64
 }
 
 template <int S, bool WRITE>
-__device__ __forceinline__ uint32_t search_last_children(const KParams &p, const Lds &tab, const SearchNode &n,
-                                                         uint32_t x, uint32_t k, uint32_t flags, uint32_t bound,
+__device__ __forceinline__ uint32_t search_last_children(const KParams &p, const Lds &tab, const SearchTab &sx,
+                                                         const SearchNode &n, uint32_t x, uint32_t k, uint32_t flags,
+                                                         uint32_t bound,
                                                          LastStage &lp, const SearchParams &q, uint64_t base,
                                                          const uint32_t (&w)[Codes<S>::kWords]) {
     const uint32_t row_len = p.L + 1;
@@ -259,14 +332,13 @@ __device__ __forceinline__ uint32_t search_last_children(const KParams &p, const
         // Eq. 2: the end points below g0 fail
         uint32_t g0 = r0;
         if (stage && r0 <= h1) {
-            const uint64_t *ct = tab.cost + n.t * row_len, *cs = tab.cost + n.tS * row_len;
-            const uint64_t cl = ct[n.lo], cL = cs[p.L];
-            // g(hi) = C + G(hi) > bound  <=>  G(hi) > bound - C.  Every prefix time
-            // and M times any type's prefix stays below 2^31 (checked at load), so
-            // G fits 32 bits; the threshold is clamped to that range
-            const int64_t C = (int64_t)n.pre_f - (int64_t)(uint32_t)cl - (int64_t)(cl >> 32) +
-                              (x == 0 ? 0 : (int64_t)(n.inner + n.last_b)) +
-                              (int64_t)p.M * ((int64_t)(uint32_t)cL + (int64_t)(cL >> 32));
+            const uint32_t *ft = sx.fb + n.t * row_len, *ms = sx.mfb + n.tS * row_len;
+            // g(hi) = C + G(hi) > bound  <=>  G(hi) > bound - C, with
+            // G(hi) = fb_t[hi] - mfb_tS[hi].  Every prefix time and M times any
+            // type's prefix stays below 2^31 (checked at load), so G fits 32
+            // bits; the threshold is clamped to that range
+            const int64_t C = (int64_t)n.pre_f - (int64_t)ft[n.lo] + (x == 0 ? 0 : (int64_t)(n.inner + n.last_b)) +
+                              (int64_t)ms[p.L];
             const int64_t thr64 = (int64_t)bound - C;
             const int32_t thr = thr64 > INT32_MAX ? INT32_MAX : thr64 < INT32_MIN ? INT32_MIN : (int32_t)thr64;
             const bool none = thr64 < INT32_MIN;   // every G(hi) > thr (G > -2^31 always)
@@ -278,10 +350,8 @@ __device__ __forceinline__ uint32_t search_last_children(const KParams &p, const
                 if (b >= H) continue;
                 const uint32_t t = j + (1u << b);
                 const uint32_t h = r0 + min(t, len) - 1;
-                const uint64_t ch = ct[h], sh = cs[h];
-                const int32_t G = (int32_t)((uint32_t)ch + (uint32_t)(ch >> 32)) -
-                                  (int32_t)(p.M * ((uint32_t)sh + (uint32_t)(sh >> 32)));
-                j = (t <= len && (none || G > thr)) ? t : j;
+                const int32_t G = (int32_t)ft[h] - (int32_t)ms[h];
+                j = ((t <= len) & (none | (G > thr))) ? t : j;
             }
             g0 = r0 + j;
             lp.bound += j;
@@ -347,6 +417,8 @@ __device__ __forceinline__ void search_flush(const SearchParams &q, unsigned int
     if (threadIdx.x < 5 && c[threadIdx.x]) atomicAdd(&q.stats[threadIdx.x], (unsigned long long)c[threadIdx.x]);
 }
 
+// The count kernel's counters: summed over the block in LDS, then one
+// atomic per counter into the block's slot of q.stats_part.
 __device__ __forceinline__ void search_block_counts(const SearchParams &q, unsigned int visited, unsigned int evaluated,
                                                     unsigned int mem, unsigned int ridge, unsigned int bound) {
     __shared__ unsigned int c[5];
@@ -358,7 +430,8 @@ __device__ __forceinline__ void search_block_counts(const SearchParams &q, unsig
     if (ridge) atomicAdd(&c[3], ridge);
     if (bound) atomicAdd(&c[4], bound);
     __syncthreads();
-    if (threadIdx.x < 5) q.blk_cnt[(uint64_t)threadIdx.x * q.blk_stride + blockIdx.x] = c[threadIdx.x];
+    if (threadIdx.x < 5 && c[threadIdx.x])
+        atomicAdd(&q.stats_part[threadIdx.x * kStatSlots + blockIdx.x % kStatSlots], (unsigned long long)c[threadIdx.x]);
 }
 
 template <int S>
@@ -381,12 +454,12 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
     extern __shared__ __align__(16) unsigned char smem[];
     const uint32_t n_in = search_n_in(q);
     if (blockIdx.x * kBlock >= n_in) {
-        // a block past the level's nodes (grid from an upper bound): zero totals
-        if (threadIdx.x < 5) q.blk_cnt[(uint64_t)threadIdx.x * q.blk_stride + blockIdx.x] = 0;
+        // a block past the level's nodes (grid from an upper bound): zero total
         if (threadIdx.x == 0) q.blk_tot[blockIdx.x] = 0;
         return;
     }
     const Lds tab = stage_tables(p, smem);
+    const SearchTab sx = search_tables(p, tab, smem);
     const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
     const bool active = i < n_in;
     const uint32_t bound = *q.bound;
@@ -399,9 +472,9 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
         const uint32_t x = q.level;
         const SearchNode n = search_node<S>(p, tab, row, w, x, ty, cut);
         const uint32_t hmax = p.L - (S - 1 - x);   // every later stage keeps one layer
-        const uint32_t acc = search_accepted(p, tab, n, x, hmax, q.flags, bound);
+        const uint32_t acc = search_accepted(p, tab, sx, n, x, hmax, q.flags, bound);
         // the rule that stopped the range (0: it ran to its structural end)
-        const int why = n.lo + acc < hmax ? search_try(p, tab, n, x, n.lo + acc + 1, q.flags, bound) : 0;
+        const int why = search_stop(p, tab, sx, n, x, acc, hmax, q.flags, bound);
         visited = acc;
         why_mem = why == 1;
         why_ridge = why == 2;
@@ -412,16 +485,16 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
             // stage are kept (complete configurations)
             for (uint32_t c = n.lo + 1; c <= n.lo + acc; ++c) {
                 const SearchNode m = search_child(p, tab, n, x, c);
-                const uint32_t acc2 = search_accepted(p, tab, m, x + 1, p.L - 1, q.flags, bound);
-                const int why2 = m.lo + acc2 < p.L - 1 ? search_try(p, tab, m, x + 1, m.lo + acc2 + 1, q.flags, bound) : 0;
+                const uint32_t acc2 = search_accepted(p, tab, sx, m, x + 1, p.L - 1, q.flags, bound);
+                const int why2 = search_stop(p, tab, sx, m, x + 1, acc2, p.L - 1, q.flags, bound);
                 visited += acc2;
                 why_mem += why2 == 1;
                 why_ridge += why2 == 2;
                 why_bound += why2 == 3;
-                cnt += search_last_children<S, false>(p, tab, m, x + 1, acc2, q.flags, bound, lp, q, 0, w);
+                cnt += search_last_children<S, false>(p, tab, sx, m, x + 1, acc2, q.flags, bound, lp, q, 0, w);
             }
         } else {
-            cnt = x + 2 == (uint32_t)S ? search_last_children<S, false>(p, tab, n, x, acc, q.flags, bound, lp, q, 0, w)
+            cnt = x + 2 == (uint32_t)S ? search_last_children<S, false>(p, tab, sx, n, x, acc, q.flags, bound, lp, q, 0, w)
                                        : acc;
         }
         q.node_cnt[i] = (uint16_t)cnt;   // at most (L - 1)^2 < 2^16 children (fused), else L - 1
@@ -433,8 +506,6 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
     if ((threadIdx.x & 63) == 0 && wsum) atomicAdd(&tot, wsum);
     // a child that completes the configuration and passes the last stage
     // counts as visited twice (its stage x+1 and its stage S) and evaluated.
-    // The block's counts go to per-block slots that the scan kernel sums
-    // (one global atomic per counter and launch instead of per block).
     search_block_counts(q, visited + lp.pass, lp.pass, why_mem + lp.mem, why_ridge + lp.ridge, why_bound + lp.bound);
     if (threadIdx.x == 0) q.blk_tot[blockIdx.x] = tot;
 }
@@ -448,6 +519,7 @@ __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchP
     const uint32_t n_in = search_n_in(q);
     if (blk * kBlock >= n_in) return;   // past the level's nodes
     const Lds tab = stage_tables(p, smem);
+    const SearchTab sx = search_tables(p, tab, smem);
     const uint32_t i = blk * kBlock + threadIdx.x;
     const bool active = i < n_in;
     const uint32_t bound = *q.bound;
@@ -466,21 +538,21 @@ __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchP
             // the complete configurations under each child, child by child
             LastStage lp;
             const SearchNode n = search_node<S>(p, tab, row, w, x, ty, cut);
-            const uint32_t acc = search_accepted(p, tab, n, x, p.L - (S - 1 - x), q.flags, bound);
+            const uint32_t acc = search_accepted(p, tab, sx, n, x, p.L - (S - 1 - x), q.flags, bound);
             uint64_t o = base;
             for (uint32_t c = n.lo + 1; c <= n.lo + acc; ++c) {
                 const SearchNode m = search_child(p, tab, n, x, c);
-                const uint32_t acc2 = search_accepted(p, tab, m, x + 1, p.L - 1, q.flags, bound);
+                const uint32_t acc2 = search_accepted(p, tab, sx, m, x + 1, p.L - 1, q.flags, bound);
                 uint32_t wc[NW];
 #pragma unroll
                 for (int k = 0; k < NW; ++k) wc[k] = (uint32_t)k == (x >> 2) ? (w[k] | (c << (8 * (x & 3)))) : w[k];
-                o += search_last_children<S, true>(p, tab, m, x + 1, acc2, q.flags, bound, lp, q, o, wc);
+                o += search_last_children<S, true>(p, tab, sx, m, x + 1, acc2, q.flags, bound, lp, q, o, wc);
             }
         } else if (x + 2 == (uint32_t)S) {
             LastStage lp;
             const SearchNode n = search_node<S>(p, tab, row, w, x, ty, cut);
-            const uint32_t acc = search_accepted(p, tab, n, x, p.L - (S - 1 - x), q.flags, bound);
-            search_last_children<S, true>(p, tab, n, x, acc, q.flags, bound, lp, q, base, w);
+            const uint32_t acc = search_accepted(p, tab, sx, n, x, p.L - (S - 1 - x), q.flags, bound);
+            search_last_children<S, true>(p, tab, sx, n, x, acc, q.flags, bound, lp, q, base, w);
         } else {
             // every accepted choice is a child: c_{x+1} = lo+1 .. lo+cnt
             uint32_t lo = 0;

@@ -25,7 +25,7 @@ POSEIDON_E_RANGE = -2
 POSEIDON_E_DEVICE = -3
 POSEIDON_E_NOMEM = -4
 SCHEDULE_1F1B, SCHEDULE_EAGER_1F1B, SCHEDULE_INTERLEAVED_1F1B = 0, 1, 2
-SEARCH_RIDGE, SEARCH_NO_STAGE_PRUNING = 1, 2
+SEARCH_RIDGE, SEARCH_NO_STAGE_PRUNING, SEARCH_RAMP = 1, 2, 4
 S_MAX, L_MAX, T_MAX = 16, 256, 8
 
 
@@ -268,11 +268,14 @@ def poseidon_argmin(ctx: Context, makespan, feasible_bits=None, *, count: Option
 
 
 def poseidon_search(ctx: Context, bound: int = 2 ** 31 - 1, *, first_row: int = 0, n_rows: Optional[int] = None,
-                    rows_per_chunk: int = 0, ridge: bool = False, stage_pruning: bool = True, stream=None):
+                    rows_per_chunk: int = 0, ridge: bool = False, stage_pruning: bool = True, ramp: bool = False,
+                    stream=None):
     """Pruned configuration search over assignment rows; returns (Best, SearchStats).
-    Best.index is the joint index rank * A + row."""
+    Best.index is the joint index rank * A + row.  With ramp the chunks grow
+    1, 2, 4, ... rows up to rows_per_chunk."""
     n = ctx.A - first_row if n_rows is None else n_rows
-    flags = (SEARCH_RIDGE if ridge else 0) | (0 if stage_pruning else SEARCH_NO_STAGE_PRUNING)
+    flags = (SEARCH_RIDGE if ridge else 0) | (0 if stage_pruning else SEARCH_NO_STAGE_PRUNING) | \
+        (SEARCH_RAMP if ramp else 0)
     b, s = _Best(), _SearchStats()
     rc = lib().poseidon_search(ctx.handle, int(first_row), int(n), int(bound), int(rows_per_chunk), flags,
                                C.byref(b), C.byref(s), _stream(stream))

@@ -56,7 +56,7 @@ def test_search_random_problems(dev):
             To, fo = coracle.evaluate(prob, W.random_candidates(rng, prob, 200))
             bound = int(To[fo].min()) if fo.any() else 2 ** 31 - 1
         for kw in (dict(), dict(rows_per_chunk=1), dict(ridge=True, rows_per_chunk=3),
-                   dict(stage_pruning=False)):
+                   dict(stage_pruning=False), dict(ramp=True, rows_per_chunk=4)):
             check(prob, bound, dev, **kw)
 
 
@@ -131,7 +131,8 @@ def test_search_frontier_pieces(dev):
 
 def test_search_workload4_rows(dev):
     """The 8-stage, 3-type workload: 48 assignment rows, bound from its 500
-    warm-up samples, chunks of 16 rows, with and without the ridge filter."""
+    warm-up samples, chunks of 16 rows, with and without the ridge filter, and
+    in chunks growing from one row to 16."""
     wl = W.workload(4)
     c = wl.cands
     To, fo = coracle.evaluate(wl.problem, W.Candidates(comp_rank=c.comp_rank[:500].copy(),
@@ -139,6 +140,7 @@ def test_search_workload4_rows(dev):
     bound = int(To[fo].min())
     check(wl.problem, bound, dev, first_row=0, n_rows=48, rows_per_chunk=16)
     check(wl.problem, bound, dev, first_row=3000, n_rows=48, rows_per_chunk=16, ridge=True)
+    check(wl.problem, bound, dev, first_row=100, n_rows=40, rows_per_chunk=16, ramp=True)
 
 
 def test_search_workload6_eager_rows(dev):

@@ -189,6 +189,54 @@ def test_c_search_equals_python_search():
                 assert a == b
 
 
+def test_ramp_chunks_cover_the_rows_once_in_doubling_sizes():
+    for n in (0, 1, 2, 7, 64, 100):
+        for rpc in (1, 3, 8, 1000):
+            b = SR.chunk_bounds(n, rpc, True)
+            assert [c0 for c0, _ in b] == ([0] + [c1 for _, c1 in b][:-1] if n else [])
+            assert (b[-1][1] if b else 0) == n
+            sizes = [c1 - c0 for c0, c1 in b]
+            for k, sz in enumerate(sizes[:-1]):
+                assert sz == min(2 ** k, rpc)
+            assert SR.chunk_bounds(n, rpc, False) == [(c0, min(n, c0 + rpc)) for c0 in range(0, n, rpc)]
+
+
+def test_ramp_search_is_the_chain_of_its_chunks():
+    """R17 with growing chunks: the search equals one fixed-chunk search per
+    chunk, each against min(bound, best of the chunks before), with the
+    counters summed and the first strictly better result kept."""
+    rng = np.random.default_rng(36)
+    for trial in range(12):
+        S = int(rng.integers(1, 5))
+        L = S + int(rng.integers(0, 7))
+        M = int(rng.integers(1, 9))
+        T = int(rng.integers(2, 4))
+        prob = W.random_problem(rng, L, S, M, T, mem_hi=30, cap=int(rng.integers(30, 150)),
+                                assign_rows=13)
+        prob.schedule = trial % 2
+        bound = 2 ** 31 if trial % 3 == 0 else int(coracle.evaluate(
+            prob, W.random_candidates(rng, prob, 30))[0].min())
+        for rpc, ridge in ((4, False), (16, True), (0, False)):
+            got = SR.stage_search(prob, bound, rows_per_chunk=rpc, ridge=ridge, ramp=True)
+            want = dict(visited=0, evaluated=0, pruned_memory=0, pruned_ridge=0, pruned_bound=0)
+            best = None
+            size, c0 = 1, 0
+            cap = rpc if rpc > 0 else prob.A
+            while c0 < prob.A:
+                n = min(size, cap, prob.A - c0)
+                b = bound if best is None else min(bound, best[1])
+                r = SR.stage_search(prob, b, first_row=c0, n_rows=n, ridge=ridge)
+                for k in want:
+                    want[k] += r[k]
+                if r["best"] is not None and (best is None or r["best"][1] < best[1]):
+                    best = r["best"]
+                c0 += n
+                size *= 2
+            want["best"] = best
+            assert got == want
+            assert coracle.search(prob, bound, rows_per_chunk=rpc, ridge=ridge, ramp=True, nthreads=3) == got
+
+
 def test_evaluated_candidates_are_those_within_eq2_of_the_bound():
     """With a fixed bound (one chunk) the search evaluates exactly the
     feasible candidates whose Eq. 2 bound max_x g(S_x) is <= b: every prefix
