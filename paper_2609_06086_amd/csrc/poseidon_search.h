@@ -46,7 +46,7 @@ struct SearchNode {
 };
 
 // Prefix quantities of a node at level x (stages 1..x fixed).
-template <int S>
+template <int S, bool AR>
 __device__ __forceinline__ SearchNode search_node(const KParams &p, const Lds &tab, uint32_t row,
                                                   const uint32_t (&w)[Codes<S>::kWords], uint32_t x,
                                                   uint32_t (&ty)[S], uint32_t (&cut)[S + 1]) {
@@ -85,7 +85,7 @@ __device__ __forceinline__ SearchNode search_node(const KParams &p, const Lds &t
             const uint64_t *c = tab.cost + ty[s] * row_len;
             const uint64_t hi = c[cut[s + 1]], lo = c[cut[s]];
             const uint32_t f = (uint32_t)hi - (uint32_t)lo, b = (uint32_t)(hi >> 32) - (uint32_t)(lo >> 32);
-            const uint32_t d = p.has_ar ? tab.pd[ty[s] * row_len + cut[s + 1]] - tab.pd[ty[s] * row_len + cut[s]] : 0u;
+            const uint32_t d = AR ? tab.pd[ty[s] * row_len + cut[s + 1]] - tab.pd[ty[s] * row_len + cut[s]] : 0u;
             n.inner = s == 0 ? d : max(n.inner + n.last_b, d);
             n.pre_f += f;
             n.last_b = b;
@@ -111,13 +111,14 @@ __device__ __forceinline__ SearchNode search_node(const KParams &p, const Lds &t
 // quantities at level x+1, extended by that one stage (the type of its
 // stage x+3 is not tracked: used for the level that fixes the last cut,
 // whose children are complete).
+template <bool AR>
 __device__ __forceinline__ SearchNode search_child(const KParams &p, const Lds &tab, const SearchNode &n, uint32_t x,
                                                    uint32_t c) {
     const uint32_t row_len = p.L + 1;
     const uint64_t *ct = tab.cost + n.t * row_len;
     const uint64_t ch = ct[c], cl = ct[n.lo];
     const uint32_t f = (uint32_t)ch - (uint32_t)cl, b = (uint32_t)(ch >> 32) - (uint32_t)(cl >> 32);
-    const uint32_t d = p.has_ar ? tab.pd[n.t * row_len + c] - tab.pd[n.t * row_len + n.lo] : 0u;
+    const uint32_t d = AR ? tab.pd[n.t * row_len + c] - tab.pd[n.t * row_len + n.lo] : 0u;
     const int32_t l = (int32_t)(c - n.lo);
     SearchNode m = n;
     m.lo = c;
@@ -139,6 +140,7 @@ __device__ __forceinline__ SearchNode search_child(const KParams &p, const Lds &
 }
 
 // Outcome of trying stage x+1 = [lo, hi): 0 accepted, 1 memory, 2 ridge, 3 bound.
+template <bool AR>
 __device__ __forceinline__ int search_try(const KParams &p, const Lds &tab, const SearchNode &n, uint32_t x,
                                           uint32_t hi, uint32_t flags, uint32_t bound) {
     const uint32_t row_len = p.L + 1;
@@ -149,7 +151,7 @@ __device__ __forceinline__ int search_try(const KParams &p, const Lds &tab, cons
         const uint64_t *c = tab.cost + n.t * row_len;
         const uint64_t ch = c[hi], cl = c[n.lo];
         const uint32_t f = (uint32_t)ch - (uint32_t)cl, b = (uint32_t)(ch >> 32) - (uint32_t)(cl >> 32);
-        const uint32_t d = p.has_ar ? tab.pd[n.t * row_len + hi] - tab.pd[n.t * row_len + n.lo] : 0u;
+        const uint32_t d = AR ? tab.pd[n.t * row_len + hi] - tab.pd[n.t * row_len + n.lo] : 0u;
         const uint32_t inn = x == 0 ? d : max(n.inner + n.last_b, d);
         // Eq. 2: g(S_{x+1}) = sum_{i<=x} F_i + M (F_{x+1} + B_{x+1}) + inner
         if (n.pre_f + p.M * (f + b) + inn > bound) return 3;
@@ -197,12 +199,13 @@ __device__ __forceinline__ SearchTab search_tables(const KParams &p, const Lds &
 // hmax): the first test end point lo+k+1 fails, in the order memory, ridge,
 // bound.  Without all-reduce times the memory and ridge outcomes are range
 // limits, and a maximal range that neither ended must have met the bound.
+template <bool AR>
 __device__ __forceinline__ int search_stop(const KParams &p, const Lds &tab, const SearchTab &sx,
                                            const SearchNode &n, uint32_t x, uint32_t k, uint32_t hmax,
                                            uint32_t flags, uint32_t bound) {
     const uint32_t h = n.lo + k + 1;
     if (h > hmax) return 0;
-    if (p.has_ar) return search_try(p, tab, n, x, h, flags, bound);
+    if (AR) return search_try<AR>(p, tab, n, x, h, flags, bound);
     if (h > sx.hm[n.t * (p.L + 1) + n.lo]) return 1;
     if ((flags & kSearchRidge) && n.last_l >= 0 && n.falling && (int32_t)(h - n.lo) > n.last_l) return 2;
     return 3;
@@ -219,6 +222,7 @@ struct LastStage {
 // and g(S_{x+1}) only grow with it; a falling type's ridge test fails for
 // every count above its last one), so k is found by a binary search over
 // the end points instead of trying them one by one.
+template <bool AR>
 __device__ __forceinline__ uint32_t search_accepted(const KParams &p, const Lds &tab, const SearchTab &sx,
                                                     const SearchNode &n, uint32_t x, uint32_t hmax, uint32_t flags,
                                                     uint32_t bound) {
@@ -226,7 +230,7 @@ __device__ __forceinline__ uint32_t search_accepted(const KParams &p, const Lds 
     uint32_t len = hmax - n.lo;
     if ((flags & kSearchRidge) && n.last_l >= 0 && n.falling) len = min(len, (uint32_t)n.last_l);
     const int H = (int)decode_levels(p.L);   // (uniform: the steps above it are skipped by scalar branches)
-    if (!p.has_ar) {
+    if (!AR) {
         // memory caps the range; Eq. 2, pre_f + M (fb[h] - fb[lo]) + inn <= bound
         // with inn = inner + last_b (0 for the first stage), is mfb[h] <= thr
         const uint32_t *mf = sx.mfb + n.t * row_len;
@@ -250,7 +254,7 @@ __device__ __forceinline__ uint32_t search_accepted(const KParams &p, const Lds 
     const uint64_t cl = ct[n.lo];
     const uint32_t pml = tab.pm[n.lo], capt = tab.cap[n.t];
     const uint32_t *pdt = tab.pd + n.t * row_len;
-    const uint32_t dl = p.has_ar ? pdt[n.lo] : 0u;
+    const uint32_t dl = AR ? pdt[n.lo] : 0u;
     const bool stage = !(flags & kSearchNoStage);
     const uint32_t carry = n.inner + n.last_b;
     uint32_t k = 0;
@@ -263,7 +267,7 @@ __device__ __forceinline__ uint32_t search_accepted(const KParams &p, const Lds 
         if (stage) {
             const uint64_t ch = ct[h];
             const uint32_t f = (uint32_t)ch - (uint32_t)cl, bw = (uint32_t)(ch >> 32) - (uint32_t)(cl >> 32);
-            const uint32_t d = p.has_ar ? pdt[h] - dl : 0u;
+            const uint32_t d = AR ? pdt[h] - dl : 0u;
             const uint32_t inn = x == 0 ? d : max(carry, d);
             ok = ok && n.pre_f + p.M * (f + bw) + inn <= bound;
         }
@@ -299,7 +303,7 @@ __device__ __forceinline__ void search_write_child(const SearchParams &q, uint64
     }
 }
 
-template <int S, bool WRITE>
+template <int S, bool AR, bool WRITE>
 __device__ __forceinline__ uint32_t search_last_children(const KParams &p, const Lds &tab, const SearchTab &sx,
                                                          const SearchNode &n, uint32_t x, uint32_t k, uint32_t flags,
                                                          uint32_t bound,
@@ -312,7 +316,7 @@ __device__ __forceinline__ uint32_t search_last_children(const KParams &p, const
     lp.mem += (h0 <= h1 ? h0 : h1 + 1) - (n.lo + 1);
     const bool ridge = (flags & kSearchRidge) != 0, stage = !(flags & kSearchNoStage);
     const bool same = n.t == n.tS;
-    if (!p.has_ar && ((p.g_mono >> (8 * n.t + n.tS)) & 1ull)) {
+    if (!AR && ((p.g_mono >> (8 * n.t + n.tS)) & 1ull)) {
         if (h0 > h1) return 0;
         // ridge: the end points below r0 fail
         uint32_t r0 = h0;
@@ -343,15 +347,20 @@ __device__ __forceinline__ uint32_t search_last_children(const KParams &p, const
             const int32_t thr = thr64 > INT32_MAX ? INT32_MAX : thr64 < INT32_MIN ? INT32_MIN : (int32_t)thr64;
             const bool none = thr64 < INT32_MIN;   // every G(hi) > thr (G > -2^31 always)
             const uint32_t len = h1 + 1 - r0;
-            const int H = (int)decode_levels(p.L);
-            uint32_t j = 0;
+            // G is smallest at h1: if even that fails, every end point does
+            // (the usual case, so the search below mostly runs on no lane)
+            uint32_t j = len;
+            if (!(none | ((int32_t)ft[h1] - (int32_t)ms[h1] > thr))) {
+                const int H = (int)decode_levels(p.L);
+                j = 0;
 #pragma unroll
-            for (int b = 7; b >= 0; --b) {
-                if (b >= H) continue;
-                const uint32_t t = j + (1u << b);
-                const uint32_t h = r0 + min(t, len) - 1;
-                const int32_t G = (int32_t)ft[h] - (int32_t)ms[h];
-                j = ((t <= len) & (none | (G > thr))) ? t : j;
+                for (int b = 7; b >= 0; --b) {
+                    if (b >= H) continue;
+                    const uint32_t t = j + (1u << b);
+                    const uint32_t h = r0 + min(t, len) - 1;
+                    const int32_t G = (int32_t)ft[h] - (int32_t)ms[h];
+                    j = ((t <= len) & (G > thr)) ? t : j;
+                }
             }
             g0 = r0 + j;
             lp.bound += j;
@@ -365,7 +374,7 @@ __device__ __forceinline__ uint32_t search_last_children(const KParams &p, const
     const uint64_t *ct = tab.cost + n.t * row_len, *cs = tab.cost + n.tS * row_len;
     const uint64_t cl = ct[n.lo], cL = cs[p.L];
     const uint32_t *pdt = tab.pd + n.t * row_len, *pds = tab.pd + n.tS * row_len;
-    const uint32_t dl = p.has_ar ? pdt[n.lo] : 0u, dL = p.has_ar ? pds[p.L] : 0u;
+    const uint32_t dl = AR ? pdt[n.lo] : 0u, dL = AR ? pds[p.L] : 0u;
     const uint32_t carry = n.inner + n.last_b;
     uint32_t out = 0;
     for (uint32_t hi = h0; hi <= h1; ++hi) {
@@ -386,10 +395,10 @@ __device__ __forceinline__ uint32_t search_last_children(const KParams &p, const
         if (stage) {
             const uint64_t ch = ct[hi], sh = cs[hi];
             const uint32_t f = (uint32_t)ch - (uint32_t)cl, b = (uint32_t)(ch >> 32) - (uint32_t)(cl >> 32);
-            const uint32_t d = p.has_ar ? pdt[hi] - dl : 0u;
+            const uint32_t d = AR ? pdt[hi] - dl : 0u;
             const uint32_t inn = x == 0 ? d : max(carry, d);
             const uint32_t fS = (uint32_t)cL - (uint32_t)sh, bS = (uint32_t)(cL >> 32) - (uint32_t)(sh >> 32);
-            const uint32_t dS = p.has_ar ? dL - pds[hi] : 0u;
+            const uint32_t dS = AR ? dL - pds[hi] : 0u;
             // Eq. 2 for the last stage: g(S_S) = sum_{i<S} F_i + M (F_S + B_S) + max(inner + B_{S-1}, d_S)
             if (n.pre_f + f + p.M * (fS + bS) + max(inn + b, dS) > bound) {
                 lp.bound += 1;
@@ -449,7 +458,7 @@ __device__ __forceinline__ uint32_t search_n_in(const SearchParams &q) {
 }
 
 // Count the children of every node of the piece; one total per block.
-template <int S>
+template <int S, bool AR>
 __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchParams q) {
     extern __shared__ __align__(16) unsigned char smem[];
     const uint32_t n_in = search_n_in(q);
@@ -470,11 +479,11 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
     uint32_t why_mem = 0, why_ridge = 0, why_bound = 0;
     if (active) {
         const uint32_t x = q.level;
-        const SearchNode n = search_node<S>(p, tab, row, w, x, ty, cut);
+        const SearchNode n = search_node<S, AR>(p, tab, row, w, x, ty, cut);
         const uint32_t hmax = p.L - (S - 1 - x);   // every later stage keeps one layer
-        const uint32_t acc = search_accepted(p, tab, sx, n, x, hmax, q.flags, bound);
+        const uint32_t acc = search_accepted<AR>(p, tab, sx, n, x, hmax, q.flags, bound);
         // the rule that stopped the range (0: it ran to its structural end)
-        const int why = search_stop(p, tab, sx, n, x, acc, hmax, q.flags, bound);
+        const int why = search_stop<AR>(p, tab, sx, n, x, acc, hmax, q.flags, bound);
         visited = acc;
         why_mem = why == 1;
         why_ridge = why == 2;
@@ -484,17 +493,17 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
             // once; its children fix the last cut, and those that pass the last
             // stage are kept (complete configurations)
             for (uint32_t c = n.lo + 1; c <= n.lo + acc; ++c) {
-                const SearchNode m = search_child(p, tab, n, x, c);
-                const uint32_t acc2 = search_accepted(p, tab, sx, m, x + 1, p.L - 1, q.flags, bound);
-                const int why2 = search_stop(p, tab, sx, m, x + 1, acc2, p.L - 1, q.flags, bound);
+                const SearchNode m = search_child<AR>(p, tab, n, x, c);
+                const uint32_t acc2 = search_accepted<AR>(p, tab, sx, m, x + 1, p.L - 1, q.flags, bound);
+                const int why2 = search_stop<AR>(p, tab, sx, m, x + 1, acc2, p.L - 1, q.flags, bound);
                 visited += acc2;
                 why_mem += why2 == 1;
                 why_ridge += why2 == 2;
                 why_bound += why2 == 3;
-                cnt += search_last_children<S, false>(p, tab, sx, m, x + 1, acc2, q.flags, bound, lp, q, 0, w);
+                cnt += search_last_children<S, AR, false>(p, tab, sx, m, x + 1, acc2, q.flags, bound, lp, q, 0, w);
             }
         } else {
-            cnt = x + 2 == (uint32_t)S ? search_last_children<S, false>(p, tab, sx, n, x, acc, q.flags, bound, lp, q, 0, w)
+            cnt = x + 2 == (uint32_t)S ? search_last_children<S, AR, false>(p, tab, sx, n, x, acc, q.flags, bound, lp, q, 0, w)
                                        : acc;
         }
         q.node_cnt[i] = (uint16_t)cnt;   // at most (L - 1)^2 < 2^16 children (fused), else L - 1
@@ -512,7 +521,7 @@ __global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchP
 
 // Write the children of blocks [blk_base, blk_base + gridDim.x) in node
 // order, the first one at position 0 of the output.
-template <int S>
+template <int S, bool AR>
 __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchParams q) {
     extern __shared__ __align__(16) unsigned char smem[];
     const uint32_t blk = q.blk_base + blockIdx.x;
@@ -537,22 +546,22 @@ __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchP
         if (q.fused) {
             // the complete configurations under each child, child by child
             LastStage lp;
-            const SearchNode n = search_node<S>(p, tab, row, w, x, ty, cut);
-            const uint32_t acc = search_accepted(p, tab, sx, n, x, p.L - (S - 1 - x), q.flags, bound);
+            const SearchNode n = search_node<S, AR>(p, tab, row, w, x, ty, cut);
+            const uint32_t acc = search_accepted<AR>(p, tab, sx, n, x, p.L - (S - 1 - x), q.flags, bound);
             uint64_t o = base;
             for (uint32_t c = n.lo + 1; c <= n.lo + acc; ++c) {
-                const SearchNode m = search_child(p, tab, n, x, c);
-                const uint32_t acc2 = search_accepted(p, tab, sx, m, x + 1, p.L - 1, q.flags, bound);
+                const SearchNode m = search_child<AR>(p, tab, n, x, c);
+                const uint32_t acc2 = search_accepted<AR>(p, tab, sx, m, x + 1, p.L - 1, q.flags, bound);
                 uint32_t wc[NW];
 #pragma unroll
                 for (int k = 0; k < NW; ++k) wc[k] = (uint32_t)k == (x >> 2) ? (w[k] | (c << (8 * (x & 3)))) : w[k];
-                o += search_last_children<S, true>(p, tab, sx, m, x + 1, acc2, q.flags, bound, lp, q, o, wc);
+                o += search_last_children<S, AR, true>(p, tab, sx, m, x + 1, acc2, q.flags, bound, lp, q, o, wc);
             }
         } else if (x + 2 == (uint32_t)S) {
             LastStage lp;
-            const SearchNode n = search_node<S>(p, tab, row, w, x, ty, cut);
-            const uint32_t acc = search_accepted(p, tab, sx, n, x, p.L - (S - 1 - x), q.flags, bound);
-            search_last_children<S, true>(p, tab, sx, n, x, acc, q.flags, bound, lp, q, base, w);
+            const SearchNode n = search_node<S, AR>(p, tab, row, w, x, ty, cut);
+            const uint32_t acc = search_accepted<AR>(p, tab, sx, n, x, p.L - (S - 1 - x), q.flags, bound);
+            search_last_children<S, AR, true>(p, tab, sx, n, x, acc, q.flags, bound, lp, q, base, w);
         } else {
             // every accepted choice is a child: c_{x+1} = lo+1 .. lo+cnt
             uint32_t lo = 0;
@@ -583,9 +592,9 @@ __global__ __launch_bounds__(kBlock) void search_leaf_kernel(KParams p, SearchPa
     int why = 4;
     unsigned long long key = ~0ull;
     if (active) {
-        const SearchNode n = search_node<S>(p, tab, row, w, S - 1, ty, cut);
+        const SearchNode n = search_node<S, AR>(p, tab, row, w, S - 1, ty, cut);
         // for S > 1 the level that fixed the last cut already tested the last stage
-        why = S == 1 ? search_try(p, tab, n, S - 1, p.L, q.flags, bound) : 0;
+        why = S == 1 ? search_try<AR>(p, tab, n, S - 1, p.L, q.flags, bound) : 0;
     }
     const bool leaf = why == 0;
     if (leaf) {
@@ -644,8 +653,14 @@ hipError_t launch_search_s(int op, const KParams &p, const SearchParams &q, uint
                            hipStream_t st) {
     const dim3 g(grid), b(kBlock);
     switch (op) {
-    case kSearchOpCount: hipLaunchKernelGGL((search_count_kernel<S>), g, b, lds, st, p, q); break;
-    case kSearchOpWrite: hipLaunchKernelGGL((search_write_kernel<S>), g, b, lds, st, p, q); break;
+    case kSearchOpCount:
+        if (p.has_ar) hipLaunchKernelGGL((search_count_kernel<S, true>), g, b, lds, st, p, q);
+        else hipLaunchKernelGGL((search_count_kernel<S, false>), g, b, lds, st, p, q);
+        break;
+    case kSearchOpWrite:
+        if (p.has_ar) hipLaunchKernelGGL((search_write_kernel<S, true>), g, b, lds, st, p, q);
+        else hipLaunchKernelGGL((search_write_kernel<S, false>), g, b, lds, st, p, q);
+        break;
     case kSearchOpLeaf: {
         const bool sch = p.sched != 0;
         if (p.has_ar && sch) hipLaunchKernelGGL((search_leaf_kernel<S, true, true>), g, b, lds, st, p, q);
