@@ -527,22 +527,53 @@ __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchP
     const uint32_t blk = q.blk_base + blockIdx.x;
     const uint32_t n_in = search_n_in(q);
     if (blk * kBlock >= n_in) return;   // past the level's nodes
-    const Lds tab = stage_tables(p, smem);
-    const SearchTab sx = search_tables(p, tab, smem);
+    constexpr int NW = Codes<S>::kWords;
     const uint32_t i = blk * kBlock + threadIdx.x;
     const bool active = i < n_in;
-    const uint32_t bound = *q.bound;
+    const uint32_t x = q.level;
     // the count kernel left each node's number of children: nodes without
     // any (most of them at the level that fixes the last cut) do nothing
     const uint32_t cnt = active ? q.node_cnt[i] : 0u;
     unsigned long long total;
     const unsigned long long local = block_exclusive_scan_u64(cnt, total);
+    const uint64_t blk0 = q.blk_off[blk] - q.blk_off[q.blk_base];
+    if (!q.fused && x + 2 != (uint32_t)S) {
+        // every accepted choice is a child: c_{x+1} = lo+1 .. lo+cnt.  The
+        // wave writes the children of its nodes together, 64 consecutive ones
+        // per store: lane j takes child o0 + j of the wave's run, and its
+        // parent is the first lane whose inclusive count exceeds that
+        // (a binary search over the lanes)
+        uint32_t row, w[NW];
+        search_load<S>(q, i, active, row, w);
+        uint32_t lo = 0;
+#pragma unroll
+        for (int s = 1; s < S; ++s)
+            if ((uint32_t)s == x) lo = (w[(s - 1) >> 2] >> (8 * ((s - 1) & 3))) & 0xFFu;
+        const uint32_t lane = threadIdx.x & 63;
+        const unsigned long long l0 = __shfl(local, 0, 64);
+        const uint32_t incl = (uint32_t)(local - l0) + cnt;
+        const uint32_t wtot = __shfl(incl, 63, 64);
+        for (uint32_t o0 = 0; o0 < wtot; o0 += 64) {
+            const uint32_t o = o0 + lane;
+            uint32_t pl = 0;
+#pragma unroll
+            for (uint32_t b = 32; b; b >>= 1) pl = __shfl(incl, (int)(pl + b - 1), 64) <= o ? pl + b : pl;
+            const uint32_t first = __shfl(incl - cnt, (int)pl, 64);
+            const uint32_t prow = __shfl(row, (int)pl, 64), plo = __shfl(lo, (int)pl, 64);
+            uint32_t pw[NW];
+#pragma unroll
+            for (int k = 0; k < NW; ++k) pw[k] = __shfl(w[k], (int)pl, 64);
+            if (o < wtot) search_write_child<S>(q, blk0 + l0 + o, prow, x, plo + 1 + (o - first), pw);
+        }
+        return;
+    }
+    const Lds tab = stage_tables(p, smem);
+    const SearchTab sx = search_tables(p, tab, smem);
+    const uint32_t bound = *q.bound;
     if (cnt) {
-        constexpr int NW = Codes<S>::kWords;
         uint32_t row, w[NW], ty[S], cut[S + 1];
-        const uint32_t x = q.level;
         search_load<S>(q, i, true, row, w);
-        const uint64_t base = q.blk_off[blk] - q.blk_off[q.blk_base] + local;
+        const uint64_t base = blk0 + local;
         if (q.fused) {
             // the complete configurations under each child, child by child
             LastStage lp;
@@ -557,18 +588,11 @@ __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchP
                 for (int k = 0; k < NW; ++k) wc[k] = (uint32_t)k == (x >> 2) ? (w[k] | (c << (8 * (x & 3)))) : w[k];
                 o += search_last_children<S, AR, true>(p, tab, sx, m, x + 1, acc2, q.flags, bound, lp, q, o, wc);
             }
-        } else if (x + 2 == (uint32_t)S) {
+        } else {   // x + 2 == S
             LastStage lp;
             const SearchNode n = search_node<S, AR>(p, tab, row, w, x, ty, cut);
             const uint32_t acc = search_accepted<AR>(p, tab, sx, n, x, p.L - (S - 1 - x), q.flags, bound);
             search_last_children<S, AR, true>(p, tab, sx, n, x, acc, q.flags, bound, lp, q, base, w);
-        } else {
-            // every accepted choice is a child: c_{x+1} = lo+1 .. lo+cnt
-            uint32_t lo = 0;
-#pragma unroll
-            for (int s = 1; s < S; ++s)
-                if ((uint32_t)s == x) lo = (w[(s - 1) >> 2] >> (8 * ((s - 1) & 3))) & 0xFFu;
-            for (uint32_t c = 0; c < cnt; ++c) search_write_child<S>(q, base + c, row, x, lo + 1 + c, w);
         }
     }
 }
