@@ -457,9 +457,12 @@ __device__ __forceinline__ uint32_t search_n_in(const SearchParams &q) {
     return q.n_dev ? (uint32_t)*q.n_dev : q.n_in;
 }
 
-// Count the children of every node of the piece; one total per block.
+// Count the children of every node of the piece; one total per block.  The
+// kernel waits on chains of dependent LDS loads (binary searches), so it
+// asks for 7 waves per SIMD (72 VGPRs, no spills for any S) rather than the
+// compiler's choice of 6.
 template <int S, bool AR>
-__global__ __launch_bounds__(kBlock) void search_count_kernel(KParams p, SearchParams q) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7, 8))) void search_count_kernel(KParams p, SearchParams q) {
     extern __shared__ __align__(16) unsigned char smem[];
     const uint32_t n_in = search_n_in(q);
     if (blockIdx.x * kBlock >= n_in) {
