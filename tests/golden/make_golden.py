@@ -9,6 +9,10 @@ word i / 32), the number of feasible candidates and the argmin.  For
 workloads 4 and 6 it also records the early-stop pass: the warm-up bound (best of
 the first 500 list entries) and, per chunk size, the oracle's
 (best, evaluated, pruned, infeasible); likewise for 4e and 5e.
+"4s" records the pruned search (Sec. 4.2.3) over every assignment row and
+composition of workload 4, against that warm-up bound, in chunks that grow
+1, 2, 4, ... rows up to 512: the best (joint index, makespan) and the five
+counters, without and with the ridge filter.
 
 Run from the repository root:  python tests/golden/make_golden.py [workload ...]
 """
@@ -36,12 +40,34 @@ def pack_bits(f: np.ndarray) -> np.ndarray:
     return np.packbits(np.concatenate([f.astype(bool), np.zeros(pad, bool)]), bitorder="little").view("<u4")
 
 
+SEARCH_RPC = 512
+
+
+def search_entry():
+    wl = W.workload(4)
+    c = wl.cands
+    T, f = coracle.evaluate(wl.problem, W.Candidates(comp_rank=c.comp_rank[:WARMUP].copy(),
+                                                     assign_idx=c.assign_idx[:WARMUP].copy()))
+    bound = coracle.argmin(T, f)[1]
+    ent = {"warmup": WARMUP, "bound": bound, "rows_per_chunk": SEARCH_RPC, "ramp": True}
+    for name, ridge in (("plain", False), ("ridge", True)):
+        t0 = time.time()
+        r = coracle.search(wl.problem, bound, rows_per_chunk=SEARCH_RPC, ridge=ridge, ramp=True)
+        ent[name] = {"best_index": r["best"][0], "best_makespan": r["best"][1],
+                     **{k: r[k] for k in coracle.SEARCH_COUNTERS}, "oracle_seconds": round(time.time() - t0, 1)}
+    return ent
+
+
 def main():
     res = {"note": "written by tests/golden/make_golden.py from the C oracle; see that script"}
-    only = sys.argv[1:] or ["3", "4", "5", "6", "4e", "5e", "5i"]
+    only = sys.argv[1:] or ["3", "4", "5", "6", "4e", "5e", "5i", "4s"]
     if os.path.exists(OUT):
         res.update({k: v for k, v in json.load(open(OUT)).items() if k != "note"})
     for spec in only:
+        if spec == "4s":
+            res["cfg4_search"] = search_entry()
+            print(spec, res["cfg4_search"], flush=True)
+            continue
         eager, ilv = spec.endswith("e"), spec.endswith("i")
         cfg = int(spec.rstrip("ei"))
         wl = W.workload(cfg)

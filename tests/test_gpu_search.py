@@ -5,6 +5,9 @@ force and the paper's theorems in tests/test_search_pins.py.
 Everything is integer: the best (joint index, makespan) and all five
 counters must be identical for the same bound and chunking.
 """
+import json
+import os
+
 import numpy as np
 import pytest
 
@@ -152,3 +155,27 @@ def test_search_workload6_eager_rows(dev):
     To, fo = coracle.evaluate(prob, W.Candidates(comp_rank=c.comp_rank[:500].copy(),
                                                  assign_idx=c.assign_idx[:500].copy()))
     check(prob, int(To[fo].min()), dev, first_row=100, n_rows=24, rows_per_chunk=8, ridge=True)
+
+
+def test_search_workload4_full_golden(dev):
+    """The whole 8-stage, 3-type search as the benchmark runs it (all 6561
+    rows x C(79,7) compositions, warm-up bound, chunks growing to 512 rows),
+    without and with the ridge filter, against the oracle's result and
+    counters stored by tests/golden/make_golden.py."""
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "full_workloads.json")))["cfg4_search"]
+    wl = W.workload(4)
+    c = wl.cands
+    To, fo = coracle.evaluate(wl.problem, W.Candidates(comp_rank=c.comp_rank[:gold["warmup"]].copy(),
+                                                       assign_idx=c.assign_idx[:gold["warmup"]].copy()))
+    assert int(To[fo].min()) == gold["bound"]
+    ctx = P.poseidon_load_costs(wl.problem, 0)
+    try:
+        for name, ridge in (("plain", False), ("ridge", True)):
+            b, st = P.poseidon_search(ctx, gold["bound"], rows_per_chunk=gold["rows_per_chunk"], ridge=ridge,
+                                      ramp=gold["ramp"])
+            g = gold[name]
+            assert (b.index, b.makespan) == (g["best_index"], g["best_makespan"])
+            assert (st.visited, st.evaluated, st.pruned_memory, st.pruned_ridge, st.pruned_bound) == \
+                (g["visited"], g["evaluated"], g["pruned_memory"], g["pruned_ridge"], g["pruned_bound"])
+    finally:
+        ctx.close()
