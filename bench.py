@@ -305,7 +305,11 @@ def main():
                      # hardware side: VALU wave-instructions the call issues (counters) x 4 cycles
                      # over all SIMD cycles at peak clock during the measured call time
                      "valu_issue_frac": None if ctr is None else
-                     ctr["valu_wave_insts_per_call"] * 4 / (N_SIMD * PEAK_CLOCK * k_avg * 1e-3)},
+                     ctr["valu_wave_insts_per_call"] * 4 / (N_SIMD * PEAK_CLOCK * k_avg * 1e-3),
+                     # INT32 lane-ops the call executes (counters: INT32 wave-instructions x
+                     # mean active lanes per kernel) over the measured call time, against the peak
+                     "valu_int32_lane_frac": None if ctr is None or "valu_int32_lane_ops_per_call" not in ctr else
+                     ctr["valu_int32_lane_ops_per_call"] / (k_avg * 1e-3) / 1e12 / PEAK_INT32_TOPS},
         "early_stop": es,
     }
     if not args.no_cpu_baseline:
