@@ -220,7 +220,8 @@ int poseidon_argmin(poseidon_ctx *ctx, const uint32_t *makespan, const uint32_t 
  * its joint index rank * A + row.  Theorem 1 makes it the exhaustive
  * optimum of those candidates.  POSEIDON_NO_FEASIBLE if there is none.
  * best_out and stats_out are HOST pointers (either may be NULL); the call
- * synchronises the stream after every level of the search.  The frontier
+ * synchronises the stream wherever it reads a level's size back (levels
+ * that may need more than one frontier piece) and at its end.  The frontier
  * memory, 4 Mi partial configurations per stage of (6 + 4 ceil((S-1)/4))
  * bytes each (1.5 GB at S = 16), is allocated on the first call and kept by
  * the context.  The work grows with the pruned tree, which for many stages

@@ -110,7 +110,7 @@ def test_search_deep_pipelines(dev):
         prob = W.random_problem(rng, L, S, M, 2, cost_hi=300, mem_hi=30, cap=int(rng.integers(60, 200)),
                                 assign_rows=int(rng.integers(1, 6)))
         prob.schedule = S % 2
-        for kw in (dict(), dict(ridge=True, rows_per_chunk=2)):
+        for kw in (dict(), dict(ridge=True, rows_per_chunk=2), dict(ramp=True, rows_per_chunk=2)):
             check(prob, 2 ** 31 - 1, dev, **kw)
 
 
