@@ -114,6 +114,25 @@ def test_search_deep_pipelines(dev):
             check(prob, 2 ** 31 - 1, dev, **kw)
 
 
+def test_search_maximum_layer_and_type_counts(dev):
+    """T = 8 with L = 256 (the largest tables: cut values up to 255, LDS stage
+    and search tables for 8 types; above the fused-level limit) and with
+    L = 120, S = 4 (fused), with and without all-reduce times, the ridge
+    filter and growing chunks."""
+    rng = np.random.default_rng(124)
+    for trial in range(6):
+        L, S = (256, 3) if trial < 4 else (120, 4)
+        prob = W.random_problem(rng, L, S, 6, 8, cost_lo=50, cost_hi=400, mem_hi=20, cap=int(rng.integers(900, 3000)),
+                                assign_rows=5)
+        if trial % 2:
+            prob.allreduce = rng.integers(0, 3000, size=(8, L)).astype(np.uint32)
+        prob.schedule = (trial // 2) % 2
+        To, fo = coracle.evaluate(prob, W.random_candidates(rng, prob, 300))
+        bound = int(To[fo].min()) if fo.any() else 2 ** 31 - 1
+        for kw in (dict(), dict(ridge=True, rows_per_chunk=2), dict(ramp=True, rows_per_chunk=2)):
+            check(prob, bound, dev, **kw)
+
+
 def test_search_row_ranges_and_no_result(dev):
     rng = np.random.default_rng(121)
     prob = W.random_problem(rng, 12, 4, 9, 3, mem_hi=30, cap=90)
