@@ -298,6 +298,8 @@ struct poseidon_ctx {
     void *ws;              // cut codes + straggler queues of the steady-state cascade
     uint64_t ws_cap;       // candidates per chunk the workspace holds
     void *sws;             // search frontiers (allocated on the first poseidon_search)
+    unsigned long long *shost;   // pinned host words for the search's read-backs (level totals
+                                 // and block offsets), allocated with sws
 };
 
 extern "C" {
@@ -588,6 +590,7 @@ void poseidon_free(poseidon_ctx *ctx) {
     if (hipGetDevice(&prev) == hipSuccess && hipSetDevice(ctx->device) == hipSuccess) {
         if (ctx->ws) (void)hipFree(ctx->ws);
         if (ctx->sws) (void)hipFree(ctx->sws);
+        if (ctx->shost) (void)hipHostFree(ctx->shost);
         (void)hipFree(ctx->dmem);
         (void)hipSetDevice(prev);
     }
@@ -913,9 +916,10 @@ struct SearchRun {
 };
 
 int search_read_total(SearchRun &r, uint32_t x, unsigned long long *total) {
-    if (hipMemcpyAsync(total, r.w.words + SW_TOTAL + x, 8, hipMemcpyDeviceToHost, r.st) != hipSuccess ||
+    if (hipMemcpyAsync(r.ctx->shost, r.w.words + SW_TOTAL + x, 8, hipMemcpyDeviceToHost, r.st) != hipSuccess ||
         hipStreamSynchronize(r.st) != hipSuccess)
         return POSEIDON_E_DEVICE;
+    *total = r.ctx->shost[0];
     return POSEIDON_OK;
 }
 
@@ -983,10 +987,12 @@ int search_expand(SearchRun &r, uint32_t x, uint64_t n, const unsigned long long
     // more children than a level holds: write and expand them in pieces of
     // whole blocks (one block has at most 256 (L - 1) < kSearchCap children,
     // or 256 (L - 1)^2 <= kSearchCap when fused)
-    std::vector<unsigned long long> off(grid + 1);
-    if (hipMemcpyAsync(off.data(), q.blk_off, (grid + 1) * 8, hipMemcpyDeviceToHost, r.st) != hipSuccess ||
+    // (into the pinned words, grid + 1 <= kSearchBlk + 1 of them; the pieces'
+    // own expansions reuse those words, so the offsets are copied out first)
+    if (hipMemcpyAsync(r.ctx->shost, q.blk_off, (grid + 1) * 8, hipMemcpyDeviceToHost, r.st) != hipSuccess ||
         hipStreamSynchronize(r.st) != hipSuccess)
         return POSEIDON_E_DEVICE;
+    const std::vector<unsigned long long> off(r.ctx->shost, r.ctx->shost + grid + 1);
     uint32_t b0 = 0;
     while (b0 < grid) {
         uint32_t b1 = b0 + 1;
@@ -1020,6 +1026,13 @@ extern "C" int poseidon_search(poseidon_ctx *ctx, uint64_t first_row, uint64_t n
         if (hipMalloc(&ctx->sws, bytes) != hipSuccess) {
             (void)hipGetLastError();
             ctx->sws = nullptr;
+            return POSEIDON_E_NOMEM;
+        }
+    }
+    if (!ctx->shost) {
+        if (hipHostMalloc((void **)&ctx->shost, ((size_t)kSearchBlk + 2) * 8, hipHostMallocDefault) != hipSuccess) {
+            (void)hipGetLastError();
+            ctx->shost = nullptr;
             return POSEIDON_E_NOMEM;
         }
     }
