@@ -337,20 +337,15 @@ __device__ __forceinline__ uint32_t search_last_children(const KParams &p, const
         uint32_t g0 = r0;
         if (stage && r0 <= h1) {
             const uint32_t *ft = sx.fb + n.t * row_len, *ms = sx.mfb + n.tS * row_len;
-            // g(hi) = C + G(hi) > bound  <=>  G(hi) > bound - C, with
-            // G(hi) = fb_t[hi] - mfb_tS[hi].  Every prefix time and M times any
-            // type's prefix stays below 2^31 (checked at load), so G fits 32
-            // bits; the threshold is clamped to that range
-            const int64_t C = (int64_t)n.pre_f - (int64_t)ft[n.lo] + (x == 0 ? 0 : (int64_t)(n.inner + n.last_b)) +
-                              (int64_t)ms[p.L];
-            const int64_t thr64 = (int64_t)bound - C;
-            const int32_t thr = thr64 > INT32_MAX ? INT32_MAX : thr64 < INT32_MIN ? INT32_MIN : (int32_t)thr64;
-            const bool none = thr64 < INT32_MIN;   // every G(hi) > thr (G > -2^31 always)
+            // g(hi) = C + G(hi), G(hi) = fb_t[hi] - mfb_tS[hi].  g is an Eq. 2
+            // value, below 2^31 like every path weight (checked at load), so
+            // C + G evaluates exactly in 32-bit modular arithmetic
+            const uint32_t C = n.pre_f - ft[n.lo] + (x == 0 ? 0u : n.inner + n.last_b) + ms[p.L];
             const uint32_t len = h1 + 1 - r0;
-            // G is smallest at h1: if even that fails, every end point does
+            // g is smallest at h1: if even that fails, every end point does
             // (the usual case, so the search below mostly runs on no lane)
             uint32_t j = len;
-            if (!(none | ((int32_t)ft[h1] - (int32_t)ms[h1] > thr))) {
+            if (C + ft[h1] - ms[h1] <= bound) {
                 const int H = (int)decode_levels(p.L);
                 j = 0;
 #pragma unroll
@@ -358,8 +353,7 @@ __device__ __forceinline__ uint32_t search_last_children(const KParams &p, const
                     if (b >= H) continue;
                     const uint32_t t = j + (1u << b);
                     const uint32_t h = r0 + min(t, len) - 1;
-                    const int32_t G = (int32_t)ft[h] - (int32_t)ms[h];
-                    j = ((t <= len) & (G > thr)) ? t : j;
+                    j = ((t <= len) & (C + ft[h] - ms[h] > bound)) ? t : j;
                 }
             }
             g0 = r0 + j;
