@@ -253,8 +253,9 @@ __device__ __forceinline__ uint32_t search_accepted(const KParams &p, const Lds 
     const uint64_t *ct = tab.cost + n.t * row_len;
     const uint64_t cl = ct[n.lo];
     const uint32_t pml = tab.pm[n.lo], capt = tab.cap[n.t];
+    // with all-reduce times: each probe evaluates the memory and Eq. 2 tests
     const uint32_t *pdt = tab.pd + n.t * row_len;
-    const uint32_t dl = AR ? pdt[n.lo] : 0u;
+    const uint32_t dl = pdt[n.lo];
     const bool stage = !(flags & kSearchNoStage);
     const uint32_t carry = n.inner + n.last_b;
     uint32_t k = 0;
@@ -267,7 +268,7 @@ __device__ __forceinline__ uint32_t search_accepted(const KParams &p, const Lds 
         if (stage) {
             const uint64_t ch = ct[h];
             const uint32_t f = (uint32_t)ch - (uint32_t)cl, bw = (uint32_t)(ch >> 32) - (uint32_t)(cl >> 32);
-            const uint32_t d = AR ? pdt[h] - dl : 0u;
+            const uint32_t d = pdt[h] - dl;
             const uint32_t inn = x == 0 ? d : max(carry, d);
             ok = ok && n.pre_f + p.M * (f + bw) + inn <= bound;
         }
@@ -286,8 +287,8 @@ __device__ __forceinline__ uint32_t search_accepted(const KParams &p, const Lds 
 // constant and a function of hi alone:
 //   g(S_S) = C + G(hi),  G(hi) = Pf_t[hi] + Pb_t[hi] - M (Pf_tS[hi] + Pb_tS[hi])
 // (t, tS the types of stages S-1 and S, Pf / Pb the prefix times).  G falls
-// as hi grows when every layer costs at least M times more on tS than on t
-// (checked per type pair on the host: bit 8 t + tS of p.g_mono), and the
+// as hi grows when no layer's forward + backward time on t exceeds M times
+// that on tS (checked per type pair on the host: bit 8 t + tS of p.g_mono), and the
 // last stage's ridge test fails on a prefix of the end points too, so then
 // every outcome count is a range length: the ridge prefix in closed form,
 // the bound prefix by a binary search.  Otherwise the end points are tried
