@@ -534,6 +534,7 @@ __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchP
     const uint32_t cnt = active ? q.node_cnt[i] : 0u;
     unsigned long long total;
     const unsigned long long local = block_exclusive_scan_u64(cnt, total);
+    if (total == 0) return;   // no child in the block (most blocks of the last-cut level)
     const uint64_t blk0 = q.blk_off[blk] - q.blk_off[q.blk_base];
     if (!q.fused && x + 2 != (uint32_t)S) {
         // every accepted choice is a child: c_{x+1} = lo+1 .. lo+cnt.  The
