@@ -4,6 +4,7 @@ import math
 import os
 import re
 import subprocess
+import sys
 
 import numpy as np
 import pytest
@@ -177,3 +178,13 @@ def test_joint_index_overflow_is_refused():
     index rank * A + a."""
     p = W.random_problem(np.random.default_rng(8), 256, 8, 4, 8)
     assert _status(p) == P.POSEIDON_E_RANGE
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """The benchmark measures one GPU: --gpus N > 1 exits with status 2 and a
+    message, before it imports torch or touches a device."""
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120, cwd=root)
+    assert r.returncode == 2
+    assert "measures one GPU" in r.stderr and r.stdout == ""
