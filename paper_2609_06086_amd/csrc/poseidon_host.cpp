@@ -457,6 +457,10 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
                        (uint64_t)M * ((uint64_t)p->fwd_us[(size_t)u * L + l] + p->bwd_us[(size_t)u * L + l]);
             if (mono) kp.g_mono |= 1ull << (8 * t + u);
         }
+    kp.g_mono_all = 1;
+    for (uint32_t t = 0; t < T; ++t)
+        for (uint32_t u = 0; u < T; ++u)
+            if (!((kp.g_mono >> (8 * t + u)) & 1ull)) kp.g_mono_all = 0;
     if (ilv) {
         // the compiled schedule (prologue, `trips` periods, cool-down) is used
         // only if it equals this problem's own slot table word for word

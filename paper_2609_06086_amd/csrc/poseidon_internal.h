@@ -33,6 +33,8 @@ struct KParams {
     uint32_t sched;               // POSEIDON_SCHEDULE_*
     uint32_t ndev;                // devices: S, or S / V under Interleaved 1F1B
     uint32_t last_lo[8];          // per type t: smallest c with pm[L] - pm[c] <= cap[t] (search)
+    uint32_t g_mono_all;          // every type pair has its g_mono bit (the search kernels then
+                                  // compile the closed-form last stage only)
     uint64_t g_mono;              // bit 8 t + u: every layer's fwd + bwd on t is at most M times
                                   // that on u (the search's last-stage Eq. 2 then falls with the cut)
     uint32_t ilv_compiled, ilv_trips; // Interleaved 1F1B: the schedule runs as compiled code with

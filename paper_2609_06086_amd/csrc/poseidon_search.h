@@ -304,7 +304,7 @@ __device__ __forceinline__ void search_write_child(const SearchParams &q, uint64
     }
 }
 
-template <int S, bool AR, bool WRITE>
+template <int S, bool AR, bool WRITE, bool MONO>
 __device__ __forceinline__ uint32_t search_last_children(const KParams &p, const Lds &tab, const SearchTab &sx,
                                                          const SearchNode &n, uint32_t x, uint32_t k, uint32_t flags,
                                                          uint32_t bound,
@@ -317,7 +317,7 @@ __device__ __forceinline__ uint32_t search_last_children(const KParams &p, const
     lp.mem += (h0 <= h1 ? h0 : h1 + 1) - (n.lo + 1);
     const bool ridge = (flags & kSearchRidge) != 0, stage = !(flags & kSearchNoStage);
     const bool same = n.t == n.tS;
-    if (!AR && ((p.g_mono >> (8 * n.t + n.tS)) & 1ull)) {
+    if (!AR && (MONO || ((p.g_mono >> (8 * n.t + n.tS)) & 1ull))) {
         if (h0 > h1) return 0;
         // ridge: the end points below r0 fail
         uint32_t r0 = h0;
@@ -456,7 +456,7 @@ __device__ __forceinline__ uint32_t search_n_in(const SearchParams &q) {
 // kernel waits on chains of dependent LDS loads (binary searches), so it
 // asks for 7 waves per SIMD (72 VGPRs, no spills for any S) rather than the
 // compiler's choice of 6.
-template <int S, bool AR>
+template <int S, bool AR, bool MONO>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7, 8))) void search_count_kernel(KParams p, SearchParams q) {
     extern __shared__ __align__(16) unsigned char smem[];
     const uint32_t n_in = search_n_in(q);
@@ -498,10 +498,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7, 8))) 
                 why_mem += why2 == 1;
                 why_ridge += why2 == 2;
                 why_bound += why2 == 3;
-                cnt += search_last_children<S, AR, false>(p, tab, sx, m, x + 1, acc2, q.flags, bound, lp, q, 0, w);
+                cnt += search_last_children<S, AR, false, MONO>(p, tab, sx, m, x + 1, acc2, q.flags, bound, lp, q, 0, w);
             }
         } else {
-            cnt = x + 2 == (uint32_t)S ? search_last_children<S, AR, false>(p, tab, sx, n, x, acc, q.flags, bound, lp, q, 0, w)
+            cnt = x + 2 == (uint32_t)S ? search_last_children<S, AR, false, MONO>(p, tab, sx, n, x, acc, q.flags, bound, lp, q, 0, w)
                                        : acc;
         }
         q.node_cnt[i] = (uint16_t)cnt;   // at most (L - 1)^2 < 2^16 children (fused), else L - 1
@@ -519,7 +519,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7, 8))) 
 
 // Write the children of blocks [blk_base, blk_base + gridDim.x) in node
 // order, the first one at position 0 of the output.
-template <int S, bool AR>
+template <int S, bool AR, bool MONO>
 __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchParams q) {
     extern __shared__ __align__(16) unsigned char smem[];
     const uint32_t blk = q.blk_base + blockIdx.x;
@@ -585,13 +585,13 @@ __global__ __launch_bounds__(kBlock) void search_write_kernel(KParams p, SearchP
                 uint32_t wc[NW];
 #pragma unroll
                 for (int k = 0; k < NW; ++k) wc[k] = (uint32_t)k == (x >> 2) ? (w[k] | (c << (8 * (x & 3)))) : w[k];
-                o += search_last_children<S, AR, true>(p, tab, sx, m, x + 1, acc2, q.flags, bound, lp, q, o, wc);
+                o += search_last_children<S, AR, true, MONO>(p, tab, sx, m, x + 1, acc2, q.flags, bound, lp, q, o, wc);
             }
         } else {   // x + 2 == S
             LastStage lp;
             const SearchNode n = search_node<S, AR>(p, tab, row, w, x, ty, cut);
             const uint32_t acc = search_accepted<AR>(p, tab, sx, n, x, p.L - (S - 1 - x), q.flags, bound);
-            search_last_children<S, AR, true>(p, tab, sx, n, x, acc, q.flags, bound, lp, q, base, w);
+            search_last_children<S, AR, true, MONO>(p, tab, sx, n, x, acc, q.flags, bound, lp, q, base, w);
         }
     }
 }
@@ -677,12 +677,14 @@ hipError_t launch_search_s(int op, const KParams &p, const SearchParams &q, uint
     const dim3 g(grid), b(kBlock);
     switch (op) {
     case kSearchOpCount:
-        if (p.has_ar) hipLaunchKernelGGL((search_count_kernel<S, true>), g, b, lds, st, p, q);
-        else hipLaunchKernelGGL((search_count_kernel<S, false>), g, b, lds, st, p, q);
+        if (p.has_ar) hipLaunchKernelGGL((search_count_kernel<S, true, false>), g, b, lds, st, p, q);
+        else if (p.g_mono_all) hipLaunchKernelGGL((search_count_kernel<S, false, true>), g, b, lds, st, p, q);
+        else hipLaunchKernelGGL((search_count_kernel<S, false, false>), g, b, lds, st, p, q);
         break;
     case kSearchOpWrite:
-        if (p.has_ar) hipLaunchKernelGGL((search_write_kernel<S, true>), g, b, lds, st, p, q);
-        else hipLaunchKernelGGL((search_write_kernel<S, false>), g, b, lds, st, p, q);
+        if (p.has_ar) hipLaunchKernelGGL((search_write_kernel<S, true, false>), g, b, lds, st, p, q);
+        else if (p.g_mono_all) hipLaunchKernelGGL((search_write_kernel<S, false, true>), g, b, lds, st, p, q);
+        else hipLaunchKernelGGL((search_write_kernel<S, false, false>), g, b, lds, st, p, q);
         break;
     case kSearchOpLeaf: {
         const bool sch = p.sched != 0;
