@@ -51,14 +51,17 @@ __global__ __launch_bounds__(kBlock) void argmin_kernel(const uint32_t *T, const
 // each thread then scans a contiguous run there, and the offsets go back
 // out coalesced.  The kernel sits between the count and write launches of
 // every level and its time is the latency of its loads, so it reads nothing
-// else (the counters go to slots the host sums).  A level piece has at most
-// kSearchScanMax blocks, each with at most 256 (L - 1) children, so every
-// offset fits 32 bits.
+// else (the counters go to slots the host sums).  A block has at most
+// 256 (L - 1)^2 < 2^22 children (fused levels, L <= 129) and a run at most
+// kSearchScanMax / 256 = 64 blocks, so an offset within its run fits 32 bits
+// in LDS; the run's own 64-bit start is kept beside it (a whole piece can
+// exceed 2^32 children).
 
 __device__ __forceinline__ uint32_t scan_pad(uint32_t b) { return b + (b >> 6); }
 
 __global__ __launch_bounds__(kBlock) void search_scan_kernel(SearchParams q, uint32_t nblk) {
     __shared__ uint32_t cnt[kSearchScanMax + kSearchScanMax / 64];
+    __shared__ unsigned long long run0[kBlock];
 #pragma unroll 8
     for (uint32_t b = threadIdx.x; b < nblk; b += kBlock) cnt[scan_pad(b)] = q.blk_tot[b];
     __syncthreads();
@@ -67,20 +70,24 @@ __global__ __launch_bounds__(kBlock) void search_scan_kernel(SearchParams q, uin
     unsigned long long s = 0;
     for (uint32_t b = b0; b < b1; ++b) s += cnt[scan_pad(b)];
     unsigned long long total;
-    unsigned long long off = block_exclusive_scan_u64(s, total);
+    run0[threadIdx.x] = block_exclusive_scan_u64(s, total);
+    uint32_t rel = 0;
     for (uint32_t b = b0; b < b1; ++b) {
         const uint32_t v = cnt[scan_pad(b)];
-        cnt[scan_pad(b)] = (uint32_t)off;
-        off += v;
+        cnt[scan_pad(b)] = rel;
+        rel += v;
     }
     __syncthreads();
 #pragma unroll 8
-    for (uint32_t b = threadIdx.x; b < nblk; b += kBlock) q.blk_off[b] = cnt[scan_pad(b)];
+    for (uint32_t b = threadIdx.x; b < nblk; b += kBlock) q.blk_off[b] = run0[b / per] + cnt[scan_pad(b)];
     if (threadIdx.x == 0) {
         q.blk_off[nblk] = total;
         *q.total = total;
     }
 }
+
+static_assert((uint64_t)(kSearchScanMax / kBlock) * kBlock * 128 * 128 < (1ull << 32),
+              "a scan run's offsets must fit 32 bits");
 
 // Start of a chunk: its bound is min(caller's bound, best so far).
 __global__ void search_bound_kernel(SearchParams q, uint32_t bound) {
