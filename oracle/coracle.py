@@ -57,6 +57,8 @@ def lib():
         _lib.oc_search.argtypes = [C.POINTER(_Problem), C.c_uint64, C.c_uint64, C.c_uint32, C.c_uint64,
                                    C.c_uint32, C.POINTER(C.c_uint64), C.POINTER(C.c_uint32),
                                    C.POINTER(C.c_uint64), C.c_int]
+        _lib.oc_finish_times.restype = C.c_int64
+        _lib.oc_finish_times.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int] + [C.c_void_p] * 7
         _lib.oc_dag_counts.restype = C.c_int
         _lib.oc_dag_counts.argtypes = [C.c_int, C.c_int] + [C.POINTER(C.c_int)] * 5
     return _lib
@@ -160,6 +162,25 @@ def search(prob, bound: int, first_row: int = 0, n_rows: Optional[int] = None, r
     out = {k: int(v) for k, v in zip(SEARCH_COUNTERS, cnt)}
     out["best"] = None if bi.value == 2**64 - 1 else (int(bi.value), int(bt.value))
     return out
+
+
+def finish_times(S: int, M: int, F, B, cf, cb, d=None, schedule: int = 0, V: int = 1):
+    """(T, fin_F, fin_B): the makespan and the finish time of every compute
+    node, fin_F[s-1, m-1] = finish(F_{s,m}) (likewise fin_B), for one
+    candidate's stage weights; d is the per-stage (per-device under
+    Interleaved 1F1B) all-reduce weight, or None."""
+    f = np.ascontiguousarray(F, dtype=np.uint64)
+    b = np.ascontiguousarray(B, dtype=np.uint64)
+    dd = None if d is None else np.ascontiguousarray(d, dtype=np.uint64)
+    tf = np.ascontiguousarray(cf if S > 1 else [0], dtype=np.uint32)
+    tb = np.ascontiguousarray(cb if S > 1 else [0], dtype=np.uint32)
+    fin_f = np.zeros((S, M), dtype=np.uint64)
+    fin_b = np.zeros((S, M), dtype=np.uint64)
+    T = lib().oc_finish_times(S, M, schedule, V, _ptr(f), _ptr(b), _ptr(dd), _ptr(tf), _ptr(tb),
+                              _ptr(fin_f), _ptr(fin_b))
+    if T < 0:
+        raise RuntimeError("oc_finish_times failed")
+    return int(T), fin_f, fin_b
 
 
 def dag_counts(S: int, M: int):

@@ -49,7 +49,10 @@ docstring; the list of readings:
   (k div VN) N + k mod N + 1, backward step k runs chunk V-1 - (k mod VN) div N
   on the same micro-batch; a warm-up of min(2(N-p-1) + (V-1) N, VM) forward
   steps (all VM of them if M = N), then pairs (forward step w+i, backward
-  step i), then the remaining backward steps.  The intra-stage edges follow
+  step i), then the remaining backward steps.  For M >= 2N that warm-up is
+  the one that keeps the device busy until its first backward can start and
+  starts it at once (with unit weights and no transfer time); with M = N no
+  warm-up can, and every forward runs first.  The intra-stage edges follow
   each device's order; one all-reduce node per device follows its last node
   and weighs the device's summed per-layer all-reduce time; a device fits
   when the summed memory of all its chunks' layers fits its cap.

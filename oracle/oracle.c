@@ -473,6 +473,31 @@ int oc_bounded(const oc_problem *p, uint64_t first, uint64_t count, const uint64
 }
 
 /* DAG shape for pins: compute nodes, edges by kind. */
+/* Finish time of every compute node of one pipeline under the given stage
+ * weights (Sec. 4.1, App. B.1): fin_F[(s-1) M + m-1] = finish(F_{s,m}),
+ * likewise fin_B; D (stage or device all-reduce weights) may be NULL.
+ * Returns T = finish(end), or -1 on a bad shape or allocation failure. */
+int64_t oc_finish_times(int S, int M, int schedule, int V, const uint64_t *F, const uint64_t *B,
+                        const uint64_t *D, const uint32_t *cf, const uint32_t *cb,
+                        uint64_t *fin_F, uint64_t *fin_B) {
+    if (S < 1 || S > 64 || M < 1 || schedule < 0 || schedule > 2) return -1;
+    if (schedule == 2 && (V < 2 || S % V || M % (S / V))) return -1;
+    oc_dag *g = dag_build(S, M, schedule, V);
+    if (!g) return -1;
+    uint64_t zero[64] = {0};
+    uint64_t *fin = malloc(sizeof(uint64_t) * (size_t)g->n);
+    if (!fin) { dag_free(g); return -1; }
+    uint64_t T = dag_longest(g, F, B, D ? D : zero, cf, cb, fin);
+    for (int s = 1; s <= S; ++s)
+        for (int m = 1; m <= M; ++m) {
+            fin_F[(size_t)(s - 1) * M + (m - 1)] = fin[idF(M, s, m)];
+            fin_B[(size_t)(s - 1) * M + (m - 1)] = fin[idB(M, s, m)];
+        }
+    free(fin);
+    dag_free(g);
+    return (int64_t)T;
+}
+
 int oc_dag_counts(int S, int M, int *n_nodes, int *n_fwd, int *n_bwd, int *n_intra, int *n_other) {
     oc_dag *g = dag_build(S, M, 0, 1);
     if (!g) return -1;

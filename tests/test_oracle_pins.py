@@ -705,3 +705,160 @@ def test_interleaved_weights_per_device():
     F, B, mem, d, ok = dag.interleaved_weights(prob, (1, 2, 3, 4, 5), (0, 1), ar)
     assert F == [1, 2 << 8, 4, 8 << 8, 16, 32 << 8] and B == [2 * x for x in F]
     assert mem == [0b010101, 0b101010] and d == [0b010101, 0b101010 << 8] and ok
+
+
+# ---------------------------- Interleaved 1F1B warm-up: the fill property
+
+def _python_finish_arrays(S, M, schedule, V, F, B):
+    T, fin = dag.longest_path(dag.dag_for(S, M, schedule, V), F, B, [0] * (S - 1), [0] * (S - 1),
+                              return_finish=True)
+    fF = np.array([[fin[("F", s, m)] for m in range(1, M + 1)] for s in range(1, S + 1)])
+    fB = np.array([[fin[("B", s, m)] for m in range(1, M + 1)] for s in range(1, S + 1)])
+    return T, fF, fB
+
+
+def _fill_violations(fin_F, fin_B, N, V, M):
+    """Devices (0-based) that break the interleaved warm-up's defining
+    property under unit node weights and no transfer time.
+
+    Every node then takes one time unit and a device runs one node at a
+    time, so the finish times of a device's nodes, sorted, are its order.
+    The warm-up of the interleaved schedule (Narayanan et al., the paper's
+    reference for it) is sized so that the device stays busy until its
+    first backward can start and starts that backward the moment its input
+    exists.  The earliest finish of B on virtual stage j (1-based) is the
+    chain F_{1,1} .. F_{S,1}, B_{S,1} .. B_{j,1}: S + (S - j + 1) nodes.
+    So: (a) the device's nodes up to its first backward finish at
+    consecutive times, and (b) that backward finishes at 2S - j + 1.
+    A warm-up one forward shorter leaves an idle unit before the first
+    backward (a fails); one forward longer delays it (b fails)."""
+    S = N * V
+    bad = []
+    for q in range(N):
+        stages = [j for j in range(S) if j % N == q]
+        tb, jb = min((int(fin_B[j, m]), j) for j in stages for m in range(M))
+        times = sorted(int(fin_F[j, m]) for j in stages for m in range(M))
+        times = sorted(times + [int(fin_B[j, m]) for j in stages for m in range(M)])
+        upto = [t for t in times if t <= tb]
+        if upto != list(range(upto[0], upto[0] + len(upto))) or tb != 2 * S - (jb + 1) + 1:
+            bad.append(q)
+    return bad
+
+
+_FILL_CASES = [(N, V, M) for N in range(2, 7) for V in range(2, 5) if N * V <= 18 for M in (2 * N, 3 * N)]
+
+
+def test_interleaved_warmup_fills_until_the_first_backward():
+    """Python and C oracles: with M >= 2N micro-batches every device of the
+    Interleaved 1F1B DAG satisfies the fill property (see
+    _fill_violations).  Both oracles' warm-up lengths are pinned by it;
+    the closed form (VM + N - 1)(f + b) does not separate a warm-up one
+    step shorter or longer."""
+    for N, V, M in _FILL_CASES:
+        S = N * V
+        _, fF, fB = _python_finish_arrays(S, M, 2, V, [1] * S, [1] * S)
+        assert _fill_violations(fF, fB, N, V, M) == [], (N, V, M)
+        _, cF, cB = coracle.finish_times(S, M, [1] * S, [1] * S, [0] * (S - 1), [0] * (S - 1), schedule=2, V=V)
+        assert _fill_violations(cF, cB, N, V, M) == [], (N, V, M)
+        assert (cF == fF).all() and (cB == fB).all()
+
+
+def test_interleaved_one_group_runs_every_forward_first():
+    """M = N micro-batches (one group): each device runs all V M forwards
+    before any backward, the special case of the interleaved schedule's
+    reference implementation (Megatron-LM), where no warm-up can fill the
+    time of the first device.  Checked on the C oracle's finish times with
+    unit weights; this case is structural, no closed form separates it."""
+    for N in range(2, 7):
+        for V in range(2, 4):
+            S = N * V
+            _, cF, cB = coracle.finish_times(S, N, [1] * S, [1] * S, [0] * (S - 1), [0] * (S - 1), schedule=2, V=V)
+            for q in range(N):
+                st = [j for j in range(S) if j % N == q]
+                assert max(int(cF[j].max()) for j in st) < min(int(cB[j].min()) for j in st)
+
+
+def _shifted_interleaved_order(delta):
+    def order(N, V, M, p):
+        q, total = p - 1, V * M
+        w = total if M == N else max(0, min(2 * (N - q - 1) + (V - 1) * N + delta, total))
+        mb = lambda k: (k // (N * V)) * N + k % N + 1                                    # noqa: E731
+        fwd = lambda k: ("F", ((k % (N * V)) // N) * N + q + 1, mb(k))                     # noqa: E731
+        bwd = lambda k: ("B", (V - 1 - (k % (N * V)) // N) * N + q + 1, mb(k))             # noqa: E731
+        o = [fwd(k) for k in range(w)]
+        for i in range(total - w):
+            o += [fwd(w + i), bwd(i)]
+        return o + [bwd(k) for k in range(total - w, total)]
+    return order
+
+
+@pytest.mark.parametrize("delta", [-1, 1])
+def test_planted_interleaved_warmup_mistakes_fail_the_fill_pin(delta, monkeypatch, tmp_path):
+    """A warm-up one forward shorter or longer, planted in the Python oracle
+    and in a copy of the C oracle, fails the fill property on every case."""
+    import ctypes
+    import subprocess
+
+    monkeypatch.setattr(dag, "interleaved_order", _shifted_interleaved_order(delta))
+    monkeypatch.setattr(dag, "_DAG_CACHE", {})
+    src = open(coracle.SRC).read()
+    expr = "2 * (N - q - 1) + (V - 1) * N"
+    assert src.count(expr) == 2
+    mutated = src.replace(expr, f"(2 * (N - q - 1) + (V - 1) * N + ({delta}))")
+    (tmp_path / "oracle.c").write_text(mutated)
+    so = tmp_path / "libmut.so"
+    subprocess.run(["gcc", "-O1", "-std=c11", "-shared", "-fPIC", "-pthread", str(tmp_path / "oracle.c"),
+                    "-o", str(so)], check=True)
+    mut = ctypes.CDLL(str(so))
+    mut.oc_finish_times.restype = ctypes.c_int64
+    mut.oc_finish_times.argtypes = [ctypes.c_int] * 4 + [ctypes.c_void_p] * 7
+    for N, V, M in _FILL_CASES:
+        S = N * V
+        _, fF, fB = _python_finish_arrays(S, M, 2, V, [1] * S, [1] * S)
+        assert _fill_violations(fF, fB, N, V, M), ("python", N, V, M)
+        one = np.ones(S, dtype=np.uint64)
+        zero = np.zeros(max(S - 1, 1), dtype=np.uint32)
+        cF = np.zeros((S, M), dtype=np.uint64)
+        cB = np.zeros((S, M), dtype=np.uint64)
+        assert mut.oc_finish_times(S, M, 2, V, one.ctypes.data, one.ctypes.data, None, zero.ctypes.data,
+                                   zero.ctypes.data, cF.ctypes.data, cB.ctypes.data) > 0
+        assert _fill_violations(cF, cB, N, V, M), ("C", N, V, M)
+
+
+# ------------------------------------------ Eq. 2's all-reduce term d_i
+
+def test_eq2_is_exact_for_one_stage_with_allreduce():
+    """S = 1: the stage runs its 2M nodes back to back and then its
+    all-reduce node, so T = M (f_1 + b_1) + d_1, which is exactly g(S_1) of
+    Eq. 2.  Python: eq2_bound equals that value and the DAG's T.  C: the
+    early-stop pass prunes the candidate at bound T - 1 and keeps it at T,
+    which fails if d_1 were dropped from either side (d_1 >= 1 here)."""
+    rng = np.random.default_rng(44)
+    for trial in range(40):
+        L, M, T = int(rng.integers(1, 6)), int(rng.integers(1, 20)), int(rng.integers(1, 4))
+        prob = W.random_problem(rng, L, 1, M, T, mem_hi=5, cap=1000)
+        prob.allreduce = rng.integers(1, 5000, size=(T, L)).astype(np.uint32)
+        for t in range(T):
+            f, b, d = int(prob.fwd[t].sum()), int(prob.bwd[t].sum()), int(prob.allreduce[t].sum())
+            exact = M * (f + b) + d
+            assert dag.eq2_bound([f], [b], M, [d]) == exact
+            assert dag.longest_path(dag.dag_for(1, M), [f], [b], [], [], [d]) == exact
+            cands = W.Candidates(first=t, count=1)
+            assert coracle.bounded(prob, cands, exact - 1)[1:3] == (0, 1)
+            best, ev, pr, _ = coracle.bounded(prob, cands, exact)
+            assert (ev, pr) == (1, 0) and best == (0, exact)
+
+
+def test_eq2_is_exact_when_the_last_stage_dominates():
+    """S = 2 with a weightless first stage and no transfer time: stage 2
+    runs alone, so T = M (f_2 + b_2) + max(d_1, d_2) (B_{1,M} ends with
+    B_{2,M}); Eq. 2's g(S_2) = M (f_2 + b_2) + max(b_1 + d_1, d_2) equals it."""
+    rng = np.random.default_rng(45)
+    for _ in range(60):
+        M = int(rng.integers(1, 12))
+        f2, b2 = int(rng.integers(1, 500)), int(rng.integers(1, 500))
+        d = [int(rng.integers(0, 3000)), int(rng.integers(0, 3000))]
+        exact = M * (f2 + b2) + max(d)
+        assert dag.longest_path(dag.dag_for(2, M), [0, f2], [0, b2], [0], [0], d) == exact
+        assert dag.eq2_bound([0, f2], [0, b2], M, d) == exact
+        assert coracle.finish_times(2, M, [0, f2], [0, b2], [0], [0], d=d)[0] == exact
