@@ -38,8 +38,11 @@
  * caller's table, or, without a table, the base-T digits of a with stage 1
  * the most significant digit.  In range mode candidate i of a call is the
  * joint index first + i = comp_rank * A + a; in list mode it is the pair
- * (comp_rank[i], assign_idx[i]).  "index" in results is always i, the
- * position within the call.
+ * (comp_rank[i], assign_idx[i]).  "index" in results of the evaluation
+ * calls is the joint index first + i in range mode and the position i in
+ * list mode; either way, among candidates with equal makespans the smallest
+ * index wins.  The search (poseidon_search) enumerates in its own order,
+ * assignment row first, and reports the first optimum in that order.
  *
  * Errors: 0 = OK, 1 = POSEIDON_NO_FEASIBLE (the call completed but no
  * candidate qualified; best.index = UINT64_MAX), negative = error.  All
@@ -61,6 +64,8 @@ extern "C" {
 #define POSEIDON_S_MAX 16   /* stages */
 #define POSEIDON_L_MAX 256  /* layers */
 #define POSEIDON_T_MAX 8    /* device types */
+#define POSEIDON_M_MAX (1u << 20)   /* micro-batches: the schedule the kernels hard-code is
+                                       checked against a simulation for every M up to this */
 
 /* Pipeline schedules (poseidon_problem.schedule). */
 enum {
@@ -85,7 +90,7 @@ typedef struct poseidon_ctx poseidon_ctx;
 /* Per-layer profile of one model on T device types (Sec. 4.1.3): all
  * HOST pointers, read during poseidon_load_costs only. */
 typedef struct {
-    uint32_t L, S, M, T;          /* 1 <= S <= min(L, S_MAX), M >= 1, 1 <= T <= T_MAX */
+    uint32_t L, S, M, T;          /* 1 <= S <= min(L, S_MAX), 1 <= M <= M_MAX, 1 <= T <= T_MAX */
     const uint32_t *fwd_us;       /* [T][L] forward time of layer l on type t */
     const uint32_t *bwd_us;       /* [T][L] backward time */
     const uint32_t *comm_fwd_us;  /* [S-1] weight of F_{b,m}->F_{b+1,m} (NULL iff S == 1) */
@@ -129,7 +134,8 @@ typedef struct {
 } poseidon_cands;
 
 typedef struct {
-    uint64_t index;     /* position within the call, UINT64_MAX if none */
+    uint64_t index;     /* range mode: joint index first + i; list mode: position i;
+                           UINT64_MAX if none */
     uint32_t makespan;  /* critical-path length T in microseconds */
     uint32_t feasible;  /* 1 if every stage fits its memory cap */
 } poseidon_best;
@@ -150,8 +156,11 @@ int poseidon_validate(const poseidon_problem *problem, uint64_t *n_candidates);
  * per-layer costs and memory, the Pascal table used to unrank compositions,
  * and the slot schedule of the problem's DAG for (S, M) and its schedule
  * (Sec. 5: the DAG depends only on the pipeline depth, so it is built once
- * and only re-weighted); the schedule the kernels hard-code is checked
- * against a simulation of it, and a mismatch fails with POSEIDON_E_INVAL.  Fails
+ * and only re-weighted).  For every problem, the slot pattern the kernels
+ * hard-code (1F1B with M >= S, Eager 1F1B with M >= 2S-1) is compared slot
+ * by slot with a simulation of the unit-weight schedule, and the
+ * Interleaved 1F1B program with the problem's own slot table; a mismatch
+ * fails with POSEIDON_E_INVAL.  Fails
  * with POSEIDON_E_RANGE if some candidate's makespan could reach 2^31.  The
  * caller may free the host tables after return; the context owns its device
  * memory until poseidon_free. */
@@ -171,8 +180,9 @@ int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands,
                              uint32_t *makespan_out, uint32_t *feasible_bits_out,
                              poseidon_best *best_out, void *hip_stream);
 
-/* Result of the most recent poseidon_eval_candidates on this context
- * (synchronises the stream). */
+/* Result of the most recent poseidon_eval_candidates (or poseidon_argmin)
+ * on this context, with the index as that call reported it (synchronises
+ * the stream). */
 int poseidon_last_best(poseidon_ctx *ctx, poseidon_best *best_out, void *hip_stream);
 
 /* Early-stop search (Eq. 2, Theorem 1).  The candidates are processed in

@@ -33,10 +33,21 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
 
 
-def build(verbose: bool = False, jobs: int = 0) -> str:
+def _stale(src: str, obj: str) -> bool:
+    """An object is stale when it is older than its source or any header."""
+    if not os.path.exists(obj):
+        return True
+    deps = [src] + glob.glob(os.path.join(CSRC, "*.h")) + glob.glob(os.path.join(ROOT, "include", "*.h"))
+    return os.path.getmtime(obj) < max(os.path.getmtime(d) for d in deps)
+
+
+def build(verbose: bool = False, jobs: int = 0, incremental: bool = False) -> str:
+    """Compile every source (or, with incremental, only stale objects) and
+    link the library."""
     os.makedirs(OBJ, exist_ok=True)
     srcs = sources()
     objs = [os.path.join(OBJ, os.path.basename(s) + ".o") for s in srcs]
+    todo = [(s, o) for s, o in zip(srcs, objs) if not incremental or _stale(s, o)]
 
     def compile_one(pair):
         src, obj = pair
@@ -46,10 +57,10 @@ def build(verbose: bool = False, jobs: int = 0) -> str:
         r = subprocess.run(cmd, capture_output=True, text=True)
         return src, r
 
-    jobs = jobs or min(len(srcs), max(1, os.cpu_count() or 1), 16)
+    jobs = jobs or min(max(len(todo), 1), max(1, os.cpu_count() or 1), 16)
     failed = []
     with ThreadPoolExecutor(max_workers=jobs) as ex:
-        for src, r in ex.map(compile_one, zip(srcs, objs)):
+        for src, r in ex.map(compile_one, todo):
             err = "\n".join(l for l in r.stderr.splitlines() if "packed-fp32-ops" not in l)
             if err.strip() and (verbose or r.returncode):
                 print(err, file=sys.stderr, flush=True)
@@ -67,4 +78,4 @@ def build(verbose: bool = False, jobs: int = 0) -> str:
 
 
 if __name__ == "__main__":
-    build(verbose="-v" in sys.argv)
+    build(verbose="-v" in sys.argv, incremental="-i" in sys.argv)

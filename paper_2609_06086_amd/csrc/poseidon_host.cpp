@@ -57,20 +57,27 @@ bool pow_fits(uint64_t base, uint64_t e, uint64_t limit, uint64_t *out) {
 // Order of stage s (1-based) under a schedule; kind 0 = F, 1 = B.
 //   1F1B:       min(S-s, M) forwards, then (F, B) pairs, then the remaining backwards.
 //   Eager 1F1B: min(2(S-s)+1, M) forwards, then (B, F) pairs, then the remaining backwards.
+// Node at position `pos` (0-based) of stage s's order, as (kind, m) with
+// kind 0 = forward, 1 = backward: w warm-up forwards, then M - w pairs
+// (F_{w+i}, B_i) under 1F1B or (B_i, F_{w+i}) under Eager 1F1B, then the
+// remaining backwards.
+std::pair<int, int> stage_node(int S, int M, int s, int schedule, int pos) {
+    const bool eager = schedule == POSEIDON_SCHEDULE_EAGER_1F1B;
+    const int w = eager ? std::min(2 * (S - s) + 1, M) : std::min(S - s, M);
+    if (pos < w) return {0, pos + 1};
+    const int q = pos - w;
+    if (q < 2 * (M - w)) {
+        const int i = q / 2 + 1;
+        const bool first_of_pair = (q & 1) == 0;
+        if (eager) return first_of_pair ? std::make_pair(1, i) : std::make_pair(0, w + i);
+        return first_of_pair ? std::make_pair(0, w + i) : std::make_pair(1, i);
+    }
+    return {1, M - w + 1 + (q - 2 * (M - w))};
+}
+
 void stage_order(int S, int M, int s, int schedule, std::vector<std::pair<int, int>> &o) {
     o.clear();
-    const int w = schedule == POSEIDON_SCHEDULE_EAGER_1F1B ? std::min(2 * (S - s) + 1, M) : std::min(S - s, M);
-    for (int m = 1; m <= w; ++m) o.push_back({0, m});
-    for (int i = 1; i <= M - w; ++i) {
-        if (schedule == POSEIDON_SCHEDULE_EAGER_1F1B) {
-            o.push_back({1, i});
-            o.push_back({0, w + i});
-        } else {
-            o.push_back({0, w + i});
-            o.push_back({1, i});
-        }
-    }
-    for (int m = M - w + 1; m <= M; ++m) o.push_back({1, m});
+    for (int pos = 0; pos < 2 * M; ++pos) o.push_back(stage_node(S, M, s, schedule, pos));
 }
 
 // Unit-weight as-soon-as-possible slots of every node of the DAG; fills
@@ -249,36 +256,62 @@ bool build_interleaved_slots(int N, int V, int M, int max_db, std::vector<uint32
     return true;
 }
 
-// The closed-form slot pattern the fast kernel path hard-codes, checked
-// against the simulated schedule (M >= S).
-bool closed_form_matches(int S, int M, const std::vector<uint32_t> &masks) {
-    const int n = 2 * (M + S - 1);
-    for (int k = 0; k < n; ++k) {
+// The closed-form slot pattern the kernels hard-code (1F1B with M >= S,
+// Eager 1F1B with M >= 2S-1), checked slot by slot against the unit-weight
+// as-soon-as-possible schedule, simulated here with O(S) state so that any
+// M is checked.  In slot k every stage whose next node's input finished in
+// an earlier slot runs that node.  The simulation also checks what the
+// stencil relies on: under 1F1B every input is still the newest node of its
+// stage (either kind); under Eager 1F1B a backward reads the newest backward
+// of the stage below and a forward the newest or second-newest forward of
+// the stage above (op 3 marks the second-newest).  Ops: 0 idle, 1 forward,
+// 2 backward, 3 forward reading the upstream's previous forward.
+bool closed_form_check(int S, int M, int schedule) {
+    const bool eager = schedule == POSEIDON_SCHEDULE_EAGER_1F1B;
+    // per stage: next position in its order, forwards / backwards done,
+    // kind of the newest node (-1 none); index 0 and S+1 are sentinels
+    std::vector<int> pos(S + 2, 0), nf(S + 2, 0), nb(S + 2, 0), last(S + 2, -1), op(S + 2, 0);
+    const int64_t n = 2 * ((int64_t)M + S - 1);
+    for (int64_t k = 0; k < n; ++k) {
         for (int s = 1; s <= S; ++s) {
-            int op;
-            if (k < 2 * S - 1) op = pk::prologue_op(S, s, k);
-            else if (k <= 2 * M - 1) op = ((k - s - 1) & 1) == 0 ? 1 : 2;
-            else op = pk::epilogue_op(S, s, k - 2 * M);
-            const int f = (masks[3 * k] >> (s - 1)) & 1u, b = (masks[3 * k + 2] >> (s - 1)) & 1u;
-            const int sim = f ? 1 : (b ? 2 : 0);
-            if (sim != op) return false;
+            op[s] = 0;
+            if (pos[s] >= 2 * M) continue;
+            const std::pair<int, int> v = stage_node(S, M, s, schedule, pos[s]);
+            const int m = v.second;
+            if (v.first == 0) {
+                if (s == 1) { op[s] = 1; continue; }
+                if (nf[s - 1] < m) continue;                     // input not finished
+                if (eager) {
+                    if (nf[s - 1] > m + 1) return false;          // more than one newer forward
+                    op[s] = nf[s - 1] == m + 1 ? 3 : 1;
+                } else {
+                    if (nf[s - 1] != m || last[s - 1] != 0) return false;
+                    op[s] = 1;
+                }
+            } else {
+                if (s == S) { op[s] = 2; continue; }
+                if (nb[s + 1] < m) continue;
+                if (nb[s + 1] != m || (!eager && last[s + 1] != 1)) return false;
+                op[s] = 2;
+            }
+        }
+        for (int s = 1; s <= S; ++s) {
+            int want;
+            if (eager) want = pk::eager_op(S, M, s, (int)k);
+            else if (k < 2 * S - 1) want = pk::prologue_op(S, s, (int)k);
+            else if (k <= 2 * (int64_t)M - 1) want = ((k - s - 1) & 1) == 0 ? 1 : 2;
+            else want = pk::epilogue_op(S, s, (int)(k - 2 * (int64_t)M));
+            if (op[s] != want) return false;
+            if (op[s]) {
+                ++pos[s];
+                if (op[s] == 2) ++nb[s];
+                else ++nf[s];
+                last[s] = op[s] == 2 ? 1 : 0;
+            }
         }
     }
-    return true;
-}
-
-// The Eager 1F1B closed form (M >= 2S-1), including which forwards read
-// the upstream stage's previous forward, checked against the simulation.
-bool eager_closed_form_matches(int S, int M, const std::vector<uint32_t> &masks) {
-    const int n = 2 * (M + S - 1);
-    if (masks.size() != 3 * (size_t)n) return false;
-    for (int k = 0; k < n; ++k)
-        for (int s = 1; s <= S; ++s) {
-            const int f = (masks[3 * k] >> (s - 1)) & 1u, d = (masks[3 * k + 1] >> (s - 1)) & 1u,
-                      b = (masks[3 * k + 2] >> (s - 1)) & 1u;
-            const int sim = f ? (d ? 3 : 1) : (b ? 2 : 0);
-            if (sim != pk::eager_op(S, M, s, k)) return false;
-        }
+    for (int s = 1; s <= S; ++s)
+        if (pos[s] != 2 * M) return false;
     return true;
 }
 
@@ -300,6 +333,8 @@ struct poseidon_ctx {
     void *sws;             // search frontiers (allocated on the first poseidon_search)
     unsigned long long *shost;   // pinned host words for the search's read-backs (level totals
                                  // and block offsets), allocated with sws
+    uint64_t result_base = 0;    // added to the position the last evaluation or argmin published:
+                                 // `first` in range mode (the joint index), else 0 or index_base
 };
 
 extern "C" {
@@ -318,7 +353,8 @@ const char *poseidon_strerror(int status) {
 
 int poseidon_validate(const poseidon_problem *p, uint64_t *n_candidates) {
     if (!p) return POSEIDON_E_INVAL;
-    if (p->S < 1 || p->S > POSEIDON_S_MAX || p->L < p->S || p->L > POSEIDON_L_MAX || p->M < 1 || p->T < 1 ||
+    if (p->S < 1 || p->S > POSEIDON_S_MAX || p->L < p->S || p->L > POSEIDON_L_MAX || p->M < 1 ||
+        p->M > POSEIDON_M_MAX || p->T < 1 ||
         p->T > POSEIDON_T_MAX)
         return POSEIDON_E_INVAL;
     if (!p->fwd_us || !p->bwd_us || !p->mem_mb || !p->cap_mb) return POSEIDON_E_INVAL;
@@ -394,11 +430,10 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     if (ilv) {
         if (!build_interleaved_slots((int)ndev, (int)p->V, (int)M, pk::ilv_max_db((int)ndev), &masks, &nslots))
             return POSEIDON_E_INVAL;
-    } else if (table_path || (uint64_t)S * M <= 4096) {
+    } else if (table_path) {
         if (!build_slots((int)S, (int)M, (int)sched, !eager, &masks, &nslots)) return POSEIDON_E_INVAL;
-        if (!table_path && !(eager ? eager_closed_form_matches((int)S, (int)M, masks)
-                                   : closed_form_matches((int)S, (int)M, masks)))
-            return POSEIDON_E_INVAL;
+    } else if (!closed_form_check((int)S, (int)M, (int)sched)) {
+        return POSEIDON_E_INVAL;
     }
 
     // host images of the device tables
@@ -627,7 +662,10 @@ struct DeviceGuard {
     }
 };
 
-int read_best(poseidon_ctx *ctx, hipStream_t st, unsigned long long word_index, poseidon_best *best) {
+// The device word holds (T << 32 | position within the call); the index
+// returned is base + position.
+int read_best(poseidon_ctx *ctx, hipStream_t st, unsigned long long word_index, uint64_t base,
+              poseidon_best *best) {
     unsigned long long w[W_COUNT];
     if (hipMemcpyAsync(w, ctx->state, sizeof(w), hipMemcpyDeviceToHost, st) != hipSuccess ||
         hipStreamSynchronize(st) != hipSuccess)
@@ -644,7 +682,7 @@ int read_best(poseidon_ctx *ctx, hipStream_t st, unsigned long long word_index, 
         best->feasible = 0;
         return POSEIDON_NO_FEASIBLE;
     }
-    best->index = k & 0xFFFFFFFFull;
+    best->index = base + (k & 0xFFFFFFFFull);
     best->makespan = (uint32_t)(k >> 32);
     best->feasible = 1;
     return POSEIDON_OK;
@@ -714,10 +752,11 @@ int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands, uin
     hipStream_t st = (hipStream_t)hip_stream;
     DeviceGuard g(ctx->device);
     if (!g.ok) return POSEIDON_E_DEVICE;
+    ctx->result_base = cands->comp_rank ? 0 : cands->first;
     if (cands->count == 0) {
         // nothing to evaluate: publish an empty result
         if (pk::launch_fill(ctx->base.result, 1, ~0ull, st) != hipSuccess) return POSEIDON_E_DEVICE;
-        if (best_out) return read_best(ctx, st, W_RESULT, best_out);
+        if (best_out) return read_best(ctx, st, W_RESULT, ctx->result_base, best_out);
         return POSEIDON_OK;
     }
     pk::KParams kp = ctx->base;
@@ -759,7 +798,7 @@ int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands, uin
         for (uint32_t l = 1; l <= kp.nlevels; ++l)
             if (pk::launch_resume(kp, lc, st, l) != hipSuccess) return rearm(ctx, st);
     }
-    if (best_out) return read_best(ctx, st, W_RESULT, best_out);
+    if (best_out) return read_best(ctx, st, W_RESULT, ctx->result_base, best_out);
     return POSEIDON_OK;
 }
 
@@ -767,7 +806,7 @@ int poseidon_last_best(poseidon_ctx *ctx, poseidon_best *best_out, void *hip_str
     if (!ctx || !best_out) return POSEIDON_E_INVAL;
     DeviceGuard g(ctx->device);
     if (!g.ok) return POSEIDON_E_DEVICE;
-    return read_best(ctx, (hipStream_t)hip_stream, W_RESULT, best_out);
+    return read_best(ctx, (hipStream_t)hip_stream, W_RESULT, ctx->result_base, best_out);
 }
 
 int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *cands, uint32_t bound,
@@ -838,7 +877,8 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
         b.index = UINT64_MAX; b.makespan = 0xFFFFFFFFu; b.feasible = 0;
         out = POSEIDON_NO_FEASIBLE;
     } else {
-        b.index = k & 0xFFFFFFFFull; b.makespan = (uint32_t)(k >> 32); b.feasible = 1;
+        b.index = (cands->comp_rank ? 0 : cands->first) + (k & 0xFFFFFFFFull);
+        b.makespan = (uint32_t)(k >> 32); b.feasible = 1;
         out = POSEIDON_OK;
     }
     if (best_out) *best_out = b;
@@ -860,9 +900,8 @@ int poseidon_argmin(poseidon_ctx *ctx, const uint32_t *makespan, const uint32_t 
                               st) != hipSuccess)
             return POSEIDON_E_DEVICE;
     }
-    int rc = read_best(ctx, st, W_RESULT, best_out);
-    if (rc == POSEIDON_OK) best_out->index += index_base;
-    return rc;
+    ctx->result_base = index_base;
+    return read_best(ctx, st, W_RESULT, index_base, best_out);
 }
 
 }  // extern "C"

@@ -26,7 +26,7 @@ POSEIDON_E_DEVICE = -3
 POSEIDON_E_NOMEM = -4
 SCHEDULE_1F1B, SCHEDULE_EAGER_1F1B, SCHEDULE_INTERLEAVED_1F1B = 0, 1, 2
 SEARCH_RIDGE, SEARCH_NO_STAGE_PRUNING, SEARCH_RAMP = 1, 2, 4
-S_MAX, L_MAX, T_MAX = 16, 256, 8
+S_MAX, L_MAX, T_MAX, M_MAX = 16, 256, 8, 1 << 20
 
 
 class PoseidonError(RuntimeError):
@@ -226,7 +226,9 @@ def poseidon_eval_candidates(ctx: Context, *, first: int = 0, count: int = 0, co
                              assign_idx=None, makespan_out=None, feasible_bits_out=None,
                              want_best: bool = True, stream=None) -> Optional[Best]:
     """Range mode (first, count) or list mode (comp_rank[, assign_idx]
-    device tensors).  Returns the best (synchronising) if want_best."""
+    device tensors).  Returns the best (synchronising) if want_best; its
+    index is the joint index first + i in range mode, the position i in
+    list mode."""
     c = _cands(first, count, comp_rank, assign_idx)
     b = _Best()
     rc = lib().poseidon_eval_candidates(ctx.handle, C.byref(c), _addr(makespan_out), _addr(feasible_bits_out),

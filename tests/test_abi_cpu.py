@@ -125,12 +125,24 @@ def test_closed_form_schedules_pass_the_host_self_check():
     rng = np.random.default_rng(4)
     for sched in (P.SCHEDULE_1F1B, P.SCHEDULE_EAGER_1F1B):
         for S in range(1, 17):
-            for M in list(range(1, 2 * S + 6)) + [64, 255]:
-                p = W.random_problem(rng, S + 2, S, M, 1)
+            Ms = list(range(1, 2 * S + 6)) + [64, 255, 256, 600, 2048]
+            if S in (8, 15, 16):
+                Ms += [4097, 65537, P.M_MAX]
+            for M in Ms:
+                p = W.random_problem(rng, S + 2, S, M, 1, cost_lo=0, cost_hi=0 if M > 60000 else 1000,
+                                     comm_hi=0 if M > 60000 else 100)
                 p.schedule = sched
                 with pytest.raises(P.PoseidonError) as ei:
                     P.poseidon_load_costs(p, 0)
                 assert ei.value.status == P.POSEIDON_E_DEVICE, (sched, S, M)
+
+
+def test_micro_batch_limit():
+    """M above POSEIDON_M_MAX (2^20) is refused before any device call."""
+    p = W.random_problem(np.random.default_rng(9), 20, 16, P.M_MAX, 2, cost_lo=0, cost_hi=0, comm_hi=0)
+    assert P.poseidon_validate(p) > 0
+    p.M = P.M_MAX + 1
+    assert _status(p) == P.POSEIDON_E_INVAL
 
 
 def test_search_rejects_bad_arguments_before_device():

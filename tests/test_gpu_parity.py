@@ -7,6 +7,7 @@ digests of the full output arrays and the argmin with values the committed
 script tests/golden/make_golden.py wrote from the oracle.
 """
 import hashlib
+import itertools
 import json
 import math
 import os
@@ -75,9 +76,14 @@ def check_against_oracle(prob, cands, dev, python_oracle=False):
     if ob is None:
         assert best.status == P.POSEIDON_NO_FEASIBLE and best.index is None
     else:
-        assert (best.index, best.makespan) == ob
+        # range mode reports the joint index first + position, list mode the position
+        assert (best.index, best.makespan) == (ob[0] + index_base(cands), ob[1])
     ctx.close()
     return Tg, fg, best
+
+
+def index_base(cands):
+    return 0 if cands.is_list else cands.first
 
 
 # ------------------------------------------------------------ named workloads
@@ -165,6 +171,48 @@ def test_random_problems_python_oracle(dev):
         check_against_oracle(prob, W.Candidates(first=0, count=prob.n_candidates), dev, python_oracle=True)
 
 
+def _lex_rank(L, cuts):
+    """Lexicographic rank of a sorted cut tuple among all (S-1)-subsets of
+    {1..L-1}: the tuples that share the first j-1 cuts and have a smaller
+    j-th cut come first."""
+    k, r, prev = len(cuts), 0, 0
+    for j, c in enumerate(cuts, start=1):
+        for v in range(prev + 1, c):
+            r += math.comb(L - 1 - v, k - j)
+        prev = c
+    return r
+
+
+def test_memory_cap_equality_is_feasible(dev):
+    """A stage whose memory equals its type's cap fits; one MB less does not
+    (Sec. 3.2; the comparison is inclusive), through the evaluation, the
+    early-stop pass and the search.  Every layer takes 100 MB, so a stage of
+    n layers takes 100 n MB."""
+    rng = np.random.default_rng(115)
+    for S, L in ((1, 4), (3, 9), (8, 20), (16, 30)):
+        prob = W.random_problem(rng, L, S, 2 * S, 2, cost_hi=300, mem_lo=100, mem_hi=100, assign_rows=1)
+        prob.assign = np.zeros((1, S), np.uint8)
+        counts = np.array([len(c) for c in np.array_split(np.arange(L), S)])
+        cuts = tuple(int(x) for x in np.cumsum(counts)[:-1])
+        rank = _lex_rank(L, cuts)
+        assert dag.unrank_composition(L, S, rank) == cuts
+        cands = W.Candidates(comp_rank=np.array([rank], np.uint64), assign_idx=np.array([0], np.uint32))
+        for cap, ok in ((100 * int(counts.max()), True), (100 * int(counts.max()) - 1, False)):
+            prob.cap = np.array([cap, cap], np.uint32)
+            _, fg, best = check_against_oracle(prob, cands, dev)
+            assert bool(fg[0]) == ok and (best.index == 0) == ok
+            b, st = bounded_vs_oracle(prob, cands, 2 ** 31 - 1, 0, dev)
+            assert (st.evaluated, st.infeasible) == ((1, 0) if ok else (0, 1))
+        if S > 1:
+            # every composition of the single row, cap equal to the largest stage of the balanced one
+            prob.cap = np.array([100 * int(counts.max())] * 2, np.uint32)
+            ctx = P.poseidon_load_costs(prob, 0)
+            b, st = P.poseidon_search(ctx, 2 ** 31 - 1)
+            o = coracle.search(prob, 2 ** 31 - 1)
+            ctx.close()
+            assert (b.index, b.makespan) == o["best"] and st.pruned_memory == o["pruned_memory"] > 0
+
+
 def test_duplicates_tie_to_smallest_index(dev):
     wl = W.workload(2)
     rng = np.random.default_rng(104)
@@ -196,8 +244,42 @@ def test_empty_and_single(dev):
     T = torch.zeros(1, dtype=torch.int32, device=dev)
     b = P.poseidon_eval_candidates(ctx, first=71919, count=1, makespan_out=T)
     assert int(T.cpu().numpy().view(np.uint32)[0]) == int(To[0])
-    assert (b.index, b.makespan) == (0, int(To[0]))
+    assert (b.index, b.makespan) == (71919, int(To[0]))
     ctx.close()
+
+
+def test_range_mode_reports_the_joint_index(dev):
+    """Range mode: best.index is the joint index rank * A + a of the winning
+    candidate (not its position in the call), for the evaluation, the
+    early-stop pass and poseidon_last_best.  The expected index comes from
+    enumerating the candidates in the oracle's own order."""
+    rng = np.random.default_rng(150)
+    for trial in range(8):
+        S = int(rng.integers(2, 5))
+        L = S + int(rng.integers(1, 6))
+        T = int(rng.integers(2, 4))
+        prob = W.random_problem(rng, L, S, int(rng.integers(1, 12)), T, mem_hi=30, cap=int(rng.integers(60, 150)),
+                                assign_rows=None if trial % 2 else 5)
+        n = prob.n_candidates
+        first = int(rng.integers(1, n // 2 + 1))
+        count = n - first
+        lst = dag.candidate_list(prob, W.Candidates(first=0, count=n))
+        To, fo = dag.evaluate(prob, W.Candidates(first=0, count=n))
+        win = min((int(To[i]), i) for i in range(first, n) if fo[i]) if fo[first:].any() else None
+        ctx = P.poseidon_load_costs(prob, 0)
+        b = P.poseidon_eval_candidates(ctx, first=first, count=count)
+        lb = P.poseidon_last_best(ctx)
+        bb, _ = P.poseidon_eval_candidates_bounded(ctx, 2 ** 31 - 1, chunk=3, first=first, count=count)
+        ctx.close()
+        if win is None:
+            assert b.index is None and bb.index is None
+            continue
+        t, i = win
+        cuts, types = lst[i][1], lst[i][2]
+        rank = list(itertools.combinations(range(1, L), S - 1)).index(tuple(cuts))
+        a = dag.all_assignments(prob).index(tuple(types))
+        assert rank * prob.A + a == i
+        assert (b.index, b.makespan) == (lb.index, lb.makespan) == (bb.index, bb.makespan) == (i, t)
 
 
 def test_invalid_rank_in_list_reports_einval(dev):
@@ -288,7 +370,7 @@ def bounded_vs_oracle(prob, cands, bound, chunk, dev):
     b, st = P.poseidon_eval_candidates_bounded(ctx, bound, chunk=chunk, **to_dev(cands, dev))
     ob, ev, pr, inf = coracle.bounded(prob, cands, bound, chunk)
     got = (b.index, b.makespan) if b.index is not None else None
-    assert got == ob
+    assert got == (None if ob is None else (ob[0] + index_base(cands), ob[1]))
     assert (st.evaluated, st.pruned, st.infeasible) == (ev, pr, inf)
     ctx.close()
     return b, st
@@ -526,6 +608,20 @@ def test_eager_closed_form_edges(dev):
                                 assign_rows=None if 2 ** S < 5000 else 5)
         prob.schedule = P.SCHEDULE_EAGER_1F1B
         check_against_oracle(prob, W.random_candidates(rng, prob, int(rng.integers(100, 1200))), dev)
+
+
+def test_long_pipelines_both_schedules(dev):
+    """S * M well above 4096 under 1F1B and Eager 1F1B (the closed forms'
+    host check simulates every M), with and without all-reduce times."""
+    rng = np.random.default_rng(114)
+    for schedule in (P.SCHEDULE_1F1B, P.SCHEDULE_EAGER_1F1B):
+        for S, M in ((16, 300), (8, 700), (12, 1001)):
+            prob = W.random_problem(rng, S + 9, S, M, 2, cost_hi=300, comm_hi=60, mem_hi=30, cap=300,
+                                    assign_rows=None if 2 ** S < 5000 else 6)
+            prob.schedule = schedule
+            if M == 700:
+                _with_allreduce(rng, prob, hi=400 * M)
+            check_against_oracle(prob, W.random_candidates(rng, prob, 2500), dev)
 
 
 def test_eager_python_oracle_and_bounded(dev):
