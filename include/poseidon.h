@@ -180,6 +180,28 @@ int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands,
                              uint32_t *makespan_out, uint32_t *feasible_bits_out,
                              poseidon_best *best_out, void *hip_stream);
 
+/* The same evaluation as poseidon_eval_candidates (same arguments, outputs,
+ * index and status semantics), for callers that cannot allocate device
+ * memory during the call: code under stream capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  It allocates nothing.  Instead of the
+ * context's workspace it uses a fixed scratch array of
+ * POSEIDON_NOALLOC_SCRATCH_BYTES that the library holds once per GPU (from
+ * its first poseidon_load_costs on that GPU until the process ends), and it
+ * processes the call in chunks sized so that the cut codes and straggler
+ * queues of one chunk fit that array (2^18 candidates per chunk for
+ * S = 16 under 1F1B, 2^17 under Eager 1F1B; more chunks mean more launches
+ * than poseidon_eval_candidates needs).  Nothing in the scratch needs clearing:
+ * every word a kernel reads was written earlier in the same chunk.  All
+ * calls on one GPU share its array, so calls of this function that overlap
+ * in time on one GPU (other threads, other streams) race and give wrong
+ * results; serialise them.  Returns POSEIDON_E_RANGE if even the smallest
+ * chunk of the problem does not fit the scratch, POSEIDON_E_DEVICE if the
+ * scratch could not be located on the context's GPU. */
+#define POSEIDON_NOALLOC_SCRATCH_BYTES (64u << 20)
+int poseidon_eval_candidates_noalloc(poseidon_ctx *ctx, const poseidon_cands *cands,
+                                     uint32_t *makespan_out, uint32_t *feasible_bits_out,
+                                     poseidon_best *best_out, void *hip_stream);
+
 /* Result of the most recent poseidon_eval_candidates (or poseidon_argmin)
  * on this context, with the index as that call reported it (synchronises
  * the stream). */

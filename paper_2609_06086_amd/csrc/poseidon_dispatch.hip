@@ -4,9 +4,47 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
+#include "../../include/poseidon.h"
 #include "poseidon_search.h"
 
 namespace pk {
+
+// Scratch of poseidon_eval_candidates_noalloc: one copy per GPU, resident
+// from the code object's load until the process ends.  In host code
+// `scratch` names a host-side stand-in, not device memory, so host code
+// only ever uses the address hipGetSymbolAddress returns for the current
+// device.
+static __device__ __align__(256) uint32_t scratch[POSEIDON_NOALLOC_SCRATCH_BYTES / 4];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+bool g_scratch_done[kMaxDevices];
+void *g_scratch_ptr[kMaxDevices];
+}  // namespace
+
+void *noalloc_scratch(int device) {
+    if (device < 0 || device >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_done[device]) {
+        g_scratch_done[device] = true;
+        int prev = 0;
+        void *ptr = nullptr;
+        if (hipGetDevice(&prev) == hipSuccess && hipSetDevice(device) == hipSuccess) {
+            if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) {
+                (void)hipGetLastError();
+                ptr = nullptr;
+            }
+            (void)hipSetDevice(prev);
+        }
+        g_scratch_ptr[device] = ptr;
+    }
+    return g_scratch_ptr[device];
+}
+
+size_t noalloc_scratch_bytes() { return sizeof(scratch); }
 
 #define PK_EXTERN(S)                                                                                     \
     extern template hipError_t launch_eval_s<S, uint32_t>(const KParams &, const LaunchCfg &, hipStream_t);    \

@@ -317,6 +317,11 @@ bool closed_form_check(int S, int M, int schedule) {
 
 }  // namespace
 
+struct poseidon_ctx;
+namespace {
+uint64_t noalloc_chunk_for(const poseidon_ctx *ctx);
+}  // namespace
+
 struct poseidon_ctx {
     int device;
     uint32_t L, S, M, T;
@@ -335,6 +340,8 @@ struct poseidon_ctx {
                                  // and block offsets), allocated with sws
     uint64_t result_base = 0;    // added to the position the last evaluation or argmin published:
                                  // `first` in range mode (the joint index), else 0 or index_base
+    void *scratch;               // the library's fixed scratch on this device (allocation-free calls)
+    uint64_t noalloc_chunk;      // candidates per chunk whose workspace fits that scratch (0: none)
 };
 
 extern "C" {
@@ -619,6 +626,10 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     ctx->A = A; ctx->n_comp = n_comp; ctx->wide = wide; ctx->NB = NB;
     ctx->base = kp;
     ctx->dmem = d;
+    // the allocation-free evaluation's scratch on this device (looked up once
+    // per device) and the chunk size whose workspace fits it
+    ctx->scratch = pk::noalloc_scratch(hip_device);
+    ctx->noalloc_chunk = noalloc_chunk_for(ctx);
     *out = ctx;
     return POSEIDON_OK;
 }
@@ -741,6 +752,81 @@ int rearm(poseidon_ctx *ctx, hipStream_t st) {
     return POSEIDON_E_DEVICE;
 }
 
+// Grid of the evaluation kernels for a chunk of n candidates, and the queue
+// slots its blocks own: block b of every level holds seg_cap entries, so a
+// chunk's queues need grid * seg_cap slots (non-decreasing in n).
+struct ChunkGrid {
+    uint32_t grid;
+    uint64_t seg_cap;
+};
+ChunkGrid chunk_grid(const poseidon_ctx *ctx, uint64_t n) {
+    ChunkGrid g;
+    g.grid = (uint32_t)std::min<uint64_t>((n + 255) / 256, ctx->grid_max);
+    const uint64_t stride = (uint64_t)g.grid * 256;
+    g.seg_cap = (n + stride - 1) / stride * 256;
+    return g;
+}
+
+// Largest power-of-two chunk (at least one wave) whose cut codes, straggler
+// queues and queue counts fit the allocation-free scratch; 0 if none does.
+uint64_t noalloc_chunk_for(const poseidon_ctx *ctx) {
+    const uint64_t words = (uint64_t)pk::code_words((int)ctx->S), ent = 1 + words + queue_state_words(ctx);
+    const uint64_t cap_words = pk::noalloc_scratch_bytes() / 4;
+    for (uint64_t n = kChunk; n >= 64; n >>= 1) {
+        const ChunkGrid g = chunk_grid(ctx, n);
+        uint64_t need = words * n;
+        if (ctx->base.nlevels) need += 2 * ent * g.grid * g.seg_cap + (uint64_t)pk::kMaxLevels * g.grid;
+        if (need <= cap_words) return n;
+    }
+    return 0;
+}
+
+// One evaluation call in chunks of at most `chunk` candidates on a
+// workspace: cut codes [words][ccap] at `codes`; with a cascade, two
+// straggler queues of qcap entries of (1 + words + state words) at `queues`,
+// followed by the per-block queue counts [levels][grid].
+int eval_chunks(poseidon_ctx *ctx, const poseidon_cands *cands, uint32_t *makespan_out,
+                uint32_t *feasible_bits_out, poseidon_best *best_out, hipStream_t st, uint64_t chunk,
+                uint32_t *codes, uint64_t ccap, uint32_t *queues, uint64_t qcap) {
+    pk::KParams kp = ctx->base;
+    kp.first = cands->first;
+    kp.count = cands->count;
+    kp.comp_rank = cands->comp_rank;
+    kp.assign_idx = cands->assign_idx;
+    kp.makespan_out = makespan_out;
+    kp.feas_bits_out = feasible_bits_out;
+    kp.nwords = (cands->count + 31) / 32;
+    const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
+    kp.codes = codes;
+    kp.ccap = ccap;
+    if (kp.nlevels) {
+        kp.qcap = qcap;
+        kp.queue[0] = queues;
+        kp.queue[1] = kp.queue[0] + (1 + words + queue_state_words(ctx)) * kp.qcap;
+        kp.qcount = kp.queue[1] + (1 + words + queue_state_words(ctx)) * kp.qcap;
+    }
+    for (uint64_t c0 = 0; c0 < cands->count; c0 += chunk) {
+        kp.first_i = c0;
+        kp.n_i = std::min(chunk, cands->count - c0);
+        kp.accumulate = c0 > 0;
+        const ChunkGrid g = chunk_grid(ctx, kp.n_i);
+        pk::LaunchCfg lc;
+        lc.lds_bytes = ctx->lds_bytes;
+        lc.grid = g.grid;
+        // queue segments: block b of every level owns seg_cap slots
+        kp.nseg = lc.grid;
+        kp.seg_cap = g.seg_cap;
+        pk::LaunchCfg ld = lc;
+        ld.grid = (uint32_t)std::min<uint64_t>((kp.n_i + 4 * 256 - 1) / (4 * 256), ctx->grid_max);
+        if (pk::launch_decode(kp, ld, st) != hipSuccess) return rearm(ctx, st);
+        if (pk::launch_eval(kp, lc, st) != hipSuccess) return rearm(ctx, st);
+        for (uint32_t l = 1; l <= kp.nlevels; ++l)
+            if (pk::launch_resume(kp, lc, st, l) != hipSuccess) return rearm(ctx, st);
+    }
+    if (best_out) return read_best(ctx, st, W_RESULT, ctx->result_base, best_out);
+    return POSEIDON_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -759,47 +845,39 @@ int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands, uin
         if (best_out) return read_best(ctx, st, W_RESULT, ctx->result_base, best_out);
         return POSEIDON_OK;
     }
-    pk::KParams kp = ctx->base;
-    kp.first = cands->first;
-    kp.count = cands->count;
-    kp.comp_rank = cands->comp_rank;
-    kp.assign_idx = cands->assign_idx;
-    kp.makespan_out = makespan_out;
-    kp.feas_bits_out = feasible_bits_out;
-    kp.nwords = (cands->count + 31) / 32;
     const uint64_t chunk = std::min<uint64_t>(cands->count, kChunk);
     rc = ensure_workspace(ctx, chunk, st);
     if (rc != POSEIDON_OK) return rc;
-    const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
+    // workspace: cut codes [words][cap], survivor indices [cap] and counts
+    // [grid_max] of the early-stop pass, then the straggler queues
     uint32_t *ws = (uint32_t *)ctx->ws;
-    kp.codes = ws;
-    kp.ccap = ctx->ws_cap;
-    if (kp.nlevels) {
-        kp.qcap = queue_cap(ctx, ctx->ws_cap);
-        kp.queue[0] = ws + (words + 1) * ctx->ws_cap + ctx->grid_max;
-        kp.queue[1] = kp.queue[0] + (1 + words + queue_state_words(ctx)) * kp.qcap;
-        kp.qcount = kp.queue[1] + (1 + words + queue_state_words(ctx)) * kp.qcap;
+    const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
+    return eval_chunks(ctx, cands, makespan_out, feasible_bits_out, best_out, st, chunk, ws, ctx->ws_cap,
+                       ws + (words + 1) * ctx->ws_cap + ctx->grid_max, queue_cap(ctx, ctx->ws_cap));
+}
+
+int poseidon_eval_candidates_noalloc(poseidon_ctx *ctx, const poseidon_cands *cands, uint32_t *makespan_out,
+                                     uint32_t *feasible_bits_out, poseidon_best *best_out, void *hip_stream) {
+    int rc = check_cands(ctx, cands);
+    if (rc != POSEIDON_OK) return rc;
+    if (!ctx->scratch) return POSEIDON_E_DEVICE;
+    if (ctx->noalloc_chunk == 0) return POSEIDON_E_RANGE;
+    hipStream_t st = (hipStream_t)hip_stream;
+    DeviceGuard g(ctx->device);
+    if (!g.ok) return POSEIDON_E_DEVICE;
+    ctx->result_base = cands->comp_rank ? 0 : cands->first;
+    if (cands->count == 0) {
+        if (pk::launch_fill(ctx->base.result, 1, ~0ull, st) != hipSuccess) return POSEIDON_E_DEVICE;
+        if (best_out) return read_best(ctx, st, W_RESULT, ctx->result_base, best_out);
+        return POSEIDON_OK;
     }
-    for (uint64_t c0 = 0; c0 < cands->count; c0 += chunk) {
-        kp.first_i = c0;
-        kp.n_i = std::min(chunk, cands->count - c0);
-        kp.accumulate = c0 > 0;
-        pk::LaunchCfg lc;
-        lc.lds_bytes = ctx->lds_bytes;
-        lc.grid = (uint32_t)std::min<uint64_t>((kp.n_i + 255) / 256, ctx->grid_max);
-        // queue segments: block b of every level owns seg_cap slots
-        const uint64_t stride = (uint64_t)lc.grid * 256;
-        kp.nseg = lc.grid;
-        kp.seg_cap = (kp.n_i + stride - 1) / stride * 256;
-        pk::LaunchCfg ld = lc;
-        ld.grid = (uint32_t)std::min<uint64_t>((kp.n_i + 4 * 256 - 1) / (4 * 256), ctx->grid_max);
-        if (pk::launch_decode(kp, ld, st) != hipSuccess) return rearm(ctx, st);
-        if (pk::launch_eval(kp, lc, st) != hipSuccess) return rearm(ctx, st);
-        for (uint32_t l = 1; l <= kp.nlevels; ++l)
-            if (pk::launch_resume(kp, lc, st, l) != hipSuccess) return rearm(ctx, st);
-    }
-    if (best_out) return read_best(ctx, st, W_RESULT, ctx->result_base, best_out);
-    return POSEIDON_OK;
+    // scratch: cut codes [words][chunk], then the straggler queues
+    const uint64_t chunk = ctx->noalloc_chunk;
+    const ChunkGrid cg = chunk_grid(ctx, chunk);
+    uint32_t *scr = (uint32_t *)ctx->scratch;
+    const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
+    return eval_chunks(ctx, cands, makespan_out, feasible_bits_out, best_out, st, chunk, scr, chunk,
+                       scr + words * chunk, (uint64_t)cg.grid * cg.seg_cap);
 }
 
 int poseidon_last_best(poseidon_ctx *ctx, poseidon_best *best_out, void *hip_stream) {

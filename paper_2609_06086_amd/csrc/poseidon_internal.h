@@ -140,6 +140,11 @@ bool ilv_program_words(uint32_t S, uint32_t N, int *start, int *tail, uint32_t *
 hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,
                          unsigned long long *acc, unsigned int *done, unsigned long long *result, hipStream_t st);
 hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, hipStream_t st);
+// Scratch of the allocation-free evaluation: the device address of the
+// library's fixed scratch array on `device`, looked up once per device
+// (with that device current) and kept; null if the lookup failed.
+void *noalloc_scratch(int device);
+size_t noalloc_scratch_bytes();
 hipError_t launch_search(int op, const KParams &p, const SearchParams &q, uint32_t grid, size_t lds, hipStream_t st);
 hipError_t launch_search_scan(const SearchParams &q, uint32_t nblk, hipStream_t st);
 hipError_t launch_search_bound(const SearchParams &q, uint32_t bound, hipStream_t st);

@@ -86,8 +86,8 @@ class SearchStats:
 
 
 EXPORTS = ("poseidon_validate", "poseidon_load_costs", "poseidon_eval_candidates",
-           "poseidon_last_best", "poseidon_eval_candidates_bounded", "poseidon_argmin",
-           "poseidon_search", "poseidon_free", "poseidon_strerror")
+           "poseidon_eval_candidates_noalloc", "poseidon_last_best", "poseidon_eval_candidates_bounded",
+           "poseidon_argmin", "poseidon_search", "poseidon_free", "poseidon_strerror")
 
 _lib = None
 
@@ -106,6 +106,8 @@ def lib():
         L.poseidon_eval_candidates.argtypes = [C.c_void_p, C.POINTER(_Cands), C.c_void_p, C.c_void_p,
                                                C.POINTER(_Best), C.c_void_p]
         L.poseidon_eval_candidates.restype = C.c_int
+        L.poseidon_eval_candidates_noalloc.argtypes = L.poseidon_eval_candidates.argtypes
+        L.poseidon_eval_candidates_noalloc.restype = C.c_int
         L.poseidon_last_best.argtypes = [C.c_void_p, C.POINTER(_Best), C.c_void_p]
         L.poseidon_last_best.restype = C.c_int
         L.poseidon_eval_candidates_bounded.argtypes = [C.c_void_p, C.POINTER(_Cands), C.c_uint32, C.c_uint64,
@@ -235,6 +237,21 @@ def poseidon_eval_candidates(ctx: Context, *, first: int = 0, count: int = 0, co
                                         C.byref(b) if want_best else None, _stream(stream))
     if rc < 0:
         raise PoseidonError(rc, "poseidon_eval_candidates")
+    return _best(rc, b) if want_best else None
+
+
+def poseidon_eval_candidates_noalloc(ctx: Context, *, first: int = 0, count: int = 0, comp_rank=None,
+                                     assign_idx=None, makespan_out=None, feasible_bits_out=None,
+                                     want_best: bool = True, stream=None) -> Optional[Best]:
+    """poseidon_eval_candidates on the library's fixed per-GPU scratch (no
+    device allocation during the call); same arguments and results."""
+    c = _cands(first, count, comp_rank, assign_idx)
+    b = _Best()
+    rc = lib().poseidon_eval_candidates_noalloc(ctx.handle, C.byref(c), _addr(makespan_out),
+                                                _addr(feasible_bits_out), C.byref(b) if want_best else None,
+                                                _stream(stream))
+    if rc < 0:
+        raise PoseidonError(rc, "poseidon_eval_candidates_noalloc")
     return _best(rc, b) if want_best else None
 
 
