@@ -322,6 +322,8 @@ namespace {
 uint64_t noalloc_chunk_for(const poseidon_ctx *ctx);
 }  // namespace
 
+static_assert(pk::kEntRow >= POSEIDON_L_MAX + 1, "an entry field row holds every end point");
+
 struct poseidon_ctx {
     int device;
     uint32_t L, S, M, T;
@@ -331,7 +333,8 @@ struct poseidon_ctx {
     pk::KParams base;      // table pointers and problem constants
     void *dmem;
     unsigned long long *state;
-    size_t lds_bytes;
+    size_t lds_bytes;      // cost, pm, cap (and pd): search and Interleaved 1F1B kernels
+    size_t ent_lds_bytes;  // stage entries (and pdx): evaluation and early-stop kernels
     uint32_t grid_max;
     void *ws;              // cut codes + straggler queues of the steady-state cascade
     uint64_t ws_cap;       // candidates per chunk the workspace holds
@@ -461,6 +464,25 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     for (uint32_t t = 0; has_ar && t < T; ++t)
         for (uint32_t l = 0; l < L; ++l)
             pd[(size_t)t * (L + 1) + l + 1] = pd[(size_t)t * (L + 1) + l] + p->allreduce_us[(size_t)t * L + l];
+    // stage entries (the evaluation and early-stop kernels' table): per type
+    // t the field rows Pf, Pb, hm (and Pd) over end points j,
+    // where hm_t[j] is the largest end point h >= j whose stage [j, h) fits
+    // type t's memory (Pm only grows, so the stages that fit are those
+    // ending at or before hm_t[j])
+    const uint32_t nfield = pk::entry_fields(has_ar);
+    std::vector<uint32_t> ent((size_t)T * nfield * pk::kEntRow, 0);
+    for (uint32_t t = 0; t < T; ++t)
+        for (uint32_t j = 0; j <= L; ++j) {
+            const uint64_t c = cost[(size_t)t * (L + 1) + j];
+            uint32_t *e = &ent[(size_t)t * nfield * pk::kEntRow + j];
+            const uint32_t f = (uint32_t)c, b = (uint32_t)(c >> 32);
+            e[pk::kEPf * pk::kEntRow] = f;
+            e[pk::kEPb * pk::kEntRow] = b;
+            uint32_t h = j;
+            while (h < L && pm[h + 1] - pm[j] <= p->cap_mb[t]) ++h;
+            e[pk::kEHm * pk::kEntRow] = h;
+            if (has_ar) e[pk::kEPd * pk::kEntRow] = pd[(size_t)t * (L + 1) + j];
+        }
     const size_t rsz = wide ? 8 : 4;
     std::vector<unsigned char> binom((size_t)S * NB * rsz);
     for (uint32_t k = 0; k < S; ++k)
@@ -521,6 +543,14 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         }
     }
     for (uint32_t s = 1; s < S; ++s) kp.psi[s] = kp.psi[s - 1] + kp.cf[s - 1];
+    // closed-form drain of the 1F1B epilogue: ek[s] = cb_0 + .. + cb_{s-1} - phi_s
+    // (phi_s = cf_s + .. + cf_{S-2}), modulo 2^32
+    for (uint32_t s = 0; s < S; ++s) {
+        uint32_t cbs = 0, phi = 0;
+        for (uint32_t i = 0; i < s; ++i) cbs += kp.cb[i];
+        for (uint32_t i = s; i + 1 < S; ++i) phi += kp.cf[i];
+        kp.ek[s] = cbs - phi;
+    }
     // cascade checkpoints of the steady loop: K0, 2 K0, 4 K0, ... below M - S
     // (steady iterations: 1F1B slot pairs after its prologue, Eager 1F1B
     // slot pairs between its prologue and epilogue)
@@ -548,6 +578,32 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         kp.assign_mode = pk::kAssignDigits;
         kp.magicT = (uint32_t)((1ull << 32) / T + 1);
     }
+    // the evaluation kernels' digit table (base-T digits, T <= 4, one stage
+    // per device): for r < T^4 the entry-block offsets of r's four digits,
+    // most significant first, in 16-bit fields
+    const uint32_t erow = nfield * pk::kEntField;
+    const uint32_t ent_bytes = (uint32_t)(ent.size() * 4);
+    if (kp.assign_mode == pk::kAssignDigits && T <= 4 && !ilv) {
+        const uint32_t tg = T * T * T * T;
+        for (uint32_t r = 0; r < tg; ++r) {
+            uint64_t w = 0;
+            for (uint32_t i = 0, x = r, div = T * T * T; i < 4; ++i, div = div > 1 ? div / T : 1) {
+                const uint32_t d = x / div;
+                x -= d * div;
+                w |= (uint64_t)(d * erow) << (16 * i);
+            }
+            ent.push_back((uint32_t)w);
+            ent.push_back((uint32_t)(w >> 32));
+        }
+        kp.dig_tg = tg;
+        kp.dig_magic = (uint32_t)((1ull << 32) / tg + 1);
+    }
+    // a stage's F + B is at most its type's total over all layers
+    kp.g24 = M < (1u << 24);
+    for (uint32_t t = 0; t < T; ++t)
+        if ((cost[(size_t)t * (L + 1) + L] & 0xFFFFFFFFull) + (cost[(size_t)t * (L + 1) + L] >> 32) >= (1ull << 24))
+            kp.g24 = 0;
+    static_assert(7 * 4 * pk::kEntField < 65536, "entry-block offsets fit 16 bits");
 
     // one device block: state words | cost | pm | cap | binom | assign | slots
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
@@ -560,6 +616,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     const size_t o_assign = off; off = al(off + (has_table ? (size_t)A * ndev : 0));
     const size_t o_slots = off; off = al(off + (table_path ? masks.size() * 4 : 0));
     const size_t o_pd = off; off = al(off + pd.size() * 4);
+    const size_t o_ent = off; off = al(off + ent.size() * 4);
     const size_t total = off;
 
     poseidon_ctx *ctx = new (std::nothrow) poseidon_ctx;
@@ -587,6 +644,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         if (ok && table_path)
             ok = hipMemcpy(b + o_slots, masks.data(), masks.size() * 4, hipMemcpyHostToDevice) == hipSuccess;
         if (ok && has_ar) ok = hipMemcpy(b + o_pd, pd.data(), pd.size() * 4, hipMemcpyHostToDevice) == hipSuccess;
+        if (ok) ok = hipMemcpy(b + o_ent, ent.data(), ent.size() * 4, hipMemcpyHostToDevice) == hipSuccess;
         if (!ok) { status = POSEIDON_E_DEVICE; break; }
         kp.cost = (const uint64_t *)(b + o_cost);
         kp.pm = (const uint32_t *)(b + o_pm);
@@ -595,6 +653,10 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         kp.assign = has_table ? (const uint8_t *)(b + o_assign) : nullptr;
         kp.slot_mask = table_path ? (const uint32_t *)(b + o_slots) : nullptr;
         kp.pd = has_ar ? (const uint32_t *)(b + o_pd) : nullptr;
+        kp.ent = (const uint32_t *)(b + o_ent);
+        kp.erow = erow;
+        kp.ent_bytes = ent_bytes;
+        kp.ent_lds = (uint32_t)((ent.size() * 4 + 15) & ~(size_t)15);
         kp.nslots = table_path ? nslots : 0;
         ctx->state = (unsigned long long *)(b + o_state);
         kp.acc = ctx->state + W_ACC;
@@ -605,14 +667,17 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         kp.err = (unsigned int *)(ctx->state + W_ERR);
         kp.done = (unsigned int *)(ctx->state + W_DONE);
         const size_t lds = ((cost.size() * 8 + pm.size() * 4 + (size_t)T * 4 + pd.size() * 4) + 15) & ~(size_t)15;
-        if (lds > 64 * 1024) { status = POSEIDON_E_RANGE; break; }
+        const size_t elds = kp.ent_lds;
+        if (lds > 64 * 1024 || elds > 64 * 1024) { status = POSEIDON_E_RANGE; break; }
         int occ = 0;
         hipDeviceProp_t prop;
-        if (pk::eval_occupancy(kp, lds, &occ) != hipSuccess || hipGetDeviceProperties(&prop, hip_device) != hipSuccess) {
+        if (pk::eval_occupancy(kp, ilv ? lds : elds, &occ) != hipSuccess ||
+            hipGetDeviceProperties(&prop, hip_device) != hipSuccess) {
             status = POSEIDON_E_DEVICE;
             break;
         }
         ctx->lds_bytes = lds;
+        ctx->ent_lds_bytes = elds;
         ctx->grid_max = (uint32_t)std::max(1, occ) * (uint32_t)std::max(1, prop.multiProcessorCount);
     } while (0);
     (void)hipSetDevice(prev);
@@ -811,7 +876,7 @@ int eval_chunks(poseidon_ctx *ctx, const poseidon_cands *cands, uint32_t *makesp
         kp.accumulate = c0 > 0;
         const ChunkGrid g = chunk_grid(ctx, kp.n_i);
         pk::LaunchCfg lc;
-        lc.lds_bytes = ctx->lds_bytes;
+        lc.lds_bytes = ctx->base.sched == POSEIDON_SCHEDULE_INTERLEAVED_1F1B ? ctx->lds_bytes : ctx->ent_lds_bytes;
         lc.grid = g.grid;
         // queue segments: block b of every level owns seg_cap slots
         kp.nseg = lc.grid;
@@ -919,7 +984,7 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
     kp.scount = (unsigned int *)(kp.sidx + ctx->ws_cap);
     kp.es_bound = bound;
     pk::LaunchCfg lc;
-    lc.lds_bytes = ctx->lds_bytes;
+    lc.lds_bytes = ctx->ent_lds_bytes;
     for (uint64_t lo = 0; lo < n; lo += chunk) {
         const uint64_t hi = std::min(n, lo + chunk);
         for (uint64_t s0 = lo; s0 < hi; s0 += kChunk) {

@@ -24,6 +24,15 @@ struct KParams {
     const uint32_t *slot_mask; // [nslots][3] forward / deep-forward / backward stage masks
                                // ([nslots][4] under Interleaved 1F1B: + backward depths)
     const uint32_t *pd;        // [T][L+1] prefix all-reduce time (has_ar)
+    const uint32_t *ent;       // stage entries of the evaluation kernels: [T][fields][kEntRow], then
+                               // (dig_tg > 0) the assignment-digit table [dig_tg] of uint64
+    uint32_t erow;             // bytes of one type's block of entry fields
+    uint32_t ent_bytes;        // bytes of the entries (the digit table starts there)
+    uint32_t ent_lds;          // LDS bytes the entries and the digit table take
+    uint32_t dig_tg, dig_magic;   // base-T assignment digits with T <= 4: T^4 and floor(2^32 / T^4) + 1
+                                  // (0: no digit table)
+    uint32_t g24;                 // every stage's F + B is below 2^24 (and M is), so M (F + B) is a
+                                  // 24-bit multiply
     uint64_t A, n_comp;
     uint32_t L, S, M, T, NB, nslots;
     uint32_t magicT, assign_mode;
@@ -40,6 +49,8 @@ struct KParams {
     uint32_t ilv_compiled, ilv_trips; // Interleaved 1F1B: the schedule runs as compiled code with
                                       // this many steady periods
     uint32_t psi[kSMax];          // cf_0 + ... + cf_{s-1}: undoes the per-stage shift at the end
+    uint32_t ek[kSMax];           // cb_0 + .. + cb_{s-1} - (cf_s + .. + cf_{S-2}) mod 2^32: the closed-form
+                                  // drain's constant per stage
     uint8_t fixed_types[kSMax];
     // candidates of the call
     uint64_t first, count;
@@ -116,9 +127,21 @@ struct SearchParams {
 
 enum SearchOp { kSearchOpCount = 0, kSearchOpWrite = 1, kSearchOpLeaf = 2, kSearchOpMerge = 3, kSearchOpRoot = 4 };
 
+// Stage entries of the evaluation kernels: per device type a block of
+// field rows of kEntRow uint32 (end points 0..L <= 256, padded), so that a
+// field sits at a compile-time byte offset from its end point's address.
+constexpr uint32_t kEntRow = 264;
+constexpr uint32_t kEntField = 4 * kEntRow;   // bytes per field row
+enum EntField : uint32_t { kEPf = 0, kEPb = 1, kEHm = 2, kEPd = 3 };
+__host__ __device__ constexpr uint32_t entry_fields(bool ar) { return ar ? 4u : 3u; }
+__host__ __device__ constexpr size_t entry_bytes(uint32_t T, bool ar) {
+    return (size_t)T * entry_fields(ar) * kEntField;
+}
+
 struct LaunchCfg {
     uint32_t grid;
-    size_t lds_bytes;     // eval / resume / early-stop kernels: cost, pm, cap
+    size_t lds_bytes;     // stage tables: the entries (evaluation, early-stop kernels) or cost, pm,
+                          // cap (search and Interleaved 1F1B kernels)
 };
 
 hipError_t launch_eval(const KParams &p, const LaunchCfg &lc, hipStream_t st);

@@ -50,6 +50,50 @@ __device__ __forceinline__ Lds stage_tables(const KParams &p, unsigned char *sme
     return Lds{cost, pm, cap, pd};
 }
 
+// Stage entries of the evaluation and early-stop kernels.  For device type
+// t and end point j = 0..L the fields
+//   Pf_t[j], Pb_t[j]   prefix forward and backward time,
+//   hm_t[j]            the largest end point h >= j with Pm[h] - Pm[j] <= cap[t],
+//   Pd_t[j]            prefix all-reduce time (with all-reduce times only)
+// are uint32 at byte t * erow + field * kEntField + 4 j.  A stage [c0, c1) on
+// type t then has F = Pf(c1) - Pf(c0), B = Pb(c1) - Pb(c0) and fits its
+// memory iff c1 <= hm_t[c0].  Every load is 4 bytes wide at a per-lane
+// address and the fields of one end point are a constant distance apart
+// (the load's immediate offset): wider loads at per-lane addresses
+// serialise on the LDS banks.
+//
+// With base-T assignment digits and T <= 4, the digit table follows: for
+// every r < T^4 the entry-block offsets of the four digits of r (most
+// significant first) as 16-bit fields of a uint64, so the types of four
+// stages cost one division by T^4 and one load.
+struct Ent {
+    const unsigned char *e;    // entry blocks (byte addressed)
+    const uint64_t *dig;       // [T^4] packed offsets of four digits (dig_tg > 0)
+};
+
+__device__ __forceinline__ Ent entry_tables(const KParams &p, unsigned char *smem) {
+    uint4 *e = reinterpret_cast<uint4 *>(smem);
+    const uint4 *g = reinterpret_cast<const uint4 *>(p.ent);
+    const uint32_t n = (p.ent_bytes + 8 * p.dig_tg) / 16;
+    for (uint32_t i = threadIdx.x; i < n; i += kBlock) e[i] = g[i];
+    if (threadIdx.x == 0 && (p.dig_tg & 1u))   // an odd number of 8-byte digit entries
+        reinterpret_cast<uint64_t *>(smem + p.ent_bytes)[p.dig_tg - 1] =
+            reinterpret_cast<const uint64_t *>(reinterpret_cast<const unsigned char *>(p.ent) + p.ent_bytes)[p.dig_tg - 1];
+    __syncthreads();
+    return Ent{smem, reinterpret_cast<const uint64_t *>(smem + p.ent_bytes)};
+}
+
+__device__ __forceinline__ Ent entry_global(const KParams &p) {
+    const unsigned char *e = reinterpret_cast<const unsigned char *>(p.ent);
+    return Ent{e, reinterpret_cast<const uint64_t *>(e + p.ent_bytes)};
+}
+
+// field F of end point c in the type block at byte offset `to` (= t * erow)
+template <uint32_t F>
+__device__ __forceinline__ uint32_t ent(const Ent &t, uint32_t c, uint32_t to) {
+    return *reinterpret_cast<const uint32_t *>(t.e + ((c << 2) + to) + F * kEntField);
+}
+
 // ---------------------------------------------------------------------------
 // (a1) decode
 // ---------------------------------------------------------------------------
@@ -119,6 +163,41 @@ __device__ __forceinline__ void decode_types(const KParams &p, uint32_t a, uint3
     }
 }
 
+// Stage types as byte offsets of their entry blocks (t * erow; both factors
+// fit 24 bits, so this is the full-rate 24-bit multiply).  Base-T digits
+// with T <= 4 go four stages at a time through the digit table: the stages
+// S-4..S-1 are the digits of a mod T^4, the four before them those of
+// (a div T^4) mod T^4, and so on (stage 1 most significant).
+template <int S>
+__device__ __forceinline__ void decode_toff(const KParams &p, const Ent &t, uint32_t a, uint32_t (&to)[S]) {
+    if (p.assign_mode == kAssignDigits && p.dig_tg) {
+        constexpr int NG = (S + 3) / 4;
+        uint32_t q = a;
+#pragma unroll
+        for (int k = 0; k < NG; ++k) {
+            uint32_t r = q;
+            if (k + 1 < NG) {
+                uint32_t d = __umulhi(q, p.dig_magic);   // floor(q / T^4) or one more
+                int32_t rem = (int32_t)(q - d * p.dig_tg);
+                if (rem < 0) { d -= 1; rem += (int32_t)p.dig_tg; }
+                r = (uint32_t)rem;
+                q = d;
+            }
+            const uint64_t w = t.dig[r];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int s = S - 4 * k - 4 + i;   // digit i (most significant first) of group k
+                if (s >= 0) to[s] = (uint32_t)(w >> (16 * i)) & 0xFFFFu;
+            }
+        }
+        return;
+    }
+    uint32_t ty[S];
+    decode_types<S>(p, a, ty);
+#pragma unroll
+    for (int s = 0; s < S; ++s) to[s] = __umul24(ty[s], p.erow);
+}
+
 // Candidate i of the call -> (rank, assignment); false if out of range.
 template <typename R>
 __device__ __forceinline__ bool candidate(const KParams &p, uint64_t i, R &r, uint32_t &a) {
@@ -161,6 +240,37 @@ __device__ __forceinline__ bool stage_weights(const KParams &p, const Lds &t,
         B[s] = (uint32_t)(hi >> 32) - (uint32_t)(lo >> 32);
         const uint32_t mem = t.pm[cut[s + 1]] - t.pm[cut[s]];
         feas = feas && (mem <= t.cap[ty[s]]);
+    }
+    return feas;
+}
+
+// The same from the stage entries: no multiply, one address per end point.
+template <int S>
+__device__ __forceinline__ bool stage_weights(const KParams &p, const Ent &t, const uint32_t (&cut)[S + 1],
+                                              const uint32_t (&to)[S], uint32_t (&F)[S], uint32_t (&B)[S]) {
+    bool feas = true;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        F[s] = ent<kEPf>(t, cut[s + 1], to[s]) - ent<kEPf>(t, cut[s], to[s]);
+        B[s] = ent<kEPb>(t, cut[s + 1], to[s]) - ent<kEPb>(t, cut[s], to[s]);
+        feas = feas && (cut[s + 1] <= ent<kEHm>(t, cut[s], to[s]));
+    }
+    return feas;
+}
+
+// ... and G_s = M (F_s + B_s), the stage's term of Eq. 2 (below 2^31 like
+// every path weight; a full-rate 24-bit multiply when both factors fit).
+template <int S>
+__device__ __forceinline__ bool stage_weights_g(const KParams &p, const Ent &t, const uint32_t (&cut)[S + 1],
+                                                const uint32_t (&to)[S], uint32_t (&F)[S], uint32_t (&B)[S],
+                                                uint32_t (&G)[S]) {
+    const bool feas = stage_weights<S>(p, t, cut, to, F, B);
+    if (p.g24) {
+#pragma unroll
+        for (int s = 0; s < S; ++s) G[s] = __umul24(p.M, F[s] + B[s]);
+    } else {
+#pragma unroll
+        for (int s = 0; s < S; ++s) G[s] = p.M * (F[s] + B[s]);
     }
     return feas;
 }
@@ -248,13 +358,35 @@ __device__ __forceinline__ void steady_slot(int parity, uint32_t (&Y)[S], const 
     for (int s = 0; s < S; ++s) Y[s] = N[s];
 }
 
-// init + prologue (slots 0 .. 2S-2)
+// k * x for a small compile-time k; the full-rate 24-bit multiply when the
+// problem's stage weights fit 24 bits (u24)
+__device__ __forceinline__ uint32_t mul_small(uint32_t x, uint32_t k, bool u24) {
+    return u24 ? __umul24(x, k) : x * k;
+}
+
+// Prologue (slots 0 .. 2S-2) with its warm-up forwards in closed form.
+// Stage s (0-based) first runs S - s forwards F_{s,1..S-s} in slots
+// s .. S-1; each reads only its own stage's previous forward and the same
+// micro-batch's forward upstream, and with the potential shift every
+// forward edge weighs 0.  So the longest path to F_{s,m} is the heaviest
+// monotone path through a grid whose row i carries the constant weight F_i:
+// it visits rows 0..s once each and spends its other m - 1 steps on the
+// heaviest of them,
+//     Y[s] = phi_0 + (F_0 + ... + F_s) + (m - 1) max(F_0, ..., F_s),  m = S - s.
+// Slots S .. 2S-2 (the first backwards and the forwards between them) run
+// on the stencil.  u24: every stage weight is below 2^24.
 template <int S>
 __device__ __forceinline__ void dp_prologue(uint32_t (&Y)[S], const uint32_t (&F)[S], const uint32_t (&B)[S],
-                                            const Comm<S> &c) {
-    dp_init<S>(Y, c);
+                                            const Comm<S> &c, bool u24) {
+    uint32_t pre = c.phi0, mx = 0;
 #pragma unroll
-    for (int k = 0; k < 2 * S - 1; ++k) {
+    for (int s = 0; s < S; ++s) {
+        pre += F[s];
+        mx = max(mx, F[s]);
+        Y[s] = pre + mul_small(mx, S - 1 - s, u24);
+    }
+#pragma unroll
+    for (int k = S; k < 2 * S - 1; ++k) {
         uint32_t N[S];
 #pragma unroll
         for (int s = 0; s < S; ++s) N[s] = node<S>(pro_op(S, s + 1, k), s, Y, F, B, c);
@@ -287,10 +419,73 @@ __device__ __forceinline__ void dp_finish(uint32_t (&Y)[S], const uint32_t (&F)[
     }
 }
 
+// The last steady slot and the epilogue with the drain in closed form, for
+// the DAG without all-reduce nodes; returns T = finish(B_{1,M}).
+// Stage s (0-based) ends with its last forward F_{s,M} and then its drain,
+// the S - s backwards B_{s,m}, m = M-S+s+1 .. M.  Each drain node's
+// predecessors are drain nodes, except at the drain's first node: its own
+// stage's F_{s,M} and the stage below's last backward before its drain,
+// B_{s+1,M-S+s+1} (edge cb_s); and no node outside the drains reads a drain
+// node.  Inside the drains a path from stage s to B_{1,M} runs down the
+// stages s, s-1, .., 0 (edges cb_i) and takes S - 1 - s more steps along
+// its stages, best spent on the heaviest backward, so
+//   T = max_s [ max(fin F_{s,M}, fin B_{s+1,M-S+s+1} + cb_s)
+//              + (B_0 + .. + B_s) + (cb_0 + .. + cb_{s-1}) + (S-1-s) max(B_0 .. B_s) ].
+// The stencil below computes only the nodes outside the drains and keeps,
+// per stage, its register just before (Yb) and after (Yf) its last forward:
+// the backward before F_{s,M} is B_{s,M-S+s}, the one stage s-1's drain
+// starts from.  In shifted registers the bracket is
+//   max(Yf[s], Yb[s+1] + cf_s + cb_s) - phi_s, and p.ek[s] holds
+//   cb_0 + .. + cb_{s-1} - phi_s (modulo 2^32: every sum that reaches T is a
+// path length below 2^31).
 template <int S>
-__device__ __forceinline__ void dp_1f1b(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S],
+__device__ __forceinline__ uint32_t dp_finish_t(const KParams &p, uint32_t (&Y)[S], const uint32_t (&F)[S],
+                                                const uint32_t (&B)[S], const Comm<S> &c) {
+    uint32_t Yf[S], Yb[S];
+    Yf[0] = Y[0];                         // stage 0's last forward ran in slot 2M-2
+    Yb[S > 1 ? 1 : 0] = Y[S > 1 ? 1 : 0];  // stage 1's runs in slot 2M-1
+    {
+        // slot 2M-1 without stage 0's backward (the first of its drain)
+        uint32_t N[S];
+#pragma unroll
+        for (int s = 0; s < S; ++s) N[s] = node<S>(s == 0 ? kIdle : ((s & 1) ? kFwd : kBwd), s, Y, F, B, c);
+#pragma unroll
+        for (int s = 0; s < S; ++s) Y[s] = N[s];
+    }
+    if (S > 1) Yf[1] = Y[1];
+    // epilogue slots 2M + j: stage s >= 2 runs its last forward at j = s - 2;
+    // its backwards from j = s - 1 on are drain nodes
+#pragma unroll
+    for (int j = 0; j + 2 < S; ++j) {
+        uint32_t N[S];
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            int op = epi_op(S, s + 1, j);
+            if (op == kBwd && j >= s - 1) op = kIdle;
+            if (op == kFwd && j == s - 2) Yb[s] = Y[s];
+            N[s] = node<S>(op, s, Y, F, B, c);
+        }
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            if (epi_op(S, s + 1, j) == kFwd && j == s - 2) Yf[s] = N[s];
+            Y[s] = N[s];
+        }
+    }
+    uint32_t T = 0, pb = 0, mxb = 0;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        pb += B[s];
+        mxb = max(mxb, B[s]);
+        const uint32_t a = s + 1 < S ? max(Yf[s], Yb[s + 1 < S ? s + 1 : 0] + c.e[s + 1 < S ? s : 0]) : Yf[s];
+        T = max(T, a + pb + mul_small(mxb, S - 1 - s, p.g24 != 0) + p.ek[s]);
+    }
+    return T;
+}
+
+template <int S>
+__device__ __forceinline__ void dp_1f1b(uint32_t M, bool u24, const uint32_t (&F)[S], const uint32_t (&B)[S],
                                         const Comm<S> &c, uint32_t (&Y)[S]) {
-    dp_prologue<S>(Y, F, B, c);
+    dp_prologue<S>(Y, F, B, c, u24);
     for (uint32_t it = S; it < M; ++it) dp_iter<S>(Y, F, B, c);
     dp_finish<S>(Y, F, B, c);
 }
@@ -571,7 +766,7 @@ __device__ __forceinline__ void dp_full(const KParams &p, const uint32_t (&F)[S]
                                         const Comm<S> &c, uint32_t (&Y)[S]) {
     if (SCH && p.nslots) dp_sched<S>(p, F, B, c, Y);
     else if (SCH) dp_eager<S>(p.M, F, B, c, Y);
-    else if (p.M >= (uint32_t)S) dp_1f1b<S>(p.M, F, B, c, Y);
+    else if (p.M >= (uint32_t)S) dp_1f1b<S>(p.M, p.g24 != 0, F, B, c, Y);
     else dp_table<S>(p, F, B, c, Y);
 }
 
@@ -581,37 +776,6 @@ __device__ __forceinline__ void dp_full(const KParams &p, const uint32_t (&F)[S]
 // settled (jumped to its end) or reached it.
 constexpr uint32_t kSurvStep = 8;
 
-template <int S, bool SCH>
-__device__ __forceinline__ void dp_full_settle(const KParams &p, const uint32_t (&F)[S], const uint32_t (&B)[S],
-                                               const Comm<S> &c, uint32_t (&Y)[S]) {
-    const unsigned long long act = __ballot(true);
-    if (SCH && !p.nslots) {
-        uint32_t Fn[S], Fp[S];
-        eager_prologue<S>(Y, Fn, Fp, F, B, c);
-        const uint32_t np = p.M - 2 * S + 1;
-        bool done = false;
-        for (uint32_t k = 0; k < np;) {
-            const uint32_t k1 = min(k + kSurvStep, np);
-            if (!done) done = eager_advance<S>(Y, Fn, Fp, F, B, c, k, k1, np);
-            k = k1;
-            if (__ballot(done) == act) break;
-        }
-        eager_epilogue<S>(Y, Fn, Fp, F, B, c);
-    } else if (!SCH && p.M >= (uint32_t)S) {
-        dp_prologue<S>(Y, F, B, c);
-        const uint32_t nit = p.M - S;
-        bool done = false;
-        for (uint32_t k = 0; k < nit;) {
-            const uint32_t k1 = min(k + kSurvStep, nit);
-            if (!done) done = dp_advance<S>(Y, F, B, c, k, k1, nit);
-            k = k1;
-            if (__ballot(done) == act) break;
-        }
-        dp_finish<S>(Y, F, B, c);
-    } else {
-        dp_full<S, SCH>(p, F, B, c, Y);
-    }
-}
 
 template <int S>
 __device__ __forceinline__ Comm<S> load_comm(const KParams &p) {
@@ -643,6 +807,20 @@ __device__ __forceinline__ uint32_t eq2_bound(uint32_t M, const uint32_t (&F)[S]
     return lb;
 }
 
+// The same with G_x = M (F_x + B_x) from the stage entries.
+template <int S>
+__device__ __forceinline__ uint32_t eq2_bound_g(const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                                const uint32_t (&G)[S], const uint32_t (&D)[S]) {
+    uint32_t pre = 0, inner = 0, lb = 0;
+#pragma unroll
+    for (int x = 0; x < S; ++x) {
+        inner = x == 0 ? D[0] : max(inner + B[x - 1], D[x]);
+        lb = max(lb, pre + G[x] + inner);
+        pre += F[x];
+    }
+    return lb;
+}
+
 // ---------------------------------------------------------------------------
 // end of the iteration: the end node E follows every R_s (Sec. 4.1.1), and
 // R_s follows B_{s,M} with the stage's summed per-layer all-reduce time
@@ -654,6 +832,13 @@ __device__ __forceinline__ void stage_allreduce(const KParams &p, const Lds &t, 
     const uint32_t row = p.L + 1;
 #pragma unroll
     for (int s = 0; s < S; ++s) D[s] = t.pd[ty[s] * row + cut[s + 1]] - t.pd[ty[s] * row + cut[s]];
+}
+
+template <int S>
+__device__ __forceinline__ void stage_allreduce(const KParams &p, const Ent &t, const uint32_t (&cut)[S + 1],
+                                                const uint32_t (&to)[S], uint32_t (&D)[S]) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) D[s] = ent<kEPd>(t, cut[s + 1], to[s]) - ent<kEPd>(t, cut[s], to[s]);
 }
 
 // T from the registers after the epilogue; with all-reduce times the
@@ -671,6 +856,73 @@ __device__ __forceinline__ uint32_t end_time(const KParams &p, const Lds &t, con
 #pragma unroll
     for (int s = 0; s < S; ++s) e = max(e, Y[s] + p.psi[s] + D[s]);
     return e - c.phi0;
+}
+
+template <int S, bool AR>
+__device__ __forceinline__ uint32_t end_time(const KParams &p, const Ent &t, const uint32_t (&Y)[S],
+                                             const Comm<S> &c, const uint32_t (&w)[Codes<S>::kWords], uint32_t a) {
+    if (!AR) return Y[0] - c.phi0;
+    uint32_t cut[S + 1], to[S], D[S];
+    unpack_cuts<S>(w, p.L, cut);
+    decode_toff<S>(p, t, a, to);
+    stage_allreduce<S>(p, t, cut, to, D);
+    uint32_t e = 0;
+#pragma unroll
+    for (int s = 0; s < S; ++s) e = max(e, Y[s] + p.psi[s] + D[s]);
+    return e - c.phi0;
+}
+
+// After the steady part: T from the last steady slot, the epilogue and the
+// end node (1F1B; closed-form drain without all-reduce times).
+template <int S, bool AR, typename TAB>
+__device__ __forceinline__ uint32_t dp_end(const KParams &p, const TAB &t, uint32_t (&Y)[S], const uint32_t (&F)[S],
+                                           const uint32_t (&B)[S], const Comm<S> &c,
+                                           const uint32_t (&w)[Codes<S>::kWords], uint32_t a) {
+    if constexpr (AR) {
+        dp_finish<S>(Y, F, B, c);
+        return end_time<S, true>(p, t, Y, c, w, a);
+    } else {
+        return dp_finish_t<S>(p, Y, F, B, c);
+    }
+}
+
+// The whole DP of one candidate with a settle check every kSurvStep steady
+// iterations (the wave leaves the steady loop once all its lanes settled),
+// ending in T (the end node: closed-form drain for 1F1B without all-reduce
+// times, else the full epilogue and the all-reduce nodes).
+template <int S, bool SCH, bool AR, typename TAB>
+__device__ __forceinline__ uint32_t dp_full_settle(const KParams &p, const TAB &t, const uint32_t (&F)[S],
+                                                   const uint32_t (&B)[S], const Comm<S> &c,
+                                                   const uint32_t (&w)[Codes<S>::kWords], uint32_t a) {
+    const unsigned long long act = __ballot(true);
+    uint32_t Y[S];
+    if (SCH && !p.nslots) {
+        uint32_t Fn[S], Fp[S];
+        eager_prologue<S>(Y, Fn, Fp, F, B, c);
+        const uint32_t np = p.M - 2 * S + 1;
+        bool done = false;
+        for (uint32_t k = 0; k < np;) {
+            const uint32_t k1 = min(k + kSurvStep, np);
+            if (!done) done = eager_advance<S>(Y, Fn, Fp, F, B, c, k, k1, np);
+            k = k1;
+            if (__ballot(done) == act) break;
+        }
+        eager_epilogue<S>(Y, Fn, Fp, F, B, c);
+    } else if (!SCH && p.M >= (uint32_t)S) {
+        dp_prologue<S>(Y, F, B, c, p.g24 != 0);
+        const uint32_t nit = p.M - S;
+        bool done = false;
+        for (uint32_t k = 0; k < nit;) {
+            const uint32_t k1 = min(k + kSurvStep, nit);
+            if (!done) done = dp_advance<S>(Y, F, B, c, k, k1, nit);
+            k = k1;
+            if (__ballot(done) == act) break;
+        }
+        return dp_end<S, AR>(p, t, Y, F, B, c, w, a);
+    } else {
+        dp_full<S, SCH>(p, F, B, c, Y);
+    }
+    return end_time<S, AR>(p, t, Y, c, w, a);
 }
 
 // ---------------------------------------------------------------------------
@@ -965,7 +1217,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(KParams p) {
 template <int S, bool AR>
 __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Lds tab = stage_tables(p, smem);
+    const Ent tab = entry_tables(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     unsigned long long best = ~0ull;
@@ -983,22 +1235,23 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
         uint32_t w[NW];
 #pragma unroll
         for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[(uint64_t)k * p.ccap + i] : 0u;
-        uint32_t cut[S + 1], ty[S], F[S], B[S], Y[S];
+        uint32_t cut[S + 1], to[S], F[S], B[S], Y[S];
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = ok ? assign_of(p, gi) : 0u;
-        decode_types<S>(p, a, ty);
-        const bool feas = stage_weights<S>(p, tab, cut, ty, F, B) && ok && active;
+        decode_toff<S>(p, tab, a, to);
+        const bool feas = stage_weights<S>(p, tab, cut, to, F, B) && ok && active;
         bool done_here = true;
+        uint32_t T;
         if (p.M < (uint32_t)S) {
             dp_table<S>(p, F, B, comm, Y);
+            T = end_time<S, AR>(p, tab, Y, comm, w, a);
         } else {
-            dp_prologue<S>(Y, F, B, comm);
+            dp_prologue<S>(Y, F, B, comm, p.g24 != 0);
             const uint32_t k1 = p.nlevels ? p.lvl_k[0] : nit;
             done_here = dp_advance<S>(Y, F, B, comm, 0, k1, nit);
             if (p.nlevels) enqueue<S, S>(p, 0, &nq, !done_here && active && ok, (uint32_t)gi, w, Y);
-            dp_finish<S>(Y, F, B, comm);
+            T = dp_end<S, AR>(p, tab, Y, F, B, comm, w, a);
         }
-        uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, a);
         if (!ok) T = 0xFFFFFFFFu;
         const bool write = active && (done_here || !ok);
         if (write && p.makespan_out) p.makespan_out[gi] = T;
@@ -1027,7 +1280,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
 template <int S, bool AR, bool TAB>
 __global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Lds tab = stage_tables(p, smem);
+    const Ent tab = entry_tables(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     unsigned long long best = ~0ull;
@@ -1044,11 +1297,11 @@ __global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
         uint32_t w[NW];
 #pragma unroll
         for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[(uint64_t)k * p.ccap + i] : 0u;
-        uint32_t cut[S + 1], ty[S], F[S], B[S], Y[S];
+        uint32_t cut[S + 1], to[S], F[S], B[S], Y[S];
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = ok ? assign_of(p, gi) : 0u;
-        decode_types<S>(p, a, ty);
-        const bool feas = stage_weights<S>(p, tab, cut, ty, F, B) && ok && active;
+        decode_toff<S>(p, tab, a, to);
+        const bool feas = stage_weights<S>(p, tab, cut, to, F, B) && ok && active;
         bool done_here = true;
         if (TAB) {
             dp_sched<S>(p, F, B, comm, Y);
@@ -1092,7 +1345,7 @@ __global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
 template <int S, bool AR, bool SCH>
 __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Lds tab = stage_tables(p, smem);
+    const Ent tab = entry_tables(p, smem);
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     constexpr int NX = SCH ? 2 * S : S;
@@ -1113,16 +1366,17 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
         const uint32_t q = it * kBlock + threadIdx.x;
         const bool active = q < n;
         const uint32_t i = active ? qin.idx[seg + q] : 0u;
-        uint32_t w[NW], cut[S + 1], ty[S], F[S], B[S], X[NX], Y[S];
+        uint32_t w[NW], cut[S + 1], to[S], F[S], B[S], X[NX], Y[S];
 #pragma unroll
         for (int k = 0; k < NW; ++k) w[k] = active ? qin.codes[(uint64_t)k * p.qcap + seg + q] : 0u;
 #pragma unroll
         for (int s = 0; s < NX; ++s) X[s] = active ? qin.Y[(uint64_t)s * p.qcap + seg + q] : 0u;
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = ok ? assign_of(p, i) : 0u;
-        decode_types<S>(p, a, ty);
-        const bool feas = stage_weights<S>(p, tab, cut, ty, F, B);
+        decode_toff<S>(p, tab, a, to);
+        const bool feas = stage_weights<S>(p, tab, cut, to, F, B);
         bool settled;
+        uint32_t T;
         if constexpr (SCH) {
             uint32_t Fn[S], Fp[S];
             eager_unpack<S>(X, Y, Fn, Fp);
@@ -1132,14 +1386,14 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
                 enqueue<S, NX>(p, lvl & 1, &nq, active && !settled, i, w, X);
             }
             eager_epilogue<S>(Y, Fn, Fp, F, B, comm);
+            T = end_time<S, AR>(p, tab, Y, comm, w, a);
         } else {
 #pragma unroll
             for (int s = 0; s < S; ++s) Y[s] = X[s];
             settled = dp_advance<S>(Y, F, B, comm, k0, k1, nit);
             if (lvl < p.nlevels) enqueue<S, S>(p, lvl & 1, &nq, active && !settled, i, w, Y);
-            dp_finish<S>(Y, F, B, comm);
+            T = dp_end<S, AR>(p, tab, Y, F, B, comm, w, a);
         }
-        const uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, a);
         if (active && settled) {
             if (p.makespan_out) p.makespan_out[i] = T;
             const unsigned long long key = make_key(feas, T, i);
@@ -1162,7 +1416,7 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
 // counting them in LDS.  surv_kernel evaluates the list on the DAG (a3) and
 // folds it into the running best (a4).
 template <int S, typename R, int H, bool AR>
-__device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const Lds &tab, uint32_t b,
+__device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const Ent &tab, uint32_t b,
                                            unsigned int *nq, uint32_t &n_keep, uint32_t &n_pruned,
                                            uint32_t &n_infeas, bool &bad) {
     constexpr int NW = Codes<S>::kWords;
@@ -1177,12 +1431,12 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
         decode_ilp<S, R, H>(p, sorted, ey, base, stride, act, ok, asg, w);
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) {
-            uint32_t cut[S + 1], ty[S], F[S], B[S], D[S];
+            uint32_t cut[S + 1], to[S], F[S], B[S], G[S], D[S];
             unpack_cuts<S>(w[u], p.L, cut);
-            decode_types<S>(p, ok[u] ? asg[u] : 0u, ty);
-            const bool feas = stage_weights<S>(p, tab, cut, ty, F, B);
+            decode_toff<S>(p, tab, ok[u] ? asg[u] : 0u, to);
+            const bool feas = stage_weights_g<S>(p, tab, cut, to, F, B, G);
             if (AR) {
-                stage_allreduce<S>(p, tab, cut, ty, D);
+                stage_allreduce<S>(p, tab, cut, to, D);
             } else {
 #pragma unroll
                 for (int s = 0; s < S; ++s) D[s] = 0;
@@ -1191,7 +1445,7 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
             if (act[u]) {
                 if (!ok[u]) bad = true;
                 else if (!feas) ++n_infeas;
-                else if (eq2_bound<S>(p.M, F, B, D) > b) ++n_pruned;
+                else if (eq2_bound_g<S>(F, B, G, D) > b) ++n_pruned;
                 else keep = true;
             }
             // survivors go to this block's segment of the list (LDS counter:
@@ -1214,17 +1468,23 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
     }
 }
 
-// GTAB: the stage tables are read from global memory (L2) instead of LDS,
-// for the largest Pascal columns (L > 128 with 64-bit ranks), which fill
-// the 64 KB of LDS one block may use on their own.
+// GTAB: the stage entries are read from global memory (L2) instead of LDS,
+// when they and the Pascal columns together exceed the 64 KB of LDS one
+// block may use (the largest columns: L > 128 with 64-bit ranks).  LDS:
+// the stage entries first (unless GTAB), then the Pascal columns.
 template <int S, typename R, bool AR, bool GTAB>
 __global__ __launch_bounds__(kBlock) void filter_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
-    R *pas = reinterpret_cast<R *>(smem);
     const uint32_t H = decode_levels(p.L);
-    Lds tab;
-    if constexpr (GTAB) tab = Lds{p.cost, p.pm, p.cap, p.pd};
-    else tab = stage_tables(p, smem + pascal_bytes<S, R>(p.L));   // (its barrier covers both tables)
+    Ent tab;
+    R *pas;
+    if constexpr (GTAB) {
+        tab = entry_global(p);
+        pas = reinterpret_cast<R *>(smem);
+    } else {
+        pas = reinterpret_cast<R *>(smem + p.ent_lds);
+        tab = entry_tables(p, smem);
+    }
     // bound in force: min(caller's bound, best of the chunks before this one)
     const unsigned long long rb = __hip_atomic_load(p.snap, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t rbT = (uint32_t)(rb >> 32);
@@ -1275,7 +1535,7 @@ __global__ __launch_bounds__(kBlock) void surv_kernel(KParams p, uint32_t publis
             pre[j + 1] = t;
         }
     }
-    const Lds tab = stage_tables(p, smem);   // (its barrier also publishes pre)
+    const Ent tab = entry_tables(p, smem);   // (its barrier also publishes pre)
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     const uint32_t n = pre[ns];
@@ -1285,15 +1545,14 @@ __global__ __launch_bounds__(kBlock) void surv_kernel(KParams p, uint32_t publis
         while (j + 1 < ns && pre[j + 1] <= k) ++j;
         const uint64_t at = (uint64_t)(s0 + j) * p.seg_cap + (k - pre[j]);
         const uint32_t i = p.sidx[at];
-        uint32_t w[NW], cut[S + 1], ty[S], F[S], B[S], Y[S];
+        uint32_t w[NW], cut[S + 1], to[S], F[S], B[S];
 #pragma unroll
         for (int kk = 0; kk < NW; ++kk) w[kk] = p.codes[(uint64_t)kk * p.ccap + at];
         unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = assign_of(p, i);
-        decode_types<S>(p, a, ty);
-        stage_weights<S>(p, tab, cut, ty, F, B);
-        dp_full_settle<S, SCH>(p, F, B, comm, Y);
-        const uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, a);
+        decode_toff<S>(p, tab, a, to);
+        stage_weights<S>(p, tab, cut, to, F, B);
+        const uint32_t T = dp_full_settle<S, SCH, AR>(p, tab, F, B, comm, w, a);
         const unsigned long long key = make_key(true, T, i);
         best = key < best ? key : best;
     }

@@ -621,10 +621,9 @@ __global__ __launch_bounds__(kBlock) void search_leaf_kernel(KParams p, SearchPa
     }
     const bool leaf = why == 0;
     if (leaf) {
-        uint32_t F[S], B[S], Y[S];
+        uint32_t F[S], B[S];
         stage_weights<S>(p, tab, cut, ty, F, B);
-        dp_full_settle<S, SCH>(p, F, B, comm, Y);
-        const uint32_t T = end_time<S, AR>(p, tab, Y, comm, w, row);
+        const uint32_t T = dp_full_settle<S, SCH, AR>(p, tab, F, B, comm, w, row);
         if (T <= bound) key = ((unsigned long long)T << 32) | i;
     }
     if (S == 1) search_flush(q, leaf, leaf, why == 1, why == 2, why == 3);
