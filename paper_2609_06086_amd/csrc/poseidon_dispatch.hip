@@ -61,6 +61,8 @@ size_t noalloc_scratch_bytes() { return sizeof(scratch); }
                                                               uint32_t);                                      \
     extern template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool, bool);                                 \
     extern template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool, bool);                                 \
+    extern template hipError_t filter_occupancy_s<S, uint32_t>(const KParams &, size_t, int *);                     \
+    extern template hipError_t filter_occupancy_s<S, uint64_t>(const KParams &, size_t, int *);                     \
     extern template hipError_t launch_search_s<S, uint32_t>(int, const KParams &, const SearchParams &, uint32_t,   \
                                                              size_t, hipStream_t);                                  \
     extern template hipError_t launch_search_s<S, uint64_t>(int, const KParams &, const SearchParams &, uint32_t,   \
@@ -180,6 +182,10 @@ hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, 
 
 hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t publish) {
     PK_DISPATCH(launch_bounded_s, p.S, p.wide, p, lc, st, publish)
+}
+
+hipError_t filter_occupancy(const KParams &p, size_t ent_lds, int *blocks) {
+    PK_DISPATCH(filter_occupancy_s, p.S, p.wide, p, ent_lds, blocks)
 }
 
 hipError_t eval_occupancy(const KParams &p, size_t lds, int *blocks) {

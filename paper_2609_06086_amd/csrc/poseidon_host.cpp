@@ -335,6 +335,7 @@ struct poseidon_ctx {
     unsigned long long *state;
     size_t lds_bytes;      // cost, pm, cap (and pd): search and Interleaved 1F1B kernels
     size_t ent_lds_bytes;  // stage entries (and pdx): evaluation and early-stop kernels
+    uint32_t filter_grid;  // blocks of the early-stop filter that are resident at once
     uint32_t grid_max;
     void *ws;              // cut codes + straggler queues of the steady-state cascade
     uint64_t ws_cap;       // candidates per chunk the workspace holds
@@ -678,7 +679,18 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         }
         ctx->lds_bytes = lds;
         ctx->ent_lds_bytes = elds;
+        // the early-stop filter's grid: one block per resident slot, each
+        // block looping over its share of a piece (a larger grid leaves a
+        // partial second wave of blocks, each paying for its LDS tables)
+        int focc = 0;
+        if (!ilv && pk::filter_occupancy(kp, elds, &focc) != hipSuccess) {
+            status = POSEIDON_E_DEVICE;
+            break;
+        }
         ctx->grid_max = (uint32_t)std::max(1, occ) * (uint32_t)std::max(1, prop.multiProcessorCount);
+        // (at most grid_max: the survivor segments are sized for that many blocks)
+        ctx->filter_grid = std::min(ctx->grid_max,
+                                    (uint32_t)std::max(1, focc) * (uint32_t)std::max(1, prop.multiProcessorCount));
     } while (0);
     (void)hipSetDevice(prev);
     if (status != POSEIDON_OK) {
@@ -993,7 +1005,7 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
             kp.n_i = s1 - s0;
             pk::LaunchCfg ld = lc;
             const uint64_t batch = (uint64_t)pk::kDecodeIlp * 256;
-            ld.grid = (uint32_t)std::min<uint64_t>((kp.n_i + batch - 1) / batch, ctx->grid_max);
+            ld.grid = (uint32_t)std::min<uint64_t>((kp.n_i + batch - 1) / batch, ctx->filter_grid);
             // block b filters kDecodeIlp candidates per lane per pass, ceil(n / (grid * batch)) passes
             kp.seg_cap = (kp.n_i + ld.grid * batch - 1) / (ld.grid * batch) * batch;
             if (pk::launch_bounded(kp, ld, st, s1 == hi) != hipSuccess) return rearm(ctx, st);

@@ -18,6 +18,8 @@
                                                        uint32_t);                                              \
     template hipError_t occupancy_s<S, uint32_t>(int *, size_t, bool, bool);                                        \
     template hipError_t occupancy_s<S, uint64_t>(int *, size_t, bool, bool);                                        \
+    template hipError_t filter_occupancy_s<S, uint32_t>(const KParams &, size_t, int *);                            \
+    template hipError_t filter_occupancy_s<S, uint64_t>(const KParams &, size_t, int *);                            \
     template hipError_t launch_search_s<S, uint32_t>(int, const KParams &, const SearchParams &, uint32_t, size_t,  \
                                                       hipStream_t);                                                 \
     template hipError_t launch_search_s<S, uint64_t>(int, const KParams &, const SearchParams &, uint32_t, size_t,  \

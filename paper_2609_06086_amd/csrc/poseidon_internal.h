@@ -150,6 +150,7 @@ hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, 
 hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t publish);
 constexpr int kDecodeIlp = 4;   // candidates per lane of the decode and early-stop filter kernels
 hipError_t eval_occupancy(const KParams &p, size_t lds, int *blocks);
+hipError_t filter_occupancy(const KParams &p, size_t ent_lds, int *blocks);
 hipError_t launch_ilv(const KParams &p, const LaunchCfg &lc, hipStream_t st);
 hipError_t ilv_occupancy(const KParams &p, size_t lds, int *blocks);
 hipError_t launch_ilv_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl);

@@ -1623,6 +1623,20 @@ hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t s
     return hipGetLastError();
 }
 
+// Resident blocks per CU of the early-stop filter instance launch_bounded_s
+// picks (its LDS: the Pascal columns plus the stage entries of `ent_lds`).
+template <int S, typename R>
+hipError_t filter_occupancy_s(const KParams &p, size_t ent_lds, int *blocks) {
+    const size_t pas = pascal_bytes<S, R>(p.L);
+    if (pas + ent_lds > kLdsBlockMax) {
+        if (p.has_ar) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, true, true>, kBlock, pas);
+        return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, false, true>, kBlock, pas);
+    }
+    if (p.has_ar)
+        return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, true, false>, kBlock, pas + ent_lds);
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, false, false>, kBlock, pas + ent_lds);
+}
+
 template <int S, typename R>
 hipError_t occupancy_s(int *blocks, size_t lds, bool ar, bool sched) {
     // schedules other than 1F1B: the closed-form kernel (the table kernel
