@@ -1087,12 +1087,68 @@ __device__ __forceinline__ uint32_t tree_step(uint32_t t, uint32_t probe, uint32
     return t;
 }
 
+// With 64-bit ranks the searches over columns 0 .. kNarrow-1 run in 32 bits:
+// C(n, k) < 2^32 for every n <= 255 and k <= 4, and at the search of a cut
+// whose column is k + 1 the remaining rank is below C(L - a, k + 1), so the
+// rank, Q and every probe fit 32 bits there.  Those columns are kept in LDS
+// as uint32 (half the bytes per probe); the others as R.
+template <int S, typename R>
+__host__ __device__ constexpr int narrow_cols() {
+    return sizeof(R) == 8 ? (S < 5 ? S : 5) : 0;
+}
+
+// LDS image of the Pascal columns: columns NN..S-1 as R, in order then in
+// tree order, followed by columns 0..NN-1 as uint32 the same way (NN =
+// narrow_cols), 2^H entries per column.
 template <int S, typename R, int H>
-__device__ __forceinline__ void decode_ilp(const KParams &p, const R *sorted, const R *ey, uint64_t base,
+struct Pascal {
+    static constexpr uint32_t NH = 1u << H;
+    static constexpr int NN = narrow_cols<S, R>();
+    const R *ws, *wt;                 // wide columns (sorted, tree), column c at (c - NN) * NH
+    const uint32_t *ns, *nt;          // narrow columns, column c at c * NH
+    __device__ __forceinline__ explicit Pascal(const void *base) {
+        ws = reinterpret_cast<const R *>(base);
+        wt = ws + (uint32_t)(S - NN) * NH;
+        ns = reinterpret_cast<const uint32_t *>(wt + (uint32_t)(S - NN) * NH);
+        nt = ns + (uint32_t)NN * NH;
+    }
+};
+
+// One cut's search for kIlp candidates over a column of type V (R or
+// uint32): Q = C(L - a, k + 1) - r, the smallest n with C(n, k + 1) >= Q by
+// the tree, the rank left C(n, k + 1) - Q, the cut L - n.
+template <typename V, typename R, int H>
+__device__ __forceinline__ void search_cut(const KParams &p, const V *col, const V *tree, R (&r)[kIlp],
+                                           uint32_t (&at)[kIlp], uint32_t (&cut)[kIlp]) {
+    constexpr uint32_t NH = 1u << H;
+    V Q[kIlp];
+    uint32_t t[kIlp];   // tree node
+#pragma unroll
+    for (int u = 0; u < kIlp; ++u) {
+        Q[u] = col[p.L - at[u]] - (V)r[u];
+        t[u] = 1;
+    }
+#pragma unroll
+    for (int b = 0; b < H; ++b) {
+#pragma unroll
+        for (int u = 0; u < kIlp; ++u) t[u] = tree_step(t[u], tree[t[u]], Q[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < kIlp; ++u) {
+        const uint32_t pos = t[u] - NH;
+        r[u] = (R)(col[pos] - Q[u]);
+        cut[u] = p.L - pos;
+        at[u] = cut[u] + 1;
+    }
+}
+
+template <int S, typename R, int H>
+__device__ __forceinline__ void decode_ilp(const KParams &p, const Pascal<S, R, H> &pc, uint64_t base,
                                            uint64_t stride, bool (&act)[kIlp], bool (&ok)[kIlp],
                                            uint32_t (&asg)[kIlp], uint32_t (&w)[kIlp][Codes<S>::kWords]) {
     constexpr int NW = Codes<S>::kWords;
     constexpr uint32_t NH = 1u << H;
+    constexpr int NN = Pascal<S, R, H>::NN;
     R r[kIlp];
     uint32_t at[kIlp];
 #pragma unroll
@@ -1105,31 +1161,16 @@ __device__ __forceinline__ void decode_ilp(const KParams &p, const R *sorted, co
         for (int k = 0; k < NW; ++k) w[u][k] = 0;
     }
     // the searches, cut by cut, interleaved over the kIlp candidates; each
-    // cut goes straight into its byte of the code words
+    // cut goes straight into its byte of the code words (cut j searches
+    // column S - j)
 #pragma unroll
     for (int j = 1; j <= S - 2; ++j) {
-        const R *col = sorted + (S - j) * NH;
-        const R *tree = ey + (S - j) * NH;
-        R Q[kIlp];
-        uint32_t t[kIlp];   // tree node
+        const int c = S - j;
+        uint32_t cut[kIlp];
+        if (c < NN) search_cut<uint32_t, R, H>(p, pc.ns + (uint32_t)c * NH, pc.nt + (uint32_t)c * NH, r, at, cut);
+        else search_cut<R, R, H>(p, pc.ws + (uint32_t)(c - NN) * NH, pc.wt + (uint32_t)(c - NN) * NH, r, at, cut);
 #pragma unroll
-        for (int u = 0; u < kIlp; ++u) {
-            Q[u] = col[p.L - at[u]] - r[u];
-            t[u] = 1;
-        }
-#pragma unroll
-        for (int b = 0; b < H; ++b) {
-#pragma unroll
-            for (int u = 0; u < kIlp; ++u) t[u] = tree_step(t[u], tree[t[u]], Q[u]);
-        }
-#pragma unroll
-        for (int u = 0; u < kIlp; ++u) {
-            const uint32_t pos = t[u] - NH;
-            r[u] = col[pos] - Q[u];
-            const uint32_t c = p.L - pos;
-            w[u][(j - 1) / 4] |= c << (8 * ((j - 1) % 4));
-            at[u] = c + 1;
-        }
+        for (int u = 0; u < kIlp; ++u) w[u][(j - 1) / 4] |= cut[u] << (8 * ((j - 1) % 4));
     }
     if (S >= 2) {
 #pragma unroll
@@ -1146,12 +1187,12 @@ __device__ __forceinline__ void decode_ilp(const KParams &p, const R *sorted, co
 }
 
 template <int S, typename R, int H>
-__device__ __forceinline__ void decode_batch(const KParams &p, const R *sorted, const R *ey, uint64_t base,
+__device__ __forceinline__ void decode_batch(const KParams &p, const Pascal<S, R, H> &pc, uint64_t base,
                                              uint64_t stride, bool &bad) {
     constexpr int NW = Codes<S>::kWords;
     bool act[kIlp], ok[kIlp];
     uint32_t asg[kIlp], w[kIlp][NW];
-    decode_ilp<S, R, H>(p, sorted, ey, base, stride, act, ok, asg, w);
+    decode_ilp<S, R, H>(p, pc, base, stride, act, ok, asg, w);
 #pragma unroll
     for (int u = 0; u < kIlp; ++u) {
         const uint64_t i = base + u * stride;
@@ -1164,36 +1205,47 @@ __device__ __forceinline__ void decode_batch(const KParams &p, const R *sorted, 
 }
 
 // Columns 0 .. S-1 of the Pascal table, 2^H entries each, into LDS in order
-// and in tree order; the tree node at depth l and offset m probes sorted
-// position (2m + 1) 2^(H-1-l) - 1 (entry 0 of the tree is unused).
+// and in tree order (layout of Pascal<S, R, H>); the tree node at depth l
+// and offset m probes sorted position (2m + 1) 2^(H-1-l) - 1 (entry 0 of
+// the tree is unused).  Narrow columns saturate at 2^32 - 1, which keeps
+// them sorted (no value of a column below 5 reaches it for n <= 255).
 template <int S, typename R, int H>
-__device__ __forceinline__ void pascal_tables(const KParams &p, R *lds) {
+__device__ __forceinline__ void pascal_tables(const KParams &p, void *lds) {
     constexpr uint32_t NH = 1u << H;
-    R *sorted = lds, *ey = lds + (uint32_t)S * NH;
+    constexpr int NN = narrow_cols<S, R>();
+    R *ws = reinterpret_cast<R *>(lds), *wt = ws + (uint32_t)(S - NN) * NH;
+    uint32_t *ns = reinterpret_cast<uint32_t *>(wt + (uint32_t)(S - NN) * NH), *nt = ns + (uint32_t)NN * NH;
     const R *gb = reinterpret_cast<const R *>(p.binom);
     for (uint32_t e = threadIdx.x; e < (uint32_t)S * NH; e += kBlock) {
         const uint32_t k = e / NH, i = e % NH;
-        sorted[e] = gb[k * kNB + i];
         const uint32_t l = i ? 31u - __clz(i) : 0u, m = i - (1u << l);
-        ey[e] = i ? gb[k * kNB + (2 * m + 1) * (NH >> (l + 1)) - 1] : (R)0;
+        const R vs = gb[k * kNB + i];
+        const R vt = i ? gb[k * kNB + (2 * m + 1) * (NH >> (l + 1)) - 1] : (R)0;
+        if ((int)k >= NN) {
+            ws[(k - NN) * NH + i] = vs;
+            wt[(k - NN) * NH + i] = vt;
+        } else {
+            ns[k * NH + i] = vs > (R)0xFFFFFFFFu ? 0xFFFFFFFFu : (uint32_t)vs;
+            nt[k * NH + i] = vt > (R)0xFFFFFFFFu ? 0xFFFFFFFFu : (uint32_t)vt;
+        }
     }
 }
 
 // LDS bytes of both copies of the S Pascal columns
 template <int S, typename R>
 __host__ __device__ constexpr size_t pascal_bytes(uint32_t L) {
-    return 2 * (size_t)S * ((size_t)1 << decode_levels(L)) * sizeof(R);
+    return 2 * ((size_t)1 << decode_levels(L)) * ((size_t)(S - narrow_cols<S, R>()) * sizeof(R) +
+                                                  (size_t)narrow_cols<S, R>() * 4);
 }
 
 template <int S, typename R, int H>
-__device__ __forceinline__ void decode_all(const KParams &p, R *lds, bool &bad) {
-    constexpr uint32_t NH = 1u << H;
-    R *sorted = lds, *ey = lds + (uint32_t)S * NH;
+__device__ __forceinline__ void decode_all(const KParams &p, void *lds, bool &bad) {
     pascal_tables<S, R, H>(p, lds);
     __syncthreads();
+    const Pascal<S, R, H> pc(lds);
     const uint64_t stride = (uint64_t)gridDim.x * kBlock;
     for (uint64_t base = (uint64_t)blockIdx.x * kBlock + threadIdx.x; base < p.n_i; base += kIlp * stride)
-        decode_batch<S, R, H>(p, sorted, ey, base, stride, bad);
+        decode_batch<S, R, H>(p, pc, base, stride, bad);
 }
 
 template <int S, typename R>
@@ -1421,14 +1473,14 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
                                            uint32_t &n_infeas, bool &bad) {
     constexpr int NW = Codes<S>::kWords;
     constexpr uint32_t NH = 1u << H;
-    const R *sorted = pas, *ey = pas + (uint32_t)S * NH;
+    const Pascal<S, R, H> pc(pas);
     const uint64_t stride = (uint64_t)gridDim.x * kBlock;
     const unsigned int lane = threadIdx.x & 63;
     const uint64_t seg = (uint64_t)blockIdx.x * p.seg_cap;
     for (uint64_t base = (uint64_t)blockIdx.x * kBlock + threadIdx.x; base < p.n_i; base += kIlp * stride) {
         bool act[kIlp], ok[kIlp];
         uint32_t asg[kIlp], w[kIlp][NW];
-        decode_ilp<S, R, H>(p, sorted, ey, base, stride, act, ok, asg, w);
+        decode_ilp<S, R, H>(p, pc, base, stride, act, ok, asg, w);
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) {
             uint32_t cut[S + 1], to[S], F[S], B[S], G[S], D[S];
