@@ -218,6 +218,20 @@ hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, 
     return hipGetLastError();
 }
 
+// Several short fills in one launch (one thread per word).
+__global__ void fill_u64_ranges(FillRanges r) {
+    uint32_t base = 0;
+    for (uint32_t k = 0; k < r.n && k < 4; ++k) {
+        if (threadIdx.x >= base && threadIdx.x < base + r.count[k]) r.ptr[k][threadIdx.x - base] = r.value[k];
+        base += r.count[k];
+    }
+}
+
+hipError_t launch_fills(const FillRanges &r, hipStream_t st) {
+    hipLaunchKernelGGL(fill_u64_ranges, dim3(1), dim3(64), 0, st, r);
+    return hipGetLastError();
+}
+
 int code_words(int S) { return S > 1 ? (S - 1 + 3) / 4 : 1; }
 int prologue_op(int S, int s, int k) { return pro_op(S, s, k); }
 int eager_op(int S, int M, int s, int k) {

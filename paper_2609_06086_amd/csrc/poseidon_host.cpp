@@ -973,11 +973,14 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
     hipStream_t st = (hipStream_t)hip_stream;
     DeviceGuard g(ctx->device);
     if (!g.ok) return POSEIDON_E_DEVICE;
-    // re-arm the running best, its snapshot and the counters (fill kernels, not memsets)
-    if (pk::launch_fill(ctx->state + W_RUN, 1, ~0ull, st) != hipSuccess ||
-        pk::launch_fill(ctx->state + W_SNAP, 1, ~0ull, st) != hipSuccess ||
-        pk::launch_fill(ctx->state + W_STAT_EVAL, 3, 0ull, st) != hipSuccess)
-        return POSEIDON_E_DEVICE;
+    // re-arm the running best, its snapshot and the counters (one fill
+    // kernel, not memsets)
+    pk::FillRanges fr;
+    fr.n = 3;
+    fr.ptr[0] = ctx->state + W_RUN; fr.count[0] = 1; fr.value[0] = ~0ull;
+    fr.ptr[1] = ctx->state + W_SNAP; fr.count[1] = 1; fr.value[1] = ~0ull;
+    fr.ptr[2] = ctx->state + W_STAT_EVAL; fr.count[2] = 3; fr.value[2] = 0ull;
+    if (pk::launch_fills(fr, st) != hipSuccess) return POSEIDON_E_DEVICE;
     pk::KParams kp = ctx->base;
     kp.first = cands->first;
     kp.count = cands->count;

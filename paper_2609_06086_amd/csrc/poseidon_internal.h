@@ -164,6 +164,14 @@ bool ilv_program_words(uint32_t S, uint32_t N, int *start, int *tail, uint32_t *
 hipError_t launch_argmin(const uint32_t *T, const uint32_t *bits, uint64_t count, uint32_t grid,
                          unsigned long long *acc, unsigned int *done, unsigned long long *result, hipStream_t st);
 hipError_t launch_fill(unsigned long long *p, uint32_t n, unsigned long long v, hipStream_t st);
+// up to four ranges of words, 64 words in all, filled by one launch
+struct FillRanges {
+    uint32_t n;
+    unsigned long long *ptr[4];
+    uint32_t count[4];
+    unsigned long long value[4];
+};
+hipError_t launch_fills(const FillRanges &r, hipStream_t st);
 // Scratch of the allocation-free evaluation: the device address of the
 // library's fixed scratch array on `device`, looked up once per device
 // (with that device current) and kept; null if the lookup failed.
