@@ -260,6 +260,10 @@ def search_bench(args):
     warm = P.poseidon_eval_candidates(ctx, comp_rank=torch.from_numpy(c.comp_rank[:500].view(np.int64)).to(dev),
                                       assign_idx=torch.from_numpy(c.assign_idx[:500].view(np.int32)).to(dev))
     bound = warm.makespan
+    if args.copy_calibration_mib:
+        a = torch.empty(args.copy_calibration_mib << 18, dtype=torch.int32, device=dev)
+        torch.empty_like(a).copy_(a)
+        torch.cuda.synchronize()
     rpc = args.rows_per_chunk
     ramp = not args.fixed_chunks
     chunking = f"chunks of 1, 2, 4, ... up to {rpc} rows" if ramp else f"{rpc} rows per chunk"
@@ -335,7 +339,7 @@ def profile_only(args):
 PASS_KERNELS = {
     "exhaustive": r"pk::(decode_kernel|eval_kernel|sched_kernel|resume_kernel|ilv_kernel|ilv_resume_kernel)",
     "early_stop": r"pk::(filter_kernel|surv_kernel|fill_u64)",
-    "search": r"pk::(search_|fill_u64|decode_kernel|eval_kernel|resume_kernel)",
+    "search": r"pk::(search_|fill_u64)",
 }
 
 
@@ -514,7 +518,8 @@ def main():
                          "up to --rows-per-chunk)")
     ap.add_argument("--ridge", action="store_true", help="with --search: layer-level (ridge) pruning")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
-                    help="with --only: also run one plain device copy of this size (for counter scaling)")
+                    help="with --only or --search: also run one plain device copy of this size (for counter "
+                         "scaling)")
     # summaries of rocprofv3 output
     ap.add_argument("--summarize", metavar="DIR")
     ap.add_argument("--tag")
