@@ -49,7 +49,8 @@ PEAK_INT32_TOPS = 256 * 64 * 2.4e9 / 1e12   # CUs x lanes x clock: one 32-bit op
 N_SIMD, PEAK_CLOCK = 256 * 4, 2.4e9
 CSRC = os.path.join(ROOT, "paper_2609_06086_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
-ES_CHUNK = 1 << 22          # early-stop chunk: the bound tightens to the best found every 4 Mi candidates
+ES_CHUNK = 0                # early-stop chunk (0 = one chunk: every candidate is filtered against the
+                            # warm-up bound; the survivors are few, so more chunks cost more than they prune)
 ES_WARMUP = 500             # warm-up samples that set the first bound (Sec. 4.2.3)
 
 
@@ -182,8 +183,8 @@ class Eval:
         wb = self.P.poseidon_eval_candidates(self.ctx, **warm)
         return wb.makespan if wb.makespan is not None else 2 ** 31
 
-    def bounded(self, bound):
-        return self.P.poseidon_eval_candidates_bounded(self.ctx, bound, chunk=ES_CHUNK, stream=self.stream,
+    def bounded(self, bound, chunk=ES_CHUNK, ramp=False):
+        return self.P.poseidon_eval_candidates_bounded(self.ctx, bound, chunk=chunk, ramp=ramp, stream=self.stream,
                                                        **self.cand)
 
     def close(self):
@@ -208,18 +209,20 @@ def eval_record(wl, dev, args, schedule="1f1b", early_stop=True, cpu_s=0.0):
                                 algo_bytes, "one poseidon_eval_candidates call: decode, eval and resume kernels")}
     if early_stop and wl.cands.is_list and schedule != "interleaved":
         bound = e.warm_bound()
-        es_ms_wall, es_ms, (bb, st) = timed(torch, lambda: e.bounded(bound), max(1, args.steps // 5),
-                                            max(1, args.warmup // 5), e.stream)
+        es_ms_wall, es_ms, (bb, st) = timed(torch, lambda: e.bounded(bound, args.es_chunk, args.es_ramp),
+                                            max(1, args.steps // 5), max(1, args.warmup // 5), e.stream)
+        chunking = ("one chunk" if args.es_chunk == 0 else
+                    f"chunks of {args.es_chunk}, doubling" if args.es_ramp else f"chunks of {args.es_chunk}")
         rec["early_stop"] = {
             "ms": es_ms_wall, "kernel_ms": es_ms, "candidates_per_s": n / (es_ms_wall * 1e-3),
             "speedup_vs_exhaustive": ms_wall / es_ms_wall,
-            "warmup_samples": ES_WARMUP, "warmup_bound": bound, "chunk": ES_CHUNK,
+            "warmup_samples": ES_WARMUP, "warmup_bound": bound, "chunk": args.es_chunk, "ramp": args.es_ramp,
             "evaluated": st.evaluated, "pruned": st.pruned, "infeasible": st.infeasible,
             "best_index": bb.index, "best_makespan": bb.makespan,
             "same_argmin_as_exhaustive": (bb.index, bb.makespan) == (best.index, best.makespan),
             "roofline": roofline(committed_counters(profile_tag("early_stop", prob, schedule)), es_ms, None, None,
-                                 "one poseidon_eval_candidates_bounded call: filter and survivor kernels "
-                                 "per 4 Mi chunk")}
+                                 "one poseidon_eval_candidates_bounded call: filter and survivor kernels, "
+                                 + chunking)}
     e.close()
     if cpu_s > 0:
         rec["cpu_baseline"] = cpu_baseline(wl, cpu_s)
@@ -328,7 +331,8 @@ def profile_only(args):
         ms, call_ms, _ = timed(torch, e.step, args.steps, args.warmup, e.stream)
     else:
         bound = e.warm_bound()
-        ms, call_ms, _ = timed(torch, lambda: e.bounded(bound), args.steps, args.warmup, e.stream)
+        ms, call_ms, _ = timed(torch, lambda: e.bounded(bound, args.es_chunk, args.es_ramp), args.steps, args.warmup,
+                               e.stream)
     e.close()
     print(json.dumps({"pass": args.only, "workload": wl.description, "calls": args.steps + args.warmup,
                       "ms": ms, "kernel_ms": call_ms}), flush=True)
@@ -504,6 +508,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-early-stop", action="store_true")
+    ap.add_argument("--es-chunk", type=int, default=ES_CHUNK,
+                    help="early-stop chunk in candidates (0 = one chunk: every candidate against the warm-up bound)")
+    ap.add_argument("--es-ramp", action="store_true", help="early-stop chunks double: es-chunk, 2 es-chunk, ...")
     ap.add_argument("--no-sub", action="store_true", help="headline workload only (no sub-records)")
     ap.add_argument("--schedule", default="1f1b", choices=["1f1b", "eager", "interleaved"],
                     help="pipeline schedule of the DAG (1F1B, Eager 1F1B, or Interleaved 1F1B with "

@@ -208,18 +208,25 @@ int poseidon_eval_candidates_noalloc(poseidon_ctx *ctx, const poseidon_cands *ca
 int poseidon_last_best(poseidon_ctx *ctx, poseidon_best *best_out, void *hip_stream);
 
 /* Early-stop search (Eq. 2, Theorem 1).  The candidates are processed in
- * consecutive chunks of `chunk` entries (0 = one chunk).  Within a chunk,
+ * consecutive chunks of `chunk` entries (0 = one chunk); with flag
+ * POSEIDON_BOUNDED_RAMP the chunks grow instead as chunk, 2 chunk, 4 chunk,
+ * ... entries, so that an early chunk sets a bound soon and the later ones
+ * pay the fixed cost of a chunk (one pass of the filter and survivor kernels)
+ * fewer times.  Within a chunk,
  * a feasible candidate whose lower bound max_x g(S_x) exceeds
  * b = min(bound, best makespan found in earlier chunks) is skipped; all
  * other feasible candidates are evaluated exactly.  The reduction is the
  * same as poseidon_eval_candidates', over evaluated candidates; if its
  * makespan is > bound the call returns POSEIDON_NO_FEASIBLE.  The result
- * is deterministic for a given chunk size.  best_out and stats_out are HOST
- * pointers (either may be NULL); the call synchronises the stream.
- * POSEIDON_E_INVAL for Interleaved 1F1B problems. */
+ * is deterministic for a given chunk size and flags.  best_out and
+ * stats_out are HOST pointers (either may be NULL); the call synchronises
+ * the stream.  POSEIDON_E_INVAL for Interleaved 1F1B problems or unknown
+ * flags. */
+#define POSEIDON_BOUNDED_RAMP 1u
 int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *cands,
-                                     uint32_t bound, uint64_t chunk, poseidon_best *best_out,
-                                     poseidon_prune_stats *stats_out, void *hip_stream);
+                                     uint32_t bound, uint64_t chunk, uint32_t flags,
+                                     poseidon_best *best_out, poseidon_prune_stats *stats_out,
+                                     void *hip_stream);
 
 /* Argmin over arrays a previous evaluation wrote (DEVICE pointers,
  * `count` entries, layouts as for poseidon_eval_candidates; feasible_bits

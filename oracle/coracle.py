@@ -49,7 +49,7 @@ def lib():
                                  C.c_void_p, C.c_void_p, C.c_void_p, C.c_int]
         _lib.oc_bounded.restype = C.c_int
         _lib.oc_bounded.argtypes = [C.POINTER(_Problem), C.c_uint64, C.c_uint64, C.c_void_p,
-                                    C.c_void_p, C.c_uint32, C.c_uint64,
+                                    C.c_void_p, C.c_uint32, C.c_uint64, C.c_int,
                                     C.POINTER(C.c_uint64), C.POINTER(C.c_uint32),
                                     C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
                                     C.POINTER(C.c_uint64), C.c_int]
@@ -118,8 +118,10 @@ def evaluate(prob, cands, nthreads: Optional[int] = None, lo: int = 0, hi: Optio
     return out_T, out_f.astype(bool)
 
 
-def bounded(prob, cands, bound: int, chunk: int = 0, nthreads: Optional[int] = None):
-    """Early-stop pass; returns (best (idx, T) or None, evaluated, pruned, infeasible)."""
+def bounded(prob, cands, bound: int, chunk: int = 0, nthreads: Optional[int] = None, ramp: bool = False):
+    """Early-stop pass (chunks of `chunk` candidates, or with ramp chunk,
+    2 chunk, 4 chunk, ...); returns (best (idx, T) or None, evaluated,
+    pruned, infeasible)."""
     st, keep = _problem(prob)
     n = len(cands)
     bi, bt = C.c_uint64(), C.c_uint32()
@@ -127,11 +129,11 @@ def bounded(prob, cands, bound: int, chunk: int = 0, nthreads: Optional[int] = N
     if cands.is_list:
         rank = np.ascontiguousarray(cands.comp_rank, dtype=np.uint64)
         aidx = None if cands.assign_idx is None else np.ascontiguousarray(cands.assign_idx, dtype=np.uint32)
-        rc = lib().oc_bounded(C.byref(st), 0, n, _ptr(rank), _ptr(aidx), bound, chunk,
+        rc = lib().oc_bounded(C.byref(st), 0, n, _ptr(rank), _ptr(aidx), bound, chunk, int(ramp),
                               C.byref(bi), C.byref(bt), C.byref(ev), C.byref(pr), C.byref(inf),
                               nthreads or default_threads())
     else:
-        rc = lib().oc_bounded(C.byref(st), cands.first, n, None, None, bound, chunk,
+        rc = lib().oc_bounded(C.byref(st), cands.first, n, None, None, bound, chunk, int(ramp),
                               C.byref(bi), C.byref(bt), C.byref(ev), C.byref(pr), C.byref(inf),
                               nthreads or default_threads())
     if rc != 0:

@@ -457,11 +457,11 @@ def eq2_bound(F: Sequence[int], B: Sequence[int], M: int,
     return best
 
 
-def bounded_search(prob, cands, bound: int, chunk: int = 0):
+def bounded_search(prob, cands, bound: int, chunk: int = 0, ramp: bool = False):
     """Early-stop pass (Thm. 1, reading R10) over a candidate list.
 
     The list is cut into consecutive chunks of `chunk` entries (0 = one
-    chunk).  Each chunk prunes against b = min(bound, best makespan found in
+    chunk), or with ramp into chunks of chunk, 2 chunk, 4 chunk, ... entries.  Each chunk prunes against b = min(bound, best makespan found in
     earlier chunks); a feasible candidate with max_x g(S_x) > b is pruned,
     every other feasible one is evaluated exactly.  The result is the
     (makespan, index)-smallest evaluated candidate if its makespan is
@@ -472,12 +472,16 @@ def bounded_search(prob, cands, bound: int, chunk: int = 0):
     dag = dag_for(prob.S, prob.M, getattr(prob, "schedule", 0))
     lst = candidate_list(prob, cands)
     n = len(lst)
-    chunk = n if chunk <= 0 else chunk
+    size = n if chunk <= 0 else chunk
     best = None
     evaluated = pruned = infeasible = 0
-    for c0 in range(0, n, chunk):
+    c0 = 0
+    while c0 < n:
+        c1 = min(n, c0 + size)
+        if ramp:
+            size *= 2
         b = bound if best is None else min(bound, best[1])
-        for i, cuts, types in lst[c0:c0 + chunk]:
+        for i, cuts, types in lst[c0:c1]:
             F, B, _, D, ok = stage_weights(prob, cuts, types, allreduce)
             d = D if allreduce is not None else None
             if not ok:
@@ -490,6 +494,7 @@ def bounded_search(prob, cands, bound: int, chunk: int = 0):
             t = longest_path(dag, F, B, prob.comm_fwd, prob.comm_bwd, d)
             if best is None or (t, i) < best[::-1]:
                 best = (i, t)
+        c0 = c1
     if best is not None and best[1] > bound:
         best = None
     return best, evaluated, pruned, infeasible

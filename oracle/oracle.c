@@ -438,7 +438,7 @@ int oc_eval(const oc_problem *p, uint64_t first, uint64_t count, const uint64_t 
 /* Early-stop pass in chunks (0 = one chunk); see header comment.  Returns 0
  * with *best_idx = UINT64_MAX if nothing evaluated has makespan <= bound. */
 int oc_bounded(const oc_problem *p, uint64_t first, uint64_t count, const uint64_t *rank,
-               const uint32_t *aidx, uint32_t bound, uint64_t chunk, uint64_t *best_idx,
+               const uint32_t *aidx, uint32_t bound, uint64_t chunk, int ramp, uint64_t *best_idx,
                uint32_t *best_T, uint64_t *evaluated, uint64_t *pruned, uint64_t *infeasible,
                int nthreads) {
     if (check(p) || p->schedule == 2) return -1;   /* Eq. 2 is stated for one stage per device */
@@ -452,8 +452,11 @@ int oc_bounded(const oc_problem *p, uint64_t first, uint64_t count, const uint64
     uint64_t bT = UINT64_MAX, bI = UINT64_MAX, ev = 0, pr = 0, inf = 0;
     int err = 0;
     oc_job jobs[256];
-    for (uint64_t c0 = 0; c0 < count && !err; c0 += chunk) {
-        uint64_t c1 = c0 + chunk < count ? c0 + chunk : count;
+    /* chunks of `chunk` candidates, or (ramp) chunk, 2 chunk, 4 chunk, ... */
+    uint64_t size = chunk;
+    for (uint64_t c0 = 0, c1; c0 < count && !err; c0 = c1) {
+        c1 = count - c0 > size ? c0 + size : count;
+        if (ramp && size < count) size *= 2;
         proto.bound = bT < bound ? bT : bound;
         int nt = run_jobs(&proto, c0, c1, nthreads, jobs);
         for (int t = 0; t < nt; ++t) {

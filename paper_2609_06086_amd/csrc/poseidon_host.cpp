@@ -965,11 +965,13 @@ int poseidon_last_best(poseidon_ctx *ctx, poseidon_best *best_out, void *hip_str
 }
 
 int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *cands, uint32_t bound,
-                                     uint64_t chunk, poseidon_best *best_out, poseidon_prune_stats *stats_out,
-                                     void *hip_stream) {
+                                     uint64_t chunk, uint32_t flags, poseidon_best *best_out,
+                                     poseidon_prune_stats *stats_out, void *hip_stream) {
     int rc = check_cands(ctx, cands);
     if (rc != POSEIDON_OK) return rc;
     if (ctx->base.sched == POSEIDON_SCHEDULE_INTERLEAVED_1F1B) return POSEIDON_E_INVAL;
+    if (flags & ~POSEIDON_BOUNDED_RAMP) return POSEIDON_E_INVAL;
+    const bool ramp = flags & POSEIDON_BOUNDED_RAMP;
     hipStream_t st = (hipStream_t)hip_stream;
     DeviceGuard g(ctx->device);
     if (!g.ok) return POSEIDON_E_DEVICE;
@@ -991,7 +993,7 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
     // the survivor list has room for the survivors of kChunk candidates; a
     // longer chunk is filtered in pieces that all see the bound in force at
     // the chunk's start (the snapshot moves only at chunk ends)
-    rc = ensure_workspace(ctx, std::min<uint64_t>(chunk, kChunk), st);
+    rc = ensure_workspace(ctx, std::min<uint64_t>(ramp ? n : chunk, kChunk), st);
     if (rc != POSEIDON_OK) return rc;
     kp.codes = (uint32_t *)ctx->ws;
     kp.ccap = ctx->ws_cap;
@@ -1000,8 +1002,10 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
     kp.es_bound = bound;
     pk::LaunchCfg lc;
     lc.lds_bytes = ctx->ent_lds_bytes;
-    for (uint64_t lo = 0; lo < n; lo += chunk) {
-        const uint64_t hi = std::min(n, lo + chunk);
+    uint64_t size = chunk;
+    for (uint64_t lo = 0, hi; lo < n; lo = hi) {
+        hi = n - lo > size ? lo + size : n;
+        if (ramp && size < n) size *= 2;
         for (uint64_t s0 = lo; s0 < hi; s0 += kChunk) {
             const uint64_t s1 = std::min(hi, s0 + kChunk);
             kp.first_i = s0;

@@ -26,6 +26,7 @@ POSEIDON_E_DEVICE = -3
 POSEIDON_E_NOMEM = -4
 SCHEDULE_1F1B, SCHEDULE_EAGER_1F1B, SCHEDULE_INTERLEAVED_1F1B = 0, 1, 2
 SEARCH_RIDGE, SEARCH_NO_STAGE_PRUNING, SEARCH_RAMP = 1, 2, 4
+BOUNDED_RAMP = 1
 S_MAX, L_MAX, T_MAX, M_MAX = 16, 256, 8, 1 << 20
 
 
@@ -111,7 +112,8 @@ def lib():
         L.poseidon_last_best.argtypes = [C.c_void_p, C.POINTER(_Best), C.c_void_p]
         L.poseidon_last_best.restype = C.c_int
         L.poseidon_eval_candidates_bounded.argtypes = [C.c_void_p, C.POINTER(_Cands), C.c_uint32, C.c_uint64,
-                                                       C.POINTER(_Best), C.POINTER(_Stats), C.c_void_p]
+                                                       C.c_uint32, C.POINTER(_Best), C.POINTER(_Stats),
+                                                       C.c_void_p]
         L.poseidon_eval_candidates_bounded.restype = C.c_int
         L.poseidon_argmin.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_uint64, C.c_uint64,
                                       C.POINTER(_Best), C.c_void_p]
@@ -264,12 +266,15 @@ def poseidon_last_best(ctx: Context, stream=None) -> Best:
 
 
 def poseidon_eval_candidates_bounded(ctx: Context, bound: int, *, chunk: int = 0, first: int = 0,
-                                     count: int = 0, comp_rank=None, assign_idx=None, stream=None):
-    """Early-stop pass; returns (Best, PruneStats)."""
+                                     count: int = 0, comp_rank=None, assign_idx=None, ramp: bool = False,
+                                     stream=None):
+    """Early-stop pass (chunks of `chunk`, or with ramp chunk, 2 chunk,
+    4 chunk, ...); returns (Best, PruneStats)."""
     c = _cands(first, count, comp_rank, assign_idx)
     b, s = _Best(), _Stats()
-    rc = lib().poseidon_eval_candidates_bounded(ctx.handle, C.byref(c), int(bound), int(chunk), C.byref(b),
-                                                C.byref(s), _stream(stream))
+    rc = lib().poseidon_eval_candidates_bounded(ctx.handle, C.byref(c), int(bound), int(chunk),
+                                                BOUNDED_RAMP if ramp else 0, C.byref(b), C.byref(s),
+                                                _stream(stream))
     if rc < 0:
         raise PoseidonError(rc, "poseidon_eval_candidates_bounded")
     return _best(rc, b), PruneStats(int(s.evaluated), int(s.pruned), int(s.infeasible))

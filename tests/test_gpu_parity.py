@@ -365,10 +365,10 @@ def test_async_then_last_best(dev):
 
 # ------------------------------------------------------------- early stop
 
-def bounded_vs_oracle(prob, cands, bound, chunk, dev):
+def bounded_vs_oracle(prob, cands, bound, chunk, dev, ramp=False):
     ctx = P.poseidon_load_costs(prob, 0)
-    b, st = P.poseidon_eval_candidates_bounded(ctx, bound, chunk=chunk, **to_dev(cands, dev))
-    ob, ev, pr, inf = coracle.bounded(prob, cands, bound, chunk)
+    b, st = P.poseidon_eval_candidates_bounded(ctx, bound, chunk=chunk, ramp=ramp, **to_dev(cands, dev))
+    ob, ev, pr, inf = coracle.bounded(prob, cands, bound, chunk, ramp=ramp)
     got = (b.index, b.makespan) if b.index is not None else None
     assert got == (None if ob is None else (ob[0] + index_base(cands), ob[1]))
     assert (st.evaluated, st.pruned, st.infeasible) == (ev, pr, inf)
@@ -404,8 +404,8 @@ def test_bounded_random(dev):
         To, fo = coracle.evaluate(prob, cands)
         warm = coracle.argmin(To[:50], fo[:50])
         bound = warm[1] if warm else 2 ** 31
-        for chunk in (0, 4096, 777):
-            b, _ = bounded_vs_oracle(prob, cands, bound, chunk, dev)
+        for chunk, ramp in ((0, False), (4096, False), (777, False), (100, True)):
+            b, _ = bounded_vs_oracle(prob, cands, bound, chunk, dev, ramp)
             ex = coracle.argmin(To, fo)
             if ex is not None and ex[1] <= bound:
                 assert (b.index, b.makespan) == ex   # Theorem 1: same argmin as exhaustive
@@ -417,8 +417,8 @@ def test_bounded_workload4_prefix(dev):
     c = W.Candidates(comp_rank=wl.cands.comp_rank[:n].copy(), assign_idx=wl.cands.assign_idx[:n].copy())
     To, fo = coracle.evaluate(wl.problem, W.Candidates(comp_rank=c.comp_rank[:500], assign_idx=c.assign_idx[:500]))
     bound = coracle.argmin(To, fo)[1]
-    for chunk in (0, 1 << 16, 100_000):
-        b, st = bounded_vs_oracle(wl.problem, c, bound, chunk, dev)
+    for chunk, ramp in ((0, False), (1 << 16, False), (100_000, False), (1 << 12, True)):
+        b, st = bounded_vs_oracle(wl.problem, c, bound, chunk, dev, ramp)
         assert st.pruned > 0
 
 

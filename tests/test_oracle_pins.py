@@ -342,10 +342,10 @@ def test_bounded_search_theorem1():
             continue
         warm = dag.argmin(Tx[:20], fx[:20])
         bound = warm[1] if warm else 2 ** 32 - 1
-        for chunk in (0, 17, 64):
-            best, ev, pr, inf = dag.bounded_search(prob, lst, bound, chunk)
+        for chunk, ramp in ((0, False), (17, False), (64, False), (1, True), (9, True)):
+            best, ev, pr, inf = dag.bounded_search(prob, lst, bound, chunk, ramp=ramp)
             assert best == exact
-            bc = coracle.bounded(prob, lst, bound, chunk, nthreads=3)
+            bc = coracle.bounded(prob, lst, bound, chunk, nthreads=3, ramp=ramp)
             assert bc == (best, ev, pr, inf)
             assert ev + pr + inf == len(lst) and inf == int((~fx).sum())
         # every candidate pruned against the fixed bound is strictly worse than it
@@ -353,6 +353,33 @@ def test_bounded_search_theorem1():
             F, B, _, _, ok = dag.stage_weights(prob, cuts, types)
             if ok and dag.eq2_bound(F, B, M) > bound:
                 assert Tx[i] > bound
+
+
+def test_bounded_ramp_chunks_double():
+    """With ramp the chunks are [0, c), [c, 3c), [3c, 7c), ...: running the
+    fixed-chunk pass on each piece in turn, the bound of each piece being the
+    best makespan of the pieces before it, gives the same counts."""
+    rng = np.random.default_rng(16)
+    for trial in range(6):
+        prob = W.random_problem(rng, 12, 4, int(rng.integers(2, 9)), 2, mem_hi=15, cap=90)
+        n = int(rng.integers(40, 130))
+        cands = W.random_candidates(rng, prob, n)
+        bound = 2 ** 32 - 1
+        c = int(rng.integers(1, 6))
+        lo, size, best, tot = 0, c, None, [0, 0, 0]
+        while lo < n:
+            hi = min(n, lo + size)
+            size *= 2
+            piece = W.Candidates(comp_rank=cands.comp_rank[lo:hi],
+                                 assign_idx=None if cands.assign_idx is None else cands.assign_idx[lo:hi])
+            b = bound if best is None else min(bound, best[1])
+            pb, ev, pr, inf = dag.bounded_search(prob, piece, b)
+            tot = [tot[0] + ev, tot[1] + pr, tot[2] + inf]
+            if pb is not None and (best is None or (pb[1], pb[0] + lo) < (best[1], best[0])):
+                best = (pb[0] + lo, pb[1])
+            lo = hi
+        assert dag.bounded_search(prob, cands, bound, c, ramp=True) == (best, *tot)
+        assert coracle.bounded(prob, cands, bound, c, ramp=True) == (best, *tot)
 
 
 def test_bounded_search_no_candidate_under_bound():
