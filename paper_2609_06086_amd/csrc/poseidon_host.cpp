@@ -1002,6 +1002,9 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
     kp.es_bound = bound;
     pk::LaunchCfg lc;
     lc.lds_bytes = ctx->ent_lds_bytes;
+    // survivor kernel: as many blocks as the evaluation kernel keeps resident
+    // (those the survivors need run, the others leave at once)
+    lc.grid2 = ctx->grid_max;
     uint64_t size = chunk;
     for (uint64_t lo = 0, hi; lo < n; lo = hi) {
         hi = n - lo > size ? lo + size : n;

@@ -139,8 +139,9 @@ __host__ __device__ constexpr size_t entry_bytes(uint32_t T, bool ar) {
 }
 
 struct LaunchCfg {
-    uint32_t grid;
-    size_t lds_bytes;     // stage tables: the entries (evaluation, early-stop kernels) or cost, pm,
+    uint32_t grid = 0;
+    uint32_t grid2 = 0;   // early stop: blocks of the survivor kernel
+    size_t lds_bytes = 0;     // stage tables: the entries (evaluation, early-stop kernels) or cost, pm,
                           // cap (search and Interleaved 1F1B kernels)
 };
 

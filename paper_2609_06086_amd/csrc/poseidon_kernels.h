@@ -946,7 +946,8 @@ __device__ __forceinline__ void block_min_and_finish(unsigned long long v, unsig
                                                      unsigned int *done, unsigned long long *result,
                                                      unsigned long long *run_best, bool finalize,
                                                      bool accumulate = false,
-                                                     unsigned long long *snap = nullptr) {
+                                                     unsigned long long *snap = nullptr,
+                                                     uint32_t nblocks = 0) {
     __shared__ unsigned long long part[kWaves];
     v = wave_min(v);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -960,7 +961,7 @@ __device__ __forceinline__ void block_min_and_finish(unsigned long long v, unsig
         if (finalize) {
             __threadfence();
             const unsigned int ticket = atomicAdd(done, 1u);
-            if (ticket == gridDim.x - 1) {
+            if (ticket == (nblocks ? nblocks : gridDim.x) - 1) {
                 __threadfence();
                 const unsigned long long k = atomicExch(acc, ~0ull);
                 if (result) {
@@ -1567,35 +1568,45 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(KParams p) {
     if (bad) atomicOr(p.err, 1u);
 }
 
-// Block b evaluates segments [b kSurvSegs, (b + 1) kSurvSegs) of the survivor
-// list (those of filter_kernel's blocks), their entries spread over its
-// threads as one list.  Fewer blocks than segments: each block pays for the
-// LDS tables and one ticket on the grid's done counter, whose single address
-// serialises the blocks.
-constexpr uint32_t kSurvSegs = 8;
-
+// surv_kernel takes the survivor list as one sequence in segment order
+// (segment j: scount[j] entries from j seg_cap).  Every block scans the nseg
+// segment counts into LDS, after the stage entries; survivor k then goes to
+// thread k mod (grid kBlock), found by a binary search of the scan, so the
+// DPs of however many survivors spread over the whole grid, 64 to a wave.
+// Only the blocks the list needs (one per kBlock survivors, at least one)
+// go on: the others leave before loading the entries and take no ticket on
+// the done counter.
 template <int S, bool AR, bool SCH>
 __global__ __launch_bounds__(kBlock) void surv_kernel(KParams p, uint32_t publish, uint32_t nseg) {
     extern __shared__ __align__(16) unsigned char smem[];
-    __shared__ uint32_t pre[kSurvSegs + 1];
-    const uint32_t s0 = blockIdx.x * kSurvSegs, ns = min(kSurvSegs, nseg - s0);
-    if (threadIdx.x == 0) {
-        uint32_t t = 0;
-        pre[0] = 0;
-        for (uint32_t j = 0; j < ns; ++j) {
-            t += __hip_atomic_load(&p.scount[s0 + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            pre[j + 1] = t;
-        }
+    uint32_t *pre = reinterpret_cast<uint32_t *>(smem + p.ent_lds);   // nseg + 1 entries
+    // exclusive scan of the segment counts, kPer consecutive segments a thread
+    const uint32_t per = (nseg + kBlock - 1) / kBlock, j0 = threadIdx.x * per;
+    uint32_t mine = 0;
+    for (uint32_t j = j0; j < j0 + per && j < nseg; ++j)
+        mine += __hip_atomic_load(&p.scount[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    unsigned long long total;
+    uint32_t run = (uint32_t)block_exclusive_scan_u64(mine, total);
+    for (uint32_t j = j0; j < j0 + per && j < nseg; ++j) {
+        pre[j] = run;
+        run += __hip_atomic_load(&p.scount[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    const uint32_t n = (uint32_t)total;
+    const uint32_t need = n == 0 ? 1u : min(gridDim.x, (n + kBlock - 1) / kBlock);
+    if (blockIdx.x >= need) return;   // (block-uniform: every thread has the same n)
     const Ent tab = entry_tables(p, smem);   // (its barrier also publishes pre)
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
-    const uint32_t n = pre[ns];
     unsigned long long best = ~0ull;
-    for (uint32_t k = threadIdx.x; k < n; k += kBlock) {
-        uint32_t j = 0;
-        while (j + 1 < ns && pre[j + 1] <= k) ++j;
-        const uint64_t at = (uint64_t)(s0 + j) * p.seg_cap + (k - pre[j]);
+    for (uint32_t k = blockIdx.x * kBlock + threadIdx.x; k < n; k += gridDim.x * kBlock) {
+        // the last segment j with pre[j] <= k holds survivor k
+        uint32_t lo = 0, hi = nseg;
+        while (hi - lo > 1) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (pre[mid] <= k) lo = mid;
+            else hi = mid;
+        }
+        const uint64_t at = (uint64_t)lo * p.seg_cap + (k - pre[lo]);
         const uint32_t i = p.sidx[at];
         uint32_t w[NW], cut[S + 1], to[S], F[S], B[S];
 #pragma unroll
@@ -1608,7 +1619,7 @@ __global__ __launch_bounds__(kBlock) void surv_kernel(KParams p, uint32_t publis
         const unsigned long long key = make_key(true, T, i);
         best = key < best ? key : best;
     }
-    block_min_and_finish(best, p.acc, p.done, nullptr, p.run_best, true, false, publish ? p.snap : nullptr);
+    block_min_and_finish(best, p.acc, p.done, nullptr, p.run_best, true, false, publish ? p.snap : nullptr, need);
 }
 
 // host-side launchers
@@ -1648,7 +1659,8 @@ hipError_t launch_resume_s(const KParams &p, const LaunchCfg &lc, hipStream_t st
 
 // One piece of an early-stop chunk: filter_kernel on the grid in lc (LDS:
 // Pascal columns, then the stage tables of lc.lds_bytes), then surv_kernel
-// (one block per kSurvSegs survivor segments).
+// on lc.grid2 blocks (LDS: the stage entries, then the scan of the lc.grid
+// segment counts).
 constexpr size_t kLdsBlockMax = 64 * 1024;   // LDS bytes one block of these kernels may use
 
 template <int S, typename R>
@@ -1666,12 +1678,14 @@ hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t s
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const uint32_t nseg = lc.grid;
-    const dim3 g((nseg + kSurvSegs - 1) / kSurvSegs), b(kBlock);
+    const dim3 g(lc.grid2), b(kBlock);
+    const size_t sl = (size_t)p.ent_lds + ((size_t)nseg + 1) * 4;
+    if (sl > kLdsBlockMax || lc.grid2 == 0) return hipErrorInvalidValue;
     const bool sch = p.sched != 0;
-    if (p.has_ar && sch) hipLaunchKernelGGL((surv_kernel<S, true, true>), g, b, lc.lds_bytes, st, p, publish, nseg);
-    else if (p.has_ar) hipLaunchKernelGGL((surv_kernel<S, true, false>), g, b, lc.lds_bytes, st, p, publish, nseg);
-    else if (sch) hipLaunchKernelGGL((surv_kernel<S, false, true>), g, b, lc.lds_bytes, st, p, publish, nseg);
-    else hipLaunchKernelGGL((surv_kernel<S, false, false>), g, b, lc.lds_bytes, st, p, publish, nseg);
+    if (p.has_ar && sch) hipLaunchKernelGGL((surv_kernel<S, true, true>), g, b, sl, st, p, publish, nseg);
+    else if (p.has_ar) hipLaunchKernelGGL((surv_kernel<S, true, false>), g, b, sl, st, p, publish, nseg);
+    else if (sch) hipLaunchKernelGGL((surv_kernel<S, false, true>), g, b, sl, st, p, publish, nseg);
+    else hipLaunchKernelGGL((surv_kernel<S, false, false>), g, b, sl, st, p, publish, nseg);
     return hipGetLastError();
 }
 
