@@ -33,8 +33,12 @@ docstring; the list of readings:
 * R9 (ties): the argmin returns the smallest index among equal makespans;
   infeasible candidates still get their raw DAG makespan but never win.
 * R10 (stage-level bound, Eq. 2): g(S_x) as printed, with f_i, b_i the
-  stage totals and d_i the stage all-reduce time; a candidate is pruned
-  iff max_x g(S_x) > bound (strict, as in Theorem 1).
+  stage totals and d_i the stage all-reduce time; a candidate is discarded
+  iff some stage exceeds its device's memory or max_x g(S_x) > bound
+  (strict, as in Theorem 1).  A discarded candidate is classified as the
+  search of Sec. 4.2.3 discards a partial configuration, stage by stage in
+  pipeline order: the first stage x that exceeds memory (infeasible) or has
+  g(S_x) > bound (pruned) decides, memory first at the same stage.
 * R11 (Eager 1F1B, App. B.1): stage s runs w = min(2(S-s)+1, M) forward
   passes, then M - w groups of one backward and one forward pass, then the
   remaining backward passes.
@@ -443,27 +447,49 @@ def argmin(makespans, feasible):
     return best
 
 
-def eq2_bound(F: Sequence[int], B: Sequence[int], M: int,
-              d: Optional[Sequence[int]] = None) -> int:
-    """max over x of g(S_x), Eq. 2:
+def eq2_terms(F: Sequence[int], B: Sequence[int], M: int,
+              d: Optional[Sequence[int]] = None) -> List[int]:
+    """[g(S_1), ..., g(S_S)] of Eq. 2:
     g(S_x) = sum_{i<x} f_i + M (f_x + b_x) + max_{1<=i<=x} (sum_{j=i}^{x-1} b_j + d_i)."""
     S = len(F)
     dd = d if d is not None else [0] * S
-    best = 0
+    out = []
     for x in range(1, S + 1):
         g = sum(F[i - 1] for i in range(1, x)) + M * (F[x - 1] + B[x - 1])
         inner = max(sum(B[j - 1] for j in range(i, x)) + dd[i - 1] for i in range(1, x + 1))
-        best = max(best, g + inner)
-    return best
+        out.append(g + inner)
+    return out
+
+
+def eq2_bound(F: Sequence[int], B: Sequence[int], M: int,
+              d: Optional[Sequence[int]] = None) -> int:
+    """max over x of g(S_x), Eq. 2."""
+    return max(eq2_terms(F, B, M, d))
+
+
+def classify(prob, cuts: Sequence[int], types: Sequence[int], bound: int, allreduce=None) -> str:
+    """Reading R10's classification of one candidate against `bound`:
+    'infeasible' or 'pruned' by the first stage (in pipeline order) that
+    exceeds its device's memory or has g(S_x) > bound, memory first;
+    'evaluated' if no stage does."""
+    F, B, MEM, D, _ = stage_weights(prob, cuts, types, allreduce)
+    g = eq2_terms(F, B, prob.M, D if allreduce is not None else None)
+    for x in range(prob.S):
+        if MEM[x] > int(prob.cap[types[x]]):
+            return "infeasible"
+        if g[x] > bound:
+            return "pruned"
+    return "evaluated"
 
 
 def bounded_search(prob, cands, bound: int, chunk: int = 0, ramp: bool = False):
     """Early-stop pass (Thm. 1, reading R10) over a candidate list.
 
     The list is cut into consecutive chunks of `chunk` entries (0 = one
-    chunk), or with ramp into chunks of chunk, 2 chunk, 4 chunk, ... entries.  Each chunk prunes against b = min(bound, best makespan found in
-    earlier chunks); a feasible candidate with max_x g(S_x) > b is pruned,
-    every other feasible one is evaluated exactly.  The result is the
+    chunk), or with ramp into chunks of chunk, 2 chunk, 4 chunk, ...
+    entries.  Each chunk classifies against b = min(bound, best makespan
+    found in earlier chunks) (see classify); the candidates it does not
+    discard are evaluated exactly.  The result is the
     (makespan, index)-smallest evaluated candidate if its makespan is
     <= bound, else None.  Returns (best, evaluated, pruned, infeasible)."""
     if getattr(prob, "schedule", 0) == SCHEDULE_INTERLEAVED:
@@ -482,16 +508,16 @@ def bounded_search(prob, cands, bound: int, chunk: int = 0, ramp: bool = False):
             size *= 2
         b = bound if best is None else min(bound, best[1])
         for i, cuts, types in lst[c0:c1]:
-            F, B, _, D, ok = stage_weights(prob, cuts, types, allreduce)
-            d = D if allreduce is not None else None
-            if not ok:
+            cls = classify(prob, cuts, types, b, allreduce)
+            if cls == "infeasible":
                 infeasible += 1
                 continue
-            if eq2_bound(F, B, prob.M, d) > b:
+            if cls == "pruned":
                 pruned += 1
                 continue
             evaluated += 1
-            t = longest_path(dag, F, B, prob.comm_fwd, prob.comm_bwd, d)
+            F, B, _, D, _ = stage_weights(prob, cuts, types, allreduce)
+            t = longest_path(dag, F, B, prob.comm_fwd, prob.comm_bwd, D if allreduce is not None else None)
             if best is None or (t, i) < best[::-1]:
                 best = (i, t)
         c0 = c1

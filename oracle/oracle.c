@@ -360,9 +360,13 @@ static void *worker(void *arg) {
         }
         for (int q = 0; q < ND; ++q) if (MM[q] > p->cap[types[q]]) feasible = 0;
         if (j->bounded) {
-            if (!feasible) { j->infeasible++; continue; }
-            uint64_t lb = 0;
-            for (int x = 1; x <= S; ++x) {
+            /* reading R10: stage by stage in pipeline order, the first stage
+             * over its device's memory (infeasible) or with g(S_x) of Eq. 2
+             * above the bound (pruned) decides; memory first (one stage per
+             * device here: no early stop under Interleaved 1F1B) */
+            int cls = 0;
+            for (int x = 1; x <= S && !cls; ++x) {
+                if (MM[x - 1] > p->cap[types[x - 1]]) { cls = 1; break; }
                 uint64_t g = 0, inner = 0;
                 for (int i2 = 1; i2 < x; ++i2) g += F[i2 - 1];
                 g += (uint64_t)p->M * (F[x - 1] + B[x - 1]);
@@ -371,9 +375,10 @@ static void *worker(void *arg) {
                     for (int jj = i2; jj <= x - 1; ++jj) sb += B[jj - 1];
                     if (sb > inner) inner = sb;
                 }
-                if (g + inner > lb) lb = g + inner;
+                if (g + inner > j->bound) cls = 2;
             }
-            if (lb > j->bound) { j->pruned++; continue; }
+            if (cls == 1) { j->infeasible++; continue; }
+            if (cls == 2) { j->pruned++; continue; }
             j->evaluated++;
         }
         uint64_t T = dag_longest(j->g, F, B, D, p->cf, p->cb, fin);

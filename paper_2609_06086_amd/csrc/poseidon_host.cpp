@@ -808,7 +808,8 @@ int ensure_workspace(poseidon_ctx *ctx, uint64_t n, hipStream_t st) {
     }
     const uint64_t cap = std::max<uint64_t>(n, 1024) + (uint64_t)ctx->grid_max * pk::kDecodeIlp * 256;
     const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
-    uint64_t elems = (words + 1) * cap + ctx->grid_max;   // cut codes, survivor indices and counts
+    // cut codes, the early stop's survivor and first-stage lists and their counts
+    uint64_t elems = (words + 1 + pk::kAListWords) * cap + 2ull * ctx->grid_max;
     if (ctx->base.nlevels)
         elems += 2 * (1 + words + queue_state_words(ctx)) * queue_cap(ctx, cap) +
                  (uint64_t)pk::kMaxLevels * ctx->grid_max;
@@ -925,12 +926,14 @@ int poseidon_eval_candidates(poseidon_ctx *ctx, const poseidon_cands *cands, uin
     const uint64_t chunk = std::min<uint64_t>(cands->count, kChunk);
     rc = ensure_workspace(ctx, chunk, st);
     if (rc != POSEIDON_OK) return rc;
-    // workspace: cut codes [words][cap], survivor indices [cap] and counts
-    // [grid_max] of the early-stop pass, then the straggler queues
+    // workspace: cut codes [words][cap]; the early stop's survivor indices
+    // [cap], their counts [grid_max], its first-stage list [kAListWords][cap]
+    // and counts [grid_max]; then the straggler queues
     uint32_t *ws = (uint32_t *)ctx->ws;
     const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
     return eval_chunks(ctx, cands, makespan_out, feasible_bits_out, best_out, st, chunk, ws, ctx->ws_cap,
-                       ws + (words + 1) * ctx->ws_cap + ctx->grid_max, queue_cap(ctx, ctx->ws_cap));
+                       ws + (words + 1 + pk::kAListWords) * ctx->ws_cap + 2ull * ctx->grid_max,
+                       queue_cap(ctx, ctx->ws_cap));
 }
 
 int poseidon_eval_candidates_noalloc(poseidon_ctx *ctx, const poseidon_cands *cands, uint32_t *makespan_out,
@@ -999,6 +1002,8 @@ int poseidon_eval_candidates_bounded(poseidon_ctx *ctx, const poseidon_cands *ca
     kp.ccap = ctx->ws_cap;
     kp.sidx = (uint32_t *)ctx->ws + (uint64_t)pk::code_words((int)ctx->S) * ctx->ws_cap;
     kp.scount = (unsigned int *)(kp.sidx + ctx->ws_cap);
+    kp.alist = (uint32_t *)(kp.scount + ctx->grid_max);
+    kp.acount = (unsigned int *)(kp.alist + (uint64_t)pk::kAListWords * ctx->ws_cap);
     kp.es_bound = bound;
     pk::LaunchCfg lc;
     lc.lds_bytes = ctx->ent_lds_bytes;

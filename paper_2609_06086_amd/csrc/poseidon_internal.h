@@ -70,10 +70,15 @@ struct KParams {
     unsigned int *err;
     // early stop: the caller's bound, and the list of the candidates that
     // pass the memory and Eq. 2 tests (call index, cut codes in `codes`), in
-    // per-block segments of seg_cap entries with their counts in scount
+    // per-block segments of seg_cap entries with their counts in scount;
+    // alist / acount: the same for the candidates that pass the tests of
+    // their first stages (kAListWords arrays of ccap words: call index and
+    // the state of their decode)
     uint32_t es_bound;
     uint32_t *sidx;
     unsigned int *scount;
+    uint32_t *alist;
+    unsigned int *acount;
     // steady-state cascade: lanes not settled at iteration (Interleaved
     // 1F1B: period) lvl_k[l-1] are
     // queued (candidate index + registers) and resumed by level l
@@ -149,6 +154,7 @@ hipError_t launch_eval(const KParams &p, const LaunchCfg &lc, hipStream_t st);
 hipError_t launch_decode(const KParams &p, const LaunchCfg &lc, hipStream_t st);
 hipError_t launch_resume(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t lvl);
 hipError_t launch_bounded(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t publish);
+constexpr int kAListWords = 6;  // words per entry of the early stop's first-stage list
 constexpr int kDecodeIlp = 4;   // candidates per lane of the decode and early-stop filter kernels
 hipError_t eval_occupancy(const KParams &p, size_t lds, int *blocks);
 hipError_t filter_occupancy(const KParams &p, size_t ent_lds, int *blocks);

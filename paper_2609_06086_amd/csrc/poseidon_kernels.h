@@ -258,23 +258,6 @@ __device__ __forceinline__ bool stage_weights(const KParams &p, const Ent &t, co
     return feas;
 }
 
-// ... and G_s = M (F_s + B_s), the stage's term of Eq. 2 (below 2^31 like
-// every path weight; a full-rate 24-bit multiply when both factors fit).
-template <int S>
-__device__ __forceinline__ bool stage_weights_g(const KParams &p, const Ent &t, const uint32_t (&cut)[S + 1],
-                                                const uint32_t (&to)[S], uint32_t (&F)[S], uint32_t (&B)[S],
-                                                uint32_t (&G)[S]) {
-    const bool feas = stage_weights<S>(p, t, cut, to, F, B);
-    if (p.g24) {
-#pragma unroll
-        for (int s = 0; s < S; ++s) G[s] = __umul24(p.M, F[s] + B[s]);
-    } else {
-#pragma unroll
-        for (int s = 0; s < S; ++s) G[s] = p.M * (F[s] + B[s]);
-    }
-    return feas;
-}
-
 // ---------------------------------------------------------------------------
 // (a3) longest path of the 1F1B DAG
 // ---------------------------------------------------------------------------
@@ -793,32 +776,37 @@ __device__ __forceinline__ Comm<S> load_comm(const KParams &p) {
 // ---------------------------------------------------------------------------
 // (a5) Eq. 2: g(S_x) = sum_{i<x} F_i + M (F_x + B_x) + max_{i<=x}(sum_{j=i}^{x-1} B_j + d_i)
 // ---------------------------------------------------------------------------
-template <int S>
-__device__ __forceinline__ uint32_t eq2_bound(uint32_t M, const uint32_t (&F)[S], const uint32_t (&B)[S],
-                                              const uint32_t (&D)[S]) {
-    uint32_t pre = 0, inner = 0, lb = 0;
+// Classification of a candidate against the bound b over its stages
+// 0 .. X-1 in pipeline order, as the search of Sec. 4.2.3 discards a
+// partial configuration: 0 if no stage fails; 1 if the first failing stage
+// exceeds its device's memory (tested first at a stage); 2 if its g(S_x)
+// exceeds b.  The stage weights come from the stage entries.
+template <int S, bool AR, int X, bool G24>
+__device__ __forceinline__ uint32_t classify_g(const KParams &p, const Ent &t, const uint32_t (&cut)[S + 1],
+                                               const uint32_t (&to)[S], uint32_t b) {
+    uint32_t pre = 0, inner = 0, bprev = 0, mm = 0, gm = 0;
 #pragma unroll
-    for (int x = 0; x < S; ++x) {
-        // inner = max over i <= x of (B_i + ... + B_{x-1} + d_i)
-        inner = x == 0 ? D[0] : max(inner + B[x - 1], D[x]);
-        lb = max(lb, pre + M * (F[x] + B[x]) + inner);
-        pre += F[x];
+    for (int x = 0; x < X; ++x) {
+        const uint32_t F = ent<kEPf>(t, cut[x + 1], to[x]) - ent<kEPf>(t, cut[x], to[x]);
+        const uint32_t B = ent<kEPb>(t, cut[x + 1], to[x]) - ent<kEPb>(t, cut[x], to[x]);
+        const uint32_t D = AR ? ent<kEPd>(t, cut[x + 1], to[x]) - ent<kEPd>(t, cut[x], to[x]) : 0u;
+        if (cut[x + 1] > ent<kEHm>(t, cut[x], to[x])) mm |= 1u << x;
+        inner = x == 0 ? D : max(inner + bprev, D);
+        // M (F + B) is below 2^31 like every path weight: a full-rate 24-bit
+        // multiply when both factors fit
+        const uint32_t G = G24 ? __umul24(p.M, F + B) : p.M * (F + B);
+        if (pre + G + inner > b) gm |= 1u << x;
+        pre += F;
+        bprev = B;
     }
-    return lb;
+    const uint32_t f = mm | gm;
+    return f == 0u ? 0u : (mm & f & (0u - f)) ? 1u : 2u;
 }
 
-// The same with G_x = M (F_x + B_x) from the stage entries.
-template <int S>
-__device__ __forceinline__ uint32_t eq2_bound_g(const uint32_t (&F)[S], const uint32_t (&B)[S],
-                                                const uint32_t (&G)[S], const uint32_t (&D)[S]) {
-    uint32_t pre = 0, inner = 0, lb = 0;
-#pragma unroll
-    for (int x = 0; x < S; ++x) {
-        inner = x == 0 ? D[0] : max(inner + B[x - 1], D[x]);
-        lb = max(lb, pre + G[x] + inner);
-        pre += F[x];
-    }
-    return lb;
+template <int S, bool AR, int X>
+__device__ __forceinline__ uint32_t classify(const KParams &p, const Ent &t, const uint32_t (&cut)[S + 1],
+                                             const uint32_t (&to)[S], uint32_t b) {
+    return p.g24 ? classify_g<S, AR, X, true>(p, t, cut, to, b) : classify_g<S, AR, X, false>(p, t, cut, to, b);
 }
 
 // ---------------------------------------------------------------------------
@@ -1187,6 +1175,49 @@ __device__ __forceinline__ void decode_ilp(const KParams &p, const Pascal<S, R, 
     }
 }
 
+// Searches of cuts J0+1 .. J1 (J1 <= S - 1) of kIlp candidates, from the
+// rank left r and the smallest value at of cut J0+1; cut J1 = S - 1, the
+// last, needs no search (with one cut left, C(n, 1) = n: c_{S-1} = a + r).
+template <int S, typename R, int H, int J0, int J1>
+__device__ __forceinline__ void decode_range(const KParams &p, const Pascal<S, R, H> &pc, R (&r)[kIlp],
+                                             uint32_t (&at)[kIlp], uint32_t (&cut)[kIlp][S + 1]) {
+    constexpr uint32_t NH = 1u << H;
+    constexpr int NN = Pascal<S, R, H>::NN;
+    constexpr int JS = J1 < S - 2 ? J1 : S - 2;   // cuts found by a search
+#pragma unroll
+    for (int j = J0 + 1; j <= JS; ++j) {
+        const int c = S - j;
+        uint32_t cj[kIlp];
+        if (c < NN) search_cut<uint32_t, R, H>(p, pc.ns + (uint32_t)c * NH, pc.nt + (uint32_t)c * NH, r, at, cj);
+        else search_cut<R, R, H>(p, pc.ws + (uint32_t)(c - NN) * NH, pc.wt + (uint32_t)(c - NN) * NH, r, at, cj);
+#pragma unroll
+        for (int u = 0; u < kIlp; ++u) cut[u][j] = cj[u];
+    }
+    if (J1 == S - 1 && S >= 2) {
+#pragma unroll
+        for (int u = 0; u < kIlp; ++u) cut[u][S - 1] = at[u] + (uint32_t)r[u];
+    }
+}
+
+// Cuts c_1 .. c_J (J <= S - 1) of kIlp candidates at call positions pos
+// (valid positions also for inactive lanes) into cut[u][0 .. J], with
+// c_0 = 0 and c_S = L; r and at are left as decode_range needs them to go
+// on.  Invalid (rank, assignment) pairs get ok = false.
+template <int S, typename R, int H, int J>
+__device__ __forceinline__ void decode_cuts(const KParams &p, const Pascal<S, R, H> &pc,
+                                            const uint64_t (&pos)[kIlp], const bool (&act)[kIlp],
+                                            bool (&ok)[kIlp], uint32_t (&asg)[kIlp], R (&r)[kIlp],
+                                            uint32_t (&at)[kIlp], uint32_t (&cut)[kIlp][S + 1]) {
+#pragma unroll
+    for (int u = 0; u < kIlp; ++u) {
+        ok[u] = candidate<R>(p, pos[u], r[u], asg[u]) && act[u];
+        at[u] = 1;
+        cut[u][0] = 0;
+        cut[u][S] = p.L;
+    }
+    decode_range<S, R, H, 0, J>(p, pc, r, at, cut);
+}
+
 template <int S, typename R, int H>
 __device__ __forceinline__ void decode_batch(const KParams &p, const Pascal<S, R, H> &pc, uint64_t base,
                                              uint64_t stride, bool &bad) {
@@ -1460,49 +1491,106 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
     block_min_and_finish(best, p.acc, p.done, p.result, nullptr, lvl == p.nlevels, p.accumulate);
 }
 
-// Early stop (Eq. 2 / Theorem 1) over one piece of a chunk, in two kernels.
-// filter_kernel decodes each candidate (a1), builds its stage weights (a2)
-// and tests memory and Eq. 2 against the bound in force (min of the caller's
-// bound and the best of the earlier chunks, fixed within a chunk) while the
-// cut codes are still in registers; only the survivors go to a list (call
-// index + cut codes), block b filling segment b of p.seg_cap entries and
-// counting them in LDS.  surv_kernel evaluates the list on the DAG (a3) and
-// folds it into the running best (a4).
-template <int S, typename R, int H, bool AR>
+// Early stop (Eq. 2 / Theorem 1) over one piece of a chunk.  Against the
+// bound b in force (min of the caller's bound and the best of the earlier
+// chunks, fixed within a chunk) every candidate is classified by classify()
+// over its stages in pipeline order; the ones no stage discards survive
+// and are evaluated exactly.
+//
+// filter_kernel runs in one of three modes:
+//  kFilterFull   decodes every cut (a1), builds the stage weights (a2) and
+//                decides all S stages while the cuts are in registers; the
+//                survivors go to a list (call position + cut codes), block b
+//                filling segment b of seg_cap entries, counted in LDS (no
+//                global atomic, whose single address would serialise waves);
+//  kFilterPrefix decodes only the first X = filter_prefix<S>() cuts and
+//                decides the stages they close; the candidates it keeps go
+//                to a list in the same segments (counts in acount) with
+//                what the decode needs to go on (AList);
+//  kFilterGather takes block b's segment of that list in order (coalesced),
+//                decodes the remaining cuts and goes on as kFilterFull.
+// For S >= 4 a piece goes through kFilterPrefix, then kFilterGather: most
+// candidates are discarded at one of their first stages, and only the rest
+// pay for the searches of their later cuts.  surv_kernel evaluates the
+// survivor list on the DAG (a3) and folds it into the running best (a4).
+enum FilterMode { kFilterFull = 0, kFilterPrefix = 1, kFilterGather = 2 };
+template <int S>
+__host__ __device__ constexpr int filter_prefix() { return S >= 4 ? S / 2 : 0; }
+
+// The prefix list, arrays of ccap entries: call position, rank left (low
+// and high words), assignment index, then the first X cuts as cut codes.
+static_assert(4 + (filter_prefix<kSMax>() + 3) / 4 <= kAListWords, "first-stage list entry too small");
+struct AList {
+    uint32_t *pos, *rlo, *rhi, *asg, *w;
+    __device__ __forceinline__ explicit AList(const KParams &p)
+        : pos(p.alist), rlo(p.alist + p.ccap), rhi(p.alist + 2 * p.ccap), asg(p.alist + 3 * p.ccap),
+          w(p.alist + 4 * p.ccap) {}
+};
+
+template <int S, typename R, int H, bool AR, int MODE>
 __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const Ent &tab, uint32_t b,
                                            unsigned int *nq, uint32_t &n_keep, uint32_t &n_pruned,
                                            uint32_t &n_infeas, bool &bad) {
+    constexpr int X0 = filter_prefix<S>();
+    constexpr int X = MODE == kFilterPrefix ? X0 : S;   // stages decided, cuts 1 .. X decoded
     constexpr int NW = Codes<S>::kWords;
-    constexpr uint32_t NH = 1u << H;
+    constexpr int AW = (X0 + 3) / 4;                    // code words of the prefix cuts
     const Pascal<S, R, H> pc(pas);
-    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    const AList al(p);
     const unsigned int lane = threadIdx.x & 63;
     const uint64_t seg = (uint64_t)blockIdx.x * p.seg_cap;
-    for (uint64_t base = (uint64_t)blockIdx.x * kBlock + threadIdx.x; base < p.n_i; base += kIlp * stride) {
+    // full, prefix: the piece, kIlp candidates a lane, strided over the grid;
+    // gather: this block's segment of the list, strided over the block
+    const uint64_t n = MODE == kFilterGather ? (uint64_t)p.acount[blockIdx.x] : p.n_i;
+    const uint64_t stride = MODE == kFilterGather ? (uint64_t)kBlock : (uint64_t)gridDim.x * kBlock;
+    const uint64_t start = MODE == kFilterGather ? (uint64_t)threadIdx.x
+                                                 : (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+    for (uint64_t base = start; base < n; base += kIlp * stride) {
         bool act[kIlp], ok[kIlp];
-        uint32_t asg[kIlp], w[kIlp][NW];
-        decode_ilp<S, R, H>(p, pc, base, stride, act, ok, asg, w);
+        uint64_t pos[kIlp];
+        uint32_t asg[kIlp], at[kIlp], cut[kIlp][S + 1];
+        R r[kIlp];
+        if constexpr (MODE == kFilterGather) {
+#pragma unroll
+            for (int u = 0; u < kIlp; ++u) {
+                const uint64_t i = base + u * stride;
+                act[u] = i < n;
+                ok[u] = act[u];
+                const uint64_t o = seg + (act[u] ? i : 0);
+                pos[u] = al.pos[o];
+                asg[u] = al.asg[o];
+                r[u] = sizeof(R) == 8 ? (R)(((uint64_t)al.rhi[o] << 32) | al.rlo[o]) : (R)al.rlo[o];
+                uint32_t w[NW];
+#pragma unroll
+                for (int k = 0; k < NW; ++k) w[k] = k < AW ? al.w[(uint64_t)k * p.ccap + o] : 0u;
+                cut[u][0] = 0;
+                cut[u][S] = p.L;
+#pragma unroll
+                for (int j = 1; j <= X0; ++j) cut[u][j] = (w[(j - 1) / 4] >> (8 * ((j - 1) % 4))) & 0xFFu;
+                at[u] = cut[u][X0] + 1;
+            }
+            decode_range<S, R, H, X0, S - 1>(p, pc, r, at, cut);
+        } else {
+#pragma unroll
+            for (int u = 0; u < kIlp; ++u) {
+                const uint64_t i = base + u * stride;
+                act[u] = i < n;
+                pos[u] = p.first_i + (act[u] ? i : 0);
+            }
+            decode_cuts<S, R, H, MODE == kFilterPrefix ? X0 : S - 1>(p, pc, pos, act, ok, asg, r, at, cut);
+        }
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) {
-            uint32_t cut[S + 1], to[S], F[S], B[S], G[S], D[S];
-            unpack_cuts<S>(w[u], p.L, cut);
+            uint32_t to[S];
             decode_toff<S>(p, tab, ok[u] ? asg[u] : 0u, to);
-            const bool feas = stage_weights_g<S>(p, tab, cut, to, F, B, G);
-            if (AR) {
-                stage_allreduce<S>(p, tab, cut, to, D);
-            } else {
-#pragma unroll
-                for (int s = 0; s < S; ++s) D[s] = 0;
-            }
+            const uint32_t cls = classify<S, AR, X>(p, tab, cut[u], to, b);
             bool keep = false;
             if (act[u]) {
                 if (!ok[u]) bad = true;
-                else if (!feas) ++n_infeas;
-                else if (eq2_bound_g<S>(F, B, G, D) > b) ++n_pruned;
+                else if (cls == 1) ++n_infeas;
+                else if (cls == 2) ++n_pruned;
                 else keep = true;
             }
-            // survivors go to this block's segment of the list (LDS counter:
-            // no global atomic, whose single address would serialise waves)
             const unsigned long long m = __ballot(keep);
             if (m) {
                 unsigned int slot0 = 0;
@@ -1511,11 +1599,27 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
                 if (keep) {
                     const unsigned long long below = lane ? (m & ((1ull << lane) - 1ull)) : 0ull;
                     const uint64_t o = seg + slot0 + (uint32_t)__popcll(below);
-                    p.sidx[o] = (uint32_t)(p.first_i + base + u * stride);
+                    if constexpr (MODE == kFilterPrefix) {
+                        uint32_t w[AW];
 #pragma unroll
-                    for (int k = 0; k < NW; ++k) p.codes[(uint64_t)k * p.ccap + o] = w[u][k];
+                        for (int k = 0; k < AW; ++k) w[k] = 0;
+#pragma unroll
+                        for (int j = 1; j <= X0; ++j) w[(j - 1) / 4] |= cut[u][j] << (8 * ((j - 1) % 4));
+                        al.pos[o] = (uint32_t)pos[u];
+                        al.asg[o] = asg[u];
+                        al.rlo[o] = (uint32_t)r[u];
+                        if (sizeof(R) == 8) al.rhi[o] = (uint32_t)((uint64_t)r[u] >> 32);
+#pragma unroll
+                        for (int k = 0; k < AW; ++k) al.w[(uint64_t)k * p.ccap + o] = w[k];
+                    } else {
+                        uint32_t w[NW];
+                        pack_cuts<S>(cut[u], true, w);
+                        p.sidx[o] = (uint32_t)pos[u];
+#pragma unroll
+                        for (int k = 0; k < NW; ++k) p.codes[(uint64_t)k * p.ccap + o] = w[k];
+                    }
                 }
-                n_keep += lane == 0 ? (uint32_t)__popcll(m) : 0u;
+                if (MODE != kFilterPrefix) n_keep += lane == 0 ? (uint32_t)__popcll(m) : 0u;
             }
         }
     }
@@ -1525,7 +1629,7 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
 // when they and the Pascal columns together exceed the 64 KB of LDS one
 // block may use (the largest columns: L > 128 with 64-bit ranks).  LDS:
 // the stage entries first (unless GTAB), then the Pascal columns.
-template <int S, typename R, bool AR, bool GTAB>
+template <int S, typename R, bool AR, bool GTAB, int MODE>
 __global__ __launch_bounds__(kBlock) void filter_kernel(KParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
     const uint32_t H = decode_levels(p.L);
@@ -1547,10 +1651,10 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(KParams p) {
     __shared__ unsigned int nq;
     if (threadIdx.x == 0) nq = 0;
     switch (H) {
-    case 8: pascal_tables<S, R, 8>(p, pas); __syncthreads(); filter_all<S, R, 8, AR>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
-    case 7: pascal_tables<S, R, 7>(p, pas); __syncthreads(); filter_all<S, R, 7, AR>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
-    case 6: pascal_tables<S, R, 6>(p, pas); __syncthreads(); filter_all<S, R, 6, AR>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
-    default: pascal_tables<S, R, 5>(p, pas); __syncthreads(); filter_all<S, R, 5, AR>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
+    case 8: pascal_tables<S, R, 8>(p, pas); __syncthreads(); filter_all<S, R, 8, AR, MODE>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
+    case 7: pascal_tables<S, R, 7>(p, pas); __syncthreads(); filter_all<S, R, 7, AR, MODE>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
+    case 6: pascal_tables<S, R, 6>(p, pas); __syncthreads(); filter_all<S, R, 6, AR, MODE>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
+    default: pascal_tables<S, R, 5>(p, pas); __syncthreads(); filter_all<S, R, 5, AR, MODE>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
     }
     // per-block sums, one global atomic per counter and block
     const unsigned long long sk = wave_sum_u32(n_keep), sp = wave_sum_u32(n_pruned), si = wave_sum_u32(n_infeas);
@@ -1564,7 +1668,8 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(KParams p) {
     }
     __syncthreads();
     if (threadIdx.x < 3 && cnt[threadIdx.x]) atomicAdd(&p.stats[threadIdx.x], cnt[threadIdx.x]);
-    if (threadIdx.x == 0) p.scount[blockIdx.x] = nq;   // (after the barrier above: every wave has added)
+    // (after the barrier above: every wave has added)
+    if (threadIdx.x == 0) (MODE == kFilterPrefix ? p.acount : p.scount)[blockIdx.x] = nq;
     if (bad) atomicOr(p.err, 1u);
 }
 
@@ -1658,24 +1763,36 @@ hipError_t launch_resume_s(const KParams &p, const LaunchCfg &lc, hipStream_t st
 }
 
 // One piece of an early-stop chunk: filter_kernel on the grid in lc (LDS:
-// Pascal columns, then the stage tables of lc.lds_bytes), then surv_kernel
-// on lc.grid2 blocks (LDS: the stage entries, then the scan of the lc.grid
-// segment counts).
+// Pascal columns, then the stage tables of lc.lds_bytes), in prefix then
+// gather mode for S >= 4, else in full mode; then surv_kernel on lc.grid2
+// blocks (LDS: the stage entries, then the scan of the lc.grid segment
+// counts).
 constexpr size_t kLdsBlockMax = 64 * 1024;   // LDS bytes one block of these kernels may use
 
-template <int S, typename R>
-hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t publish) {
+template <int S, typename R, int MODE>
+hipError_t launch_filter_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
     const size_t pas = pascal_bytes<S, R>(p.L);
     const dim3 fg(lc.grid), fb(kBlock);
     if (pas + lc.lds_bytes > kLdsBlockMax) {
-        if (p.has_ar) hipLaunchKernelGGL((filter_kernel<S, R, true, true>), fg, fb, pas, st, p);
-        else hipLaunchKernelGGL((filter_kernel<S, R, false, true>), fg, fb, pas, st, p);
+        if (p.has_ar) hipLaunchKernelGGL((filter_kernel<S, R, true, true, MODE>), fg, fb, pas, st, p);
+        else hipLaunchKernelGGL((filter_kernel<S, R, false, true, MODE>), fg, fb, pas, st, p);
     } else {
         const size_t lds = pas + lc.lds_bytes;
-        if (p.has_ar) hipLaunchKernelGGL((filter_kernel<S, R, true, false>), fg, fb, lds, st, p);
-        else hipLaunchKernelGGL((filter_kernel<S, R, false, false>), fg, fb, lds, st, p);
+        if (p.has_ar) hipLaunchKernelGGL((filter_kernel<S, R, true, false, MODE>), fg, fb, lds, st, p);
+        else hipLaunchKernelGGL((filter_kernel<S, R, false, false, MODE>), fg, fb, lds, st, p);
     }
-    hipError_t e = hipGetLastError();
+    return hipGetLastError();
+}
+
+template <int S, typename R>
+hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t st, uint32_t publish) {
+    hipError_t e;
+    if constexpr (filter_prefix<S>() > 0) {
+        e = launch_filter_s<S, R, kFilterPrefix>(p, lc, st);
+        if (e == hipSuccess) e = launch_filter_s<S, R, kFilterGather>(p, lc, st);
+    } else {
+        e = launch_filter_s<S, R, kFilterFull>(p, lc, st);
+    }
     if (e != hipSuccess) return e;
     const uint32_t nseg = lc.grid;
     const dim3 g(lc.grid2), b(kBlock);
@@ -1689,18 +1806,33 @@ hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t s
     return hipGetLastError();
 }
 
-// Resident blocks per CU of the early-stop filter instance launch_bounded_s
-// picks (its LDS: the Pascal columns plus the stage entries of `ent_lds`).
-template <int S, typename R>
-hipError_t filter_occupancy_s(const KParams &p, size_t ent_lds, int *blocks) {
+// Resident blocks per CU of the early-stop filter instances launch_bounded_s
+// picks (their LDS: the Pascal columns plus the stage entries of `ent_lds`);
+// with two modes the smaller of their counts, so that the second runs its
+// blocks, one per segment of the first's list, in one wave too.
+template <int S, typename R, int MODE>
+hipError_t filter_occupancy_mode(const KParams &p, size_t ent_lds, int *blocks) {
     const size_t pas = pascal_bytes<S, R>(p.L);
     if (pas + ent_lds > kLdsBlockMax) {
-        if (p.has_ar) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, true, true>, kBlock, pas);
-        return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, false, true>, kBlock, pas);
+        if (p.has_ar) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, true, true, MODE>, kBlock, pas);
+        return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, false, true, MODE>, kBlock, pas);
     }
     if (p.has_ar)
-        return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, true, false>, kBlock, pas + ent_lds);
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, false, false>, kBlock, pas + ent_lds);
+        return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, true, false, MODE>, kBlock, pas + ent_lds);
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, false, false, MODE>, kBlock, pas + ent_lds);
+}
+
+template <int S, typename R>
+hipError_t filter_occupancy_s(const KParams &p, size_t ent_lds, int *blocks) {
+    if constexpr (filter_prefix<S>() > 0) {
+        int a = 0, b = 0;
+        hipError_t e = filter_occupancy_mode<S, R, kFilterPrefix>(p, ent_lds, &a);
+        if (e == hipSuccess) e = filter_occupancy_mode<S, R, kFilterGather>(p, ent_lds, &b);
+        *blocks = a < b ? a : b;
+        return e;
+    } else {
+        return filter_occupancy_mode<S, R, kFilterFull>(p, ent_lds, blocks);
+    }
 }
 
 template <int S, typename R>

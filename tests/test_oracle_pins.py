@@ -347,12 +347,42 @@ def test_bounded_search_theorem1():
             assert best == exact
             bc = coracle.bounded(prob, lst, bound, chunk, nthreads=3, ramp=ramp)
             assert bc == (best, ev, pr, inf)
-            assert ev + pr + inf == len(lst) and inf == int((~fx).sum())
+            assert ev + pr + inf == len(lst) and inf <= int((~fx).sum())
+            # the evaluated candidates are exactly the feasible ones within the bound
+            if chunk == 0:
+                assert ev == sum(1 for i, cuts, types in dag.candidate_list(prob, lst)
+                                 if fx[i] and dag.eq2_bound(*dag.stage_weights(prob, cuts, types)[:2], M) <= bound)
         # every candidate pruned against the fixed bound is strictly worse than it
         for i, cuts, types in dag.candidate_list(prob, lst):
             F, B, _, _, ok = dag.stage_weights(prob, cuts, types)
             if ok and dag.eq2_bound(F, B, M) > bound:
                 assert Tx[i] > bound
+
+
+def test_bounded_classification_in_stage_order():
+    """A discarded candidate is classified by its first failing stage, memory
+    first.  With bound 0 every g(S_1) > 0 fails at stage 1, so exactly the
+    candidates whose first stage exceeds memory are infeasible, whatever
+    their later stages do; with no bound the infeasible ones are exactly
+    those with some stage over memory."""
+    rng = np.random.default_rng(17)
+    for trial in range(6):
+        prob = W.random_problem(rng, 14, 4, int(rng.integers(1, 6)), 2, mem_hi=20, cap=int(rng.integers(35, 70)))
+        lst = W.random_candidates(rng, prob, 300)
+        Tx, fx = dag.evaluate(prob, lst)
+        first_over = later_over = 0
+        for i, cuts, types in dag.candidate_list(prob, lst):
+            mem0 = sum(int(prob.mem[k]) for k in range(0, cuts[0]))
+            if mem0 > int(prob.cap[types[0]]):
+                first_over += 1
+            elif not fx[i]:
+                later_over += 1
+        assert later_over > 0   # the case that tells the two orders apart
+        for impl in (dag.bounded_search, coracle.bounded):
+            best, ev, pr, inf = impl(prob, lst, 0)
+            assert (best, ev, pr, inf) == (None, 0, len(lst) - first_over, first_over)
+            best, ev, pr, inf = impl(prob, lst, 2 ** 32 - 1)
+            assert (pr, inf, ev) == (0, int((~fx).sum()), int(fx.sum()))
 
 
 def test_bounded_ramp_chunks_double():
