@@ -239,7 +239,7 @@ __device__ __forceinline__ bool stage_weights(const KParams &p, const Lds &t,
         F[s] = (uint32_t)hi - (uint32_t)lo;
         B[s] = (uint32_t)(hi >> 32) - (uint32_t)(lo >> 32);
         const uint32_t mem = t.pm[cut[s + 1]] - t.pm[cut[s]];
-        feas = feas && (mem <= t.cap[ty[s]]);
+        feas &= mem <= t.cap[ty[s]];   // (no short circuit: no branch per stage)
     }
     return feas;
 }
@@ -253,7 +253,7 @@ __device__ __forceinline__ bool stage_weights(const KParams &p, const Ent &t, co
     for (int s = 0; s < S; ++s) {
         F[s] = ent<kEPf>(t, cut[s + 1], to[s]) - ent<kEPf>(t, cut[s], to[s]);
         B[s] = ent<kEPb>(t, cut[s + 1], to[s]) - ent<kEPb>(t, cut[s], to[s]);
-        feas = feas && (cut[s + 1] <= ent<kEHm>(t, cut[s], to[s]));
+        feas &= cut[s + 1] <= ent<kEHm>(t, cut[s], to[s]);   // (no short circuit: no branch per stage)
     }
     return feas;
 }
@@ -341,10 +341,13 @@ __device__ __forceinline__ void steady_slot(int parity, uint32_t (&Y)[S], const 
     for (int s = 0; s < S; ++s) Y[s] = N[s];
 }
 
-// k * x for a small compile-time k; the full-rate 24-bit multiply when the
-// problem's stage weights fit 24 bits (u24)
-__device__ __forceinline__ uint32_t mul_small(uint32_t x, uint32_t k, bool u24) {
-    return u24 ? __umul24(x, k) : x * k;
+// k * x for a small k; U24: the full-rate 24-bit multiply (the problem's
+// stage weights fit 24 bits).  The callers take U24 as a template argument
+// and branch once on it, so that no select merges the two products into one
+// slow 32-bit multiply.
+template <bool U24>
+__device__ __forceinline__ uint32_t mul_small(uint32_t x, uint32_t k) {
+    return U24 ? __umul24(x, k) : x * k;
 }
 
 // Prologue (slots 0 .. 2S-2) with its warm-up forwards in closed form.
@@ -357,16 +360,16 @@ __device__ __forceinline__ uint32_t mul_small(uint32_t x, uint32_t k, bool u24) 
 // heaviest of them,
 //     Y[s] = phi_0 + (F_0 + ... + F_s) + (m - 1) max(F_0, ..., F_s),  m = S - s.
 // Slots S .. 2S-2 (the first backwards and the forwards between them) run
-// on the stencil.  u24: every stage weight is below 2^24.
-template <int S>
-__device__ __forceinline__ void dp_prologue(uint32_t (&Y)[S], const uint32_t (&F)[S], const uint32_t (&B)[S],
-                                            const Comm<S> &c, bool u24) {
+// on the stencil.  U24: every stage weight is below 2^24.
+template <int S, bool U24>
+__device__ __forceinline__ void dp_prologue_t(uint32_t (&Y)[S], const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                              const Comm<S> &c) {
     uint32_t pre = c.phi0, mx = 0;
 #pragma unroll
     for (int s = 0; s < S; ++s) {
         pre += F[s];
         mx = max(mx, F[s]);
-        Y[s] = pre + mul_small(mx, S - 1 - s, u24);
+        Y[s] = pre + mul_small<U24>(mx, S - 1 - s);
     }
 #pragma unroll
     for (int k = S; k < 2 * S - 1; ++k) {
@@ -376,6 +379,13 @@ __device__ __forceinline__ void dp_prologue(uint32_t (&Y)[S], const uint32_t (&F
 #pragma unroll
         for (int s = 0; s < S; ++s) Y[s] = N[s];
     }
+}
+
+template <int S>
+__device__ __forceinline__ void dp_prologue(uint32_t (&Y)[S], const uint32_t (&F)[S], const uint32_t (&B)[S],
+                                            const Comm<S> &c, bool u24) {
+    if (u24) dp_prologue_t<S, true>(Y, F, B, c);
+    else dp_prologue_t<S, false>(Y, F, B, c);
 }
 
 // one steady iteration: an odd slot then an even slot (slots 2S-1+2i, 2S+2i)
@@ -421,7 +431,7 @@ __device__ __forceinline__ void dp_finish(uint32_t (&Y)[S], const uint32_t (&F)[
 //   max(Yf[s], Yb[s+1] + cf_s + cb_s) - phi_s, and p.ek[s] holds
 //   cb_0 + .. + cb_{s-1} - phi_s (modulo 2^32: every sum that reaches T is a
 // path length below 2^31).
-template <int S>
+template <int S, bool U24>
 __device__ __forceinline__ uint32_t dp_finish_t(const KParams &p, uint32_t (&Y)[S], const uint32_t (&F)[S],
                                                 const uint32_t (&B)[S], const Comm<S> &c) {
     uint32_t Yf[S], Yb[S];
@@ -460,7 +470,7 @@ __device__ __forceinline__ uint32_t dp_finish_t(const KParams &p, uint32_t (&Y)[
         pb += B[s];
         mxb = max(mxb, B[s]);
         const uint32_t a = s + 1 < S ? max(Yf[s], Yb[s + 1 < S ? s + 1 : 0] + c.e[s + 1 < S ? s : 0]) : Yf[s];
-        T = max(T, a + pb + mul_small(mxb, S - 1 - s, p.g24 != 0) + p.ek[s]);
+        T = max(T, a + pb + mul_small<U24>(mxb, S - 1 - s) + p.ek[s]);
     }
     return T;
 }
@@ -870,7 +880,8 @@ __device__ __forceinline__ uint32_t dp_end(const KParams &p, const TAB &t, uint3
         dp_finish<S>(Y, F, B, c);
         return end_time<S, true>(p, t, Y, c, w, a);
     } else {
-        return dp_finish_t<S>(p, Y, F, B, c);
+        if (p.g24) return dp_finish_t<S, true>(p, Y, F, B, c);
+        return dp_finish_t<S, false>(p, Y, F, B, c);
     }
 }
 
