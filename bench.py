@@ -11,11 +11,15 @@ before timing starts.
 Default run: the headline line is the 16-stage workload (L=126 layers, S=16
 stages, M=128 micro-batches, T=4 device types, 2^24 sampled compositions),
 with the early-stop pass over the same list.  The same line carries
-sub-records for the two other large workloads: the exhaustive 8-stage
-2-type range (C(47,7) = 62,891,499 compositions) and the 8-stage 3-type
-list of 2^26 sampled (composition, assignment) pairs, the latter also as an
-early-stop pass with the same-argmin check.  Every record has the CPU oracle
-timed beside it on a bounded sample.  Prints one JSON line.
+sub-records for the other workloads: the two small exhaustive ranges (8
+layers on 2 stages, 28 candidates; 32 layers on 4 stages, 71,920
+candidates), the exhaustive 8-stage 2-type range (C(47,7) = 62,891,499
+compositions) and the 8-stage 3-type list of 2^26 sampled (composition,
+assignment) pairs, the latter also as an early-stop pass with the
+same-argmin check.  Every record has the CPU oracle timed beside it on a
+bounded sample, and `oracle_check` compares the timed pass's makespans and
+mask bits with the oracle's on that sample (and the argmin, when the sample
+is the whole list).  Prints one JSON line.
 
 Roofline fields: the path is 32-bit integer add/max on the vector ALUs.
 `roofline.achieved` is the INT32 lane-operations one call executes, counted
@@ -131,7 +135,8 @@ def timed(torch, step, steps, warmup, stream):
 
 def cpu_baseline(wl, target_s):
     """The C oracle as it stands on all host threads, on a prefix of the same
-    candidates sized for about target_s seconds."""
+    candidates sized for about target_s seconds.  Returns the record and the
+    oracle's makespans and feasibility of that prefix."""
     from oracle import coracle
     coracle.lib()
     threads = coracle.default_threads()
@@ -142,13 +147,32 @@ def cpu_baseline(wl, target_s):
     dt = time.perf_counter() - t0
     m = int(min(n, max(probe, probe * target_s / max(dt, 1e-6))))
     t0 = time.perf_counter()
-    coracle.evaluate(wl.problem, wl.cands, nthreads=threads, lo=0, hi=m)
+    T, feas = coracle.evaluate(wl.problem, wl.cands, nthreads=threads, lo=0, hi=m)
     dt = time.perf_counter() - t0
     S, M = wl.problem.S, wl.problem.M
     return {"value": m / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
             "dag_nodes_per_s": m * 2 * S * M / dt,
             "sample": f"first {m} of the {n} candidates of the same workload, C oracle (explicit DAG, "
-                      f"Kahn order, topological DP) on {threads} host threads, {dt:.1f} s"}
+                      f"Kahn order, topological DP) on {threads} host threads, {dt:.1f} s"}, T, feas
+
+
+def oracle_check(e, best, T_o, f_o):
+    """The timed pass's outputs against the oracle's on its prefix: every
+    makespan and mask bit, and (when the prefix is the whole list) the argmin."""
+    import numpy as np
+    from oracle import coracle
+    m = len(T_o)
+    Tg = e.T[:m].cpu().numpy().view(np.uint32)
+    words = e.bits[:(m + 31) // 32].cpu().numpy().view(np.uint32)
+    i = np.arange(m)
+    fg = ((words[i >> 5] >> (i & 31).astype(np.uint32)) & 1).astype(bool)
+    rec = {"compared": m, "makespan_mismatches": int(np.count_nonzero(Tg != T_o)),
+           "mask_mismatches": int(np.count_nonzero(fg != f_o))}
+    if m == e.n:
+        ob = coracle.argmin(T_o, f_o)
+        rec["oracle_best"] = None if ob is None else {"index": ob[0], "makespan_us": ob[1]}
+        rec["same_argmin"] = ob == (best.index, best.makespan)
+    return rec
 
 
 class Eval:
@@ -223,9 +247,10 @@ def eval_record(wl, dev, args, schedule="1f1b", early_stop=True, cpu_s=0.0):
             "roofline": roofline(committed_counters(profile_tag("early_stop", prob, schedule)), es_ms, None, None,
                                  "one poseidon_eval_candidates_bounded call: filter and survivor kernels, "
                                  + chunking)}
-    e.close()
     if cpu_s > 0:
-        rec["cpu_baseline"] = cpu_baseline(wl, cpu_s)
+        rec["cpu_baseline"], T_o, f_o = cpu_baseline(wl, cpu_s)
+        rec["oracle_check"] = oracle_check(e, best, T_o, f_o)
+    e.close()
     return rec
 
 
@@ -586,9 +611,13 @@ def main():
     }
     if "cpu_baseline" in rec:
         out["cpu_baseline"] = rec["cpu_baseline"]
+        out["oracle_check"] = rec["oracle_check"]
     if not args.no_sub and args.workload == 5 and args.schedule == "1f1b":
         sub_cpu = 0.0 if args.no_cpu_baseline else max(2.0, args.cpu_seconds / 2)
+        tiny_cpu = 0.0 if args.no_cpu_baseline else 0.5
         out["workloads"] = {
+            "cfg1": eval_record(load_workload(1, "1f1b"), dev, args, early_stop=False, cpu_s=tiny_cpu),
+            "cfg2": eval_record(load_workload(2, "1f1b"), dev, args, early_stop=False, cpu_s=tiny_cpu),
             "cfg3": eval_record(load_workload(3, "1f1b"), dev, args, early_stop=False, cpu_s=sub_cpu),
             "cfg4": eval_record(load_workload(4, "1f1b"), dev, args, early_stop=not args.no_early_stop,
                                 cpu_s=sub_cpu),
