@@ -784,7 +784,7 @@ constexpr uint64_t kChunk = 1ull << 26;
 // the early-stop survivor indices [cap] and per-block survivor counts
 // [grid_max] (cap = n plus one decode batch per block of slack, so the
 // per-block survivor segments fit) and, with a cascade, two straggler
-// queues of qcap x (1 + words + S) uint32
+// queues of qcap entries of queue_entry_words uint32
 // (qcap = n plus one block of slack per segment) and the per-block queue
 // counts [levels][grid_max].  Grown on demand; the old buffer is released
 // only after the stream has drained.
@@ -796,6 +796,13 @@ uint64_t queue_state_words(const poseidon_ctx *ctx) {
     if (ctx->base.sched == POSEIDON_SCHEDULE_INTERLEAVED_1F1B)
         return (uint64_t)pk::ilv_state_words(ctx->S, ctx->base.ndev);
     return ctx->base.sched ? 2ull * ctx->S : ctx->S;
+}
+
+// Words of one queue entry: candidate index, cut codes, the assignment
+// index (room for it whenever the problem has more than one assignment;
+// used by calls with a list of assignment indices) and the DP state.
+uint64_t queue_entry_words(const poseidon_ctx *ctx) {
+    return 1 + (uint64_t)pk::code_words((int)ctx->S) + (ctx->A > 1 ? 1 : 0) + queue_state_words(ctx);
 }
 
 int ensure_workspace(poseidon_ctx *ctx, uint64_t n, hipStream_t st) {
@@ -811,8 +818,12 @@ int ensure_workspace(poseidon_ctx *ctx, uint64_t n, hipStream_t st) {
     // cut codes, the early stop's survivor and first-stage lists and their counts
     uint64_t elems = (words + 1 + pk::kAListWords) * cap + 2ull * ctx->grid_max;
     if (ctx->base.nlevels)
-        elems += 2 * (1 + words + queue_state_words(ctx)) * queue_cap(ctx, cap) +
+        elems += 2 * queue_entry_words(ctx) * queue_cap(ctx, cap) +
                  (uint64_t)pk::kMaxLevels * ctx->grid_max;
+    // the kernels address the code words, each list and each queue with
+    // 32-bit word offsets (n is at most kChunk, so this always holds)
+    if ((words + pk::kAListWords) * cap >= (1ull << 32) || queue_entry_words(ctx) * queue_cap(ctx, cap) >= (1ull << 32))
+        return POSEIDON_E_RANGE;
     void *q = nullptr;
     if (hipMalloc(&q, elems * 4) != hipSuccess) {
         (void)hipGetLastError();
@@ -848,7 +859,7 @@ ChunkGrid chunk_grid(const poseidon_ctx *ctx, uint64_t n) {
 // Largest power-of-two chunk (at least one wave) whose cut codes, straggler
 // queues and queue counts fit the allocation-free scratch; 0 if none does.
 uint64_t noalloc_chunk_for(const poseidon_ctx *ctx) {
-    const uint64_t words = (uint64_t)pk::code_words((int)ctx->S), ent = 1 + words + queue_state_words(ctx);
+    const uint64_t words = (uint64_t)pk::code_words((int)ctx->S), ent = queue_entry_words(ctx);
     const uint64_t cap_words = pk::noalloc_scratch_bytes() / 4;
     for (uint64_t n = kChunk; n >= 64; n >>= 1) {
         const ChunkGrid g = chunk_grid(ctx, n);
@@ -861,7 +872,7 @@ uint64_t noalloc_chunk_for(const poseidon_ctx *ctx) {
 
 // One evaluation call in chunks of at most `chunk` candidates on a
 // workspace: cut codes [words][ccap] at `codes`; with a cascade, two
-// straggler queues of qcap entries of (1 + words + state words) at `queues`,
+// straggler queues of qcap entries of queue_entry_words at `queues`,
 // followed by the per-block queue counts [levels][grid].
 int eval_chunks(poseidon_ctx *ctx, const poseidon_cands *cands, uint32_t *makespan_out,
                 uint32_t *feasible_bits_out, poseidon_best *best_out, hipStream_t st, uint64_t chunk,
@@ -871,6 +882,8 @@ int eval_chunks(poseidon_ctx *ctx, const poseidon_cands *cands, uint32_t *makesp
     kp.count = cands->count;
     kp.comp_rank = cands->comp_rank;
     kp.assign_idx = cands->assign_idx;
+    // queue entries have room for the assignment index only when A > 1
+    kp.qasg = cands->comp_rank && cands->assign_idx && ctx->A > 1 ? 1u : 0u;
     kp.makespan_out = makespan_out;
     kp.feas_bits_out = feasible_bits_out;
     kp.nwords = (cands->count + 31) / 32;
@@ -880,8 +893,8 @@ int eval_chunks(poseidon_ctx *ctx, const poseidon_cands *cands, uint32_t *makesp
     if (kp.nlevels) {
         kp.qcap = qcap;
         kp.queue[0] = queues;
-        kp.queue[1] = kp.queue[0] + (1 + words + queue_state_words(ctx)) * kp.qcap;
-        kp.qcount = kp.queue[1] + (1 + words + queue_state_words(ctx)) * kp.qcap;
+        kp.queue[1] = kp.queue[0] + queue_entry_words(ctx) * kp.qcap;
+        kp.qcount = kp.queue[1] + queue_entry_words(ctx) * kp.qcap;
     }
     for (uint64_t c0 = 0; c0 < cands->count; c0 += chunk) {
         kp.first_i = c0;

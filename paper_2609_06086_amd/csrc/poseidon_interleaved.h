@@ -483,18 +483,20 @@ __global__ __launch_bounds__(kBlock) void ilv_kernel(KParams p) {
     constexpr int NW = Codes<S>::kWords, DB = IlvDepth<N>::kB;
     constexpr const IlvPattern<N, S / N> &pat = IlvConst<N, S / N>::kPat;
     unsigned long long best = ~0ull;
-    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-    const uint64_t span = (p.n_i + stride - 1) / stride;
+    // 32-bit positions: a chunk holds at most 2^26 candidates, a call fewer than 2^32
+    const uint32_t stride = gridDim.x * kBlock, n_i = (uint32_t)p.n_i, ccap = (uint32_t)p.ccap;
+    const uint32_t first_i = (uint32_t)p.first_i;
+    const uint32_t span = (n_i + stride - 1) / stride;
     __shared__ unsigned int nq;
     if (threadIdx.x == 0) nq = 0;
     __syncthreads();
-    uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
-    for (uint64_t it = 0; it < span; ++it, i += stride) {
-        const bool active = i < p.n_i;
-        const uint64_t gi = p.first_i + i;
+    uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+    for (uint32_t it = 0; it < span; ++it, i += stride) {
+        const bool active = i < n_i;
+        const uint32_t gi = first_i + i;
         uint32_t w[NW];
 #pragma unroll
-        for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[(uint64_t)k * p.ccap + i] : 0u;
+        for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[k * ccap + i] : 0u;
         uint32_t cut[S + 1], tyd[N], F[S], B[S], X[N], Fq0[S], Fq1[S], Bq[DB][S];
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = ok ? assign_of(p, gi) : 0u;
@@ -511,7 +513,7 @@ __global__ __launch_bounds__(kBlock) void ilv_kernel(KParams p) {
                 uint32_t Z[NL];
                 IlvPack<NL> pack{Z};
                 ilv_each_live<S, N>(X, Fq0, Fq1, Bq, pack);
-                enqueue<S, NL>(p, 0, &nq, !done_here && active && ok, (uint32_t)gi, w, Z);
+                enqueue<S, NL>(p, 0, &nq, !done_here && active && ok, gi, w, -1, Z);
             }
             ilv_section_ct<S, N, 2>(std::make_integer_sequence<int, pat.tail>{}, p, F, B, X, Fq0, Fq1, Bq);
         } else {
@@ -523,12 +525,12 @@ __global__ __launch_bounds__(kBlock) void ilv_kernel(KParams p) {
         if (write && p.makespan_out) p.makespan_out[gi] = T;
         if (p.feas_bits_out) {
             const unsigned long long bits = __ballot(feas);
-            const uint64_t w0 = (gi - (threadIdx.x & 63)) >> 5;
-            if ((threadIdx.x & 63) == 0 && w0 < p.nwords) p.feas_bits_out[w0] = (uint32_t)bits;
-            if ((threadIdx.x & 63) == 32 && w0 + 1 < p.nwords) p.feas_bits_out[w0 + 1] = (uint32_t)(bits >> 32);
+            const uint32_t w0 = (gi - (threadIdx.x & 63)) >> 5, nwords = (uint32_t)p.nwords;
+            if ((threadIdx.x & 63) == 0 && w0 < nwords) p.feas_bits_out[w0] = (uint32_t)bits;
+            if ((threadIdx.x & 63) == 32 && w0 + 1 < nwords) p.feas_bits_out[w0 + 1] = (uint32_t)(bits >> 32);
         }
         if (write) {
-            const unsigned long long key = make_key(feas, T, (uint32_t)gi);
+            const unsigned long long key = make_key(feas, T, gi);
             best = key < best ? key : best;
         }
     }
@@ -560,18 +562,19 @@ __global__ __launch_bounds__(kBlock) void ilv_resume_kernel(KParams p, uint32_t 
     __syncthreads();
     unsigned long long best = ~0ull;
     const uint32_t span = (n + kBlock - 1) / kBlock;
-    const uint64_t seg = (uint64_t)blockIdx.x * p.seg_cap;
+    // 32-bit word offsets: a queue holds fewer than 2^32 words
+    const uint32_t seg = blockIdx.x * (uint32_t)p.seg_cap, qcap = (uint32_t)p.qcap;
     for (uint32_t it = 0; it < span; ++it) {
-        const uint32_t q = it * kBlock + threadIdx.x;
-        const bool active = q < n;
-        const uint32_t i = active ? qin.idx[seg + q] : 0u;
+        const uint32_t q = seg + it * kBlock + threadIdx.x;
+        const bool active = it * kBlock + threadIdx.x < n;
+        const uint32_t i = active ? qin.idx[q] : 0u;
         uint32_t w[NW], Z[NL], cut[S + 1], tyd[N], F[S], B[S], X[N], Fq0[S], Fq1[S], Bq[DB][S];
 #pragma unroll
-        for (int k = 0; k < NW; ++k) w[k] = active ? qin.codes[(uint64_t)k * p.qcap + seg + q] : 0u;
+        for (int k = 0; k < NW; ++k) w[k] = active ? qin.codes[k * qcap + q] : 0u;
 #pragma unroll
-        for (int s = 0; s < NL; ++s) Z[s] = active ? qin.Y[(uint64_t)s * p.qcap + seg + q] : 0u;
+        for (int s = 0; s < NL; ++s) Z[s] = active ? qin.Y[s * qcap + q] : 0u;
         const bool ok = unpack_cuts<S>(w, p.L, cut);
-        const uint32_t a = ok ? assign_of(p, i) : 0u;
+        const uint32_t a = !active ? 0u : p.qasg ? qin.asg[q] : assign_of(p, i);
         const bool feas = ilv_weights<S, N>(p, tab, cut, a, tyd, F, B);
         // dead registers are written before any read, so zero is as good as any value
         ilv_init<S, N>(X, Fq0, Fq1, Bq);
@@ -583,7 +586,7 @@ __global__ __launch_bounds__(kBlock) void ilv_resume_kernel(KParams p, uint32_t 
             if (lvl < p.nlevels) {
                 IlvPack<NL> pack{Z};
                 ilv_each_live<S, N>(X, Fq0, Fq1, Bq, pack);
-                enqueue<S, NL>(p, lvl & 1, &nq, active && !settled, i, w, Z);
+                enqueue<S, NL>(p, lvl & 1, &nq, active && !settled, i, w, a, Z);
             }
             ilv_section_ct<S, N, 2>(std::make_integer_sequence<int, pat.tail>{}, p, F, B, X, Fq0, Fq1, Bq);
         }

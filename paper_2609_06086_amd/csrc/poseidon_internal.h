@@ -86,10 +86,12 @@ struct KParams {
     uint32_t lvl_k[kMaxLevels];
     unsigned int *qcount;             // [level][nseg]: entries block b queued for level + 1
     uint32_t *queue[2];               // ping-pong queues: level l reads queue (l-1) & 1;
-                                      // each idx[qcap] | codes[words][qcap] | Y[NX][qcap]
-                                      // (NX = S for 1F1B, 2S for Eager 1F1B, the live
-                                      // registers under Interleaved 1F1B),
+                                      // each idx[qcap] | codes[words][qcap] | asg[qcap] (if qasg)
+                                      // | Y[NX][qcap] (NX = S for 1F1B, 2S for Eager 1F1B, the
+                                      // live registers under Interleaved 1F1B),
                                       // block b owning slots [b * seg_cap, (b+1) * seg_cap)
+    uint32_t qasg;                    // queue entries carry the assignment index (calls with a
+                                      // list of assignment indices)
     uint64_t qcap, seg_cap;
     uint32_t nseg;                    // blocks of the level-0 grid (= every level's grid)
     // the current chunk of the call: candidates first_i .. first_i + n_i - 1

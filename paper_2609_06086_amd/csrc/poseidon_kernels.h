@@ -428,9 +428,9 @@ __device__ __forceinline__ void dp_finish(uint32_t (&Y)[S], const uint32_t (&F)[
 // per stage, its register just before (Yb) and after (Yf) its last forward:
 // the backward before F_{s,M} is B_{s,M-S+s}, the one stage s-1's drain
 // starts from.  In shifted registers the bracket is
-//   max(Yf[s], Yb[s+1] + cf_s + cb_s) - phi_s, and p.ek[s] holds
-//   cb_0 + .. + cb_{s-1} - phi_s (modulo 2^32: every sum that reaches T is a
-// path length below 2^31).
+//   max(Yf[s], Yb[s+1] + cf_s + cb_s) - phi_s, and the constant
+//   cb_0 + .. + cb_{s-1} - phi_s is -phi_0 + (cf_0 + cb_0) + .. + (cf_{s-1} + cb_{s-1})
+// (modulo 2^32: every sum that reaches T is a path length below 2^31).
 template <int S, bool U24>
 __device__ __forceinline__ uint32_t dp_finish_t(const KParams &p, uint32_t (&Y)[S], const uint32_t (&F)[S],
                                                 const uint32_t (&B)[S], const Comm<S> &c) {
@@ -464,13 +464,15 @@ __device__ __forceinline__ uint32_t dp_finish_t(const KParams &p, uint32_t (&Y)[
             Y[s] = N[s];
         }
     }
-    uint32_t T = 0, pb = 0, mxb = 0;
+    // ek = cb_0 + .. + cb_{s-1} - phi_s = -phi_0 + e_0 + .. + e_{s-1} (mod 2^32)
+    uint32_t T = 0, pb = 0, mxb = 0, ek = 0u - c.phi0;
 #pragma unroll
     for (int s = 0; s < S; ++s) {
         pb += B[s];
         mxb = max(mxb, B[s]);
         const uint32_t a = s + 1 < S ? max(Yf[s], Yb[s + 1 < S ? s + 1 : 0] + c.e[s + 1 < S ? s : 0]) : Yf[s];
-        T = max(T, a + pb + mul_small<U24>(mxb, S - 1 - s) + p.ek[s]);
+        T = max(T, a + pb + mul_small<U24>(mxb, S - 1 - s) + ek);
+        if (s + 1 < S) ek += c.e[s + 1 < S ? s : 0];
     }
     return T;
 }
@@ -1017,24 +1019,35 @@ __device__ __forceinline__ unsigned long long make_key(bool feasible, uint32_t T
 // kernels
 // ---------------------------------------------------------------------------
 
-// Layout of one straggler queue: idx[cap] | codes[kWords][cap] | Y[S][cap].
+// Layout of one straggler queue: idx[cap] | codes[kWords][cap] | asg[cap]
+// (calls with a list of assignment indices) | Y[NX][cap].  The entry holds
+// the assignment index rather than the next level re-reading it from the
+// caller's list: a 4-byte read at a scattered index costs a whole memory
+// sector.
 template <int S>
 struct QueueView {
-    uint32_t *idx, *codes, *Y;
+    uint32_t *idx, *codes, *asg, *Y;
     __device__ __forceinline__ QueueView(const KParams &p, int which) {
         idx = p.queue[which];
         codes = idx + p.qcap;
-        Y = codes + (uint64_t)Codes<S>::kWords * p.qcap;
+        asg = codes + (uint64_t)Codes<S>::kWords * p.qcap;
+        Y = asg + (p.qasg ? p.qcap : 0ull);
     }
 };
 
-// Queue a wave's unsettled lanes (candidate index, cut codes, registers)
-// for the next level.  Block b owns slots [b * seg_cap, (b + 1) * seg_cap)
-// of the queue and counts its entries in LDS (*nq), so no global atomic is
-// involved; every lane of the wave must call this.
+// Queue a wave's unsettled lanes (candidate index, cut codes, assignment
+// index, registers) for the next level.  Block b owns slots
+// [b * seg_cap, (b + 1) * seg_cap) of the queue and counts its entries in
+// LDS (*nq), so no global atomic is involved; every lane of the wave must
+// call this.  The assignment index (list mode with assignment indices only)
+// is `a`, or with a < 0 read again from the caller's list for candidate idx
+// of the call: the evaluation kernels would otherwise keep it in a register
+// through the DP, which costs them more than the reload of the few lanes
+// that are queued.
 template <int S, int NX>
 __device__ __forceinline__ void enqueue(const KParams &p, int which, unsigned int *nq, bool want, uint32_t idx,
-                                        const uint32_t (&w)[Codes<S>::kWords], const uint32_t (&Y)[NX]) {
+                                        const uint32_t (&w)[Codes<S>::kWords], int64_t a,
+                                        const uint32_t (&Y)[NX]) {
     const unsigned long long m = __ballot(want);
     if (m == 0) return;
     const unsigned int lane = threadIdx.x & 63;
@@ -1043,13 +1056,15 @@ __device__ __forceinline__ void enqueue(const KParams &p, int which, unsigned in
     base = __shfl(base, 0, 64);
     if (want) {
         const unsigned long long below = lane ? (m & ((1ull << lane) - 1ull)) : 0ull;
-        const uint64_t slot = (uint64_t)blockIdx.x * p.seg_cap + base + __popcll(below);
+        // 32-bit word offsets: a queue holds fewer than 2^32 words
+        const uint32_t slot = blockIdx.x * (uint32_t)p.seg_cap + base + __popcll(below), qcap = (uint32_t)p.qcap;
         const QueueView<S> q(p, which);
         q.idx[slot] = idx;
 #pragma unroll
-        for (int k = 0; k < Codes<S>::kWords; ++k) q.codes[(uint64_t)k * p.qcap + slot] = w[k];
+        for (int k = 0; k < Codes<S>::kWords; ++k) q.codes[k * qcap + slot] = w[k];
+        if (p.qasg) q.asg[slot] = a >= 0 ? (uint32_t)a : __builtin_nontemporal_load(p.assign_idx + idx);
 #pragma unroll
-        for (int s = 0; s < NX; ++s) q.Y[(uint64_t)s * p.qcap + slot] = Y[s];
+        for (int s = 0; s < NX; ++s) q.Y[s * qcap + slot] = Y[s];
     }
 }
 
@@ -1143,8 +1158,8 @@ __device__ __forceinline__ void search_cut(const KParams &p, const V *col, const
 }
 
 template <int S, typename R, int H>
-__device__ __forceinline__ void decode_ilp(const KParams &p, const Pascal<S, R, H> &pc, uint64_t base,
-                                           uint64_t stride, bool (&act)[kIlp], bool (&ok)[kIlp],
+__device__ __forceinline__ void decode_ilp(const KParams &p, const Pascal<S, R, H> &pc, uint32_t base,
+                                           uint32_t stride, bool (&act)[kIlp], bool (&ok)[kIlp],
                                            uint32_t (&asg)[kIlp], uint32_t (&w)[kIlp][Codes<S>::kWords]) {
     constexpr int NW = Codes<S>::kWords;
     constexpr uint32_t NH = 1u << H;
@@ -1153,9 +1168,9 @@ __device__ __forceinline__ void decode_ilp(const KParams &p, const Pascal<S, R, 
     uint32_t at[kIlp];
 #pragma unroll
     for (int u = 0; u < kIlp; ++u) {
-        const uint64_t i = base + u * stride;
-        act[u] = i < p.n_i;
-        ok[u] = candidate<R>(p, p.first_i + (act[u] ? i : 0), r[u], asg[u]) && act[u];
+        const uint32_t i = base + u * stride;
+        act[u] = i < (uint32_t)p.n_i;
+        ok[u] = candidate<R>(p, (uint32_t)p.first_i + (act[u] ? i : 0u), r[u], asg[u]) && act[u];
         at[u] = 1;
 #pragma unroll
         for (int k = 0; k < NW; ++k) w[u][k] = 0;
@@ -1216,7 +1231,7 @@ __device__ __forceinline__ void decode_range(const KParams &p, const Pascal<S, R
 // on.  Invalid (rank, assignment) pairs get ok = false.
 template <int S, typename R, int H, int J>
 __device__ __forceinline__ void decode_cuts(const KParams &p, const Pascal<S, R, H> &pc,
-                                            const uint64_t (&pos)[kIlp], const bool (&act)[kIlp],
+                                            const uint32_t (&pos)[kIlp], const bool (&act)[kIlp],
                                             bool (&ok)[kIlp], uint32_t (&asg)[kIlp], R (&r)[kIlp],
                                             uint32_t (&at)[kIlp], uint32_t (&cut)[kIlp][S + 1]) {
 #pragma unroll
@@ -1230,19 +1245,19 @@ __device__ __forceinline__ void decode_cuts(const KParams &p, const Pascal<S, R,
 }
 
 template <int S, typename R, int H>
-__device__ __forceinline__ void decode_batch(const KParams &p, const Pascal<S, R, H> &pc, uint64_t base,
-                                             uint64_t stride, bool &bad) {
+__device__ __forceinline__ void decode_batch(const KParams &p, const Pascal<S, R, H> &pc, uint32_t base,
+                                             uint32_t stride, bool &bad) {
     constexpr int NW = Codes<S>::kWords;
     bool act[kIlp], ok[kIlp];
     uint32_t asg[kIlp], w[kIlp][NW];
     decode_ilp<S, R, H>(p, pc, base, stride, act, ok, asg, w);
 #pragma unroll
     for (int u = 0; u < kIlp; ++u) {
-        const uint64_t i = base + u * stride;
+        const uint32_t i = base + u * stride;
         bad |= act[u] && !ok[u];
         if (act[u]) {
 #pragma unroll
-            for (int k = 0; k < NW; ++k) p.codes[(uint64_t)k * p.ccap + i] = w[u][k];
+            for (int k = 0; k < NW; ++k) p.codes[k * (uint32_t)p.ccap + i] = w[u][k];
         }
     }
 }
@@ -1286,8 +1301,9 @@ __device__ __forceinline__ void decode_all(const KParams &p, void *lds, bool &ba
     pascal_tables<S, R, H>(p, lds);
     __syncthreads();
     const Pascal<S, R, H> pc(lds);
-    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-    for (uint64_t base = (uint64_t)blockIdx.x * kBlock + threadIdx.x; base < p.n_i; base += kIlp * stride)
+    // 32-bit positions: a chunk holds at most 2^26 candidates, a call fewer than 2^32
+    const uint32_t stride = gridDim.x * kBlock, n_i = (uint32_t)p.n_i;
+    for (uint32_t base = blockIdx.x * kBlock + threadIdx.x; base < n_i; base += kIlp * stride)
         decode_batch<S, R, H>(p, pc, base, stride, bad);
 }
 
@@ -1316,20 +1332,24 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     unsigned long long best = ~0ull;
-    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    // 32-bit positions: a chunk holds at most 2^26 candidates, a call fewer
+    // than 2^32, and the code buffer fewer than 2^30 words (fewer scalar
+    // registers than 64-bit ones, which this kernel is short of)
+    const uint32_t stride = gridDim.x * kBlock, n_i = (uint32_t)p.n_i, ccap = (uint32_t)p.ccap;
+    const uint32_t first_i = (uint32_t)p.first_i;
     // every wave runs the same trip count so that ballots see whole waves
-    const uint64_t span = (p.n_i + stride - 1) / stride;
+    const uint32_t span = (n_i + stride - 1) / stride;
     const uint32_t nit = p.M >= (uint32_t)S ? p.M - S : 0u;
     __shared__ unsigned int nq;
     if (threadIdx.x == 0) nq = 0;
     __syncthreads();
-    uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
-    for (uint64_t it = 0; it < span; ++it, i += stride) {
-        const bool active = i < p.n_i;
-        const uint64_t gi = p.first_i + i;   // index within the call
+    uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+    for (uint32_t it = 0; it < span; ++it, i += stride) {
+        const bool active = i < n_i;
+        const uint32_t gi = first_i + i;   // index within the call
         uint32_t w[NW];
 #pragma unroll
-        for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[(uint64_t)k * p.ccap + i] : 0u;
+        for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[k * ccap + i] : 0u;
         uint32_t cut[S + 1], to[S], F[S], B[S], Y[S];
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = ok ? assign_of(p, gi) : 0u;
@@ -1344,7 +1364,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
             dp_prologue<S>(Y, F, B, comm, p.g24 != 0);
             const uint32_t k1 = p.nlevels ? p.lvl_k[0] : nit;
             done_here = dp_advance<S>(Y, F, B, comm, 0, k1, nit);
-            if (p.nlevels) enqueue<S, S>(p, 0, &nq, !done_here && active && ok, (uint32_t)gi, w, Y);
+            if (p.nlevels) enqueue<S, S>(p, 0, &nq, !done_here && active && ok, gi, w, -1, Y);
             T = dp_end<S, AR>(p, tab, Y, F, B, comm, w, a);
         }
         if (!ok) T = 0xFFFFFFFFu;
@@ -1353,12 +1373,12 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
         if (p.feas_bits_out) {
             // chunks start at multiples of 64, so a wave covers 64 aligned candidates
             const unsigned long long bits = __ballot(feas);
-            const uint64_t w0 = (gi - (threadIdx.x & 63)) >> 5;
-            if ((threadIdx.x & 63) == 0 && w0 < p.nwords) p.feas_bits_out[w0] = (uint32_t)bits;
-            if ((threadIdx.x & 63) == 32 && w0 + 1 < p.nwords) p.feas_bits_out[w0 + 1] = (uint32_t)(bits >> 32);
+            const uint32_t w0 = (gi - (threadIdx.x & 63)) >> 5, nwords = (uint32_t)p.nwords;
+            if ((threadIdx.x & 63) == 0 && w0 < nwords) p.feas_bits_out[w0] = (uint32_t)bits;
+            if ((threadIdx.x & 63) == 32 && w0 + 1 < nwords) p.feas_bits_out[w0 + 1] = (uint32_t)(bits >> 32);
         }
         if (write) {
-            const unsigned long long key = make_key(feas, T, (uint32_t)gi);
+            const unsigned long long key = make_key(feas, T, gi);
             best = key < best ? key : best;
         }
     }
@@ -1379,19 +1399,21 @@ __global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
     const Comm<S> comm = load_comm<S>(p);
     constexpr int NW = Codes<S>::kWords;
     unsigned long long best = ~0ull;
-    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-    const uint64_t span = (p.n_i + stride - 1) / stride;
+    // 32-bit positions, as in eval_kernel
+    const uint32_t stride = gridDim.x * kBlock, n_i = (uint32_t)p.n_i, ccap = (uint32_t)p.ccap;
+    const uint32_t first_i = (uint32_t)p.first_i;
+    const uint32_t span = (n_i + stride - 1) / stride;
     const uint32_t npairs = TAB ? 0u : p.M - 2 * S + 1;
     __shared__ unsigned int nq;
     if (threadIdx.x == 0) nq = 0;
     __syncthreads();
-    uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
-    for (uint64_t it = 0; it < span; ++it, i += stride) {
-        const bool active = i < p.n_i;
-        const uint64_t gi = p.first_i + i;
+    uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+    for (uint32_t it = 0; it < span; ++it, i += stride) {
+        const bool active = i < n_i;
+        const uint32_t gi = first_i + i;
         uint32_t w[NW];
 #pragma unroll
-        for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[(uint64_t)k * p.ccap + i] : 0u;
+        for (int k = 0; k < NW; ++k) w[k] = active ? p.codes[k * ccap + i] : 0u;
         uint32_t cut[S + 1], to[S], F[S], B[S], Y[S];
         const bool ok = unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = ok ? assign_of(p, gi) : 0u;
@@ -1408,7 +1430,7 @@ __global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
             if (p.nlevels) {
                 uint32_t X[2 * S];
                 eager_pack<S>(Y, Fn, Fp, X);
-                enqueue<S, 2 * S>(p, 0, &nq, !done_here && active && ok, (uint32_t)gi, w, X);
+                enqueue<S, 2 * S>(p, 0, &nq, !done_here && active && ok, gi, w, -1, X);
             }
             eager_epilogue<S>(Y, Fn, Fp, F, B, comm);
         }
@@ -1418,12 +1440,12 @@ __global__ __launch_bounds__(kBlock) void sched_kernel(KParams p) {
         if (write && p.makespan_out) p.makespan_out[gi] = T;
         if (p.feas_bits_out) {
             const unsigned long long bits = __ballot(feas);
-            const uint64_t w0 = (gi - (threadIdx.x & 63)) >> 5;
-            if ((threadIdx.x & 63) == 0 && w0 < p.nwords) p.feas_bits_out[w0] = (uint32_t)bits;
-            if ((threadIdx.x & 63) == 32 && w0 + 1 < p.nwords) p.feas_bits_out[w0 + 1] = (uint32_t)(bits >> 32);
+            const uint32_t w0 = (gi - (threadIdx.x & 63)) >> 5, nwords = (uint32_t)p.nwords;
+            if ((threadIdx.x & 63) == 0 && w0 < nwords) p.feas_bits_out[w0] = (uint32_t)bits;
+            if ((threadIdx.x & 63) == 32 && w0 + 1 < nwords) p.feas_bits_out[w0 + 1] = (uint32_t)(bits >> 32);
         }
         if (write) {
-            const unsigned long long key = make_key(feas, T, (uint32_t)gi);
+            const unsigned long long key = make_key(feas, T, gi);
             best = key < best ? key : best;
         }
     }
@@ -1456,18 +1478,19 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
     __syncthreads();
     unsigned long long best = ~0ull;
     const uint32_t span = (n + kBlock - 1) / kBlock;
-    const uint64_t seg = (uint64_t)blockIdx.x * p.seg_cap;
+    // 32-bit word offsets: a queue holds fewer than 2^32 words
+    const uint32_t seg = blockIdx.x * (uint32_t)p.seg_cap, qcap = (uint32_t)p.qcap;
     for (uint32_t it = 0; it < span; ++it) {
-        const uint32_t q = it * kBlock + threadIdx.x;
-        const bool active = q < n;
-        const uint32_t i = active ? qin.idx[seg + q] : 0u;
+        const uint32_t q = seg + it * kBlock + threadIdx.x;
+        const bool active = it * kBlock + threadIdx.x < n;
+        const uint32_t i = active ? qin.idx[q] : 0u;
         uint32_t w[NW], cut[S + 1], to[S], F[S], B[S], X[NX], Y[S];
 #pragma unroll
-        for (int k = 0; k < NW; ++k) w[k] = active ? qin.codes[(uint64_t)k * p.qcap + seg + q] : 0u;
+        for (int k = 0; k < NW; ++k) w[k] = active ? qin.codes[k * qcap + q] : 0u;
 #pragma unroll
-        for (int s = 0; s < NX; ++s) X[s] = active ? qin.Y[(uint64_t)s * p.qcap + seg + q] : 0u;
+        for (int s = 0; s < NX; ++s) X[s] = active ? qin.Y[s * qcap + q] : 0u;
         const bool ok = unpack_cuts<S>(w, p.L, cut);
-        const uint32_t a = ok ? assign_of(p, i) : 0u;
+        const uint32_t a = !active ? 0u : p.qasg ? qin.asg[q] : assign_of(p, i);
         decode_toff<S>(p, tab, a, to);
         const bool feas = stage_weights<S>(p, tab, cut, to, F, B);
         bool settled;
@@ -1478,7 +1501,7 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
             settled = eager_advance<S>(Y, Fn, Fp, F, B, comm, k0, k1, nit);
             if (lvl < p.nlevels) {
                 eager_pack<S>(Y, Fn, Fp, X);
-                enqueue<S, NX>(p, lvl & 1, &nq, active && !settled, i, w, X);
+                enqueue<S, NX>(p, lvl & 1, &nq, active && !settled, i, w, a, X);
             }
             eager_epilogue<S>(Y, Fn, Fp, F, B, comm);
             T = end_time<S, AR>(p, tab, Y, comm, w, a);
@@ -1486,7 +1509,7 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
 #pragma unroll
             for (int s = 0; s < S; ++s) Y[s] = X[s];
             settled = dp_advance<S>(Y, F, B, comm, k0, k1, nit);
-            if (lvl < p.nlevels) enqueue<S, S>(p, lvl & 1, &nq, active && !settled, i, w, Y);
+            if (lvl < p.nlevels) enqueue<S, S>(p, lvl & 1, &nq, active && !settled, i, w, a, Y);
             T = dp_end<S, AR>(p, tab, Y, F, B, comm, w, a);
         }
         if (active && settled) {
@@ -1549,31 +1572,34 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
     const Pascal<S, R, H> pc(pas);
     const AList al(p);
     const unsigned int lane = threadIdx.x & 63;
-    const uint64_t seg = (uint64_t)blockIdx.x * p.seg_cap;
+    // 32-bit positions and word offsets: a piece holds at most 2^26
+    // candidates, a call fewer than 2^32, and each list fewer than 2^32
+    // words (fewer scalar registers than 64-bit ones)
+    const uint32_t seg = blockIdx.x * (uint32_t)p.seg_cap, ccap = (uint32_t)p.ccap;
+    const uint32_t first_i = (uint32_t)p.first_i;
     // full, prefix: the piece, kIlp candidates a lane, strided over the grid;
     // gather: this block's segment of the list, strided over the block
-    const uint64_t n = MODE == kFilterGather ? (uint64_t)p.acount[blockIdx.x] : p.n_i;
-    const uint64_t stride = MODE == kFilterGather ? (uint64_t)kBlock : (uint64_t)gridDim.x * kBlock;
-    const uint64_t start = MODE == kFilterGather ? (uint64_t)threadIdx.x
-                                                 : (uint64_t)blockIdx.x * kBlock + threadIdx.x;
-    for (uint64_t base = start; base < n; base += kIlp * stride) {
+    const uint32_t n = MODE == kFilterGather ? p.acount[blockIdx.x] : (uint32_t)p.n_i;
+    const uint32_t stride = MODE == kFilterGather ? (uint32_t)kBlock : gridDim.x * kBlock;
+    const uint32_t start = MODE == kFilterGather ? threadIdx.x : blockIdx.x * kBlock + threadIdx.x;
+    for (uint32_t base = start; base < n; base += kIlp * stride) {
         bool act[kIlp], ok[kIlp];
-        uint64_t pos[kIlp];
+        uint32_t pos[kIlp];
         uint32_t asg[kIlp], at[kIlp], cut[kIlp][S + 1];
         R r[kIlp];
         if constexpr (MODE == kFilterGather) {
 #pragma unroll
             for (int u = 0; u < kIlp; ++u) {
-                const uint64_t i = base + u * stride;
+                const uint32_t i = base + u * stride;
                 act[u] = i < n;
                 ok[u] = act[u];
-                const uint64_t o = seg + (act[u] ? i : 0);
+                const uint32_t o = seg + (act[u] ? i : 0);
                 pos[u] = al.pos[o];
                 asg[u] = al.asg[o];
                 r[u] = sizeof(R) == 8 ? (R)(((uint64_t)al.rhi[o] << 32) | al.rlo[o]) : (R)al.rlo[o];
                 uint32_t w[NW];
 #pragma unroll
-                for (int k = 0; k < NW; ++k) w[k] = k < AW ? al.w[(uint64_t)k * p.ccap + o] : 0u;
+                for (int k = 0; k < NW; ++k) w[k] = k < AW ? al.w[k * ccap + o] : 0u;
                 cut[u][0] = 0;
                 cut[u][S] = p.L;
 #pragma unroll
@@ -1584,9 +1610,9 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
         } else {
 #pragma unroll
             for (int u = 0; u < kIlp; ++u) {
-                const uint64_t i = base + u * stride;
+                const uint32_t i = base + u * stride;
                 act[u] = i < n;
-                pos[u] = p.first_i + (act[u] ? i : 0);
+                pos[u] = first_i + (act[u] ? i : 0);
             }
             decode_cuts<S, R, H, MODE == kFilterPrefix ? X0 : S - 1>(p, pc, pos, act, ok, asg, r, at, cut);
         }
@@ -1609,25 +1635,25 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
                 slot0 = __shfl(slot0, 0, 64);
                 if (keep) {
                     const unsigned long long below = lane ? (m & ((1ull << lane) - 1ull)) : 0ull;
-                    const uint64_t o = seg + slot0 + (uint32_t)__popcll(below);
+                    const uint32_t o = seg + slot0 + (uint32_t)__popcll(below);
                     if constexpr (MODE == kFilterPrefix) {
                         uint32_t w[AW];
 #pragma unroll
                         for (int k = 0; k < AW; ++k) w[k] = 0;
 #pragma unroll
                         for (int j = 1; j <= X0; ++j) w[(j - 1) / 4] |= cut[u][j] << (8 * ((j - 1) % 4));
-                        al.pos[o] = (uint32_t)pos[u];
+                        al.pos[o] = pos[u];
                         al.asg[o] = asg[u];
                         al.rlo[o] = (uint32_t)r[u];
                         if (sizeof(R) == 8) al.rhi[o] = (uint32_t)((uint64_t)r[u] >> 32);
 #pragma unroll
-                        for (int k = 0; k < AW; ++k) al.w[(uint64_t)k * p.ccap + o] = w[k];
+                        for (int k = 0; k < AW; ++k) al.w[k * ccap + o] = w[k];
                     } else {
                         uint32_t w[NW];
                         pack_cuts<S>(cut[u], true, w);
-                        p.sidx[o] = (uint32_t)pos[u];
+                        p.sidx[o] = pos[u];
 #pragma unroll
-                        for (int k = 0; k < NW; ++k) p.codes[(uint64_t)k * p.ccap + o] = w[k];
+                        for (int k = 0; k < NW; ++k) p.codes[k * ccap + o] = w[k];
                     }
                 }
                 if (MODE != kFilterPrefix) n_keep += lane == 0 ? (uint32_t)__popcll(m) : 0u;
@@ -1722,11 +1748,11 @@ __global__ __launch_bounds__(kBlock) void surv_kernel(KParams p, uint32_t publis
             if (pre[mid] <= k) lo = mid;
             else hi = mid;
         }
-        const uint64_t at = (uint64_t)lo * p.seg_cap + (k - pre[lo]);
+        const uint32_t at = lo * (uint32_t)p.seg_cap + (k - pre[lo]);
         const uint32_t i = p.sidx[at];
         uint32_t w[NW], cut[S + 1], to[S], F[S], B[S];
 #pragma unroll
-        for (int kk = 0; kk < NW; ++kk) w[kk] = p.codes[(uint64_t)kk * p.ccap + at];
+        for (int kk = 0; kk < NW; ++kk) w[kk] = p.codes[kk * (uint32_t)p.ccap + at];
         unpack_cuts<S>(w, p.L, cut);
         const uint32_t a = assign_of(p, i);
         decode_toff<S>(p, tab, a, to);
