@@ -544,14 +544,6 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         }
     }
     for (uint32_t s = 1; s < S; ++s) kp.psi[s] = kp.psi[s - 1] + kp.cf[s - 1];
-    // closed-form drain of the 1F1B epilogue: ek[s] = cb_0 + .. + cb_{s-1} - phi_s
-    // (phi_s = cf_s + .. + cf_{S-2}), modulo 2^32
-    for (uint32_t s = 0; s < S; ++s) {
-        uint32_t cbs = 0, phi = 0;
-        for (uint32_t i = 0; i < s; ++i) cbs += kp.cb[i];
-        for (uint32_t i = s; i + 1 < S; ++i) phi += kp.cf[i];
-        kp.ek[s] = cbs - phi;
-    }
     // cascade checkpoints of the steady loop: K0, 2 K0, 4 K0, ... below M - S
     // (steady iterations: 1F1B slot pairs after its prologue, Eager 1F1B
     // slot pairs between its prologue and epilogue)

@@ -49,8 +49,6 @@ struct KParams {
     uint32_t ilv_compiled, ilv_trips; // Interleaved 1F1B: the schedule runs as compiled code with
                                       // this many steady periods
     uint32_t psi[kSMax];          // cf_0 + ... + cf_{s-1}: undoes the per-stage shift at the end
-    uint32_t ek[kSMax];           // cb_0 + .. + cb_{s-1} - (cf_s + .. + cf_{S-2}) mod 2^32: the closed-form
-                                  // drain's constant per stage
     uint8_t fixed_types[kSMax];
     // candidates of the call
     uint64_t first, count;
