@@ -76,19 +76,24 @@ def kernel_sha():
 
 
 def profile_tag(kind, prob, schedule="1f1b"):
-    """Name of a profile: pass kind and workload shape."""
+    """Name of a profile: pass kind and workload shape (and whether the DAG
+    has all-reduce nodes, which other kernel instances evaluate)."""
     sched = {"1f1b": "", "eager": "_eager", "interleaved": f"_interleaved_N{prob.S // 2}"}[schedule]
-    return f"{kind}{sched}_L{prob.L}_S{prob.S}_M{prob.M}"
+    ar = "_allreduce" if getattr(prob, "allreduce", None) is not None else ""
+    return f"{kind}{sched}{ar}_L{prob.L}_S{prob.S}_M{prob.M}"
 
 
-def committed_counters(tag):
+def committed_counters(tag, candidates=None):
     """Per-call counter figures of the committed summary for `tag`, or None
-    if it is missing or the kernel / launch code changed since it was taken."""
+    if it is missing, was taken on another number of candidates per call,
+    or the kernel / launch code changed since it was taken."""
     path = os.path.join(PROFILES, tag + ".counters.json")
     if not os.path.exists(path):
         return None
     t = json.load(open(path))
     if t.get("source_sha256") != kernel_sha():
+        return None
+    if candidates is not None and t.get("candidates") != candidates:
         return None
     t["path"] = os.path.relpath(path, ROOT)
     return t
@@ -229,7 +234,7 @@ def eval_record(wl, dev, args, schedule="1f1b", early_stop=True, cpu_s=0.0):
            "dag_nodes_per_candidate": 2 * S * M, "ms": ms_wall, "kernel_ms": call_ms,
            "candidates_per_s": n / (ms_wall * 1e-3), "dag_nodes_per_s": n * 2 * S * M / (ms_wall * 1e-3),
            "best": {"index": best.index, "makespan_us": best.makespan},
-           "roofline": roofline(committed_counters(profile_tag("eval_pipeline", prob, schedule)), call_ms, ops,
+           "roofline": roofline(committed_counters(profile_tag("eval_pipeline", prob, schedule), n), call_ms, ops,
                                 algo_bytes, "one poseidon_eval_candidates call: decode, eval and resume kernels")}
     if early_stop and wl.cands.is_list and schedule != "interleaved":
         bound = e.warm_bound()
@@ -244,7 +249,7 @@ def eval_record(wl, dev, args, schedule="1f1b", early_stop=True, cpu_s=0.0):
             "evaluated": st.evaluated, "pruned": st.pruned, "infeasible": st.infeasible,
             "best_index": bb.index, "best_makespan": bb.makespan,
             "same_argmin_as_exhaustive": (bb.index, bb.makespan) == (best.index, best.makespan),
-            "roofline": roofline(committed_counters(profile_tag("early_stop", prob, schedule)), es_ms, None, None,
+            "roofline": roofline(committed_counters(profile_tag("early_stop", prob, schedule), n), es_ms, None, None,
                                  "one poseidon_eval_candidates_bounded call: filter and survivor kernels, "
                                  + chunking)}
     if cpu_s > 0:
@@ -398,7 +403,7 @@ def summarize(args):
     d, tag, calls, timed_calls = args.summarize, args.tag, args.calls, args.timed_calls
     pat = re.compile(PASS_KERNELS[args.pass_kind])
     out = {"tag": tag, "pass": args.pass_kind, "source_sha256": kernel_sha(), "calls_profiled": calls,
-           "commands": args.commands}
+           "candidates": args.candidates or None, "commands": args.commands}
     md = [f"# {args.title}\n", args.description + "\n" if args.description else ""]
     kt = _csv(os.path.join(d, "kt"), "_kernel_trace.csv")
     if kt:
