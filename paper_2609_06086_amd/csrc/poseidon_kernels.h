@@ -192,6 +192,22 @@ __device__ __forceinline__ void decode_toff(const KParams &p, const Ent &t, uint
         }
         return;
     }
+    if (p.assign_mode == kAssignFixed) {
+        // the same offsets for every candidate: four stage types a word, each
+        // word passed through an empty asm so that the offsets are unpacked
+        // (scalar instructions) where they are used instead of S loop-
+        // invariant values holding scalar registers through the whole kernel
+#pragma unroll
+        for (int g = 0; g < (S + 3) / 4; ++g) {
+            uint32_t wd = (uint32_t)p.fixed_types[4 * g] | (uint32_t)p.fixed_types[4 * g + 1] << 8 |
+                          (uint32_t)p.fixed_types[4 * g + 2] << 16 | (uint32_t)p.fixed_types[4 * g + 3] << 24;
+            asm volatile("" : "+s"(wd));
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (4 * g + i < S) to[4 * g + i < S ? 4 * g + i : 0] = ((wd >> (8 * i)) & 0xFFu) * p.erow;
+        }
+        return;
+    }
     uint32_t ty[S];
     decode_types<S>(p, a, ty);
 #pragma unroll
