@@ -805,7 +805,8 @@ int ensure_workspace(poseidon_ctx *ctx, uint64_t n, hipStream_t st) {
         ctx->ws = nullptr;
         ctx->ws_cap = 0;
     }
-    const uint64_t cap = std::max<uint64_t>(n, 1024) + (uint64_t)ctx->grid_max * pk::kDecodeIlp * 256;
+    // (a multiple of 4 words: the range-mode decode stores four code words at once)
+    const uint64_t cap = (std::max<uint64_t>(n, 1024) + (uint64_t)ctx->grid_max * pk::kDecodeIlp * 256 + 3) & ~3ull;
     const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
     // cut codes, the early stop's survivor and first-stage lists and their counts
     uint64_t elems = (words + 1 + pk::kAListWords) * cap + 2ull * ctx->grid_max;

@@ -1148,24 +1148,24 @@ struct Pascal {
 // One cut's search for kIlp candidates over a column of type V (R or
 // uint32): Q = C(L - a, k + 1) - r, the smallest n with C(n, k + 1) >= Q by
 // the tree, the rank left C(n, k + 1) - Q, the cut L - n.
-template <typename V, typename R, int H>
-__device__ __forceinline__ void search_cut(const KParams &p, const V *col, const V *tree, R (&r)[kIlp],
-                                           uint32_t (&at)[kIlp], uint32_t (&cut)[kIlp]) {
+template <typename V, typename R, int H, int NI = kIlp>
+__device__ __forceinline__ void search_cut(const KParams &p, const V *col, const V *tree, R (&r)[NI],
+                                           uint32_t (&at)[NI], uint32_t (&cut)[NI]) {
     constexpr uint32_t NH = 1u << H;
-    V Q[kIlp];
-    uint32_t t[kIlp];   // tree node
+    V Q[NI];
+    uint32_t t[NI];   // tree node
 #pragma unroll
-    for (int u = 0; u < kIlp; ++u) {
+    for (int u = 0; u < NI; ++u) {
         Q[u] = col[p.L - at[u]] - (V)r[u];
         t[u] = 1;
     }
 #pragma unroll
     for (int b = 0; b < H; ++b) {
 #pragma unroll
-        for (int u = 0; u < kIlp; ++u) t[u] = tree_step(t[u], tree[t[u]], Q[u]);
+        for (int u = 0; u < NI; ++u) t[u] = tree_step(t[u], tree[t[u]], Q[u]);
     }
 #pragma unroll
-    for (int u = 0; u < kIlp; ++u) {
+    for (int u = 0; u < NI; ++u) {
         const uint32_t pos = t[u] - NH;
         r[u] = (R)(col[pos] - Q[u]);
         cut[u] = p.L - pos;
@@ -1312,11 +1312,77 @@ __host__ __device__ constexpr size_t pascal_bytes(uint32_t L) {
                                                   (size_t)narrow_cols<S, R>() * 4);
 }
 
+// Range mode with one assignment: candidate i of the chunk is composition
+// rank first + first_i + i, so consecutive candidates are consecutive
+// ranks.  A lane takes kIlp consecutive candidates: it unranks the first
+// (one search per cut) and steps to the others by the lexicographic
+// successor, in which the last cut that can still grow (cut j may reach
+// L - S + j) grows by one and the cuts after it follow it at distance 1.
+// The lane's kIlp code words of one word index are contiguous: one 16-byte
+// store (the code rows hold a multiple of 4 words).
+template <int S>
+__device__ __forceinline__ void next_cuts(uint32_t L, uint32_t (&c)[S + 1]) {
+    // js = the last cut that can grow, b = c_js + 1 - js (no register index
+    // is dynamic: both are selected in the scan)
+    uint32_t js = 0, b = 1;
+#pragma unroll
+    for (int j = 1; j <= S - 1; ++j) {
+        const bool grow = c[j] < L - S + j;
+        js = grow ? (uint32_t)j : js;
+        b = grow ? c[j] + 1 - j : b;
+    }
+#pragma unroll
+    for (int m = 1; m <= S - 1; ++m) c[m] = (uint32_t)m < js ? c[m] : b + m;
+}
+
+template <int S, typename R, int H>
+__device__ __forceinline__ void decode_succ(const KParams &p, const Pascal<S, R, H> &pc, uint32_t base, bool &bad) {
+    static_assert(kIlp == 4, "one 16-byte store per code word");
+    constexpr int NW = Codes<S>::kWords;
+    constexpr uint32_t NH = 1u << H;
+    constexpr int NN = Pascal<S, R, H>::NN;
+    const uint64_t rank0 = p.first + (uint32_t)p.first_i + base;
+    R r[1] = {(R)(rank0 < p.n_comp ? rank0 : 0)};
+    uint32_t at[1] = {1u}, c[S + 1];
+    c[0] = 0;
+    c[S] = p.L;
+#pragma unroll
+    for (int j = 1; j <= S - 2; ++j) {
+        const int col = S - j;
+        uint32_t cj[1];
+        if (col < NN)
+            search_cut<uint32_t, R, H, 1>(p, pc.ns + (uint32_t)col * NH, pc.nt + (uint32_t)col * NH, r, at, cj);
+        else
+            search_cut<R, R, H, 1>(p, pc.ws + (uint32_t)(col - NN) * NH, pc.wt + (uint32_t)(col - NN) * NH, r, at, cj);
+        c[j] = cj[0];
+    }
+    if (S >= 2) c[S - 1] = at[0] + (uint32_t)r[0];
+    uint32_t w[kIlp][NW];
+#pragma unroll
+    for (int u = 0; u < kIlp; ++u) {
+        if (u > 0) next_cuts<S>(p.L, c);
+        const bool act = base + u < (uint32_t)p.n_i;
+        const bool ok = rank0 + u < p.n_comp;
+        bad |= act && !ok;
+        pack_cuts<S>(c, ok, w[u]);
+    }
+    const uint32_t ccap = (uint32_t)p.ccap;
+#pragma unroll
+    for (int k = 0; k < NW; ++k)
+        *reinterpret_cast<uint4 *>(p.codes + k * ccap + base) = make_uint4(w[0][k], w[1][k], w[2][k], w[3][k]);
+}
+
 template <int S, typename R, int H>
 __device__ __forceinline__ void decode_all(const KParams &p, void *lds, bool &bad) {
     pascal_tables<S, R, H>(p, lds);
     __syncthreads();
     const Pascal<S, R, H> pc(lds);
+    if (!p.comp_rank && p.A == 1) {
+        const uint32_t stride = gridDim.x * kBlock * kIlp, n_i = (uint32_t)p.n_i;
+        for (uint32_t base = (blockIdx.x * kBlock + threadIdx.x) * kIlp; base < n_i; base += stride)
+            decode_succ<S, R, H>(p, pc, base, bad);
+        return;
+    }
     // 32-bit positions: a chunk holds at most 2^26 candidates, a call fewer than 2^32
     const uint32_t stride = gridDim.x * kBlock, n_i = (uint32_t)p.n_i;
     for (uint32_t base = blockIdx.x * kBlock + threadIdx.x; base < n_i; base += kIlp * stride)
