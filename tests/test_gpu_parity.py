@@ -512,6 +512,19 @@ def test_call_longer_than_one_chunk(dev):
     ctx.close()
 
 
+def test_range_mode_consecutive_ranks_across_chunks(dev):
+    """Range mode with one assignment decodes four consecutive ranks per lane
+    (the first unranked, the next three by the lexicographic successor): a
+    range of 2^26 + 3,001 compositions from an odd offset spans two chunks,
+    and ranges that end at the last composition put the successor step past
+    it on lanes beyond the call only."""
+    rng = np.random.default_rng(120)
+    prob = W.random_problem(rng, 60, 8, 12, 2, cost_hi=400, comm_hi=50, mem_hi=30, cap=300, assign_rows=1)
+    n_comp = math.comb(59, 7)
+    for first, count in ((123457, (1 << 26) + 3001), (n_comp - 5001, 5001), (n_comp - 3, 3), (0, 1)):
+        check_against_oracle(prob, W.Candidates(first=first, count=count), dev)
+
+
 # ------------------------------------------------------ DP all-reduce
 
 def _with_allreduce(rng, prob, hi=3000):
