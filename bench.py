@@ -161,6 +161,34 @@ def cpu_baseline(wl, target_s):
                       f"Kahn order, topological DP) on {threads} host threads, {dt:.1f} s"}, T, feas
 
 
+def python_oracle_baseline(wl, target_s):
+    """The pure-Python oracle (explicit DAG, Kahn order, one thread) on a
+    prefix of the candidates sized for about target_s seconds.  Returns the
+    record and its makespans and feasibility."""
+    from oracle import dag
+    from paper_2609_06086_amd import workloads as W
+    c = wl.cands
+    n = len(c)
+
+    def prefix(m):
+        if c.is_list:
+            return W.Candidates(comp_rank=c.comp_rank[:m],
+                                assign_idx=None if c.assign_idx is None else c.assign_idx[:m])
+        return W.Candidates(first=c.first, count=m)
+
+    probe = min(n, 200)
+    t0 = time.perf_counter()
+    dag.evaluate(wl.problem, prefix(probe))
+    dt = time.perf_counter() - t0
+    m = int(min(n, max(probe, probe * target_s / max(dt, 1e-6))))
+    t0 = time.perf_counter()
+    T, feas = dag.evaluate(wl.problem, prefix(m))
+    dt = time.perf_counter() - t0
+    return {"value": m / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {m} of the {n} candidates, Python oracle (explicit DAG, Kahn order, "
+                      f"topological DP) on one thread, {dt:.2f} s"}, T.astype("uint32"), feas
+
+
 def oracle_check(e, best, T_o, f_o):
     """The timed pass's outputs against the oracle's on its prefix: every
     makespan and mask bit, and (when the prefix is the whole list) the argmin."""
@@ -220,7 +248,7 @@ class Eval:
         self.ctx.close()
 
 
-def eval_record(wl, dev, args, schedule="1f1b", early_stop=True, cpu_s=0.0):
+def eval_record(wl, dev, args, schedule="1f1b", early_stop=True, cpu_s=0.0, py_s=0.0):
     """Exhaustive pass (and early-stop pass) of one workload as a record."""
     import torch
     e = Eval(wl, dev)
@@ -255,7 +283,12 @@ def eval_record(wl, dev, args, schedule="1f1b", early_stop=True, cpu_s=0.0):
     if cpu_s > 0:
         rec["cpu_baseline"], T_o, f_o = cpu_baseline(wl, cpu_s)
         rec["oracle_check"] = oracle_check(e, best, T_o, f_o)
+    if py_s > 0:
+        rec["python_oracle"], T_p, f_p = python_oracle_baseline(wl, py_s)
+        rec["python_oracle"]["check"] = oracle_check(e, best, T_p, f_p)
     e.close()
+    if "python_oracle" in rec or rec["roofline"]["achieved"] is None and n < (1 << 20):
+        rec["note"] = "launch-bound (a few microseconds of kernel work per call): no counter profile"
     return rec
 
 
@@ -621,8 +654,10 @@ def main():
         sub_cpu = 0.0 if args.no_cpu_baseline else max(2.0, args.cpu_seconds / 2)
         tiny_cpu = 0.0 if args.no_cpu_baseline else 0.5
         out["workloads"] = {
-            "cfg1": eval_record(load_workload(1, "1f1b"), dev, args, early_stop=False, cpu_s=tiny_cpu),
-            "cfg2": eval_record(load_workload(2, "1f1b"), dev, args, early_stop=False, cpu_s=tiny_cpu),
+            "cfg1": eval_record(load_workload(1, "1f1b"), dev, args, early_stop=False, cpu_s=tiny_cpu,
+                                py_s=tiny_cpu),
+            "cfg2": eval_record(load_workload(2, "1f1b"), dev, args, early_stop=False, cpu_s=tiny_cpu,
+                                py_s=tiny_cpu),
             "cfg3": eval_record(load_workload(3, "1f1b"), dev, args, early_stop=False, cpu_s=sub_cpu),
             "cfg4": eval_record(load_workload(4, "1f1b"), dev, args, early_stop=not args.no_early_stop,
                                 cpu_s=sub_cpu),
