@@ -1415,7 +1415,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(KParams p) {
     constexpr int NW = Codes<S>::kWords;
     unsigned long long best = ~0ull;
     // 32-bit positions: a chunk holds at most 2^26 candidates, a call fewer
-    // than 2^32, and the code buffer fewer than 2^30 words (fewer scalar
+    // than 2^32, and the code buffer fewer than 2^32 words (fewer scalar
     // registers than 64-bit ones, which this kernel is short of)
     const uint32_t stride = gridDim.x * kBlock, n_i = (uint32_t)p.n_i, ccap = (uint32_t)p.ccap;
     const uint32_t first_i = (uint32_t)p.first_i;
