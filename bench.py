@@ -25,7 +25,9 @@ Roofline fields: the path is 32-bit integer add/max on the vector ALUs.
 `roofline.achieved` is the INT32 lane-operations one call executes, counted
 by rocprofv3 (INT32 VALU wave-instructions x the mean active lanes of each
 kernel's VALU cycles, summed over the call's kernels), divided by the call
-time measured here with HIP events; `frac` = achieved / 39.32 Top/s.  The
+time measured here with HIP events; `frac` = achieved / 39.32 Top/s.
+`dominant_kernel` gives the same rate for the kernel with the largest share
+of the call, over its own time in the committed kernel trace.  The
 counts come from the committed summary profiles/<tag>.counters.json and are
 used only while its hash of the kernel and launch sources matches the
 current ones (else null).  The plain longest-path recurrence's 6SM - 4M - S
@@ -99,6 +101,25 @@ def committed_counters(tag, candidates=None):
     return t
 
 
+def dominant_kernel(ctr):
+    """The kernel with the largest share of a call in the committed trace,
+    with its INT32 lane-op rate over its own traced time."""
+    if not ctr or not ctr.get("kernels") or not ctr.get("per_kernel"):
+        return None
+    calls = ctr["calls_profiled"]
+    per_call = {k: v["avg_ns"] * v["dispatches"] / calls * 1e-6 for k, v in ctr["kernels"].items()}
+    name = max(per_call, key=per_call.get)
+    k = ctr["per_kernel"].get(name, {})
+    ms = per_call[name]
+    ops = k.get("int32_lane_ops")
+    achieved = None if ops is None else ops / (ms * 1e-3) / 1e12
+    return {"name": name, "ms_per_call": ms, "share": ms / sum(per_call.values()),
+            "int32_lane_ops_per_call": ops, "achieved": achieved,
+            "frac": None if achieved is None else achieved / PEAK_INT32_TOPS,
+            "valu_issue_frac": None if "SQ_INSTS_VALU" not in k else
+            k["SQ_INSTS_VALU"] * 4 / (N_SIMD * PEAK_CLOCK * ms * 1e-3)}
+
+
 def roofline(ctr, call_ms, nominal_ops, algo_bytes, launch):
     """Hardware roofline of one call (see the module docstring)."""
     lane_ops = None if ctr is None else ctr.get("valu_int32_lane_ops_per_call")
@@ -116,6 +137,7 @@ def roofline(ctr, call_ms, nominal_ops, algo_bytes, launch):
             "valu_issue_frac": None if ctr is None else
             ctr["valu_wave_insts_per_call"] * 4 / (N_SIMD * PEAK_CLOCK * call_ms * 1e-3),
             "counters": None if ctr is None else ctr["path"],
+            "dominant_kernel": dominant_kernel(ctr),
             "launch": launch}
 
 
