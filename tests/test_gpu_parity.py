@@ -525,6 +525,24 @@ def test_range_mode_consecutive_ranks_across_chunks(dev):
         check_against_oracle(prob, W.Candidates(first=first, count=count), dev)
 
 
+def test_range_mode_consecutive_ranks_every_stage_count(dev):
+    """The range-mode successor decode for S = 1..16 and for L up to 256 (64-bit
+    ranks, the Pascal table's full column): ragged ranges from random
+    offsets, the first ranks and the last ones."""
+    rng = np.random.default_rng(121)
+    for S in range(1, 17):
+        # the longest model up to 256 layers whose compositions are counted below 2^63
+        L_max = max(L for L in range(S, 257) if math.comb(L - 1, S - 1) < 2 ** 63)
+        for L in (S, S + int(rng.integers(1, 30)), L_max):
+            M = S + int(rng.integers(0, 20))
+            prob = W.random_problem(rng, L, S, M, 2, cost_hi=400, comm_hi=50, mem_hi=30,
+                                    cap=int(rng.integers(60, 3000)), assign_rows=1)
+            n_comp = math.comb(L - 1, S - 1)
+            count = int(min(n_comp, rng.integers(1, 9000)))
+            for first in {0, int(rng.integers(0, n_comp - count + 1)), n_comp - count}:
+                check_against_oracle(prob, W.Candidates(first=first, count=count), dev)
+
+
 # ------------------------------------------------------ DP all-reduce
 
 def _with_allreduce(rng, prob, hi=3000):
