@@ -522,12 +522,13 @@ __global__ __launch_bounds__(kBlock) void ilv_kernel(KParams p) {
         uint32_t T = ilv_end<S, N, AR>(p, tab, X, cut, tyd);
         if (!ok) T = 0xFFFFFFFFu;
         const bool write = active && (done_here || !ok);
-        if (write && p.makespan_out) p.makespan_out[gi] = T;
+        // outputs are read back only by the host or the argmin pass: stream them past the caches
+        if (write && p.makespan_out) __builtin_nontemporal_store(T, p.makespan_out + gi);
         if (p.feas_bits_out) {
             const unsigned long long bits = __ballot(feas);
             const uint32_t w0 = (gi - (threadIdx.x & 63)) >> 5, nwords = (uint32_t)p.nwords;
-            if ((threadIdx.x & 63) == 0 && w0 < nwords) p.feas_bits_out[w0] = (uint32_t)bits;
-            if ((threadIdx.x & 63) == 32 && w0 + 1 < nwords) p.feas_bits_out[w0 + 1] = (uint32_t)(bits >> 32);
+            if ((threadIdx.x & 63) == 0 && w0 < nwords) __builtin_nontemporal_store((uint32_t)bits, p.feas_bits_out + w0);
+            if ((threadIdx.x & 63) == 32 && w0 + 1 < nwords) __builtin_nontemporal_store((uint32_t)(bits >> 32), p.feas_bits_out + w0 + 1);
         }
         if (write) {
             const unsigned long long key = make_key(feas, T, gi);
@@ -592,7 +593,8 @@ __global__ __launch_bounds__(kBlock) void ilv_resume_kernel(KParams p, uint32_t 
         }
         const uint32_t T = ilv_end<S, N, AR>(p, tab, X, cut, tyd);
         if (active && settled) {
-            if (p.makespan_out) p.makespan_out[i] = T;
+            // scattered one-word writes: the nontemporal hint keeps them out of L2 write-allocate
+            if (p.makespan_out) __builtin_nontemporal_store(T, p.makespan_out + i);
             const unsigned long long key = make_key(feas, T, i);
             best = key < best ? key : best;
         }
