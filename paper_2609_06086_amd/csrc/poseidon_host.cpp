@@ -570,6 +570,11 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     } else {
         kp.assign_mode = pk::kAssignDigits;
         kp.magicT = (uint32_t)((1ull << 32) / T + 1);
+        // T^(ndev-1) <= A / T < 2^32, and it is at least 2 here (T >= 2, ndev >= 2)
+        uint64_t d = 1;
+        for (uint32_t s = 1; s < ndev; ++s) d *= T;
+        kp.s1_div = (uint32_t)d;
+        kp.s1_magic = d > 1 ? (uint32_t)((1ull << 32) / d + 1) : 0u;
     }
     // the evaluation kernels' digit table (base-T digits, T <= 4, one stage
     // per device): for r < T^4 the entry-block offsets of r's four digits,
@@ -880,7 +885,6 @@ int eval_chunks(poseidon_ctx *ctx, const poseidon_cands *cands, uint32_t *makesp
     kp.makespan_out = makespan_out;
     kp.feas_bits_out = feasible_bits_out;
     kp.nwords = (cands->count + 31) / 32;
-    const uint64_t words = (uint64_t)pk::code_words((int)ctx->S);
     kp.codes = codes;
     kp.ccap = ccap;
     if (kp.nlevels) {

@@ -574,7 +574,7 @@ __global__ __launch_bounds__(kBlock) void ilv_resume_kernel(KParams p, uint32_t 
         for (int k = 0; k < NW; ++k) w[k] = active ? qin.codes[k * qcap + q] : 0u;
 #pragma unroll
         for (int s = 0; s < NL; ++s) Z[s] = active ? qin.Y[s * qcap + q] : 0u;
-        const bool ok = unpack_cuts<S>(w, p.L, cut);
+        unpack_cuts<S>(w, p.L, cut);   // (a queued entry's codes were valid when it was queued)
         const uint32_t a = !active ? 0u : p.qasg ? qin.asg[q] : assign_of(p, i);
         const bool feas = ilv_weights<S, N>(p, tab, cut, a, tyd, F, B);
         // dead registers are written before any read, so zero is as good as any value

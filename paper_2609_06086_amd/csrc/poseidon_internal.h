@@ -36,6 +36,8 @@ struct KParams {
     uint64_t A, n_comp;
     uint32_t L, S, M, T, NB, nslots;
     uint32_t magicT, assign_mode;
+    uint32_t s1_div, s1_magic;    // base-T assignment digits: T^(S-1) and floor(2^32 / T^(S-1)) + 1,
+                                  // so that stage 1's type (the top digit) is one multiply-high
     uint32_t wide;
     uint32_t cf[kSMax], cb[kSMax];
     uint32_t has_ar;              // the problem has DP all-reduce times

@@ -1128,21 +1128,31 @@ __host__ __device__ constexpr int narrow_cols() {
     return sizeof(R) == 8 ? (S < 5 ? S : 5) : 0;
 }
 
-// LDS image of the Pascal columns: columns NN..S-1 as R, in order then in
-// tree order, followed by columns 0..NN-1 as uint32 the same way (NN =
-// narrow_cols), 2^H entries per column.
-template <int S, typename R, int H>
+// LDS image of Pascal columns C0 .. C1, the ones a kernel searches (cut j
+// searches column S - j, so no search reads columns 0 and 1): the wide
+// columns among them (NN and up, NN = narrow_cols) as R, in order then in
+// tree order, followed by the narrow ones as uint32 the same way, 2^H
+// entries per column.
+template <int S, typename R, int H, int C0 = 2, int C1 = S - 1>
 struct Pascal {
     static constexpr uint32_t NH = 1u << H;
     static constexpr int NN = narrow_cols<S, R>();
-    const R *ws, *wt;                 // wide columns (sorted, tree), column c at (c - NN) * NH
-    const uint32_t *ns, *nt;          // narrow columns, column c at c * NH
+    static constexpr int WL = C0 > NN ? C0 : NN;              // first wide column held
+    static constexpr int NWC = C1 >= WL ? C1 - WL + 1 : 0;   // wide columns held
+    static constexpr int NHI = C1 < NN - 1 ? C1 : NN - 1;    // last narrow column held
+    static constexpr int NNC = NHI >= C0 ? NHI - C0 + 1 : 0; // narrow columns held
+    const R *ws, *wt;                 // wide columns (sorted, tree), column c at (c - WL) * NH
+    const uint32_t *ns, *nt;          // narrow columns, column c at (c - C0) * NH
     __device__ __forceinline__ explicit Pascal(const void *base) {
         ws = reinterpret_cast<const R *>(base);
-        wt = ws + (uint32_t)(S - NN) * NH;
-        ns = reinterpret_cast<const uint32_t *>(wt + (uint32_t)(S - NN) * NH);
-        nt = ns + (uint32_t)NN * NH;
+        wt = ws + (uint32_t)NWC * NH;
+        ns = reinterpret_cast<const uint32_t *>(wt + (uint32_t)NWC * NH);
+        nt = ns + (uint32_t)NNC * NH;
     }
+    __device__ __forceinline__ const R *wcol(int c) const { return ws + (uint32_t)(c - WL) * NH; }
+    __device__ __forceinline__ const R *wtree(int c) const { return wt + (uint32_t)(c - WL) * NH; }
+    __device__ __forceinline__ const uint32_t *ncol(int c) const { return ns + (uint32_t)(c - C0) * NH; }
+    __device__ __forceinline__ const uint32_t *ntree(int c) const { return nt + (uint32_t)(c - C0) * NH; }
 };
 
 // One cut's search for kIlp candidates over a column of type V (R or
@@ -1173,13 +1183,12 @@ __device__ __forceinline__ void search_cut(const KParams &p, const V *col, const
     }
 }
 
-template <int S, typename R, int H>
-__device__ __forceinline__ void decode_ilp(const KParams &p, const Pascal<S, R, H> &pc, uint32_t base,
+template <int S, typename R, int H, typename PC>
+__device__ __forceinline__ void decode_ilp(const KParams &p, const PC &pc, uint32_t base,
                                            uint32_t stride, bool (&act)[kIlp], bool (&ok)[kIlp],
                                            uint32_t (&asg)[kIlp], uint32_t (&w)[kIlp][Codes<S>::kWords]) {
     constexpr int NW = Codes<S>::kWords;
-    constexpr uint32_t NH = 1u << H;
-    constexpr int NN = Pascal<S, R, H>::NN;
+    constexpr int NN = PC::NN;
     R r[kIlp];
     uint32_t at[kIlp];
 #pragma unroll
@@ -1198,8 +1207,8 @@ __device__ __forceinline__ void decode_ilp(const KParams &p, const Pascal<S, R, 
     for (int j = 1; j <= S - 2; ++j) {
         const int c = S - j;
         uint32_t cut[kIlp];
-        if (c < NN) search_cut<uint32_t, R, H>(p, pc.ns + (uint32_t)c * NH, pc.nt + (uint32_t)c * NH, r, at, cut);
-        else search_cut<R, R, H>(p, pc.ws + (uint32_t)(c - NN) * NH, pc.wt + (uint32_t)(c - NN) * NH, r, at, cut);
+        if (c < NN) search_cut<uint32_t, R, H>(p, pc.ncol(c), pc.ntree(c), r, at, cut);
+        else search_cut<R, R, H>(p, pc.wcol(c), pc.wtree(c), r, at, cut);
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) w[u][(j - 1) / 4] |= cut[u] << (8 * ((j - 1) % 4));
     }
@@ -1220,18 +1229,17 @@ __device__ __forceinline__ void decode_ilp(const KParams &p, const Pascal<S, R, 
 // Searches of cuts J0+1 .. J1 (J1 <= S - 1) of kIlp candidates, from the
 // rank left r and the smallest value at of cut J0+1; cut J1 = S - 1, the
 // last, needs no search (with one cut left, C(n, 1) = n: c_{S-1} = a + r).
-template <int S, typename R, int H, int J0, int J1>
-__device__ __forceinline__ void decode_range(const KParams &p, const Pascal<S, R, H> &pc, R (&r)[kIlp],
+template <int S, typename R, int H, int J0, int J1, typename PC>
+__device__ __forceinline__ void decode_range(const KParams &p, const PC &pc, R (&r)[kIlp],
                                              uint32_t (&at)[kIlp], uint32_t (&cut)[kIlp][S + 1]) {
-    constexpr uint32_t NH = 1u << H;
-    constexpr int NN = Pascal<S, R, H>::NN;
+    constexpr int NN = PC::NN;
     constexpr int JS = J1 < S - 2 ? J1 : S - 2;   // cuts found by a search
 #pragma unroll
     for (int j = J0 + 1; j <= JS; ++j) {
         const int c = S - j;
         uint32_t cj[kIlp];
-        if (c < NN) search_cut<uint32_t, R, H>(p, pc.ns + (uint32_t)c * NH, pc.nt + (uint32_t)c * NH, r, at, cj);
-        else search_cut<R, R, H>(p, pc.ws + (uint32_t)(c - NN) * NH, pc.wt + (uint32_t)(c - NN) * NH, r, at, cj);
+        if (c < NN) search_cut<uint32_t, R, H>(p, pc.ncol(c), pc.ntree(c), r, at, cj);
+        else search_cut<R, R, H>(p, pc.wcol(c), pc.wtree(c), r, at, cj);
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) cut[u][j] = cj[u];
     }
@@ -1245,8 +1253,8 @@ __device__ __forceinline__ void decode_range(const KParams &p, const Pascal<S, R
 // (valid positions also for inactive lanes) into cut[u][0 .. J], with
 // c_0 = 0 and c_S = L; r and at are left as decode_range needs them to go
 // on.  Invalid (rank, assignment) pairs get ok = false.
-template <int S, typename R, int H, int J>
-__device__ __forceinline__ void decode_cuts(const KParams &p, const Pascal<S, R, H> &pc,
+template <int S, typename R, int H, int J, typename PC>
+__device__ __forceinline__ void decode_cuts(const KParams &p, const PC &pc,
                                             const uint32_t (&pos)[kIlp], const bool (&act)[kIlp],
                                             bool (&ok)[kIlp], uint32_t (&asg)[kIlp], R (&r)[kIlp],
                                             uint32_t (&at)[kIlp], uint32_t (&cut)[kIlp][S + 1]) {
@@ -1260,8 +1268,8 @@ __device__ __forceinline__ void decode_cuts(const KParams &p, const Pascal<S, R,
     decode_range<S, R, H, 0, J>(p, pc, r, at, cut);
 }
 
-template <int S, typename R, int H>
-__device__ __forceinline__ void decode_batch(const KParams &p, const Pascal<S, R, H> &pc, uint32_t base,
+template <int S, typename R, int H, typename PC>
+__device__ __forceinline__ void decode_batch(const KParams &p, const PC &pc, uint32_t base,
                                              uint32_t stride, bool &bad) {
     constexpr int NW = Codes<S>::kWords;
     bool act[kIlp], ok[kIlp];
@@ -1278,38 +1286,40 @@ __device__ __forceinline__ void decode_batch(const KParams &p, const Pascal<S, R
     }
 }
 
-// Columns 0 .. S-1 of the Pascal table, 2^H entries each, into LDS in order
-// and in tree order (layout of Pascal<S, R, H>); the tree node at depth l
-// and offset m probes sorted position (2m + 1) 2^(H-1-l) - 1 (entry 0 of
-// the tree is unused).  Narrow columns saturate at 2^32 - 1, which keeps
-// them sorted (no value of a column below 5 reaches it for n <= 255).
-template <int S, typename R, int H>
+// Columns C0 .. C1 of the Pascal table, 2^H entries each, into LDS in
+// order and in tree order (layout of Pascal<S, R, H, C0, C1>); the tree node
+// at depth l and offset m probes sorted position (2m + 1) 2^(H-1-l) - 1
+// (entry 0 of the tree is unused).  Narrow columns saturate at 2^32 - 1,
+// which keeps them sorted (no value of a column below 5 reaches it for
+// n <= 255).
+template <int S, typename R, int H, int C0 = 2, int C1 = S - 1>
 __device__ __forceinline__ void pascal_tables(const KParams &p, void *lds) {
-    constexpr uint32_t NH = 1u << H;
-    constexpr int NN = narrow_cols<S, R>();
-    R *ws = reinterpret_cast<R *>(lds), *wt = ws + (uint32_t)(S - NN) * NH;
-    uint32_t *ns = reinterpret_cast<uint32_t *>(wt + (uint32_t)(S - NN) * NH), *nt = ns + (uint32_t)NN * NH;
+    using PC = Pascal<S, R, H, C0, C1>;
+    constexpr uint32_t NH = PC::NH, NC = C1 >= C0 ? (uint32_t)(C1 - C0 + 1) : 0u;
+    R *ws = reinterpret_cast<R *>(lds), *wt = ws + (uint32_t)PC::NWC * NH;
+    uint32_t *ns = reinterpret_cast<uint32_t *>(wt + (uint32_t)PC::NWC * NH), *nt = ns + (uint32_t)PC::NNC * NH;
     const R *gb = reinterpret_cast<const R *>(p.binom);
-    for (uint32_t e = threadIdx.x; e < (uint32_t)S * NH; e += kBlock) {
-        const uint32_t k = e / NH, i = e % NH;
+    for (uint32_t e = threadIdx.x; e < NC * NH; e += kBlock) {
+        const uint32_t k = C0 + e / NH, i = e % NH;
         const uint32_t l = i ? 31u - __clz(i) : 0u, m = i - (1u << l);
         const R vs = gb[k * kNB + i];
         const R vt = i ? gb[k * kNB + (2 * m + 1) * (NH >> (l + 1)) - 1] : (R)0;
-        if ((int)k >= NN) {
-            ws[(k - NN) * NH + i] = vs;
-            wt[(k - NN) * NH + i] = vt;
+        if ((int)k >= PC::NN) {
+            ws[(k - PC::WL) * NH + i] = vs;
+            wt[(k - PC::WL) * NH + i] = vt;
         } else {
-            ns[k * NH + i] = vs > (R)0xFFFFFFFFu ? 0xFFFFFFFFu : (uint32_t)vs;
-            nt[k * NH + i] = vt > (R)0xFFFFFFFFu ? 0xFFFFFFFFu : (uint32_t)vt;
+            ns[(k - C0) * NH + i] = vs > (R)0xFFFFFFFFu ? 0xFFFFFFFFu : (uint32_t)vs;
+            nt[(k - C0) * NH + i] = vt > (R)0xFFFFFFFFu ? 0xFFFFFFFFu : (uint32_t)vt;
         }
     }
 }
 
-// LDS bytes of both copies of the S Pascal columns
-template <int S, typename R>
+// LDS bytes of both copies of Pascal columns C0 .. C1 (the column counts do
+// not depend on H)
+template <int S, typename R, int C0 = 2, int C1 = S - 1>
 __host__ __device__ constexpr size_t pascal_bytes(uint32_t L) {
-    return 2 * ((size_t)1 << decode_levels(L)) * ((size_t)(S - narrow_cols<S, R>()) * sizeof(R) +
-                                                  (size_t)narrow_cols<S, R>() * 4);
+    using PC = Pascal<S, R, 5, C0, C1>;
+    return 2 * ((size_t)1 << decode_levels(L)) * ((size_t)PC::NWC * sizeof(R) + (size_t)PC::NNC * 4);
 }
 
 // Range mode with one assignment: candidate i of the chunk is composition
@@ -1335,12 +1345,11 @@ __device__ __forceinline__ void next_cuts(uint32_t L, uint32_t (&c)[S + 1]) {
     for (int m = 1; m <= S - 1; ++m) c[m] = (uint32_t)m < js ? c[m] : b + m;
 }
 
-template <int S, typename R, int H>
-__device__ __forceinline__ void decode_succ(const KParams &p, const Pascal<S, R, H> &pc, uint32_t base, bool &bad) {
+template <int S, typename R, int H, typename PC>
+__device__ __forceinline__ void decode_succ(const KParams &p, const PC &pc, uint32_t base, bool &bad) {
     static_assert(kIlp == 4, "one 16-byte store per code word");
     constexpr int NW = Codes<S>::kWords;
-    constexpr uint32_t NH = 1u << H;
-    constexpr int NN = Pascal<S, R, H>::NN;
+    constexpr int NN = PC::NN;
     const uint64_t rank0 = p.first + (uint32_t)p.first_i + base;
     R r[1] = {(R)(rank0 < p.n_comp ? rank0 : 0)};
     uint32_t at[1] = {1u}, c[S + 1];
@@ -1351,9 +1360,9 @@ __device__ __forceinline__ void decode_succ(const KParams &p, const Pascal<S, R,
         const int col = S - j;
         uint32_t cj[1];
         if (col < NN)
-            search_cut<uint32_t, R, H, 1>(p, pc.ns + (uint32_t)col * NH, pc.nt + (uint32_t)col * NH, r, at, cj);
+            search_cut<uint32_t, R, H, 1>(p, pc.ncol(col), pc.ntree(col), r, at, cj);
         else
-            search_cut<R, R, H, 1>(p, pc.ws + (uint32_t)(col - NN) * NH, pc.wt + (uint32_t)(col - NN) * NH, r, at, cj);
+            search_cut<R, R, H, 1>(p, pc.wcol(col), pc.wtree(col), r, at, cj);
         c[j] = cj[0];
     }
     if (S >= 2) c[S - 1] = at[0] + (uint32_t)r[0];
@@ -1575,7 +1584,7 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
         for (int k = 0; k < NW; ++k) w[k] = active ? qin.codes[k * qcap + q] : 0u;
 #pragma unroll
         for (int s = 0; s < NX; ++s) X[s] = active ? qin.Y[s * qcap + q] : 0u;
-        const bool ok = unpack_cuts<S>(w, p.L, cut);
+        unpack_cuts<S>(w, p.L, cut);   // (a queued entry's codes were valid when it was queued)
         const uint32_t a = !active ? 0u : p.qasg ? qin.asg[q] : assign_of(p, i);
         decode_toff<S>(p, tab, a, to);
         const bool feas = stage_weights<S>(p, tab, cut, to, F, B);
@@ -1637,6 +1646,13 @@ __global__ __launch_bounds__(kBlock) void resume_kernel(KParams p, uint32_t lvl)
 enum FilterMode { kFilterFull = 0, kFilterPrefix = 1, kFilterGather = 2 };
 template <int S>
 __host__ __device__ constexpr int filter_prefix() { return S >= 4 ? S / 2 : 0; }
+// Pascal columns a mode searches: the prefix mode cuts 1 .. X (columns
+// S-X .. S-1), the gather mode the cuts after them (columns 2 .. S-X-1), the
+// full mode every cut (columns 2 .. S-1)
+template <int S, int MODE>
+__host__ __device__ constexpr int filter_col_lo() { return MODE == kFilterPrefix ? S - filter_prefix<S>() : 2; }
+template <int S, int MODE>
+__host__ __device__ constexpr int filter_col_hi() { return MODE == kFilterGather ? S - filter_prefix<S>() - 1 : S - 1; }
 
 // The prefix list, arrays of ccap entries: call position, rank left (low
 // and high words), assignment index, then the first X cuts as cut codes.
@@ -1648,17 +1664,239 @@ struct AList {
           w(p.alist + 4 * p.ccap) {}
 };
 
-template <int S, typename R, int H, bool AR, int MODE>
-__device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const Ent &tab, uint32_t b,
-                                           unsigned int *nq, uint32_t &n_keep, uint32_t &n_pruned,
-                                           uint32_t &n_infeas, bool &bad) {
+// Stage-1 screen of the prefix mode.  Stage 1 = [0, c_1) on type t fits its
+// memory iff c_1 <= hm_t(0), and g(S_1) = M (F_1 + B_1) + d_1 only grows
+// with c_1, so it passes Eq. 2 iff c_1 <= hb_t, the largest end point with
+// g(S_1) <= b.  Ranks are lexicographic with c_1 the most significant cut,
+// so the compositions with c_1 <= h hold the ranks below
+//   N(h) = C(L-1, S-1) - C(L-1-h, S-1)
+// (the others have all S-1 cuts in h+1 .. L-1).  A candidate therefore
+// fails stage 1 iff its rank is at least N(min(hm_t, hb_t)), and fails it on
+// memory (tested first at a stage) iff its rank is at least N(hm_t): one
+// compare decides it before any cut is decoded.  thr[2t], thr[2t+1] = those
+// two limits for every type t (threads t < T; the caller's barrier
+// publishes them).
+constexpr uint32_t kScreenTypes = 8;   // device types (POSEIDON_T_MAX)
+template <int S, typename R>
+__device__ __forceinline__ void stage1_limits(const KParams &p, const Ent &tab, uint32_t b, unsigned long long *thr) {
+    if (threadIdx.x >= p.T) return;
+    const uint32_t to = threadIdx.x * p.erow, L = p.L, hmax = L - S + 1;   // hmax: the largest c_1
+    const uint32_t pf0 = ent<kEPf>(tab, 0, to), pb0 = ent<kEPb>(tab, 0, to);
+    const uint32_t pd0 = p.has_ar ? ent<kEPd>(tab, 0, to) : 0u;
+    // g(S_1) is nondecreasing in c_1: the largest passing end point by halving
+    // steps (hb = 0: none passes; every c_1 is at least 1)
+    uint32_t hb = 0;
+    for (uint32_t st = 128; st; st >>= 1) {
+        const uint32_t c = hb + st;
+        if (c <= hmax) {
+            const uint32_t F = ent<kEPf>(tab, c, to) - pf0, B = ent<kEPb>(tab, c, to) - pb0;
+            const uint32_t D = p.has_ar ? ent<kEPd>(tab, c, to) - pd0 : 0u;
+            // M (F + B) + d_1 is an Eq. 2 value, below 2^31 like every path weight
+            if (p.M * (F + B) + D <= b) hb = c;
+        }
+    }
+    const uint32_t hm = min(ent<kEHm>(tab, 0, to), hmax), h1 = min(hb, hm);
+    const R *bin = reinterpret_cast<const R *>(p.binom);
+    thr[2 * threadIdx.x] = p.n_comp - (uint64_t)bin[(S - 1) * kNB + (L - 1 - h1)];
+    thr[2 * threadIdx.x + 1] = p.n_comp - (uint64_t)bin[(S - 1) * kNB + (L - 1 - hm)];
+}
+
+// Type of stage 1 of assignment a (valid a).
+template <int S>
+__device__ __forceinline__ uint32_t first_stage_type(const KParams &p, uint32_t a) {
+    if (p.assign_mode == kAssignFixed) return p.fixed_types[0];
+    if (p.assign_mode == kAssignTable) return p.assign[(uint64_t)a * S];
+    // the top base-T digit: floor(a / T^(S-1)), from a multiply-high that
+    // gives it or one more
+    uint32_t q = __umulhi(a, p.s1_magic);
+    if ((uint64_t)q * p.s1_div > a) q -= 1;
+    return q;
+}
+
+// LDS words that lanes of one wave wrote are visible to the wave's other
+// lanes after this (their writes complete; no code moves across it).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Buffered positions of one wave in the screened prefix mode: fewer than one
+// batch of kIlp * 64 before a screened tile of as many adds to it.
+constexpr uint32_t kScreenBuf = 2 * kIlp * 64;
+// The screen costs a second load of every kept candidate and the buffer's
+// bookkeeping, and saves the prefix work of the ones it discards.  It pays
+// when that work is large: five or more prefix cuts (S >= 10), or stage
+// tests with all-reduce terms (measured: 8 % faster at 16 stages, 6 % at 8
+// stages with all-reduce times, 3.5 % slower at 8 stages without).
+template <int S, bool AR, int MODE>
+__host__ __device__ constexpr bool filter_screens() {
+    return MODE == kFilterPrefix && (filter_prefix<S>() >= 5 || AR);
+}
+template <int S, bool AR, int MODE>
+__host__ __device__ constexpr size_t filter_static_lds() {
+    return filter_screens<S, AR, MODE>() ? (size_t)kScreenBuf * 4 * (kBlock / 64) + 16 * kScreenTypes : 0;
+}
+
+// The tests of kIlp decoded candidates of one lane (cuts 1 .. X of
+// filter_all's mode in cut[u]): classification, counts, and the list entry
+// of each candidate kept (the prefix list, or the survivor list).
+template <int S, typename R, bool AR, int MODE>
+__device__ __forceinline__ void filter_emit(const KParams &p, const Ent &tab, uint32_t b, unsigned int *nq,
+                                            const bool (&act)[kIlp], const bool (&ok)[kIlp],
+                                            const uint32_t (&pos)[kIlp], const uint32_t (&asg)[kIlp],
+                                            const R (&r)[kIlp], const uint32_t (&cut)[kIlp][S + 1],
+                                            uint32_t &n_keep, uint32_t &n_pruned, uint32_t &n_infeas, bool &bad) {
     constexpr int X0 = filter_prefix<S>();
     constexpr int X = MODE == kFilterPrefix ? X0 : S;   // stages decided, cuts 1 .. X decoded
     constexpr int NW = Codes<S>::kWords;
     constexpr int AW = (X0 + 3) / 4;                    // code words of the prefix cuts
-    const Pascal<S, R, H> pc(pas);
     const AList al(p);
     const unsigned int lane = threadIdx.x & 63;
+    const uint32_t seg = blockIdx.x * (uint32_t)p.seg_cap, ccap = (uint32_t)p.ccap;
+#pragma unroll
+    for (int u = 0; u < kIlp; ++u) {
+        uint32_t to[S];
+        decode_toff<S>(p, tab, ok[u] ? asg[u] : 0u, to);
+        const uint32_t cls = classify<S, AR, X>(p, tab, cut[u], to, b);
+        bool keep = false;
+        if (act[u]) {
+            if (!ok[u]) bad = true;
+            else if (cls == 1) ++n_infeas;
+            else if (cls == 2) ++n_pruned;
+            else keep = true;
+        }
+        const unsigned long long m = __ballot(keep);
+        if (m) {
+            unsigned int slot0 = 0;
+            if (lane == 0) slot0 = atomicAdd(nq, (unsigned int)__popcll(m));
+            slot0 = __shfl(slot0, 0, 64);
+            if (keep) {
+                const unsigned long long below = lane ? (m & ((1ull << lane) - 1ull)) : 0ull;
+                const uint32_t o = seg + slot0 + (uint32_t)__popcll(below);
+                if constexpr (MODE == kFilterPrefix) {
+                    uint32_t w[AW];
+#pragma unroll
+                    for (int k = 0; k < AW; ++k) w[k] = 0;
+#pragma unroll
+                    for (int j = 1; j <= X0; ++j) w[(j - 1) / 4] |= cut[u][j] << (8 * ((j - 1) % 4));
+                    al.pos[o] = pos[u];
+                    al.asg[o] = asg[u];
+                    al.rlo[o] = (uint32_t)r[u];
+                    if (sizeof(R) == 8) al.rhi[o] = (uint32_t)((uint64_t)r[u] >> 32);
+#pragma unroll
+                    for (int k = 0; k < AW; ++k) al.w[k * ccap + o] = w[k];
+                } else {
+                    uint32_t w[NW];
+                    pack_cuts<S>(cut[u], true, w);
+                    p.sidx[o] = pos[u];
+#pragma unroll
+                    for (int k = 0; k < NW; ++k) p.codes[k * ccap + o] = w[k];
+                }
+            }
+            if (MODE != kFilterPrefix) n_keep += lane == 0 ? (uint32_t)__popcll(m) : 0u;
+        }
+    }
+}
+
+// Prefix mode: each wave screens tiles of kIlp * 64 consecutive candidates
+// of the piece (its stream: tiles gw, gw + nwave, ...) on stage 1 alone
+// (stage1_limits), keeps the positions of the rest in its LDS buffer buf,
+// and decodes and tests them kIlp * 64 at a time, so that the searches of
+// the first cuts run only for candidates that pass stage 1 (about two in
+// three on the workloads here) and every lane has a candidate to decode.
+template <int S, typename R, int H, bool AR, typename PC>
+__device__ __forceinline__ void filter_screened(const KParams &p, const PC &pc, const Ent &tab,
+                                                uint32_t b, unsigned int *nq, uint32_t *buf,
+                                                const unsigned long long *thr, uint32_t &n_keep,
+                                                uint32_t &n_pruned, uint32_t &n_infeas, bool &bad) {
+    constexpr int X0 = filter_prefix<S>();
+    constexpr uint32_t kTile = kIlp * 64;
+    const unsigned int lane = threadIdx.x & 63;
+    const unsigned long long below = lane ? (~0ull >> (64 - lane)) : 0ull;
+    // 32-bit positions: a piece holds at most 2^26 candidates, a call fewer than 2^32
+    const uint32_t n = (uint32_t)p.n_i, first_i = (uint32_t)p.first_i;
+    const uint32_t nwave = gridDim.x * (kBlock / 64);
+    uint32_t tile = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);   // next tile of the stream
+    uint32_t cnt = 0;                                                  // positions in buf
+    for (;;) {
+        // screen tiles until a batch is buffered or the stream ends
+        while (cnt < kTile && tile * kTile < n) {
+            const uint32_t t0 = tile * kTile;
+            tile += nwave;
+            bool keep[kIlp];
+#pragma unroll
+            for (int u = 0; u < kIlp; ++u) {
+                const uint32_t i = t0 + (uint32_t)u * 64 + lane;
+                keep[u] = false;
+                if (i < n) {
+                    R r;
+                    uint32_t a;
+                    if (!candidate<R>(p, first_i + i, r, a)) {
+                        keep[u] = true;   // out of range: the batch raises the error flag
+                    } else {
+                        const uint32_t t = first_stage_type<S>(p, a);
+                        const uint64_t rk = (uint64_t)r;
+                        if (rk < thr[2 * t]) keep[u] = true;
+                        else if (rk >= thr[2 * t + 1]) ++n_infeas;
+                        else ++n_pruned;
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kIlp; ++u) {
+                const unsigned long long m = __ballot(keep[u]);
+                if (keep[u]) buf[cnt + (uint32_t)__popcll(m & below)] = t0 + (uint32_t)u * 64 + lane;
+                cnt += (uint32_t)__popcll(m);
+            }
+        }
+        if (cnt == 0) break;
+        wave_lds_sync();
+        const uint32_t nb = cnt < kTile ? cnt : kTile;
+        bool act[kIlp], ok[kIlp];
+        uint32_t pos[kIlp], asg[kIlp], at[kIlp], cut[kIlp][S + 1];
+        R r[kIlp];
+#pragma unroll
+        for (int u = 0; u < kIlp; ++u) {
+            const uint32_t j = (uint32_t)u * 64 + lane;
+            act[u] = j < nb;
+            pos[u] = first_i + (act[u] ? buf[j] : 0u);   // (position 0 of the piece for idle lanes)
+        }
+        decode_cuts<S, R, H, X0>(p, pc, pos, act, ok, asg, r, at, cut);
+        filter_emit<S, R, AR, kFilterPrefix>(p, tab, b, nq, act, ok, pos, asg, r, cut, n_keep, n_pruned, n_infeas, bad);
+        // the positions past the batch (fewer than kTile) move to the front
+        if (cnt > kTile) {
+            uint32_t v[kIlp];
+#pragma unroll
+            for (int u = 0; u < kIlp; ++u) {
+                const uint32_t j = kTile + (uint32_t)u * 64 + lane;
+                v[u] = j < cnt ? buf[j] : 0u;
+            }
+            wave_lds_sync();
+#pragma unroll
+            for (int u = 0; u < kIlp; ++u) {
+                const uint32_t j = (uint32_t)u * 64 + lane;
+                if (kTile + j < cnt) buf[j] = v[u];
+            }
+        }
+        cnt -= nb;
+        wave_lds_sync();
+    }
+}
+
+template <int S, typename R, int H, bool AR, int MODE>
+__device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const Ent &tab, uint32_t b,
+                                           unsigned int *nq, uint32_t *buf, const unsigned long long *thr,
+                                           uint32_t &n_keep, uint32_t &n_pruned, uint32_t &n_infeas, bool &bad) {
+    constexpr int X0 = filter_prefix<S>();
+    constexpr int NW = Codes<S>::kWords;
+    constexpr int AW = (X0 + 3) / 4;                    // code words of the prefix cuts
+    const Pascal<S, R, H, filter_col_lo<S, MODE>(), filter_col_hi<S, MODE>()> pc(pas);
+    if constexpr (filter_screens<S, AR, MODE>()) {
+        filter_screened<S, R, H, AR>(p, pc, tab, b, nq, buf, thr, n_keep, n_pruned, n_infeas, bad);
+        return;
+    }
+    const AList al(p);
     // 32-bit positions and word offsets: a piece holds at most 2^26
     // candidates, a call fewer than 2^32, and each list fewer than 2^32
     // words (fewer scalar registers than 64-bit ones)
@@ -1699,53 +1937,11 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
             for (int u = 0; u < kIlp; ++u) {
                 const uint32_t i = base + u * stride;
                 act[u] = i < n;
-                pos[u] = first_i + (act[u] ? i : 0);
+                pos[u] = first_i + (act[u] ? i : 0u);
             }
             decode_cuts<S, R, H, MODE == kFilterPrefix ? X0 : S - 1>(p, pc, pos, act, ok, asg, r, at, cut);
         }
-#pragma unroll
-        for (int u = 0; u < kIlp; ++u) {
-            uint32_t to[S];
-            decode_toff<S>(p, tab, ok[u] ? asg[u] : 0u, to);
-            const uint32_t cls = classify<S, AR, X>(p, tab, cut[u], to, b);
-            bool keep = false;
-            if (act[u]) {
-                if (!ok[u]) bad = true;
-                else if (cls == 1) ++n_infeas;
-                else if (cls == 2) ++n_pruned;
-                else keep = true;
-            }
-            const unsigned long long m = __ballot(keep);
-            if (m) {
-                unsigned int slot0 = 0;
-                if (lane == 0) slot0 = atomicAdd(nq, (unsigned int)__popcll(m));
-                slot0 = __shfl(slot0, 0, 64);
-                if (keep) {
-                    const unsigned long long below = lane ? (m & ((1ull << lane) - 1ull)) : 0ull;
-                    const uint32_t o = seg + slot0 + (uint32_t)__popcll(below);
-                    if constexpr (MODE == kFilterPrefix) {
-                        uint32_t w[AW];
-#pragma unroll
-                        for (int k = 0; k < AW; ++k) w[k] = 0;
-#pragma unroll
-                        for (int j = 1; j <= X0; ++j) w[(j - 1) / 4] |= cut[u][j] << (8 * ((j - 1) % 4));
-                        al.pos[o] = pos[u];
-                        al.asg[o] = asg[u];
-                        al.rlo[o] = (uint32_t)r[u];
-                        if (sizeof(R) == 8) al.rhi[o] = (uint32_t)((uint64_t)r[u] >> 32);
-#pragma unroll
-                        for (int k = 0; k < AW; ++k) al.w[k * ccap + o] = w[k];
-                    } else {
-                        uint32_t w[NW];
-                        pack_cuts<S>(cut[u], true, w);
-                        p.sidx[o] = pos[u];
-#pragma unroll
-                        for (int k = 0; k < NW; ++k) p.codes[k * ccap + o] = w[k];
-                    }
-                }
-                if (MODE != kFilterPrefix) n_keep += lane == 0 ? (uint32_t)__popcll(m) : 0u;
-            }
-        }
+        filter_emit<S, R, AR, MODE>(p, tab, b, nq, act, ok, pos, asg, r, cut, n_keep, n_pruned, n_infeas, bad);
     }
 }
 
@@ -1774,11 +1970,22 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(KParams p) {
     bool bad = false;
     __shared__ unsigned int nq;
     if (threadIdx.x == 0) nq = 0;
+    // prefix mode: the waves' position buffers and the stage-1 rank limits
+    // (published by the barrier after the Pascal columns)
+    uint32_t *buf = nullptr;
+    const unsigned long long *thr = nullptr;
+    if constexpr (filter_screens<S, AR, MODE>()) {
+        __shared__ uint32_t screen_buf[kScreenBuf * (kBlock / 64)];
+        __shared__ unsigned long long screen_thr[2 * kScreenTypes];
+        stage1_limits<S, R>(p, tab, b, screen_thr);
+        buf = screen_buf + (threadIdx.x >> 6) * kScreenBuf;
+        thr = screen_thr;
+    }
     switch (H) {
-    case 8: pascal_tables<S, R, 8>(p, pas); __syncthreads(); filter_all<S, R, 8, AR, MODE>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
-    case 7: pascal_tables<S, R, 7>(p, pas); __syncthreads(); filter_all<S, R, 7, AR, MODE>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
-    case 6: pascal_tables<S, R, 6>(p, pas); __syncthreads(); filter_all<S, R, 6, AR, MODE>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
-    default: pascal_tables<S, R, 5>(p, pas); __syncthreads(); filter_all<S, R, 5, AR, MODE>(p, pas, tab, b, &nq, n_keep, n_pruned, n_infeas, bad); break;
+    case 8: pascal_tables<S, R, 8, filter_col_lo<S, MODE>(), filter_col_hi<S, MODE>()>(p, pas); __syncthreads(); filter_all<S, R, 8, AR, MODE>(p, pas, tab, b, &nq, buf, thr, n_keep, n_pruned, n_infeas, bad); break;
+    case 7: pascal_tables<S, R, 7, filter_col_lo<S, MODE>(), filter_col_hi<S, MODE>()>(p, pas); __syncthreads(); filter_all<S, R, 7, AR, MODE>(p, pas, tab, b, &nq, buf, thr, n_keep, n_pruned, n_infeas, bad); break;
+    case 6: pascal_tables<S, R, 6, filter_col_lo<S, MODE>(), filter_col_hi<S, MODE>()>(p, pas); __syncthreads(); filter_all<S, R, 6, AR, MODE>(p, pas, tab, b, &nq, buf, thr, n_keep, n_pruned, n_infeas, bad); break;
+    default: pascal_tables<S, R, 5, filter_col_lo<S, MODE>(), filter_col_hi<S, MODE>()>(p, pas); __syncthreads(); filter_all<S, R, 5, AR, MODE>(p, pas, tab, b, &nq, buf, thr, n_keep, n_pruned, n_infeas, bad); break;
     }
     // per-block sums, one global atomic per counter and block
     const unsigned long long sk = wave_sum_u32(n_keep), sp = wave_sum_u32(n_pruned), si = wave_sum_u32(n_infeas);
@@ -1870,7 +2077,7 @@ hipError_t launch_eval_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) 
 
 template <int S, typename R>
 hipError_t launch_decode_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
-    const size_t lds = pascal_bytes<S, R>(p.L);
+    const size_t lds = pascal_bytes<S, R>(p.L);   // (columns 2 .. S-1)
     hipLaunchKernelGGL((decode_kernel<S, R>), dim3(lc.grid), dim3(kBlock), lds, st, p);
     return hipGetLastError();
 }
@@ -1895,9 +2102,10 @@ constexpr size_t kLdsBlockMax = 64 * 1024;   // LDS bytes one block of these ker
 
 template <int S, typename R, int MODE>
 hipError_t launch_filter_s(const KParams &p, const LaunchCfg &lc, hipStream_t st) {
-    const size_t pas = pascal_bytes<S, R>(p.L);
+    const size_t pas = pascal_bytes<S, R, filter_col_lo<S, MODE>(), filter_col_hi<S, MODE>()>(p.L);
+    const size_t fixed = p.has_ar ? filter_static_lds<S, true, MODE>() : filter_static_lds<S, false, MODE>();
     const dim3 fg(lc.grid), fb(kBlock);
-    if (pas + lc.lds_bytes > kLdsBlockMax) {
+    if (pas + lc.lds_bytes + fixed > kLdsBlockMax) {
         if (p.has_ar) hipLaunchKernelGGL((filter_kernel<S, R, true, true, MODE>), fg, fb, pas, st, p);
         else hipLaunchKernelGGL((filter_kernel<S, R, false, true, MODE>), fg, fb, pas, st, p);
     } else {
@@ -1936,8 +2144,9 @@ hipError_t launch_bounded_s(const KParams &p, const LaunchCfg &lc, hipStream_t s
 // blocks, one per segment of the first's list, in one wave too.
 template <int S, typename R, int MODE>
 hipError_t filter_occupancy_mode(const KParams &p, size_t ent_lds, int *blocks) {
-    const size_t pas = pascal_bytes<S, R>(p.L);
-    if (pas + ent_lds > kLdsBlockMax) {
+    const size_t pas = pascal_bytes<S, R, filter_col_lo<S, MODE>(), filter_col_hi<S, MODE>()>(p.L);
+    const size_t fixed = p.has_ar ? filter_static_lds<S, true, MODE>() : filter_static_lds<S, false, MODE>();
+    if (pas + ent_lds + fixed > kLdsBlockMax) {
         if (p.has_ar) return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, true, true, MODE>, kBlock, pas);
         return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, filter_kernel<S, R, false, true, MODE>, kBlock, pas);
     }

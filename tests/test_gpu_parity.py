@@ -422,6 +422,57 @@ def test_bounded_workload4_prefix(dev):
         assert st.pruned > 0
 
 
+def test_bounded_stage1_screen(dev):
+    """Early stop where the prefix filter decides stage 1 from the
+    composition rank before decoding any cut (S >= 10, or all-reduce times):
+    base-T digit, table and fixed assignments, list and range mode, pieces
+    of 1, 255, 257 and several thousand candidates (a screened tile holds
+    256), three chunkings, caps and bounds under which many candidates fail
+    stage 1 on memory and many on Eq. 2.  Counts and argmin equal the
+    oracle's."""
+    rng = np.random.default_rng(151)
+    seen_mem = seen_bound = 0
+    for S, T, rows, ar in ((10, 2, None, False), (12, 3, None, False), (16, 2, None, False), (11, 3, 6, False),
+                           (16, 4, 1, False), (5, 3, None, True), (8, 2, 4, True)):
+        L = S + int(rng.integers(2, 50))
+        M = int(rng.integers(S, 3 * S + 1))
+        cap = int(40 * L / S * 0.9)   # stages well above the mean length exceed it
+        prob = W.random_problem(rng, L, S, M, T, cost_lo=20, cost_hi=400, mem_hi=40, cap=cap, assign_rows=rows)
+        if ar:
+            _with_allreduce(rng, prob, hi=2000)
+        total = prob.n_compositions * prob.A
+        sets = [W.random_candidates(rng, prob, n) for n in (1, 255, 257, 6000)]
+        n = min(5000, total)
+        sets.append(W.Candidates(first=int(rng.integers(0, total - n + 1)), count=n))
+        for cands in sets:
+            To, fo = coracle.evaluate(prob, cands)
+            ok = np.sort(To[fo])
+            bound = int(ok[len(ok) // 10]) if len(ok) else 2 ** 31 - 1
+            for chunk, ramp in ((0, False), (777, False), (64, True)):
+                _, st = bounded_vs_oracle(prob, cands, bound, chunk, dev, ramp)
+                seen_mem += st.infeasible
+                seen_bound += st.pruned
+    assert seen_mem > 0 and seen_bound > 0
+
+
+def test_bounded_stage1_screen_invalid_rank(dev):
+    """An out-of-range rank reaches the screened prefix filter's error flag
+    (it is kept for the decode, which reports it) and the context stays
+    usable."""
+    rng = np.random.default_rng(152)
+    prob = W.random_problem(rng, 30, 12, 20, 2, mem_hi=20)
+    cands = W.random_candidates(rng, prob, 1000)
+    bad = cands.comp_rank.copy()
+    bad[600] = prob.n_compositions
+    ctx = P.poseidon_load_costs(prob, 0)
+    d = to_dev(W.Candidates(comp_rank=bad, assign_idx=cands.assign_idx), dev)
+    with pytest.raises(P.PoseidonError) as ei:
+        P.poseidon_eval_candidates_bounded(ctx, 2 ** 31 - 1, **d)
+    assert ei.value.status == P.POSEIDON_E_INVAL
+    ctx.close()
+    bounded_vs_oracle(prob, cands, 2 ** 31 - 1, 0, dev)
+
+
 def test_bounded_bound_below_optimum(dev):
     wl = W.workload(2)
     To, fo = coracle.evaluate(wl.problem, wl.cands)
