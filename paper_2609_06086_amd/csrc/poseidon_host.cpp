@@ -496,6 +496,26 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
             }
         }
 
+    // bucket tables of the unranking searches: per column k, per key, the
+    // first row n < 2^H whose (stored) entry reaches the bucket's smallest
+    // value (at most 2^H - 1: no search sees a larger value); 64-bit keys for
+    // the wide columns of 64-bit ranks, 32-bit keys for the others
+    const uint32_t NHd = 1u << pk::decode_levels(L);
+    const uint32_t n_narrow = wide ? std::min<uint32_t>(S, 5) : 0;
+    std::vector<uint8_t> btab((size_t)S * pk::kBucketTab, 0);
+    for (uint32_t k = 0; k < S; ++k) {
+        const int w = (wide && k >= n_narrow) ? 64 : 32;
+        const unsigned __int128 vmax = w == 64 ? (unsigned __int128)UINT64_MAX : (unsigned __int128)0xFFFFFFFFu;
+        std::vector<unsigned __int128> col(NHd);
+        for (uint32_t n = 0; n < NHd; ++n) col[n] = std::min<unsigned __int128>(binom_sat(n, k), vmax);
+        for (int z = 0; z < w; ++z)
+            for (int m = 0; m < 16; ++m) {
+                const unsigned __int128 lo = pk::bucket_lo(w, z, m);
+                const uint32_t n = (uint32_t)(std::lower_bound(col.begin(), col.end(), lo) - col.begin());
+                btab[(size_t)k * pk::kBucketTab + 16 * z + m] = (uint8_t)std::min(n, NHd - 1);
+            }
+    }
+
     pk::KParams kp;
     memset(&kp, 0, sizeof(kp));
     kp.A = A;
@@ -611,6 +631,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
     const size_t o_pm = off; off = al(off + pm.size() * 4);
     const size_t o_cap = off; off = al(off + (size_t)T * 4);
     const size_t o_binom = off; off = al(off + binom.size());
+    const size_t o_btab = off; off = al(off + btab.size());
     const size_t o_assign = off; off = al(off + (has_table ? (size_t)A * ndev : 0));
     const size_t o_slots = off; off = al(off + (table_path ? masks.size() * 4 : 0));
     const size_t o_pd = off; off = al(off + pd.size() * 4);
@@ -636,7 +657,8 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
                   hipMemcpy(b + o_cost, cost.data(), cost.size() * 8, hipMemcpyHostToDevice) == hipSuccess &&
                   hipMemcpy(b + o_pm, pm.data(), pm.size() * 4, hipMemcpyHostToDevice) == hipSuccess &&
                   hipMemcpy(b + o_cap, p->cap_mb, (size_t)T * 4, hipMemcpyHostToDevice) == hipSuccess &&
-                  hipMemcpy(b + o_binom, binom.data(), binom.size(), hipMemcpyHostToDevice) == hipSuccess;
+                  hipMemcpy(b + o_binom, binom.data(), binom.size(), hipMemcpyHostToDevice) == hipSuccess &&
+                  hipMemcpy(b + o_btab, btab.data(), btab.size(), hipMemcpyHostToDevice) == hipSuccess;
         if (ok && has_table)
             ok = hipMemcpy(b + o_assign, p->assign, (size_t)A * ndev, hipMemcpyHostToDevice) == hipSuccess;
         if (ok && table_path)
@@ -648,6 +670,7 @@ int poseidon_load_costs(const poseidon_problem *p, int hip_device, poseidon_ctx 
         kp.pm = (const uint32_t *)(b + o_pm);
         kp.cap = (const uint32_t *)(b + o_cap);
         kp.binom = b + o_binom;
+        kp.btab = (const uint8_t *)(b + o_btab);
         kp.assign = has_table ? (const uint8_t *)(b + o_assign) : nullptr;
         kp.slot_mask = table_path ? (const uint32_t *)(b + o_slots) : nullptr;
         kp.pd = has_ar ? (const uint32_t *)(b + o_pd) : nullptr;

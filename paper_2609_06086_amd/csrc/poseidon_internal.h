@@ -8,6 +8,28 @@ namespace pk {
 
 constexpr int kSMax = 16;
 constexpr uint32_t kNB = 256;   // Pascal-table column length (n = 0..255; L <= 256)
+
+// Buckets of the unranking searches.  A value Q >= 1 of a w-bit type falls in
+// bucket (z, m): z its number of leading zeros in w bits, m the 4 bits after
+// its leading one (zero-filled when fewer follow it); key = 16 z + m.  The
+// bucket holds [bucket_lo(z, m), bucket_lo of the next key), the next key
+// being (z, m + 1), or (z - 1, 0) after m = 15; keys that no value has get
+// an empty range.  For each Pascal column the host tabulates, per key, the
+// first row whose entry reaches bucket_lo (kBucketTab bytes a column), so a
+// search starts there and needs only a few halvings.
+// Halvings of one cut search over a whole Pascal column: the smallest H with
+// L <= 2^H (at least 5); the columns hold rows n < 2^H.
+__host__ __device__ constexpr uint32_t decode_levels(uint32_t L) {
+    return L > 128 ? 8u : L > 64 ? 7u : L > 32 ? 6u : 5u;
+}
+
+constexpr uint32_t kBucketTab = 1024;   // 64 z values x 16 m values, one byte each
+__host__ __device__ constexpr unsigned __int128 bucket_lo(int w, int z, int m) {
+    // the smallest value whose leading one is bit e = w - 1 - z and whose next
+    // four bits are at least m
+    return (w - 1 - z) >= 4 ? (unsigned __int128)(16 + m) << ((w - 1 - z) - 4)
+                            : ((unsigned __int128)(16 + m) + ((1u << (4 - (w - 1 - z))) - 1)) >> (4 - (w - 1 - z));
+}
 constexpr int kMaxLevels = 6;   // cascade checkpoints of the steady loop
 constexpr uint32_t kSearchScanMax = 16384;   // blocks of one search level piece (search_scan_kernel's LDS)
 
@@ -20,6 +42,7 @@ struct KParams {
     const uint32_t *pm;        // [L+1] prefix memory
     const uint32_t *cap;       // [T]
     const void *binom;         // [S][kNB] C(n, k), uint32 or uint64 (wide)
+    const uint8_t *btab;       // [S][kBucketTab] per column: first row reaching each bucket
     const uint8_t *assign;     // [A][S] (table mode)
     const uint32_t *slot_mask; // [nslots][3] forward / deep-forward / backward stage masks
                                // ([nslots][4] under Interleaved 1F1B: + backward depths)

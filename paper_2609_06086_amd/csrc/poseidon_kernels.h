@@ -15,6 +15,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
 #include <utility>
 
 #include "poseidon_internal.h"
@@ -1091,22 +1092,16 @@ __device__ __forceinline__ void enqueue(const KParams &p, int which, unsigned in
 // raise the error flag.
 constexpr int kIlp = kDecodeIlp;
 
-// Halvings of one cut search: the smallest H with L <= 2^H (at least 5).
-__host__ __device__ constexpr uint32_t decode_levels(uint32_t L) {
-    return L > 128 ? 8u : L > 64 ? 7u : L > 32 ? 6u : 5u;
-}
-
-// kIlp candidates per lane, H halvings per search.  Each Pascal column is
-// held twice in LDS, 2^H entries each: in order (col) and in breadth-first
-// order of the search tree (ey: root at 1, children of i at 2i and 2i+1).
-// Halving b of the search probes one of 2^b neighbouring entries of ey, so
-// the lanes of a wave hit distinct banks; in sorted order those probes lie
-// 2^(H-b) entries apart and share banks.  After H steps the tree index i
-// spells the lower-bound position in its low H bits.  The last cut needs no
-// search: with one cut left, C(n, 1) = n, so c_{S-1} = a + r.
-// One halving of the tree search: t <- 2 t + (probe < Q), as a compare into
-// VCC and an add with carry-in (the compiler's select and shift-or take one
-// VALU operation more).
+// kIlp candidates per lane.  A kernel holds the Pascal columns it searches
+// in LDS, each sorted (2^H rows, then kBucketPad rows of the type's largest
+// value) and with the host's bucket table (per bucket key, the first row
+// whose entry reaches the bucket; the keys are defined with bucket_lo).  The
+// search for the smallest n with C(n, c) >= Q starts at the row Q's bucket
+// names and halves bucket_steps(w, H, c) times over the 2^steps rows after
+// it, which hold every row a value of that bucket can land on.  The last cut
+// needs no search: with one cut left, C(n, 1) = n, so c_{S-1} = a + r.
+// One halving: t <- 2 t + (probe < Q), as a compare into VCC and an add with
+// carry-in (the compiler's select and shift-or take one VALU operation more).
 __device__ __forceinline__ uint32_t tree_step(uint32_t t, uint64_t probe, uint64_t q) {
     asm("v_cmp_lt_u64_e32 vcc, %1, %2\n\tv_addc_co_u32_e32 %0, vcc, %0, %0, vcc"
                  : "+v"(t) : "v"(probe), "v"(q) : "vcc");
@@ -1118,6 +1113,61 @@ __device__ __forceinline__ uint32_t tree_step(uint32_t t, uint32_t probe, uint32
     return t;
 }
 
+// Bucket key of Q >= 1 (its leading zeros, then the 4 bits after its leading one).
+__device__ __forceinline__ uint32_t bucket_key(uint64_t q) {
+    const uint32_t z = (uint32_t)__clzll(q);
+    return 16u * z + ((uint32_t)((q << z) >> 59) & 15u);
+}
+__device__ __forceinline__ uint32_t bucket_key(uint32_t q) {
+    const uint32_t z = (uint32_t)__clz(q);
+    return 16u * z + (((q << z) >> 27) & 15u);
+}
+
+constexpr uint32_t kBucketPad = 8;   // rows past 2^H: a search reads at most 2^3 - 2 past its start
+constexpr int kBucketStepsMax = 3;
+
+// Halvings a search over column c needs after its bucket's start row: the
+// most rows the values of one bucket can land on (2^H rows of C(n, c),
+// w-bit entries saturated at the type's largest value, values up to the
+// column's last entry), as a power of two.  Evaluated at compile time.
+__host__ __device__ constexpr int bucket_steps(int w, int H, int c) {
+    const int NH = 1 << H;
+    const unsigned __int128 vmax = w == 64 ? (unsigned __int128)~0ull : (unsigned __int128)0xFFFFFFFFu;
+    unsigned __int128 col[256] = {};
+    unsigned __int128 v = c == 0 ? 1 : 0;   // C(n, c): 0 below n = c, then C(n-1, c) n / (n - c)
+    for (int n = 0; n < NH; ++n) {
+        if (n == c) v = 1;
+        else if (n > c) v = v * (unsigned)n / (unsigned)(n - c);
+        col[n] = v < vmax ? v : vmax;
+    }
+    const unsigned __int128 top = col[NH - 1];
+    int most = 1;
+    for (int z = 0; z < w; ++z)
+        for (int m = 0; m < 16; ++m) {
+            const unsigned __int128 lo = bucket_lo(w, z, m);
+            const unsigned __int128 nx = m < 15 ? bucket_lo(w, z, m + 1) : z > 0 ? bucket_lo(w, z - 1, 0) : vmax + 1;
+            const unsigned __int128 hi = nx < top + 1 ? nx : top + 1;   // the bucket's values a search sees: [lo, hi)
+            if (lo >= hi) continue;
+            int a = 0, b = 0;
+            for (int x = 0; x < 2; ++x) {   // first rows reaching lo and hi - 1
+                const unsigned __int128 t = x == 0 ? lo : hi - 1;
+                int l = 0, r = NH;
+                while (l < r) {
+                    const int mid = (l + r) / 2;
+                    if (col[mid] < t) l = mid + 1;
+                    else r = mid;
+                }
+                (x == 0 ? a : b) = l;
+            }
+            most = b - a + 1 > most ? b - a + 1 : most;
+        }
+    int h = 0;
+    while ((1 << h) < most) ++h;
+    return h;
+}
+static_assert(bucket_steps(64, 7, 2) == 2 && bucket_steps(64, 7, 15) == 1 && bucket_steps(32, 7, 3) == 2,
+              "bucket steps of the 7-level columns");
+
 // With 64-bit ranks the searches over columns 0 .. kNarrow-1 run in 32 bits:
 // C(n, k) < 2^32 for every n <= 255 and k <= 4, and at the search of a cut
 // whose column is k + 1 the remaining rank is below C(L - a, k + 1), so the
@@ -1128,58 +1178,80 @@ __host__ __device__ constexpr int narrow_cols() {
     return sizeof(R) == 8 ? (S < 5 ? S : 5) : 0;
 }
 
+// One cut's search for NI candidates over a column of type V (R or uint32)
+// with its bucket table: Q = C(L - a, k + 1) - r, the smallest n with
+// C(n, k + 1) >= Q, the rank left C(n, k + 1) - Q, the cut L - n.
+template <typename V, typename R, int HS, int NI>
+__device__ __forceinline__ void search_cut(const KParams &p, const V *col, const uint8_t *tab, R (&r)[NI],
+                                           uint32_t (&at)[NI], uint32_t (&cut)[NI]) {
+    static_assert(HS <= kBucketStepsMax, "a bucket spans at most 2^3 rows (the padding)");
+    V Q[NI];
+    uint32_t n0[NI], t[NI];
+#pragma unroll
+    for (int u = 0; u < NI; ++u) Q[u] = col[p.L - at[u]] - (V)r[u];
+#pragma unroll
+    for (int u = 0; u < NI; ++u) {
+        n0[u] = tab[bucket_key(Q[u])];
+        t[u] = 0;
+    }
+    // halving d probes the last row of the left half of rows
+    // [n0 + t 2^(HS-d), n0 + (t + 1) 2^(HS-d))
+#pragma unroll
+    for (int d = 0; d < HS; ++d) {
+#pragma unroll
+        for (int u = 0; u < NI; ++u)
+            t[u] = tree_step(t[u], col[n0[u] + (t[u] << (HS - d)) + (1u << (HS - 1 - d)) - 1u], Q[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < NI; ++u) {
+        const uint32_t n = n0[u] + t[u];
+        r[u] = (R)(col[n] - Q[u]);
+        cut[u] = p.L - n;
+        at[u] = cut[u] + 1;
+    }
+}
+
 // LDS image of Pascal columns C0 .. C1, the ones a kernel searches (cut j
 // searches column S - j, so no search reads columns 0 and 1): the wide
-// columns among them (NN and up, NN = narrow_cols) as R, in order then in
-// tree order, followed by the narrow ones as uint32 the same way, 2^H
-// entries per column.
+// columns among them (NN and up, NN = narrow_cols) as R, then the narrow ones
+// as uint32, NP rows each, then their bucket tables in column order.
 template <int S, typename R, int H, int C0 = 2, int C1 = S - 1>
 struct Pascal {
-    static constexpr uint32_t NH = 1u << H;
+    static constexpr uint32_t NH = 1u << H, NP = NH + kBucketPad;
     static constexpr int NN = narrow_cols<S, R>();
     static constexpr int WL = C0 > NN ? C0 : NN;              // first wide column held
     static constexpr int NWC = C1 >= WL ? C1 - WL + 1 : 0;   // wide columns held
     static constexpr int NHI = C1 < NN - 1 ? C1 : NN - 1;    // last narrow column held
     static constexpr int NNC = NHI >= C0 ? NHI - C0 + 1 : 0; // narrow columns held
-    const R *ws, *wt;                 // wide columns (sorted, tree), column c at (c - WL) * NH
-    const uint32_t *ns, *nt;          // narrow columns, column c at (c - C0) * NH
-    __device__ __forceinline__ explicit Pascal(const void *base) {
-        ws = reinterpret_cast<const R *>(base);
-        wt = ws + (uint32_t)NWC * NH;
-        ns = reinterpret_cast<const uint32_t *>(wt + (uint32_t)NWC * NH);
-        nt = ns + (uint32_t)NNC * NH;
+    static constexpr size_t kWideBytes = (size_t)NWC * NP * sizeof(R), kNarrowBytes = (size_t)NNC * NP * 4;
+    static constexpr size_t bytes() { return kWideBytes + kNarrowBytes + (size_t)(NWC + NNC) * kBucketTab; }
+    const unsigned char *base;
+    __device__ __forceinline__ explicit Pascal(const void *b) : base(reinterpret_cast<const unsigned char *>(b)) {}
+    template <int c>
+    __device__ __forceinline__ const auto *col() const {
+        if constexpr (c >= NN) return reinterpret_cast<const R *>(base + (size_t)(c - WL) * NP * sizeof(R));
+        else return reinterpret_cast<const uint32_t *>(base + kWideBytes + (size_t)(c - C0) * NP * 4);
     }
-    __device__ __forceinline__ const R *wcol(int c) const { return ws + (uint32_t)(c - WL) * NH; }
-    __device__ __forceinline__ const R *wtree(int c) const { return wt + (uint32_t)(c - WL) * NH; }
-    __device__ __forceinline__ const uint32_t *ncol(int c) const { return ns + (uint32_t)(c - C0) * NH; }
-    __device__ __forceinline__ const uint32_t *ntree(int c) const { return nt + (uint32_t)(c - C0) * NH; }
+    template <int c>
+    __device__ __forceinline__ const uint8_t *tab() const {
+        return base + kWideBytes + kNarrowBytes + (size_t)(c - C0) * kBucketTab;
+    }
+    // the search of a cut over column c, for NI candidates
+    template <int c, int NI>
+    __device__ __forceinline__ void search(const KParams &p, R (&r)[NI], uint32_t (&at)[NI], uint32_t (&cut)[NI]) const {
+        static_assert(c >= C0 && c <= C1, "column outside the window");
+        using V = typename std::conditional<(c >= NN), R, uint32_t>::type;
+        search_cut<V, R, bucket_steps(8 * (int)sizeof(V), H, c)>(p, col<c>(), tab<c>(), r, at, cut);
+    }
 };
 
-// One cut's search for kIlp candidates over a column of type V (R or
-// uint32): Q = C(L - a, k + 1) - r, the smallest n with C(n, k + 1) >= Q by
-// the tree, the rank left C(n, k + 1) - Q, the cut L - n.
-template <typename V, typename R, int H, int NI = kIlp>
-__device__ __forceinline__ void search_cut(const KParams &p, const V *col, const V *tree, R (&r)[NI],
-                                           uint32_t (&at)[NI], uint32_t (&cut)[NI]) {
-    constexpr uint32_t NH = 1u << H;
-    V Q[NI];
-    uint32_t t[NI];   // tree node
-#pragma unroll
-    for (int u = 0; u < NI; ++u) {
-        Q[u] = col[p.L - at[u]] - (V)r[u];
-        t[u] = 1;
-    }
-#pragma unroll
-    for (int b = 0; b < H; ++b) {
-#pragma unroll
-        for (int u = 0; u < NI; ++u) t[u] = tree_step(t[u], tree[t[u]], Q[u]);
-    }
-#pragma unroll
-    for (int u = 0; u < NI; ++u) {
-        const uint32_t pos = t[u] - NH;
-        r[u] = (R)(col[pos] - Q[u]);
-        cut[u] = p.L - pos;
-        at[u] = cut[u] + 1;
+// f(integral_constant<int, i>) for i = A .. B-1 (a loop whose index is a
+// constant expression)
+template <int A, int B, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (A < B) {
+        f(std::integral_constant<int, A>{});
+        static_for<A + 1, B>(f);
     }
 }
 
@@ -1188,7 +1260,6 @@ __device__ __forceinline__ void decode_ilp(const KParams &p, const PC &pc, uint3
                                            uint32_t stride, bool (&act)[kIlp], bool (&ok)[kIlp],
                                            uint32_t (&asg)[kIlp], uint32_t (&w)[kIlp][Codes<S>::kWords]) {
     constexpr int NW = Codes<S>::kWords;
-    constexpr int NN = PC::NN;
     R r[kIlp];
     uint32_t at[kIlp];
 #pragma unroll
@@ -1203,15 +1274,13 @@ __device__ __forceinline__ void decode_ilp(const KParams &p, const PC &pc, uint3
     // the searches, cut by cut, interleaved over the kIlp candidates; each
     // cut goes straight into its byte of the code words (cut j searches
     // column S - j)
-#pragma unroll
-    for (int j = 1; j <= S - 2; ++j) {
-        const int c = S - j;
+    static_for<1, S - 1>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
         uint32_t cut[kIlp];
-        if (c < NN) search_cut<uint32_t, R, H>(p, pc.ncol(c), pc.ntree(c), r, at, cut);
-        else search_cut<R, R, H>(p, pc.wcol(c), pc.wtree(c), r, at, cut);
+        pc.template search<S - j>(p, r, at, cut);
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) w[u][(j - 1) / 4] |= cut[u] << (8 * ((j - 1) % 4));
-    }
+    });
     if (S >= 2) {
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) w[u][(S - 2) / 4] |= (at[u] + (uint32_t)r[u]) << (8 * ((S - 2) % 4));
@@ -1232,17 +1301,14 @@ __device__ __forceinline__ void decode_ilp(const KParams &p, const PC &pc, uint3
 template <int S, typename R, int H, int J0, int J1, typename PC>
 __device__ __forceinline__ void decode_range(const KParams &p, const PC &pc, R (&r)[kIlp],
                                              uint32_t (&at)[kIlp], uint32_t (&cut)[kIlp][S + 1]) {
-    constexpr int NN = PC::NN;
     constexpr int JS = J1 < S - 2 ? J1 : S - 2;   // cuts found by a search
-#pragma unroll
-    for (int j = J0 + 1; j <= JS; ++j) {
-        const int c = S - j;
+    static_for<J0 + 1, JS + 1>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
         uint32_t cj[kIlp];
-        if (c < NN) search_cut<uint32_t, R, H>(p, pc.ncol(c), pc.ntree(c), r, at, cj);
-        else search_cut<R, R, H>(p, pc.wcol(c), pc.wtree(c), r, at, cj);
+        pc.template search<S - j>(p, r, at, cj);
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) cut[u][j] = cj[u];
-    }
+    });
     if (J1 == S - 1 && S >= 2) {
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) cut[u][S - 1] = at[u] + (uint32_t)r[u];
@@ -1286,40 +1352,39 @@ __device__ __forceinline__ void decode_batch(const KParams &p, const PC &pc, uin
     }
 }
 
-// Columns C0 .. C1 of the Pascal table, 2^H entries each, into LDS in
-// order and in tree order (layout of Pascal<S, R, H, C0, C1>); the tree node
-// at depth l and offset m probes sorted position (2m + 1) 2^(H-1-l) - 1
-// (entry 0 of the tree is unused).  Narrow columns saturate at 2^32 - 1,
-// which keeps them sorted (no value of a column below 5 reaches it for
-// n <= 255).
+// Columns C0 .. C1 of the Pascal table into LDS (layout of
+// Pascal<S, R, H, C0, C1>): 2^H rows each, then the padding rows of the
+// type's largest value (so that the columns stay sorted), then the host's
+// bucket tables of those columns.  Narrow columns saturate at 2^32 - 1 (no
+// value of a column below 5 reaches it for n <= 255).
 template <int S, typename R, int H, int C0 = 2, int C1 = S - 1>
 __device__ __forceinline__ void pascal_tables(const KParams &p, void *lds) {
     using PC = Pascal<S, R, H, C0, C1>;
-    constexpr uint32_t NH = PC::NH, NC = C1 >= C0 ? (uint32_t)(C1 - C0 + 1) : 0u;
-    R *ws = reinterpret_cast<R *>(lds), *wt = ws + (uint32_t)PC::NWC * NH;
-    uint32_t *ns = reinterpret_cast<uint32_t *>(wt + (uint32_t)PC::NWC * NH), *nt = ns + (uint32_t)PC::NNC * NH;
+    constexpr uint32_t NH = PC::NH, NP = PC::NP, NC = C1 >= C0 ? (uint32_t)(C1 - C0 + 1) : 0u;
+    unsigned char *b = reinterpret_cast<unsigned char *>(lds);
+    R *ws = reinterpret_cast<R *>(b);
+    uint32_t *ns = reinterpret_cast<uint32_t *>(b + PC::kWideBytes);
     const R *gb = reinterpret_cast<const R *>(p.binom);
-    for (uint32_t e = threadIdx.x; e < NC * NH; e += kBlock) {
-        const uint32_t k = C0 + e / NH, i = e % NH;
-        const uint32_t l = i ? 31u - __clz(i) : 0u, m = i - (1u << l);
-        const R vs = gb[k * kNB + i];
-        const R vt = i ? gb[k * kNB + (2 * m + 1) * (NH >> (l + 1)) - 1] : (R)0;
-        if ((int)k >= PC::NN) {
-            ws[(k - PC::WL) * NH + i] = vs;
-            wt[(k - PC::WL) * NH + i] = vt;
-        } else {
-            ns[(k - C0) * NH + i] = vs > (R)0xFFFFFFFFu ? 0xFFFFFFFFu : (uint32_t)vs;
-            nt[(k - C0) * NH + i] = vt > (R)0xFFFFFFFFu ? 0xFFFFFFFFu : (uint32_t)vt;
-        }
+    for (uint32_t e = threadIdx.x; e < NC * NP; e += kBlock) {
+        const uint32_t k = C0 + e / NP, i = e % NP;
+        const R v = i < NH ? gb[k * kNB + i] : ~(R)0;
+        if ((int)k >= PC::NN) ws[(k - PC::WL) * NP + i] = v;
+        else ns[(k - C0) * NP + i] = v > (R)0xFFFFFFFFu ? 0xFFFFFFFFu : (uint32_t)v;
     }
+    const uint4 *gt = reinterpret_cast<const uint4 *>(p.btab + (size_t)C0 * kBucketTab);
+    uint4 *lt = reinterpret_cast<uint4 *>(b + PC::kWideBytes + PC::kNarrowBytes);
+    for (uint32_t e = threadIdx.x; e < NC * (kBucketTab / 16); e += kBlock) lt[e] = gt[e];
 }
 
-// LDS bytes of both copies of Pascal columns C0 .. C1 (the column counts do
-// not depend on H)
+// LDS bytes of Pascal columns C0 .. C1 with their bucket tables
 template <int S, typename R, int C0 = 2, int C1 = S - 1>
 __host__ __device__ constexpr size_t pascal_bytes(uint32_t L) {
-    using PC = Pascal<S, R, 5, C0, C1>;
-    return 2 * ((size_t)1 << decode_levels(L)) * ((size_t)PC::NWC * sizeof(R) + (size_t)PC::NNC * 4);
+    switch (decode_levels(L)) {
+    case 8: return Pascal<S, R, 8, C0, C1>::bytes();
+    case 7: return Pascal<S, R, 7, C0, C1>::bytes();
+    case 6: return Pascal<S, R, 6, C0, C1>::bytes();
+    default: return Pascal<S, R, 5, C0, C1>::bytes();
+    }
 }
 
 // Range mode with one assignment: candidate i of the chunk is composition
@@ -1349,22 +1414,17 @@ template <int S, typename R, int H, typename PC>
 __device__ __forceinline__ void decode_succ(const KParams &p, const PC &pc, uint32_t base, bool &bad) {
     static_assert(kIlp == 4, "one 16-byte store per code word");
     constexpr int NW = Codes<S>::kWords;
-    constexpr int NN = PC::NN;
     const uint64_t rank0 = p.first + (uint32_t)p.first_i + base;
     R r[1] = {(R)(rank0 < p.n_comp ? rank0 : 0)};
     uint32_t at[1] = {1u}, c[S + 1];
     c[0] = 0;
     c[S] = p.L;
-#pragma unroll
-    for (int j = 1; j <= S - 2; ++j) {
-        const int col = S - j;
+    static_for<1, S - 1>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
         uint32_t cj[1];
-        if (col < NN)
-            search_cut<uint32_t, R, H, 1>(p, pc.ncol(col), pc.ntree(col), r, at, cj);
-        else
-            search_cut<R, R, H, 1>(p, pc.wcol(col), pc.wtree(col), r, at, cj);
+        pc.template search<S - j>(p, r, at, cj);
         c[j] = cj[0];
-    }
+    });
     if (S >= 2) c[S - 1] = at[0] + (uint32_t)r[0];
     uint32_t w[kIlp][NW];
 #pragma unroll
