@@ -99,12 +99,15 @@ __device__ __forceinline__ uint32_t ent(const Ent &t, uint32_t c, uint32_t to) {
 // (a1) decode
 // ---------------------------------------------------------------------------
 
-// Cut points of the composition with lexicographic rank r.  For the j-th cut
-// with k = S-1-j cuts left after it and a = c_{j-1} + 1 its smallest value,
-// the number of tuples whose j-th cut is below c is C(L-a, k+1) - C(L-c, k+1)
-// (hockey-stick identity).  With Q = C(L-a, k+1) - r the cut is c = L - n*,
-// n* the smallest n with C(n, k+1) >= Q, found by a branch-free binary
-// search over column k+1 of the Pascal table; the rank left is C(n*, k+1) - Q.
+// Cut points of the composition with lexicographic rank r (sorted cut
+// tuples c_1 < ... < c_{S-1} in 1 .. L-1).  The complements y_j = L - 1 - c_j
+// run the other way, and lexicographic order of the cuts is the reverse of
+// the co-lexicographic order of the complements, whose rank is
+// sum_j C(y_j, S - j) (combinatorial number system).  So R = C(L-1, S-1) - 1
+// - r is that rank, and the cuts follow greedily: y_j is the largest y with
+// C(y, S - j) <= R, then R <- R - C(y_j, S - j); the last (S - j = 1) is
+// y = R.  The kernels carry q = R + 1 and find n = y_j + 1 as the smallest n
+// with C(n, S - j) >= q, by a search over column S - j of the Pascal table.
 // Cut points in compact form: cut j (1-based) is byte (j-1) % 4 of word
 // (j-1) / 4; a valid composition has c_1 >= 1, so an all-zero first byte
 // marks an invalid candidate (for S = 1 the single byte is 1 when valid).
@@ -1169,26 +1172,28 @@ static_assert(bucket_steps(64, 7, 2) == 2 && bucket_steps(64, 7, 15) == 1 && buc
               "bucket steps of the 7-level columns");
 
 // With 64-bit ranks the searches over columns 0 .. kNarrow-1 run in 32 bits:
-// C(n, k) < 2^32 for every n <= 255 and k <= 4, and at the search of a cut
-// whose column is k + 1 the remaining rank is below C(L - a, k + 1), so the
-// rank, Q and every probe fit 32 bits there.  Those columns are kept in LDS
+// C(n, k) < 2^32 for every n <= 255 and k <= 4, and at the search over
+// column k the state q is at most C(y, k) for the previous cut's complement
+// y <= 254, so q, every probe and the rank left fit 32 bits there.  Those columns are kept in LDS
 // as uint32 (half the bytes per probe); the others as R.
 template <int S, typename R>
 __host__ __device__ constexpr int narrow_cols() {
     return sizeof(R) == 8 ? (S < 5 ? S : 5) : 0;
 }
 
-// One cut's search for NI candidates over a column of type V (R or uint32)
-// with its bucket table: Q = C(L - a, k + 1) - r, the smallest n with
-// C(n, k + 1) >= Q, the rank left C(n, k + 1) - Q, the cut L - n.
+// One cut's search for NI candidates over column c of type V (R or uint32)
+// with its bucket table.  q is the decode state (see decode_start): the cut's
+// complement y = L - 1 - cut is the largest y with C(y, c) <= q - 1, so
+// n = y + 1 is the smallest n with C(n, c) >= q; then q <- q - C(n - 1, c)
+// and the cut is L - n.
 template <typename V, typename R, int HS, int NI>
-__device__ __forceinline__ void search_cut(const KParams &p, const V *col, const uint8_t *tab, R (&r)[NI],
-                                           uint32_t (&at)[NI], uint32_t (&cut)[NI]) {
+__device__ __forceinline__ void search_cut(const KParams &p, const V *col, const uint8_t *tab, R (&q)[NI],
+                                           uint32_t (&cut)[NI]) {
     static_assert(HS <= kBucketStepsMax, "a bucket spans at most 2^3 rows (the padding)");
     V Q[NI];
     uint32_t n0[NI], t[NI];
 #pragma unroll
-    for (int u = 0; u < NI; ++u) Q[u] = col[p.L - at[u]] - (V)r[u];
+    for (int u = 0; u < NI; ++u) Q[u] = (V)q[u];
 #pragma unroll
     for (int u = 0; u < NI; ++u) {
         n0[u] = tab[bucket_key(Q[u])];
@@ -1204,10 +1209,9 @@ __device__ __forceinline__ void search_cut(const KParams &p, const V *col, const
     }
 #pragma unroll
     for (int u = 0; u < NI; ++u) {
-        const uint32_t n = n0[u] + t[u];
-        r[u] = (R)(col[n] - Q[u]);
+        const uint32_t n = n0[u] + t[u];   // at least 1: C(0, c) = 0 < q
+        q[u] = (R)(Q[u] - col[n - 1]);
         cut[u] = p.L - n;
-        at[u] = cut[u] + 1;
     }
 }
 
@@ -1238,10 +1242,10 @@ struct Pascal {
     }
     // the search of a cut over column c, for NI candidates
     template <int c, int NI>
-    __device__ __forceinline__ void search(const KParams &p, R (&r)[NI], uint32_t (&at)[NI], uint32_t (&cut)[NI]) const {
+    __device__ __forceinline__ void search(const KParams &p, R (&q)[NI], uint32_t (&cut)[NI]) const {
         static_assert(c >= C0 && c <= C1, "column outside the window");
         using V = typename std::conditional<(c >= NN), R, uint32_t>::type;
-        search_cut<V, R, bucket_steps(8 * (int)sizeof(V), H, c)>(p, col<c>(), tab<c>(), r, at, cut);
+        search_cut<V, R, bucket_steps(8 * (int)sizeof(V), H, c)>(p, col<c>(), tab<c>(), q, cut);
     }
 };
 
@@ -1255,19 +1259,26 @@ __device__ __forceinline__ void static_for(F &&f) {
     }
 }
 
+// The decode state of lexicographic rank r: q = C(L-1, S-1) - r, which is
+// one more than the co-lexicographic rank of the cut complements
+// y_j = L - 1 - c_j (so q >= 1 for every valid rank).
+template <typename R>
+__device__ __forceinline__ R decode_start(const KParams &p, R r) {
+    return (R)(p.n_comp - (uint64_t)r);
+}
+
 template <int S, typename R, int H, typename PC>
 __device__ __forceinline__ void decode_ilp(const KParams &p, const PC &pc, uint32_t base,
                                            uint32_t stride, bool (&act)[kIlp], bool (&ok)[kIlp],
                                            uint32_t (&asg)[kIlp], uint32_t (&w)[kIlp][Codes<S>::kWords]) {
     constexpr int NW = Codes<S>::kWords;
-    R r[kIlp];
-    uint32_t at[kIlp];
+    R q[kIlp];
 #pragma unroll
     for (int u = 0; u < kIlp; ++u) {
         const uint32_t i = base + u * stride;
         act[u] = i < (uint32_t)p.n_i;
-        ok[u] = candidate<R>(p, (uint32_t)p.first_i + (act[u] ? i : 0u), r[u], asg[u]) && act[u];
-        at[u] = 1;
+        ok[u] = candidate<R>(p, (uint32_t)p.first_i + (act[u] ? i : 0u), q[u], asg[u]) && act[u];
+        q[u] = decode_start<R>(p, q[u]);
 #pragma unroll
         for (int k = 0; k < NW; ++k) w[u][k] = 0;
     }
@@ -1277,13 +1288,13 @@ __device__ __forceinline__ void decode_ilp(const KParams &p, const PC &pc, uint3
     static_for<1, S - 1>([&](auto jc) {
         constexpr int j = decltype(jc)::value;
         uint32_t cut[kIlp];
-        pc.template search<S - j>(p, r, at, cut);
+        pc.template search<S - j>(p, q, cut);
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) w[u][(j - 1) / 4] |= cut[u] << (8 * ((j - 1) % 4));
     });
     if (S >= 2) {
 #pragma unroll
-        for (int u = 0; u < kIlp; ++u) w[u][(S - 2) / 4] |= (at[u] + (uint32_t)r[u]) << (8 * ((S - 2) % 4));
+        for (int u = 0; u < kIlp; ++u) w[u][(S - 2) / 4] |= (p.L - (uint32_t)q[u]) << (8 * ((S - 2) % 4));
     }
 #pragma unroll
     for (int u = 0; u < kIlp; ++u) {
@@ -1295,43 +1306,43 @@ __device__ __forceinline__ void decode_ilp(const KParams &p, const PC &pc, uint3
     }
 }
 
-// Searches of cuts J0+1 .. J1 (J1 <= S - 1) of kIlp candidates, from the
-// rank left r and the smallest value at of cut J0+1; cut J1 = S - 1, the
-// last, needs no search (with one cut left, C(n, 1) = n: c_{S-1} = a + r).
+// Searches of cuts J0+1 .. J1 (J1 <= S - 1) of kIlp candidates from the
+// decode state q after cut J0; cut S - 1, the last, needs no search (with
+// one cut left, C(y, 1) = y: its complement is q - 1, so c_{S-1} = L - q).
 template <int S, typename R, int H, int J0, int J1, typename PC>
-__device__ __forceinline__ void decode_range(const KParams &p, const PC &pc, R (&r)[kIlp],
-                                             uint32_t (&at)[kIlp], uint32_t (&cut)[kIlp][S + 1]) {
+__device__ __forceinline__ void decode_range(const KParams &p, const PC &pc, R (&q)[kIlp],
+                                             uint32_t (&cut)[kIlp][S + 1]) {
     constexpr int JS = J1 < S - 2 ? J1 : S - 2;   // cuts found by a search
     static_for<J0 + 1, JS + 1>([&](auto jc) {
         constexpr int j = decltype(jc)::value;
         uint32_t cj[kIlp];
-        pc.template search<S - j>(p, r, at, cj);
+        pc.template search<S - j>(p, q, cj);
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) cut[u][j] = cj[u];
     });
     if (J1 == S - 1 && S >= 2) {
 #pragma unroll
-        for (int u = 0; u < kIlp; ++u) cut[u][S - 1] = at[u] + (uint32_t)r[u];
+        for (int u = 0; u < kIlp; ++u) cut[u][S - 1] = p.L - (uint32_t)q[u];
     }
 }
 
 // Cuts c_1 .. c_J (J <= S - 1) of kIlp candidates at call positions pos
 // (valid positions also for inactive lanes) into cut[u][0 .. J], with
-// c_0 = 0 and c_S = L; r and at are left as decode_range needs them to go
-// on.  Invalid (rank, assignment) pairs get ok = false.
+// c_0 = 0 and c_S = L; q is left as decode_range needs it to go on.
+// Invalid (rank, assignment) pairs get ok = false.
 template <int S, typename R, int H, int J, typename PC>
 __device__ __forceinline__ void decode_cuts(const KParams &p, const PC &pc,
                                             const uint32_t (&pos)[kIlp], const bool (&act)[kIlp],
-                                            bool (&ok)[kIlp], uint32_t (&asg)[kIlp], R (&r)[kIlp],
-                                            uint32_t (&at)[kIlp], uint32_t (&cut)[kIlp][S + 1]) {
+                                            bool (&ok)[kIlp], uint32_t (&asg)[kIlp], R (&q)[kIlp],
+                                            uint32_t (&cut)[kIlp][S + 1]) {
 #pragma unroll
     for (int u = 0; u < kIlp; ++u) {
-        ok[u] = candidate<R>(p, pos[u], r[u], asg[u]) && act[u];
-        at[u] = 1;
+        ok[u] = candidate<R>(p, pos[u], q[u], asg[u]) && act[u];
+        q[u] = decode_start<R>(p, q[u]);
         cut[u][0] = 0;
         cut[u][S] = p.L;
     }
-    decode_range<S, R, H, 0, J>(p, pc, r, at, cut);
+    decode_range<S, R, H, 0, J>(p, pc, q, cut);
 }
 
 template <int S, typename R, int H, typename PC>
@@ -1415,17 +1426,17 @@ __device__ __forceinline__ void decode_succ(const KParams &p, const PC &pc, uint
     static_assert(kIlp == 4, "one 16-byte store per code word");
     constexpr int NW = Codes<S>::kWords;
     const uint64_t rank0 = p.first + (uint32_t)p.first_i + base;
-    R r[1] = {(R)(rank0 < p.n_comp ? rank0 : 0)};
-    uint32_t at[1] = {1u}, c[S + 1];
+    R q[1] = {decode_start<R>(p, (R)(rank0 < p.n_comp ? rank0 : 0))};
+    uint32_t c[S + 1];
     c[0] = 0;
     c[S] = p.L;
     static_for<1, S - 1>([&](auto jc) {
         constexpr int j = decltype(jc)::value;
         uint32_t cj[1];
-        pc.template search<S - j>(p, r, at, cj);
+        pc.template search<S - j>(p, q, cj);
         c[j] = cj[0];
     });
-    if (S >= 2) c[S - 1] = at[0] + (uint32_t)r[0];
+    if (S >= 2) c[S - 1] = p.L - (uint32_t)q[0];
     uint32_t w[kIlp][NW];
 #pragma unroll
     for (int u = 0; u < kIlp; ++u) {
@@ -1714,8 +1725,9 @@ __host__ __device__ constexpr int filter_col_lo() { return MODE == kFilterPrefix
 template <int S, int MODE>
 __host__ __device__ constexpr int filter_col_hi() { return MODE == kFilterGather ? S - filter_prefix<S>() - 1 : S - 1; }
 
-// The prefix list, arrays of ccap entries: call position, rank left (low
-// and high words), assignment index, then the first X cuts as cut codes.
+// The prefix list, arrays of ccap entries: call position, decode state q
+// after the first X cuts (low and high words), assignment index, then the
+// first X cuts as cut codes.
 static_assert(4 + (filter_prefix<kSMax>() + 3) / 4 <= kAListWords, "first-stage list entry too small");
 struct AList {
     uint32_t *pos, *rlo, *rhi, *asg, *w;
@@ -1914,7 +1926,7 @@ __device__ __forceinline__ void filter_screened(const KParams &p, const PC &pc, 
         wave_lds_sync();
         const uint32_t nb = cnt < kTile ? cnt : kTile;
         bool act[kIlp], ok[kIlp];
-        uint32_t pos[kIlp], asg[kIlp], at[kIlp], cut[kIlp][S + 1];
+        uint32_t pos[kIlp], asg[kIlp], cut[kIlp][S + 1];
         R r[kIlp];
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) {
@@ -1922,7 +1934,7 @@ __device__ __forceinline__ void filter_screened(const KParams &p, const PC &pc, 
             act[u] = j < nb;
             pos[u] = first_i + (act[u] ? buf[j] : 0u);   // (position 0 of the piece for idle lanes)
         }
-        decode_cuts<S, R, H, X0>(p, pc, pos, act, ok, asg, r, at, cut);
+        decode_cuts<S, R, H, X0>(p, pc, pos, act, ok, asg, r, cut);
         filter_emit<S, R, AR, kFilterPrefix>(p, tab, b, nq, act, ok, pos, asg, r, cut, n_keep, n_pruned, n_infeas, bad);
         // the positions past the batch (fewer than kTile) move to the front
         if (cnt > kTile) {
@@ -1970,7 +1982,7 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
     for (uint32_t base = start; base < n; base += kIlp * stride) {
         bool act[kIlp], ok[kIlp];
         uint32_t pos[kIlp];
-        uint32_t asg[kIlp], at[kIlp], cut[kIlp][S + 1];
+        uint32_t asg[kIlp], cut[kIlp][S + 1];
         R r[kIlp];
         if constexpr (MODE == kFilterGather) {
 #pragma unroll
@@ -1989,9 +2001,8 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
                 cut[u][S] = p.L;
 #pragma unroll
                 for (int j = 1; j <= X0; ++j) cut[u][j] = (w[(j - 1) / 4] >> (8 * ((j - 1) % 4))) & 0xFFu;
-                at[u] = cut[u][X0] + 1;
             }
-            decode_range<S, R, H, X0, S - 1>(p, pc, r, at, cut);
+            decode_range<S, R, H, X0, S - 1>(p, pc, r, cut);
         } else {
 #pragma unroll
             for (int u = 0; u < kIlp; ++u) {
@@ -1999,7 +2010,7 @@ __device__ __forceinline__ void filter_all(const KParams &p, const R *pas, const
                 act[u] = i < n;
                 pos[u] = first_i + (act[u] ? i : 0u);
             }
-            decode_cuts<S, R, H, MODE == kFilterPrefix ? X0 : S - 1>(p, pc, pos, act, ok, asg, r, at, cut);
+            decode_cuts<S, R, H, MODE == kFilterPrefix ? X0 : S - 1>(p, pc, pos, act, ok, asg, r, cut);
         }
         filter_emit<S, R, AR, MODE>(p, tab, b, nq, act, ok, pos, asg, r, cut, n_keep, n_pruned, n_infeas, bad);
     }
