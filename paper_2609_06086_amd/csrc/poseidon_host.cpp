@@ -323,6 +323,7 @@ uint64_t noalloc_chunk_for(const poseidon_ctx *ctx);
 }  // namespace
 
 static_assert(pk::kEntRow >= POSEIDON_L_MAX + 1, "an entry field row holds every end point");
+static_assert(pk::kTypesMax >= POSEIDON_T_MAX, "per-type device arrays hold every type");
 
 struct poseidon_ctx {
     int device;

@@ -8,6 +8,7 @@ namespace pk {
 
 constexpr int kSMax = 16;
 constexpr uint32_t kNB = 256;   // Pascal-table column length (n = 0..255; L <= 256)
+constexpr uint32_t kTypesMax = 8;   // device types (the ABI's limit, checked where both are seen)
 
 // Buckets of the unranking searches.  A value Q >= 1 of a w-bit type falls in
 // bucket (z, m): z its number of leading zeros in w bits, m the 4 bits after
@@ -66,7 +67,7 @@ struct KParams {
     uint32_t has_ar;              // the problem has DP all-reduce times
     uint32_t sched;               // POSEIDON_SCHEDULE_*
     uint32_t ndev;                // devices: S, or S / V under Interleaved 1F1B
-    uint32_t last_lo[8];          // per type t: smallest c with pm[L] - pm[c] <= cap[t] (search)
+    uint32_t last_lo[kTypesMax];  // per type t: smallest c with pm[L] - pm[c] <= cap[t] (search)
     uint32_t g_mono_all;          // every type pair has its g_mono bit (the search kernels then
                                   // compile the closed-form last stage only)
     uint64_t g_mono;              // bit 8 t + u: every layer's fwd + bwd on t is at most M times

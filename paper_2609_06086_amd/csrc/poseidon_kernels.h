@@ -1102,7 +1102,7 @@ constexpr int kIlp = kDecodeIlp;
 // search for the smallest n with C(n, c) >= Q starts at the row Q's bucket
 // names and halves bucket_steps(w, H, c) times over the 2^steps rows after
 // it, which hold every row a value of that bucket can land on.  The last cut
-// needs no search: with one cut left, C(n, 1) = n, so c_{S-1} = a + r.
+// needs no search (decode_range).
 // One halving: t <- 2 t + (probe < Q), as a compare into VCC and an add with
 // carry-in (the compiler's select and shift-or take one VALU operation more).
 __device__ __forceinline__ uint32_t tree_step(uint32_t t, uint64_t probe, uint64_t q) {
@@ -1174,8 +1174,9 @@ static_assert(bucket_steps(64, 7, 2) == 2 && bucket_steps(64, 7, 15) == 1 && buc
 // With 64-bit ranks the searches over columns 0 .. kNarrow-1 run in 32 bits:
 // C(n, k) < 2^32 for every n <= 255 and k <= 4, and at the search over
 // column k the state q is at most C(y, k) for the previous cut's complement
-// y <= 254, so q, every probe and the rank left fit 32 bits there.  Those columns are kept in LDS
-// as uint32 (half the bytes per probe); the others as R.
+// y <= 254 (or C(L-1, k) at the first cut), so q, every probe and the rank
+// left fit 32 bits there.  Those columns are kept in LDS as uint32 (half the
+// bytes per probe); the others as R.
 template <int S, typename R>
 __host__ __device__ constexpr int narrow_cols() {
     return sizeof(R) == 8 ? (S < 5 ? S : 5) : 0;
@@ -1748,7 +1749,6 @@ struct AList {
 // compare decides it before any cut is decoded.  thr[2t], thr[2t+1] = those
 // two limits for every type t (threads t < T; the caller's barrier
 // publishes them).
-constexpr uint32_t kScreenTypes = 8;   // device types (POSEIDON_T_MAX)
 template <int S, typename R>
 __device__ __forceinline__ void stage1_limits(const KParams &p, const Ent &tab, uint32_t b, unsigned long long *thr) {
     if (threadIdx.x >= p.T) return;
@@ -1807,7 +1807,7 @@ __host__ __device__ constexpr bool filter_screens() {
 }
 template <int S, bool AR, int MODE>
 __host__ __device__ constexpr size_t filter_static_lds() {
-    return filter_screens<S, AR, MODE>() ? (size_t)kScreenBuf * 4 * (kBlock / 64) + 16 * kScreenTypes : 0;
+    return filter_screens<S, AR, MODE>() ? (size_t)kScreenBuf * 4 * (kBlock / 64) + 16 * kTypesMax : 0;
 }
 
 // The tests of kIlp decoded candidates of one lane (cuts 1 .. X of
@@ -2047,7 +2047,7 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(KParams p) {
     const unsigned long long *thr = nullptr;
     if constexpr (filter_screens<S, AR, MODE>()) {
         __shared__ uint32_t screen_buf[kScreenBuf * (kBlock / 64)];
-        __shared__ unsigned long long screen_thr[2 * kScreenTypes];
+        __shared__ unsigned long long screen_thr[2 * kTypesMax];
         stage1_limits<S, R>(p, tab, b, screen_thr);
         buf = screen_buf + (threadIdx.x >> 6) * kScreenBuf;
         thr = screen_thr;
