@@ -377,12 +377,14 @@ def bounded_vs_oracle(prob, cands, bound, chunk, dev, ramp=False):
 
 
 def test_bounded_largest_pascal_columns(dev):
-    """S = 16 with L > 128 and 64-bit ranks: the early-stop filter's Pascal
-    columns fill a block's 64 KB of LDS, so it reads the stage tables from
-    global memory; with and without all-reduce times, several chunk sizes."""
+    """S = 16 with L > 128 (256-row Pascal columns), 64-bit ranks and eight
+    device types: with all-reduce times the prefix filter's columns, stage
+    entries and screen buffer exceed a block's 64 KB of LDS (25,088 + 33,792
+    + 8,320 bytes), so it reads the stage entries from global memory;
+    without them everything fits.  Several chunk sizes."""
     rng = np.random.default_rng(141)
     for ar in (False, True):
-        prob = W.random_problem(rng, 130, 16, 40, 3, cost_lo=50, cost_hi=400, mem_hi=20, cap=400, assign_rows=1)
+        prob = W.random_problem(rng, 130, 16, 40, 8, cost_lo=50, cost_hi=400, mem_hi=20, cap=400, assign_rows=1)
         if ar:
             _with_allreduce(rng, prob, hi=3000)
         cands = W.random_candidates(rng, prob, 6000)
