@@ -153,7 +153,8 @@ int poseidon_validate(const poseidon_problem *problem, uint64_t *n_candidates);
 
 /* Copy the profile tables to device `hip_device` and build the lookup
  * tables every candidate evaluation shares: per-type prefix sums of the
- * per-layer costs and memory, the Pascal table used to unrank compositions,
+ * per-layer costs and memory, the Pascal table used to unrank compositions
+ * (with, per column, the row each search starts from for each value range),
  * and the slot schedule of the problem's DAG for (S, M) and its schedule
  * (Sec. 5: the DAG depends only on the pipeline depth, so it is built once
  * and only re-weighted).  For every problem, the slot pattern the kernels
