@@ -133,6 +133,26 @@ def test_every_stage_count_fast_path(dev):
             check_against_oracle(prob, cands, dev)
 
 
+def test_list_decode_every_stage_count_and_column_length(dev):
+    """List-mode unranking for S = 2..16 at every Pascal column length the
+    kernels use (L up to 32, 64, 128 and 256: 5 to 8 levels, so every set of
+    bucket tables and search lengths), with 32-bit or 64-bit ranks as the
+    composition count requires (below 2^63 here): random ranks plus the first
+    two and the last two, every makespan and mask bit against the oracle."""
+    rng = np.random.default_rng(153)
+    for S in range(2, 17):
+        for lo, hi in ((S, 32), (33, 64), (65, 128), (129, 256)):
+            Ls = [L for L in range(max(lo, S), hi + 1) if math.comb(L - 1, S - 1) < 2 ** 63]
+            if not Ls:
+                continue
+            L = int(rng.choice(Ls))
+            prob = W.random_problem(rng, L, S, S, 2, cost_hi=500, mem_hi=40, cap=10 ** 6, assign_rows=1)
+            n_comp = prob.n_compositions
+            edge = np.array([0, min(1, n_comp - 1), max(n_comp - 2, 0), n_comp - 1], dtype=np.uint64)
+            ranks = np.concatenate([rng.integers(0, n_comp, size=1500, dtype=np.uint64), edge])
+            check_against_oracle(prob, W.Candidates(comp_rank=np.ascontiguousarray(ranks)), dev)
+
+
 def test_short_pipelines_table_path(dev):
     """M < S (slot-table path)."""
     rng = np.random.default_rng(101)
